@@ -1,0 +1,61 @@
+"""Each plausible mistake planted in a copy of the oracle (a dropped term, a wrong sign, a
+swapped slope, a transposed or misaligned operand) must make at least one pin fail.
+The mistakes are planted in an in-memory copy of the oracle's source, on the CPU."""
+import os
+import sys
+import types
+
+import pytest
+
+from tests import pins
+
+SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "oracle", "crown64.py")
+
+MUTANTS = {
+    "drop_relax_intercept_lower": ("bias = bias + An @ t", "bias = bias"),
+    "drop_relax_intercept_upper": ("bias = bias + Ap @ t", "bias = bias"),
+    "swap_slopes_lower": ("Az = Ap * lam + An * s", "Az = Ap * s + An * lam"),
+    "swap_slopes_upper": ("Az = Ap * s + An * lam", "Az = Ap * lam + An * s"),
+    "drop_dense_bias": ("bias = bias + Ai @ _f64(nd.b)", "bias = bias"),
+    "drop_conv_bias": ("bias = bias + A4.sum(axis=(2, 3)) @ _f64(nd.b)", "bias = bias"),
+    "dense_weight_rows_reversed": ("Ai @ _f64(nd.W))", "Ai @ _f64(nd.W)[::-1])"),
+    "ibp_wrong_operand": ("L.append(Wp @ l + Wn @ u + _f64(nd.b))", "L.append(Wp @ l + Wn @ l + _f64(nd.b))"),
+    "ibp_conv_wrong_operand": ("L.append(conv2d(l, Wp, nd.stride, nd.pad) + conv2d(u, Wn, nd.stride, nd.pad) + b)",
+                               "L.append(conv2d(l, Wp, nd.stride, nd.pad) + conv2d(l, Wn, nd.stride, nd.pad) + b)"),
+    "concretize_wrong_vertex": ("np.minimum(A_x * lo, A_x * hi)", "np.minimum(A_x * lo, A_x * lo)"),
+    "lambda_rule_flipped": ("np.where(uu > -lu, 1.0, 0.0)", "np.where(uu > -lu, 0.0, 1.0)"),
+    "chord_slope_wrong": ("su = uu / (uu - lu)", "su = -lu / (uu - lu)"),
+    "chord_intercept_sign": ("t[unstable] = -su * lu", "t[unstable] = su * lu"),
+    "add_drops_branch": ("_accumulate(acc, nd.in1, Ai)", "pass"),
+    "conv_transpose_misaligned": ("return out[:, :, pad:pad + h, pad:pad + w]", "return out[:, :, :h, :w]"),
+    "conv_transpose_unflipped_stride": ("j:j + stride * (wo - 1) + 1:stride] += contrib",
+                                        "j:j + (wo - 1) + 1:1] += contrib"),
+    "split_clamps_wrong_side": ("L[i][j] = max(L[i][j], 0.0)", "U[i][j] = max(U[i][j], 0.0)"),
+    "box_not_clipped": ("lo = np.maximum(lo, np.float32(clip[0]))", "lo = lo"),
+    "intersect_reversed": ("l = np.maximum(l, il)", "l = np.minimum(l, il)"),
+    "final_upper_uses_lower_rule": ("Au, bu = backward(net, shapes, relax, out, Cm, zero, upper=True)",
+                                    "Au, bu = backward(net, shapes, relax, out, Cm, zero, upper=False)"),
+    "direct_affine_upper_wrong": ("concretize(W, b, lo, hi, False), concretize(W, b, lo, hi, True)",
+                                  "concretize(W, b, lo, hi, False), concretize(W, b, lo, hi, False)"),
+    "infeasible_not_detected": ("if np.any(L[i] > U[i]):", "if False:"),
+}
+
+
+def _mutant(old, new):
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation anchor not unique / missing: {old!r}"
+    mod = types.ModuleType("oracle_mutant")
+    sys.modules["oracle_mutant"] = mod          # dataclasses look their module up here
+    exec(compile(src.replace(old, new), "oracle_mutant", "exec"), mod.__dict__)
+    return mod
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name):
+    mod = _mutant(*MUTANTS[name])
+    for pin in pins.ALL_PINS:
+        try:
+            pin(mod)
+        except Exception:
+            return
+    pytest.fail(f"mutant {name} passed every pin")
