@@ -1,0 +1,146 @@
+"""Throughput of batched full-CROWN bound evaluation on one MI355X.
+
+A step is one vcr_crown_bounds call over one batch of seeded synthetic inputs that are
+already resident in HBM: the IBP pass, every intermediate layer's backward A-matrix pass,
+the ReLU relaxations and the final spec pass.  Default workload: the 784-1024x6-10 ReLU
+MLP, 64 inputs, eps = 0.015, 9 margin rows per input.
+
+Prints one JSON line with the throughput (inputs/s), the dominant kernel's roofline
+(the backward-step fp32 MFMA GEMM, timed with HIP events on the stream it runs on) and the
+fp64 CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_FP32_MFMA_TFLOPS = 157.3   # MI355X dense fp32 matrix peak
+GEMM_SOURCE = os.path.join(ROOT, "paper_2606_09377_amd", "csrc", "gemm.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_traffic.json")
+
+
+def gemm_source_hash():
+    return hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()[:16]
+
+
+def traffic_for(workload):
+    """HBM bytes per GEMM launch from the committed PMC runs, if they were taken on the
+    current kernel source; else None."""
+    try:
+        t = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_sha") != gemm_source_hash():
+        return None
+    w = t.get("workloads", {}).get(workload)
+    return None if w is None else w.get("bytes_per_launch")
+
+
+def cpu_baseline(wl, budget_s):
+    """The fp64 oracle, as it stands, on the first inputs of the same batch until the time
+    budget is used (at least one input)."""
+    import threadpoolctl
+    import oracle
+    t0 = time.perf_counter()
+    n = 0
+    while n < wl.x0.shape[0]:
+        oracle.crown(wl.net, wl.x0[n], wl.eps, wl.C[n])
+        n += 1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    dt = time.perf_counter() - t0
+    threads = max((p.get("num_threads", 1) for p in threadpoolctl.threadpool_info()), default=1)
+    return {"value": n / dt, "unit": "inputs/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"first {n} of the {wl.x0.shape[0]} inputs of the same batch, {dt:.1f} s",
+            "cpu_count": os.cpu_count()}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="mlp784x1024x6")
+    ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time (0: skip)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus})",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2606_09377_amd import Ctx
+    from paper_2606_09377_amd.vcrown import OPT_TIME_GEMM
+    from workloads import make_workload
+
+    wl = make_workload(args.workload)
+    B, m = wl.C.shape[0], wl.C.shape[1]
+    ctx = Ctx(0)
+    ctx.load_net(wl.net)
+    x0 = torch.from_numpy(wl.x0).cuda()
+    C = torch.from_numpy(wl.C).cuda()
+    lb = torch.empty((B, m), dtype=torch.float32, device="cuda")
+    ub = torch.empty((B, m), dtype=torch.float32, device="cuda")
+    for _ in range(args.warmup):
+        ctx.crown_bounds(x0, wl.eps, C, out=(lb, ub))
+    torch.cuda.synchronize()
+    flops_call = ctx.stats()["gemm_flops_last_call"]
+    ctx.set_option(OPT_TIME_GEMM, 1)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        ctx.crown_bounds(x0, wl.eps, C, out=(lb, ub))
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    st = ctx.stats()
+    ctx.set_option(OPT_TIME_GEMM, 0)
+    assert np.all(np.isfinite(lb.cpu().numpy()))
+
+    ms_step = dt / args.steps * 1e3
+    value = B * args.steps / dt
+    launches = st["timed_gemm_launches"]
+    gemm_s = st["timed_gemm_ms"] / 1e3
+    achieved = st["timed_gemm_flops"] / gemm_s / 1e12 if gemm_s > 0 else None
+    traffic = traffic_for(args.workload)
+    rec = {
+        "metric": "CROWN bound evals/sec (inputs or BaB domains) at 1 GPU; % fp32 MFMA peak",
+        "value": value,
+        "unit": "inputs/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "batch": B, "eps": float(wl.eps), "spec_rows": m,
+                   "layers": [int(wl.net.nodes[0].W.shape[1])] + [int(nd.W.shape[0]) for nd in wl.net.nodes
+                                                                   if nd.op == "dense"],
+                   "method": "full CROWN (IBP-intersected intermediate bounds)"},
+        "roofline": {"bound": "mfma", "kernel": "k_gemm (fp32 v_mfma_f32_32x32x2f32)",
+                     "achieved": achieved, "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / PEAK_FP32_MFMA_TFLOPS if achieved else None,
+                     "traffic": traffic,
+                     "launches_timed": launches,
+                     "avg_launch_ms": st["timed_gemm_ms"] / launches if launches else None,
+                     "flops_per_launch": st["timed_gemm_flops"] / launches if launches else None},
+        "call_mfma_frac": flops_call / (ms_step / 1e3) / (PEAK_FP32_MFMA_TFLOPS * 1e12),
+        "gemm_flops_per_step": flops_call,
+    }
+    if args.cpu_budget > 0:
+        rec["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,177 @@
+/*
+ * vcrown — batched CROWN linear bound propagation on ReLU networks, for AMD Instinct
+ * MI355X (gfx950).  C ABI.
+ *
+ * The problem (paper, Sec. 1.1): a network f : R^n -> R^m, an admissible input set, here
+ * the L-infinity ball ||x - x0||_inf <= eps intersected with a clip box (local
+ * robustness), and linear output properties given as a specification matrix C (the
+ * linear constraints of the VNN-LIB format, Sec. 1.2).  The library returns, for every
+ * row c of C, a lower and an upper bound on c . f(x) that hold for every x in the set.
+ *
+ * Methods (paper, Sec. 2.1):
+ *   - IBP: intervals propagated layer by layer, l_y = W+ l + W- u + b, u_y = W+ u + W- l + b;
+ *   - CROWN: a backward pass composing the layer weights with diagonal ReLU slope matrices
+ *     (different slopes for the lower and the upper branch) into linear functions
+ *     A_L x + b_L <= f(x) <= A_U x + b_U (equation "crown"), which are then minimised /
+ *     maximised over the box.  "Full" CROWN: every ReLU's pre-activation bounds come from
+ *     such a backward pass from that layer to the input, intersected with the IBP bounds;
+ *   - branch-and-bound subdomains (Sec. 2.1, complete verification): each subdomain fixes
+ *     some ReLUs to the active (z >= 0) or inactive (z <= 0) state; subdomains of one root
+ *     input are bounded in one batched pass (Sec. 2.5, batch BaB).
+ *
+ * Conventions shared by every entry point:
+ *   - All tensors are float32, dense, row-major (C order).  Device pointers must come from
+ *     the context's device and be 16-byte aligned.
+ *   - Work is queued on the context's stream (vcr_set_stream; default: the null stream).
+ *     Entry points return once the work is queued; outputs are valid after the stream is
+ *     synchronised.  Entry points that must read device results say "synchronises".
+ *   - Every call returns a vcr_status.  On an error nothing is queued, the outputs are left
+ *     untouched and vcr_last_error() describes the failure.  No C++ exception crosses the
+ *     ABI.  An asynchronous device fault is reported as VCR_ERR_DEVICE by a later call.
+ *   - A context is not thread-safe; use one context per host thread / stream.
+ */
+#ifndef VCROWN_H
+#define VCROWN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define VCR_ABI_VERSION 1
+
+typedef struct vcr_ctx vcr_ctx;
+
+typedef enum {
+  VCR_OK = 0,
+  VCR_ERR_ARG = 1,          /* invalid argument value (null pointer, eps < 0, bad split) */
+  VCR_ERR_SHAPE = 2,        /* sizes inconsistent with the loaded network */
+  VCR_ERR_STATE = 3,        /* call out of order (e.g. bounds before vcr_load_net) */
+  VCR_ERR_OOM = 4,          /* device allocation failed or exceeds the workspace cap */
+  VCR_ERR_DEVICE = 5,       /* HIP runtime error (including an earlier asynchronous fault) */
+  VCR_ERR_UNSUPPORTED = 6   /* valid request this build does not implement */
+} vcr_status;
+
+/* Node kinds of a feed-forward network given in topological order. */
+typedef enum {
+  VCR_DENSE = 0,     /* y = W x + b, W (out_features, d_in) row-major, b (out_features) */
+  VCR_CONV2D = 1,    /* 2-D cross-correlation, W (out_ch, C_in, kh, kw), b (out_ch), zero padding */
+  VCR_RELU = 2,      /* y = max(x, 0) elementwise */
+  VCR_ADD = 3,       /* y = in0 + in1 (same shape) */
+  VCR_FLATTEN = 4    /* (C, H, W) -> C*H*W in C, H, W order */
+} vcr_op;
+
+typedef struct {
+  int32_t op;             /* vcr_op */
+  int32_t in0, in1;       /* producer node ids, -1 = the network input; in1 only for VCR_ADD */
+  int32_t out_features;   /* VCR_DENSE */
+  int32_t out_ch, kh, kw, stride, pad;  /* VCR_CONV2D */
+  const float *W, *b;     /* HOST pointers, copied by vcr_load_net; PyTorch layouts */
+} vcr_node;
+
+/* Branch-and-bound subdomains of one root input (paper, Sec. 2.1 and Sec. 2.5).
+ * n_domains x per_domain entries each, DEVICE pointers, row-major by domain:
+ *   relu_id[d*per_domain + k]  index of the ReLU node among the network's ReLU nodes, in
+ *                              node order (0 = first ReLU);
+ *   neuron[...]                flat index into that ReLU's tensor;
+ *   sign[...]                  +1: the pre-activation is fixed to z >= 0 (active),
+ *                              -1: fixed to z <= 0 (inactive).
+ * A domain's intermediate bounds are the root pass's, with each split neuron's interval
+ * clamped (l <- max(l, 0) for +1, u <- min(u, 0) for -1).  A domain whose clamped interval
+ * is empty (l > u) is infeasible and gets lb = +inf, ub = -inf (not an error).  A domain
+ * with an out-of-range entry, a sign other than +-1 or a neuron repeated gets NaN bounds and
+ * is counted in vcr_stats.invalid_domains. */
+typedef struct {
+  int32_t n_domains, per_domain;
+  const int32_t *relu_id;
+  const int32_t *neuron;
+  const int8_t *sign;
+} vcr_splits;
+
+/* Options (vcr_set_option). */
+enum {
+  VCR_OPT_CLIP_ENABLE = 1,          /* 1 (default): intersect the eps-ball with [CLIP_LO, CLIP_HI] */
+  VCR_OPT_CLIP_LO = 2,              /* default 0.0 */
+  VCR_OPT_CLIP_HI = 3,              /* default 1.0 */
+  VCR_OPT_INTERSECT_IBP = 4,        /* 1 (default): intersect CROWN intermediate bounds with IBP */
+  VCR_OPT_WORKSPACE_CAP_BYTES = 5,  /* device workspace cap; 0 (default) = no cap.  Inputs
+                                       (or domains) are processed in chunks that fit. */
+  VCR_OPT_SYNC_CHECK = 6,           /* 1: synchronise after each call and report device errors
+                                       and invalid split domains as the call's status */
+  VCR_OPT_TIME_GEMM = 7             /* 1: bracket every backward-step GEMM launch with HIP events
+                                       on the context's stream; vcr_get_stats reports their summed
+                                       duration.  Setting the option (either value) resets the sums. */
+};
+
+typedef struct {
+  double ms_last_call;              /* host wall time of the last bounds call (queue + wait if SYNC_CHECK) */
+  uint64_t gemm_flops_last_call;    /* algorithmic fp32 GEMM flops of the last call (2 per MAC) */
+  uint64_t peak_workspace_bytes;    /* largest device workspace held so far */
+  uint64_t workspace_bytes;         /* current device workspace */
+  int32_t n_chunks_last_call;       /* input (or domain) chunks used by the last call */
+  int32_t invalid_domains;          /* domains rejected by the last split call (synchronises) */
+  int32_t n_relu;                   /* ReLU nodes of the loaded network */
+  int32_t unstable[64];             /* unstable neurons per ReLU node, summed over inputs, last
+                                       CROWN call (synchronises); first min(n_relu, 64) valid */
+  /* with VCR_OPT_TIME_GEMM: GEMM launches timed since the option was set, their summed
+   * device duration and their algorithmic flops */
+  uint64_t timed_gemm_launches;
+  double timed_gemm_ms;
+  uint64_t timed_gemm_flops;
+} vcr_stats;
+
+/* ABI version compiled into the library (VCR_ABI_VERSION). */
+int32_t vcr_abi_version(void);
+
+/* Create a context on HIP device `hip_device`.  hip_device = -1 creates a validation-only
+ * context without a device: vcr_load_net checks the network and the bounds calls check
+ * their arguments, then return VCR_ERR_STATE instead of queueing work. */
+vcr_status vcr_create(int32_t hip_device, vcr_ctx **out);
+void vcr_destroy(vcr_ctx *ctx);
+
+/* Message of the last failed call; owned by the context, valid until its next call. */
+const char *vcr_last_error(const vcr_ctx *ctx);
+
+/* Use the caller's hipStream_t for all later work (NULL = the null stream). */
+vcr_status vcr_set_stream(vcr_ctx *ctx, void *hip_stream);
+
+vcr_status vcr_set_option(vcr_ctx *ctx, int32_t key, double value);
+
+/* Load (copy) a network.  nodes[0..n) in topological order; the last node is the output and
+ * must be VCR_DENSE.  in_chw is the input shape (C, H, W); for a flat input use
+ * (n0, 1, 1).  Weight pointers are host memory and are not retained.  Replaces any
+ * previously loaded network.  Synchronises. */
+vcr_status vcr_load_net(vcr_ctx *ctx, const vcr_node *nodes, int32_t n, const int32_t in_chw[3]);
+
+/* IBP bounds on C f(x) (paper, Sec. 2.1, IBP), C folded into the last dense layer.
+ *   x0  device (B, n0)      centres of the eps-balls (flat input, C,H,W order)
+ *   eps scalar >= 0         L-infinity radius; the box is fl32(x0 -/+ eps) then clipped
+ *   C   device (B, m, n_out) one specification matrix per input
+ *   lb, ub device (B, m)    outputs */
+vcr_status vcr_ibp_bounds(vcr_ctx *ctx, const float *x0, int32_t B, float eps,
+                          const float *C, int32_t m, float *lb, float *ub);
+
+/* Full CROWN bounds on C f(x) (paper, Sec. 2.1, equation "crown").
+ * Without splits (splits == NULL): as vcr_ibp_bounds, outputs (B, m).
+ * With splits: B must be 1; the root pass runs on x0 and every subdomain is bounded with
+ * the final pass; C is (1, m, n_out) and lb, ub are (n_domains, m). */
+vcr_status vcr_crown_bounds(vcr_ctx *ctx, const float *x0, int32_t B, float eps,
+                            const float *C, int32_t m, const vcr_splits *splits,
+                            float *lb, float *ub);
+
+/* Pre-activation bounds of ReLU node `relu_id` (0-based among ReLU nodes) from the last
+ * CROWN call, for every input: l, u device (B, numel).  Queued on the stream. */
+vcr_status vcr_get_layer_bounds(vcr_ctx *ctx, int32_t relu_id, float *l, float *u);
+
+/* Device bytes a bounds call of this size would hold (without a cap). */
+vcr_status vcr_workspace_bytes(vcr_ctx *ctx, int32_t B, int32_t m, int32_t n_domains, uint64_t *bytes);
+
+/* Statistics; synchronises the stream. */
+vcr_status vcr_get_stats(vcr_ctx *ctx, vcr_stats *out);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* VCROWN_H */

@@ -1,0 +1,908 @@
+// C ABI of vcrown: network loading, argument validation, the batching planner and the
+// sequence of kernel launches of one bounds call.
+//
+// One CROWN call on an MLP  z_k = W_k h_{k-1} + b_k,  h_k = ReLU(z_k),  f = z_L:
+//   1. box (centre/radius) and one pure IBP forward pass over all layers;
+//   2. ReLU 1: bounds of z_1 = the exact box range of one affine map (equals IBP);
+//   3. ReLU k >= 2: rows [W_k; -W_k] for every input (the lower and the negated upper
+//      bound of every neuron of z_k), relaxed through ReLU k-1, then one GEMM per layer
+//      W_{k-1} .. W_2 whose epilogue relaxes the next ReLU, and a last GEMM with W_1 whose
+//      epilogue concretizes over the box; finally l, u, intersection with IBP and the new
+//      relaxation;
+//   4. the spec pass: rows [C W_L; -C W_L] per input through the same chain.
+// With branch-and-bound splits the root input runs 1-3 once; step 4 then runs over all
+// subdomains, whose relaxations differ from the root's only at their split neurons.
+//
+// Rows never straddle inputs within a GEMM row block of an intermediate pass (2 n_k rows
+// per input), every output element has its own fixed-order K sum, and every reduction
+// runs in a fixed order: bounds are bitwise independent of batch size and chunking.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <chrono>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/vcrown.h"
+#include "kernels.h"
+
+using namespace vcr;
+
+namespace {
+
+struct DenseLayer {
+  int32_t n_in = 0, n_out = 0;
+  int64_t ld_in = 0, ld_out = 0;
+  float *Wp = nullptr;   // n_out x ld_in, zero padded
+  float *Bt = nullptr;   // ld_in x ld_out, Bt[n][k] = W[k][n], zero padded
+  float *b = nullptr;    // ld_out, zero padded
+};
+
+struct Workspace {
+  char *base = nullptr;
+  size_t cap = 0, used = 0;
+};
+
+}  // namespace
+
+struct vcr_ctx {
+  int32_t device = -1;
+  hipStream_t stream = nullptr;
+  std::string err;
+  // options
+  int32_t clip_on = 1;
+  float clip_lo = 0.f, clip_hi = 1.f;
+  int32_t intersect = 1;
+  uint64_t ws_cap = 0;
+  int32_t sync_check = 0;
+  // network
+  bool loaded = false;
+  int32_t n0 = 0;
+  std::vector<DenseLayer> layers;   // the MLP chain
+  std::vector<int32_t> relu_n;      // neurons per ReLU node
+  std::vector<vcr_node> node_desc;  // validated node list (weights not retained)
+  // workspace
+  Workspace ws;
+  uint64_t peak_ws = 0;
+  // last call
+  int32_t last_B = 0;
+  std::vector<float *> lastL, lastU;
+  int32_t *d_counters = nullptr;    // [64] unstable counts + [1] invalid domains
+  bool last_had_splits = false;
+  double ms_last = 0.0;
+  uint64_t flops_last = 0;
+  int32_t chunks_last = 0;
+  // GEMM timing (VCR_OPT_TIME_GEMM)
+  int32_t time_gemm = 0;
+  std::vector<hipEvent_t> ev_pool;      // pairs: start, stop
+  size_t ev_used = 0;                   // events recorded but not yet read
+  uint64_t timed_launches = 0, timed_flops = 0;
+  double timed_ms = 0.0;
+  std::vector<uint64_t> pending_flops;  // flops of each recorded pair
+};
+
+namespace {
+
+vcr_status fail(vcr_ctx *c, vcr_status st, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  c->err = buf;
+  return st;
+}
+
+#define HIP_TRY(c, expr)                                                                      \
+  do {                                                                                        \
+    hipError_t e_ = (expr);                                                                   \
+    if (e_ != hipSuccess) return fail((c), VCR_ERR_DEVICE, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+void free_layers(vcr_ctx *c) {
+  for (auto &L : c->layers) {
+    if (L.Wp) (void)hipFree(L.Wp);
+    if (L.Bt) (void)hipFree(L.Bt);
+    if (L.b) (void)hipFree(L.b);
+  }
+  c->layers.clear();
+}
+
+void free_ws(vcr_ctx *c) {
+  if (c->ws.base) (void)hipFree(c->ws.base);
+  c->ws = Workspace{};
+}
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// ---- workspace planning ------------------------------------------------------------
+struct Plan {
+  int32_t B = 0, m = 0, D = 0;
+  int32_t chunk_in = 0;     // inputs per intermediate-pass chunk
+  int32_t chunk_units = 0;  // inputs (or domains) per spec-pass chunk
+  size_t bytes = 0;
+};
+
+size_t al(size_t x) { return (x + 255) / 256 * 256; }
+
+int64_t max_inter_rows_per_input(const vcr_ctx *c) {
+  int64_t r = 0;
+  const int L = (int)c->layers.size();
+  for (int k = 1; k < L - 1; ++k) r = std::max<int64_t>(r, 2 * (int64_t)c->layers[k].n_out);
+  return r;
+}
+
+size_t carve_bytes(const vcr_ctx *c, const Plan &p, int32_t S);
+
+vcr_status make_plan(vcr_ctx *c, int32_t B, int32_t m, int32_t D, int32_t S, Plan *p) {
+  p->B = B;
+  p->m = m;
+  p->D = D;
+  const int64_t rpi = max_inter_rows_per_input(c);
+  const int32_t spec_units = D > 0 ? D : B;
+  const int32_t root_B = D > 0 ? 1 : B;
+  auto need = [&](int32_t ci, int32_t cu) {
+    Plan q = *p;
+    q.chunk_in = ci;
+    q.chunk_units = cu;
+    return carve_bytes(c, q, S);
+  };
+  int32_t ci = std::max(root_B, 1), cu = std::max(spec_units, 1);
+  if (c->ws_cap > 0) {
+    while (need(ci, cu) > c->ws_cap && (ci > 1 || cu > 1)) {
+      // shrink the larger row block first
+      if (rpi * ci >= 2 * (int64_t)m * cu && ci > 1)
+        ci = (ci + 1) / 2;
+      else if (cu > 1)
+        cu = (cu + 1) / 2;
+      else
+        ci = (ci + 1) / 2;
+    }
+    if (need(ci, cu) > c->ws_cap)
+      return fail(c, VCR_ERR_OOM, "workspace cap %llu bytes is below the minimum plan (%llu bytes)",
+                  (unsigned long long)c->ws_cap, (unsigned long long)need(ci, cu));
+  }
+  p->chunk_in = ci;
+  p->chunk_units = cu;
+  p->bytes = need(ci, cu);
+  return VCR_OK;
+}
+
+vcr_status ensure_ws(vcr_ctx *c, size_t bytes) {
+  if (c->ws.cap >= bytes) {
+    c->ws.used = 0;
+    return VCR_OK;
+  }
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  free_ws(c);
+  void *p = nullptr;
+  hipError_t e = hipMalloc(&p, bytes);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(c, VCR_ERR_OOM, "hipMalloc(%llu) failed: %s", (unsigned long long)bytes, hipGetErrorString(e));
+  }
+  c->ws.base = static_cast<char *>(p);
+  c->ws.cap = bytes;
+  c->ws.used = 0;
+  c->peak_ws = std::max<uint64_t>(c->peak_ws, bytes);
+  // the A buffers' padding rows/columns are read by the GEMM: start from zeros
+  HIP_TRY(c, launch_fill(reinterpret_cast<float *>(p), (int64_t)(bytes / 4), 0.f, c->stream));
+  return VCR_OK;
+}
+
+// Sub-allocation from the workspace.  With a null base it only counts bytes, which is how
+// the planner sizes a call: the same carve code runs for sizing and for the real layout.
+template <class T>
+T *take(Workspace &w, size_t count) {
+  size_t b = al(sizeof(T) * std::max<size_t>(count, 1));
+  T *p = w.base ? reinterpret_cast<T *>(w.base + w.used) : nullptr;
+  w.used += b;
+  return p;
+}
+template <class T>
+T *take(vcr_ctx *c, size_t count) {
+  return take<T>(c->ws, count);
+}
+
+// ---- validation ---------------------------------------------------------------------
+vcr_status validate_net(vcr_ctx *c, const vcr_node *nodes, int32_t n, const int32_t in_chw[3],
+                        std::vector<std::vector<int64_t>> *shapes_out) {
+  if (!nodes || n <= 0 || !in_chw) return fail(c, VCR_ERR_ARG, "empty network");
+  if (in_chw[0] <= 0 || in_chw[1] <= 0 || in_chw[2] <= 0) return fail(c, VCR_ERR_SHAPE, "bad input shape");
+  std::vector<std::vector<int64_t>> sh;
+  const std::vector<int64_t> in_shape = {in_chw[0], in_chw[1], in_chw[2]};
+  auto shape_of = [&](int32_t i) -> const std::vector<int64_t> & { return i == -1 ? in_shape : sh[i]; };
+  auto numel = [](const std::vector<int64_t> &s) {
+    int64_t p = 1;
+    for (auto v : s) p *= v;
+    return p;
+  };
+  for (int32_t i = 0; i < n; ++i) {
+    const vcr_node &nd = nodes[i];
+    if (nd.in0 < -1 || nd.in0 >= i) return fail(c, VCR_ERR_ARG, "node %d: in0=%d is not an earlier node", i, nd.in0);
+    const auto &s = shape_of(nd.in0);
+    switch (nd.op) {
+      case VCR_DENSE: {
+        if (!nd.W || !nd.b) return fail(c, VCR_ERR_ARG, "node %d: dense without weights", i);
+        if (nd.out_features <= 0) return fail(c, VCR_ERR_SHAPE, "node %d: out_features <= 0", i);
+        sh.push_back({nd.out_features, 1, 1});
+        break;
+      }
+      case VCR_CONV2D: {
+        if (!nd.W || !nd.b) return fail(c, VCR_ERR_ARG, "node %d: conv without weights", i);
+        if (nd.out_ch <= 0 || nd.kh <= 0 || nd.kw <= 0 || nd.stride <= 0 || nd.pad < 0)
+          return fail(c, VCR_ERR_SHAPE, "node %d: bad conv geometry", i);
+        const int64_t ho = (s[1] + 2 * nd.pad - nd.kh) / nd.stride + 1;
+        const int64_t wo = (s[2] + 2 * nd.pad - nd.kw) / nd.stride + 1;
+        if (ho <= 0 || wo <= 0) return fail(c, VCR_ERR_SHAPE, "node %d: conv output is empty", i);
+        sh.push_back({nd.out_ch, ho, wo});
+        break;
+      }
+      case VCR_RELU:
+        sh.push_back(s);
+        break;
+      case VCR_ADD: {
+        if (nd.in1 < -1 || nd.in1 >= i) return fail(c, VCR_ERR_ARG, "node %d: in1=%d is not an earlier node", i, nd.in1);
+        if (shape_of(nd.in1) != s) return fail(c, VCR_ERR_SHAPE, "node %d: add inputs differ in shape", i);
+        sh.push_back(s);
+        break;
+      }
+      case VCR_FLATTEN:
+        sh.push_back({numel(s), 1, 1});
+        break;
+      default:
+        return fail(c, VCR_ERR_ARG, "node %d: unknown op %d", i, nd.op);
+    }
+    (void)numel;
+  }
+  if (nodes[n - 1].op != VCR_DENSE) return fail(c, VCR_ERR_ARG, "the output node must be dense");
+  *shapes_out = sh;
+  return VCR_OK;
+}
+
+// The GPU path handles the MLP chain dense (relu dense)*; returns UNSUPPORTED otherwise.
+vcr_status check_chain(vcr_ctx *c, const vcr_node *nodes, int32_t n, const int32_t in_chw[3],
+                       const std::vector<std::vector<int64_t>> &sh) {
+  if (in_chw[1] != 1 || in_chw[2] != 1)
+    return fail(c, VCR_ERR_UNSUPPORTED, "this build bounds MLPs on flat inputs only (got a %dx%dx%d input)",
+                in_chw[0], in_chw[1], in_chw[2]);
+  (void)sh;
+  for (int32_t i = 0; i < n; ++i) {
+    const vcr_node &nd = nodes[i];
+    const bool want_dense = (i % 2 == 0);
+    if (want_dense) {
+      if (nd.op != VCR_DENSE || nd.in0 != i - 1)
+        return fail(c, VCR_ERR_UNSUPPORTED,
+                    "node %d: this build bounds chains dense (relu dense)* only (conv/add/flatten are not built)", i);
+    } else {
+      if (nd.op != VCR_RELU || nd.in0 != i - 1)
+        return fail(c, VCR_ERR_UNSUPPORTED,
+                    "node %d: this build bounds chains dense (relu dense)* only", i);
+    }
+  }
+  return VCR_OK;
+}
+
+}  // namespace
+
+// =====================================================================================
+extern "C" {
+
+int32_t vcr_abi_version(void) { return VCR_ABI_VERSION; }
+
+vcr_status vcr_create(int32_t hip_device, vcr_ctx **out) {
+  if (!out) return VCR_ERR_ARG;
+  *out = nullptr;
+  vcr_ctx *c = new (std::nothrow) vcr_ctx();
+  if (!c) return VCR_ERR_OOM;
+  c->device = hip_device;
+  if (hip_device >= 0) {
+    int n = 0;
+    hipError_t e = hipGetDeviceCount(&n);
+    if (e != hipSuccess || hip_device >= n) {
+      delete c;
+      return VCR_ERR_DEVICE;
+    }
+    if (hipSetDevice(hip_device) != hipSuccess) {
+      delete c;
+      return VCR_ERR_DEVICE;
+    }
+    if (hipMalloc(&c->d_counters, 80 * sizeof(int32_t)) != hipSuccess) {
+      delete c;
+      return VCR_ERR_OOM;
+    }
+  } else if (hip_device != -1) {
+    delete c;
+    return VCR_ERR_ARG;
+  }
+  *out = c;
+  return VCR_OK;
+}
+
+void vcr_destroy(vcr_ctx *c) {
+  if (!c) return;
+  if (c->device >= 0) {
+    (void)hipSetDevice(c->device);
+    (void)hipStreamSynchronize(c->stream);
+    free_layers(c);
+    free_ws(c);
+    if (c->d_counters) (void)hipFree(c->d_counters);
+    for (auto e : c->ev_pool) (void)hipEventDestroy(e);
+  }
+  delete c;
+}
+
+const char *vcr_last_error(const vcr_ctx *c) { return c ? c->err.c_str() : "null context"; }
+
+vcr_status vcr_set_stream(vcr_ctx *c, void *s) {
+  if (!c) return VCR_ERR_ARG;
+  c->stream = static_cast<hipStream_t>(s);
+  return VCR_OK;
+}
+
+vcr_status vcr_set_option(vcr_ctx *c, int32_t key, double v) {
+  if (!c) return VCR_ERR_ARG;
+  if (!std::isfinite(v)) return fail(c, VCR_ERR_ARG, "option %d: value is not finite", key);
+  switch (key) {
+    case VCR_OPT_CLIP_ENABLE: c->clip_on = v != 0.0; break;
+    case VCR_OPT_CLIP_LO: c->clip_lo = (float)v; break;
+    case VCR_OPT_CLIP_HI: c->clip_hi = (float)v; break;
+    case VCR_OPT_INTERSECT_IBP: c->intersect = v != 0.0; break;
+    case VCR_OPT_WORKSPACE_CAP_BYTES:
+      if (v < 0) return fail(c, VCR_ERR_ARG, "workspace cap < 0");
+      c->ws_cap = (uint64_t)v;
+      break;
+    case VCR_OPT_SYNC_CHECK: c->sync_check = v != 0.0; break;
+    case VCR_OPT_TIME_GEMM:
+      if (c->device >= 0 && c->ev_used) (void)hipStreamSynchronize(c->stream);
+      c->time_gemm = v != 0.0;
+      c->ev_used = 0;
+      c->pending_flops.clear();
+      c->timed_launches = c->timed_flops = 0;
+      c->timed_ms = 0.0;
+      break;
+    default: return fail(c, VCR_ERR_ARG, "unknown option %d", key);
+  }
+  return VCR_OK;
+}
+
+vcr_status vcr_load_net(vcr_ctx *c, const vcr_node *nodes, int32_t n, const int32_t in_chw[3]) {
+  if (!c) return VCR_ERR_ARG;
+  std::vector<std::vector<int64_t>> sh;
+  vcr_status st = validate_net(c, nodes, n, in_chw, &sh);
+  if (st != VCR_OK) return st;
+  // dense weight shapes must match their inputs
+  for (int32_t i = 0; i < n; ++i) {
+    if (nodes[i].op != VCR_DENSE) continue;
+    const auto &s = nodes[i].in0 == -1 ? std::vector<int64_t>{in_chw[0], in_chw[1], in_chw[2]} : sh[nodes[i].in0];
+    if (s[1] != 1 || s[2] != 1)
+      return fail(c, VCR_ERR_SHAPE, "node %d: dense input must be flat (insert a flatten node)", i);
+  }
+  st = check_chain(c, nodes, n, in_chw, sh);
+  if (st != VCR_OK) return st;
+  if (c->device < 0) {
+    // validation-only context: remember the shapes for argument checks
+    c->loaded = true;
+    c->n0 = in_chw[0];
+    c->layers.clear();
+    c->relu_n.clear();
+    int64_t prev = in_chw[0];
+    for (int32_t i = 0; i < n; ++i) {
+      if (nodes[i].op == VCR_DENSE) {
+        DenseLayer L;
+        L.n_in = (int32_t)prev;
+        L.n_out = nodes[i].out_features;
+        L.ld_in = ld_of(L.n_in);
+        L.ld_out = ld_of(L.n_out);
+        c->layers.push_back(L);
+        prev = L.n_out;
+      } else {
+        c->relu_n.push_back((int32_t)prev);
+      }
+    }
+    return VCR_OK;
+  }
+  HIP_TRY(c, hipSetDevice(c->device));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  free_layers(c);
+  free_ws(c);
+  c->loaded = false;
+  c->relu_n.clear();
+  c->n0 = in_chw[0];
+  int64_t prev = in_chw[0];
+  float *staging = nullptr;
+  for (int32_t i = 0; i < n; ++i) {
+    if (nodes[i].op == VCR_RELU) {
+      c->relu_n.push_back((int32_t)prev);
+      continue;
+    }
+    DenseLayer L;
+    L.n_in = (int32_t)prev;
+    L.n_out = nodes[i].out_features;
+    L.ld_in = ld_of(L.n_in);
+    L.ld_out = ld_of(L.n_out);
+    const size_t wbytes = sizeof(float) * (size_t)L.n_out * L.n_in;
+    HIP_TRY(c, hipMalloc(&staging, wbytes));
+    HIP_TRY(c, hipMemcpy(staging, nodes[i].W, wbytes, hipMemcpyHostToDevice));
+    HIP_TRY(c, hipMalloc(&L.Wp, sizeof(float) * (size_t)L.n_out * L.ld_in));
+    HIP_TRY(c, hipMalloc(&L.Bt, sizeof(float) * (size_t)L.ld_in * L.ld_out));
+    HIP_TRY(c, hipMalloc(&L.b, sizeof(float) * (size_t)L.ld_out));
+    c->layers.push_back(L);
+    // Wp: row-major copy with zero-padded rows (a transpose of the transpose)
+    HIP_TRY(c, launch_transpose_pad(staging, L.n_out, L.n_in, L.Bt, L.ld_out, L.ld_in, c->stream));
+    HIP_TRY(c, launch_transpose_pad(L.Bt, (int32_t)L.ld_in, (int32_t)L.ld_out, L.Wp, L.ld_in, L.n_out, c->stream));
+    HIP_TRY(c, launch_fill(L.b, L.ld_out, 0.f, c->stream));
+    HIP_TRY(c, hipStreamSynchronize(c->stream));
+    HIP_TRY(c, hipMemcpy(L.b, nodes[i].b, sizeof(float) * L.n_out, hipMemcpyHostToDevice));
+    HIP_TRY(c, hipFree(staging));
+    staging = nullptr;
+    prev = L.n_out;
+  }
+  HIP_TRY(c, hipDeviceSynchronize());
+  c->loaded = true;
+  return VCR_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+struct CallBufs {
+  float *c0, *r0;
+  std::vector<float *> ibp_c, ibp_r, Lb, Ub;
+  std::vector<float4 *> P;
+  float *CW, *Cb;
+  float *A[2], *beta, *part, *cpart;
+  // splits
+  int32_t *off, *ent_n, *flags;
+  float4 *ent_p;
+  const float **Lptr, **Uptr;
+  int32_t *relu_n;
+};
+
+vcr_status check_common(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m,
+                        const float *lb, const float *ub) {
+  if (!c->loaded) return fail(c, VCR_ERR_STATE, "no network loaded");
+  if (B <= 0) return fail(c, VCR_ERR_ARG, "B must be > 0");
+  if (m <= 0) return fail(c, VCR_ERR_ARG, "m must be > 0");
+  if (!(eps >= 0.f) || !std::isfinite(eps)) return fail(c, VCR_ERR_ARG, "eps must be finite and >= 0");
+  if (!x0 || !C || !lb || !ub) return fail(c, VCR_ERR_ARG, "null tensor pointer");
+  if (!aligned16(x0) || !aligned16(C) || !aligned16(lb) || !aligned16(ub))
+    return fail(c, VCR_ERR_ARG, "tensor pointers must be 16-byte aligned");
+  if ((int64_t)B * m > (int64_t)1 << 30) return fail(c, VCR_ERR_SHAPE, "B * m too large");
+  if (c->clip_on && !(c->clip_lo <= c->clip_hi)) return fail(c, VCR_ERR_ARG, "clip_lo > clip_hi");
+  return VCR_OK;
+}
+
+void carve(const vcr_ctx *c, Workspace &w, const Plan &p, int32_t S, CallBufs *bf) {
+  const int L = (int)c->layers.size();
+  const int32_t B = p.B;
+  const int64_t ld0 = ld_of(c->n0);
+  bf->c0 = take<float>(w, (size_t)B * ld0);
+  bf->r0 = take<float>(w, (size_t)B * ld0);
+  bf->ibp_c.clear(); bf->ibp_r.clear(); bf->Lb.clear(); bf->Ub.clear(); bf->P.clear();
+  for (int k = 0; k < L - 1; ++k) {
+    const int64_t ld = c->layers[k].ld_out, n = c->layers[k].n_out;
+    bf->ibp_c.push_back(take<float>(w, (size_t)B * ld));
+    bf->ibp_r.push_back(take<float>(w, (size_t)B * ld));
+    bf->Lb.push_back(take<float>(w, (size_t)B * n));
+    bf->Ub.push_back(take<float>(w, (size_t)B * n));
+    bf->P.push_back(take<float4>(w, (size_t)B * ld));
+  }
+  const int64_t ldcw = L >= 2 ? c->layers[L - 1].ld_in : ld0;
+  bf->CW = take<float>(w, (size_t)B * p.m * ldcw);
+  bf->Cb = take<float>(w, (size_t)B * p.m);
+  if (p.D > 0) {
+    const int R = (int)c->relu_n.size();
+    bf->off = take<int32_t>(w, (size_t)p.D * (R + 1));
+    bf->ent_n = take<int32_t>(w, (size_t)p.D * S);
+    bf->ent_p = take<float4>(w, (size_t)p.D * S);
+    bf->flags = take<int32_t>(w, p.D);
+    bf->Lptr = take<const float *>(w, 2 * R);
+    bf->Uptr = bf->Lptr + R;
+    bf->relu_n = take<int32_t>(w, R);
+  }
+  const int64_t rpi = max_inter_rows_per_input(c);
+  const int64_t rows = std::max<int64_t>({rpi * p.chunk_in, 2 * (int64_t)p.m * p.chunk_units, 1});
+  int64_t ldmax = 0;
+  for (int k = 0; k < L - 1; ++k) ldmax = std::max(ldmax, c->layers[k].ld_out);
+  const int64_t mp = rows_pad(rows);
+  bf->A[0] = take<float>(w, (size_t)mp * std::max<int64_t>(ldmax, 1));
+  bf->A[1] = take<float>(w, (size_t)mp * std::max<int64_t>(ldmax, 1));
+  bf->beta = take<float>(w, (size_t)mp);
+  bf->part = take<float>(w, (size_t)mp * std::max<int64_t>(ldmax / PART_COLS, 1));
+  bf->cpart = take<float>(w, (size_t)mp * (ld0 / PART_COLS));
+}
+
+size_t carve_bytes(const vcr_ctx *c, const Plan &p, int32_t S) {
+  Workspace w;
+  CallBufs bf;
+  carve(c, w, p, S, &bf);
+  return w.used;
+}
+
+// One backward pass through layers j = top .. 1 for `units` units of rows_per_unit rows
+// that start in A[0] (already relaxed for ReLU top-1... i.e. coefficients on z_top).
+// Leaves beta with the constants and cpart with the concretization partials.
+vcr_status run_chain(vcr_ctx *c, CallBufs &bf, int top, int32_t M, int32_t rows_per_unit, int32_t units,
+                     int32_t unit0, int32_t param_per_unit, const SplitTable &st, uint64_t *flops) {
+  const int32_t M_pad = (int32_t)rows_pad(M);
+  int cur = 0;
+  for (int j = top; j >= 1; --j) {
+    const DenseLayer &W = c->layers[j - 1];   // layer j: z_j = W_j h_{j-1} + b_j
+    GemmArgs g{};
+    g.A = bf.A[cur];
+    g.lda = W.ld_out;
+    g.Bt = W.Bt;
+    g.ldb = W.ld_out;
+    g.M = M;
+    g.M_pad = M_pad;
+    g.K = (int32_t)W.ld_out;
+    g.N_pad = (int32_t)W.ld_in;
+    g.rows_per_unit = param_per_unit ? rows_per_unit : M_pad;
+    g.n_units = param_per_unit ? units : 1;
+    g.splits = st;
+    const int64_t pu0 = param_per_unit ? unit0 : 0;
+    if (j >= 2) {
+      const int r = j - 2;   // ReLU on z_{j-1}
+      g.mode = EPI_RELAX;
+      g.out = bf.A[cur ^ 1];
+      g.ldo = W.ld_in;
+      g.P = bf.P[r] + pu0 * W.ld_in;
+      g.ldp = W.ld_in;
+      g.relu_index = r;
+      g.part = bf.part;
+    } else {
+      g.mode = EPI_CONCRETIZE;
+      g.c0 = bf.c0 + pu0 * ld_of(c->n0);
+      g.r0 = bf.r0 + pu0 * ld_of(c->n0);
+      g.ldc = ld_of(c->n0);
+      g.part = bf.cpart;
+    }
+    const uint64_t gf = 2ull * (uint64_t)M * (uint64_t)W.n_out * (uint64_t)W.n_in;
+    if (c->time_gemm) {
+      if (c->ev_used + 2 > c->ev_pool.size()) {
+        hipEvent_t e0, e1;
+        HIP_TRY(c, hipEventCreate(&e0));
+        HIP_TRY(c, hipEventCreate(&e1));
+        c->ev_pool.push_back(e0);
+        c->ev_pool.push_back(e1);
+      }
+      HIP_TRY(c, hipEventRecord(c->ev_pool[c->ev_used], c->stream));
+      HIP_TRY(c, launch_gemm(g, c->stream));
+      HIP_TRY(c, hipEventRecord(c->ev_pool[c->ev_used + 1], c->stream));
+      c->ev_used += 2;
+      c->pending_flops.push_back(gf);
+      if (c->ev_used >= 4096) {   // fold finished pairs in so the pool stays bounded
+        vcr_status st2 = VCR_OK;
+        HIP_TRY(c, hipEventSynchronize(c->ev_pool[c->ev_used - 1]));
+        for (size_t q = 0; q + 1 < c->ev_used; q += 2) {
+          float ms = 0.f;
+          HIP_TRY(c, hipEventElapsedTime(&ms, c->ev_pool[q], c->ev_pool[q + 1]));
+          c->timed_ms += ms;
+          c->timed_flops += c->pending_flops[q / 2];
+          ++c->timed_launches;
+        }
+        c->ev_used = 0;
+        c->pending_flops.clear();
+        (void)st2;
+      }
+    } else {
+      HIP_TRY(c, launch_gemm(g, c->stream));
+    }
+    *flops += gf;
+    if (j >= 2) {
+      HIP_TRY(c, launch_rowsum(bf.beta, bf.part, (int32_t)(W.ld_in / PART_COLS), M_pad, M, c->stream));
+      cur ^= 1;
+    }
+  }
+  return VCR_OK;
+}
+
+vcr_status crown_impl(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m,
+                      const vcr_splits *splits, float *lb, float *ub) {
+  const int L = (int)c->layers.size();
+  const int R = (int)c->relu_n.size();
+  const int32_t D = splits ? splits->n_domains : 0;
+  const int32_t S = splits ? splits->per_domain : 0;
+  Plan p;
+  vcr_status st = make_plan(c, B, m, D, S, &p);
+  if (st != VCR_OK) return st;
+  if (c->device < 0) {
+    // report the plan the call would have run
+    const int32_t units = D > 0 ? D : B;
+    const int32_t rootB = D > 0 ? 1 : B;
+    const int32_t n_inter = std::max(L - 2, 0);
+    c->chunks_last = n_inter * ((rootB + p.chunk_in - 1) / p.chunk_in) + (L >= 2 ? (units + p.chunk_units - 1) / p.chunk_units : 0);
+    return fail(c, VCR_ERR_STATE, "validation-only context: no device work");
+  }
+  HIP_TRY(c, hipSetDevice(c->device));
+  c->lastL.clear();   // the previous call's layer bounds live in the workspace
+  c->lastU.clear();
+  st = ensure_ws(c, p.bytes);
+  if (st != VCR_OK) return st;
+  CallBufs bf;
+  carve(c, c->ws, p, S, &bf);
+  if (c->ws.used > c->ws.cap) return fail(c, VCR_ERR_OOM, "internal: workspace plan too small");
+  uint64_t flops = 0;
+  int32_t chunks = 0;
+  hipStream_t s = c->stream;
+  const int64_t ld0 = ld_of(c->n0);
+
+  // 1. box and IBP
+  HIP_TRY(c, launch_box(x0, B, c->n0, ld0, eps, c->clip_on, c->clip_lo, c->clip_hi, bf.c0, bf.r0, s));
+  for (int k = 0; k < L - 1; ++k) {
+    const DenseLayer &W = c->layers[k];
+    const float *cin = k == 0 ? bf.c0 : bf.ibp_c[k - 1];
+    const float *rin = k == 0 ? bf.r0 : bf.ibp_r[k - 1];
+    HIP_TRY(c, launch_ibp_dense(W.Wp, W.ld_in, W.b, W.n_out, W.n_in, cin, rin, W.ld_in, k > 0, bf.ibp_c[k],
+                                bf.ibp_r[k], W.ld_out, B, s));
+  }
+  // 2. first ReLU
+  if (L >= 2)
+    HIP_TRY(c, launch_layer_from_ibp(bf.ibp_c[0], bf.ibp_r[0], c->layers[0].ld_out, c->layers[0].n_out, B,
+                                     c->layers[0].b, bf.Lb[0], bf.Ub[0], bf.P[0], c->layers[0].ld_out, s));
+  // 3. ReLU k >= 2 (layer index k: z_k = layers[k-1]); relu r = k-1
+  for (int k = 2; k <= L - 1; ++k) {
+    const DenseLayer &Wk = c->layers[k - 1];
+    const int32_t n = Wk.n_out;
+    for (int32_t b0 = 0; b0 < B; b0 += p.chunk_in) {
+      const int32_t bc = std::min(p.chunk_in, B - b0);
+      const int32_t M = 2 * n * bc;
+      InitArgs ia{};
+      ia.src = Wk.Wp;
+      ia.ld_src = Wk.ld_in;
+      ia.n_src = n;
+      ia.per_unit_src = 0;
+      ia.src_bias = Wk.b;
+      ia.n_cols = Wk.n_in;
+      ia.ldo = Wk.ld_in;
+      ia.M = M;
+      ia.units = bc;
+      ia.P = bf.P[k - 2] + (int64_t)b0 * Wk.ld_in;
+      ia.ldp = Wk.ld_in;
+      ia.param_per_unit = 1;
+      ia.relu_index = k - 2;
+      ia.out = bf.A[0];
+      ia.beta = bf.beta;
+      HIP_TRY(c, launch_init_rows(ia, s));
+      st = run_chain(c, bf, k - 1, M, 2 * n, bc, b0, 1, SplitTable{}, &flops);
+      if (st != VCR_OK) return st;
+      HIP_TRY(c, launch_finalize_layer(bf.beta, bf.cpart, (int32_t)(ld0 / PART_COLS), (int32_t)rows_pad(M), bc, n,
+                                       bf.ibp_c[k - 1] + (int64_t)b0 * Wk.ld_out,
+                                       bf.ibp_r[k - 1] + (int64_t)b0 * Wk.ld_out, Wk.ld_out, c->intersect, Wk.b,
+                                       bf.Lb[k - 1] + (int64_t)b0 * n, bf.Ub[k - 1] + (int64_t)b0 * n,
+                                       bf.P[k - 1] + (int64_t)b0 * Wk.ld_out, Wk.ld_out, s));
+      ++chunks;
+    }
+  }
+  // 4. spec pass
+  const DenseLayer &WL = c->layers[L - 1];
+  const int32_t Bs = D > 0 ? 1 : B;
+  HIP_TRY(c, launch_spec_cw(C, Bs, m, WL.n_out, WL.Wp, WL.ld_in, WL.b, WL.n_in, bf.CW, WL.ld_in, bf.Cb, s));
+  SplitTable tab{};
+  if (D > 0) {
+    std::vector<const float *> hp(2 * R);
+    for (int r = 0; r < R; ++r) {
+      hp[r] = bf.Lb[r];
+      hp[R + r] = bf.Ub[r];
+    }
+    HIP_TRY(c, hipMemcpyAsync(bf.Lptr, hp.data(), sizeof(void *) * 2 * R, hipMemcpyHostToDevice, s));
+    HIP_TRY(c, hipMemcpyAsync(bf.relu_n, c->relu_n.data(), sizeof(int32_t) * R, hipMemcpyHostToDevice, s));
+    HIP_TRY(c, launch_fill(reinterpret_cast<float *>(c->d_counters), 80, 0.f, s));
+    SplitPrepArgs sp{};
+    sp.relu_id = splits->relu_id;
+    sp.neuron = splits->neuron;
+    sp.sign = splits->sign;
+    sp.D = D;
+    sp.S = S;
+    sp.R = R;
+    sp.relu_n = bf.relu_n;
+    sp.L = bf.Lptr;
+    sp.U = bf.Uptr;
+    sp.off = bf.off;
+    sp.ent_n = bf.ent_n;
+    sp.ent_p = bf.ent_p;
+    sp.flags = bf.flags;
+    sp.n_invalid = c->d_counters + 64;
+    HIP_TRY(c, launch_split_prepare(sp, s));
+    // the host-side pointer array must outlive the async copy
+    HIP_TRY(c, hipStreamSynchronize(s));
+  }
+  const int32_t units = D > 0 ? D : B;
+  if (L == 1) {
+    HIP_TRY(c, launch_spec_direct(bf.CW, WL.ld_in, bf.Cb, B, m, WL.n_in, bf.c0, bf.r0, ld0, 0, lb, ub, s));
+  } else {
+    for (int32_t u0 = 0; u0 < units; u0 += p.chunk_units) {
+      const int32_t uc = std::min(p.chunk_units, units - u0);
+      const int32_t M = 2 * m * uc;
+      if (D > 0) {
+        tab.off = bf.off + (int64_t)u0 * (R + 1);
+        tab.ent_n = bf.ent_n + (int64_t)u0 * S;
+        tab.ent_p = bf.ent_p + (int64_t)u0 * S;
+        tab.R = R;
+        tab.S = S;
+        tab.D = uc;
+        tab.rows_per_domain = 2 * m;
+      }
+      InitArgs ia{};
+      ia.src = bf.CW + (D > 0 ? 0 : (int64_t)u0 * m * WL.ld_in);
+      ia.ld_src = WL.ld_in;
+      ia.n_src = m;
+      ia.per_unit_src = D > 0 ? 0 : 1;
+      ia.src_bias = bf.Cb + (D > 0 ? 0 : (int64_t)u0 * m);
+      ia.n_cols = WL.n_in;
+      ia.ldo = WL.ld_in;
+      ia.M = M;
+      ia.units = uc;
+      ia.P = bf.P[L - 2] + (D > 0 ? 0 : (int64_t)u0 * WL.ld_in);
+      ia.ldp = WL.ld_in;
+      ia.param_per_unit = D > 0 ? 0 : 1;
+      ia.relu_index = L - 2;
+      ia.splits = tab;
+      ia.out = bf.A[0];
+      ia.beta = bf.beta;
+      HIP_TRY(c, launch_init_rows(ia, s));
+      st = run_chain(c, bf, L - 1, M, 2 * m, uc, D > 0 ? 0 : u0, D > 0 ? 0 : 1, tab, &flops);
+      if (st != VCR_OK) return st;
+      HIP_TRY(c, launch_finalize_spec(bf.beta, bf.cpart, (int32_t)(ld0 / PART_COLS), (int32_t)rows_pad(M), uc, m,
+                                      D > 0 ? bf.flags + u0 : nullptr, lb + (int64_t)u0 * m,
+                                      ub + (int64_t)u0 * m, s));
+      ++chunks;
+    }
+  }
+  c->last_B = D > 0 ? 1 : B;
+  c->lastL.assign(bf.Lb.begin(), bf.Lb.end());
+  c->lastU.assign(bf.Ub.begin(), bf.Ub.end());
+  c->last_had_splits = D > 0;
+  c->flops_last = flops;
+  c->chunks_last = chunks;
+  return VCR_OK;
+}
+
+vcr_status after_call(vcr_ctx *c, vcr_status st, std::chrono::steady_clock::time_point t0) {
+  if (st == VCR_OK && c->sync_check) {
+    hipError_t e = hipStreamSynchronize(c->stream);
+    if (e != hipSuccess) st = fail(c, VCR_ERR_DEVICE, "device error: %s", hipGetErrorString(e));
+    if (st == VCR_OK && c->last_had_splits) {
+      int32_t inv = 0;
+      e = hipMemcpy(&inv, c->d_counters + 64, sizeof(int32_t), hipMemcpyDeviceToHost);
+      if (e != hipSuccess) st = fail(c, VCR_ERR_DEVICE, "device error: %s", hipGetErrorString(e));
+      else if (inv > 0) st = fail(c, VCR_ERR_ARG, "%d subdomain(s) have invalid splits (NaN bounds)", inv);
+    }
+  }
+  c->ms_last = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+  return st;
+}
+
+}  // namespace
+
+extern "C" {
+
+vcr_status vcr_crown_bounds(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m,
+                            const vcr_splits *splits, float *lb, float *ub) {
+  if (!c) return VCR_ERR_ARG;
+  const auto t0 = std::chrono::steady_clock::now();
+  vcr_status st = check_common(c, x0, B, eps, C, m, lb, ub);
+  if (st != VCR_OK) return st;
+  if (splits) {
+    if (B != 1) return fail(c, VCR_ERR_ARG, "splits need exactly one root input (B = 1)");
+    if (splits->n_domains <= 0 || splits->per_domain < 0 || splits->per_domain > 64)
+      return fail(c, VCR_ERR_ARG, "bad split sizes (n_domains > 0, 0 <= per_domain <= 64)");
+    if (splits->per_domain > 0 && (!splits->relu_id || !splits->neuron || !splits->sign))
+      return fail(c, VCR_ERR_ARG, "null split array");
+    if (c->relu_n.empty()) return fail(c, VCR_ERR_ARG, "splits need at least one ReLU");
+    if ((int64_t)splits->n_domains * m > (int64_t)1 << 30) return fail(c, VCR_ERR_SHAPE, "n_domains * m too large");
+  }
+  st = crown_impl(c, x0, B, eps, C, m, splits, lb, ub);
+  return after_call(c, st, t0);
+}
+
+vcr_status vcr_ibp_bounds(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m,
+                          float *lb, float *ub) {
+  if (!c) return VCR_ERR_ARG;
+  const auto t0 = std::chrono::steady_clock::now();
+  vcr_status st = check_common(c, x0, B, eps, C, m, lb, ub);
+  if (st != VCR_OK) return st;
+  if (c->device < 0) return fail(c, VCR_ERR_STATE, "validation-only context: no device work");
+  HIP_TRY(c, hipSetDevice(c->device));
+  const int L = (int)c->layers.size();
+  const int64_t ld0 = ld_of(c->n0);
+  size_t bytes = 2 * al(sizeof(float) * B * ld0);
+  for (int k = 0; k < L - 1; ++k) bytes += 2 * al(sizeof(float) * B * c->layers[k].ld_out);
+  bytes += al(sizeof(float) * B * m * c->layers[L - 1].ld_in) + al(sizeof(float) * B * m);
+  c->lastL.clear();   // this call reuses the workspace that held them
+  c->lastU.clear();
+  st = ensure_ws(c, bytes);
+  if (st != VCR_OK) return st;
+  hipStream_t s = c->stream;
+  float *c0 = take<float>(c, (size_t)B * ld0), *r0 = take<float>(c, (size_t)B * ld0);
+  std::vector<float *> cc, rr;
+  for (int k = 0; k < L - 1; ++k) {
+    cc.push_back(take<float>(c, (size_t)B * c->layers[k].ld_out));
+    rr.push_back(take<float>(c, (size_t)B * c->layers[k].ld_out));
+  }
+  const DenseLayer &WL = c->layers[L - 1];
+  float *CW = take<float>(c, (size_t)B * m * WL.ld_in), *Cb = take<float>(c, (size_t)B * m);
+  HIP_TRY(c, launch_box(x0, B, c->n0, ld0, eps, c->clip_on, c->clip_lo, c->clip_hi, c0, r0, s));
+  for (int k = 0; k < L - 1; ++k) {
+    const DenseLayer &W = c->layers[k];
+    HIP_TRY(c, launch_ibp_dense(W.Wp, W.ld_in, W.b, W.n_out, W.n_in, k == 0 ? c0 : cc[k - 1], k == 0 ? r0 : rr[k - 1],
+                                W.ld_in, k > 0, cc[k], rr[k], W.ld_out, B, s));
+  }
+  HIP_TRY(c, launch_spec_cw(C, B, m, WL.n_out, WL.Wp, WL.ld_in, WL.b, WL.n_in, CW, WL.ld_in, Cb, s));
+  HIP_TRY(c, launch_spec_direct(CW, WL.ld_in, Cb, B, m, WL.n_in, L >= 2 ? cc[L - 2] : c0, L >= 2 ? rr[L - 2] : r0,
+                                WL.ld_in, L >= 2, lb, ub, s));
+  return after_call(c, VCR_OK, t0);
+}
+
+vcr_status vcr_get_layer_bounds(vcr_ctx *c, int32_t relu_id, float *l, float *u) {
+  if (!c) return VCR_ERR_ARG;
+  if (c->lastL.empty()) return fail(c, VCR_ERR_STATE, "no CROWN call yet");
+  if (relu_id < 0 || relu_id >= (int32_t)c->lastL.size()) return fail(c, VCR_ERR_ARG, "relu_id out of range");
+  if (!l || !u) return fail(c, VCR_ERR_ARG, "null output");
+  const int64_t n = (int64_t)c->last_B * c->relu_n[relu_id];
+  HIP_TRY(c, launch_copy(l, c->lastL[relu_id], n, c->stream));
+  HIP_TRY(c, launch_copy(u, c->lastU[relu_id], n, c->stream));
+  return VCR_OK;
+}
+
+vcr_status vcr_workspace_bytes(vcr_ctx *c, int32_t B, int32_t m, int32_t n_domains, uint64_t *bytes) {
+  if (!c || !bytes) return VCR_ERR_ARG;
+  if (!c->loaded) return fail(c, VCR_ERR_STATE, "no network loaded");
+  if (B <= 0 || m <= 0 || n_domains < 0) return fail(c, VCR_ERR_ARG, "bad sizes");
+  const uint64_t cap = c->ws_cap;
+  c->ws_cap = 0;
+  Plan p;
+  vcr_status st = make_plan(c, B, m, n_domains, 64, &p);
+  c->ws_cap = cap;
+  if (st != VCR_OK) return st;
+  *bytes = p.bytes;
+  return VCR_OK;
+}
+
+vcr_status vcr_get_stats(vcr_ctx *c, vcr_stats *out) {
+  if (!c || !out) return VCR_ERR_ARG;
+  std::memset(out, 0, sizeof(*out));
+  out->ms_last_call = c->ms_last;
+  out->gemm_flops_last_call = c->flops_last;
+  out->peak_workspace_bytes = c->peak_ws;
+  out->workspace_bytes = c->ws.cap;
+  out->n_chunks_last_call = c->chunks_last;
+  out->n_relu = (int32_t)c->relu_n.size();
+  if (c->device < 0) return VCR_OK;
+  HIP_TRY(c, hipSetDevice(c->device));
+  if (c->ev_used) {
+    HIP_TRY(c, hipStreamSynchronize(c->stream));
+    for (size_t q = 0; q + 1 < c->ev_used; q += 2) {
+      float ms = 0.f;
+      HIP_TRY(c, hipEventElapsedTime(&ms, c->ev_pool[q], c->ev_pool[q + 1]));
+      c->timed_ms += ms;
+      c->timed_flops += c->pending_flops[q / 2];
+      ++c->timed_launches;
+    }
+    c->ev_used = 0;
+    c->pending_flops.clear();
+  }
+  out->timed_gemm_launches = c->timed_launches;
+  out->timed_gemm_ms = c->timed_ms;
+  out->timed_gemm_flops = c->timed_flops;
+  if (c->lastL.empty()) return VCR_OK;
+  int32_t *cnt = c->d_counters;
+  const int R = std::min<int>((int)c->lastL.size(), 64);
+  HIP_TRY(c, launch_fill(reinterpret_cast<float *>(cnt), 64, 0.f, c->stream));   // keeps [64] (invalid domains)
+  for (int r = 0; r < R; ++r)
+    HIP_TRY(c, launch_count_unstable(c->lastL[r], c->lastU[r], (int64_t)c->last_B * c->relu_n[r], cnt + r, c->stream));
+  int32_t host[80];
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  HIP_TRY(c, hipMemcpy(host, cnt, sizeof(host), hipMemcpyDeviceToHost));
+  for (int r = 0; r < R; ++r) out->unstable[r] = host[r];
+  out->invalid_domains = c->last_had_splits ? host[64] : 0;
+  return VCR_OK;
+}
+
+}  // extern "C"

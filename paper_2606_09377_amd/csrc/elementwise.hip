@@ -1,0 +1,545 @@
+// Bandwidth-bound kernels of the CROWN path: the input box, IBP (paper, Sec. 2.1, IBP),
+// the ReLU relaxation (Sec. 2.1, CROWN), the first coefficient rows of every backward
+// pass, the fixed-order row reductions that finish a bound, and the split table of
+// branch-and-bound subdomains.
+//
+// Relaxation parameters of a ReLU on [l, u] are packed as float4 (lam, s, t, b):
+//   u <= 0 : (0, 0, 0)  inactive;   l >= 0 : (1, 1, 0)  active;
+//   else   : s = u / (u - l), t = -s l, lam = 1 if u > -l else 0;
+// and b is the bias of the dense layer that produces the ReLU's input, which the
+// backward pass adds next.  All reductions run in a fixed order (sequential or a fixed
+// butterfly), so every bound is reproducible bit for bit and independent of batching.
+#include "kernels.h"
+
+namespace vcr {
+
+__device__ __forceinline__ float4 relax_params(float l, float u, float bias) {
+  if (u <= 0.f) return make_float4(0.f, 0.f, 0.f, bias);
+  if (l >= 0.f) return make_float4(1.f, 1.f, 0.f, bias);
+  const float s = u / (u - l);
+  const float t = -s * l;
+  const float lam = (u > -l) ? 1.f : 0.f;
+  return make_float4(lam, s, t, bias);
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+  // fixed butterfly over the 64 lanes of a wavefront
+  x += __shfl_xor(x, 32);
+  x += __shfl_xor(x, 16);
+  x += __shfl_xor(x, 8);
+  x += __shfl_xor(x, 4);
+  x += __shfl_xor(x, 2);
+  x += __shfl_xor(x, 1);
+  return x;
+}
+
+// ------------------------------------------------------------------------------------
+__global__ void k_fill(float *p, int64_t n, float v) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+hipError_t launch_fill(float *p, int64_t n, float v, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_fill, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, p, n, v);
+  return hipGetLastError();
+}
+
+__global__ void k_copy(float *dst, const float *src, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = src[i];
+}
+
+hipError_t launch_copy(float *dst, const float *src, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_copy, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, dst, src, n);
+  return hipGetLastError();
+}
+
+// Wt[j][i] = W[i][j] for i < rows, j < cols, zero elsewhere; Wt is rows_t x ldt.
+// With rows == 0 the same kernel zero-pads a plain copy (see launch_transpose_pad).
+__global__ void k_transpose_pad(const float *W, int32_t rows, int32_t cols, float *Wt, int64_t ldt,
+                                int64_t rows_t) {
+  __shared__ float tile[32][33];
+  const int64_t j0 = (int64_t)blockIdx.y * 32;   // Wt row block (W column)
+  const int64_t i0 = (int64_t)blockIdx.x * 32;   // Wt column block (W row)
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 32 x 8
+  for (int k = ty; k < 32; k += 8) {
+    const int64_t wi = i0 + k, wj = j0 + tx;
+    tile[k][tx] = (wi < rows && wj < cols) ? W[wi * cols + wj] : 0.f;
+  }
+  __syncthreads();
+  for (int k = ty; k < 32; k += 8) {
+    const int64_t tj = j0 + k, ti = i0 + tx;
+    if (tj < rows_t && ti < ldt) Wt[tj * ldt + ti] = tile[tx][k];
+  }
+}
+
+hipError_t launch_transpose_pad(const float *W, int32_t rows, int32_t cols, float *Wt, int64_t ldt,
+                                int64_t rows_t, hipStream_t s) {
+  dim3 grid((unsigned)((ldt + 31) / 32), (unsigned)((rows_t + 31) / 32));
+  hipLaunchKernelGGL(k_transpose_pad, grid, dim3(256), 0, s, W, rows, cols, Wt, ldt, rows_t);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------------
+// Input box (paper, Sec. 1.1): lo = max(fl(x0 - eps), clip_lo), hi = min(fl(x0 + eps),
+// clip_hi), stored as centre c = (lo + hi) / 2 and radius r = (hi - lo) / 2; padding
+// columns are zero.
+__global__ void k_box(const float *x0, int32_t B, int32_t n0, int64_t ld0, float eps, int32_t clip_on,
+                      float clip_lo, float clip_hi, float *c0, float *r0) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)B * ld0) return;
+  const int64_t b = idx / ld0, j = idx - b * ld0;
+  float c = 0.f, r = 0.f;
+  if (j < n0) {
+    const float x = x0[b * n0 + j];
+    float lo = __fsub_rn(x, eps), hi = __fadd_rn(x, eps);
+    if (clip_on) {
+      lo = fmaxf(lo, clip_lo);
+      hi = fminf(hi, clip_hi);
+    }
+    c = __fmul_rn(__fadd_rn(lo, hi), 0.5f);
+    r = __fmul_rn(__fsub_rn(hi, lo), 0.5f);
+  }
+  c0[idx] = c;
+  r0[idx] = r;
+}
+
+hipError_t launch_box(const float *x0, int32_t B, int32_t n0, int64_t ld0, float eps, int32_t clip_on,
+                      float clip_lo, float clip_hi, float *c0, float *r0, hipStream_t s) {
+  const int64_t n = (int64_t)B * ld0;
+  hipLaunchKernelGGL(k_box, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, x0, B, n0, ld0, eps,
+                     clip_on, clip_lo, clip_hi, c0, r0);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------------
+// IBP through a dense layer in centre/radius form: c' = W c + b, r' = |W| r, which is the
+// interval step W+ l + W- u + b, W+ u + W- l + b with l = c - r, u = c + r.  With relu_in
+// the input is first passed through ReLU: [max(l, 0), max(u, 0)].  One workgroup owns 32
+// output neurons x 16 inputs and streams W once through LDS in 64-wide K chunks.
+constexpr int IBP_TO = 32, IBP_TB = 16, IBP_KC = 64;
+
+__global__ __launch_bounds__(256) void k_ibp_dense(const float *Wp, int64_t ldw, const float *bias,
+                                                   int32_t n_out, int32_t n_in, const float *cin,
+                                                   const float *rin, int64_t ld_in, int32_t relu_in,
+                                                   float *cout, float *rout, int64_t ld_out, int32_t B) {
+  __shared__ float Ws[IBP_TO][IBP_KC + 1];
+  __shared__ float Cs[IBP_TB][IBP_KC + 1];
+  __shared__ float Rs[IBP_TB][IBP_KC + 1];
+  const int tid = threadIdx.x;
+  const int o_loc = tid >> 3, bq = tid & 7;
+  const int64_t o = (int64_t)blockIdx.x * IBP_TO + o_loc;
+  const int b0 = blockIdx.y * IBP_TB;
+  float c_a = 0.f, r_a = 0.f, c_b = 0.f, r_b = 0.f;
+  for (int64_t k0 = 0; k0 < n_in; k0 += IBP_KC) {
+    {  // W tile: 32 rows x 64, 8 floats per thread
+      const int wr = tid >> 3, wc = (tid & 7) * 8;
+      const int64_t go = (int64_t)blockIdx.x * IBP_TO + wr;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int64_t k = k0 + wc + e;
+        Ws[wr][wc + e] = (go < n_out && k < ld_in) ? Wp[go * ldw + k] : 0.f;
+      }
+    }
+    {  // input tile: 16 inputs x 64, 4 floats per thread
+      const int ib = tid >> 4, ic = (tid & 15) * 4;
+      const int gb = b0 + ib;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int64_t k = k0 + ic + e;
+        float c = 0.f, r = 0.f;
+        if (gb < B && k < ld_in) {
+          c = cin[(int64_t)gb * ld_in + k];
+          r = rin[(int64_t)gb * ld_in + k];
+          if (relu_in) {
+            const float lo = fmaxf(c - r, 0.f), hi = fmaxf(c + r, 0.f);
+            c = (lo + hi) * 0.5f;
+            r = (hi - lo) * 0.5f;
+          }
+        }
+        Cs[ib][ic + e] = c;
+        Rs[ib][ic + e] = r;
+      }
+    }
+    __syncthreads();
+#pragma unroll 8
+    for (int kk = 0; kk < IBP_KC; ++kk) {
+      const float w = Ws[o_loc][kk];
+      const float aw = fabsf(w);
+      c_a += w * Cs[bq][kk];
+      r_a += aw * Rs[bq][kk];
+      c_b += w * Cs[bq + 8][kk];
+      r_b += aw * Rs[bq + 8][kk];
+    }
+    __syncthreads();
+  }
+  if (o < ld_out) {
+    const bool real = o < n_out;
+    const float bo = real ? bias[o] : 0.f;
+    const int ba = b0 + bq, bb = b0 + bq + 8;
+    if (ba < B) {
+      cout[(int64_t)ba * ld_out + o] = real ? c_a + bo : 0.f;
+      rout[(int64_t)ba * ld_out + o] = real ? r_a : 0.f;
+    }
+    if (bb < B) {
+      cout[(int64_t)bb * ld_out + o] = real ? c_b + bo : 0.f;
+      rout[(int64_t)bb * ld_out + o] = real ? r_b : 0.f;
+    }
+  }
+}
+
+hipError_t launch_ibp_dense(const float *Wp, int64_t ldw, const float *b, int32_t n_out, int32_t n_in,
+                            const float *cin, const float *rin, int64_t ld_in, int32_t relu_in,
+                            float *cout, float *rout, int64_t ld_out, int32_t B, hipStream_t s) {
+  (void)n_in;
+  dim3 grid((unsigned)((ld_out + IBP_TO - 1) / IBP_TO), (unsigned)((B + IBP_TB - 1) / IBP_TB));
+  hipLaunchKernelGGL(k_ibp_dense, grid, dim3(256), 0, s, Wp, ldw, b, n_out, (int32_t)ld_in, cin, rin, ld_in,
+                     relu_in, cout, rout, ld_out, B);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------------
+// First ReLU layer: its pre-activation is one affine map of the input, whose exact range
+// over the box is the IBP interval [c - r, c + r].
+__global__ void k_layer_from_ibp(const float *c, const float *r, int64_t ld, int32_t n, int32_t B,
+                                 const float *bias, float *L, float *U, float4 *P, int64_t ldp) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)B * n) return;
+  const int64_t b = idx / n, i = idx - b * n;
+  const float cc = c[b * ld + i], rr = r[b * ld + i];
+  const float l = cc - rr, u = cc + rr;
+  L[idx] = l;
+  U[idx] = u;
+  P[b * ldp + i] = relax_params(l, u, bias[i]);
+}
+
+hipError_t launch_layer_from_ibp(const float *c, const float *r, int64_t ld, int32_t n, int32_t B,
+                                 const float *bias, float *L, float *U, float4 *P, int64_t ldp,
+                                 hipStream_t s) {
+  const int64_t tot = (int64_t)B * n;
+  hipLaunchKernelGGL(k_layer_from_ibp, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, c, r, ld, n, B,
+                     bias, L, U, P, ldp);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------------
+// First rows of a backward pass.  Row (unit u, direction d, i) starts as
+// (d ? -1 : 1) * src[i, :] (a weight row W_k[i] or a spec row (C W_L)[i]) with constant
+// (d ? -1 : 1) * src_bias[i]; the ReLU just below is relaxed with the lower rule and its
+// constants (relaxation intercepts and the bias of the dense layer below) are added.  One
+// wavefront per row; padding rows are zero.
+__device__ __forceinline__ float4 init_override(const SplitTable &st, int d, int relu, int col, float4 prm) {
+  const int e0 = st.off[d * (st.R + 1) + relu];
+  const int e1 = st.off[d * (st.R + 1) + relu + 1];
+  for (int e = e0; e < e1; ++e) {
+    if (st.ent_n[d * st.S + e] == col) {
+      const float4 q = st.ent_p[d * st.S + e];
+      prm.x = q.x;
+      prm.y = q.y;
+      prm.z = q.z;
+    }
+  }
+  return prm;
+}
+
+__global__ __launch_bounds__(256) void k_init_rows(const InitArgs a, int32_t M_pad) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= M_pad) return;
+  float *orow = a.out + row * a.ldo;
+  if (row >= a.M) {
+    for (int64_t c = (int64_t)lane * 4; c < a.ldo; c += 256)
+      *reinterpret_cast<float4 *>(orow + c) = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (lane == 0) a.beta[row] = 0.f;
+    return;
+  }
+  const int rpu = 2 * a.n_src;
+  const int u = (int)(row / rpu);
+  const int r2 = (int)(row - (int64_t)u * rpu);
+  const int dir = r2 >= a.n_src;
+  const int i = r2 - dir * a.n_src;
+  const float sgn = dir ? -1.f : 1.f;
+  const int64_t srow = a.per_unit_src ? (int64_t)u * a.n_src + i : i;
+  const float *src = a.src + srow * a.ld_src;
+  const float4 *P = a.P + (a.param_per_unit ? (int64_t)u * a.ldp : 0);
+  const bool has_splits = a.splits.D > 0;
+  float acc = 0.f;
+  for (int64_t c = (int64_t)lane * 4; c < a.ldo; c += 256) {
+    const float4 w = *reinterpret_cast<const float4 *>(src + c);
+    const float wv[4] = {w.x, w.y, w.z, w.w};
+    float ov[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float4 prm = P[c + e];
+      if (has_splits) prm = init_override(a.splits, u, a.relu_index, (int)(c + e), prm);
+      const float x = sgn * wv[e];
+      const float ap = x > 0.f ? x * prm.x : x * prm.y;
+      acc += fminf(x, 0.f) * prm.z + ap * prm.w;
+      ov[e] = ap;
+    }
+    *reinterpret_cast<float4 *>(orow + c) = make_float4(ov[0], ov[1], ov[2], ov[3]);
+  }
+  acc = wave_sum(acc);
+  if (lane == 0) a.beta[row] = sgn * a.src_bias[srow] + acc;
+}
+
+hipError_t launch_init_rows(const InitArgs &a, hipStream_t s) {
+  if (a.ldo % 4) return hipErrorInvalidValue;
+  const int32_t M_pad = (int32_t)rows_pad(a.M);
+  hipLaunchKernelGGL(k_init_rows, dim3((unsigned)((M_pad + 3) / 4)), dim3(256), 0, s, a, M_pad);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------------
+// beta[row] += sum_p part[p][row], p ascending.
+__global__ void k_rowsum(float *beta, const float *part, int32_t n_parts, int32_t M_pad, int32_t M) {
+  const int64_t row = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (row >= M) return;
+  float s = 0.f;
+  for (int p = 0; p < n_parts; ++p) s += part[(int64_t)p * M_pad + row];
+  beta[row] += s;
+}
+
+hipError_t launch_rowsum(float *beta, const float *part, int32_t n_parts, int32_t M_pad, int32_t M,
+                         hipStream_t s) {
+  hipLaunchKernelGGL(k_rowsum, dim3((unsigned)((M + 255) / 256)), dim3(256), 0, s, beta, part, n_parts, M_pad, M);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------------
+// Bounds of one ReLU layer's pre-activations from the finished backward pass: lower rows
+// (b, 0, i) give l, negated upper rows (b, 1, i) give -u; then intersection with IBP and
+// the relaxation for the passes above.
+__global__ void k_finalize_layer(const float *beta, const float *cpart, int32_t n_parts, int32_t M_pad,
+                                 int32_t B, int32_t n, const float *ibp_c, const float *ibp_r, int64_t ld_ibp,
+                                 int32_t intersect, const float *bias_next, float *L, float *U, float4 *P,
+                                 int64_t ldp) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)B * n) return;
+  const int64_t b = idx / n, i = idx - b * n;
+  const int64_t ml = b * 2 * n + i, mu = ml + n;
+  float sl = 0.f, su = 0.f;
+  for (int p = 0; p < n_parts; ++p) {
+    sl += cpart[(int64_t)p * M_pad + ml];
+    su += cpart[(int64_t)p * M_pad + mu];
+  }
+  float l = beta[ml] + sl;
+  float u = -(beta[mu] + su);
+  if (intersect) {
+    const float c = ibp_c[b * ld_ibp + i], r = ibp_r[b * ld_ibp + i];
+    l = fmaxf(l, c - r);
+    u = fminf(u, c + r);
+  }
+  L[idx] = l;
+  U[idx] = u;
+  P[b * ldp + i] = relax_params(l, u, bias_next[i]);
+}
+
+hipError_t launch_finalize_layer(const float *beta, const float *cpart, int32_t n_parts, int32_t M_pad,
+                                 int32_t B, int32_t n, const float *ibp_c, const float *ibp_r,
+                                 int64_t ld_ibp, int32_t intersect, const float *bias_next,
+                                 float *L, float *U, float4 *P, int64_t ldp, hipStream_t s) {
+  const int64_t tot = (int64_t)B * n;
+  hipLaunchKernelGGL(k_finalize_layer, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, beta, cpart,
+                     n_parts, M_pad, B, n, ibp_c, ibp_r, ld_ibp, intersect, bias_next, L, U, P, ldp);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------------
+// Spec rows folded into the last dense layer: CW[b, i, :] = C[b, i, :] W_L and
+// Cb[b, i] = C[b, i, :] b_L (sequential over the output neurons).
+__global__ void k_spec_cw(const float *C, int32_t B, int32_t m, int32_t n_out, const float *Wp, int64_t ldw,
+                          const float *bias, int32_t n_in, float *CW, int64_t ld_cw, float *Cb) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t rows = (int64_t)B * m;
+  if (idx >= rows * ld_cw) return;
+  const int64_t row = idx / ld_cw, n = idx - row * ld_cw;
+  const float *c = C + row * n_out;
+  float s = 0.f;
+  if (n < n_in)
+    for (int o = 0; o < n_out; ++o) s += c[o] * Wp[(int64_t)o * ldw + n];
+  CW[idx] = s;
+  if (n == 0) {
+    float sb = 0.f;
+    for (int o = 0; o < n_out; ++o) sb += c[o] * bias[o];
+    Cb[row] = sb;
+  }
+}
+
+hipError_t launch_spec_cw(const float *C, int32_t B, int32_t m, int32_t n_out, const float *Wp,
+                          int64_t ldw, const float *b, int32_t n_in, float *CW, int64_t ld_cw,
+                          float *Cb, hipStream_t s) {
+  const int64_t tot = (int64_t)B * m * ld_cw;
+  hipLaunchKernelGGL(k_spec_cw, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, C, B, m, n_out, Wp, ldw,
+                     b, n_in, CW, ld_cw, Cb);
+  return hipGetLastError();
+}
+
+// lb = CW . c - |CW| . r + Cb, ub = CW . c + |CW| . r + Cb over an input interval given as
+// centre/radius (optionally passed through ReLU first).  One wavefront per spec row.
+__global__ __launch_bounds__(256) void k_spec_direct(const float *CW, int64_t ld_cw, const float *Cb, int32_t B,
+                                                     int32_t m, int32_t n_in, const float *c, const float *r,
+                                                     int64_t ld_in, int32_t relu_in, float *lb, float *ub) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= (int64_t)B * m) return;
+  const int64_t b = row / m;
+  float dc = 0.f, dr = 0.f;
+  for (int64_t k = lane; k < n_in; k += 64) {
+    const float w = CW[row * ld_cw + k];
+    float cc = c[b * ld_in + k], rr = r[b * ld_in + k];
+    if (relu_in) {
+      const float lo = fmaxf(cc - rr, 0.f), hi = fmaxf(cc + rr, 0.f);
+      cc = (lo + hi) * 0.5f;
+      rr = (hi - lo) * 0.5f;
+    }
+    dc += w * cc;
+    dr += fabsf(w) * rr;
+  }
+  dc = wave_sum(dc);
+  dr = wave_sum(dr);
+  if (lane == 0) {
+    lb[row] = dc - dr + Cb[row];
+    ub[row] = dc + dr + Cb[row];
+  }
+}
+
+hipError_t launch_spec_direct(const float *CW, int64_t ld_cw, const float *Cb, int32_t B, int32_t m,
+                              int32_t n_in, const float *c, const float *r, int64_t ld_in,
+                              int32_t relu_in, float *lb, float *ub, hipStream_t s) {
+  const int64_t rows = (int64_t)B * m;
+  hipLaunchKernelGGL(k_spec_direct, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, CW, ld_cw, Cb, B, m,
+                     n_in, c, r, ld_in, relu_in, lb, ub);
+  return hipGetLastError();
+}
+
+// Final bounds per spec row: lb = beta + sum of concretization partials of the lower row,
+// ub = -(same for the negated row).  Infeasible units give (+inf, -inf), invalid ones NaN.
+__global__ void k_finalize_spec(const float *beta, const float *cpart, int32_t n_parts, int32_t M_pad,
+                                int32_t units, int32_t m, const int32_t *flags, float *lb, float *ub) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)units * m) return;
+  const int64_t u = idx / m, i = idx - u * m;
+  const int64_t ml = u * 2 * m + i, mu = ml + m;
+  float sl = 0.f, su = 0.f;
+  for (int p = 0; p < n_parts; ++p) {
+    sl += cpart[(int64_t)p * M_pad + ml];
+    su += cpart[(int64_t)p * M_pad + mu];
+  }
+  float l = beta[ml] + sl;
+  float h = -(beta[mu] + su);
+  const int f = flags ? flags[u] : 0;
+  if (f == 1) {
+    l = __int_as_float(0x7f800000);
+    h = -l;
+  } else if (f == 2) {
+    l = __int_as_float(0x7fc00000);
+    h = l;
+  }
+  lb[idx] = l;
+  ub[idx] = h;
+}
+
+hipError_t launch_finalize_spec(const float *beta, const float *cpart, int32_t n_parts, int32_t M_pad,
+                                int32_t units, int32_t m, const int32_t *unit_flags, float *lb,
+                                float *ub, hipStream_t s) {
+  const int64_t tot = (int64_t)units * m;
+  hipLaunchKernelGGL(k_finalize_spec, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, beta, cpart,
+                     n_parts, M_pad, units, m, unit_flags, lb, ub);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------------
+// Split table of branch-and-bound subdomains (paper, Sec. 2.1, complete verification).
+// One thread per domain validates its entries, clamps each split neuron's root interval
+// (active: l <- max(l, 0); inactive: u <- min(u, 0)), marks the domain infeasible if an
+// interval becomes empty, and stores the entries sorted by ReLU with their relaxation.
+constexpr int MAX_SPLITS = 64;
+
+__global__ void k_split_prepare(const SplitPrepArgs a) {
+  const int d = blockIdx.x * blockDim.x + threadIdx.x;
+  if (d >= a.D) return;
+  int er[MAX_SPLITS], en[MAX_SPLITS], es[MAX_SPLITS];
+  bool invalid = a.S > MAX_SPLITS;
+  int cnt = 0;
+  for (int k = 0; k < a.S && !invalid; ++k) {
+    const int r = a.relu_id[(int64_t)d * a.S + k];
+    const int j = a.neuron[(int64_t)d * a.S + k];
+    const int sg = a.sign[(int64_t)d * a.S + k];
+    if (r < 0 || r >= a.R || (sg != 1 && sg != -1)) {
+      invalid = true;
+      break;
+    }
+    if (j < 0 || j >= a.relu_n[r]) {
+      invalid = true;
+      break;
+    }
+    for (int e = 0; e < cnt; ++e)
+      if (er[e] == r && en[e] == j) invalid = true;
+    // insertion keeps entries sorted by ReLU (stable)
+    int pos = cnt;
+    while (pos > 0 && er[pos - 1] > r) {
+      er[pos] = er[pos - 1];
+      en[pos] = en[pos - 1];
+      es[pos] = es[pos - 1];
+      --pos;
+    }
+    er[pos] = r;
+    en[pos] = j;
+    es[pos] = sg;
+    ++cnt;
+  }
+  int32_t *off = a.off + (int64_t)d * (a.R + 1);
+  if (invalid) {
+    for (int r = 0; r <= a.R; ++r) off[r] = 0;
+    a.flags[d] = 2;
+    atomicAdd(a.n_invalid, 1);
+    return;
+  }
+  bool infeasible = false;
+  int e = 0;
+  for (int r = 0; r <= a.R; ++r) {
+    while (e < cnt && er[e] < r) ++e;
+    off[r] = e;
+  }
+  for (int k = 0; k < cnt; ++k) {
+    float l = a.L[er[k]][en[k]], u = a.U[er[k]][en[k]];
+    if (es[k] > 0)
+      l = fmaxf(l, 0.f);
+    else
+      u = fminf(u, 0.f);
+    if (l > u) infeasible = true;
+    a.ent_n[(int64_t)d * a.S + k] = en[k];
+    a.ent_p[(int64_t)d * a.S + k] = relax_params(l, u, 0.f);
+  }
+  a.flags[d] = infeasible ? 1 : 0;
+}
+
+hipError_t launch_split_prepare(const SplitPrepArgs &a, hipStream_t s) {
+  if (a.D <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_split_prepare, dim3((unsigned)((a.D + 63) / 64)), dim3(64), 0, s, a);
+  return hipGetLastError();
+}
+
+// Number of unstable neurons (l < 0 < u) in n entries.
+__global__ void k_count_unstable(const float *L, const float *U, int64_t n, int32_t *count) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  int v = (i < n && L[i] < 0.f && U[i] > 0.f) ? 1 : 0;
+  v += __shfl_xor(v, 32);
+  v += __shfl_xor(v, 16);
+  v += __shfl_xor(v, 8);
+  v += __shfl_xor(v, 4);
+  v += __shfl_xor(v, 2);
+  v += __shfl_xor(v, 1);
+  if ((threadIdx.x & 63) == 0 && v) atomicAdd(count, v);
+}
+
+hipError_t launch_count_unstable(const float *L, const float *U, int64_t n, int32_t *count, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_count_unstable, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, L, U, n, count);
+  return hipGetLastError();
+}
+
+}  // namespace vcr

@@ -1,0 +1,255 @@
+// fp32 MFMA GEMM of the CROWN backward step (paper, Sec. 2.1, equation "crown"; the
+// per-layer step A <- A Lambda_i W_i of Sec. 3.3.2), with the next ReLU's relaxation and
+// the bias accumulation fused into the epilogue.
+//
+// One launch computes, for coefficient rows A' (already relaxed for layer j) and the layer
+// weight W_j (given transposed, Bt = W_j^T, so both operands are K-contiguous):
+//
+//   a   = (A' W_j)[row, n]                           coefficient on h_{j-1}, neuron n
+//   EPI_RELAX      : a'  = a > 0 ? lam a : s a       lower rule of ReLU j-1 at neuron n
+//                    out[row, n] = a'
+//                    part[row] += min(a, 0) t + a' b_{j-1}[n]
+//                    (the relaxation intercept and the next linear layer's bias, i.e. the
+//                    constant terms this neuron adds to the bound)
+//   EPI_CONCRETIZE : part[row] += a c[n] - |a| r[n]  (j = 1: minimum of a . x over the box
+//                    with centre c and radius r); A_0 itself is never written
+//
+// Upper bounds run through the same code on negated rows (max f = -min(-f)).
+//
+// Tiling for gfx950: 256 threads = 4 wave64 in a 2 x 2 grid, each wave owns a 64 x 64
+// block of the 128 x 128 tile as 2 x 2 v_mfma_f32_32x32x2f32 accumulators (64 fp32 each
+// lane).  K advances 32 at a time through double-buffered LDS (rows padded to 36 floats so
+// the 128-bit LDS reads of 8/16 consecutive lanes hit distinct banks).  Each lane consumes
+// 16 consecutive k of its operand rows per K tile, so every MFMA operand comes from one
+// 128-bit LDS read (the k order inside a tile is permuted identically for A and B, which
+// leaves the contraction unchanged).  Partial sums per row are reduced over the 32 columns
+// a lane group holds with a fixed butterfly, so results are deterministic and do not depend
+// on which other rows share the tile.
+#include "kernels.h"
+
+namespace vcr {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int LDS_LD = BK + 4;
+constexpr int NTHREADS = 256;
+constexpr int GROUP_M = 8;
+
+__device__ __forceinline__ void map_tile(int bid, int G, int n_mt, int n_nt, int &mt, int &nt) {
+  // Workgroup ids are spread over the 8 XCDs round robin; hand each XCD a contiguous range
+  // of logical tiles so the tiles sharing operands also share that XCD's L2.
+  const int x = bid & 7, t = bid >> 3;
+  const int q = G >> 3, rem = G & 7;
+  const int logical = x * q + min(x, rem) + t;
+  // Grouped order: GROUP_M row blocks sweep every column tile together.
+  const int per_group = GROUP_M * n_nt;
+  const int g = logical / per_group;
+  const int first_m = g * GROUP_M;
+  const int gm = min(GROUP_M, n_mt - first_m);
+  const int idx = logical - g * per_group;
+  mt = first_m + idx % gm;
+  nt = idx / gm;
+}
+
+__device__ __forceinline__ float4 split_override(const SplitTable &st, int row, int relu, int n, float4 prm) {
+  int d = row / st.rows_per_domain;
+  d = d < st.D ? d : st.D - 1;
+  const int e0 = st.off[d * (st.R + 1) + relu];
+  const int e1 = st.off[d * (st.R + 1) + relu + 1];
+  for (int e = e0; e < e1; ++e) {
+    if (st.ent_n[d * st.S + e] == n) {
+      const float4 q = st.ent_p[d * st.S + e];
+      prm.x = q.x;
+      prm.y = q.y;
+      prm.z = q.z;
+    }
+  }
+  return prm;
+}
+
+__global__ __launch_bounds__(NTHREADS, 2) void k_gemm(const GemmArgs p) {
+  __shared__ __attribute__((aligned(16))) float As[2][BM * LDS_LD];
+  __shared__ __attribute__((aligned(16))) float Bs[2][BN * LDS_LD];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int n_mt = p.M_pad / BM, n_nt = p.N_pad / BN;
+  int mt, nt;
+  map_tile(blockIdx.x, n_mt * n_nt, n_mt, n_nt, mt, nt);
+  const int m0 = mt * BM, n0 = nt * BN;
+
+  // global -> register staging: thread t moves rows t/8 + 32q, columns 4(t%8)..+3
+  const int lrow = tid >> 3, lcol = (tid & 7) << 2;
+  const float *Ag = p.A + (int64_t)(m0 + lrow) * p.lda + lcol;
+  const float *Bg = p.Bt + (int64_t)(n0 + lrow) * p.ldb + lcol;
+  const int64_t a_step = 32 * p.lda, b_step = 32 * p.ldb;
+  f32x4 ra[4], rb[4];
+
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  const int KT = p.K / BK;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    ra[q] = *reinterpret_cast<const f32x4 *>(Ag + q * a_step);
+    rb[q] = *reinterpret_cast<const f32x4 *>(Bg + q * b_step);
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    *reinterpret_cast<f32x4 *>(&As[0][(lrow + 32 * q) * LDS_LD + lcol]) = ra[q];
+    *reinterpret_cast<f32x4 *>(&Bs[0][(lrow + 32 * q) * LDS_LD + lcol]) = rb[q];
+  }
+  __syncthreads();
+
+  const int r32 = lane & 31;
+  const int kq = (lane >> 5) * 16;
+  const int a_off0 = (wm * 64 + r32) * LDS_LD + kq;
+  const int a_off1 = a_off0 + 32 * LDS_LD;
+  const int b_off0 = (wn * 64 + r32) * LDS_LD + kq;
+  const int b_off1 = b_off0 + 32 * LDS_LD;
+
+  for (int kt = 0; kt < KT; ++kt) {
+    const int cur = kt & 1;
+    const bool more = kt + 1 < KT;
+    if (more) {
+      const int k0 = (kt + 1) * BK;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        ra[q] = *reinterpret_cast<const f32x4 *>(Ag + q * a_step + k0);
+        rb[q] = *reinterpret_cast<const f32x4 *>(Bg + q * b_step + k0);
+      }
+    }
+    const float *as = As[cur];
+    const float *bs = Bs[cur];
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      const f32x4 a0 = *reinterpret_cast<const f32x4 *>(as + a_off0 + 4 * h);
+      const f32x4 a1 = *reinterpret_cast<const f32x4 *>(as + a_off1 + 4 * h);
+      const f32x4 b0 = *reinterpret_cast<const f32x4 *>(bs + b_off0 + 4 * h);
+      const f32x4 b1 = *reinterpret_cast<const f32x4 *>(bs + b_off1 + 4 * h);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0[e], b0[e], acc[0][0], 0, 0, 0);
+        acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0[e], b1[e], acc[0][1], 0, 0, 0);
+        acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[e], b0[e], acc[1][0], 0, 0, 0);
+        acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[e], b1[e], acc[1][1], 0, 0, 0);
+      }
+    }
+    if (more) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        *reinterpret_cast<f32x4 *>(&As[cur ^ 1][(lrow + 32 * q) * LDS_LD + lcol]) = ra[q];
+        *reinterpret_cast<f32x4 *>(&Bs[cur ^ 1][(lrow + 32 * q) * LDS_LD + lcol]) = rb[q];
+      }
+    }
+    __syncthreads();
+  }
+
+  // ---- epilogue ---------------------------------------------------------------------
+  // 32x32 accumulator layout: lane holds column (lane % 32) and rows
+  // 8 (v / 4) + 4 (lane / 32) + (v % 4), v = 0..15.
+  const int half = lane >> 5;
+  const bool uniform_unit = (p.rows_per_unit % BM) == 0;
+  int unit_tile = m0 / p.rows_per_unit;
+  unit_tile = unit_tile < p.n_units ? unit_tile : p.n_units - 1;
+  const bool has_splits = p.splits.D > 0;
+
+  float rp[2][16];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) rp[i][v] = 0.f;
+
+#pragma unroll
+  for (int bj = 0; bj < 2; ++bj) {
+    const int n = n0 + wn * 64 + bj * 32 + r32;
+    if (p.mode == EPI_RELAX) {
+      float4 prm_tile = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (uniform_unit) prm_tile = p.P[(int64_t)unit_tile * p.ldp + n];
+#pragma unroll
+      for (int bi = 0; bi < 2; ++bi) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int row = m0 + wm * 64 + bi * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
+          float4 prm = prm_tile;
+          if (!uniform_unit) {
+            int u = row / p.rows_per_unit;
+            u = u < p.n_units ? u : p.n_units - 1;
+            prm = p.P[(int64_t)u * p.ldp + n];
+          }
+          if (has_splits) prm = split_override(p.splits, row, p.relu_index, n, prm);
+          const float a = acc[bi][bj][v];
+          const float ap = a > 0.f ? a * prm.x : a * prm.y;
+          p.out[(int64_t)row * p.ldo + n] = ap;
+          rp[bi][v] += fminf(a, 0.f) * prm.z + ap * prm.w;
+        }
+      }
+    } else {
+      float c_tile = 0.f, r_tile = 0.f;
+      if (uniform_unit) {
+        c_tile = p.c0[(int64_t)unit_tile * p.ldc + n];
+        r_tile = p.r0[(int64_t)unit_tile * p.ldc + n];
+      }
+#pragma unroll
+      for (int bi = 0; bi < 2; ++bi) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int row = m0 + wm * 64 + bi * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
+          float c = c_tile, r = r_tile;
+          if (!uniform_unit) {
+            int u = row / p.rows_per_unit;
+            u = u < p.n_units ? u : p.n_units - 1;
+            c = p.c0[(int64_t)u * p.ldc + n];
+            r = p.r0[(int64_t)u * p.ldc + n];
+          }
+          const float a = acc[bi][bj][v];
+          rp[bi][v] += a * c - fabsf(a) * r;
+        }
+      }
+    }
+  }
+
+  // fixed butterfly over the 32 lanes that share rows
+#pragma unroll
+  for (int bi = 0; bi < 2; ++bi) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      float x = rp[bi][v];
+      x += __shfl_xor(x, 16);
+      x += __shfl_xor(x, 8);
+      x += __shfl_xor(x, 4);
+      x += __shfl_xor(x, 2);
+      x += __shfl_xor(x, 1);
+      rp[bi][v] = x;
+    }
+  }
+  if (r32 == 0) {
+    float *dst = p.part + (int64_t)(nt * 2 + wn) * p.M_pad;
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = m0 + wm * 64 + bi * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
+        dst[row] = rp[bi][v];
+      }
+  }
+}
+
+hipError_t launch_gemm(const GemmArgs &a, hipStream_t s) {
+  if (a.M_pad % BM || a.N_pad % BN || a.K % BK || a.K <= 0 || a.M_pad <= 0 || a.N_pad <= 0)
+    return hipErrorInvalidValue;
+  const int64_t grid = (int64_t)(a.M_pad / BM) * (a.N_pad / BN);
+  if (grid > 0x7fffffff) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_gemm, dim3((unsigned)grid), dim3(NTHREADS), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace vcr

@@ -1,0 +1,120 @@
+// Internal launch interface of the vcrown HIP kernels (not part of the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace vcr {
+
+// GEMM tile: BM x BN output per workgroup, BK deep K steps; every padded width is a
+// multiple of LD_ALIGN so a padded row is whole tiles in both the K and the N role.
+constexpr int BM = 128;
+constexpr int BN = 128;
+constexpr int BK = 32;
+constexpr int LD_ALIGN = 128;
+constexpr int PART_COLS = 64;   // columns summed into one bias partial (one wave's slab)
+
+inline int64_t ld_of(int64_t n) { return (n + LD_ALIGN - 1) / LD_ALIGN * LD_ALIGN; }
+inline int64_t rows_pad(int64_t m) { return (m + BM - 1) / BM * BM; }
+
+// Per-domain ReLU overrides for branch-and-bound subdomains, built on the device.
+struct SplitTable {
+  const int32_t *off = nullptr;   // [D][R+1] start of each ReLU's entries in ent_*
+  const int32_t *ent_n = nullptr; // [D][S] neuron of each entry (sorted by ReLU)
+  const float4 *ent_p = nullptr;  // [D][S] (lam, s, t, 0) after the split is applied
+  int32_t R = 0, S = 0, D = 0;
+  int32_t rows_per_domain = 0;
+};
+
+enum EpiMode : int32_t { EPI_RELAX = 0, EPI_CONCRETIZE = 1 };
+
+struct GemmArgs {
+  const float *A;      // M_pad x lda, coefficient rows (already relaxed), zero padded
+  const float *Bt;     // N_pad x ldb, the layer weight transposed, zero padded
+  int64_t lda, ldb;
+  int32_t M;           // real rows (rows >= M are padding)
+  int32_t M_pad;       // multiple of BM
+  int32_t K;           // multiple of BK (padded)
+  int32_t N_pad;       // multiple of BN
+  int32_t mode;        // EpiMode
+  // relax epilogue: out = relax(A Bt^T) with the per-unit parameters of the next ReLU
+  float *out;
+  int64_t ldo;
+  const float4 *P;     // [units][ldp] (lam, s, t, bias of the layer below)
+  int64_t ldp;
+  int32_t relu_index;  // which ReLU the parameters belong to (split lookup)
+  SplitTable splits;   // D == 0: no splits
+  // concretize epilogue: partial sums of a.c - |a|.r per row
+  const float *c0, *r0;
+  int64_t ldc;
+  int32_t rows_per_unit;   // rows of one input (intermediate: 2 n_k; final: 2 m)
+  int32_t n_units;         // number of inputs that own rows (clamp for padding rows)
+  float *part;             // [N_pad / PART_COLS][M_pad] per-row partial sums
+};
+
+hipError_t launch_gemm(const GemmArgs &a, hipStream_t s);
+
+// ---- bandwidth-bound kernels -------------------------------------------------------
+hipError_t launch_fill(float *p, int64_t n, float v, hipStream_t s);
+hipError_t launch_transpose_pad(const float *W, int32_t rows, int32_t cols, float *Wt, int64_t ldt,
+                                int64_t rows_t, hipStream_t s);
+hipError_t launch_box(const float *x0, int32_t B, int32_t n0, int64_t ld0, float eps, int32_t clip_on,
+                      float clip_lo, float clip_hi, float *c0, float *r0, hipStream_t s);
+hipError_t launch_ibp_dense(const float *Wp, int64_t ldw, const float *b, int32_t n_out, int32_t n_in,
+                            const float *cin, const float *rin, int64_t ld_in, int32_t relu_in,
+                            float *cout, float *rout, int64_t ld_out, int32_t B, hipStream_t s);
+hipError_t launch_layer_from_ibp(const float *c, const float *r, int64_t ld, int32_t n, int32_t B,
+                                 const float *bias, float *L, float *U, float4 *P, int64_t ldp,
+                                 hipStream_t s);
+struct InitArgs {
+  const float *src;      // source rows (W_k, or C W_L per input)
+  int64_t ld_src;
+  int32_t n_src;         // rows of one direction (n_k or m)
+  int32_t per_unit_src;  // 1: unit u reads rows u*n_src + i (spec per input); 0: shared rows
+  const float *src_bias; // (n_src) or (units * n_src) like src
+  int32_t n_cols;        // real columns (width of the layer below)
+  int64_t ldo;           // output row stride (padded)
+  int32_t M;             // rows = units * 2 * n_src
+  int32_t units;
+  const float4 *P;       // params of the ReLU below, [param_units][ldp]
+  int64_t ldp;
+  int32_t param_per_unit;  // 1: unit u uses P row u; 0: row 0 (BaB: all domains share the root)
+  int32_t relu_index;
+  SplitTable splits;
+  float *out;            // M_pad x ldo
+  float *beta;           // M_pad
+};
+hipError_t launch_init_rows(const InitArgs &a, hipStream_t s);
+hipError_t launch_rowsum(float *beta, const float *part, int32_t n_parts, int32_t M_pad, int32_t M,
+                         hipStream_t s);
+hipError_t launch_finalize_layer(const float *beta, const float *cpart, int32_t n_parts, int32_t M_pad,
+                                 int32_t B, int32_t n, const float *ibp_c, const float *ibp_r,
+                                 int64_t ld_ibp, int32_t intersect, const float *bias_next,
+                                 float *L, float *U, float4 *P, int64_t ldp, hipStream_t s);
+hipError_t launch_spec_cw(const float *C, int32_t B, int32_t m, int32_t n_out, const float *Wp,
+                          int64_t ldw, const float *b, int32_t n_in, float *CW, int64_t ld_cw,
+                          float *Cb, hipStream_t s);
+hipError_t launch_spec_direct(const float *CW, int64_t ld_cw, const float *Cb, int32_t B, int32_t m,
+                              int32_t n_in, const float *c, const float *r, int64_t ld_in,
+                              int32_t relu_in, float *lb, float *ub, hipStream_t s);
+hipError_t launch_finalize_spec(const float *beta, const float *cpart, int32_t n_parts, int32_t M_pad,
+                                int32_t units, int32_t m, const int32_t *unit_flags, float *lb,
+                                float *ub, hipStream_t s);
+struct SplitPrepArgs {
+  const int32_t *relu_id, *neuron;
+  const int8_t *sign;
+  int32_t D, S, R;
+  const int32_t *relu_n;     // [R] neurons per ReLU (device)
+  const float *const *L;     // [R] device pointers to the root's lower bounds
+  const float *const *U;     // [R] upper bounds
+  int32_t *off;              // [D][R+1]
+  int32_t *ent_n;            // [D][S]
+  float4 *ent_p;             // [D][S]
+  int32_t *flags;            // [D] 0 ok, 1 infeasible, 2 invalid
+  int32_t *n_invalid;        // one counter
+};
+hipError_t launch_split_prepare(const SplitPrepArgs &a, hipStream_t s);
+hipError_t launch_count_unstable(const float *L, const float *U, int64_t n, int32_t *count, hipStream_t s);
+hipError_t launch_copy(float *dst, const float *src, int64_t n, hipStream_t s);
+
+}  // namespace vcr
