@@ -62,6 +62,29 @@ def cpu_baseline(wl, budget_s):
             "cpu_count": os.cpu_count()}
 
 
+def cpu_baseline_bab(wl, sp, budget_s):
+    """The fp64 oracle on the same subdomains: its root pass, then domains until the time
+    budget is used; reported as domains/s of the domain evaluations plus the root pass."""
+    import threadpoolctl
+    import oracle
+    from workloads import Splits
+    splits = Splits(sp["relu_id"], sp["neuron"], sp["sign"])
+    t0 = time.perf_counter()
+    root = oracle.crown(wl.net, wl.x0[0], wl.eps, wl.C[0])
+    t_root = time.perf_counter() - t0
+    n = 0
+    t1 = time.perf_counter()
+    while n < splits.n_domains and time.perf_counter() - t0 < budget_s:
+        oracle.crown_domains(wl.net, root, wl.C[0], splits, domains=range(n, n + 16))
+        n += 16
+    t_dom = time.perf_counter() - t1
+    total = t_root + t_dom * splits.n_domains / n
+    threads = max((p.get("num_threads", 1) for p in threadpoolctl.threadpool_info()), default=1)
+    return {"value": splits.n_domains / total, "unit": "domains/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"root pass ({t_root:.1f} s) + first {n} of {splits.n_domains} domains ({t_dom:.1f} s), "
+                      f"domain time scaled to all domains", "cpu_count": os.cpu_count()}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -69,7 +92,20 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="mlp784x1024x6")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time (0: skip)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB three times (HBM counter calibration)")
     args = ap.parse_args()
+    if args.copy_calibration:
+        import torch
+        n = args.copy_calibration * (1 << 20) // 4
+        src = torch.rand(n, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "launches": 3}))
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus})",
               file=sys.stderr)
@@ -87,25 +123,50 @@ def main():
     ctx.load_net(wl.net)
     x0 = torch.from_numpy(wl.x0).cuda()
     C = torch.from_numpy(wl.C).cuda()
-    lb = torch.empty((B, m), dtype=torch.float32, device="cuda")
-    ub = torch.empty((B, m), dtype=torch.float32, device="cuda")
+    splits = None
+    units, unit = B, "inputs/s"
+    if args.workload.startswith("bab_"):
+        # subdomains drawn once from the oracle root pass (stored with the tests)
+        sp = np.load(os.path.join(ROOT, "tests", "golden", f"{args.workload}_splits.npz"))
+        splits = tuple(torch.from_numpy(np.ascontiguousarray(sp[k])).cuda() for k in ("relu_id", "neuron", "sign"))
+        units, unit = splits[0].shape[0], "domains/s"
+    lb = torch.empty((units, m), dtype=torch.float32, device="cuda")
+    ub = torch.empty((units, m), dtype=torch.float32, device="cuda")
+
+    def step():
+        ctx.crown_bounds(x0, wl.eps, C, splits=splits, out=(lb, ub))
+
     for _ in range(args.warmup):
-        ctx.crown_bounds(x0, wl.eps, C, out=(lb, ub))
+        step()
     torch.cuda.synchronize()
     flops_call = ctx.stats()["gemm_flops_last_call"]
     ctx.set_option(OPT_TIME_GEMM, 1)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        ctx.crown_bounds(x0, wl.eps, C, out=(lb, ub))
+        step()
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     st = ctx.stats()
     ctx.set_option(OPT_TIME_GEMM, 0)
     assert np.all(np.isfinite(lb.cpu().numpy()))
+    extra = {}
+    if splits is not None:
+        # the root pass alone (one input, no subdomains), to report domains/s without it
+        rl = torch.empty((1, m), dtype=torch.float32, device="cuda")
+        ru = torch.empty((1, m), dtype=torch.float32, device="cuda")
+        ctx.crown_bounds(x0, wl.eps, C, out=(rl, ru))
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        for _ in range(args.steps):
+            ctx.crown_bounds(x0, wl.eps, C, out=(rl, ru))
+        torch.cuda.synchronize()
+        root_ms = (time.perf_counter() - t1) / args.steps * 1e3
+        extra = {"root_pass_ms": root_ms,
+                 "domains_per_s_without_root": units / ((dt / args.steps * 1e3 - root_ms) / 1e3)}
 
     ms_step = dt / args.steps * 1e3
-    value = B * args.steps / dt
+    value = units * args.steps / dt
     launches = st["timed_gemm_launches"]
     gemm_s = st["timed_gemm_ms"] / 1e3
     achieved = st["timed_gemm_flops"] / gemm_s / 1e12 if gemm_s > 0 else None
@@ -113,7 +174,7 @@ def main():
     rec = {
         "metric": "CROWN bound evals/sec (inputs or BaB domains) at 1 GPU; % fp32 MFMA peak",
         "value": value,
-        "unit": "inputs/s",
+        "unit": unit,
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -124,6 +185,7 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": args.workload, "batch": B, "eps": float(wl.eps), "spec_rows": m,
+                   "domains": units if splits is not None else None,
                    "layers": [int(wl.net.nodes[0].W.shape[1])] + [int(nd.W.shape[0]) for nd in wl.net.nodes
                                                                    if nd.op == "dense"],
                    "method": "full CROWN (IBP-intersected intermediate bounds)"},
@@ -137,8 +199,11 @@ def main():
         "call_mfma_frac": flops_call / (ms_step / 1e3) / (PEAK_FP32_MFMA_TFLOPS * 1e12),
         "gemm_flops_per_step": flops_call,
     }
-    if args.cpu_budget > 0:
+    rec.update(extra)
+    if args.cpu_budget > 0 and splits is None:
         rec["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
+    elif args.cpu_budget > 0:
+        rec["cpu_baseline"] = cpu_baseline_bab(wl, sp, args.cpu_budget)
     print(json.dumps(rec), flush=True)
 
 

@@ -1,9 +1,13 @@
-"""Write the stored oracle results used by the GPU parity tests.
+"""Write the stored oracle results used by the GPU parity tests and the bench.
 
-Calls only the fp64 oracle (oracle/) on the seeded workloads (workloads/).  Each file holds
-the final bounds and every ReLU layer's pre-activation bounds of the listed inputs.
+Calls only the fp64 oracle (oracle/) on the seeded workloads (workloads/).
+  * <workload>.npz: the final bounds and every ReLU layer's pre-activation bounds of the
+    listed inputs;
+  * bab_mlp784x1024x6_splits.npz: the branch-and-bound subdomains of that workload, drawn
+    from the oracle root pass's unstable neurons (the draw continues the workload's seeded
+    generator, so it equals what the tests draw at run time).
 
-  python tests/golden/make_goldens.py [name ...]
+  python tests/golden/make_goldens.py [name ...]     (name "bab" for the split file)
 """
 import os
 import sys
@@ -42,7 +46,21 @@ def make(name, inputs):
     print("wrote", path)
 
 
+def make_bab_splits():
+    from workloads import draw_splits
+    wl = make_workload("bab_mlp784x1024x6")
+    root = oracle.crown(wl.net, wl.x0[0], wl.eps, wl.C[0])
+    pool = oracle.unstable_pool(wl.net, root)
+    sp = draw_splits(wl.rng, pool, 4096, 8)
+    path = os.path.join(HERE, "bab_mlp784x1024x6_splits.npz")
+    np.savez_compressed(path, relu_id=sp.relu_id, neuron=sp.neuron, sign=sp.sign)
+    print("wrote", path, "pool", len(pool))
+
+
 if __name__ == "__main__":
-    names = sys.argv[1:] or list(GOLDENS)
+    names = sys.argv[1:] or list(GOLDENS) + ["bab"]
     for n in names:
-        make(n, GOLDENS[n])
+        if n == "bab":
+            make_bab_splits()
+        else:
+            make(n, GOLDENS[n])
