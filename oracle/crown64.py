@@ -90,7 +90,7 @@ def conv2d(x, W, stride, pad):
     for i in range(kh):
         for j in range(kw):
             patch = xp[:, i:i + stride * (ho - 1) + 1:stride, j:j + stride * (wo - 1) + 1:stride]
-            out += np.einsum("oc,cyx->oyx", W[:, :, i, j], patch)
+            out += np.tensordot(W[:, :, i, j], patch, axes=([1], [0]))
     return out
 
 
@@ -109,7 +109,7 @@ def conv2d_transpose(A, W, stride, pad, in_hw):
     out = np.zeros((rows, ci, hp, wp))
     for i in range(kh):
         for j in range(kw):
-            contrib = np.einsum("royx,oc->rcyx", A, W[:, :, i, j])
+            contrib = np.tensordot(A, W[:, :, i, j], axes=([1], [0])).transpose(0, 3, 1, 2)
             out[:, :, i:i + stride * (ho - 1) + 1:stride, j:j + stride * (wo - 1) + 1:stride] += contrib
     return out[:, :, pad:pad + h, pad:pad + w]
 

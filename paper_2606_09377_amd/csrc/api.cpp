@@ -27,81 +27,21 @@
 #include <string>
 #include <vector>
 
-#include "../../include/vcrown.h"
-#include "kernels.h"
+#include "ctx.h"
 
 using namespace vcr;
 
-namespace {
-
-struct DenseLayer {
-  int32_t n_in = 0, n_out = 0;
-  int64_t ld_in = 0, ld_out = 0;
-  float *Wp = nullptr;   // n_out x ld_in, zero padded
-  float *Bt = nullptr;   // ld_in x ld_out, Bt[n][k] = W[k][n], zero padded
-  float *b = nullptr;    // ld_out, zero padded
-};
-
-struct Workspace {
-  char *base = nullptr;
-  size_t cap = 0, used = 0;
-};
-
-}  // namespace
-
-struct vcr_ctx {
-  int32_t device = -1;
-  hipStream_t stream = nullptr;
-  std::string err;
-  // options
-  int32_t clip_on = 1;
-  float clip_lo = 0.f, clip_hi = 1.f;
-  int32_t intersect = 1;
-  uint64_t ws_cap = 0;
-  int32_t sync_check = 0;
-  // network
-  bool loaded = false;
-  int32_t n0 = 0;
-  std::vector<DenseLayer> layers;   // the MLP chain
-  std::vector<int32_t> relu_n;      // neurons per ReLU node
-  std::vector<vcr_node> node_desc;  // validated node list (weights not retained)
-  // workspace
-  Workspace ws;
-  uint64_t peak_ws = 0;
-  // last call
-  int32_t last_B = 0;
-  std::vector<float *> lastL, lastU;
-  int32_t *d_counters = nullptr;    // [64] unstable counts + [1] invalid domains
-  bool last_had_splits = false;
-  double ms_last = 0.0;
-  uint64_t flops_last = 0;
-  int32_t chunks_last = 0;
-  // GEMM timing (VCR_OPT_TIME_GEMM)
-  int32_t time_gemm = 0;
-  std::vector<hipEvent_t> ev_pool;      // pairs: start, stop
-  size_t ev_used = 0;                   // events recorded but not yet read
-  uint64_t timed_launches = 0, timed_flops = 0;
-  double timed_ms = 0.0;
-  std::vector<uint64_t> pending_flops;  // flops of each recorded pair
-};
+namespace vcr {
+vcr_status graph_load(vcr_ctx *c, const vcr_node *nodes, int32_t n, const int32_t in_chw[3],
+                      const std::vector<std::vector<int64_t>> &sh);
+vcr_status graph_crown(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m,
+                       const vcr_splits *splits, float *lb, float *ub);
+vcr_status graph_ibp(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m, float *lb,
+                     float *ub);
+size_t graph_workspace_bytes(vcr_ctx *c, int32_t B, int32_t m);
+}  // namespace vcr
 
 namespace {
-
-vcr_status fail(vcr_ctx *c, vcr_status st, const char *fmt, ...) {
-  char buf[512];
-  va_list ap;
-  va_start(ap, fmt);
-  vsnprintf(buf, sizeof(buf), fmt, ap);
-  va_end(ap);
-  c->err = buf;
-  return st;
-}
-
-#define HIP_TRY(c, expr)                                                                      \
-  do {                                                                                        \
-    hipError_t e_ = (expr);                                                                   \
-    if (e_ != hipSuccess) return fail((c), VCR_ERR_DEVICE, "%s: %s", #expr, hipGetErrorString(e_)); \
-  } while (0)
 
 void free_layers(vcr_ctx *c) {
   for (auto &L : c->layers) {
@@ -127,7 +67,6 @@ struct Plan {
   size_t bytes = 0;
 };
 
-size_t al(size_t x) { return (x + 255) / 256 * 256; }
 
 int64_t max_inter_rows_per_input(const vcr_ctx *c) {
   int64_t r = 0;
@@ -172,6 +111,8 @@ vcr_status make_plan(vcr_ctx *c, int32_t B, int32_t m, int32_t D, int32_t S, Pla
   return VCR_OK;
 }
 
+}  // namespace
+
 vcr_status ensure_ws(vcr_ctx *c, size_t bytes) {
   if (c->ws.cap >= bytes) {
     c->ws.used = 0;
@@ -194,19 +135,8 @@ vcr_status ensure_ws(vcr_ctx *c, size_t bytes) {
   return VCR_OK;
 }
 
-// Sub-allocation from the workspace.  With a null base it only counts bytes, which is how
-// the planner sizes a call: the same carve code runs for sizing and for the real layout.
-template <class T>
-T *take(Workspace &w, size_t count) {
-  size_t b = al(sizeof(T) * std::max<size_t>(count, 1));
-  T *p = w.base ? reinterpret_cast<T *>(w.base + w.used) : nullptr;
-  w.used += b;
-  return p;
-}
-template <class T>
-T *take(vcr_ctx *c, size_t count) {
-  return take<T>(c->ws, count);
-}
+namespace {
+
 
 // ---- validation ---------------------------------------------------------------------
 vcr_status validate_net(vcr_ctx *c, const vcr_node *nodes, int32_t n, const int32_t in_chw[3],
@@ -333,6 +263,7 @@ void vcr_destroy(vcr_ctx *c) {
     if (c->d_counters) (void)hipFree(c->d_counters);
     for (auto e : c->ev_pool) (void)hipEventDestroy(e);
   }
+  destroy_graph(c->graph);
   delete c;
 }
 
@@ -383,7 +314,25 @@ vcr_status vcr_load_net(vcr_ctx *c, const vcr_node *nodes, int32_t n, const int3
       return fail(c, VCR_ERR_SHAPE, "node %d: dense input must be flat (insert a flatten node)", i);
   }
   st = check_chain(c, nodes, n, in_chw, sh);
+  if (st == VCR_ERR_UNSUPPORTED) {
+    // not an MLP chain: the convolutional-network path
+    const std::string mlp_err = c->err;
+    if (c->device >= 0) {
+      HIP_TRY(c, hipSetDevice(c->device));
+      HIP_TRY(c, hipStreamSynchronize(c->stream));
+      free_layers(c);
+      free_ws(c);
+    }
+    c->loaded = false;
+    c->layers.clear();
+    st = graph_load(c, nodes, n, in_chw, sh);
+    if (st != VCR_OK) return st;
+    c->loaded = true;
+    return VCR_OK;
+  }
   if (st != VCR_OK) return st;
+  destroy_graph(c->graph);
+  c->graph = nullptr;
   if (c->device < 0) {
     // validation-only context: remember the shapes for argument checks
     c->loaded = true;
@@ -798,7 +747,7 @@ vcr_status vcr_crown_bounds(vcr_ctx *c, const float *x0, int32_t B, float eps, c
     if (c->relu_n.empty()) return fail(c, VCR_ERR_ARG, "splits need at least one ReLU");
     if ((int64_t)splits->n_domains * m > (int64_t)1 << 30) return fail(c, VCR_ERR_SHAPE, "n_domains * m too large");
   }
-  st = crown_impl(c, x0, B, eps, C, m, splits, lb, ub);
+  st = c->graph ? graph_crown(c, x0, B, eps, C, m, splits, lb, ub) : crown_impl(c, x0, B, eps, C, m, splits, lb, ub);
   return after_call(c, st, t0);
 }
 
@@ -809,6 +758,7 @@ vcr_status vcr_ibp_bounds(vcr_ctx *c, const float *x0, int32_t B, float eps, con
   vcr_status st = check_common(c, x0, B, eps, C, m, lb, ub);
   if (st != VCR_OK) return st;
   if (c->device < 0) return fail(c, VCR_ERR_STATE, "validation-only context: no device work");
+  if (c->graph) return after_call(c, graph_ibp(c, x0, B, eps, C, m, lb, ub), t0);
   HIP_TRY(c, hipSetDevice(c->device));
   const int L = (int)c->layers.size();
   const int64_t ld0 = ld_of(c->n0);
@@ -855,6 +805,11 @@ vcr_status vcr_workspace_bytes(vcr_ctx *c, int32_t B, int32_t m, int32_t n_domai
   if (!c || !bytes) return VCR_ERR_ARG;
   if (!c->loaded) return fail(c, VCR_ERR_STATE, "no network loaded");
   if (B <= 0 || m <= 0 || n_domains < 0) return fail(c, VCR_ERR_ARG, "bad sizes");
+  if (c->graph) {
+    if (n_domains > 0) return fail(c, VCR_ERR_UNSUPPORTED, "subdomain splits are built for MLPs only");
+    *bytes = graph_workspace_bytes(c, B, m);
+    return VCR_OK;
+  }
   const uint64_t cap = c->ws_cap;
   c->ws_cap = 0;
   Plan p;

@@ -1,0 +1,88 @@
+// Internal launch interface of the convolutional-path kernels (not part of the C ABI).
+#pragma once
+
+#include "kernels.h"
+
+namespace vcr {
+
+// floor(n / d) by multiply-high (n < 2^31), computed on the host
+struct FastDiv {
+  uint32_t mul = 0, shift = 0;
+};
+FastDiv make_fastdiv(uint32_t d);
+
+struct ConvTArgs {
+  const float *A;          // source windows [R][S_out][S_out][C_out]
+  int64_t row_stride_out;  // S_out^2 C_out
+  int32_t S_out, C_out;
+  const float *Bt;         // [N_pad][ldb], ldb = K = 9 C_out
+  int64_t ldb;
+  int32_t K, N_pad;
+  int32_t C_in, S_in, H_in;  // destination channels, window size, image size
+  int64_t row_stride_in;     // S_in^2 C_in
+  int32_t stride, delta;
+  int32_t M, M_pad;          // GEMM rows R * S_in^2
+  FastDiv div_S2, div_S;
+  const int4 *rows;          // per coefficient row: (unit, anchor y, anchor x, -)
+  int32_t dense, scale, h_in;  // window origin = anchor * scale - h_in (dense: 0)
+  const float *res;          // optional residual windows on the same node
+  int64_t res_row_stride;
+  int32_t res_S, res_off;
+  const float4 *P_pos;       // ReLU parameters [unit][H][H][C_in], or null (identity)
+  const float *bias;         // identity: constant per channel
+  float *out;                // [R][S_in][S_in][C_in]
+  float *part;               // [N_pad / 64][M_pad]
+};
+hipError_t launch_convt(const ConvTArgs &a, hipStream_t s);
+
+struct StemArgs {
+  const float *A;
+  int64_t row_stride_out;
+  int32_t S_out, C_out;
+  const float *W;          // [C_out][C_in][3][3]
+  int32_t C_in, S_in, H_in, stride, delta;
+  int32_t R, cc;           // rows, channels staged per LDS pass
+  const int4 *rows;
+  int32_t dense, scale, h_in;
+  const float *c0, *r0;    // box centre / radius, CHW per unit
+  int64_t ld_box;          // floats per unit in c0 / r0
+  float *part;             // [R][S_in^2]
+};
+hipError_t launch_stem(const StemArgs &a, hipStream_t s);
+
+struct ConvInitArgs {
+  const float *W;          // start convolution [C_src][C_in][3][3]
+  const float *b;          // its bias
+  int32_t C_src, H_src;    // start node shape (C_src, H_src, H_src)
+  int32_t C_in, H_in;      // the convolution's input node
+  int32_t S, h, scale;     // window 3, half 1, stride
+  int64_t R;
+  const int4 *rows;
+  const float4 *P_pos;     // ReLU below (channels-last) or null
+  const float *bias_next;  // identity constants per input channel
+  float *out;
+  float *beta;
+};
+hipError_t launch_init_conv(const ConvInitArgs &a, hipStream_t s);
+hipError_t launch_rowsum_win(float *beta, const float *part, int32_t n_parts, int64_t M_pad, int64_t R,
+                             int32_t per_row, hipStream_t s);
+hipError_t launch_row_table(int4 *rows, int64_t R, int32_t rows_per_unit, int32_t C, int32_t H, int32_t W,
+                            int32_t windowed, int32_t unit0, hipStream_t s);
+hipError_t launch_finalize_conv(const float *beta, int32_t B, int32_t C, int32_t H, const float *ibp_c,
+                                const float *ibp_r, int64_t ld_ibp, int32_t intersect, const float *bias_next,
+                                float *L, float *U, float4 *P, hipStream_t s);
+hipError_t launch_conv_layer_from_ibp(const float *ibp_c, const float *ibp_r, int64_t ld_ibp, int32_t B, int32_t C,
+                                      int32_t H, const float *bias_next, float *L, float *U, float4 *P,
+                                      hipStream_t s);
+hipError_t launch_ibp_conv(const float *W, const float *bias, int32_t Co, int32_t Ci, int32_t Hin, int32_t Hout,
+                           int32_t stride, int32_t pad, const float *cin, const float *rin, int64_t ld_in,
+                           float *cout, float *rout, int64_t ld_out, int32_t B, hipStream_t s);
+hipError_t launch_ibp_relu(const float *cin, const float *rin, float *cout, float *rout, int64_t n, hipStream_t s);
+hipError_t launch_ibp_add(const float *c1, const float *r1, const float *c2, const float *r2, float *cout,
+                          float *rout, int64_t n, hipStream_t s);
+hipError_t launch_repack_convt(const float *W, int32_t Co, int32_t Ci, int32_t Ci_pad, float *Bt, hipStream_t s);
+hipError_t launch_permute_hwc(const float *W, int32_t rows, int32_t C, int32_t HW, float *Wo, int64_t ldo,
+                              hipStream_t s);
+hipError_t launch_identity_params(const float *b, int32_t C, int64_t n, int64_t ld, float4 *P, hipStream_t s);
+
+}  // namespace vcr

@@ -1,0 +1,586 @@
+// CROWN backward through convolutions (paper, Sec. 4.8 extends bound propagation to
+// BoundConv; the step is the transpose of the convolution applied to every coefficient
+// row), residual additions and flatten, on windowed coefficient rows.
+//
+// Coefficient rows of a convolutional node are stored channels-last, one square window per
+// row: A[r][u][w][c], u, w in [0, S), c in [0, C).  A row that starts at one neuron (c0, i, j)
+// of a 3x3 convolution output is nonzero only inside that neuron's receptive field, so the
+// window has half-size h around the row's anchor (i, j) (scaled to the node's resolution)
+// and grows by one per stride-1 3x3 convolution (2h + 1 through stride 2).  Rows of a
+// dense node (spec rows, fully connected neurons) use the whole image: origin 0, S = H.
+// Window positions outside the image are the convolution's zero padding and are kept at 0.
+//
+// The transposed convolution of one row is an implicit GEMM:
+//   out[(r, u, w), ci] = sum_{tap=(ky,kx), co} A_out[r][u'][w'][co] * W[co][ci][ky][kx]
+//   u' = (u + delta - ky) / stride (only when divisible and inside the source window)
+// with M = rows x S_in^2, N = C_in, K = 9 C_out.  The weights are repacked at load time as
+// Bt[ci][tap * C_out + co] (K-contiguous).  The epilogue applies, per output element at
+// global position (gy, gx):
+//   outside the image          -> 0
+//   + residual (same node, smaller window aligned on the same anchor)
+//   relaxation (lam, s, t, b)  -> a' and the constant terms min(a,0) t + a' b, where the
+//                                 parameters are the ReLU's at (unit, gy, gx, ci), or the
+//                                 identity (1, 1, 0, b[ci]) when the node is not a ReLU
+// and reduces the constants over the tile's columns into one partial per GEMM row.
+#include "conv.h"
+
+namespace vcr {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint32_t fdiv(uint32_t n, FastDiv d) {
+  // floor(n / d) for n < 2^31 with the precomputed magic of FastDiv
+  const uint64_t t = (uint64_t)__umulhi(n, d.mul) + n;
+  return (uint32_t)(t >> d.shift);
+}
+
+constexpr int CT_BM = 128, CT_BN = 64, CT_BK = 32, CT_LD = CT_BK + 4;
+
+__global__ __launch_bounds__(256, 2) void k_convt(const ConvTArgs p) {
+  __shared__ __attribute__((aligned(16))) float As[2][CT_BM * CT_LD];
+  __shared__ __attribute__((aligned(16))) float Bs[2][CT_BN * CT_LD];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n_nt = p.N_pad / CT_BN;
+  const int mt = blockIdx.x / n_nt, nt = blockIdx.x - mt * n_nt;
+  const int m0 = mt * CT_BM, n0 = nt * CT_BN;
+  const int S_in2 = p.S_in * p.S_in;
+
+  // per-thread source rows for the A tile: rows lrow + 32 q
+  const int lrow = tid >> 3, lcol = (tid & 7) << 2;
+  int64_t a_row_base[4];
+  int ru[4], rw[4];
+  bool rvalid[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t m = (uint32_t)(m0 + lrow + 32 * q);
+    rvalid[q] = m < (uint32_t)p.M;
+    const uint32_t r = fdiv(m, p.div_S2);
+    const uint32_t pos = m - r * (uint32_t)S_in2;
+    const uint32_t u = fdiv(pos, p.div_S);
+    ru[q] = (int)u;
+    rw[q] = (int)(pos - u * (uint32_t)p.S_in);
+    a_row_base[q] = (int64_t)r * p.row_stride_out;
+  }
+  const float *Bg = p.Bt + (int64_t)(n0 + lrow) * p.ldb + lcol;
+  f32x4 ra[4], rb[2];
+  auto gload = [&](int kt) {
+    const int k0 = kt * CT_BK;
+    const int tap = k0 / p.C_out;
+    const int co = k0 - tap * p.C_out + lcol;
+    const int ky = tap / 3, kx = tap - 3 * (tap / 3);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      int yy = ru[q] + p.delta - ky, xx = rw[q] + p.delta - kx;
+      bool ok = rvalid[q];
+      if (p.stride == 2) {
+        ok = ok && ((yy | xx) & 1) == 0;
+        yy >>= 1;
+        xx >>= 1;
+      }
+      ok = ok && yy >= 0 && xx >= 0 && yy < p.S_out && xx < p.S_out;
+      f32x4 v = {0.f, 0.f, 0.f, 0.f};
+      if (ok) v = *reinterpret_cast<const f32x4 *>(p.A + a_row_base[q] + ((int64_t)yy * p.S_out + xx) * p.C_out + co);
+      ra[q] = v;
+    }
+#pragma unroll
+    for (int q = 0; q < 2; ++q) rb[q] = *reinterpret_cast<const f32x4 *>(Bg + (int64_t)q * 32 * p.ldb + k0);
+  };
+  auto lstore = [&](int buf) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) *reinterpret_cast<f32x4 *>(&As[buf][(lrow + 32 * q) * CT_LD + lcol]) = ra[q];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) *reinterpret_cast<f32x4 *>(&Bs[buf][(lrow + 32 * q) * CT_LD + lcol]) = rb[q];
+  };
+
+  f32x16 acc[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[j][v] = 0.f;
+
+  const int KT = p.K / CT_BK;
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  const int r32 = lane & 31, kq = (lane >> 5) * 16;
+  const int a_off = (wave * 32 + r32) * CT_LD + kq;
+  const int b_off0 = r32 * CT_LD + kq, b_off1 = (32 + r32) * CT_LD + kq;
+  for (int kt = 0; kt < KT; ++kt) {
+    const int cur = kt & 1;
+    const bool more = kt + 1 < KT;
+    if (more) gload(kt + 1);
+    const float *as = As[cur];
+    const float *bs = Bs[cur];
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      const f32x4 a = *reinterpret_cast<const f32x4 *>(as + a_off + 4 * h);
+      const f32x4 b0 = *reinterpret_cast<const f32x4 *>(bs + b_off0 + 4 * h);
+      const f32x4 b1 = *reinterpret_cast<const f32x4 *>(bs + b_off1 + 4 * h);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc[0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[e], b0[e], acc[0], 0, 0, 0);
+        acc[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[e], b1[e], acc[1], 0, 0, 0);
+      }
+    }
+    if (more) lstore(cur ^ 1);
+    __syncthreads();
+  }
+
+  // ---- epilogue ----------------------------------------------------------------------
+  const int half = lane >> 5;
+  float rp[16];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) rp[v] = 0.f;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int m = m0 + wave * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
+    if (m >= p.M) continue;
+    const uint32_t r = fdiv((uint32_t)m, p.div_S2);
+    const uint32_t pos = (uint32_t)m - r * (uint32_t)S_in2;
+    const uint32_t u = fdiv(pos, p.div_S);
+    const int w = (int)(pos - u * (uint32_t)p.S_in);
+    const int4 an = p.rows[r];   // (unit, anchor y, anchor x, -)
+    const int gy = p.dense ? (int)u : an.y * p.scale - p.h_in + (int)u;
+    const int gx = p.dense ? w : an.z * p.scale - p.h_in + w;
+    const bool inside = gy >= 0 && gx >= 0 && gy < p.H_in && gx < p.H_in;
+    float *orow = p.out + (int64_t)r * p.row_stride_in + ((int64_t)u * p.S_in + w) * p.C_in;
+#pragma unroll
+    for (int bj = 0; bj < 2; ++bj) {
+      const int n = n0 + bj * 32 + r32;
+      if (n >= p.C_in) continue;
+      float a = acc[bj][v];
+      float ap = 0.f;
+      if (inside) {
+        if (p.res) {
+          const int du = (int)u - p.res_off, dw = w - p.res_off;
+          if (du >= 0 && dw >= 0 && du < p.res_S && dw < p.res_S)
+            a += p.res[(int64_t)r * p.res_row_stride + ((int64_t)du * p.res_S + dw) * p.C_in + n];
+        }
+        float4 prm;
+        if (p.P_pos) {
+          prm = p.P_pos[(((int64_t)an.x * p.H_in + gy) * p.H_in + gx) * p.C_in + n];
+        } else {
+          prm = make_float4(1.f, 1.f, 0.f, p.bias[n]);
+        }
+        ap = a > 0.f ? a * prm.x : a * prm.y;
+        rp[v] += fminf(a, 0.f) * prm.z + ap * prm.w;
+      }
+      orow[n] = ap;
+    }
+  }
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    float x = rp[v];
+    x += __shfl_xor(x, 16);
+    x += __shfl_xor(x, 8);
+    x += __shfl_xor(x, 4);
+    x += __shfl_xor(x, 2);
+    x += __shfl_xor(x, 1);
+    rp[v] = x;
+  }
+  if (r32 == 0) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int m = m0 + wave * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
+      if (m < p.M) p.part[(int64_t)nt * p.M_pad + m] = rp[v];
+    }
+  }
+}
+
+hipError_t launch_convt(const ConvTArgs &a, hipStream_t s) {
+  if (a.N_pad % CT_BN || a.K % CT_BK || a.C_out % CT_BK || a.M <= 0 || a.M_pad < a.M) return hipErrorInvalidValue;
+  const int64_t grid = (int64_t)((a.M + CT_BM - 1) / CT_BM) * (a.N_pad / CT_BN);
+  if (grid > 0x7fffffff) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_convt, dim3((unsigned)grid), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------------
+// Transposed stem convolution onto the network input (few input channels, so VALU), fused
+// with the concretization: for every input-window position (r, u, w) and channel ci,
+//   a = sum_{tap, co} A_out[r][u'][w'][co] W[co][ci][ky][kx]
+//   part[(r, u, w)] += a c[unit][ci][gy][gx] - |a| r[unit][ci][gy][gx]   (inside the image)
+// One workgroup per coefficient row; the row's source window is staged through LDS in
+// channel chunks.
+constexpr int STEM_MAX_CIN = 4;
+
+__global__ __launch_bounds__(256) void k_stem(const StemArgs p) {
+  extern __shared__ float lds[];   // [S_out * S_out][cc]
+  float *wsh = lds + (int64_t)p.S_out * p.S_out * p.cc;   // [cc][C_in][9]
+  const int r = blockIdx.x;
+  const int4 an = p.rows[r];
+  const int S_in2 = p.S_in * p.S_in;
+  const float *src = p.A + (int64_t)r * p.row_stride_out;
+  float acc[8][STEM_MAX_CIN];   // up to 8 positions per thread
+  const int npos = (S_in2 + blockDim.x - 1) / blockDim.x;
+  for (int k = 0; k < 8; ++k)
+    for (int c = 0; c < STEM_MAX_CIN; ++c) acc[k][c] = 0.f;
+  for (int c0 = 0; c0 < p.C_out; c0 += p.cc) {
+    __syncthreads();
+    const int nsrc = p.S_out * p.S_out * p.cc;
+    for (int i = threadIdx.x; i < nsrc; i += blockDim.x) {
+      const int pos = i / p.cc, c = i - pos * p.cc;
+      lds[i] = src[(int64_t)pos * p.C_out + c0 + c];
+    }
+    for (int i = threadIdx.x; i < p.cc * p.C_in * 9; i += blockDim.x) {
+      const int c = i / (p.C_in * 9), rest = i - c * p.C_in * 9;
+      const int ci = rest / 9, tap = rest - ci * 9;
+      wsh[i] = p.W[(((int64_t)(c0 + c) * p.C_in + ci) * 3 + tap / 3) * 3 + tap % 3];
+    }
+    __syncthreads();
+    for (int k = 0; k < npos && k < 8; ++k) {
+      const int pos = threadIdx.x + k * blockDim.x;
+      if (pos >= S_in2) break;
+      const int u = pos / p.S_in, w = pos - u * p.S_in;
+      for (int tap = 0; tap < 9; ++tap) {
+        const int ky = tap / 3, kx = tap - 3 * ky;
+        int yy = u + p.delta - ky, xx = w + p.delta - kx;
+        if (p.stride == 2) {
+          if ((yy | xx) & 1) continue;
+          yy >>= 1;
+          xx >>= 1;
+        }
+        if (yy < 0 || xx < 0 || yy >= p.S_out || xx >= p.S_out) continue;
+        const float *sp = lds + (yy * p.S_out + xx) * p.cc;
+        for (int c = 0; c < p.cc; ++c) {
+          const float a = sp[c];
+          const float *wp = wsh + c * p.C_in * 9 + tap;
+          for (int ci = 0; ci < p.C_in; ++ci) acc[k][ci] += a * wp[ci * 9];
+        }
+      }
+    }
+  }
+  for (int k = 0; k < npos && k < 8; ++k) {
+    const int pos = threadIdx.x + k * blockDim.x;
+    if (pos >= S_in2) break;
+    const int u = pos / p.S_in, w = pos - u * p.S_in;
+    const int gy = p.dense ? u : an.y * p.scale - p.h_in + u;
+    const int gx = p.dense ? w : an.z * p.scale - p.h_in + w;
+    float part = 0.f;
+    if (gy >= 0 && gx >= 0 && gy < p.H_in && gx < p.H_in) {
+      for (int ci = 0; ci < p.C_in; ++ci) {
+        const int64_t bi = (int64_t)an.x * p.ld_box + ((int64_t)ci * p.H_in + gy) * p.H_in + gx;
+        const float a = acc[k][ci];
+        part += a * p.c0[bi] - fabsf(a) * p.r0[bi];
+      }
+    }
+    p.part[(int64_t)r * S_in2 + pos] = part;
+  }
+}
+
+hipError_t launch_stem(const StemArgs &a, hipStream_t s) {
+  if (a.C_in > STEM_MAX_CIN || a.S_in * a.S_in > 8 * 256 || a.C_out % a.cc) return hipErrorInvalidValue;
+  const size_t lds = sizeof(float) * ((size_t)a.S_out * a.S_out * a.cc + (size_t)a.cc * a.C_in * 9);
+  if (lds > 64 * 1024) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_stem, dim3((unsigned)a.R), dim3(256), lds, s, a);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------------
+// First rows of a pass that starts at a 3x3 convolution's output neurons: row (unit, dir,
+// c0, i, j) is (dir ? -1 : 1) W[c0][ci][u][w] on the convolution's input window around
+// (stride i, stride j), zero outside the image; relaxed (or identity) like the GEMM
+// epilogue; beta = (dir ? -1 : 1) b[c0] + the window's constant terms.  One wave per row.
+__global__ __launch_bounds__(256) void k_init_conv(const ConvInitArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= a.R) return;
+  const int4 an = a.rows[r];
+  const int n_src = a.C_src * a.H_src * a.H_src;
+  const int q = (int)(r % (2 * n_src));
+  const int dir = q >= n_src;
+  const int nq = q - dir * n_src;
+  const int c0 = nq / (a.H_src * a.H_src);
+  const float sg = dir ? -1.f : 1.f;
+  const int S = a.S;   // kernel window (3)
+  float *orow = a.out + r * (int64_t)S * S * a.C_in;
+  float acc = 0.f;
+  for (int e = lane; e < S * S * a.C_in; e += 64) {
+    const int pos = e / a.C_in, ci = e - pos * a.C_in;
+    const int u = pos / S, w = pos - u * S;
+    const int gy = an.y * a.scale - a.h + u, gx = an.z * a.scale - a.h + w;
+    float ap = 0.f;
+    if (gy >= 0 && gx >= 0 && gy < a.H_in && gx < a.H_in) {
+      const float x = sg * a.W[(((int64_t)c0 * a.C_in + ci) * 3 + u) * 3 + w];
+      float4 prm;
+      if (a.P_pos)
+        prm = a.P_pos[(((int64_t)an.x * a.H_in + gy) * a.H_in + gx) * a.C_in + ci];
+      else
+        prm = make_float4(1.f, 1.f, 0.f, a.bias_next[ci]);
+      ap = x > 0.f ? x * prm.x : x * prm.y;
+      acc += fminf(x, 0.f) * prm.z + ap * prm.w;
+    }
+    orow[e] = ap;
+  }
+  acc += __shfl_xor(acc, 32);
+  acc += __shfl_xor(acc, 16);
+  acc += __shfl_xor(acc, 8);
+  acc += __shfl_xor(acc, 4);
+  acc += __shfl_xor(acc, 2);
+  acc += __shfl_xor(acc, 1);
+  if (lane == 0) a.beta[r] = sg * a.b[c0] + acc;
+}
+
+hipError_t launch_init_conv(const ConvInitArgs &a, hipStream_t s) {
+  hipLaunchKernelGGL(k_init_conv, dim3((unsigned)((a.R + 3) / 4)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// beta[r] += sum_{q < per_row} sum_p part[p][r * per_row + q]   (fixed order)
+__global__ void k_rowsum_win(float *beta, const float *part, int32_t n_parts, int64_t M_pad, int64_t R,
+                             int32_t per_row) {
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= R) return;
+  float s = 0.f;
+  for (int q = 0; q < per_row; ++q) {
+    const int64_t m = r * per_row + q;
+    for (int p = 0; p < n_parts; ++p) s += part[p * M_pad + m];
+  }
+  beta[r] += s;
+}
+
+hipError_t launch_rowsum_win(float *beta, const float *part, int32_t n_parts, int64_t M_pad, int64_t R,
+                             int32_t per_row, hipStream_t s) {
+  hipLaunchKernelGGL(k_rowsum_win, dim3((unsigned)((R + 255) / 256)), dim3(256), 0, s, beta, part, n_parts,
+                     M_pad, R, per_row);
+  return hipGetLastError();
+}
+
+// Row table of a pass: row r -> (unit, anchor y, anchor x) for rows that start at the
+// neurons of a (C, H, W) node in (unit, direction, c, y, x) order; dense rows get anchor 0.
+__global__ void k_row_table(int4 *rows, int64_t R, int32_t rows_per_unit, int32_t C, int32_t H, int32_t Wd,
+                            int32_t windowed, int32_t unit0) {
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= R) return;
+  const int u = (int)(r / rows_per_unit);
+  int ay = 0, ax = 0;
+  if (windowed) {
+    const int n = C * H * Wd;
+    const int q = (int)(r - (int64_t)u * rows_per_unit) % n;
+    const int hw = q % (H * Wd);
+    ay = hw / Wd;
+    ax = hw % Wd;
+  }
+  rows[r] = make_int4(u + unit0, ay, ax, 0);
+}
+
+hipError_t launch_row_table(int4 *rows, int64_t R, int32_t rows_per_unit, int32_t C, int32_t H, int32_t W,
+                            int32_t windowed, int32_t unit0, hipStream_t s) {
+  hipLaunchKernelGGL(k_row_table, dim3((unsigned)((R + 255) / 256)), dim3(256), 0, s, rows, R, rows_per_unit, C, H,
+                     W, windowed, unit0);
+  return hipGetLastError();
+}
+
+// Bounds of a convolutional ReLU layer from its finished pass: neuron q = (c, y, x) of unit
+// b has rows (b, 0, q) (lower) and (b, 1, q) (negated upper); intersection with IBP; the
+// relaxation is stored channels-last [b][y][x][c] for the windowed epilogues above.
+__global__ void k_finalize_conv(const float *beta, int32_t B, int32_t C, int32_t H, const float *ibp_c,
+                                const float *ibp_r, int64_t ld_ibp, int32_t intersect, const float *bias_next,
+                                float *L, float *U, float4 *P) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t n = (int64_t)C * H * H;
+  if (idx >= B * n) return;
+  const int64_t b = idx / n, q = idx - b * n;
+  float l = beta[b * 2 * n + q];
+  float u = -beta[b * 2 * n + n + q];
+  if (intersect) {
+    const int64_t j = b * ld_ibp + q;
+    l = fmaxf(l, ibp_c[j] - ibp_r[j]);
+    u = fminf(u, ibp_c[j] + ibp_r[j]);
+  }
+  L[idx] = l;
+  U[idx] = u;
+  const int c = (int)(q / (H * H)), hw = (int)(q % (H * H));
+  float4 prm;
+  if (u <= 0.f) prm = make_float4(0.f, 0.f, 0.f, 0.f);
+  else if (l >= 0.f) prm = make_float4(1.f, 1.f, 0.f, 0.f);
+  else {
+    const float s = u / (u - l);
+    prm = make_float4(u > -l ? 1.f : 0.f, s, -s * l, 0.f);
+  }
+  prm.w = bias_next ? bias_next[c] : 0.f;
+  P[(b * H * H + hw) * C + c] = prm;
+}
+
+hipError_t launch_finalize_conv(const float *beta, int32_t B, int32_t C, int32_t H, const float *ibp_c,
+                                const float *ibp_r, int64_t ld_ibp, int32_t intersect, const float *bias_next,
+                                float *L, float *U, float4 *P, hipStream_t s) {
+  const int64_t tot = (int64_t)B * C * H * H;
+  hipLaunchKernelGGL(k_finalize_conv, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, beta, B, C, H, ibp_c,
+                     ibp_r, ld_ibp, intersect, bias_next, L, U, P);
+  return hipGetLastError();
+}
+
+// A ReLU layer whose input is one convolution of the network input: its exact range over
+// the box is the IBP interval [c - r, c + r]; relaxation stored channels-last.
+__global__ void k_conv_layer_from_ibp(const float *ibp_c, const float *ibp_r, int64_t ld_ibp, int32_t B, int32_t C,
+                                      int32_t H, const float *bias_next, float *L, float *U, float4 *P) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t n = (int64_t)C * H * H;
+  if (idx >= B * n) return;
+  const int64_t b = idx / n, q = idx - b * n;
+  const float cc = ibp_c[b * ld_ibp + q], rr = ibp_r[b * ld_ibp + q];
+  const float l = cc - rr, u = cc + rr;
+  L[idx] = l;
+  U[idx] = u;
+  const int c = (int)(q / (H * H)), hw = (int)(q % (H * H));
+  float4 prm;
+  if (u <= 0.f) prm = make_float4(0.f, 0.f, 0.f, 0.f);
+  else if (l >= 0.f) prm = make_float4(1.f, 1.f, 0.f, 0.f);
+  else {
+    const float s = u / (u - l);
+    prm = make_float4(u > -l ? 1.f : 0.f, s, -s * l, 0.f);
+  }
+  prm.w = bias_next[c];
+  P[(b * H * H + hw) * C + c] = prm;
+}
+
+hipError_t launch_conv_layer_from_ibp(const float *ibp_c, const float *ibp_r, int64_t ld_ibp, int32_t B, int32_t C,
+                                      int32_t H, const float *bias_next, float *L, float *U, float4 *P,
+                                      hipStream_t s) {
+  const int64_t tot = (int64_t)B * C * H * H;
+  hipLaunchKernelGGL(k_conv_layer_from_ibp, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, ibp_c, ibp_r,
+                     ld_ibp, B, C, H, bias_next, L, U, P);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------------
+// IBP of a convolution in centre/radius form, c' = conv(W, c) + b, r' = conv(|W|, r), over
+// CHW tensors.  One thread per output element.
+__global__ void k_ibp_conv(const float *W, const float *bias, int32_t Co, int32_t Ci, int32_t Hin, int32_t Hout,
+                           int32_t stride, int32_t pad, const float *cin, const float *rin, int64_t ld_in,
+                           float *cout, float *rout, int64_t ld_out, int32_t B) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t per = (int64_t)Co * Hout * Hout;
+  if (idx >= B * per) return;
+  const int64_t b = idx / per, q = idx - b * per;
+  const int co = (int)(q / (Hout * Hout)), hw = (int)(q % (Hout * Hout));
+  const int oy = hw / Hout, ox = hw % Hout;
+  float c = 0.f, r = 0.f;
+  for (int ci = 0; ci < Ci; ++ci) {
+    const float *wp = W + ((int64_t)co * Ci + ci) * 9;
+    const float *cp = cin + b * ld_in + (int64_t)ci * Hin * Hin;
+    const float *rq = rin + b * ld_in + (int64_t)ci * Hin * Hin;
+    for (int ky = 0; ky < 3; ++ky) {
+      const int iy = oy * stride - pad + ky;
+      if (iy < 0 || iy >= Hin) continue;
+      for (int kx = 0; kx < 3; ++kx) {
+        const int ix = ox * stride - pad + kx;
+        if (ix < 0 || ix >= Hin) continue;
+        const float w = wp[ky * 3 + kx];
+        c += w * cp[iy * Hin + ix];
+        r += fabsf(w) * rq[iy * Hin + ix];
+      }
+    }
+  }
+  cout[b * ld_out + q] = c + bias[co];
+  rout[b * ld_out + q] = r;
+}
+
+hipError_t launch_ibp_conv(const float *W, const float *bias, int32_t Co, int32_t Ci, int32_t Hin, int32_t Hout,
+                           int32_t stride, int32_t pad, const float *cin, const float *rin, int64_t ld_in,
+                           float *cout, float *rout, int64_t ld_out, int32_t B, hipStream_t s) {
+  const int64_t tot = (int64_t)B * Co * Hout * Hout;
+  hipLaunchKernelGGL(k_ibp_conv, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, W, bias, Co, Ci, Hin, Hout,
+                     stride, pad, cin, rin, ld_in, cout, rout, ld_out, B);
+  return hipGetLastError();
+}
+
+// IBP of ReLU (interval [max(l,0), max(u,0)]) and of a sum, in centre/radius form.
+__global__ void k_ibp_relu(const float *cin, const float *rin, float *cout, float *rout, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const float lo = fmaxf(cin[i] - rin[i], 0.f), hi = fmaxf(cin[i] + rin[i], 0.f);
+  cout[i] = (lo + hi) * 0.5f;
+  rout[i] = (hi - lo) * 0.5f;
+}
+
+__global__ void k_ibp_add(const float *c1, const float *r1, const float *c2, const float *r2, float *cout,
+                          float *rout, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  cout[i] = c1[i] + c2[i];
+  rout[i] = r1[i] + r2[i];
+}
+
+hipError_t launch_ibp_relu(const float *cin, const float *rin, float *cout, float *rout, int64_t n, hipStream_t s) {
+  hipLaunchKernelGGL(k_ibp_relu, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, cin, rin, cout, rout, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_ibp_add(const float *c1, const float *r1, const float *c2, const float *r2, float *cout,
+                          float *rout, int64_t n, hipStream_t s) {
+  hipLaunchKernelGGL(k_ibp_add, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, c1, r1, c2, r2, cout, rout, n);
+  return hipGetLastError();
+}
+
+// Conv weights repacked for the transposed-convolution GEMM: Bt[ci][tap * Co + co] =
+// W[co][ci][tap] for ci < Ci, zero rows up to Ci_pad.
+__global__ void k_repack_convt(const float *W, int32_t Co, int32_t Ci, int32_t Ci_pad, float *Bt) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t K = 9 * (int64_t)Co;
+  if (idx >= Ci_pad * K) return;
+  const int ci = (int)(idx / K), k = (int)(idx % K);
+  const int tap = k / Co, co = k % Co;
+  Bt[idx] = ci < Ci ? W[((int64_t)co * Ci + ci) * 9 + tap] : 0.f;
+}
+
+hipError_t launch_repack_convt(const float *W, int32_t Co, int32_t Ci, int32_t Ci_pad, float *Bt, hipStream_t s) {
+  const int64_t tot = (int64_t)Ci_pad * 9 * Co;
+  hipLaunchKernelGGL(k_repack_convt, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, W, Co, Ci, Ci_pad, Bt);
+  return hipGetLastError();
+}
+
+// Dense weight columns from flatten (C, H, W) order to channels-last (H, W, C) order.
+__global__ void k_permute_hwc(const float *W, int32_t rows, int32_t C, int32_t HW, float *Wo, int64_t ldo) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t n = (int64_t)C * HW;
+  if (idx >= rows * ldo) return;
+  const int64_t o = idx / ldo, j = idx % ldo;   // j = hw * C + c
+  float v = 0.f;
+  if (j < n) {
+    const int64_t hw = j / C, c = j % C;
+    v = W[o * n + c * HW + hw];
+  }
+  Wo[idx] = v;
+}
+
+hipError_t launch_permute_hwc(const float *W, int32_t rows, int32_t C, int32_t HW, float *Wo, int64_t ldo,
+                              hipStream_t s) {
+  const int64_t tot = (int64_t)rows * ldo;
+  hipLaunchKernelGGL(k_permute_hwc, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, W, rows, C, HW, Wo, ldo);
+  return hipGetLastError();
+}
+
+// Identity relaxation with a per-channel bias for channels-last columns: P[j] =
+// (1, 1, 0, b[j % C]) for j < n, zero beyond.
+__global__ void k_identity_params(const float *b, int32_t C, int64_t n, int64_t ld, float4 *P) {
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= ld) return;
+  P[j] = j < n ? make_float4(1.f, 1.f, 0.f, b ? b[j % C] : 0.f) : make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
+hipError_t launch_identity_params(const float *b, int32_t C, int64_t n, int64_t ld, float4 *P, hipStream_t s) {
+  hipLaunchKernelGGL(k_identity_params, dim3((unsigned)((ld + 255) / 256)), dim3(256), 0, s, b, C, n, ld, P);
+  return hipGetLastError();
+}
+
+// Relaxation parameters of a dense-output ReLU from channels-last bounds stay in the MLP
+// layout [b][n]; a ReLU on a conv node keeps [b][y][x][c].  Both are produced by the
+// finalize kernels.
+
+FastDiv make_fastdiv(uint32_t d) {
+  FastDiv f;
+  uint32_t l = 0;
+  while ((1ull << l) < d) ++l;
+  f.shift = l;
+  f.mul = (uint32_t)(((1ull << 32) * ((1ull << l) - d)) / d + 1);
+  if (d == 1) {
+    f.mul = 0;
+    f.shift = 0;
+  }
+  return f;
+}
+
+}  // namespace vcr

@@ -1,0 +1,112 @@
+// Internal context of the vcrown library, shared by the MLP path (api.cpp) and the
+// convolutional-network path (graph.cpp).  Not part of the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <memory>
+#include <string>
+#include <vector>
+
+#include "../../include/vcrown.h"
+#include "kernels.h"
+
+namespace vcr {
+struct GraphNet;   // the convolutional-network path (graph.cpp)
+void destroy_graph(GraphNet *g);
+}
+
+namespace vcr_internal {
+
+struct DenseLayer {
+  int32_t n_in = 0, n_out = 0;
+  int64_t ld_in = 0, ld_out = 0;
+  float *Wp = nullptr;   // n_out x ld_in, zero padded
+  float *Bt = nullptr;   // ld_in x ld_out, Bt[n][k] = W[k][n], zero padded
+  float *b = nullptr;    // ld_out, zero padded
+};
+
+struct Workspace {
+  char *base = nullptr;
+  size_t cap = 0, used = 0;
+};
+
+}  // namespace vcr_internal
+
+using vcr_internal::DenseLayer;
+using vcr_internal::Workspace;
+
+struct vcr_ctx {
+  int32_t device = -1;
+  hipStream_t stream = nullptr;
+  std::string err;
+  // options
+  int32_t clip_on = 1;
+  float clip_lo = 0.f, clip_hi = 1.f;
+  int32_t intersect = 1;
+  uint64_t ws_cap = 0;
+  int32_t sync_check = 0;
+  // network
+  bool loaded = false;
+  int32_t n0 = 0;
+  std::vector<DenseLayer> layers;   // the MLP chain
+  std::vector<int32_t> relu_n;      // neurons per ReLU node
+  std::vector<vcr_node> node_desc;  // validated node list (weights not retained)
+  // workspace
+  Workspace ws;
+  uint64_t peak_ws = 0;
+  // last call
+  int32_t last_B = 0;
+  std::vector<float *> lastL, lastU;
+  int32_t *d_counters = nullptr;    // [64] unstable counts + [1] invalid domains
+  bool last_had_splits = false;
+  double ms_last = 0.0;
+  uint64_t flops_last = 0;
+  int32_t chunks_last = 0;
+  // convolutional-network path (null for MLPs)
+  vcr::GraphNet *graph = nullptr;
+  // GEMM timing (VCR_OPT_TIME_GEMM)
+  int32_t time_gemm = 0;
+  std::vector<hipEvent_t> ev_pool;      // pairs: start, stop
+  size_t ev_used = 0;                   // events recorded but not yet read
+  uint64_t timed_launches = 0, timed_flops = 0;
+  double timed_ms = 0.0;
+  std::vector<uint64_t> pending_flops;  // flops of each recorded pair
+};
+
+inline vcr_status fail(vcr_ctx *c, vcr_status st, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  c->err = buf;
+  return st;
+}
+
+#define HIP_TRY(c, expr)                                                                      \
+  do {                                                                                        \
+    hipError_t e_ = (expr);                                                                   \
+    if (e_ != hipSuccess) return fail((c), VCR_ERR_DEVICE, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+inline size_t al(size_t x) { return (x + 255) / 256 * 256; }
+
+// Sub-allocation from the workspace.  With a null base it only counts bytes, which is how
+// the planners size a call: the same carve code runs for sizing and for the real layout.
+template <class T>
+T *take(Workspace &w, size_t count) {
+  size_t b = al(sizeof(T) * (count > 0 ? count : 1));
+  T *p = w.base ? reinterpret_cast<T *>(w.base + w.used) : nullptr;
+  w.used += b;
+  return p;
+}
+
+template <class T>
+T *take(vcr_ctx *c, size_t count) {
+  return take<T>(c->ws, count);
+}
+
+vcr_status ensure_ws(vcr_ctx *c, size_t bytes);

@@ -1,0 +1,89 @@
+"""GPU parity of CROWN through convolutions, residual blocks and flatten.
+
+Small networks with the ResNet workload's topology (and a plain conv chain with a stride-2
+convolution under a ReLU) are compared with the fp64 oracle on every bound; the full-size
+ResNet is checked on neurons the oracle can compute one by one, and by properties that
+hold at any size."""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from tests.gpu_util import assert_close, check_input, gpu_crown, gpu_ctx, log, to_dev
+from workloads import Net, Node, Workload, make_workload
+from workloads.gen import margin_spec, resnet_net
+
+pytestmark = pytest.mark.gpu
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def small_resnet(seed, hw=8, c1=32, c2=64, fc=32, n_out=10, batch=2, eps=2 / 255):
+    rng = np.random.default_rng(seed)
+    net = resnet_net(rng, in_chw=(3, hw, hw), c1=c1, c2=c2, fc=fc, n_out=n_out)
+    x0 = rng.random((batch, net.n_in)).astype(np.float32)
+    return Workload(f"resnet{hw}", net, x0, np.float32(eps), margin_spec(net, x0))
+
+
+def conv_chain(seed, batch=2, eps=0.02):
+    """conv -> ReLU -> stride-2 conv -> ReLU -> conv -> ReLU -> flatten -> dense -> ReLU ->
+    dense, on 3x8x8 (no residual; ReLUs directly after convolutions, one under a stride-2)."""
+    rng = np.random.default_rng(seed)
+
+    def cw(co, ci):
+        return ((rng.standard_normal((co, ci, 3, 3)) * np.sqrt(2 / (ci * 9))).astype(np.float32),
+                (rng.standard_normal(co) * 0.05).astype(np.float32))
+
+    W0, b0 = cw(32, 3)
+    W1, b1 = cw(32, 32)
+    W2, b2 = cw(64, 32)
+    Wd = (rng.standard_normal((40, 64 * 16)) * np.sqrt(2 / 1024)).astype(np.float32)
+    bd = (rng.standard_normal(40) * 0.05).astype(np.float32)
+    Wo = (rng.standard_normal((6, 40)) * np.sqrt(2 / 40)).astype(np.float32)
+    bo = (rng.standard_normal(6) * 0.05).astype(np.float32)
+    nodes = [Node("conv2d", -1, W=W0, b=b0, stride=1, pad=1), Node("relu", 0),
+             Node("conv2d", 1, W=W1, b=b1, stride=2, pad=1), Node("relu", 2),
+             Node("conv2d", 3, W=W2, b=b2, stride=1, pad=1), Node("relu", 4),
+             Node("flatten", 5), Node("dense", 6, W=Wd, b=bd), Node("relu", 7), Node("dense", 8, W=Wo, b=bo)]
+    net = Net((3, 8, 8), nodes)
+    x0 = rng.random((batch, net.n_in)).astype(np.float32)
+    return Workload("convchain", net, x0, np.float32(eps), margin_spec(net, x0))
+
+
+@pytest.mark.parametrize("make", [lambda: small_resnet(301), lambda: conv_chain(302)], ids=["resnet8", "convchain"])
+def test_small_conv_nets_all_bounds(make):
+    wl = make()
+    log("case", wl.name)
+    ctx = gpu_ctx(wl.net)
+    lb, ub, layers = gpu_crown(ctx, wl)
+    for b in range(wl.x0.shape[0]):
+        log("oracle input", b)
+        check_input(wl.net, wl.x0[b], wl.eps, wl.C[b], lb[b], ub[b], [(l[b], u[b]) for l, u in layers],
+                    what=f"{wl.name} input {b}")
+
+
+def test_conv_ibp_bounds():
+    wl = small_resnet(303)
+    ctx = gpu_ctx(wl.net)
+    lb, ub = ctx.ibp_bounds(to_dev(wl.x0), wl.eps, to_dev(wl.C))
+    lb, ub = lb.cpu().numpy(), ub.cpu().numpy()
+    for b in range(wl.x0.shape[0]):
+        il, iu = oracle.ibp_spec_bounds(wl.net, wl.x0[b], wl.eps, wl.C[b])
+        assert_close(lb[b], il, "ibp lb")
+        assert_close(ub[b], iu, "ibp ub")
+
+
+def test_conv_batch_invariance_and_chunking():
+    from paper_2606_09377_amd.vcrown import OPT_WORKSPACE_CAP_BYTES
+    wl = small_resnet(304, batch=4)
+    ctx = gpu_ctx(wl.net)
+    lb, ub, layers = gpu_crown(ctx, wl)
+    lb1, ub1, lay1 = gpu_crown(ctx, wl, inputs=[2])
+    assert np.array_equal(lb1[0], lb[2]) and np.array_equal(ub1[0], ub[2])
+    for r in range(len(layers)):
+        assert np.array_equal(lay1[r][0][0], layers[r][0][2]) and np.array_equal(lay1[r][1][0], layers[r][1][2])
+    full = ctx.workspace_bytes(4, wl.C.shape[1])
+    ctx.set_option(OPT_WORKSPACE_CAP_BYTES, full // 3)
+    lb3, ub3, _ = gpu_crown(ctx, wl)
+    assert ctx.stats()["n_chunks_last_call"] > len(layers) + 1
+    assert np.array_equal(lb3, lb) and np.array_equal(ub3, ub)
