@@ -45,7 +45,7 @@ import numpy as np
 __all__ = [
     "input_box", "node_shapes", "forward", "ibp", "ibp_spec_bounds", "relu_relaxation",
     "conv2d", "conv2d_transpose", "backward", "concretize", "crown", "CrownResult",
-    "apply_splits", "crown_domains", "unstable_pool",
+    "apply_splits", "crown_domains", "unstable_pool", "support", "crown_sampled",
 ]
 
 
@@ -456,3 +456,91 @@ def unstable_pool(net, root, tau_abs=1e-4, tau_rel=1e-4):
         for j in np.nonzero(ok)[0]:
             pool.append((r, int(j)))
     return np.asarray(pool, dtype=np.int64).reshape(-1, 2)
+
+
+# --------------------------------------------------------------------------------------
+# bounds of selected neurons without computing whole layers
+
+def support(net, shapes, start, rows_mask):
+    """Structural support of a backward pass: for a boolean mask over the neurons of node
+    `start` (one row per set entry, all rows together), which neurons of every ReLU node
+    below can carry a nonzero coefficient.  Computed by propagating the mask with the
+    absolute weights (every entry >= 0, so a sum is nonzero exactly when some path is),
+    with every ReLU passed through unchanged.  Returns {relu node id: flat bool mask}."""
+    acc = {start: np.asarray(rows_mask, np.float64).reshape(1, -1)}
+    out = {}
+    for i in range(start, -1, -1):
+        if i not in acc:
+            continue
+        Ai = (acc.pop(i) > 0).astype(np.float64)
+        nd = net.nodes[i]
+        if nd.op == "dense":
+            _accumulate(acc, nd.in0, Ai @ np.abs(_f64(nd.W)))
+        elif nd.op == "conv2d":
+            co, ho, wo = shapes[i]
+            in_shape = tuple(net.in_shape) if nd.in0 == -1 else shapes[nd.in0]
+            Ain = conv2d_transpose(Ai.reshape(1, co, ho, wo), np.abs(_f64(nd.W)), nd.stride, nd.pad, in_shape[1:])
+            _accumulate(acc, nd.in0, Ain.reshape(1, -1))
+        elif nd.op == "relu":
+            out[i] = Ai.reshape(-1) > 0
+            _accumulate(acc, nd.in0, Ai)
+        elif nd.op in ("add",):
+            _accumulate(acc, nd.in0, Ai)
+            _accumulate(acc, nd.in1, Ai)
+        elif nd.op == "flatten":
+            _accumulate(acc, nd.in0, Ai)
+    return out
+
+
+def crown_sampled(net, x0, eps, targets, clip=(0.0, 1.0), intersect_ibp=True, chunk=256):
+    """Full-CROWN bounds of selected pre-activation neurons, computing at each lower ReLU
+    only the neurons the selected rows can reach (their receptive fields).
+
+    targets: {relu node id: array of flat neuron indices}.  The bound of every computed
+    neuron is the same sequence of operations as in `crown`: the rows that are not
+    computed would only ever be multiplied by exact zeros.  Returns {relu node id:
+    (indices, l, u)} for every ReLU node that needed neurons."""
+    shapes = node_shapes(net)
+    lo, hi = input_box(x0, eps, clip)
+    IL, IU = ibp(net, lo, hi)
+    relus = [i for i, nd in enumerate(net.nodes) if nd.op == "relu"]
+    need = {i: np.zeros(int(np.prod(shapes[i])), bool) for i in relus}
+    for i, idx in targets.items():
+        need[i][np.asarray(idx, np.int64)] = True
+    # top-down: the neurons every selected row reaches at the ReLUs below it
+    for i in reversed(relus):
+        if not need[i].any():
+            continue
+        z = net.nodes[i].in0
+        for k, mask in support(net, shapes, z, need[i]).items():
+            need[k] |= mask
+    relax = {}
+    out = {}
+    for i in relus:
+        z = net.nodes[i].in0
+        n = int(np.prod(shapes[i]))
+        idx = np.nonzero(need[i])[0]
+        l = np.zeros(n)
+        u = np.zeros(n)
+        if len(idx):
+            nd = net.nodes[z]
+            if nd.op == "dense" and nd.in0 == -1:
+                W, b = _f64(nd.W)[idx], _f64(nd.b)[idx]
+                l[idx], u[idx] = concretize(W, b, lo, hi, False), concretize(W, b, lo, hi, True)
+            else:
+                for r0 in range(0, len(idx), chunk):
+                    sel = idx[r0:r0 + chunk]
+                    I = np.zeros((len(sel), n))
+                    I[np.arange(len(sel)), sel] = 1.0
+                    zero = np.zeros(len(sel))
+                    Al, bl = backward(net, shapes, relax, z, I, zero, upper=False)
+                    Au, bu = backward(net, shapes, relax, z, I, zero, upper=True)
+                    l[sel] = concretize(Al, bl, lo, hi, False)
+                    u[sel] = concretize(Au, bu, lo, hi, True)
+            if intersect_ibp:
+                l[idx] = np.maximum(l[idx], IL[z].reshape(-1)[idx])
+                u[idx] = np.minimum(u[idx], IU[z].reshape(-1)[idx])
+            out[i] = (idx, l[idx], u[idx])
+        # neurons outside the set are never reached; (0, 0) makes them inactive
+        relax[i] = relu_relaxation(l, u)
+    return out

@@ -200,66 +200,85 @@ hipError_t launch_convt(const ConvTArgs &a, hipStream_t s) {
 // Transposed stem convolution onto the network input (few input channels, so VALU), fused
 // with the concretization: for every input-window position (r, u, w) and channel ci,
 //   a = sum_{tap, co} A_out[r][u'][w'][co] W[co][ci][ky][kx]
-//   part[(r, u, w)] += a c[unit][ci][gy][gx] - |a| r[unit][ci][gy][gx]   (inside the image)
-// One workgroup per coefficient row; the row's source window is staged through LDS in
-// channel chunks.
-constexpr int STEM_MAX_CIN = 4;
-
+//   part[(r, u, w)] = sum_ci a c[unit][ci][gy][gx] - |a| r[unit][ci][gy][gx]   (inside the image)
+// One workgroup per coefficient row; the row's source window is staged through LDS
+// channel-major (odd row pitch, so neighbouring positions hit neighbouring banks) in channel
+// chunks; the weights are read with wave-uniform addresses.
+template <int CIN, int MAXP>
 __global__ __launch_bounds__(256) void k_stem(const StemArgs p) {
-  extern __shared__ float lds[];   // [S_out * S_out][cc]
-  float *wsh = lds + (int64_t)p.S_out * p.S_out * p.cc;   // [cc][C_in][9]
+  extern __shared__ float lds[];   // [cc][pitch]
   const int r = blockIdx.x;
   const int4 an = p.rows[r];
+  const int S_out2 = p.S_out * p.S_out;
+  const int pitch = S_out2 | 1;
   const int S_in2 = p.S_in * p.S_in;
   const float *src = p.A + (int64_t)r * p.row_stride_out;
-  float acc[8][STEM_MAX_CIN];   // up to 8 positions per thread
-  const int npos = (S_in2 + blockDim.x - 1) / blockDim.x;
-  for (int k = 0; k < 8; ++k)
-    for (int c = 0; c < STEM_MAX_CIN; ++c) acc[k][c] = 0.f;
+  const float *__restrict__ Wg = p.W;
+  float acc[MAXP][CIN];
+  int sidx[MAXP][9];
+  bool live[MAXP];
+#pragma unroll
+  for (int k = 0; k < MAXP; ++k) {
+    const int pos = threadIdx.x + k * 256;
+    const int u = pos / p.S_in, w = pos - (pos / p.S_in) * p.S_in;
+    const int gy = p.dense ? u : an.y * p.scale - p.h_in + u;
+    const int gx = p.dense ? w : an.z * p.scale - p.h_in + w;
+    live[k] = pos < S_in2 && gy >= 0 && gx >= 0 && gy < p.H_in && gx < p.H_in;
+#pragma unroll
+    for (int tap = 0; tap < 9; ++tap) {
+      const int ky = tap / 3, kx = tap % 3;
+      int yy = u + p.delta - ky, xx = w + p.delta - kx;
+      bool ok = live[k];
+      if (p.stride == 2) {
+        ok = ok && ((yy | xx) & 1) == 0;
+        yy >>= 1;
+        xx >>= 1;
+      }
+      ok = ok && yy >= 0 && xx >= 0 && yy < p.S_out && xx < p.S_out;
+      sidx[k][tap] = ok ? yy * p.S_out + xx : -1;
+    }
+#pragma unroll
+    for (int ci = 0; ci < CIN; ++ci) acc[k][ci] = 0.f;
+  }
   for (int c0 = 0; c0 < p.C_out; c0 += p.cc) {
     __syncthreads();
-    const int nsrc = p.S_out * p.S_out * p.cc;
-    for (int i = threadIdx.x; i < nsrc; i += blockDim.x) {
+    const int nsrc = S_out2 * p.cc;
+    for (int i = threadIdx.x; i < nsrc; i += 256) {
       const int pos = i / p.cc, c = i - pos * p.cc;
-      lds[i] = src[(int64_t)pos * p.C_out + c0 + c];
-    }
-    for (int i = threadIdx.x; i < p.cc * p.C_in * 9; i += blockDim.x) {
-      const int c = i / (p.C_in * 9), rest = i - c * p.C_in * 9;
-      const int ci = rest / 9, tap = rest - ci * 9;
-      wsh[i] = p.W[(((int64_t)(c0 + c) * p.C_in + ci) * 3 + tap / 3) * 3 + tap % 3];
+      lds[c * pitch + pos] = src[(int64_t)pos * p.C_out + c0 + c];
     }
     __syncthreads();
-    for (int k = 0; k < npos && k < 8; ++k) {
-      const int pos = threadIdx.x + k * blockDim.x;
-      if (pos >= S_in2) break;
-      const int u = pos / p.S_in, w = pos - u * p.S_in;
+    for (int c = 0; c < p.cc; ++c) {
+      const float *lc = lds + c * pitch;
+      const float *wc = Wg + (int64_t)(c0 + c) * CIN * 9;
+#pragma unroll
       for (int tap = 0; tap < 9; ++tap) {
-        const int ky = tap / 3, kx = tap - 3 * ky;
-        int yy = u + p.delta - ky, xx = w + p.delta - kx;
-        if (p.stride == 2) {
-          if ((yy | xx) & 1) continue;
-          yy >>= 1;
-          xx >>= 1;
-        }
-        if (yy < 0 || xx < 0 || yy >= p.S_out || xx >= p.S_out) continue;
-        const float *sp = lds + (yy * p.S_out + xx) * p.cc;
-        for (int c = 0; c < p.cc; ++c) {
-          const float a = sp[c];
-          const float *wp = wsh + c * p.C_in * 9 + tap;
-          for (int ci = 0; ci < p.C_in; ++ci) acc[k][ci] += a * wp[ci * 9];
+        float wv[CIN];
+#pragma unroll
+        for (int ci = 0; ci < CIN; ++ci) wv[ci] = wc[ci * 9 + tap];
+#pragma unroll
+        for (int k = 0; k < MAXP; ++k) {
+          const int si = sidx[k][tap];
+          if (si >= 0) {
+            const float a = lc[si];
+#pragma unroll
+            for (int ci = 0; ci < CIN; ++ci) acc[k][ci] += a * wv[ci];
+          }
         }
       }
     }
   }
-  for (int k = 0; k < npos && k < 8; ++k) {
-    const int pos = threadIdx.x + k * blockDim.x;
-    if (pos >= S_in2) break;
-    const int u = pos / p.S_in, w = pos - u * p.S_in;
+#pragma unroll
+  for (int k = 0; k < MAXP; ++k) {
+    const int pos = threadIdx.x + k * 256;
+    if (pos >= S_in2) continue;
+    const int u = pos / p.S_in, w = pos - (pos / p.S_in) * p.S_in;
     const int gy = p.dense ? u : an.y * p.scale - p.h_in + u;
     const int gx = p.dense ? w : an.z * p.scale - p.h_in + w;
     float part = 0.f;
-    if (gy >= 0 && gx >= 0 && gy < p.H_in && gx < p.H_in) {
-      for (int ci = 0; ci < p.C_in; ++ci) {
+    if (live[k]) {
+#pragma unroll
+      for (int ci = 0; ci < CIN; ++ci) {
         const int64_t bi = (int64_t)an.x * p.ld_box + ((int64_t)ci * p.H_in + gy) * p.H_in + gx;
         const float a = acc[k][ci];
         part += a * p.c0[bi] - fabsf(a) * p.r0[bi];
@@ -269,12 +288,30 @@ __global__ __launch_bounds__(256) void k_stem(const StemArgs p) {
   }
 }
 
-hipError_t launch_stem(const StemArgs &a, hipStream_t s) {
-  if (a.C_in > STEM_MAX_CIN || a.S_in * a.S_in > 8 * 256 || a.C_out % a.cc) return hipErrorInvalidValue;
-  const size_t lds = sizeof(float) * ((size_t)a.S_out * a.S_out * a.cc + (size_t)a.cc * a.C_in * 9);
-  if (lds > 64 * 1024) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_stem, dim3((unsigned)a.R), dim3(256), lds, s, a);
+template <int CIN>
+hipError_t launch_stem_t(const StemArgs &a, hipStream_t s) {
+  const int S_in2 = a.S_in * a.S_in;
+  const size_t lds = sizeof(float) * (size_t)a.cc * ((a.S_out * a.S_out) | 1);
+  if (lds > 64 * 1024 || a.C_out % a.cc) return hipErrorInvalidValue;
+  if (S_in2 <= 256)
+    hipLaunchKernelGGL((k_stem<CIN, 1>), dim3((unsigned)a.R), dim3(256), lds, s, a);
+  else if (S_in2 <= 512)
+    hipLaunchKernelGGL((k_stem<CIN, 2>), dim3((unsigned)a.R), dim3(256), lds, s, a);
+  else if (S_in2 <= 1024)
+    hipLaunchKernelGGL((k_stem<CIN, 4>), dim3((unsigned)a.R), dim3(256), lds, s, a);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
+}
+
+hipError_t launch_stem(const StemArgs &a, hipStream_t s) {
+  switch (a.C_in) {
+    case 1: return launch_stem_t<1>(a, s);
+    case 2: return launch_stem_t<2>(a, s);
+    case 3: return launch_stem_t<3>(a, s);
+    case 4: return launch_stem_t<4>(a, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 // ------------------------------------------------------------------------------------

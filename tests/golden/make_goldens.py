@@ -26,6 +26,13 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 # workload name -> inputs of the full batch to store
 GOLDENS = {
     "mlp3072x8192x4": [0, 15],
+    "resnet3x16x16": [0, 1],
+}
+
+# full-size workloads whose bounds are stored for sampled neurons (with every neuron their
+# receptive fields reach): {workload: (inputs, {ReLU position: number of target neurons})}
+SAMPLED = {
+    "resnet3x32x32": ([0], {0: 128, 1: 3, 2: 1}),
 }
 
 
@@ -46,6 +53,28 @@ def make(name, inputs):
     print("wrote", path)
 
 
+def make_sampled(name, inputs, counts):
+    wl = make_workload(name)
+    relus = [i for i, nd in enumerate(wl.net.nodes) if nd.op == "relu"]
+    shapes = oracle.node_shapes(wl.net)
+    out = {"inputs": np.array(inputs), "relus": np.array(relus)}
+    rng = np.random.default_rng(2024)
+    for b in inputs:
+        targets = {relus[k]: np.sort(rng.choice(int(np.prod(shapes[relus[k]])), c, replace=False))
+                   for k, c in counts.items()}
+        t = time.time()
+        res = oracle.crown_sampled(wl.net, wl.x0[b], wl.eps, targets)
+        for i, (idx, l, u) in res.items():
+            out[f"idx_{b}_{i}"] = idx
+            out[f"l_{b}_{i}"] = l
+            out[f"u_{b}_{i}"] = u
+            print(f"{name} input {b} relu {i}: {len(idx)} neurons", flush=True)
+        print(f"{name} input {b}: {time.time() - t:.1f} s", flush=True)
+    path = os.path.join(HERE, f"{name}_sampled.npz")
+    np.savez_compressed(path, **out)
+    print("wrote", path)
+
+
 def make_bab_splits():
     from workloads import draw_splits
     wl = make_workload("bab_mlp784x1024x6")
@@ -58,9 +87,11 @@ def make_bab_splits():
 
 
 if __name__ == "__main__":
-    names = sys.argv[1:] or list(GOLDENS) + ["bab"]
+    names = sys.argv[1:] or list(GOLDENS) + ["bab"] + [f"{k}_sampled" for k in SAMPLED]
     for n in names:
         if n == "bab":
             make_bab_splits()
+        elif n.endswith("_sampled"):
+            make_sampled(n[:-len("_sampled")], *SAMPLED[n[:-len("_sampled")]])
         else:
             make(n, GOLDENS[n])

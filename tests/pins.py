@@ -536,11 +536,33 @@ def pin_ibp_sound_and_contains_crown(o):
     assert_sound(il, iu, spec_values(wl.net, wl.C[0], X), what="ibp spec")
 
 
+def pin_sampled_equals_full(o):
+    """Bounds of selected neurons computed through their receptive fields equal the full
+    pass's bounds of those neurons (same arithmetic; the skipped rows only meet zeros)."""
+    net = tiny_resnet(75, c=4, hw=8)
+    x0 = np.random.default_rng(76).random(net.n_in).astype(np.float32)
+    C = np.random.default_rng(77).standard_normal((2, 5)).astype(np.float32)
+    full = o.crown(net, x0, 0.05, C)
+    relus = sorted(full.layer_l)
+    rng = np.random.default_rng(78)
+    targets = {relus[1]: rng.choice(full.layer_l[relus[1]].size, 3, replace=False),
+               relus[0]: rng.choice(full.layer_l[relus[0]].size, 2, replace=False)}
+    got = o.crown_sampled(net, x0, 0.05, targets)
+    for i, idx in targets.items():
+        gi, gl, gu = got[i]
+        pos = np.searchsorted(gi, idx)
+        np.testing.assert_allclose(gl[pos], full.layer_l[i][idx], rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(gu[pos], full.layer_u[i][idx], rtol=1e-12, atol=1e-12)
+    # the receptive field of a second-block neuron does not cover the whole first layer
+    assert len(got[relus[0]][0]) < full.layer_l[relus[0]].size
+
+
 # fastest first (the mutant test stops at the first pin that fails)
 ALL_PINS = [
     pin_relu_hand_values, pin_relu_net_bounds, pin_single_affine, pin_paper_wrapping_example,
     pin_wrapping_example_intermediate, pin_all_stable, pin_inactive_layer_constant, pin_eps_zero,
     pin_residual_closed_form, pin_ibp_sound_and_contains_crown, pin_conv_library,
-    pin_upper_is_negated_lower, pin_bab_invariants, pin_conv_net_equals_unrolled, pin_lp_sandwich,
+    pin_upper_is_negated_lower, pin_bab_invariants, pin_conv_net_equals_unrolled, pin_sampled_equals_full,
+    pin_lp_sandwich,
     pin_soundness_mlps, pin_lambda_rules_sound, pin_grid_bruteforce,
 ]

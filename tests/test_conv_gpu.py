@@ -87,3 +87,86 @@ def test_conv_batch_invariance_and_chunking():
     lb3, ub3, _ = gpu_crown(ctx, wl)
     assert ctx.stats()["n_chunks_last_call"] > len(layers) + 1
     assert np.array_equal(lb3, lb) and np.array_equal(ub3, ub)
+
+
+def torch_forward(net, X):
+    """fp32 forward of many points on the GPU with torch's own conv/linear (an evaluation
+    independent of the library)."""
+    import torch
+    n = X.shape[0]
+    inp = X.reshape((n,) + tuple(net.in_shape))
+    vals = []
+    get = lambda i: inp if i == -1 else vals[i]  # noqa: E731
+    for nd in net.nodes:
+        v = get(nd.in0)
+        if nd.op == "dense":
+            vals.append(torch.nn.functional.linear(v.reshape(n, -1), to_dev(nd.W), to_dev(nd.b)))
+        elif nd.op == "conv2d":
+            vals.append(torch.nn.functional.conv2d(v, to_dev(nd.W), to_dev(nd.b), stride=nd.stride, padding=nd.pad))
+        elif nd.op == "relu":
+            vals.append(torch.relu(v))
+        elif nd.op == "add":
+            vals.append(v + get(nd.in1))
+        elif nd.op == "flatten":
+            vals.append(v.reshape(n, -1))
+    return vals
+
+
+def test_resnet3x16x16_all_bounds_golden():
+    g = np.load(os.path.join(GOLDEN, "resnet3x16x16.npz"))
+    wl = make_workload("resnet3x16x16")
+    ctx = gpu_ctx(wl.net)
+    lb, ub, layers = gpu_crown(ctx, wl)
+    relu_ids = [i for i, nd in enumerate(wl.net.nodes) if nd.op == "relu"]
+    for b in g["inputs"]:
+        assert_close(lb[b], g[f"lb_{b}"], f"input {b} lb")
+        assert_close(ub[b], g[f"ub_{b}"], f"input {b} ub")
+        for r, i in enumerate(relu_ids):
+            assert_close(layers[r][0][b], g[f"l_{b}_{i}"], f"input {b} relu {r} l")
+            assert_close(layers[r][1][b], g[f"u_{b}_{i}"], f"input {b} relu {r} u")
+
+
+def test_resnet3x32x32_full_size():
+    """The full ResNet workload (8 inputs): the oracle's bounds of sampled neurons and every
+    neuron their receptive fields reach; soundness of the spec bounds on sampled points and
+    box corners; one input alone equals its row of the batch bit for bit."""
+    import torch
+    g = np.load(os.path.join(GOLDEN, "resnet3x32x32_sampled.npz"))
+    wl = make_workload("resnet3x32x32")
+    ctx = gpu_ctx(wl.net)
+    log("gpu run B=8")
+    lb, ub, layers = gpu_crown(ctx, wl)
+    relu_ids = [i for i, nd in enumerate(wl.net.nodes) if nd.op == "relu"]
+    n_checked = 0
+    for b in g["inputs"]:
+        for r, i in enumerate(relu_ids):
+            key = f"idx_{b}_{i}"
+            if key not in g:
+                continue
+            idx = g[key]
+            assert_close(layers[r][0][b][idx], g[f"l_{b}_{i}"], f"input {b} relu {r} l")
+            assert_close(layers[r][1][b][idx], g[f"u_{b}_{i}"], f"input {b} relu {r} u")
+            n_checked += len(idx)
+    log("sampled neurons checked", n_checked)
+    assert n_checked > 1000
+    for r in range(len(layers)):
+        assert np.all(layers[r][0] <= layers[r][1])
+    assert np.all(lb <= ub)
+    # soundness on samples and corners (fp32 forward; slack = parity tolerance)
+    from tests.pins import box_of
+    rng = np.random.default_rng(9)
+    for b in (0, 5):
+        lo, hi = box_of(wl.x0[b], wl.eps, wl.clip)
+        X = lo + (hi - lo) * rng.random((2048, lo.size))
+        Xc = np.where(rng.random((1024, lo.size)) < 0.5, lo, hi)
+        for P in (X, Xc):
+            with torch.no_grad():
+                y = torch_forward(wl.net, torch.from_numpy(P.astype(np.float32)).cuda())[-1]
+                Y = (y.double() @ torch.from_numpy(wl.C[b].astype(np.float64)).cuda().T).cpu().numpy()
+            slack = 1e-4 + 1e-4 * np.abs(Y)
+            assert np.all(Y >= lb[b][None] - slack), np.max(lb[b][None] - Y)
+            assert np.all(Y <= ub[b][None] + slack), np.max(Y - ub[b][None])
+    lb1, ub1, lay1 = gpu_crown(ctx, wl, inputs=[3])
+    assert np.array_equal(lb1[0], lb[3]) and np.array_equal(ub1[0], ub[3])
+    for r in range(len(layers)):
+        assert np.array_equal(lay1[r][0][0], layers[r][0][3])

@@ -274,6 +274,10 @@ WORKLOADS = {
                               batch=1, eps=0.02, n_domains=4096, per_domain=8),
     # ResNet-style CNN on 3x32x32, 8 inputs, 100 classes
     "resnet3x32x32": dict(kind="resnet", seed=4, batch=8, eps=1.0 / 255.0),
+    # the same topology at 3x16x16 with 32/64 channels, FC 64, 10 classes (small enough for
+    # the oracle to compute every bound)
+    "resnet3x16x16": dict(kind="resnet", seed=41, batch=2, eps=2.0 / 255.0,
+                          arch=dict(in_chw=(3, 16, 16), c1=32, c2=64, fc=64, n_out=10)),
 }
 
 
@@ -289,7 +293,7 @@ def make_workload(name: str, batch: int | None = None, **overrides) -> Workload:
         x0 = rng.random((cfg["batch"], cfg["dims"][0])).astype(np.float32)
     elif kind == "resnet":
         rng = np.random.default_rng(cfg["seed"])
-        net = resnet_net(rng)
+        net = resnet_net(rng, **cfg.get("arch", {}))
         x0 = rng.random((cfg["batch"], net.n_in)).astype(np.float32)
     elif kind == "bab":
         net = mlp_net(np.random.default_rng(cfg["net_seed"]), cfg["dims"])
