@@ -17,7 +17,7 @@
  *     such a backward pass from that layer to the input, intersected with the IBP bounds;
  *   - branch-and-bound subdomains (Sec. 2.1, complete verification): each subdomain fixes
  *     some ReLUs to the active (z >= 0) or inactive (z <= 0) state; subdomains of one root
- *     input are bounded in one batched pass (Sec. 2.5, batch BaB).
+ *     input are bounded in one batched pass (Sec. 2.4, batch BaB).
  *
  * Conventions shared by every entry point:
  *   - All tensors are float32, dense, row-major (C order).  Device pointers must come from
@@ -71,7 +71,7 @@ typedef struct {
   const float *W, *b;     /* HOST pointers, copied by vcr_load_net; PyTorch layouts */
 } vcr_node;
 
-/* Branch-and-bound subdomains of one root input (paper, Sec. 2.1 and Sec. 2.5).
+/* Branch-and-bound subdomains of one root input (paper, Sec. 2.1.1 and Sec. 2.4).
  * n_domains x per_domain entries each, DEVICE pointers, row-major by domain:
  *   relu_id[d*per_domain + k]  index of the ReLU node among the network's ReLU nodes, in
  *                              node order (0 = first ReLU);
