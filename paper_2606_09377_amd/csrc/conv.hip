@@ -35,77 +35,89 @@ __device__ __forceinline__ uint32_t fdiv(uint32_t n, FastDiv d) {
   return (uint32_t)(t >> d.shift);
 }
 
-constexpr int CT_BM = 128, CT_BN = 64, CT_BK = 32, CT_LD = CT_BK + 4;
-
+// Tile shapes: BM x BN outputs per workgroup of 4 wave64 arranged WM x WN, each wave
+// owning (BM / WM) x (BN / WN) as 32 x 32 MFMA blocks; BK-deep K tiles through
+// double-buffered LDS (pitch BK + 4 floats).  A K tile never straddles two taps
+// (C_out is a multiple of 32).
+template <int BM, int BN, int BK, int WM, int WN>
 __global__ __launch_bounds__(256, 2) void k_convt(const ConvTArgs p) {
-  __shared__ __attribute__((aligned(16))) float As[2][CT_BM * CT_LD];
-  __shared__ __attribute__((aligned(16))) float Bs[2][CT_BN * CT_LD];
+  constexpr int LD = BK + 4;
+  constexpr int MB = BM / WM / 32, NB = BN / WN / 32;
+  constexpr int TPR = BK / 4;                 // threads per tile row (float4 each)
+  constexpr int RPP = 256 / TPR;              // tile rows per load pass
+  constexpr int QA = BM / RPP, QB = BN / RPP;
+  __shared__ __attribute__((aligned(16))) float As[2][BM * LD];
+  __shared__ __attribute__((aligned(16))) float Bs[2][BN * LD];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int n_nt = p.N_pad / CT_BN;
+  const int wm = wave / WN, wn = wave % WN;
+  const int n_nt = p.N_pad / BN;
   const int mt = blockIdx.x / n_nt, nt = blockIdx.x - mt * n_nt;
-  const int m0 = mt * CT_BM, n0 = nt * CT_BN;
+  const int m0 = mt * BM, n0 = nt * BN;
   const int S_in2 = p.S_in * p.S_in;
 
-  // per-thread source rows for the A tile: rows lrow + 32 q
-  const int lrow = tid >> 3, lcol = (tid & 7) << 2;
-  int64_t a_row_base[4];
-  int ru[4], rw[4];
-  bool rvalid[4];
+  // Per tile row: its source row pointer and its position in the source window before the
+  // tap shift.  With stride s, tap (ky, kx) reads source (ys - (ky >> (s-1)), xs - (kx >> (s-1)))
+  // where ys = (u + delta) >> (s-1), and for s = 2 only taps with ky = u + delta (mod 2); the
+  // tap part of the offset is therefore the same for every row (a wave-uniform value).
+  const int lrow = tid / TPR, lcol = (tid % TPR) * 4;
+  const float *a_row[QA];
+  int ys[QA], xs[QA], par[QA];
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const uint32_t m = (uint32_t)(m0 + lrow + 32 * q);
-    rvalid[q] = m < (uint32_t)p.M;
+  for (int q = 0; q < QA; ++q) {
+    const uint32_t m = (uint32_t)(m0 + lrow + RPP * q);
+    const bool valid = m < (uint32_t)p.M;
     const uint32_t r = fdiv(m, p.div_S2);
     const uint32_t pos = m - r * (uint32_t)S_in2;
     const uint32_t u = fdiv(pos, p.div_S);
-    ru[q] = (int)u;
-    rw[q] = (int)(pos - u * (uint32_t)p.S_in);
-    a_row_base[q] = (int64_t)r * p.row_stride_out;
+    const int uu = (int)u + p.delta, ww = (int)(pos - u * (uint32_t)p.S_in) + p.delta;
+    a_row[q] = p.A + (valid ? (int64_t)r * p.row_stride_out : 0);
+    const int sh = p.stride == 2 ? 1 : 0;
+    ys[q] = valid ? (uu >> sh) : -(1 << 20);   // an invalid row matches no tap
+    xs[q] = ww >> sh;
+    par[q] = sh ? ((uu & 1) | ((ww & 1) << 1)) : 0;
   }
   const float *Bg = p.Bt + (int64_t)(n0 + lrow) * p.ldb + lcol;
-  f32x4 ra[4], rb[2];
+  f32x4 ra[QA], rb[QB];
   auto gload = [&](int kt) {
-    const int k0 = kt * CT_BK;
+    const int k0 = kt * BK;
     const int tap = k0 / p.C_out;
     const int co = k0 - tap * p.C_out + lcol;
     const int ky = tap / 3, kx = tap - 3 * (tap / 3);
+    const int sh = p.stride == 2 ? 1 : 0;
+    const int ty = ky >> sh, tx = kx >> sh;
+    const int tpar = sh ? ((ky & 1) | ((kx & 1) << 1)) : 0;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      int yy = ru[q] + p.delta - ky, xx = rw[q] + p.delta - kx;
-      bool ok = rvalid[q];
-      if (p.stride == 2) {
-        ok = ok && ((yy | xx) & 1) == 0;
-        yy >>= 1;
-        xx >>= 1;
-      }
-      ok = ok && yy >= 0 && xx >= 0 && yy < p.S_out && xx < p.S_out;
-      f32x4 v = {0.f, 0.f, 0.f, 0.f};
-      if (ok) v = *reinterpret_cast<const f32x4 *>(p.A + a_row_base[q] + ((int64_t)yy * p.S_out + xx) * p.C_out + co);
-      ra[q] = v;
+    for (int q = 0; q < QA; ++q) {
+      const int yy = ys[q] - ty, xx = xs[q] - tx;
+      const bool ok = par[q] == tpar && (unsigned)yy < (unsigned)p.S_out && (unsigned)xx < (unsigned)p.S_out;
+      const int off = ok ? (yy * p.S_out + xx) * p.C_out + co : lcol;
+      const f32x4 v = *reinterpret_cast<const f32x4 *>(a_row[q] + off);
+      const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+      ra[q] = ok ? v : z;
     }
 #pragma unroll
-    for (int q = 0; q < 2; ++q) rb[q] = *reinterpret_cast<const f32x4 *>(Bg + (int64_t)q * 32 * p.ldb + k0);
+    for (int q = 0; q < QB; ++q) rb[q] = *reinterpret_cast<const f32x4 *>(Bg + (int64_t)q * RPP * p.ldb + k0);
   };
   auto lstore = [&](int buf) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) *reinterpret_cast<f32x4 *>(&As[buf][(lrow + 32 * q) * CT_LD + lcol]) = ra[q];
+    for (int q = 0; q < QA; ++q) *reinterpret_cast<f32x4 *>(&As[buf][(lrow + RPP * q) * LD + lcol]) = ra[q];
 #pragma unroll
-    for (int q = 0; q < 2; ++q) *reinterpret_cast<f32x4 *>(&Bs[buf][(lrow + 32 * q) * CT_LD + lcol]) = rb[q];
+    for (int q = 0; q < QB; ++q) *reinterpret_cast<f32x4 *>(&Bs[buf][(lrow + RPP * q) * LD + lcol]) = rb[q];
   };
 
-  f32x16 acc[2];
+  f32x16 acc[MB][NB];
 #pragma unroll
-  for (int j = 0; j < 2; ++j)
+  for (int i = 0; i < MB; ++i)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) acc[j][v] = 0.f;
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  const int KT = p.K / CT_BK;
+  const int KT = p.K / BK;
   gload(0);
   lstore(0);
   __syncthreads();
-  const int r32 = lane & 31, kq = (lane >> 5) * 16;
-  const int a_off = (wave * 32 + r32) * CT_LD + kq;
-  const int b_off0 = r32 * CT_LD + kq, b_off1 = (32 + r32) * CT_LD + kq;
+  const int r32 = lane & 31, kq = (lane >> 5) * (BK / 2);
   for (int kt = 0; kt < KT; ++kt) {
     const int cur = kt & 1;
     const bool more = kt + 1 < KT;
@@ -113,15 +125,21 @@ __global__ __launch_bounds__(256, 2) void k_convt(const ConvTArgs p) {
     const float *as = As[cur];
     const float *bs = Bs[cur];
 #pragma unroll
-    for (int h = 0; h < 4; ++h) {
-      const f32x4 a = *reinterpret_cast<const f32x4 *>(as + a_off + 4 * h);
-      const f32x4 b0 = *reinterpret_cast<const f32x4 *>(bs + b_off0 + 4 * h);
-      const f32x4 b1 = *reinterpret_cast<const f32x4 *>(bs + b_off1 + 4 * h);
+    for (int h = 0; h < BK / 8; ++h) {
+      f32x4 a[MB], b[NB];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        acc[0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[e], b0[e], acc[0], 0, 0, 0);
-        acc[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[e], b1[e], acc[1], 0, 0, 0);
-      }
+      for (int i = 0; i < MB; ++i)
+        a[i] = *reinterpret_cast<const f32x4 *>(as + (wm * (BM / WM) + i * 32 + r32) * LD + kq + 4 * h);
+#pragma unroll
+      for (int j = 0; j < NB; ++j)
+        b[j] = *reinterpret_cast<const f32x4 *>(bs + (wn * (BN / WN) + j * 32 + r32) * LD + kq + 4 * h);
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+#pragma unroll
+        for (int i = 0; i < MB; ++i)
+#pragma unroll
+          for (int j = 0; j < NB; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][e], b[j][e], acc[i][j], 0, 0, 0);
     }
     if (more) lstore(cur ^ 1);
     __syncthreads();
@@ -129,70 +147,80 @@ __global__ __launch_bounds__(256, 2) void k_convt(const ConvTArgs p) {
 
   // ---- epilogue ----------------------------------------------------------------------
   const int half = lane >> 5;
-  float rp[16];
 #pragma unroll
-  for (int v = 0; v < 16; ++v) rp[v] = 0.f;
+  for (int i = 0; i < MB; ++i) {
+    float rp[16];
 #pragma unroll
-  for (int v = 0; v < 16; ++v) {
-    const int m = m0 + wave * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
-    if (m >= p.M) continue;
-    const uint32_t r = fdiv((uint32_t)m, p.div_S2);
-    const uint32_t pos = (uint32_t)m - r * (uint32_t)S_in2;
-    const uint32_t u = fdiv(pos, p.div_S);
-    const int w = (int)(pos - u * (uint32_t)p.S_in);
-    const int4 an = p.rows[r];   // (unit, anchor y, anchor x, -)
-    const int gy = p.dense ? (int)u : an.y * p.scale - p.h_in + (int)u;
-    const int gx = p.dense ? w : an.z * p.scale - p.h_in + w;
-    const bool inside = gy >= 0 && gx >= 0 && gy < p.H_in && gx < p.H_in;
-    float *orow = p.out + (int64_t)r * p.row_stride_in + ((int64_t)u * p.S_in + w) * p.C_in;
-#pragma unroll
-    for (int bj = 0; bj < 2; ++bj) {
-      const int n = n0 + bj * 32 + r32;
-      if (n >= p.C_in) continue;
-      float a = acc[bj][v];
-      float ap = 0.f;
-      if (inside) {
-        if (p.res) {
-          const int du = (int)u - p.res_off, dw = w - p.res_off;
-          if (du >= 0 && dw >= 0 && du < p.res_S && dw < p.res_S)
-            a += p.res[(int64_t)r * p.res_row_stride + ((int64_t)du * p.res_S + dw) * p.C_in + n];
-        }
-        float4 prm;
-        if (p.P_pos) {
-          prm = p.P_pos[(((int64_t)an.x * p.H_in + gy) * p.H_in + gx) * p.C_in + n];
-        } else {
-          prm = make_float4(1.f, 1.f, 0.f, p.bias[n]);
-        }
-        ap = a > 0.f ? a * prm.x : a * prm.y;
-        rp[v] += fminf(a, 0.f) * prm.z + ap * prm.w;
-      }
-      orow[n] = ap;
-    }
-  }
-#pragma unroll
-  for (int v = 0; v < 16; ++v) {
-    float x = rp[v];
-    x += __shfl_xor(x, 16);
-    x += __shfl_xor(x, 8);
-    x += __shfl_xor(x, 4);
-    x += __shfl_xor(x, 2);
-    x += __shfl_xor(x, 1);
-    rp[v] = x;
-  }
-  if (r32 == 0) {
+    for (int v = 0; v < 16; ++v) rp[v] = 0.f;
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      const int m = m0 + wave * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
-      if (m < p.M) p.part[(int64_t)nt * p.M_pad + m] = rp[v];
+      const int m = m0 + wm * (BM / WM) + i * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
+      if (m >= p.M) continue;
+      const uint32_t r = fdiv((uint32_t)m, p.div_S2);
+      const uint32_t pos = (uint32_t)m - r * (uint32_t)S_in2;
+      const uint32_t u = fdiv(pos, p.div_S);
+      const int w = (int)(pos - u * (uint32_t)p.S_in);
+      const int4 an = p.rows[r];   // (unit, anchor y, anchor x, -)
+      const int gy = p.dense ? (int)u : an.y * p.scale - p.h_in + (int)u;
+      const int gx = p.dense ? w : an.z * p.scale - p.h_in + w;
+      const bool inside = gy >= 0 && gx >= 0 && gy < p.H_in && gx < p.H_in;
+      float *orow = p.out + (int64_t)r * p.row_stride_in + ((int64_t)u * p.S_in + w) * p.C_in;
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        const int n = n0 + wn * (BN / WN) + j * 32 + r32;
+        if (n >= p.C_in) continue;
+        float a = acc[i][j][v];
+        float ap = 0.f;
+        if (inside) {
+          if (p.res) {
+            const int du = (int)u - p.res_off, dw = w - p.res_off;
+            if (du >= 0 && dw >= 0 && du < p.res_S && dw < p.res_S)
+              a += p.res[(int64_t)r * p.res_row_stride + ((int64_t)du * p.res_S + dw) * p.C_in + n];
+          }
+          float4 prm;
+          if (p.P_pos)
+            prm = p.P_pos[(((int64_t)an.x * p.H_in + gy) * p.H_in + gx) * p.C_in + n];
+          else
+            prm = make_float4(1.f, 1.f, 0.f, p.bias[n]);
+          ap = a > 0.f ? a * prm.x : a * prm.y;
+          rp[v] += fminf(a, 0.f) * prm.z + ap * prm.w;
+        }
+        orow[n] = ap;
+      }
+    }
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      float x = rp[v];
+      x += __shfl_xor(x, 16);
+      x += __shfl_xor(x, 8);
+      x += __shfl_xor(x, 4);
+      x += __shfl_xor(x, 2);
+      x += __shfl_xor(x, 1);
+      rp[v] = x;
+    }
+    if (r32 == 0) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int m = m0 + wm * (BM / WM) + i * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
+        if (m < p.M) p.part[(int64_t)(nt * WN + wn) * p.M_pad + m] = rp[v];
+      }
     }
   }
 }
 
 hipError_t launch_convt(const ConvTArgs &a, hipStream_t s) {
-  if (a.N_pad % CT_BN || a.K % CT_BK || a.C_out % CT_BK || a.M <= 0 || a.M_pad < a.M) return hipErrorInvalidValue;
-  const int64_t grid = (int64_t)((a.M + CT_BM - 1) / CT_BM) * (a.N_pad / CT_BN);
-  if (grid > 0x7fffffff) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_convt, dim3((unsigned)grid), dim3(256), 0, s, a);
+  if (a.K % 32 || a.C_out % 32 || a.M <= 0 || a.M_pad < a.M || a.N_pad % 64) return hipErrorInvalidValue;
+  if (a.N_pad % 128 == 0) {
+    // 128 x 128 tiles, 2 x 2 waves of 64 x 64: partial sums per 64 columns
+    const int64_t grid = (int64_t)((a.M + 127) / 128) * (a.N_pad / 128);
+    if (grid > 0x7fffffff) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_convt<128, 128, 32, 2, 2>), dim3((unsigned)grid), dim3(256), 0, s, a);
+  } else {
+    // 256 x 64 tiles, 4 x 1 waves of 64 x 64
+    const int64_t grid = (int64_t)((a.M + 255) / 256) * (a.N_pad / 64);
+    if (grid > 0x7fffffff) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_convt<256, 64, 16, 4, 1>), dim3((unsigned)grid), dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 
@@ -206,24 +234,32 @@ hipError_t launch_convt(const ConvTArgs &a, hipStream_t s) {
 // chunks; the weights are read with wave-uniform addresses.
 template <int CIN, int MAXP>
 __global__ __launch_bounds__(256) void k_stem(const StemArgs p) {
-  extern __shared__ float lds[];   // [cc][pitch]
-  const int r = blockIdx.x;
-  const int4 an = p.rows[r];
+  // LDS: rpw rows x cc channels x pitch; cell S_out^2 of every channel row is a zero that
+  // invalid taps read, so the inner loop has no branches
+  extern __shared__ float lds[];
   const int S_out2 = p.S_out * p.S_out;
-  const int pitch = S_out2 | 1;
+  const int pitch = (S_out2 + 1) | 1;
   const int S_in2 = p.S_in * p.S_in;
-  const float *src = p.A + (int64_t)r * p.row_stride_out;
+  const int r0 = blockIdx.x * p.rpw;
   const float *__restrict__ Wg = p.W;
   float acc[MAXP][CIN];
   int sidx[MAXP][9];
+  int lbase[MAXP];
+  int rloc[MAXP], ppos[MAXP];
   bool live[MAXP];
 #pragma unroll
   for (int k = 0; k < MAXP; ++k) {
-    const int pos = threadIdx.x + k * 256;
+    const int j = threadIdx.x + k * 256;
+    const int rl = j / S_in2, pos = j - (j / S_in2) * S_in2;
+    rloc[k] = rl;
+    ppos[k] = pos;
+    const bool row_ok = rl < p.rpw && r0 + rl < p.R;
+    const int4 an = row_ok ? p.rows[r0 + rl] : make_int4(0, 0, 0, 0);
     const int u = pos / p.S_in, w = pos - (pos / p.S_in) * p.S_in;
     const int gy = p.dense ? u : an.y * p.scale - p.h_in + u;
     const int gx = p.dense ? w : an.z * p.scale - p.h_in + w;
-    live[k] = pos < S_in2 && gy >= 0 && gx >= 0 && gy < p.H_in && gx < p.H_in;
+    live[k] = row_ok && gy >= 0 && gx >= 0 && gy < p.H_in && gx < p.H_in;
+    lbase[k] = (row_ok ? rl : 0) * p.cc * pitch;
 #pragma unroll
     for (int tap = 0; tap < 9; ++tap) {
       const int ky = tap / 3, kx = tap % 3;
@@ -235,21 +271,25 @@ __global__ __launch_bounds__(256) void k_stem(const StemArgs p) {
         xx >>= 1;
       }
       ok = ok && yy >= 0 && xx >= 0 && yy < p.S_out && xx < p.S_out;
-      sidx[k][tap] = ok ? yy * p.S_out + xx : -1;
+      sidx[k][tap] = ok ? yy * p.S_out + xx : S_out2;
     }
 #pragma unroll
     for (int ci = 0; ci < CIN; ++ci) acc[k][ci] = 0.f;
   }
+  // zero cells (staging never writes them)
+  for (int i = threadIdx.x; i < p.rpw * p.cc; i += 256) lds[i * pitch + S_out2] = 0.f;
+  const int per_row = S_out2 * p.cc;
   for (int c0 = 0; c0 < p.C_out; c0 += p.cc) {
     __syncthreads();
-    const int nsrc = S_out2 * p.cc;
-    for (int i = threadIdx.x; i < nsrc; i += 256) {
-      const int pos = i / p.cc, c = i - pos * p.cc;
-      lds[c * pitch + pos] = src[(int64_t)pos * p.C_out + c0 + c];
+    for (int i = threadIdx.x; i < p.rpw * per_row; i += 256) {
+      const int rl = i / per_row, rem = i - rl * per_row;
+      const int pos = rem >> p.lg_cc, c = rem & (p.cc - 1);
+      if (r0 + rl < p.R)
+        lds[(rl * p.cc + c) * pitch + pos] =
+            p.A[(int64_t)(r0 + rl) * p.row_stride_out + (int64_t)pos * p.C_out + c0 + c];
     }
     __syncthreads();
     for (int c = 0; c < p.cc; ++c) {
-      const float *lc = lds + c * pitch;
       const float *wc = Wg + (int64_t)(c0 + c) * CIN * 9;
 #pragma unroll
       for (int tap = 0; tap < 9; ++tap) {
@@ -258,20 +298,18 @@ __global__ __launch_bounds__(256) void k_stem(const StemArgs p) {
         for (int ci = 0; ci < CIN; ++ci) wv[ci] = wc[ci * 9 + tap];
 #pragma unroll
         for (int k = 0; k < MAXP; ++k) {
-          const int si = sidx[k][tap];
-          if (si >= 0) {
-            const float a = lc[si];
+          const float a = lds[lbase[k] + c * pitch + sidx[k][tap]];
 #pragma unroll
-            for (int ci = 0; ci < CIN; ++ci) acc[k][ci] += a * wv[ci];
-          }
+          for (int ci = 0; ci < CIN; ++ci) acc[k][ci] += a * wv[ci];
         }
       }
     }
   }
 #pragma unroll
   for (int k = 0; k < MAXP; ++k) {
-    const int pos = threadIdx.x + k * 256;
-    if (pos >= S_in2) continue;
+    const int rl = rloc[k], pos = ppos[k];
+    if (rl >= p.rpw || r0 + rl >= p.R) continue;
+    const int4 an = p.rows[r0 + rl];
     const int u = pos / p.S_in, w = pos - (pos / p.S_in) * p.S_in;
     const int gy = p.dense ? u : an.y * p.scale - p.h_in + u;
     const int gx = p.dense ? w : an.z * p.scale - p.h_in + w;
@@ -284,23 +322,42 @@ __global__ __launch_bounds__(256) void k_stem(const StemArgs p) {
         part += a * p.c0[bi] - fabsf(a) * p.r0[bi];
       }
     }
-    p.part[(int64_t)r * S_in2 + pos] = part;
+    p.part[(int64_t)(r0 + rl) * S_in2 + pos] = part;
   }
 }
 
 template <int CIN>
-hipError_t launch_stem_t(const StemArgs &a, hipStream_t s) {
+hipError_t launch_stem_t(StemArgs a, hipStream_t s) {
   const int S_in2 = a.S_in * a.S_in;
-  const size_t lds = sizeof(float) * (size_t)a.cc * ((a.S_out * a.S_out) | 1);
-  if (lds > 64 * 1024 || a.C_out % a.cc) return hipErrorInvalidValue;
-  if (S_in2 <= 256)
-    hipLaunchKernelGGL((k_stem<CIN, 1>), dim3((unsigned)a.R), dim3(256), lds, s, a);
-  else if (S_in2 <= 512)
-    hipLaunchKernelGGL((k_stem<CIN, 2>), dim3((unsigned)a.R), dim3(256), lds, s, a);
-  else if (S_in2 <= 1024)
-    hipLaunchKernelGGL((k_stem<CIN, 4>), dim3((unsigned)a.R), dim3(256), lds, s, a);
+  const int pitch = (a.S_out * a.S_out + 1) | 1;
+  // slots per thread and rows per workgroup with the best lane use
+  int best_p = 0, best_r = 0;
+  double best_u = 0.0;
+  for (int mp : {1, 2, 4}) {
+    const int rpw = 256 * mp / S_in2;
+    if (rpw < 1) continue;
+    const double util = (double)rpw * S_in2 / (256.0 * mp);
+    if (util > best_u + 1e-9) {
+      best_u = util;
+      best_p = mp;
+      best_r = rpw;
+    }
+  }
+  if (!best_p) return hipErrorInvalidValue;
+  a.rpw = best_r;
+  a.cc = a.C_out;
+  while (a.cc > 1 && ((int64_t)a.rpw * a.cc * pitch > 16384 || a.C_out % a.cc)) a.cc /= 2;
+  if ((int64_t)a.rpw * a.cc * pitch > 16384 || (a.cc & (a.cc - 1))) return hipErrorInvalidValue;
+  a.lg_cc = 0;
+  while ((1 << a.lg_cc) < a.cc) ++a.lg_cc;
+  const size_t lds = sizeof(float) * (size_t)a.rpw * a.cc * pitch;
+  const unsigned grid = (unsigned)((a.R + a.rpw - 1) / a.rpw);
+  if (best_p == 1)
+    hipLaunchKernelGGL((k_stem<CIN, 1>), dim3(grid), dim3(256), lds, s, a);
+  else if (best_p == 2)
+    hipLaunchKernelGGL((k_stem<CIN, 2>), dim3(grid), dim3(256), lds, s, a);
   else
-    return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_stem<CIN, 4>), dim3(grid), dim3(256), lds, s, a);
   return hipGetLastError();
 }
 

@@ -796,9 +796,7 @@ vcr_status run_pass(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &pp, int 
         a.stride = nd.stride;
         a.delta = st.src.dense ? 1 : 0;
         a.R = (int32_t)R;
-        int cc = nd.C;
-        while (cc > 1 && ((int64_t)cc * ((a.S_out * a.S_out) | 1) > 16384 || nd.C % cc)) cc /= 2;
-        a.cc = cc;
+
         a.rows = bf.rows;
         a.dense = st.src.dense ? 1 : 0;
         a.scale = st.dst.scale;
