@@ -134,6 +134,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="mlp784x1024x6")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time (0: skip)")
+    ap.add_argument("--graph", action="store_true",
+                    help="replay the call as a recorded HIP graph (the roofline then comes from a "
+                         "second timed pass without the graph)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB three times (HBM counter calibration)")
     args = ap.parse_args()
@@ -181,13 +184,25 @@ def main():
         step()
     torch.cuda.synchronize()
     flops_call = ctx.stats()["gemm_flops_last_call"]
-    ctx.set_option(OPT_TIME_GEMM, 1)
+    if args.graph:
+        from paper_2606_09377_amd.vcrown import OPT_GRAPH
+        ctx.set_option(OPT_GRAPH, 1)
+        step()          # records the graph
+        torch.cuda.synchronize()
+    else:
+        ctx.set_option(OPT_TIME_GEMM, 1)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
+    if args.graph:
+        ctx.set_option(OPT_GRAPH, 0)
+        ctx.set_option(OPT_TIME_GEMM, 1)
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
     st = ctx.stats()
     ctx.set_option(OPT_TIME_GEMM, 0)
     assert np.all(np.isfinite(lb.cpu().numpy()))
@@ -238,6 +253,7 @@ def main():
                      "avg_launch_ms": st["timed_gemm_ms"] / launches if launches else None,
                      "flops_per_launch": st["timed_gemm_flops"] / launches if launches else None},
         "call_mfma_frac": flops_call / (ms_step / 1e3) / (PEAK_FP32_MFMA_TFLOPS * 1e12),
+        "graph_replay": bool(args.graph),
         "gemm_flops_per_step": flops_call,
     }
     rec.update(extra)

@@ -100,9 +100,15 @@ enum {
                                        (or domains) are processed in chunks that fit. */
   VCR_OPT_SYNC_CHECK = 6,           /* 1: synchronise after each call and report device errors
                                        and invalid split domains as the call's status */
-  VCR_OPT_TIME_GEMM = 7             /* 1: bracket every backward-step GEMM launch with HIP events
+  VCR_OPT_TIME_GEMM = 7,            /* 1: bracket every backward-step GEMM launch with HIP events
                                        on the context's stream; vcr_get_stats reports their summed
                                        duration.  Setting the option (either value) resets the sums. */
+  VCR_OPT_GRAPH = 8                 /* 1: vcr_crown_bounds without splits records its kernel launches
+                                       into a HIP graph (captured on a private stream after one
+                                       ordinary call with the same arguments) and, while the
+                                       arguments, options, network and workspace stay the same,
+                                       replays the graph on the context's stream instead of
+                                       launching kernel by kernel.  Ignored while TIME_GEMM is on. */
 };
 
 typedef struct {

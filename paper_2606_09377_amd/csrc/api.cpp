@@ -262,6 +262,8 @@ void vcr_destroy(vcr_ctx *c) {
     free_ws(c);
     if (c->d_counters) (void)hipFree(c->d_counters);
     for (auto e : c->ev_pool) (void)hipEventDestroy(e);
+    if (c->gexec) (void)hipGraphExecDestroy(c->gexec);
+    if (c->cap_stream) (void)hipStreamDestroy(c->cap_stream);
   }
   destroy_graph(c->graph);
   delete c;
@@ -288,6 +290,13 @@ vcr_status vcr_set_option(vcr_ctx *c, int32_t key, double v) {
       c->ws_cap = (uint64_t)v;
       break;
     case VCR_OPT_SYNC_CHECK: c->sync_check = v != 0.0; break;
+    case VCR_OPT_GRAPH:
+      c->use_graph = v != 0.0;
+      if (!c->use_graph && c->gexec) {
+        (void)hipGraphExecDestroy(c->gexec);
+        c->gexec = nullptr;
+      }
+      break;
     case VCR_OPT_TIME_GEMM:
       if (c->device >= 0 && c->ev_used) (void)hipStreamSynchronize(c->stream);
       c->time_gemm = v != 0.0;
@@ -303,6 +312,11 @@ vcr_status vcr_set_option(vcr_ctx *c, int32_t key, double v) {
 
 vcr_status vcr_load_net(vcr_ctx *c, const vcr_node *nodes, int32_t n, const int32_t in_chw[3]) {
   if (!c) return VCR_ERR_ARG;
+  ++c->net_epoch;   // any recorded graph refers to the previous weights
+  if (c->gexec) {
+    (void)hipGraphExecDestroy(c->gexec);
+    c->gexec = nullptr;
+  }
   std::vector<std::vector<int64_t>> sh;
   vcr_status st = validate_net(c, nodes, n, in_chw, &sh);
   if (st != VCR_OK) return st;
@@ -747,8 +761,56 @@ vcr_status vcr_crown_bounds(vcr_ctx *c, const float *x0, int32_t B, float eps, c
     if (c->relu_n.empty()) return fail(c, VCR_ERR_ARG, "splits need at least one ReLU");
     if ((int64_t)splits->n_domains * m > (int64_t)1 << 30) return fail(c, VCR_ERR_SHAPE, "n_domains * m too large");
   }
-  st = c->graph ? graph_crown(c, x0, B, eps, C, m, splits, lb, ub) : crown_impl(c, x0, B, eps, C, m, splits, lb, ub);
-  return after_call(c, st, t0);
+  auto run = [&]() {
+    return c->graph ? graph_crown(c, x0, B, eps, C, m, splits, lb, ub) : crown_impl(c, x0, B, eps, C, m, splits, lb, ub);
+  };
+  if (!c->use_graph || splits || c->time_gemm || c->device < 0) return after_call(c, run(), t0);
+  // graph replay: the key names everything a recorded launch sequence depends on
+  std::vector<uint64_t> key = {(uint64_t)(uintptr_t)x0, (uint64_t)B, (uint64_t)*reinterpret_cast<const uint32_t *>(&eps),
+                               (uint64_t)(uintptr_t)C, (uint64_t)m, (uint64_t)(uintptr_t)lb, (uint64_t)(uintptr_t)ub,
+                               (uint64_t)c->clip_on, (uint64_t)*reinterpret_cast<const uint32_t *>(&c->clip_lo),
+                               (uint64_t)*reinterpret_cast<const uint32_t *>(&c->clip_hi), (uint64_t)c->intersect,
+                               c->ws_cap, c->net_epoch, (uint64_t)(uintptr_t)c->ws.base, (uint64_t)c->ws.cap};
+  if (c->gexec && key == c->gkey) {
+    HIP_TRY(c, hipSetDevice(c->device));
+    HIP_TRY(c, hipGraphLaunch(c->gexec, c->stream));
+    return after_call(c, VCR_OK, t0);
+  }
+  // one ordinary call (allocates the workspace and produces this call's results) ...
+  st = run();
+  if (st != VCR_OK) return after_call(c, st, t0);
+  // ... then the same launches recorded on a private stream
+  if (c->gexec) {
+    (void)hipGraphExecDestroy(c->gexec);
+    c->gexec = nullptr;
+  }
+  if (!c->cap_stream) HIP_TRY(c, hipStreamCreateWithFlags(&c->cap_stream, hipStreamNonBlocking));
+  key[13] = (uint64_t)(uintptr_t)c->ws.base;
+  key[14] = (uint64_t)c->ws.cap;
+  hipStream_t user = c->stream;
+  c->stream = c->cap_stream;
+  hipGraph_t g = nullptr;
+  hipError_t e = hipStreamBeginCapture(c->cap_stream, hipStreamCaptureModeThreadLocal);
+  if (e == hipSuccess) {
+    st = run();
+    hipError_t e2 = hipStreamEndCapture(c->cap_stream, &g);
+    if (e == hipSuccess) e = e2;
+  }
+  c->stream = user;
+  if (st != VCR_OK || e != hipSuccess) {
+    if (g) (void)hipGraphDestroy(g);
+    (void)hipGetLastError();
+    if (st == VCR_OK) st = fail(c, VCR_ERR_DEVICE, "graph capture failed: %s", hipGetErrorString(e));
+    return after_call(c, st, t0);
+  }
+  e = hipGraphInstantiate(&c->gexec, g, nullptr, nullptr, 0);
+  (void)hipGraphDestroy(g);
+  if (e != hipSuccess) {
+    c->gexec = nullptr;
+    return after_call(c, fail(c, VCR_ERR_DEVICE, "graph instantiation failed: %s", hipGetErrorString(e)), t0);
+  }
+  c->gkey = key;
+  return after_call(c, VCR_OK, t0);
 }
 
 vcr_status vcr_ibp_bounds(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m,

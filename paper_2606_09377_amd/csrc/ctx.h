@@ -67,6 +67,12 @@ struct vcr_ctx {
   int32_t chunks_last = 0;
   // convolutional-network path (null for MLPs)
   vcr::GraphNet *graph = nullptr;
+  // HIP graph replay of a repeated call (VCR_OPT_GRAPH)
+  int32_t use_graph = 0;
+  uint64_t net_epoch = 0;
+  hipStream_t cap_stream = nullptr;
+  hipGraphExec_t gexec = nullptr;
+  std::vector<uint64_t> gkey;
   // GEMM timing (VCR_OPT_TIME_GEMM)
   int32_t time_gemm = 0;
   std::vector<hipEvent_t> ev_pool;      // pairs: start, stop

@@ -20,7 +20,7 @@ VCR_OK, VCR_ERR_ARG, VCR_ERR_SHAPE, VCR_ERR_STATE, VCR_ERR_OOM, VCR_ERR_DEVICE, 
 STATUS_NAMES = ["OK", "ERR_ARG", "ERR_SHAPE", "ERR_STATE", "ERR_OOM", "ERR_DEVICE", "ERR_UNSUPPORTED"]
 OPS = {"dense": 0, "conv2d": 1, "relu": 2, "add": 3, "flatten": 4}
 (OPT_CLIP_ENABLE, OPT_CLIP_LO, OPT_CLIP_HI, OPT_INTERSECT_IBP, OPT_WORKSPACE_CAP_BYTES, OPT_SYNC_CHECK,
- OPT_TIME_GEMM) = range(1, 8)
+ OPT_TIME_GEMM, OPT_GRAPH) = range(1, 9)
 
 
 class VcrNode(ctypes.Structure):
