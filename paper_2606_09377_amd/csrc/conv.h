@@ -11,18 +11,31 @@ struct FastDiv {
 };
 FastDiv make_fastdiv(uint32_t d);
 
+// One output-parity class of a transposed convolution.  With stride 2 an output position
+// (u, w) of the destination window only receives the taps whose (ky, kx) have the parity of
+// (u + delta, w + delta), so the GEMM runs as four classes, each with only its own taps (4, 2,
+// 2 and 1 of the 9); with stride 1 there is one class with all 9.  Positions of a class:
+// u = u0 + stride iy, w = w0 + stride ix; taps: (ky0 + kstep ty, kx0 + kstep tx).
+struct ConvClass {
+  int32_t blk0;              // first workgroup of the class (classes are consecutive)
+  int32_t M;                 // GEMM rows of the class: R ny nx
+  int32_t ny, nx, u0, w0;
+  int32_t nty, ntx, ky0, kx0, kstep;
+  FastDiv div_yx, div_x;
+};
+
 struct ConvTArgs {
   const float *A;          // source windows [R][S_out][S_out][C_out]
   int64_t row_stride_out;  // S_out^2 C_out
   int32_t S_out, C_out;
-  const float *Bt;         // [N_pad][ldb], ldb = K = 9 C_out
+  const float *Bt;         // [N_pad][ldb], ldb = 9 C_out: Bt[ci][(3 ky + kx) C_out + co]
   int64_t ldb;
-  int32_t K, N_pad;
+  int32_t N_pad;
   int32_t C_in, S_in, H_in;  // destination channels, window size, image size
   int64_t row_stride_in;     // S_in^2 C_in
   int32_t stride, delta;
-  int32_t M, M_pad;          // GEMM rows R * S_in^2
-  FastDiv div_S2, div_S;
+  int32_t R;                 // coefficient rows
+  int32_t M_pad;             // partial-sum pitch (>= R S_in^2)
   const int4 *rows;          // per coefficient row: (unit, anchor y, anchor x, -)
   int32_t dense, scale, h_in;  // window origin = anchor * scale - h_in (dense: 0)
   const float *res;          // optional residual windows on the same node
@@ -32,6 +45,9 @@ struct ConvTArgs {
   const float *bias;         // identity: constant per channel
   float *out;                // [R][S_in][S_in][C_in]
   float *part;               // [N_pad / 64][M_pad]
+  // filled by launch_convt
+  int32_t n_cls;
+  ConvClass cls[4];
 };
 hipError_t launch_convt(const ConvTArgs &a, hipStream_t s);
 

@@ -13,7 +13,8 @@
 // The transposed convolution of one row is an implicit GEMM:
 //   out[(r, u, w), ci] = sum_{tap=(ky,kx), co} A_out[r][u'][w'][co] * W[co][ci][ky][kx]
 //   u' = (u + delta - ky) / stride (only when divisible and inside the source window)
-// with M = rows x S_in^2, N = C_in, K = 9 C_out.  The weights are repacked at load time as
+// with M = rows x S_in^2, N = C_in, K = 9 C_out (with stride 2, split by output parity into
+// four GEMMs over their own taps only).  The weights are repacked at load time as
 // Bt[ci][tap * C_out + co] (K-contiguous).  The epilogue applies, per output element at
 // global position (gy, gx):
 //   outside the image          -> 0
@@ -37,72 +38,86 @@ __device__ __forceinline__ uint32_t fdiv(uint32_t n, FastDiv d) {
 
 // Tile shapes: BM x BN outputs per workgroup of 4 wave64 arranged WM x WN, each wave
 // owning (BM / WM) x (BN / WN) as 32 x 32 MFMA blocks; BK-deep K tiles through
-// double-buffered LDS (pitch BK + 4 floats).  A K tile never straddles two taps
-// (C_out is a multiple of 32).
-template <int BM, int BN, int BK, int WM, int WN>
-__global__ __launch_bounds__(256, 2) void k_convt(const ConvTArgs p) {
-  constexpr int LD = BK + 4;
+// double-buffered LDS.  A K tile never straddles two taps (C_out is a multiple of 32).
+//
+// LDS rows hold BK floats unpadded, as BK / 4 16-byte chunks; chunk c of tile row q sits at
+// chunk c ^ swz(q).  The tile stores (BK / 4 threads per row) and the MFMA operand reads (8
+// consecutive rows at one chunk per 8 lanes) then both touch 8 distinct 4-bank groups.
+template <int BK>
+__device__ __forceinline__ int lds_swz(int row) {
+  constexpr int CPR = BK / 4, RPG = 8 / CPR;
+  return (row / RPG) & (CPR - 1);
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int MINB>
+__global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
+  static_assert(BK == 16 || BK == 32, "LDS swizzle assumes 4 or 8 chunks per row");
+  constexpr int CPR = BK / 4;                 // 16-byte chunks per tile row
   constexpr int MB = BM / WM / 32, NB = BN / WN / 32;
-  constexpr int TPR = BK / 4;                 // threads per tile row (float4 each)
+  constexpr int TPR = CPR;                    // threads per tile row (one chunk each)
   constexpr int RPP = 256 / TPR;              // tile rows per load pass
   constexpr int QA = BM / RPP, QB = BN / RPP;
-  __shared__ __attribute__((aligned(16))) float As[2][BM * LD];
-  __shared__ __attribute__((aligned(16))) float Bs[2][BN * LD];
+  __shared__ __attribute__((aligned(16))) float As[2][BM * BK];
+  __shared__ __attribute__((aligned(16))) float Bs[2][BN * BK];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
-  const int n_nt = p.N_pad / BN;
-  const int mt = blockIdx.x / n_nt, nt = blockIdx.x - mt * n_nt;
-  const int m0 = mt * BM, n0 = nt * BN;
-  const int S_in2 = p.S_in * p.S_in;
 
-  // Per tile row: its source row pointer and its position in the source window before the
-  // tap shift.  With stride s, tap (ky, kx) reads source (ys - (ky >> (s-1)), xs - (kx >> (s-1)))
-  // where ys = (u + delta) >> (s-1), and for s = 2 only taps with ky = u + delta (mod 2); the
-  // tap part of the offset is therefore the same for every row (a wave-uniform value).
+  // parity class of this workgroup (wave-uniform selects, no indexed argument access)
+  const int bid = blockIdx.x;
+  const int c = (bid >= p.cls[1].blk0) + (bid >= p.cls[2].blk0) + (bid >= p.cls[3].blk0);
+  const ConvClass cl = c == 0 ? p.cls[0] : c == 1 ? p.cls[1] : c == 2 ? p.cls[2] : p.cls[3];
+  const int n_nt = p.N_pad / BN;
+  const int lb = bid - cl.blk0;
+  const int mt = lb / n_nt, nt = lb - mt * n_nt;
+  const int m0 = mt * BM, n0 = nt * BN;
+  const int nyx = cl.ny * cl.nx;
+  const int sh = p.stride == 2 ? 1 : 0;
+
+  // Per tile row: its source row pointer and its class position (iy, ix).  Tap (ty, tx) of
+  // the class reads source position (iy + dy, ix + dx) with a wave-uniform shift (dy, dx).
   const int lrow = tid / TPR, lcol = (tid % TPR) * 4;
+  const int scol = (((tid % TPR)) ^ lds_swz<BK>(lrow)) * 4;
   const float *a_row[QA];
-  int ys[QA], xs[QA], par[QA];
+  int ys[QA], xs[QA];
 #pragma unroll
   for (int q = 0; q < QA; ++q) {
     const uint32_t m = (uint32_t)(m0 + lrow + RPP * q);
-    const bool valid = m < (uint32_t)p.M;
-    const uint32_t r = fdiv(m, p.div_S2);
-    const uint32_t pos = m - r * (uint32_t)S_in2;
-    const uint32_t u = fdiv(pos, p.div_S);
-    const int uu = (int)u + p.delta, ww = (int)(pos - u * (uint32_t)p.S_in) + p.delta;
+    const bool valid = m < (uint32_t)cl.M;
+    const uint32_t r = fdiv(m, cl.div_yx);
+    const uint32_t pos = m - r * (uint32_t)nyx;
+    const uint32_t iy = fdiv(pos, cl.div_x);
     a_row[q] = p.A + (valid ? (int64_t)r * p.row_stride_out : 0);
-    const int sh = p.stride == 2 ? 1 : 0;
-    ys[q] = valid ? (uu >> sh) : -(1 << 20);   // an invalid row matches no tap
-    xs[q] = ww >> sh;
-    par[q] = sh ? ((uu & 1) | ((ww & 1) << 1)) : 0;
+    ys[q] = valid ? (int)iy : -(1 << 20);   // an invalid row matches no tap
+    xs[q] = (int)(pos - iy * (uint32_t)cl.nx);
   }
   const float *Bg = p.Bt + (int64_t)(n0 + lrow) * p.ldb + lcol;
   f32x4 ra[QA], rb[QB];
   auto gload = [&](int kt) {
     const int k0 = kt * BK;
-    const int tap = k0 / p.C_out;
-    const int co = k0 - tap * p.C_out + lcol;
-    const int ky = tap / 3, kx = tap - 3 * (tap / 3);
-    const int sh = p.stride == 2 ? 1 : 0;
-    const int ty = ky >> sh, tx = kx >> sh;
-    const int tpar = sh ? ((ky & 1) | ((kx & 1) << 1)) : 0;
+    const int t = k0 / p.C_out;
+    const int co0 = k0 - t * p.C_out;
+    const int ty = t / cl.ntx, tx = t - ty * cl.ntx;
+    const int ky = cl.ky0 + cl.kstep * ty, kx = cl.kx0 + cl.kstep * tx;
+    const int dy = (cl.u0 + p.delta - ky) >> sh, dx = (cl.w0 + p.delta - kx) >> sh;   // exact
+    const int co = co0 + lcol;
 #pragma unroll
     for (int q = 0; q < QA; ++q) {
-      const int yy = ys[q] - ty, xx = xs[q] - tx;
-      const bool ok = par[q] == tpar && (unsigned)yy < (unsigned)p.S_out && (unsigned)xx < (unsigned)p.S_out;
+      const int yy = ys[q] + dy, xx = xs[q] + dx;
+      const bool ok = (unsigned)yy < (unsigned)p.S_out && (unsigned)xx < (unsigned)p.S_out;
       const int off = ok ? (yy * p.S_out + xx) * p.C_out + co : lcol;
       const f32x4 v = *reinterpret_cast<const f32x4 *>(a_row[q] + off);
       const f32x4 z = {0.f, 0.f, 0.f, 0.f};
       ra[q] = ok ? v : z;
     }
+    const int kb = (3 * ky + kx) * p.C_out + co0;
 #pragma unroll
-    for (int q = 0; q < QB; ++q) rb[q] = *reinterpret_cast<const f32x4 *>(Bg + (int64_t)q * RPP * p.ldb + k0);
+    for (int q = 0; q < QB; ++q) rb[q] = *reinterpret_cast<const f32x4 *>(Bg + (int64_t)q * RPP * p.ldb + kb);
   };
   auto lstore = [&](int buf) {
 #pragma unroll
-    for (int q = 0; q < QA; ++q) *reinterpret_cast<f32x4 *>(&As[buf][(lrow + RPP * q) * LD + lcol]) = ra[q];
+    for (int q = 0; q < QA; ++q) *reinterpret_cast<f32x4 *>(&As[buf][(lrow + RPP * q) * BK + scol]) = ra[q];
 #pragma unroll
-    for (int q = 0; q < QB; ++q) *reinterpret_cast<f32x4 *>(&Bs[buf][(lrow + RPP * q) * LD + lcol]) = rb[q];
+    for (int q = 0; q < QB; ++q) *reinterpret_cast<f32x4 *>(&Bs[buf][(lrow + RPP * q) * BK + scol]) = rb[q];
   };
 
   f32x16 acc[MB][NB];
@@ -113,26 +128,28 @@ __global__ __launch_bounds__(256, 2) void k_convt(const ConvTArgs p) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  const int KT = p.K / BK;
+  const int KT = cl.nty * cl.ntx * p.C_out / BK;
   gload(0);
   lstore(0);
   __syncthreads();
-  const int r32 = lane & 31, kq = (lane >> 5) * (BK / 2);
+  // operand reads: lane (r32, half) takes chunks half * CPR / 2 + h, h < CPR / 2, of row r32
+  const int r32 = lane & 31, sw = lds_swz<BK>(r32);
+  int roff[CPR / 2];
+#pragma unroll
+  for (int h = 0; h < CPR / 2; ++h) roff[h] = ((((lane >> 5) * (CPR / 2)) + h) ^ sw) * 4;
   for (int kt = 0; kt < KT; ++kt) {
     const int cur = kt & 1;
     const bool more = kt + 1 < KT;
     if (more) gload(kt + 1);
-    const float *as = As[cur];
-    const float *bs = Bs[cur];
+    const float *as = As[cur] + (wm * (BM / WM) + r32) * BK;
+    const float *bs = Bs[cur] + (wn * (BN / WN) + r32) * BK;
 #pragma unroll
-    for (int h = 0; h < BK / 8; ++h) {
+    for (int h = 0; h < CPR / 2; ++h) {
       f32x4 a[MB], b[NB];
 #pragma unroll
-      for (int i = 0; i < MB; ++i)
-        a[i] = *reinterpret_cast<const f32x4 *>(as + (wm * (BM / WM) + i * 32 + r32) * LD + kq + 4 * h);
+      for (int i = 0; i < MB; ++i) a[i] = *reinterpret_cast<const f32x4 *>(as + i * 32 * BK + roff[h]);
 #pragma unroll
-      for (int j = 0; j < NB; ++j)
-        b[j] = *reinterpret_cast<const f32x4 *>(bs + (wn * (BN / WN) + j * 32 + r32) * LD + kq + 4 * h);
+      for (int j = 0; j < NB; ++j) b[j] = *reinterpret_cast<const f32x4 *>(bs + j * 32 * BK + roff[h]);
 #pragma unroll
       for (int e = 0; e < 4; ++e)
 #pragma unroll
@@ -146,46 +163,73 @@ __global__ __launch_bounds__(256, 2) void k_convt(const ConvTArgs p) {
   }
 
   // ---- epilogue ----------------------------------------------------------------------
+  // A lane holds 16 rows of each 32 x 32 block, as 4 groups of 4 consecutive GEMM rows.  Per
+  // group, every global load (row anchors, then relaxation parameters and residual terms for
+  // all of the lane's columns) is issued before the group's first store.
   const int half = lane >> 5;
+  const int S_in2 = p.S_in * p.S_in;
+  const float4 *__restrict__ Pp = p.P_pos;
+  const float *__restrict__ resp = p.res;
+  const float *__restrict__ biasp = p.bias;
+  const int4 *__restrict__ rowsp = p.rows;
+  float *__restrict__ outp = p.out;
 #pragma unroll
   for (int i = 0; i < MB; ++i) {
     float rp[16];
+    int mo[16];
 #pragma unroll
-    for (int v = 0; v < 16; ++v) rp[v] = 0.f;
+    for (int g = 0; g < 4; ++g) {
+      int pb[4];
+      int64_t ob[4], rb[4];
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int m = m0 + wm * (BM / WM) + i * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
-      if (m >= p.M) continue;
-      const uint32_t r = fdiv((uint32_t)m, p.div_S2);
-      const uint32_t pos = (uint32_t)m - r * (uint32_t)S_in2;
-      const uint32_t u = fdiv(pos, p.div_S);
-      const int w = (int)(pos - u * (uint32_t)p.S_in);
-      const int4 an = p.rows[r];   // (unit, anchor y, anchor x, -)
-      const int gy = p.dense ? (int)u : an.y * p.scale - p.h_in + (int)u;
-      const int gx = p.dense ? w : an.z * p.scale - p.h_in + w;
-      const bool inside = gy >= 0 && gx >= 0 && gy < p.H_in && gx < p.H_in;
-      float *orow = p.out + (int64_t)r * p.row_stride_in + ((int64_t)u * p.S_in + w) * p.C_in;
+      for (int t = 0; t < 4; ++t) {
+        const int m = m0 + wm * (BM / WM) + i * 32 + g * 8 + half * 4 + t;
+        const bool valid = m < cl.M;
+        const uint32_t r = valid ? fdiv((uint32_t)m, cl.div_yx) : 0u;
+        const uint32_t pos = valid ? (uint32_t)m - r * (uint32_t)nyx : 0u;
+        const uint32_t iy = fdiv(pos, cl.div_x);
+        const int u = cl.u0 + ((int)iy << sh);
+        const int w = cl.w0 + ((int)(pos - iy * (uint32_t)cl.nx) << sh);
+        const int4 an = rowsp[r];   // (unit, anchor y, anchor x, -)
+        const int gy = p.dense ? u : an.y * p.scale - p.h_in + u;
+        const int gx = p.dense ? w : an.z * p.scale - p.h_in + w;
+        const bool inside = valid && gy >= 0 && gx >= 0 && gy < p.H_in && gx < p.H_in;
+        const int du = u - p.res_off, dw = w - p.res_off;
+        mo[g * 4 + t] = valid ? (int)r * S_in2 + u * p.S_in + w : -1;
+        ob[t] = (int64_t)r * p.row_stride_in + ((int64_t)u * p.S_in + w) * p.C_in;
+        pb[t] = inside ? ((an.x * p.H_in + gy) * p.H_in + gx) * p.C_in : -1;
+        rb[t] = inside && resp && du >= 0 && dw >= 0 && du < p.res_S && dw < p.res_S
+                    ? (int64_t)r * p.res_row_stride + ((int64_t)du * p.res_S + dw) * p.C_in
+                    : -1;
+      }
+      float4 prm[NB][4];
+      float rv[NB][4];
 #pragma unroll
       for (int j = 0; j < NB; ++j) {
         const int n = n0 + wn * (BN / WN) + j * 32 + r32;
-        if (n >= p.C_in) continue;
-        float a = acc[i][j][v];
-        float ap = 0.f;
-        if (inside) {
-          if (p.res) {
-            const int du = (int)u - p.res_off, dw = w - p.res_off;
-            if (du >= 0 && dw >= 0 && du < p.res_S && dw < p.res_S)
-              a += p.res[(int64_t)r * p.res_row_stride + ((int64_t)du * p.res_S + dw) * p.C_in + n];
-          }
-          float4 prm;
-          if (p.P_pos)
-            prm = p.P_pos[(((int64_t)an.x * p.H_in + gy) * p.H_in + gx) * p.C_in + n];
-          else
-            prm = make_float4(1.f, 1.f, 0.f, p.bias[n]);
-          ap = a > 0.f ? a * prm.x : a * prm.y;
-          rp[v] += fminf(a, 0.f) * prm.z + ap * prm.w;
+        const bool nok = n < p.C_in;
+        const float bn = (!Pp && nok) ? biasp[n] : 0.f;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          prm[j][t] = (Pp && nok && pb[t] >= 0) ? Pp[pb[t] + n] : make_float4(1.f, 1.f, 0.f, bn);
+          rv[j][t] = (nok && rb[t] >= 0) ? resp[rb[t] + n] : 0.f;
         }
-        orow[n] = ap;
+      }
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        float x = 0.f;
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+          const int n = n0 + wn * (BN / WN) + j * 32 + r32;
+          const float a = acc[i][j][g * 4 + t] + rv[j][t];
+          float ap = 0.f;
+          if (pb[t] >= 0) {   // inside the image: relax (or identity) and constant terms
+            ap = a > 0.f ? a * prm[j][t].x : a * prm[j][t].y;
+            x += fminf(a, 0.f) * prm[j][t].z + ap * prm[j][t].w;
+          }
+          if (mo[g * 4 + t] >= 0 && n < p.C_in) outp[ob[t] + n] = ap;
+        }
+        rp[g * 4 + t] = x;
       }
     }
 #pragma unroll
@@ -200,26 +244,65 @@ __global__ __launch_bounds__(256, 2) void k_convt(const ConvTArgs p) {
     }
     if (r32 == 0) {
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int m = m0 + wm * (BM / WM) + i * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
-        if (m < p.M) p.part[(int64_t)(nt * WN + wn) * p.M_pad + m] = rp[v];
-      }
+      for (int v = 0; v < 16; ++v)
+        if (mo[v] >= 0) p.part[(int64_t)(nt * WN + wn) * p.M_pad + mo[v]] = rp[v];
     }
   }
 }
 
-hipError_t launch_convt(const ConvTArgs &a, hipStream_t s) {
-  if (a.K % 32 || a.C_out % 32 || a.M <= 0 || a.M_pad < a.M || a.N_pad % 64) return hipErrorInvalidValue;
-  if (a.N_pad % 128 == 0) {
-    // 128 x 128 tiles, 2 x 2 waves of 64 x 64: partial sums per 64 columns
-    const int64_t grid = (int64_t)((a.M + 127) / 128) * (a.N_pad / 128);
-    if (grid > 0x7fffffff) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((k_convt<128, 128, 32, 2, 2>), dim3((unsigned)grid), dim3(256), 0, s, a);
-  } else {
-    // 256 x 64 tiles, 4 x 1 waves of 64 x 64
-    const int64_t grid = (int64_t)((a.M + 255) / 256) * (a.N_pad / 64);
-    if (grid > 0x7fffffff) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((k_convt<256, 64, 16, 4, 1>), dim3((unsigned)grid), dim3(256), 0, s, a);
+// Fills the parity classes for BM-row tiles; returns the number of workgroups (or -1).
+static int64_t convt_classes(ConvTArgs &a, int BM, int BN) {
+  if (a.C_out % 32 || a.R <= 0 || a.N_pad % BN || a.N_pad <= 0 || (a.stride != 1 && a.stride != 2)) return -1;
+  if ((int64_t)a.R * a.S_in * a.S_in > a.M_pad) return -1;
+  const int n_nt = a.N_pad / BN;
+  a.n_cls = a.stride == 2 ? 4 : 1;
+  int64_t blk = 0;
+  for (int c = 0; c < 4; ++c) {
+    ConvClass &k = a.cls[c];
+    k = ConvClass{};
+    if (c >= a.n_cls) {
+      k.blk0 = 0x7fffffff;
+      continue;
+    }
+    if (a.stride == 1) {
+      k.u0 = k.w0 = 0;
+      k.ny = k.nx = a.S_in;
+      k.nty = k.ntx = 3;
+      k.ky0 = k.kx0 = 0;
+      k.kstep = 1;
+    } else {
+      const int py = c & 1, px = c >> 1;   // parity of u + delta, w + delta
+      k.u0 = (py - a.delta) & 1;
+      k.w0 = (px - a.delta) & 1;
+      k.ny = (a.S_in - k.u0 + 1) / 2;
+      k.nx = (a.S_in - k.w0 + 1) / 2;
+      k.ky0 = py;
+      k.kx0 = px;
+      k.nty = py ? 1 : 2;
+      k.ntx = px ? 1 : 2;
+      k.kstep = 2;
+    }
+    const int64_t M = (int64_t)a.R * k.ny * k.nx;
+    if (M >= ((int64_t)1 << 31)) return -1;
+    k.M = (int32_t)M;
+    k.div_yx = make_fastdiv((uint32_t)(k.ny * k.nx));
+    k.div_x = make_fastdiv((uint32_t)k.nx);
+    k.blk0 = (int32_t)blk;
+    blk += (M + BM - 1) / BM * n_nt;
+  }
+  return blk > 0x7fffffff ? -1 : blk;
+}
+
+hipError_t launch_convt(const ConvTArgs &a0, hipStream_t s) {
+  ConvTArgs a = a0;
+  if (a.N_pad % 128 == 0) {   // 128 x 128 tiles, 2 x 2 waves of 64 x 64
+    const int64_t blk = convt_classes(a, 128, 128);
+    if (blk < 0) return hipErrorInvalidValue;
+    if (blk > 0) hipLaunchKernelGGL((k_convt<128, 128, 16, 2, 2, 3>), dim3((unsigned)blk), dim3(256), 0, s, a);
+  } else {                    // 256 x 64 tiles, 4 x 1 waves of 64 x 64
+    const int64_t blk = convt_classes(a, 256, 64);
+    if (blk < 0) return hipErrorInvalidValue;
+    if (blk > 0) hipLaunchKernelGGL((k_convt<256, 64, 16, 4, 1, 3>), dim3((unsigned)blk), dim3(256), 0, s, a);
   }
   return hipGetLastError();
 }

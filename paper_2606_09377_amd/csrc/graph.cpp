@@ -749,7 +749,6 @@ vcr_status run_pass(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &pp, int 
         a.C_out = nd.C;
         a.Bt = nd.Bt;
         a.ldb = 9 * (int64_t)nd.C;
-        a.K = 9 * nd.C;
         a.N_pad = nd.Ci_pad;
         a.C_in = nd.Ci;
         a.S_in = st.dst.S();
@@ -760,10 +759,8 @@ vcr_status run_pass(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &pp, int 
         const int64_t M = R * a.S_in * a.S_in;
         if (M >= (int64_t)1 << 31) return fail(c, VCR_ERR_UNSUPPORTED, "pass too large for one launch (%lld GEMM rows)",
                                                (long long)M);
-        a.M = (int32_t)M;
+        a.R = (int32_t)R;
         a.M_pad = (int32_t)rows_pad(M);
-        a.div_S2 = make_fastdiv((uint32_t)(a.S_in * a.S_in));
-        a.div_S = make_fastdiv((uint32_t)a.S_in);
         a.rows = bf.rows;
         a.dense = st.dst.dense ? 1 : 0;
         a.scale = st.dst.scale;
