@@ -24,24 +24,28 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_FP32_MFMA_TFLOPS = 157.3   # MI355X dense fp32 matrix peak
-GEMM_SOURCE = os.path.join(ROOT, "paper_2606_09377_amd", "csrc", "gemm.hip")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_traffic.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+KERNEL_SOURCES = {"k_gemm": "gemm.hip", "k_convt": "conv.hip"}
+KERNEL_DESC = {"k_gemm": "k_gemm (dense A.W step, fp32 v_mfma_f32_32x32x2f32)",
+               "k_convt": "k_convt (transposed-conv implicit GEMM, fp32 v_mfma_f32_32x32x2f32)"}
 
 
-def gemm_source_hash():
-    return hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()[:16]
+def source_hash(kernel):
+    path = os.path.join(ROOT, "paper_2606_09377_amd", "csrc", KERNEL_SOURCES[kernel])
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
 
 
-def traffic_for(workload):
-    """HBM bytes per GEMM launch from the committed PMC runs, if they were taken on the
+def traffic_for(kernel, workload):
+    """HBM bytes per launch of `kernel` from the committed PMC runs, if they were taken on the
     current kernel source; else None."""
     try:
         t = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
         return None
-    if t.get("kernel_source_sha") != gemm_source_hash():
+    k = t.get("kernels", {}).get(kernel)
+    if not k or k.get("source_sha") != source_hash(kernel):
         return None
-    w = t.get("workloads", {}).get(workload)
+    w = k.get("workloads", {}).get(workload)
     return None if w is None else w.get("bytes_per_launch")
 
 
@@ -223,10 +227,23 @@ def main():
 
     ms_step = dt / args.steps * 1e3
     value = units * args.steps / dt
-    launches = st["timed_gemm_launches"]
-    gemm_s = st["timed_gemm_ms"] / 1e3
-    achieved = st["timed_gemm_flops"] / gemm_s / 1e12 if gemm_s > 0 else None
-    traffic = traffic_for(args.workload)
+    timed = {"k_gemm": (st["timed_gemm_launches"], st["timed_gemm_ms"], st["timed_gemm_flops"]),
+             "k_convt": (st["timed_conv_launches"], st["timed_conv_ms"], st["timed_conv_flops"])}
+
+    def roofline(kernel):
+        launches, ms, fl = timed[kernel]
+        achieved = fl / (ms / 1e3) / 1e12 if ms > 0 else None
+        return {"bound": "mfma", "kernel": KERNEL_DESC[kernel],
+                "achieved": achieved, "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
+                "frac": achieved / PEAK_FP32_MFMA_TFLOPS if achieved else None,
+                "traffic": traffic_for(kernel, args.workload),
+                "launches_timed": launches,
+                "avg_launch_ms": ms / launches if launches else None,
+                "flops_per_launch": fl / launches if launches else None,
+                "share_of_step": ms / args.steps / ms_step if launches else None}
+
+    dominant = max(timed, key=lambda k: timed[k][1])
+    other = [k for k in timed if k != dominant and timed[k][0] > 0]
     rec = {
         "metric": "CROWN bound evals/sec (inputs or BaB domains) at 1 GPU; % fp32 MFMA peak",
         "value": value,
@@ -245,17 +262,13 @@ def main():
                    "layers": [int(wl.net.nodes[0].W.shape[1])] + [int(nd.W.shape[0]) for nd in wl.net.nodes
                                                                    if nd.op == "dense"],
                    "method": "full CROWN (IBP-intersected intermediate bounds)"},
-        "roofline": {"bound": "mfma", "kernel": "k_gemm (fp32 v_mfma_f32_32x32x2f32)",
-                     "achieved": achieved, "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_FP32_MFMA_TFLOPS if achieved else None,
-                     "traffic": traffic,
-                     "launches_timed": launches,
-                     "avg_launch_ms": st["timed_gemm_ms"] / launches if launches else None,
-                     "flops_per_launch": st["timed_gemm_flops"] / launches if launches else None},
+        "roofline": roofline(dominant),
         "call_mfma_frac": flops_call / (ms_step / 1e3) / (PEAK_FP32_MFMA_TFLOPS * 1e12),
         "graph_replay": bool(args.graph),
         "gemm_flops_per_step": flops_call,
     }
+    if other:
+        rec["roofline_other"] = roofline(other[0])
     rec.update(extra)
     if args.cpu_budget > 0 and args.workload.startswith("resnet3x32x32"):
         rec["cpu_baseline"] = cpu_baseline_sampled(wl, args.cpu_budget)

@@ -100,7 +100,8 @@ enum {
                                        (or domains) are processed in chunks that fit. */
   VCR_OPT_SYNC_CHECK = 6,           /* 1: synchronise after each call and report device errors
                                        and invalid split domains as the call's status */
-  VCR_OPT_TIME_GEMM = 7,            /* 1: bracket every backward-step GEMM launch with HIP events
+  VCR_OPT_TIME_GEMM = 7,            /* 1: bracket every backward-step GEMM launch (dense and
+                                       transposed-convolution) with HIP events
                                        on the context's stream; vcr_get_stats reports their summed
                                        duration.  Setting the option (either value) resets the sums. */
   VCR_OPT_GRAPH = 8                 /* 1: vcr_crown_bounds without splits records its kernel launches
@@ -121,11 +122,16 @@ typedef struct {
   int32_t n_relu;                   /* ReLU nodes of the loaded network */
   int32_t unstable[64];             /* unstable neurons per ReLU node, summed over inputs, last
                                        CROWN call (synchronises); first min(n_relu, 64) valid */
-  /* with VCR_OPT_TIME_GEMM: GEMM launches timed since the option was set, their summed
-   * device duration and their algorithmic flops */
+  /* with VCR_OPT_TIME_GEMM: dense GEMM launches (A W steps) timed since the option was set,
+   * their summed device duration and their algorithmic flops */
   uint64_t timed_gemm_launches;
   double timed_gemm_ms;
   uint64_t timed_gemm_flops;
+  /* the same for the transposed-convolution GEMM launches (algorithmic flops: 2 per
+   * multiply-add of the convolution's scatter form over the source window) */
+  uint64_t timed_conv_launches;
+  double timed_conv_ms;
+  uint64_t timed_conv_flops;
 } vcr_stats;
 
 /* ABI version compiled into the library (VCR_ABI_VERSION). */

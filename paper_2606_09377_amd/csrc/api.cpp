@@ -220,6 +220,22 @@ vcr_status check_chain(vcr_ctx *c, const vcr_node *nodes, int32_t n, const int32
 }  // namespace
 
 // =====================================================================================
+vcr_status timing_fold(vcr_ctx *c) {
+  if (!c->ev_used) return VCR_OK;
+  HIP_TRY(c, hipEventSynchronize(c->ev_pool[c->ev_used - 1]));
+  for (size_t q = 0; q + 1 < c->ev_used; q += 2) {
+    float ms = 0.f;
+    HIP_TRY(c, hipEventElapsedTime(&ms, c->ev_pool[q], c->ev_pool[q + 1]));
+    const auto &pk = c->pending[q / 2];
+    c->timed_ms[pk.second] += ms;
+    c->timed_flops[pk.second] += pk.first;
+    ++c->timed_launches[pk.second];
+  }
+  c->ev_used = 0;
+  c->pending.clear();
+  return VCR_OK;
+}
+
 extern "C" {
 
 int32_t vcr_abi_version(void) { return VCR_ABI_VERSION; }
@@ -301,9 +317,11 @@ vcr_status vcr_set_option(vcr_ctx *c, int32_t key, double v) {
       if (c->device >= 0 && c->ev_used) (void)hipStreamSynchronize(c->stream);
       c->time_gemm = v != 0.0;
       c->ev_used = 0;
-      c->pending_flops.clear();
-      c->timed_launches = c->timed_flops = 0;
-      c->timed_ms = 0.0;
+      c->pending.clear();
+      for (int k = 0; k < 2; ++k) {
+        c->timed_launches[k] = c->timed_flops[k] = 0;
+        c->timed_ms[k] = 0.0;
+      }
       break;
     default: return fail(c, VCR_ERR_ARG, "unknown option %d", key);
   }
@@ -527,35 +545,9 @@ vcr_status run_chain(vcr_ctx *c, CallBufs &bf, int top, int32_t M, int32_t rows_
       g.part = bf.cpart;
     }
     const uint64_t gf = 2ull * (uint64_t)M * (uint64_t)W.n_out * (uint64_t)W.n_in;
-    if (c->time_gemm) {
-      if (c->ev_used + 2 > c->ev_pool.size()) {
-        hipEvent_t e0, e1;
-        HIP_TRY(c, hipEventCreate(&e0));
-        HIP_TRY(c, hipEventCreate(&e1));
-        c->ev_pool.push_back(e0);
-        c->ev_pool.push_back(e1);
-      }
-      HIP_TRY(c, hipEventRecord(c->ev_pool[c->ev_used], c->stream));
-      HIP_TRY(c, launch_gemm(g, c->stream));
-      HIP_TRY(c, hipEventRecord(c->ev_pool[c->ev_used + 1], c->stream));
-      c->ev_used += 2;
-      c->pending_flops.push_back(gf);
-      if (c->ev_used >= 4096) {   // fold finished pairs in so the pool stays bounded
-        vcr_status st2 = VCR_OK;
-        HIP_TRY(c, hipEventSynchronize(c->ev_pool[c->ev_used - 1]));
-        for (size_t q = 0; q + 1 < c->ev_used; q += 2) {
-          float ms = 0.f;
-          HIP_TRY(c, hipEventElapsedTime(&ms, c->ev_pool[q], c->ev_pool[q + 1]));
-          c->timed_ms += ms;
-          c->timed_flops += c->pending_flops[q / 2];
-          ++c->timed_launches;
-        }
-        c->ev_used = 0;
-        c->pending_flops.clear();
-        (void)st2;
-      }
-    } else {
-      HIP_TRY(c, launch_gemm(g, c->stream));
+    {
+      const vcr_status st = timed_launch(c, c->stream, 0, gf, [&] { return launch_gemm(g, c->stream); });
+      if (st != VCR_OK) return st;
     }
     *flops += gf;
     if (j >= 2) {
@@ -893,21 +885,16 @@ vcr_status vcr_get_stats(vcr_ctx *c, vcr_stats *out) {
   out->n_relu = (int32_t)c->relu_n.size();
   if (c->device < 0) return VCR_OK;
   HIP_TRY(c, hipSetDevice(c->device));
-  if (c->ev_used) {
-    HIP_TRY(c, hipStreamSynchronize(c->stream));
-    for (size_t q = 0; q + 1 < c->ev_used; q += 2) {
-      float ms = 0.f;
-      HIP_TRY(c, hipEventElapsedTime(&ms, c->ev_pool[q], c->ev_pool[q + 1]));
-      c->timed_ms += ms;
-      c->timed_flops += c->pending_flops[q / 2];
-      ++c->timed_launches;
-    }
-    c->ev_used = 0;
-    c->pending_flops.clear();
+  {
+    const vcr_status st = timing_fold(c);
+    if (st != VCR_OK) return st;
   }
-  out->timed_gemm_launches = c->timed_launches;
-  out->timed_gemm_ms = c->timed_ms;
-  out->timed_gemm_flops = c->timed_flops;
+  out->timed_gemm_launches = c->timed_launches[0];
+  out->timed_gemm_ms = c->timed_ms[0];
+  out->timed_gemm_flops = c->timed_flops[0];
+  out->timed_conv_launches = c->timed_launches[1];
+  out->timed_conv_ms = c->timed_ms[1];
+  out->timed_conv_flops = c->timed_flops[1];
   if (c->lastL.empty()) return VCR_OK;
   int32_t *cnt = c->d_counters;
   const int R = std::min<int>((int)c->lastL.size(), 64);

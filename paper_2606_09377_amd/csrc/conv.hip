@@ -314,9 +314,9 @@ hipError_t launch_convt(const ConvTArgs &a0, hipStream_t s) {
 //   part[(r, u, w)] = sum_ci a c[unit][ci][gy][gx] - |a| r[unit][ci][gy][gx]   (inside the image)
 // One workgroup per coefficient row; the row's source window is staged through LDS
 // channel-major (odd row pitch, so neighbouring positions hit neighbouring banks) in channel
-// chunks; the weights are read with wave-uniform addresses.
+// chunks, together with the chunk's weights, which every lane reads at the same address.
 template <int CIN, int MAXP>
-__global__ __launch_bounds__(256) void k_stem(const StemArgs p) {
+__global__ __launch_bounds__(256, MAXP >= 4 ? 3 : 4) void k_stem(const StemArgs p) {
   // LDS: rpw rows x cc channels x pitch; cell S_out^2 of every channel row is a zero that
   // invalid taps read, so the inner loop has no branches
   extern __shared__ float lds[];
@@ -324,6 +324,8 @@ __global__ __launch_bounds__(256) void k_stem(const StemArgs p) {
   const int pitch = (S_out2 + 1) | 1;
   const int S_in2 = p.S_in * p.S_in;
   const int r0 = blockIdx.x * p.rpw;
+  constexpr int WP = (CIN * 9 + 3) & ~3;
+  float *wlds = lds + ((p.rpw * p.cc * pitch + 3) & ~3);   // after the rows
   const float *__restrict__ Wg = p.W;
   float acc[MAXP][CIN];
   int sidx[MAXP][9];
@@ -364,26 +366,41 @@ __global__ __launch_bounds__(256) void k_stem(const StemArgs p) {
   const int per_row = S_out2 * p.cc;
   for (int c0 = 0; c0 < p.C_out; c0 += p.cc) {
     __syncthreads();
-    for (int i = threadIdx.x; i < p.rpw * per_row; i += 256) {
-      const int rl = i / per_row, rem = i - rl * per_row;
-      const int pos = rem >> p.lg_cc, c = rem & (p.cc - 1);
-      if (r0 + rl < p.R)
-        lds[(rl * p.cc + c) * pitch + pos] =
-            p.A[(int64_t)(r0 + rl) * p.row_stride_out + (int64_t)pos * p.C_out + c0 + c];
+    // stage cc channels of each row: four independent loads in flight per thread
+    for (int rl = 0; rl < p.rpw && r0 + rl < p.R; ++rl) {
+      const float *src = p.A + (int64_t)(r0 + rl) * p.row_stride_out + c0;
+      float *dst = lds + rl * p.cc * pitch;
+      for (int e0 = threadIdx.x; e0 < per_row; e0 += 1024) {
+        float v[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int e = e0 + 256 * k;
+          v[k] = e < per_row ? src[(e >> p.lg_cc) * p.C_out + (e & (p.cc - 1))] : 0.f;
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int e = e0 + 256 * k;
+          if (e < per_row) dst[(e & (p.cc - 1)) * pitch + (e >> p.lg_cc)] = v[k];
+        }
+      }
+    }
+    // the chunk's weights, WP floats per channel (wave-uniform reads, broadcast from LDS)
+    for (int i = threadIdx.x; i < p.cc * CIN * 9; i += 256) {
+      const int c = i / (CIN * 9), q = i - c * (CIN * 9);
+      wlds[c * WP + q] = Wg[(int64_t)(c0 + c) * CIN * 9 + q];
     }
     __syncthreads();
     for (int c = 0; c < p.cc; ++c) {
-      const float *wc = Wg + (int64_t)(c0 + c) * CIN * 9;
+      float wv[WP];
+#pragma unroll
+      for (int q = 0; q < WP; q += 4) *reinterpret_cast<float4 *>(&wv[q]) = *reinterpret_cast<const float4 *>(&wlds[c * WP + q]);
 #pragma unroll
       for (int tap = 0; tap < 9; ++tap) {
-        float wv[CIN];
-#pragma unroll
-        for (int ci = 0; ci < CIN; ++ci) wv[ci] = wc[ci * 9 + tap];
 #pragma unroll
         for (int k = 0; k < MAXP; ++k) {
           const float a = lds[lbase[k] + c * pitch + sidx[k][tap]];
 #pragma unroll
-          for (int ci = 0; ci < CIN; ++ci) acc[k][ci] += a * wv[ci];
+          for (int ci = 0; ci < CIN; ++ci) acc[k][ci] += a * wv[ci * 9 + tap];
         }
       }
     }
@@ -428,12 +445,15 @@ hipError_t launch_stem_t(StemArgs a, hipStream_t s) {
   }
   if (!best_p) return hipErrorInvalidValue;
   a.rpw = best_r;
+  constexpr int WP = (CIN * 9 + 3) & ~3;
+  // LDS floats: the rows' channel chunk plus the chunk's weights, within 64 KB
+  auto lds_floats = [&](int cc) { return (((int64_t)a.rpw * cc * pitch + 3) & ~(int64_t)3) + (int64_t)cc * WP; };
   a.cc = a.C_out;
-  while (a.cc > 1 && ((int64_t)a.rpw * a.cc * pitch > 16384 || a.C_out % a.cc)) a.cc /= 2;
-  if ((int64_t)a.rpw * a.cc * pitch > 16384 || (a.cc & (a.cc - 1))) return hipErrorInvalidValue;
+  while (a.cc > 1 && (lds_floats(a.cc) > 16384 || a.C_out % a.cc)) a.cc /= 2;
+  if (lds_floats(a.cc) > 16384 || (a.cc & (a.cc - 1))) return hipErrorInvalidValue;
   a.lg_cc = 0;
   while ((1 << a.lg_cc) < a.cc) ++a.lg_cc;
-  const size_t lds = sizeof(float) * (size_t)a.rpw * a.cc * pitch;
+  const size_t lds = sizeof(float) * (size_t)lds_floats(a.cc);
   const unsigned grid = (unsigned)((a.R + a.rpw - 1) / a.rpw);
   if (best_p == 1)
     hipLaunchKernelGGL((k_stem<CIN, 1>), dim3(grid), dim3(256), lds, s, a);

@@ -8,6 +8,7 @@
 #include <cstdio>
 #include <memory>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "../../include/vcrown.h"
@@ -73,13 +74,13 @@ struct vcr_ctx {
   hipStream_t cap_stream = nullptr;
   hipGraphExec_t gexec = nullptr;
   std::vector<uint64_t> gkey;
-  // GEMM timing (VCR_OPT_TIME_GEMM)
+  // timing of the GEMM launches (VCR_OPT_TIME_GEMM); kind 0 = dense k_gemm, 1 = conv k_convt
   int32_t time_gemm = 0;
   std::vector<hipEvent_t> ev_pool;      // pairs: start, stop
   size_t ev_used = 0;                   // events recorded but not yet read
-  uint64_t timed_launches = 0, timed_flops = 0;
-  double timed_ms = 0.0;
-  std::vector<uint64_t> pending_flops;  // flops of each recorded pair
+  uint64_t timed_launches[2] = {0, 0}, timed_flops[2] = {0, 0};
+  double timed_ms[2] = {0.0, 0.0};
+  std::vector<std::pair<uint64_t, int>> pending;  // (flops, kind) of each recorded pair
 };
 
 inline vcr_status fail(vcr_ctx *c, vcr_status st, const char *fmt, ...) {
@@ -97,6 +98,33 @@ inline vcr_status fail(vcr_ctx *c, vcr_status st, const char *fmt, ...) {
     hipError_t e_ = (expr);                                                                   \
     if (e_ != hipSuccess) return fail((c), VCR_ERR_DEVICE, "%s: %s", #expr, hipGetErrorString(e_)); \
   } while (0)
+
+// Reads every recorded timing pair into the sums (waits for the last one).
+vcr_status timing_fold(vcr_ctx *c);
+
+// Launches through `launch` (a callable returning hipError_t); with VCR_OPT_TIME_GEMM on, the
+// launch is bracketed by HIP events on stream s and counted under `kind` with `flops`.
+template <class F>
+vcr_status timed_launch(vcr_ctx *c, hipStream_t s, int kind, uint64_t flops, F &&launch) {
+  if (!c->time_gemm) {
+    HIP_TRY(c, launch());
+    return VCR_OK;
+  }
+  if (c->ev_used + 2 > c->ev_pool.size()) {
+    hipEvent_t e0, e1;
+    HIP_TRY(c, hipEventCreate(&e0));
+    HIP_TRY(c, hipEventCreate(&e1));
+    c->ev_pool.push_back(e0);
+    c->ev_pool.push_back(e1);
+  }
+  HIP_TRY(c, hipEventRecord(c->ev_pool[c->ev_used], s));
+  HIP_TRY(c, launch());
+  HIP_TRY(c, hipEventRecord(c->ev_pool[c->ev_used + 1], s));
+  c->ev_used += 2;
+  c->pending.emplace_back(flops, kind);
+  if (c->ev_used >= 4096) return timing_fold(c);   // keeps the pool bounded
+  return VCR_OK;
+}
 
 inline size_t al(size_t x) { return (x + 255) / 256 * 256; }
 

@@ -775,9 +775,13 @@ vcr_status run_pass(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &pp, int 
         a.bias = st.bias_off >= 0 ? g->bias_arena + st.bias_off : nullptr;
         a.out = slot(st.dst);
         a.part = bf.part;
-        HIP_TRY(c, launch_convt(a, s));
+        const uint64_t cf = 2ull * (uint64_t)R * a.S_out * a.S_out * 9ull * (uint64_t)nd.C * (uint64_t)nd.Ci;
+        {
+          const vcr_status st2 = timed_launch(c, s, 1, cf, [&] { return launch_convt(a, s); });
+          if (st2 != VCR_OK) return st2;
+        }
         HIP_TRY(c, launch_rowsum_win(bf.beta, bf.part, a.N_pad / 64, a.M_pad, R, a.S_in * a.S_in, s));
-        *flops += 2ull * (uint64_t)R * a.S_out * a.S_out * 9ull * (uint64_t)nd.C * (uint64_t)nd.Ci;
+        *flops += cf;
         break;
       }
       case ST_STEM: {
@@ -835,9 +839,13 @@ vcr_status run_pass(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &pp, int 
         ga.relu_index = 0;
         ga.part = bf.part;
         if (st.dst.row_stride != nd.ld_in) return fail(c, VCR_ERR_UNSUPPORTED, "internal: dense output width mismatch");
-        HIP_TRY(c, launch_gemm(ga, s));
+        const uint64_t df = 2ull * (uint64_t)R * (uint64_t)nd.numel * (uint64_t)g->nodes[nd.in0].numel;
+        {
+          const vcr_status st2 = timed_launch(c, s, 0, df, [&] { return launch_gemm(ga, s); });
+          if (st2 != VCR_OK) return st2;
+        }
         HIP_TRY(c, launch_rowsum_win(bf.beta, bf.part, (int32_t)(nd.ld_in / PART_COLS), ga.M_pad, R, 1, s));
-        *flops += 2ull * (uint64_t)R * (uint64_t)nd.numel * (uint64_t)g->nodes[nd.in0].numel;
+        *flops += df;
         break;
       }
     }

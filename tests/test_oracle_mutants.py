@@ -26,7 +26,8 @@ MUTANTS = {
     "lambda_rule_flipped": ("np.where(uu > -lu, 1.0, 0.0)", "np.where(uu > -lu, 0.0, 1.0)"),
     "chord_slope_wrong": ("su = uu / (uu - lu)", "su = -lu / (uu - lu)"),
     "chord_intercept_sign": ("t[unstable] = -su * lu", "t[unstable] = su * lu"),
-    "add_drops_branch": ("_accumulate(acc, nd.in1, Ai)", "pass"),
+    "add_drops_branch": ('elif nd.op == "add":\n            _accumulate(acc, nd.in0, Ai)\n            _accumulate(acc, nd.in1, Ai)',
+                         'elif nd.op == "add":\n            _accumulate(acc, nd.in0, Ai)\n            pass'),
     "conv_transpose_misaligned": ("return out[:, :, pad:pad + h, pad:pad + w]", "return out[:, :, :h, :w]"),
     "conv_transpose_unflipped_stride": ("j:j + stride * (wo - 1) + 1:stride] += contrib",
                                         "j:j + (wo - 1) + 1:1] += contrib"),
@@ -43,7 +44,9 @@ MUTANTS = {
 
 def _mutant(old, new):
     src = open(SRC).read()
-    assert src.count(old) == 1, f"mutation anchor not unique / missing: {old!r}"
+    # the mistake is planted everywhere the anchor occurs (the receptive-field sampler repeats
+    # some of the full oracle's steps)
+    assert src.count(old) >= 1, f"mutation anchor missing: {old!r}"
     mod = types.ModuleType("oracle_mutant")
     sys.modules["oracle_mutant"] = mod          # dataclasses look their module up here
     exec(compile(src.replace(old, new), "oracle_mutant", "exec"), mod.__dict__)
