@@ -7,9 +7,11 @@ import types
 
 import pytest
 
-from tests import pins
+from tests import pins, pins_alpha
 
-SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "oracle", "crown64.py")
+ORACLE_DIR = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "oracle")
+SRC = os.path.join(ORACLE_DIR, "crown64.py")
+SRC_ALPHA = os.path.join(ORACLE_DIR, "alpha64.py")
 
 MUTANTS = {
     "drop_relax_intercept_lower": ("bias = bias + An @ t", "bias = bias"),
@@ -57,6 +59,39 @@ def _mutant(old, new):
 def test_mutant_is_caught(name):
     mod = _mutant(*MUTANTS[name])
     for pin in pins.ALL_PINS:
+        try:
+            pin(mod)
+        except Exception:
+            return
+    pytest.fail(f"mutant {name} passed every pin")
+
+
+ALPHA_MUTANTS = {
+    "alpha_upper_pass_uses_lower_rule": ("        if not upper:\n                bias = bias + An @ t",
+                                         "        if True:\n                bias = bias + An @ t"),
+    "alpha_grad_branch_swapped": ("on_lam, on_chord_t = a > 0.0, a < 0.0", "on_lam, on_chord_t = a < 0.0, a > 0.0"),
+    "alpha_grad_drops_intercept": ("s[None, :] * D + np.where(on_chord_t, t[None, :], 0.0)", "s[None, :] * D"),
+    "alpha_grad_wrong_vertex": ("else c[None, :] - sgn * r[None, :]", "else c[None, :] + sgn * r[None, :]"),
+    "alpha_no_projection": ("np.clip(a[i] + sign * lr * mhat / (np.sqrt(vhat) + adam_eps), 0.0, 1.0)",
+                            "a[i] + sign * lr * mhat / (np.sqrt(vhat) + adam_eps)"),
+    "alpha_upper_ascends": ('(("l", al, gl, 1.0), ("u", au, gu, -1.0))', '(("l", al, gl, 1.0), ("u", au, gu, 1.0))'),
+    "alpha_best_not_kept": ("best_l = np.where(better_l, lb, best_l)", "best_l = lb"),
+}
+
+
+def _alpha_mutant(old, new):
+    src = open(SRC_ALPHA).read()
+    assert src.count(old) >= 1, f"mutation anchor missing: {old!r}"
+    mod = types.ModuleType("alpha_mutant")
+    sys.modules["alpha_mutant"] = mod
+    exec(compile(src.replace(old, new), "alpha_mutant", "exec"), mod.__dict__)
+    return mod
+
+
+@pytest.mark.parametrize("name", sorted(ALPHA_MUTANTS))
+def test_alpha_mutant_is_caught(name):
+    mod = _alpha_mutant(*ALPHA_MUTANTS[name])
+    for pin in pins_alpha.ALPHA_PINS:
         try:
             pin(mod)
         except Exception:

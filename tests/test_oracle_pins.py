@@ -1,11 +1,17 @@
-"""The fp64 oracle against its pins (closed forms, the paper's worked example, LP and grid
-sandwiches, library convolutions, soundness).  CPU only."""
+"""The fp64 oracles against their pins (closed forms, the paper's worked example, LP and grid
+sandwiches, library convolutions, soundness, finite differences).  CPU only."""
 import pytest
 
 import oracle
-from tests import pins
+from oracle import alpha64
+from tests import pins, pins_alpha
 
 
 @pytest.mark.parametrize("pin", pins.ALL_PINS, ids=lambda p: p.__name__)
 def test_pin(pin):
     pin(oracle)
+
+
+@pytest.mark.parametrize("pin", pins_alpha.ALPHA_PINS, ids=lambda p: p.__name__)
+def test_alpha_pin(pin):
+    pin(alpha64)
