@@ -173,6 +173,39 @@ vcr_status vcr_crown_bounds(vcr_ctx *ctx, const float *x0, int32_t B, float eps,
                             const float *C, int32_t m, const vcr_splits *splits,
                             float *lb, float *ub);
 
+/* alpha-CROWN (paper, Sec. 2.1): the lower slope of every unstable ReLU neuron becomes a
+ * parameter alpha in [0, 1], one per (ReLU layer, specification bound, input, neuron)
+ * (the alpha tensors of Sec. 4.6), raised by gradient steps on the bound it enters.
+ *
+ * Slope arrays use the compact layout [B][2m][n_total]: row q < m holds the slopes of the
+ * lower bound of specification row q, row m + q those of its upper bound; the columns are
+ * the neurons of every ReLU node in node order (n_total = sum of their sizes).  Entries of
+ * neurons that are not unstable are ignored on input and report the fixed slope on output. */
+typedef struct {
+  int32_t iters;            /* optimisation steps after the first evaluation (>= 0) */
+  float lr;                 /* Adam step size (> 0) */
+  float beta1, beta2;       /* Adam moment decays, in [0, 1) */
+  float adam_eps;           /* Adam denominator guard (> 0) */
+  const float *alpha_init;  /* device [B][2m][n_total] in [0, 1], or NULL: CROWN's lambda */
+  float *alpha_out;         /* device [B][2m][n_total] or NULL: slopes of each best bound */
+  float *grad_out;          /* device [B][2m][n_total] or NULL: d bound / d alpha at the last
+                               evaluated slopes (d lb for lower rows, d ub for upper rows) */
+  float *lb_hist, *ub_hist; /* device [iters + 1][B][m] each, or NULL: every evaluation */
+} vcr_alpha_opts;
+
+/* alpha-CROWN bounds on C f(x): the intermediate bounds are full CROWN's (as
+ * vcr_crown_bounds, IBP-intersected when that option is on); the final pass is evaluated
+ * iters + 1 times, with projected Adam steps on the slopes in between (ascent on every
+ * lower bound, descent on every upper bound), and each bound is the best one evaluated.
+ * Networks of dense and relu nodes only (VCR_ERR_UNSUPPORTED otherwise); x0, C, lb, ub as
+ * in vcr_crown_bounds without splits.  All arrays are caller-owned device memory. */
+vcr_status vcr_alpha_crown_bounds(vcr_ctx *ctx, const float *x0, int32_t B, float eps,
+                                  const float *C, int32_t m, const vcr_alpha_opts *opts,
+                                  float *lb, float *ub);
+
+/* Number of ReLU neurons over all ReLU nodes of the loaded network (n_total above). */
+int64_t vcr_relu_neurons(const vcr_ctx *ctx);
+
 /* Pre-activation bounds of ReLU node `relu_id` (0-based among ReLU nodes) from the last
  * CROWN call, for every input: l, u device (B, numel).  Queued on the stream. */
 vcr_status vcr_get_layer_bounds(vcr_ctx *ctx, int32_t relu_id, float *l, float *u);

@@ -1,0 +1,165 @@
+// alpha-CROWN state kernels (paper, Sec. 2.1: the lower slopes of unstable ReLU neurons
+// become parameters in [0, 1], raised by gradient steps; Sec. 4.6: one slope per layer,
+// specification row, input and neuron).  Every specification bound is a coefficient row
+// (unit, q): q < m the lower bound of row q, q >= m the negated upper bound of row q - m, so
+// every row maximises its own lower bound.  The per-layer state arrays are [M_pad][ld] with
+// the GEMM's row and column padding.
+#include "kernels.h"
+
+namespace vcr {
+
+__global__ void k_alpha_init(AlphaLayer l, const float *alpha_init, int64_t n_total, int32_t rows, int32_t rows_pad,
+                             int32_t rows_per_unit) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)rows_pad * l.ld) return;
+  const int64_t row = idx / l.ld;
+  const int32_t n = (int32_t)(idx - row * l.ld);
+  float a = 0.f;
+  if (row < rows && n < l.n) {
+    // unstable neurons (t > 0) take the given slope, the others keep their fixed one
+    const int64_t u = row / rows_per_unit;
+    const float4 prm = l.P[u * l.ld + n];
+    a = (alpha_init && prm.z > 0.f) ? alpha_init[row * n_total + l.col0 + n] : prm.x;
+  }
+  l.alpha[idx] = a;
+  l.best[idx] = a;
+  l.mom[idx] = 0.f;
+  l.vel[idx] = 0.f;
+  l.grad[idx] = 0.f;
+}
+
+hipError_t launch_alpha_init(const AlphaLayer &l, const float *alpha_init, int64_t n_total, int32_t rows,
+                             int32_t rows_pad, int32_t rows_per_unit, hipStream_t s) {
+  const int64_t n = (int64_t)rows_pad * l.ld;
+  hipLaunchKernelGGL(k_alpha_init, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, l, alpha_init, n_total, rows,
+                     rows_pad, rows_per_unit);
+  return hipGetLastError();
+}
+
+// E0 = c - sign(a) r: the vertex where a . x is smallest (the centre where a = 0)
+__global__ void k_alpha_vertex(const float *pre0, int64_t ld0, const float *c0, const float *r0, int32_t rows_pad,
+                               int32_t rows_per_unit, int32_t units, float *E0) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)rows_pad * ld0) return;
+  const int64_t row = idx / ld0;
+  const int64_t i = idx - row * ld0;
+  int64_t u = row / rows_per_unit;
+  u = u < units ? u : units - 1;
+  const float a = pre0[idx];
+  const float c = c0[u * ld0 + i], r = r0[u * ld0 + i];
+  E0[idx] = a > 0.f ? c - r : (a < 0.f ? c + r : c);
+}
+
+hipError_t launch_alpha_vertex(const float *pre0, int64_t ld0, const float *c0, const float *r0, int32_t rows_pad,
+                               int32_t rows_per_unit, int32_t units, float *E0, hipStream_t s) {
+  const int64_t n = (int64_t)rows_pad * ld0;
+  hipLaunchKernelGGL(k_alpha_vertex, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, pre0, ld0, c0, r0, rows_pad,
+                     rows_per_unit, units, E0);
+  return hipGetLastError();
+}
+
+__global__ void k_alpha_best(const float *beta, const float *cpart, int32_t n_parts, int32_t M_pad, int32_t rows,
+                             int32_t m, int32_t first, float *best_val, int32_t *flag, float *hist_lb,
+                             float *hist_ub) {
+  const int64_t row = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (row >= rows) return;
+  float sp = 0.f;
+  for (int p = 0; p < n_parts; ++p) sp += cpart[(int64_t)p * M_pad + row];
+  const float v = beta[row] + sp;
+  const bool better = first || v > best_val[row];
+  if (better) best_val[row] = v;
+  flag[row] = better ? 1 : 0;
+  const int64_t u = row / (2 * m);
+  const int32_t q = (int32_t)(row - u * 2 * m);
+  if (hist_lb) {
+    if (q < m)
+      hist_lb[u * m + q] = v;
+    else
+      hist_ub[u * m + q - m] = -v;
+  }
+}
+
+hipError_t launch_alpha_best(const float *beta, const float *cpart, int32_t n_parts, int32_t M_pad, int32_t rows,
+                             int32_t m, int32_t first, float *best_val, int32_t *flag, float *hist_lb,
+                             float *hist_ub, hipStream_t s) {
+  hipLaunchKernelGGL(k_alpha_best, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, s, beta, cpart, n_parts, M_pad,
+                     rows, m, first, best_val, flag, hist_lb, hist_ub);
+  return hipGetLastError();
+}
+
+__global__ void k_alpha_keep(AlphaLayer l, const int32_t *flag, int32_t rows) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)rows * l.ld) return;
+  const int64_t row = idx / l.ld;
+  if (flag[row]) l.best[idx] = l.alpha[idx];
+}
+
+hipError_t launch_alpha_keep(const AlphaLayer &l, const int32_t *flag, int32_t rows, hipStream_t s) {
+  const int64_t n = (int64_t)rows * l.ld;
+  hipLaunchKernelGGL(k_alpha_keep, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, l, flag, rows);
+  return hipGetLastError();
+}
+
+// Adam (bias-corrected moments) then projection onto [0, 1], at unstable neurons only
+__global__ void k_alpha_adam(AlphaLayer l, int32_t rows, int32_t rows_per_unit, float lr, float beta1, float beta2,
+                             float eps, float c1, float c2) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)rows * l.ld) return;
+  const int64_t row = idx / l.ld;
+  const int64_t n = idx - row * l.ld;
+  if (n >= l.n) return;
+  const int64_t u = row / rows_per_unit;
+  if (!(l.P[u * l.ld + n].z > 0.f)) return;
+  const float g = l.grad[idx];
+  const float mo = beta1 * l.mom[idx] + (1.f - beta1) * g;
+  const float ve = beta2 * l.vel[idx] + (1.f - beta2) * g * g;
+  l.mom[idx] = mo;
+  l.vel[idx] = ve;
+  const float a = l.alpha[idx] + lr * (mo * c1) / (sqrtf(ve * c2) + eps);
+  l.alpha[idx] = fminf(fmaxf(a, 0.f), 1.f);
+}
+
+hipError_t launch_alpha_adam(const AlphaLayer &l, int32_t rows, int32_t rows_per_unit, float lr, float beta1,
+                             float beta2, float eps, float c1, float c2, hipStream_t s) {
+  const int64_t n = (int64_t)rows * l.ld;
+  hipLaunchKernelGGL(k_alpha_adam, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, l, rows, rows_per_unit, lr,
+                     beta1, beta2, eps, c1, c2);
+  return hipGetLastError();
+}
+
+__global__ void k_alpha_final(const float *best_val, int32_t units, int32_t m, float *lb, float *ub) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)units * m) return;
+  const int64_t u = idx / m;
+  const int64_t q = idx - u * m;
+  lb[idx] = best_val[u * 2 * m + q];
+  ub[idx] = -best_val[u * 2 * m + m + q];
+}
+
+hipError_t launch_alpha_final(const float *best_val, int32_t units, int32_t m, float *lb, float *ub, hipStream_t s) {
+  const int64_t n = (int64_t)units * m;
+  hipLaunchKernelGGL(k_alpha_final, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, best_val, units, m, lb, ub);
+  return hipGetLastError();
+}
+
+__global__ void k_alpha_out(AlphaLayer l, int32_t rows, int32_t m, int64_t n_total, float *alpha_out,
+                            float *grad_out) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)rows * l.n) return;
+  const int64_t row = idx / l.n;
+  const int64_t n = idx - row * l.n;
+  const int64_t q = row % (2 * m);
+  const int64_t src = row * l.ld + n, dst = row * n_total + l.col0 + n;
+  if (alpha_out) alpha_out[dst] = l.best[src];
+  if (grad_out) grad_out[dst] = q < m ? l.grad[src] : -l.grad[src];
+}
+
+hipError_t launch_alpha_out(const AlphaLayer &l, int32_t rows, int32_t m, int64_t n_total, float *alpha_out,
+                            float *grad_out, hipStream_t s) {
+  const int64_t n = (int64_t)rows * l.n;
+  hipLaunchKernelGGL(k_alpha_out, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, l, rows, m, n_total, alpha_out,
+                     grad_out);
+  return hipGetLastError();
+}
+
+}  // namespace vcr

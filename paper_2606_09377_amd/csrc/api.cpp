@@ -62,6 +62,7 @@ bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 // ---- workspace planning ------------------------------------------------------------
 struct Plan {
   int32_t B = 0, m = 0, D = 0;
+  int32_t alpha = 0;        // alpha-CROWN state for the spec pass
   int32_t chunk_in = 0;     // inputs per intermediate-pass chunk
   int32_t chunk_units = 0;  // inputs (or domains) per spec-pass chunk
   size_t bytes = 0;
@@ -77,10 +78,11 @@ int64_t max_inter_rows_per_input(const vcr_ctx *c) {
 
 size_t carve_bytes(const vcr_ctx *c, const Plan &p, int32_t S);
 
-vcr_status make_plan(vcr_ctx *c, int32_t B, int32_t m, int32_t D, int32_t S, Plan *p) {
+vcr_status make_plan(vcr_ctx *c, int32_t B, int32_t m, int32_t D, int32_t S, Plan *p, int32_t alpha = 0) {
   p->B = B;
   p->m = m;
   p->D = D;
+  p->alpha = alpha;
   const int64_t rpi = max_inter_rows_per_input(c);
   const int32_t spec_units = D > 0 ? D : B;
   const int32_t root_B = D > 0 ? 1 : B;
@@ -409,13 +411,14 @@ vcr_status vcr_load_net(vcr_ctx *c, const vcr_node *nodes, int32_t n, const int3
     const size_t wbytes = sizeof(float) * (size_t)L.n_out * L.n_in;
     HIP_TRY(c, hipMalloc(&staging, wbytes));
     HIP_TRY(c, hipMemcpy(staging, nodes[i].W, wbytes, hipMemcpyHostToDevice));
-    HIP_TRY(c, hipMalloc(&L.Wp, sizeof(float) * (size_t)L.n_out * L.ld_in));
+    HIP_TRY(c, hipMalloc(&L.Wp, sizeof(float) * (size_t)L.ld_out * L.ld_in));
     HIP_TRY(c, hipMalloc(&L.Bt, sizeof(float) * (size_t)L.ld_in * L.ld_out));
     HIP_TRY(c, hipMalloc(&L.b, sizeof(float) * (size_t)L.ld_out));
     c->layers.push_back(L);
-    // Wp: row-major copy with zero-padded rows (a transpose of the transpose)
+    // Wp: row-major copy, zero-padded to [ld_out][ld_in] (a transpose of the transpose); the
+    // alpha-CROWN gradient pass uses it as a GEMM operand
     HIP_TRY(c, launch_transpose_pad(staging, L.n_out, L.n_in, L.Bt, L.ld_out, L.ld_in, c->stream));
-    HIP_TRY(c, launch_transpose_pad(L.Bt, (int32_t)L.ld_in, (int32_t)L.ld_out, L.Wp, L.ld_in, L.n_out, c->stream));
+    HIP_TRY(c, launch_transpose_pad(L.Bt, (int32_t)L.ld_in, (int32_t)L.ld_out, L.Wp, L.ld_in, L.ld_out, c->stream));
     HIP_TRY(c, launch_fill(L.b, L.ld_out, 0.f, c->stream));
     HIP_TRY(c, hipStreamSynchronize(c->stream));
     HIP_TRY(c, hipMemcpy(L.b, nodes[i].b, sizeof(float) * L.n_out, hipMemcpyHostToDevice));
@@ -443,6 +446,10 @@ struct CallBufs {
   float4 *ent_p;
   const float **Lptr, **Uptr;
   int32_t *relu_n;
+  // alpha-CROWN (one entry per ReLU), the input-layer coefficients, the best row bounds
+  std::vector<AlphaLayer> al;
+  float *pre0, *best_val;
+  int32_t *flag;
 };
 
 vcr_status check_common(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m,
@@ -491,7 +498,30 @@ void carve(const vcr_ctx *c, Workspace &w, const Plan &p, int32_t S, CallBufs *b
   const int64_t rows = std::max<int64_t>({rpi * p.chunk_in, 2 * (int64_t)p.m * p.chunk_units, 1});
   int64_t ldmax = 0;
   for (int k = 0; k < L - 1; ++k) ldmax = std::max(ldmax, c->layers[k].ld_out);
+  if (p.alpha) ldmax = std::max(ldmax, ld0);   // the gradient pass starts at the input
   const int64_t mp = rows_pad(rows);
+  bf->al.clear();
+  if (p.alpha) {
+    const int64_t ra = rows_pad(2 * (int64_t)p.m * p.chunk_units);
+    int32_t col0 = 0;
+    for (int k = 0; k < L - 1; ++k) {
+      AlphaLayer a{};
+      a.ld = c->layers[k].ld_out;
+      a.n = c->layers[k].n_out;
+      a.col0 = col0;
+      col0 += a.n;
+      a.alpha = take<float>(w, (size_t)ra * a.ld);
+      a.mom = take<float>(w, (size_t)ra * a.ld);
+      a.vel = take<float>(w, (size_t)ra * a.ld);
+      a.best = take<float>(w, (size_t)ra * a.ld);
+      a.grad = take<float>(w, (size_t)ra * a.ld);
+      a.pre = take<float>(w, (size_t)ra * a.ld);
+      bf->al.push_back(a);
+    }
+    bf->pre0 = take<float>(w, (size_t)ra * ld0);
+    bf->best_val = take<float>(w, (size_t)ra);
+    bf->flag = take<int32_t>(w, (size_t)ra);
+  }
   bf->A[0] = take<float>(w, (size_t)mp * std::max<int64_t>(ldmax, 1));
   bf->A[1] = take<float>(w, (size_t)mp * std::max<int64_t>(ldmax, 1));
   bf->beta = take<float>(w, (size_t)mp);
@@ -510,7 +540,8 @@ size_t carve_bytes(const vcr_ctx *c, const Plan &p, int32_t S) {
 // that start in A[0] (already relaxed for ReLU top-1... i.e. coefficients on z_top).
 // Leaves beta with the constants and cpart with the concretization partials.
 vcr_status run_chain(vcr_ctx *c, CallBufs &bf, int top, int32_t M, int32_t rows_per_unit, int32_t units,
-                     int32_t unit0, int32_t param_per_unit, const SplitTable &st, uint64_t *flops) {
+                     int32_t unit0, int32_t param_per_unit, const SplitTable &st, uint64_t *flops,
+                     bool with_alpha = false) {
   const int32_t M_pad = (int32_t)rows_pad(M);
   int cur = 0;
   for (int j = top; j >= 1; --j) {
@@ -537,12 +568,22 @@ vcr_status run_chain(vcr_ctx *c, CallBufs &bf, int top, int32_t M, int32_t rows_
       g.ldp = W.ld_in;
       g.relu_index = r;
       g.part = bf.part;
+      if (with_alpha) {
+        g.alpha = bf.al[r].alpha;
+        g.ld_alpha = bf.al[r].ld;
+        g.pre = bf.al[r].pre;
+        g.ld_pre = bf.al[r].ld;
+      }
     } else {
       g.mode = EPI_CONCRETIZE;
       g.c0 = bf.c0 + pu0 * ld_of(c->n0);
       g.r0 = bf.r0 + pu0 * ld_of(c->n0);
       g.ldc = ld_of(c->n0);
       g.part = bf.cpart;
+      if (with_alpha) {
+        g.pre = bf.pre0;
+        g.ld_pre = ld_of(c->n0);
+      }
     }
     const uint64_t gf = 2ull * (uint64_t)M * (uint64_t)W.n_out * (uint64_t)W.n_in;
     {
@@ -558,14 +599,121 @@ vcr_status run_chain(vcr_ctx *c, CallBufs &bf, int top, int32_t M, int32_t rows_
   return VCR_OK;
 }
 
+struct AlphaCall {
+  vcr_alpha_opts o;
+  int64_t n_total;
+};
+
+// alpha-CROWN final pass over every input chunk (after the intermediate bounds are fixed):
+// evaluate the bounds with the current slopes (backward chain with per-row slopes, keeping
+// the coefficients before each relaxation), keep each row's best, then the gradient pass
+// (the relaxed network forward from each row's box vertex) and one Adam step.
+vcr_status alpha_spec(vcr_ctx *c, CallBufs &bf, const Plan &p, const AlphaCall &ac, int32_t B, int32_t m,
+                      float *lb, float *ub, uint64_t *flops, int32_t *chunks) {
+  const int L = (int)c->layers.size();
+  const int R = L - 1;
+  const DenseLayer &WL = c->layers[L - 1];
+  const int64_t ld0 = ld_of(c->n0);
+  hipStream_t s = c->stream;
+  const vcr_alpha_opts &o = ac.o;
+  for (int32_t u0 = 0; u0 < B; u0 += p.chunk_units) {
+    const int32_t uc = std::min(p.chunk_units, B - u0);
+    const int32_t rpu = 2 * m;
+    const int32_t M = rpu * uc;
+    const int32_t M_pad = (int32_t)rows_pad(M);
+    std::vector<AlphaLayer> al = bf.al;
+    for (int r = 0; r < R; ++r) {
+      al[r].P = bf.P[r] + (int64_t)u0 * al[r].ld;
+      HIP_TRY(c, launch_alpha_init(al[r], o.alpha_init ? o.alpha_init + (int64_t)u0 * rpu * ac.n_total : nullptr,
+                                   ac.n_total, M, M_pad, rpu, s));
+    }
+    for (int32_t t = 0; t <= o.iters; ++t) {
+      // evaluate
+      InitArgs ia{};
+      ia.src = bf.CW + (int64_t)u0 * m * WL.ld_in;
+      ia.ld_src = WL.ld_in;
+      ia.n_src = m;
+      ia.per_unit_src = 1;
+      ia.src_bias = bf.Cb + (int64_t)u0 * m;
+      ia.n_cols = WL.n_in;
+      ia.ldo = WL.ld_in;
+      ia.M = M;
+      ia.units = uc;
+      ia.P = al[R - 1].P;
+      ia.ldp = WL.ld_in;
+      ia.param_per_unit = 1;
+      ia.relu_index = R - 1;
+      ia.out = bf.A[0];
+      ia.beta = bf.beta;
+      ia.alpha = al[R - 1].alpha;
+      ia.ld_alpha = al[R - 1].ld;
+      ia.pre = al[R - 1].pre;
+      HIP_TRY(c, launch_init_rows(ia, s));
+      vcr_status st = run_chain(c, bf, L - 1, M, rpu, uc, u0, 1, SplitTable{}, flops, true);
+      if (st != VCR_OK) return st;
+      HIP_TRY(c, launch_alpha_best(bf.beta, bf.cpart, (int32_t)(ld0 / PART_COLS), M_pad, M, m, t == 0, bf.best_val,
+                                   bf.flag, o.lb_hist ? o.lb_hist + ((int64_t)t * B + u0) * m : nullptr,
+                                   o.ub_hist ? o.ub_hist + ((int64_t)t * B + u0) * m : nullptr, s));
+      for (int r = 0; r < R; ++r) HIP_TRY(c, launch_alpha_keep(al[r], bf.flag, M, s));
+      const bool step = t < o.iters;
+      if (!step && !o.grad_out) break;
+      // gradient: E_0 = the row's box vertex, then E_k = line_k(W_k E_{k-1} + b_k)
+      HIP_TRY(c, launch_alpha_vertex(bf.pre0, ld0, bf.c0 + (int64_t)u0 * ld0, bf.r0 + (int64_t)u0 * ld0, M_pad, rpu,
+                                     uc, bf.A[0], s));
+      for (int k = 1; k <= R; ++k) {
+        const DenseLayer &W = c->layers[k - 1];
+        GemmArgs g{};
+        g.A = bf.A[(k - 1) & 1];
+        g.lda = W.ld_in;
+        g.Bt = W.Wp;
+        g.ldb = W.ld_in;
+        g.M = M;
+        g.M_pad = M_pad;
+        g.K = (int32_t)W.ld_in;
+        g.N_pad = (int32_t)W.ld_out;
+        g.mode = EPI_FORWARD;
+        g.out = bf.A[k & 1];
+        g.ldo = W.ld_out;
+        g.P = al[k - 1].P;
+        g.ldp = W.ld_out;
+        g.rows_per_unit = rpu;
+        g.n_units = uc;
+        g.alpha = al[k - 1].alpha;
+        g.ld_alpha = al[k - 1].ld;
+        g.pre = al[k - 1].pre;
+        g.ld_pre = al[k - 1].ld;
+        g.grad = al[k - 1].grad;
+        const uint64_t gf = 2ull * (uint64_t)M * (uint64_t)W.n_out * (uint64_t)W.n_in;
+        st = timed_launch(c, s, 0, gf, [&] { return launch_gemm(g, s); });
+        if (st != VCR_OK) return st;
+        *flops += gf;
+      }
+      if (!step) break;
+      const double c1 = 1.0 / (1.0 - std::pow((double)o.beta1, (double)(t + 1)));
+      const double c2 = 1.0 / (1.0 - std::pow((double)o.beta2, (double)(t + 1)));
+      for (int r = 0; r < R; ++r)
+        HIP_TRY(c, launch_alpha_adam(al[r], M, rpu, o.lr, o.beta1, o.beta2, o.adam_eps, (float)c1, (float)c2, s));
+    }
+    HIP_TRY(c, launch_alpha_final(bf.best_val, uc, m, lb + (int64_t)u0 * m, ub + (int64_t)u0 * m, s));
+    if (o.alpha_out || o.grad_out)
+      for (int r = 0; r < R; ++r)
+        HIP_TRY(c, launch_alpha_out(al[r], M, m, ac.n_total,
+                                    o.alpha_out ? o.alpha_out + (int64_t)u0 * rpu * ac.n_total : nullptr,
+                                    o.grad_out ? o.grad_out + (int64_t)u0 * rpu * ac.n_total : nullptr, s));
+    ++*chunks;
+  }
+  return VCR_OK;
+}
+
 vcr_status crown_impl(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m,
-                      const vcr_splits *splits, float *lb, float *ub) {
+                      const vcr_splits *splits, float *lb, float *ub,
+                      const AlphaCall *ac = nullptr) {
   const int L = (int)c->layers.size();
   const int R = (int)c->relu_n.size();
   const int32_t D = splits ? splits->n_domains : 0;
   const int32_t S = splits ? splits->per_domain : 0;
   Plan p;
-  vcr_status st = make_plan(c, B, m, D, S, &p);
+  vcr_status st = make_plan(c, B, m, D, S, &p, ac ? 1 : 0);
   if (st != VCR_OK) return st;
   if (c->device < 0) {
     // report the plan the call would have run
@@ -669,7 +817,10 @@ vcr_status crown_impl(vcr_ctx *c, const float *x0, int32_t B, float eps, const f
     HIP_TRY(c, hipStreamSynchronize(s));
   }
   const int32_t units = D > 0 ? D : B;
-  if (L == 1) {
+  if (ac) {
+    st = alpha_spec(c, bf, p, *ac, B, m, lb, ub, &flops, &chunks);
+    if (st != VCR_OK) return st;
+  } else if (L == 1) {
     HIP_TRY(c, launch_spec_direct(bf.CW, WL.ld_in, bf.Cb, B, m, WL.n_in, bf.c0, bf.r0, ld0, 0, lb, ub, s));
   } else {
     for (int32_t u0 = 0; u0 < units; u0 += p.chunk_units) {
@@ -842,6 +993,35 @@ vcr_status vcr_ibp_bounds(vcr_ctx *c, const float *x0, int32_t B, float eps, con
   HIP_TRY(c, launch_spec_direct(CW, WL.ld_in, Cb, B, m, WL.n_in, L >= 2 ? cc[L - 2] : c0, L >= 2 ? rr[L - 2] : r0,
                                 WL.ld_in, L >= 2, lb, ub, s));
   return after_call(c, VCR_OK, t0);
+}
+
+vcr_status vcr_alpha_crown_bounds(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m,
+                                  const vcr_alpha_opts *opts, float *lb, float *ub) {
+  if (!c) return VCR_ERR_ARG;
+  const auto t0 = std::chrono::steady_clock::now();
+  vcr_status st = check_common(c, x0, B, eps, C, m, lb, ub);
+  if (st != VCR_OK) return st;
+  if (!opts) return fail(c, VCR_ERR_ARG, "null alpha options");
+  if (c->graph) return fail(c, VCR_ERR_UNSUPPORTED, "alpha-CROWN is built for networks of dense and relu nodes");
+  if (c->relu_n.empty()) return fail(c, VCR_ERR_ARG, "alpha-CROWN needs at least one ReLU");
+  const vcr_alpha_opts &o = *opts;
+  if (o.iters < 0 || o.iters > 1000000) return fail(c, VCR_ERR_ARG, "iters must be in [0, 1e6]");
+  if (!(o.lr > 0.f) || !std::isfinite(o.lr)) return fail(c, VCR_ERR_ARG, "lr must be finite and > 0");
+  if (!(o.beta1 >= 0.f && o.beta1 < 1.f) || !(o.beta2 >= 0.f && o.beta2 < 1.f))
+    return fail(c, VCR_ERR_ARG, "beta1 and beta2 must be in [0, 1)");
+  if (!(o.adam_eps > 0.f) || !std::isfinite(o.adam_eps)) return fail(c, VCR_ERR_ARG, "adam_eps must be finite and > 0");
+  if ((o.lb_hist == nullptr) != (o.ub_hist == nullptr)) return fail(c, VCR_ERR_ARG, "lb_hist and ub_hist go together");
+  AlphaCall ac{o, 0};
+  for (int32_t n : c->relu_n) ac.n_total += n;
+  if ((int64_t)B * 2 * m * ac.n_total > ((int64_t)1 << 40)) return fail(c, VCR_ERR_SHAPE, "alpha tensors too large");
+  return after_call(c, crown_impl(c, x0, B, eps, C, m, nullptr, lb, ub, &ac), t0);
+}
+
+int64_t vcr_relu_neurons(const vcr_ctx *c) {
+  if (!c) return 0;
+  int64_t n = 0;
+  for (int32_t k : c->relu_n) n += k;
+  return n;
 }
 
 vcr_status vcr_get_layer_bounds(vcr_ctx *c, int32_t relu_id, float *l, float *u) {

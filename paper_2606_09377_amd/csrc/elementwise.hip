@@ -205,20 +205,26 @@ hipError_t launch_ibp_dense(const float *Wp, int64_t ldw, const float *b, int32_
 // over the box is the IBP interval [c - r, c + r].
 __global__ void k_layer_from_ibp(const float *c, const float *r, int64_t ld, int32_t n, int32_t B,
                                  const float *bias, float *L, float *U, float4 *P, int64_t ldp) {
+  // one thread per (input, column) of P, padding columns included (they get zeros)
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (int64_t)B * n) return;
-  const int64_t b = idx / n, i = idx - b * n;
+  if (idx >= (int64_t)B * ldp) return;
+  const int64_t b = idx / ldp, i = idx - b * ldp;
+  if (i >= n) {
+    P[idx] = make_float4(0.f, 0.f, 0.f, 0.f);
+    return;
+  }
   const float cc = c[b * ld + i], rr = r[b * ld + i];
   const float l = cc - rr, u = cc + rr;
-  L[idx] = l;
-  U[idx] = u;
-  P[b * ldp + i] = relax_params(l, u, bias[i]);
+  L[b * n + i] = l;
+  U[b * n + i] = u;
+  P[idx] = relax_params(l, u, bias[i]);
 }
 
 hipError_t launch_layer_from_ibp(const float *c, const float *r, int64_t ld, int32_t n, int32_t B,
                                  const float *bias, float *L, float *U, float4 *P, int64_t ldp,
                                  hipStream_t s) {
-  const int64_t tot = (int64_t)B * n;
+  if (ldp < n) return hipErrorInvalidValue;
+  const int64_t tot = (int64_t)B * ldp;
   hipLaunchKernelGGL(k_layer_from_ibp, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, c, r, ld, n, B,
                      bias, L, U, P, ldp);
   return hipGetLastError();
@@ -250,8 +256,10 @@ __global__ __launch_bounds__(256) void k_init_rows(const InitArgs a, int32_t M_p
   if (row >= M_pad) return;
   float *orow = a.out + row * a.ldo;
   if (row >= a.M) {
-    for (int64_t c = (int64_t)lane * 4; c < a.ldo; c += 256)
+    for (int64_t c = (int64_t)lane * 4; c < a.ldo; c += 256) {
       *reinterpret_cast<float4 *>(orow + c) = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (a.pre) *reinterpret_cast<float4 *>(a.pre + row * a.ldo + c) = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
     if (lane == 0) a.beta[row] = 0.f;
     return;
   }
@@ -275,11 +283,15 @@ __global__ __launch_bounds__(256) void k_init_rows(const InitArgs a, int32_t M_p
       float4 prm = P[c + e];
       if (has_splits) prm = init_override(a.splits, u, a.relu_index, (int)(c + e), prm);
       const float x = sgn * wv[e];
-      const float ap = x > 0.f ? x * prm.x : x * prm.y;
+      float lam = prm.x;
+      if (a.alpha && prm.z > 0.f) lam = a.alpha[row * a.ld_alpha + c + e];
+      const float ap = x > 0.f ? x * lam : x * prm.y;
       acc += fminf(x, 0.f) * prm.z + ap * prm.w;
       ov[e] = ap;
     }
     *reinterpret_cast<float4 *>(orow + c) = make_float4(ov[0], ov[1], ov[2], ov[3]);
+    if (a.pre)
+      *reinterpret_cast<float4 *>(a.pre + row * a.ldo + c) = make_float4(sgn * wv[0], sgn * wv[1], sgn * wv[2], sgn * wv[3]);
   }
   acc = wave_sum(acc);
   if (lane == 0) a.beta[row] = sgn * a.src_bias[srow] + acc;
@@ -316,9 +328,14 @@ __global__ void k_finalize_layer(const float *beta, const float *cpart, int32_t 
                                  int32_t B, int32_t n, const float *ibp_c, const float *ibp_r, int64_t ld_ibp,
                                  int32_t intersect, const float *bias_next, float *L, float *U, float4 *P,
                                  int64_t ldp) {
+  // one thread per (input, column) of P, padding columns included (they get zeros)
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (int64_t)B * n) return;
-  const int64_t b = idx / n, i = idx - b * n;
+  if (idx >= (int64_t)B * ldp) return;
+  const int64_t b = idx / ldp, i = idx - b * ldp;
+  if (i >= n) {
+    P[idx] = make_float4(0.f, 0.f, 0.f, 0.f);
+    return;
+  }
   const int64_t ml = b * 2 * n + i, mu = ml + n;
   float sl = 0.f, su = 0.f;
   for (int p = 0; p < n_parts; ++p) {
@@ -332,16 +349,17 @@ __global__ void k_finalize_layer(const float *beta, const float *cpart, int32_t 
     l = fmaxf(l, c - r);
     u = fminf(u, c + r);
   }
-  L[idx] = l;
-  U[idx] = u;
-  P[b * ldp + i] = relax_params(l, u, bias_next[i]);
+  L[b * n + i] = l;
+  U[b * n + i] = u;
+  P[idx] = relax_params(l, u, bias_next[i]);
 }
 
 hipError_t launch_finalize_layer(const float *beta, const float *cpart, int32_t n_parts, int32_t M_pad,
                                  int32_t B, int32_t n, const float *ibp_c, const float *ibp_r,
                                  int64_t ld_ibp, int32_t intersect, const float *bias_next,
                                  float *L, float *U, float4 *P, int64_t ldp, hipStream_t s) {
-  const int64_t tot = (int64_t)B * n;
+  if (ldp < n) return hipErrorInvalidValue;
+  const int64_t tot = (int64_t)B * ldp;
   hipLaunchKernelGGL(k_finalize_layer, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, beta, cpart,
                      n_parts, M_pad, B, n, ibp_c, ibp_r, ld_ibp, intersect, bias_next, L, U, P, ldp);
   return hipGetLastError();

@@ -13,6 +13,12 @@
 //                    constant terms this neuron adds to the bound)
 //   EPI_CONCRETIZE : part[row] += a c[n] - |a| r[n]  (j = 1: minimum of a . x over the box
 //                    with centre c and radius r); A_0 itself is never written
+//   EPI_FORWARD    : out[row, n] = the relaxation line of ReLU k at D = a + b_k[n] chosen
+//                    by the sign of the backward coefficient, and its alpha gradient
+//                    (alpha-CROWN's gradient pass: A' = E_{k-1}, Bt = W_k)
+//
+// alpha-CROWN (Sec. 2.1) replaces lam by a per-row slope at unstable neurons and records the
+// coefficients before relaxation; see kernels.h.
 //
 // Upper bounds run through the same code on negated rows (max f = -min(-f)).
 //
@@ -187,9 +193,38 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm(const GemmArgs p) {
           }
           if (has_splits) prm = split_override(p.splits, row, p.relu_index, n, prm);
           const float a = acc[bi][bj][v];
-          const float ap = a > 0.f ? a * prm.x : a * prm.y;
+          float lam = prm.x;
+          if (p.alpha && prm.z > 0.f) lam = p.alpha[(int64_t)row * p.ld_alpha + n];
+          const float ap = a > 0.f ? a * lam : a * prm.y;
           p.out[(int64_t)row * p.ldo + n] = ap;
+          if (p.pre) p.pre[(int64_t)row * p.ld_pre + n] = a;
           rp[bi][v] += fminf(a, 0.f) * prm.z + ap * prm.w;
+        }
+      }
+    } else if (p.mode == EPI_FORWARD) {
+      // the relaxed network evaluated forward: D = W_k E + b_k, then the line of ReLU k that
+      // the backward pass chose for this row (by the sign of its coefficient)
+      float4 prm_tile = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (uniform_unit) prm_tile = p.P[(int64_t)unit_tile * p.ldp + n];
+#pragma unroll
+      for (int bi = 0; bi < 2; ++bi) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int row = m0 + wm * 64 + bi * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
+          float4 prm = prm_tile;
+          if (!uniform_unit) {
+            int u = row / p.rows_per_unit;
+            u = u < p.n_units ? u : p.n_units - 1;
+            prm = p.P[(int64_t)u * p.ldp + n];
+          }
+          const bool unst = prm.z > 0.f;
+          const int64_t ia = (int64_t)row * p.ld_alpha + n;
+          const float lam = unst ? p.alpha[ia] : prm.x;
+          const float an = p.pre[(int64_t)row * p.ld_pre + n];
+          const float D = acc[bi][bj][v] + prm.w;
+          const float E = an > 0.f ? lam * D : prm.y * D + (an < 0.f ? prm.z : 0.f);
+          p.out[(int64_t)row * p.ldo + n] = E;
+          p.grad[ia] = (unst && an > 0.f) ? an * D : 0.f;
         }
       }
     } else {
@@ -211,12 +246,14 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm(const GemmArgs p) {
             r = p.r0[(int64_t)u * p.ldc + n];
           }
           const float a = acc[bi][bj][v];
+          if (p.pre) p.pre[(int64_t)row * p.ld_pre + n] = a;
           rp[bi][v] += a * c - fabsf(a) * r;
         }
       }
     }
   }
 
+  if (p.mode == EPI_FORWARD) return;
   // fixed butterfly over the 32 lanes that share rows
 #pragma unroll
   for (int bi = 0; bi < 2; ++bi) {

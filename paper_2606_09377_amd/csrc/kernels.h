@@ -26,7 +26,7 @@ struct SplitTable {
   int32_t rows_per_domain = 0;
 };
 
-enum EpiMode : int32_t { EPI_RELAX = 0, EPI_CONCRETIZE = 1 };
+enum EpiMode : int32_t { EPI_RELAX = 0, EPI_CONCRETIZE = 1, EPI_FORWARD = 2 };
 
 struct GemmArgs {
   const float *A;      // M_pad x lda, coefficient rows (already relaxed), zero padded
@@ -49,7 +49,21 @@ struct GemmArgs {
   int64_t ldc;
   int32_t rows_per_unit;   // rows of one input (intermediate: 2 n_k; final: 2 m)
   int32_t n_units;         // number of inputs that own rows (clamp for padding rows)
-  float *part;             // [N_pad / PART_COLS][M_pad] per-row partial sums
+  float *part;             // [N_pad / PART_COLS][M_pad] per-row partial sums (null: EPI_FORWARD)
+  // alpha-CROWN (all optional):
+  //   alpha [M_pad][ld_alpha]: per-row lower slope of the ReLU relaxed in the epilogue, used
+  //   at its unstable neurons (t > 0) instead of lam;
+  //   pre [M_pad][ld_pre]: receives the coefficient a before relaxation (EPI_RELAX,
+  //   EPI_CONCRETIZE); in EPI_FORWARD it is read: the sign of the coefficient on the ReLU's
+  //   output that selected its line;
+  //   EPI_FORWARD: D = (A Bt^T)[row, n] + b (P.w), out = the selected line at D
+  //   (a > 0: lam D; else s D, plus t when a < 0), grad [M_pad][ld_alpha] = a D at
+  //   unstable neurons with a > 0, else 0.
+  const float *alpha;
+  int64_t ld_alpha;
+  float *pre;
+  int64_t ld_pre;
+  float *grad;
 };
 
 hipError_t launch_gemm(const GemmArgs &a, hipStream_t s);
@@ -83,6 +97,9 @@ struct InitArgs {
   SplitTable splits;
   float *out;            // M_pad x ldo
   float *beta;           // M_pad
+  const float *alpha;    // optional per-row lower slopes [M_pad][ld_alpha] (unstable neurons)
+  int64_t ld_alpha;
+  float *pre;            // optional: receives the rows before relaxation [M_pad][ldo]
 };
 hipError_t launch_init_rows(const InitArgs &a, hipStream_t s);
 hipError_t launch_rowsum(float *beta, const float *part, int32_t n_parts, int32_t M_pad, int32_t M,
@@ -116,5 +133,37 @@ struct SplitPrepArgs {
 hipError_t launch_split_prepare(const SplitPrepArgs &a, hipStream_t s);
 hipError_t launch_count_unstable(const float *L, const float *U, int64_t n, int32_t *count, hipStream_t s);
 hipError_t launch_copy(float *dst, const float *src, int64_t n, hipStream_t s);
+
+// ---- alpha-CROWN (alpha.hip) --------------------------------------------------------
+// Rows are (unit, q), q < 2m: q < m the lower bound of spec row q, q >= m the negated upper
+// bound of spec row q - m; every row maximises its own lower bound.
+struct AlphaLayer {
+  float *alpha, *mom, *vel, *best, *grad, *pre;   // [M_pad][ld] each
+  const float4 *P;                                // [units][ld] relaxation of this ReLU
+  int64_t ld;
+  int32_t n, col0;                                // neurons, first column in the compact layout
+};
+// alpha <- alpha_init (compact [units][2m][n_total]) or lam (P.x); mom = vel = 0
+hipError_t launch_alpha_init(const AlphaLayer &l, const float *alpha_init, int64_t n_total, int32_t rows,
+                             int32_t rows_pad, int32_t rows_per_unit, hipStream_t s);
+// E0 = c - sign(pre0) r per row (the box vertex that attains the row's bound)
+hipError_t launch_alpha_vertex(const float *pre0, int64_t ld0, const float *c0, const float *r0, int32_t rows_pad,
+                               int32_t rows_per_unit, int32_t units, float *E0, hipStream_t s);
+// row bound = beta + sum of the concretization partials (the order of the final reduction);
+// best/flag update, optional history [units][m] lb and ub of this evaluation
+hipError_t launch_alpha_best(const float *beta, const float *cpart, int32_t n_parts, int32_t M_pad, int32_t rows,
+                             int32_t m, int32_t first, float *best_val, int32_t *flag, float *hist_lb,
+                             float *hist_ub, hipStream_t s);
+// best <- alpha where the row improved
+hipError_t launch_alpha_keep(const AlphaLayer &l, const int32_t *flag, int32_t rows, hipStream_t s);
+// one projected Adam step (ascent) at unstable neurons; c1 = 1 / (1 - beta1^t), c2 = 1 / (1 - beta2^t)
+hipError_t launch_alpha_adam(const AlphaLayer &l, int32_t rows, int32_t rows_per_unit, float lr, float beta1,
+                             float beta2, float eps, float c1, float c2, hipStream_t s);
+// lb / ub from the best row values
+hipError_t launch_alpha_final(const float *best_val, int32_t units, int32_t m, float *lb, float *ub, hipStream_t s);
+// compact outputs: slopes of the best bound and the last gradient (d ub / d alpha for the
+// upper rows, so the sign of the negated rows is undone)
+hipError_t launch_alpha_out(const AlphaLayer &l, int32_t rows, int32_t m, int64_t n_total, float *alpha_out,
+                            float *grad_out, hipStream_t s);
 
 }  // namespace vcr

@@ -45,6 +45,13 @@ class VcrStats(ctypes.Structure):
                 ("timed_conv_ms", ctypes.c_double), ("timed_conv_flops", ctypes.c_uint64)]
 
 
+class VcrAlphaOpts(ctypes.Structure):
+    _fields_ = [("iters", ctypes.c_int32), ("lr", ctypes.c_float), ("beta1", ctypes.c_float),
+                ("beta2", ctypes.c_float), ("adam_eps", ctypes.c_float), ("alpha_init", ctypes.c_void_p),
+                ("alpha_out", ctypes.c_void_p), ("grad_out", ctypes.c_void_p), ("lb_hist", ctypes.c_void_p),
+                ("ub_hist", ctypes.c_void_p)]
+
+
 class VcrError(RuntimeError):
     def __init__(self, status, msg):
         super().__init__(f"{STATUS_NAMES[status] if 0 <= status < 7 else status}: {msg}")
@@ -76,6 +83,8 @@ def load_library(path: str = LIB_PATH):
         "vcr_get_layer_bounds": ([P, I32, P, P], I32),
         "vcr_workspace_bytes": ([P, I32, I32, I32, ctypes.POINTER(ctypes.c_uint64)], I32),
         "vcr_get_stats": ([P, ctypes.POINTER(VcrStats)], I32),
+        "vcr_alpha_crown_bounds": ([P, P, I32, F32, P, I32, ctypes.POINTER(VcrAlphaOpts), P, P], I32),
+        "vcr_relu_neurons": ([P], ctypes.c_int64),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -196,6 +205,42 @@ class Ctx:
         self._check(self.lib.vcr_crown_bounds(self.h, _ptr(x0), B, ctypes.c_float(float(eps)), _ptr(C), m, sp,
                                               _ptr(lb), _ptr(ub)))
         return lb, ub
+
+    def alpha_crown_bounds(self, x0, eps, C, iters=20, lr=0.1, beta1=0.9, beta2=0.999, adam_eps=1e-8,
+                           alpha_init=None, want_alpha=False, want_grad=False, want_hist=False):
+        """alpha-CROWN bounds on C f(x) (x0 (B, n0), C (B, m, n_out) float32 CUDA tensors).
+
+        Returns (lb, ub, extra): extra holds "alpha" and "grad" ((B, 2m, n_total): rows q < m
+        the lower bound of spec row q, m + q its upper bound; columns the ReLU neurons in node
+        order) and "lb_hist", "ub_hist" ((iters + 1, B, m)) when asked for."""
+        import torch
+        B, m = C.shape[0], C.shape[1]
+        _check_tensor(x0, (B, None))
+        _check_tensor(C, (B, m, None))
+        n_total = int(self.lib.vcr_relu_neurons(self.h))
+        dev = x0.device
+        lb = torch.empty((B, m), dtype=torch.float32, device=dev)
+        ub = torch.empty((B, m), dtype=torch.float32, device=dev)
+        extra = {}
+        o = VcrAlphaOpts(int(iters), float(lr), float(beta1), float(beta2), float(adam_eps), None, None, None, None, None)
+        if alpha_init is not None:
+            _check_tensor(alpha_init, (B, 2 * m, n_total))
+            o.alpha_init = alpha_init.data_ptr()
+        if want_alpha:
+            extra["alpha"] = torch.empty((B, 2 * m, n_total), dtype=torch.float32, device=dev)
+            o.alpha_out = extra["alpha"].data_ptr()
+        if want_grad:
+            extra["grad"] = torch.empty((B, 2 * m, n_total), dtype=torch.float32, device=dev)
+            o.grad_out = extra["grad"].data_ptr()
+        if want_hist:
+            extra["lb_hist"] = torch.empty((iters + 1, B, m), dtype=torch.float32, device=dev)
+            extra["ub_hist"] = torch.empty((iters + 1, B, m), dtype=torch.float32, device=dev)
+            o.lb_hist = extra["lb_hist"].data_ptr()
+            o.ub_hist = extra["ub_hist"].data_ptr()
+        self._stream_sync()
+        self._check(self.lib.vcr_alpha_crown_bounds(self.h, _ptr(x0), B, ctypes.c_float(float(eps)), _ptr(C), m,
+                                                    ctypes.byref(o), _ptr(lb), _ptr(ub)))
+        return lb, ub, extra
 
     def ibp_bounds(self, x0, eps, C):
         import torch
