@@ -49,15 +49,19 @@ def traffic_for(kernel, workload):
     return None if w is None else w.get("bytes_per_launch")
 
 
-def cpu_baseline(wl, budget_s):
+def cpu_baseline(wl, budget_s, alpha_iters=0):
     """The fp64 oracle, as it stands, on the first inputs of the same batch until the time
-    budget is used (at least one input)."""
+    budget is used (at least one input); with alpha_iters the alpha-CROWN oracle."""
     import threadpoolctl
     import oracle
+    from oracle import alpha64
     t0 = time.perf_counter()
     n = 0
     while n < wl.x0.shape[0]:
-        oracle.crown(wl.net, wl.x0[n], wl.eps, wl.C[n])
+        if alpha_iters:
+            alpha64.alpha_crown(wl.net, wl.x0[n], wl.eps, wl.C[n], iters=alpha_iters)
+        else:
+            oracle.crown(wl.net, wl.x0[n], wl.eps, wl.C[n])
         n += 1
         if time.perf_counter() - t0 >= budget_s:
             break
@@ -138,6 +142,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="mlp784x1024x6")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time (0: skip)")
+    ap.add_argument("--alpha-iters", type=int, default=0,
+                    help="alpha-CROWN with this many Adam steps on the final pass (MLPs; 0: CROWN)")
     ap.add_argument("--graph", action="store_true",
                     help="replay the call as a recorded HIP graph (the roofline then comes from a "
                          "second timed pass without the graph)")
@@ -160,6 +166,10 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
+    if args.alpha_iters and not args.workload.startswith("mlp"):
+        print("--alpha-iters runs on the MLP workloads (alpha-CROWN is built for dense/relu networks)",
+              file=sys.stderr)
+        sys.exit(2)
     import torch
     from paper_2606_09377_amd import Ctx
     from paper_2606_09377_amd.vcrown import OPT_TIME_GEMM
@@ -182,7 +192,10 @@ def main():
     ub = torch.empty((units, m), dtype=torch.float32, device="cuda")
 
     def step():
-        ctx.crown_bounds(x0, wl.eps, C, splits=splits, out=(lb, ub))
+        if args.alpha_iters:
+            ctx.alpha_crown_bounds(x0, wl.eps, C, iters=args.alpha_iters, out=(lb, ub))
+        else:
+            ctx.crown_bounds(x0, wl.eps, C, splits=splits, out=(lb, ub))
 
     for _ in range(args.warmup):
         step()
@@ -261,7 +274,9 @@ def main():
                    "domains": units if splits is not None else None,
                    "layers": [int(wl.net.nodes[0].W.shape[1])] + [int(nd.W.shape[0]) for nd in wl.net.nodes
                                                                    if nd.op == "dense"],
-                   "method": "full CROWN (IBP-intersected intermediate bounds)"},
+                   "method": (f"alpha-CROWN ({args.alpha_iters} projected Adam steps on the final pass, "
+                              "full-CROWN intermediate bounds)") if args.alpha_iters
+                   else "full CROWN (IBP-intersected intermediate bounds)"},
         "roofline": roofline(dominant),
         "call_mfma_frac": flops_call / (ms_step / 1e3) / (PEAK_FP32_MFMA_TFLOPS * 1e12),
         "graph_replay": bool(args.graph),
@@ -273,7 +288,7 @@ def main():
     if args.cpu_budget > 0 and args.workload.startswith("resnet3x32x32"):
         rec["cpu_baseline"] = cpu_baseline_sampled(wl, args.cpu_budget)
     elif args.cpu_budget > 0 and splits is None:
-        rec["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
+        rec["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget, args.alpha_iters)
     elif args.cpu_budget > 0:
         rec["cpu_baseline"] = cpu_baseline_bab(wl, sp, args.cpu_budget)
     print(json.dumps(rec), flush=True)

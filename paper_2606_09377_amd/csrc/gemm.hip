@@ -74,6 +74,11 @@ __device__ __forceinline__ float4 split_override(const SplitTable &st, int row, 
   return prm;
 }
 
+// Instantiations: FWD selects the forward epilogue (alpha-CROWN's gradient pass); otherwise the
+// relax and concretize epilogues share one kernel and the mode is read at run time (this keeps
+// the register allocation of the relax epilogue spill-free).  AL adds the alpha-CROWN extras
+// (per-row slopes, stored coefficients) to the backward epilogues.
+template <bool FWD, bool AL>
 __global__ __launch_bounds__(NTHREADS, 2) void k_gemm(const GemmArgs p) {
   __shared__ __attribute__((aligned(16))) float As[2][BM * LDS_LD];
   __shared__ __attribute__((aligned(16))) float Bs[2][BN * LDS_LD];
@@ -168,6 +173,16 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm(const GemmArgs p) {
   unit_tile = unit_tile < p.n_units ? unit_tile : p.n_units - 1;
   const bool has_splits = p.splits.D > 0;
 
+  // Stores and row-wise loads address the tile from a wave-uniform base with 32-bit lane
+  // offsets (every row-indexed array of one launch shares the pitch ld).
+  const int64_t ld = p.mode == EPI_CONCRETIZE ? p.ld_pre : p.ldo;
+  const int64_t tbase = (int64_t)m0 * ld;
+  float *const out_t = p.mode == EPI_CONCRETIZE ? nullptr : p.out + tbase;
+  float *const pre_t = p.pre ? p.pre + tbase : nullptr;
+  const float *const alpha_t = p.alpha ? p.alpha + tbase : nullptr;
+  float *const grad_t = p.grad ? p.grad + tbase : nullptr;
+  const int ld32 = (int)ld;
+
   float rp[2][16];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
@@ -177,14 +192,43 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm(const GemmArgs p) {
 #pragma unroll
   for (int bj = 0; bj < 2; ++bj) {
     const int n = n0 + wn * 64 + bj * 32 + r32;
-    if (p.mode == EPI_RELAX) {
+    if constexpr (FWD) {
+      // the relaxed network evaluated forward: D = W_k E + b_k, then the line of ReLU k that
+      // the backward pass chose for this row (by the sign of its coefficient)
       float4 prm_tile = make_float4(0.f, 0.f, 0.f, 0.f);
       if (uniform_unit) prm_tile = p.P[(int64_t)unit_tile * p.ldp + n];
 #pragma unroll
       for (int bi = 0; bi < 2; ++bi) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const int row = m0 + wm * 64 + bi * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
+          const int lr = wm * 64 + bi * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
+          const int row = m0 + lr;
+          const int off = lr * ld32 + n;
+          float4 prm = prm_tile;
+          if (!uniform_unit) {
+            int u = row / p.rows_per_unit;
+            u = u < p.n_units ? u : p.n_units - 1;
+            prm = p.P[(int64_t)u * p.ldp + n];
+          }
+          const bool unst = prm.z > 0.f;
+          const float lam = unst ? alpha_t[off] : prm.x;
+          const float an = pre_t[off];
+          const float D = acc[bi][bj][v] + prm.w;
+          const float E = an > 0.f ? lam * D : prm.y * D + (an < 0.f ? prm.z : 0.f);
+          out_t[off] = E;
+          grad_t[off] = (unst && an > 0.f) ? an * D : 0.f;
+        }
+      }
+    } else if (p.mode == EPI_RELAX) {
+      float4 prm_tile = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (uniform_unit) prm_tile = p.P[(int64_t)unit_tile * p.ldp + n];
+#pragma unroll
+      for (int bi = 0; bi < 2; ++bi) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int lr = wm * 64 + bi * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
+          const int row = m0 + lr;
+          const int off = lr * ld32 + n;
           float4 prm = prm_tile;
           if (!uniform_unit) {
             int u = row / p.rows_per_unit;
@@ -194,37 +238,15 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm(const GemmArgs p) {
           if (has_splits) prm = split_override(p.splits, row, p.relu_index, n, prm);
           const float a = acc[bi][bj][v];
           float lam = prm.x;
-          if (p.alpha && prm.z > 0.f) lam = p.alpha[(int64_t)row * p.ld_alpha + n];
-          const float ap = a > 0.f ? a * lam : a * prm.y;
-          p.out[(int64_t)row * p.ldo + n] = ap;
-          if (p.pre) p.pre[(int64_t)row * p.ld_pre + n] = a;
-          rp[bi][v] += fminf(a, 0.f) * prm.z + ap * prm.w;
-        }
-      }
-    } else if (p.mode == EPI_FORWARD) {
-      // the relaxed network evaluated forward: D = W_k E + b_k, then the line of ReLU k that
-      // the backward pass chose for this row (by the sign of its coefficient)
-      float4 prm_tile = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (uniform_unit) prm_tile = p.P[(int64_t)unit_tile * p.ldp + n];
-#pragma unroll
-      for (int bi = 0; bi < 2; ++bi) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int row = m0 + wm * 64 + bi * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
-          float4 prm = prm_tile;
-          if (!uniform_unit) {
-            int u = row / p.rows_per_unit;
-            u = u < p.n_units ? u : p.n_units - 1;
-            prm = p.P[(int64_t)u * p.ldp + n];
+          if constexpr (AL) {
+            if (alpha_t && prm.z > 0.f) lam = alpha_t[off];
           }
-          const bool unst = prm.z > 0.f;
-          const int64_t ia = (int64_t)row * p.ld_alpha + n;
-          const float lam = unst ? p.alpha[ia] : prm.x;
-          const float an = p.pre[(int64_t)row * p.ld_pre + n];
-          const float D = acc[bi][bj][v] + prm.w;
-          const float E = an > 0.f ? lam * D : prm.y * D + (an < 0.f ? prm.z : 0.f);
-          p.out[(int64_t)row * p.ldo + n] = E;
-          p.grad[ia] = (unst && an > 0.f) ? an * D : 0.f;
+          const float ap = a > 0.f ? a * lam : a * prm.y;
+          out_t[off] = ap;
+          if constexpr (AL) {
+            if (pre_t) pre_t[off] = a;
+          }
+          rp[bi][v] += fminf(a, 0.f) * prm.z + ap * prm.w;
         }
       }
     } else {
@@ -237,7 +259,8 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm(const GemmArgs p) {
       for (int bi = 0; bi < 2; ++bi) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const int row = m0 + wm * 64 + bi * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
+          const int lr = wm * 64 + bi * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
+          const int row = m0 + lr;
           float c = c_tile, r = r_tile;
           if (!uniform_unit) {
             int u = row / p.rows_per_unit;
@@ -246,14 +269,16 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm(const GemmArgs p) {
             r = p.r0[(int64_t)u * p.ldc + n];
           }
           const float a = acc[bi][bj][v];
-          if (p.pre) p.pre[(int64_t)row * p.ld_pre + n] = a;
+          if constexpr (AL) {
+            if (pre_t) pre_t[lr * ld32 + n] = a;
+          }
           rp[bi][v] += a * c - fabsf(a) * r;
         }
       }
     }
   }
 
-  if (p.mode == EPI_FORWARD) return;
+  if constexpr (FWD) return;
   // fixed butterfly over the 32 lanes that share rows
 #pragma unroll
   for (int bi = 0; bi < 2; ++bi) {
@@ -283,9 +308,25 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm(const GemmArgs p) {
 hipError_t launch_gemm(const GemmArgs &a, hipStream_t s) {
   if (a.M_pad % BM || a.N_pad % BN || a.K % BK || a.K <= 0 || a.M_pad <= 0 || a.N_pad <= 0)
     return hipErrorInvalidValue;
+  // the epilogue's row-indexed arrays share one pitch and use 32-bit offsets within a tile
+  const int64_t ld = a.mode == EPI_CONCRETIZE ? a.ld_pre : a.ldo;
+  if (a.mode != EPI_CONCRETIZE && ((a.alpha && a.ld_alpha != a.ldo) || (a.pre && a.ld_pre != a.ldo)))
+    return hipErrorInvalidValue;
+  if (a.mode == EPI_FORWARD && (!a.alpha || !a.pre || !a.grad || !a.out)) return hipErrorInvalidValue;
+  if ((int64_t)BM * ld + a.N_pad >= ((int64_t)1 << 31) || (ld < a.N_pad && (a.mode != EPI_CONCRETIZE || a.pre)))
+    return hipErrorInvalidValue;
   const int64_t grid = (int64_t)(a.M_pad / BM) * (a.N_pad / BN);
   if (grid > 0x7fffffff) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_gemm, dim3((unsigned)grid), dim3(NTHREADS), 0, s, a);
+  const bool al = a.alpha || a.pre;
+  const dim3 g((unsigned)grid), t(NTHREADS);
+  if (a.mode == EPI_FORWARD)
+    hipLaunchKernelGGL((k_gemm<true, true>), g, t, 0, s, a);
+  else if (a.mode != EPI_RELAX && a.mode != EPI_CONCRETIZE)
+    return hipErrorInvalidValue;
+  else if (al)
+    hipLaunchKernelGGL((k_gemm<false, true>), g, t, 0, s, a);
+  else
+    hipLaunchKernelGGL((k_gemm<false, false>), g, t, 0, s, a);
   return hipGetLastError();
 }
 

@@ -207,7 +207,7 @@ class Ctx:
         return lb, ub
 
     def alpha_crown_bounds(self, x0, eps, C, iters=20, lr=0.1, beta1=0.9, beta2=0.999, adam_eps=1e-8,
-                           alpha_init=None, want_alpha=False, want_grad=False, want_hist=False):
+                           alpha_init=None, want_alpha=False, want_grad=False, want_hist=False, out=None):
         """alpha-CROWN bounds on C f(x) (x0 (B, n0), C (B, m, n_out) float32 CUDA tensors).
 
         Returns (lb, ub, extra): extra holds "alpha" and "grad" ((B, 2m, n_total): rows q < m
@@ -219,8 +219,13 @@ class Ctx:
         _check_tensor(C, (B, m, None))
         n_total = int(self.lib.vcr_relu_neurons(self.h))
         dev = x0.device
-        lb = torch.empty((B, m), dtype=torch.float32, device=dev)
-        ub = torch.empty((B, m), dtype=torch.float32, device=dev)
+        if out is None:
+            lb = torch.empty((B, m), dtype=torch.float32, device=dev)
+            ub = torch.empty((B, m), dtype=torch.float32, device=dev)
+        else:
+            lb, ub = out
+            _check_tensor(lb, (B, m))
+            _check_tensor(ub, (B, m))
         extra = {}
         o = VcrAlphaOpts(int(iters), float(lr), float(beta1), float(beta2), float(adam_eps), None, None, None, None, None)
         if alpha_init is not None:
