@@ -60,6 +60,9 @@ def cpu_baseline(wl, budget_s, alpha_iters=0):
     while n < wl.x0.shape[0]:
         if alpha_iters:
             alpha64.alpha_crown(wl.net, wl.x0[n], wl.eps, wl.C[n], iters=alpha_iters)
+        elif wl.name.startswith("exp1_"):
+            # one hidden layer: the oracle's row-block form (the full-matrix form needs ~40 GB)
+            oracle.crown_one_hidden(wl.net, wl.x0[n], wl.eps, wl.C[n])
         else:
             oracle.crown(wl.net, wl.x0[n], wl.eps, wl.C[n])
         n += 1
@@ -281,6 +284,7 @@ def main():
         "call_mfma_frac": flops_call / (ms_step / 1e3) / (PEAK_FP32_MFMA_TFLOPS * 1e12),
         "graph_replay": bool(args.graph),
         "gemm_flops_per_step": flops_call,
+        "device_memory": {"net_bytes": st["net_bytes"], "workspace_peak_bytes": st["peak_workspace_bytes"]},
     }
     if other:
         rec["roofline_other"] = roofline(other[0])

@@ -114,7 +114,9 @@ enum {
 
 typedef struct {
   double ms_last_call;              /* host wall time of the last bounds call (queue + wait if SYNC_CHECK) */
-  uint64_t gemm_flops_last_call;    /* algorithmic fp32 GEMM flops of the last call (2 per MAC) */
+  uint64_t gemm_flops_last_call;    /* algorithmic fp32 GEMM flops of the last call (2 per MAC): the
+                                       backward steps, and the IBP steps of large layers, which
+                                       run as GEMMs */
   uint64_t peak_workspace_bytes;    /* largest device workspace held so far */
   uint64_t workspace_bytes;         /* current device workspace */
   int32_t n_chunks_last_call;       /* input (or domain) chunks used by the last call */
@@ -132,6 +134,7 @@ typedef struct {
   uint64_t timed_conv_launches;
   double timed_conv_ms;
   uint64_t timed_conv_flops;
+  uint64_t net_bytes;               /* device memory holding the loaded network's weights */
 } vcr_stats;
 
 /* ABI version compiled into the library (VCR_ABI_VERSION). */

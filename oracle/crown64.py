@@ -20,7 +20,9 @@ What it computes (section numbers are the paper's):
     that layer down to the input, each intersected with the IBP bounds;
   * branch-and-bound subdomains that fix ReLUs to the active (z >= 0) or inactive (z <= 0)
     state (Sec. 2.1, complete verification), bounded with the root's intermediate bounds
-    and only the split neurons' own intervals clamped.
+    and only the split neurons' own intervals clamped;
+  * the same full CROWN for one-hidden-layer networks in row blocks of the first weight
+    matrix (memory-bounded, for the Exp. 1 network of Sec. 4.1).
 
 Readings where the paper is silent (each is also listed in the design notes):
   * adaptive lower slope: lambda = 1 if u > -l else 0, a tie giving 0;
@@ -45,7 +47,7 @@ import numpy as np
 __all__ = [
     "input_box", "node_shapes", "forward", "ibp", "ibp_spec_bounds", "relu_relaxation",
     "conv2d", "conv2d_transpose", "backward", "concretize", "crown", "CrownResult",
-    "apply_splits", "crown_domains", "unstable_pool", "support", "crown_sampled",
+    "apply_splits", "crown_domains", "unstable_pool", "support", "crown_sampled", "crown_one_hidden",
 ]
 
 
@@ -544,3 +546,55 @@ def crown_sampled(net, x0, eps, targets, clip=(0.0, 1.0), intersect_ibp=True, ch
         # neurons outside the set are never reached; (0, 0) makes them inactive
         relax[i] = relu_relaxation(l, u)
     return out
+
+
+# --------------------------------------------------------------------------------------
+# one hidden layer, processed in row blocks (the paper's Exp. 1 network, Sec. 4.1)
+
+def crown_one_hidden(net, x0, eps, C, clip=(0.0, 1.0), intersect_ibp=True, chunk=8192):
+    """Full CROWN for dense -> relu -> dense, the same steps as crown() written for this
+    structure so the first weight matrix is promoted to float64 one block of rows at a time
+    (the 262144 x 4096 layer would need 8.6 GB per float64 copy).
+
+    The hidden pre-activations are one affine map of the input, so their bounds are the
+    exact box range (intersected with the IBP interval W+ l + W- u + b when intersect_ibp);
+    the final pass composes C W2, the relaxation and W1 and takes the extremes over the
+    box vertex-wise."""
+    d1, r1, d2 = net.nodes
+    if not (d1.op == "dense" and d1.in0 == -1 and r1.op == "relu" and r1.in0 == 0
+            and d2.op == "dense" and d2.in0 == 1 and len(net.nodes) == 3):
+        raise ValueError("crown_one_hidden needs dense -> relu -> dense")
+    lo, hi = input_box(x0, eps, clip)
+    n1 = d1.W.shape[0]
+    l = np.empty(n1)
+    u = np.empty(n1)
+    for r0 in range(0, n1, chunk):
+        rows = slice(r0, min(n1, r0 + chunk))
+        W = _f64(d1.W[rows])
+        b = _f64(d1.b[rows])
+        l[rows] = concretize(W, b, lo, hi, False)
+        u[rows] = concretize(W, b, lo, hi, True)
+        if intersect_ibp:
+            Wp, Wn = np.maximum(W, 0.0), np.minimum(W, 0.0)
+            l[rows] = np.maximum(l[rows], Wp @ lo + Wn @ hi + b)
+            u[rows] = np.minimum(u[rows], Wp @ hi + Wn @ lo + b)
+    lam, s, t = relu_relaxation(l, u)
+    Cm = _f64(C)
+    A = Cm @ _f64(d2.W)
+    bias = Cm @ _f64(d2.b)
+    Ap, An = np.maximum(A, 0.0), np.minimum(A, 0.0)
+    Az_l, bias_l = Ap * lam + An * s, bias + An @ t          # lower: positive -> lower line
+    Az_u, bias_u = Ap * s + An * lam, bias + Ap @ t          # upper: positive -> upper line
+    n0 = lo.size
+    Ax_l, Ax_u = np.zeros((A.shape[0], n0)), np.zeros((A.shape[0], n0))
+    for r0 in range(0, n1, chunk):
+        rows = slice(r0, min(n1, r0 + chunk))
+        W = _f64(d1.W[rows])
+        b = _f64(d1.b[rows])
+        Ax_l += Az_l[:, rows] @ W
+        Ax_u += Az_u[:, rows] @ W
+        bias_l = bias_l + Az_l[:, rows] @ b
+        bias_u = bias_u + Az_u[:, rows] @ b
+    lb = concretize(Ax_l, bias_l, lo, hi, False)
+    ub = concretize(Ax_u, bias_u, lo, hi, True)
+    return lb, ub, l, u

@@ -27,6 +27,7 @@
 #include <string>
 #include <vector>
 
+#include "conv.h"
 #include "ctx.h"
 
 using namespace vcr;
@@ -427,6 +428,9 @@ vcr_status vcr_load_net(vcr_ctx *c, const vcr_node *nodes, int32_t n, const int3
     prev = L.n_out;
   }
   HIP_TRY(c, hipDeviceSynchronize());
+  c->net_bytes = 0;
+  for (const DenseLayer &L : c->layers)
+    c->net_bytes += sizeof(float) * (2 * (uint64_t)L.ld_in * L.ld_out + (uint64_t)L.ld_out);
   c->loaded = true;
   return VCR_OK;
 }
@@ -450,6 +454,7 @@ struct CallBufs {
   std::vector<AlphaLayer> al;
   float *pre0, *best_val;
   int32_t *flag;
+  float *tmp_c, *tmp_r;   // ReLU'd IBP inputs of large layers
 };
 
 vcr_status check_common(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m,
@@ -466,17 +471,70 @@ vcr_status check_common(vcr_ctx *c, const float *x0, int32_t B, float eps, const
   return VCR_OK;
 }
 
+// IBP through dense layer W (c' = W c + b, r' = |W| r, after a ReLU on the input when
+// relu_in).  Large layers run as two fp32 MFMA GEMMs; the choice depends on the layer's size
+// only, so an input's bounds do not depend on the batch it is in.  cin/rin and cout/rout
+// hold rows_pad(B) rows; tmp_c/tmp_r (same shape as cin) take the ReLU'd input.
+constexpr int64_t IBP_MFMA_MIN_WEIGHTS = (int64_t)1 << 24;
+bool ibp_on_mfma(const DenseLayer &W) { return (int64_t)W.n_out * W.n_in >= IBP_MFMA_MIN_WEIGHTS; }
+
+vcr_status ibp_layer(vcr_ctx *c, const DenseLayer &W, const float *cin, const float *rin, bool relu_in, float *cout,
+                     float *rout, int32_t B, float *tmp_c, float *tmp_r, hipStream_t s, uint64_t *flops = nullptr) {
+  if (!ibp_on_mfma(W)) {
+    HIP_TRY(c, launch_ibp_dense(W.Wp, W.ld_in, W.b, W.n_out, W.n_in, cin, rin, W.ld_in, relu_in, cout, rout, W.ld_out,
+                                B, s));
+    return VCR_OK;
+  }
+  const int64_t M_pad = rows_pad(B);
+  if (relu_in) {
+    HIP_TRY(c, launch_ibp_relu(cin, rin, tmp_c, tmp_r, M_pad * W.ld_in, s));
+    cin = tmp_c;
+    rin = tmp_r;
+  }
+  GemmArgs g{};
+  g.lda = W.ld_in;
+  g.Bt = W.Wp;
+  g.ldb = W.ld_in;
+  g.M = B;
+  g.M_pad = (int32_t)M_pad;
+  g.K = (int32_t)W.ld_in;
+  g.N_pad = (int32_t)W.ld_out;
+  g.mode = EPI_AFFINE;
+  g.ldo = W.ld_out;
+  g.rows_per_unit = (int32_t)M_pad;
+  g.n_units = 1;
+  g.A = cin;
+  g.out = cout;
+  g.bias = W.b;
+  const uint64_t gf = 2ull * (uint64_t)B * (uint64_t)W.n_out * (uint64_t)W.n_in;
+  if (flops) *flops += 2 * gf;
+  vcr_status st = timed_launch(c, s, 0, gf, [&] { return launch_gemm(g, s); });
+  if (st != VCR_OK) return st;
+  g.A = rin;
+  g.out = rout;
+  g.bias = nullptr;
+  g.abs_b = 1;
+  return timed_launch(c, s, 0, gf, [&] { return launch_gemm(g, s); });
+}
+
+bool any_ibp_relu_on_mfma(const vcr_ctx *c) {
+  for (size_t k = 1; k + 1 < c->layers.size(); ++k)
+    if (ibp_on_mfma(c->layers[k])) return true;
+  return false;
+}
+
 void carve(const vcr_ctx *c, Workspace &w, const Plan &p, int32_t S, CallBufs *bf) {
   const int L = (int)c->layers.size();
   const int32_t B = p.B;
+  const int64_t Bp = rows_pad(B);   // IBP arrays are GEMM operands on large layers
   const int64_t ld0 = ld_of(c->n0);
-  bf->c0 = take<float>(w, (size_t)B * ld0);
-  bf->r0 = take<float>(w, (size_t)B * ld0);
+  bf->c0 = take<float>(w, (size_t)Bp * ld0);
+  bf->r0 = take<float>(w, (size_t)Bp * ld0);
   bf->ibp_c.clear(); bf->ibp_r.clear(); bf->Lb.clear(); bf->Ub.clear(); bf->P.clear();
   for (int k = 0; k < L - 1; ++k) {
     const int64_t ld = c->layers[k].ld_out, n = c->layers[k].n_out;
-    bf->ibp_c.push_back(take<float>(w, (size_t)B * ld));
-    bf->ibp_r.push_back(take<float>(w, (size_t)B * ld));
+    bf->ibp_c.push_back(take<float>(w, (size_t)Bp * ld));
+    bf->ibp_r.push_back(take<float>(w, (size_t)Bp * ld));
     bf->Lb.push_back(take<float>(w, (size_t)B * n));
     bf->Ub.push_back(take<float>(w, (size_t)B * n));
     bf->P.push_back(take<float4>(w, (size_t)B * ld));
@@ -527,6 +585,11 @@ void carve(const vcr_ctx *c, Workspace &w, const Plan &p, int32_t S, CallBufs *b
   bf->beta = take<float>(w, (size_t)mp);
   bf->part = take<float>(w, (size_t)mp * std::max<int64_t>(ldmax / PART_COLS, 1));
   bf->cpart = take<float>(w, (size_t)mp * (ld0 / PART_COLS));
+  bf->tmp_c = bf->tmp_r = nullptr;
+  if (any_ibp_relu_on_mfma(c)) {
+    bf->tmp_c = take<float>(w, (size_t)Bp * std::max<int64_t>(ldmax, 1));
+    bf->tmp_r = take<float>(w, (size_t)Bp * std::max<int64_t>(ldmax, 1));
+  }
 }
 
 size_t carve_bytes(const vcr_ctx *c, const Plan &p, int32_t S) {
@@ -742,8 +805,8 @@ vcr_status crown_impl(vcr_ctx *c, const float *x0, int32_t B, float eps, const f
     const DenseLayer &W = c->layers[k];
     const float *cin = k == 0 ? bf.c0 : bf.ibp_c[k - 1];
     const float *rin = k == 0 ? bf.r0 : bf.ibp_r[k - 1];
-    HIP_TRY(c, launch_ibp_dense(W.Wp, W.ld_in, W.b, W.n_out, W.n_in, cin, rin, W.ld_in, k > 0, bf.ibp_c[k],
-                                bf.ibp_r[k], W.ld_out, B, s));
+    st = ibp_layer(c, W, cin, rin, k > 0, bf.ibp_c[k], bf.ibp_r[k], B, bf.tmp_c, bf.tmp_r, s, &flops);
+    if (st != VCR_OK) return st;
   }
   // 2. first ReLU
   if (L >= 2)
@@ -967,27 +1030,33 @@ vcr_status vcr_ibp_bounds(vcr_ctx *c, const float *x0, int32_t B, float eps, con
   HIP_TRY(c, hipSetDevice(c->device));
   const int L = (int)c->layers.size();
   const int64_t ld0 = ld_of(c->n0);
-  size_t bytes = 2 * al(sizeof(float) * B * ld0);
-  for (int k = 0; k < L - 1; ++k) bytes += 2 * al(sizeof(float) * B * c->layers[k].ld_out);
+  const int64_t Bp = rows_pad(B);   // GEMM operands on large layers
+  int64_t ldmax = 1;
+  for (int k = 0; k < L - 1; ++k) ldmax = std::max(ldmax, c->layers[k].ld_out);
+  const bool tmp = any_ibp_relu_on_mfma(c);
+  size_t bytes = 2 * al(sizeof(float) * Bp * ld0);
+  for (int k = 0; k < L - 1; ++k) bytes += 2 * al(sizeof(float) * Bp * c->layers[k].ld_out);
   bytes += al(sizeof(float) * B * m * c->layers[L - 1].ld_in) + al(sizeof(float) * B * m);
+  if (tmp) bytes += 2 * al(sizeof(float) * Bp * ldmax);
   c->lastL.clear();   // this call reuses the workspace that held them
   c->lastU.clear();
   st = ensure_ws(c, bytes);
   if (st != VCR_OK) return st;
   hipStream_t s = c->stream;
-  float *c0 = take<float>(c, (size_t)B * ld0), *r0 = take<float>(c, (size_t)B * ld0);
+  float *c0 = take<float>(c, (size_t)Bp * ld0), *r0 = take<float>(c, (size_t)Bp * ld0);
   std::vector<float *> cc, rr;
   for (int k = 0; k < L - 1; ++k) {
-    cc.push_back(take<float>(c, (size_t)B * c->layers[k].ld_out));
-    rr.push_back(take<float>(c, (size_t)B * c->layers[k].ld_out));
+    cc.push_back(take<float>(c, (size_t)Bp * c->layers[k].ld_out));
+    rr.push_back(take<float>(c, (size_t)Bp * c->layers[k].ld_out));
   }
   const DenseLayer &WL = c->layers[L - 1];
   float *CW = take<float>(c, (size_t)B * m * WL.ld_in), *Cb = take<float>(c, (size_t)B * m);
+  float *tc = tmp ? take<float>(c, (size_t)Bp * ldmax) : nullptr, *tr = tmp ? take<float>(c, (size_t)Bp * ldmax) : nullptr;
   HIP_TRY(c, launch_box(x0, B, c->n0, ld0, eps, c->clip_on, c->clip_lo, c->clip_hi, c0, r0, s));
   for (int k = 0; k < L - 1; ++k) {
     const DenseLayer &W = c->layers[k];
-    HIP_TRY(c, launch_ibp_dense(W.Wp, W.ld_in, W.b, W.n_out, W.n_in, k == 0 ? c0 : cc[k - 1], k == 0 ? r0 : rr[k - 1],
-                                W.ld_in, k > 0, cc[k], rr[k], W.ld_out, B, s));
+    st = ibp_layer(c, W, k == 0 ? c0 : cc[k - 1], k == 0 ? r0 : rr[k - 1], k > 0, cc[k], rr[k], B, tc, tr, s);
+    if (st != VCR_OK) return st;
   }
   HIP_TRY(c, launch_spec_cw(C, B, m, WL.n_out, WL.Wp, WL.ld_in, WL.b, WL.n_in, CW, WL.ld_in, Cb, s));
   HIP_TRY(c, launch_spec_direct(CW, WL.ld_in, Cb, B, m, WL.n_in, L >= 2 ? cc[L - 2] : c0, L >= 2 ? rr[L - 2] : r0,
@@ -1063,6 +1132,7 @@ vcr_status vcr_get_stats(vcr_ctx *c, vcr_stats *out) {
   out->workspace_bytes = c->ws.cap;
   out->n_chunks_last_call = c->chunks_last;
   out->n_relu = (int32_t)c->relu_n.size();
+  out->net_bytes = c->net_bytes;
   if (c->device < 0) return VCR_OK;
   HIP_TRY(c, hipSetDevice(c->device));
   {

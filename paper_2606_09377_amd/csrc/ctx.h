@@ -58,6 +58,7 @@ struct vcr_ctx {
   // workspace
   Workspace ws;
   uint64_t peak_ws = 0;
+  uint64_t net_bytes = 0;   // device memory holding the loaded network (weights in their layouts)
   // last call
   int32_t last_B = 0;
   std::vector<float *> lastL, lastU;

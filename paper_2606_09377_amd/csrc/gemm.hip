@@ -13,6 +13,8 @@
 //                    constant terms this neuron adds to the bound)
 //   EPI_CONCRETIZE : part[row] += a c[n] - |a| r[n]  (j = 1: minimum of a . x over the box
 //                    with centre c and radius r); A_0 itself is never written
+//   EPI_AFFINE     : out[row, n] = a + bias[n], with |Bt| instead of Bt when abs_b (the IBP
+//                    step c' = W c + b, r' = |W| r on the matrix cores)
 //   EPI_FORWARD    : out[row, n] = the relaxation line of ReLU k at D = a + b_k[n] chosen
 //                    by the sign of the backward coefficient, and its alpha gradient
 //                    (alpha-CROWN's gradient pass: A' = E_{k-1}, Bt = W_k)
@@ -78,7 +80,7 @@ __device__ __forceinline__ float4 split_override(const SplitTable &st, int row, 
 // relax and concretize epilogues share one kernel and the mode is read at run time (this keeps
 // the register allocation of the relax epilogue spill-free).  AL adds the alpha-CROWN extras
 // (per-row slopes, stored coefficients) to the backward epilogues.
-template <bool FWD, bool AL>
+template <bool FWD, bool AL, bool AFF = false>
 __global__ __launch_bounds__(NTHREADS, 2) void k_gemm(const GemmArgs p) {
   __shared__ __attribute__((aligned(16))) float As[2][BM * LDS_LD];
   __shared__ __attribute__((aligned(16))) float Bs[2][BN * LDS_LD];
@@ -112,6 +114,9 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm(const GemmArgs p) {
   for (int q = 0; q < 4; ++q) {
     ra[q] = *reinterpret_cast<const f32x4 *>(Ag + q * a_step);
     rb[q] = *reinterpret_cast<const f32x4 *>(Bg + q * b_step);
+    if constexpr (AFF) {
+      if (p.abs_b) rb[q] = __builtin_elementwise_abs(rb[q]);
+    }
   }
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
@@ -136,6 +141,9 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm(const GemmArgs p) {
       for (int q = 0; q < 4; ++q) {
         ra[q] = *reinterpret_cast<const f32x4 *>(Ag + q * a_step + k0);
         rb[q] = *reinterpret_cast<const f32x4 *>(Bg + q * b_step + k0);
+        if constexpr (AFF) {
+          if (p.abs_b) rb[q] = __builtin_elementwise_abs(rb[q]);
+        }
       }
     }
     const float *as = As[cur];
@@ -189,6 +197,22 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm(const GemmArgs p) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) rp[i][v] = 0.f;
 
+  if constexpr (AFF) {
+    // plain affine map (the IBP step on the matrix cores): out = A Bt^T (+ bias)
+#pragma unroll
+    for (int bj = 0; bj < 2; ++bj) {
+      const int n = n0 + wn * 64 + bj * 32 + r32;
+      const float bn = p.bias ? p.bias[n] : 0.f;
+#pragma unroll
+      for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int lr = wm * 64 + bi * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
+          out_t[lr * ld32 + n] = acc[bi][bj][v] + bn;
+        }
+    }
+    return;
+  }
 #pragma unroll
   for (int bj = 0; bj < 2; ++bj) {
     const int n = n0 + wn * 64 + bj * 32 + r32;
@@ -313,13 +337,16 @@ hipError_t launch_gemm(const GemmArgs &a, hipStream_t s) {
   if (a.mode != EPI_CONCRETIZE && ((a.alpha && a.ld_alpha != a.ldo) || (a.pre && a.ld_pre != a.ldo)))
     return hipErrorInvalidValue;
   if (a.mode == EPI_FORWARD && (!a.alpha || !a.pre || !a.grad || !a.out)) return hipErrorInvalidValue;
+  if (a.mode == EPI_AFFINE && (!a.out || a.alpha || a.pre)) return hipErrorInvalidValue;
   if ((int64_t)BM * ld + a.N_pad >= ((int64_t)1 << 31) || (ld < a.N_pad && (a.mode != EPI_CONCRETIZE || a.pre)))
     return hipErrorInvalidValue;
   const int64_t grid = (int64_t)(a.M_pad / BM) * (a.N_pad / BN);
   if (grid > 0x7fffffff) return hipErrorInvalidValue;
   const bool al = a.alpha || a.pre;
   const dim3 g((unsigned)grid), t(NTHREADS);
-  if (a.mode == EPI_FORWARD)
+  if (a.mode == EPI_AFFINE)
+    hipLaunchKernelGGL((k_gemm<false, false, true>), g, t, 0, s, a);
+  else if (a.mode == EPI_FORWARD)
     hipLaunchKernelGGL((k_gemm<true, true>), g, t, 0, s, a);
   else if (a.mode != EPI_RELAX && a.mode != EPI_CONCRETIZE)
     return hipErrorInvalidValue;

@@ -493,6 +493,7 @@ vcr_status graph_load(vcr_ctx *c, const vcr_node *nodes, int32_t n, const int32_
   if (in_chw[1] != in_chw[2]) return fail(c, VCR_ERR_UNSUPPORTED, "only square inputs are supported");
   GraphNet *g = new GraphNet();
   std::unique_ptr<GraphNet, void (*)(GraphNet *)> guard(g, destroy_graph);
+  c->net_bytes = 0;
   g->in_C = in_chw[0];
   g->in_H = in_chw[1];
   g->n0 = (int64_t)in_chw[0] * in_chw[1] * in_chw[2];
@@ -568,10 +569,13 @@ vcr_status graph_load(vcr_ctx *c, const vcr_node *nodes, int32_t n, const int32_
       const int Co = gn.C, Ci = gn.Ci;
       const size_t wn = (size_t)Co * Ci * 9;
       HIP_TRY(c, hipMalloc(&gn.W, wn * 4));
+      c->net_bytes += wn * 4;
       HIP_TRY(c, hipMemcpy(gn.W, d.W, wn * 4, hipMemcpyHostToDevice));
       HIP_TRY(c, hipMalloc(&gn.b, (size_t)Co * 4));
+      c->net_bytes += (size_t)Co * 4;
       HIP_TRY(c, hipMemcpy(gn.b, d.b, (size_t)Co * 4, hipMemcpyHostToDevice));
       HIP_TRY(c, hipMalloc(&gn.Bt, (size_t)gn.Ci_pad * 9 * Co * 4));
+      c->net_bytes += (size_t)gn.Ci_pad * 9 * Co * 4;
       HIP_TRY(c, launch_repack_convt(gn.W, Co, Ci, gn.Ci_pad, gn.Bt, s));
     } else if (d.op == VCR_DENSE) {
       const int64_t nin = d.in0 >= 0 ? g->nodes[d.in0].numel : g->n0;
@@ -580,7 +584,9 @@ vcr_status graph_load(vcr_ctx *c, const vcr_node *nodes, int32_t n, const int32_
       HIP_TRY(c, hipMalloc(&staging, (size_t)nout * nin * 4));
       HIP_TRY(c, hipMemcpy(staging, d.W, (size_t)nout * nin * 4, hipMemcpyHostToDevice));
       HIP_TRY(c, hipMalloc(&gn.Wp, (size_t)nout * gn.ld_in * 4));
+      c->net_bytes += (size_t)nout * gn.ld_in * 4;
       HIP_TRY(c, hipMalloc(&gn.Bt, (size_t)gn.ld_in * gn.ld_out * 4));
+      c->net_bytes += (size_t)gn.ld_in * gn.ld_out * 4;
       // Wp = W with zero-padded rows (via the transposed copy)
       HIP_TRY(c, launch_transpose_pad(staging, (int32_t)nout, (int32_t)nin, gn.Bt, gn.ld_out, gn.ld_in, s));
       HIP_TRY(c, launch_transpose_pad(gn.Bt, (int32_t)gn.ld_in, (int32_t)gn.ld_out, gn.Wp, gn.ld_in, nout, s));
@@ -588,10 +594,12 @@ vcr_status graph_load(vcr_ctx *c, const vcr_node *nodes, int32_t n, const int32_
         const GNode &fl = g->nodes[d.in0];
         const GNode &cv = g->nodes[fl.in0];
         HIP_TRY(c, hipMalloc(&gn.Wh, (size_t)nout * gn.ld_in * 4));
+        c->net_bytes += (size_t)nout * gn.ld_in * 4;
         HIP_TRY(c, launch_permute_hwc(staging, (int32_t)nout, cv.C, cv.H * cv.H, gn.Wh, gn.ld_in, s));
         HIP_TRY(c, launch_transpose_pad(gn.Wh, (int32_t)nout, (int32_t)gn.ld_in, gn.Bt, gn.ld_out, gn.ld_in, s));
       }
       HIP_TRY(c, hipMalloc(&gn.b, (size_t)gn.ld_out * 4));
+      c->net_bytes += (size_t)gn.ld_out * 4;
       HIP_TRY(c, launch_fill(gn.b, gn.ld_out, 0.f, s));
       HIP_TRY(c, hipStreamSynchronize(s));
       HIP_TRY(c, hipMemcpy(gn.b, d.b, (size_t)nout * 4, hipMemcpyHostToDevice));
@@ -619,10 +627,12 @@ vcr_status graph_load(vcr_ctx *c, const vcr_node *nodes, int32_t n, const int32_
   // every pass ends at the stem (checked by the planner)
   if (dev && !pl.host_bias.empty()) {
     HIP_TRY(c, hipMalloc(&g->bias_arena, pl.host_bias.size() * 4));
+    c->net_bytes += pl.host_bias.size() * 4;
     HIP_TRY(c, hipMemcpy(g->bias_arena, pl.host_bias.data(), pl.host_bias.size() * 4, hipMemcpyHostToDevice));
   }
   if (dev && !pl.host_params.empty()) {
     HIP_TRY(c, hipMalloc(&g->param_arena, pl.host_params.size() * sizeof(float4)));
+    c->net_bytes += pl.host_params.size() * sizeof(float4);
     HIP_TRY(c, hipMemcpy(g->param_arena, pl.host_params.data(), pl.host_params.size() * sizeof(float4),
                          hipMemcpyHostToDevice));
   }

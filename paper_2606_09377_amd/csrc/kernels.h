@@ -26,7 +26,7 @@ struct SplitTable {
   int32_t rows_per_domain = 0;
 };
 
-enum EpiMode : int32_t { EPI_RELAX = 0, EPI_CONCRETIZE = 1, EPI_FORWARD = 2 };
+enum EpiMode : int32_t { EPI_RELAX = 0, EPI_CONCRETIZE = 1, EPI_FORWARD = 2, EPI_AFFINE = 3 };
 
 struct GemmArgs {
   const float *A;      // M_pad x lda, coefficient rows (already relaxed), zero padded
@@ -64,6 +64,10 @@ struct GemmArgs {
   float *pre;
   int64_t ld_pre;
   float *grad;
+  // EPI_AFFINE: out = A Bt^T + bias (bias [N_pad] or null), Bt taken elementwise-absolute
+  // when abs_b (IBP: c' = W c + b, r' = |W| r)
+  const float *bias;
+  int32_t abs_b;
 };
 
 hipError_t launch_gemm(const GemmArgs &a, hipStream_t s);

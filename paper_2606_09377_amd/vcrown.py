@@ -42,7 +42,8 @@ class VcrStats(ctypes.Structure):
                 ("n_relu", ctypes.c_int32), ("unstable", ctypes.c_int32 * 64),
                 ("timed_gemm_launches", ctypes.c_uint64), ("timed_gemm_ms", ctypes.c_double),
                 ("timed_gemm_flops", ctypes.c_uint64), ("timed_conv_launches", ctypes.c_uint64),
-                ("timed_conv_ms", ctypes.c_double), ("timed_conv_flops", ctypes.c_uint64)]
+                ("timed_conv_ms", ctypes.c_double), ("timed_conv_flops", ctypes.c_uint64),
+                ("net_bytes", ctypes.c_uint64)]
 
 
 class VcrAlphaOpts(ctypes.Structure):
@@ -282,7 +283,8 @@ class Ctx:
                 "n_relu": s.n_relu, "unstable": list(s.unstable[:min(s.n_relu, 64)]),
                 "timed_gemm_launches": int(s.timed_gemm_launches), "timed_gemm_ms": s.timed_gemm_ms,
                 "timed_gemm_flops": int(s.timed_gemm_flops), "timed_conv_launches": int(s.timed_conv_launches),
-                "timed_conv_ms": s.timed_conv_ms, "timed_conv_flops": int(s.timed_conv_flops)}
+                "timed_conv_ms": s.timed_conv_ms, "timed_conv_flops": int(s.timed_conv_flops),
+                "net_bytes": int(s.net_bytes)}
 
 
 def _relu_sizes(net):

@@ -3,6 +3,9 @@
 Calls only the fp64 oracle (oracle/) on the seeded workloads (workloads/).
   * <workload>.npz: the final bounds and every ReLU layer's pre-activation bounds of the
     listed inputs;
+  * exp1_mlp4096x262144x1.npz: the paper's Exp. 1 network (one hidden layer of 262144):
+    final bounds of the listed inputs and the hidden bounds of sampled neurons, from the
+    oracle's row-block computation for one hidden layer;
   * bab_mlp784x1024x6_splits.npz: the branch-and-bound subdomains of that workload, drawn
     from the oracle root pass's unstable neurons (the draw continues the workload's seeded
     generator, so it equals what the tests draw at run time).
@@ -75,6 +78,29 @@ def make_sampled(name, inputs, counts):
     print("wrote", path)
 
 
+# one-hidden-layer workloads: {workload: (inputs, sampled hidden neurons per input)}
+ONE_HIDDEN = {
+    "exp1_mlp4096x262144x1": ([0, 1], 4096),
+}
+
+
+def make_one_hidden(name, inputs, n_sample):
+    wl = make_workload(name)
+    n1 = wl.net.nodes[0].W.shape[0]
+    rng = np.random.default_rng(2025)
+    idx = np.sort(rng.choice(n1, n_sample, replace=False))
+    out = {"inputs": np.array(inputs), "idx": idx}
+    for b in inputs:
+        t = time.time()
+        lb, ub, l, u = oracle.crown_one_hidden(wl.net, wl.x0[b], wl.eps, wl.C[b])
+        out[f"lb_{b}"], out[f"ub_{b}"] = lb, ub
+        out[f"l_{b}"], out[f"u_{b}"] = l[idx], u[idx]
+        print(f"{name} input {b}: {time.time() - t:.1f} s", flush=True)
+    path = os.path.join(HERE, f"{name}.npz")
+    np.savez_compressed(path, **out)
+    print("wrote", path)
+
+
 def make_bab_splits():
     from workloads import draw_splits
     wl = make_workload("bab_mlp784x1024x6")
@@ -87,9 +113,11 @@ def make_bab_splits():
 
 
 if __name__ == "__main__":
-    names = sys.argv[1:] or list(GOLDENS) + ["bab"] + [f"{k}_sampled" for k in SAMPLED]
+    names = sys.argv[1:] or list(GOLDENS) + ["bab"] + [f"{k}_sampled" for k in SAMPLED] + list(ONE_HIDDEN)
     for n in names:
-        if n == "bab":
+        if n in ONE_HIDDEN:
+            make_one_hidden(n, *ONE_HIDDEN[n])
+        elif n == "bab":
             make_bab_splits()
         elif n.endswith("_sampled"):
             make_sampled(n[:-len("_sampled")], *SAMPLED[n[:-len("_sampled")]])

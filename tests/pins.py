@@ -558,7 +558,29 @@ def pin_sampled_equals_full(o):
 
 
 # fastest first (the mutant test stops at the first pin that fails)
+def pin_one_hidden_equals_crown(o):
+    """The row-block computation for one hidden layer gives the full oracle's bounds (blocks
+    smaller than the layer, and a one-output property C = [[1]])."""
+    from workloads.gen import mlp_net
+    for seed, dims, eps, chunk in [(91, [6, 40, 3], 0.2, 7), (92, [20, 300, 5], 0.05, 64), (93, [64, 2000, 1], 0.01, 300)]:
+        if dims[-1] > 1:
+            wl = random_mlp(seed, dims, 2, eps)
+            net, x0, C = wl.net, wl.x0[0], wl.C[0]
+        else:
+            rng = np.random.default_rng(seed)
+            net = mlp_net(rng, dims)
+            x0 = rng.random(dims[0]).astype(np.float32)
+            C = np.ones((1, 1), np.float32)
+        ref = o.crown(net, x0, np.float32(eps), C)
+        lb, ub, l, u = o.crown_one_hidden(net, x0, np.float32(eps), C, chunk=chunk)
+        np.testing.assert_allclose(lb, ref.lb, rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(ub, ref.ub, rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(l, ref.layer_l[1], rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(u, ref.layer_u[1], rtol=1e-12, atol=1e-12)
+
+
 ALL_PINS = [
+    pin_one_hidden_equals_crown,
     pin_relu_hand_values, pin_relu_net_bounds, pin_single_affine, pin_paper_wrapping_example,
     pin_wrapping_example_intermediate, pin_all_stable, pin_inactive_layer_constant, pin_eps_zero,
     pin_residual_closed_form, pin_ibp_sound_and_contains_crown, pin_conv_library,

@@ -97,6 +97,18 @@ def _he_conv(rng, c_out, c_in, k):
     return W, b
 
 
+def _he_dense_f32(rng, d_out, d_in, chunk=8192):
+    """He-normal weights drawn as float32 normals, row block by row block (the 262144 x 4096
+    layer would need 8.6 GB as float64), then the bias as for every other layer."""
+    scale = np.float32(math.sqrt(2.0 / d_in))
+    W = np.empty((d_out, d_in), np.float32)
+    for r0 in range(0, d_out, chunk):
+        r1 = min(d_out, r0 + chunk)
+        W[r0:r1] = rng.standard_normal((r1 - r0, d_in), dtype=np.float32) * scale
+    b = (rng.standard_normal(d_out) * 0.01).astype(np.float32)
+    return W, b
+
+
 def mlp_net(rng, dims) -> Net:
     """ReLU MLP dims[0] -> dims[1] -> ... -> dims[-1]; ReLU after every hidden layer."""
     nodes = []
@@ -272,6 +284,12 @@ WORKLOADS = {
     # branch-and-bound batch on the 784-1024x6-10 network: one root input, 4096 domains
     "bab_mlp784x1024x6": dict(kind="bab", seed=3, net_seed=1, dims=[784] + [1024] * 6 + [10],
                               batch=1, eps=0.02, n_domains=4096, per_domain=8),
+    # the paper's Exp. 1 network (Sec. 4.1): one hidden layer of 262144 on a 4096-dim input,
+    # one output, 2048 inputs, eps 0.01; the property is the output itself (C = [[1]]).
+    # Weights drawn as float32 normals in row blocks (see _he_dense_f32)
+    "exp1_mlp4096x262144x1": dict(kind="exp1", seed=5, dims=[4096, 262144, 1], batch=2048, eps=0.01),
+    # the same shape family small enough for the oracle to bound every input
+    "exp1_mlp1024x16384x1": dict(kind="exp1", seed=51, dims=[1024, 16384, 1], batch=64, eps=0.01),
     # ResNet-style CNN on 3x32x32, 8 inputs, 100 classes
     "resnet3x32x32": dict(kind="resnet", seed=4, batch=8, eps=1.0 / 255.0),
     # the same topology at 3x16x16 with 32/64 channels, FC 64, 10 classes (small enough for
@@ -295,6 +313,17 @@ def make_workload(name: str, batch: int | None = None, **overrides) -> Workload:
         rng = np.random.default_rng(cfg["seed"])
         net = resnet_net(rng, **cfg.get("arch", {}))
         x0 = rng.random((cfg["batch"], net.n_in)).astype(np.float32)
+    elif kind == "exp1":
+        rng = np.random.default_rng(cfg["seed"])
+        d_in, hid, d_out = cfg["dims"]
+        W1, b1 = _he_dense_f32(rng, hid, d_in)
+        W2, b2 = _he_dense_f32(rng, d_out, hid)
+        net = Net((d_in,), [Node("dense", -1, W=W1, b=b1), Node("relu", 0), Node("dense", 1, W=W2, b=b2)])
+        x0 = rng.random((cfg["batch"], d_in)).astype(np.float32)
+        if batch is not None:
+            x0 = x0[:batch]
+        C = np.ones((x0.shape[0], 1, 1), np.float32)
+        return Workload(name, net, x0, np.float32(cfg["eps"]), C, (0.0, 1.0), rng)
     elif kind == "bab":
         net = mlp_net(np.random.default_rng(cfg["net_seed"]), cfg["dims"])
         rng = np.random.default_rng(cfg["seed"])
