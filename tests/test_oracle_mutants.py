@@ -7,7 +7,7 @@ import types
 
 import pytest
 
-from tests import pins, pins_alpha
+from tests import pins, pins_alpha, pins_beta
 
 ORACLE_DIR = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "oracle")
 SRC = os.path.join(ORACLE_DIR, "crown64.py")
@@ -92,6 +92,38 @@ def _alpha_mutant(old, new):
 def test_alpha_mutant_is_caught(name):
     mod = _alpha_mutant(*ALPHA_MUTANTS[name])
     for pin in pins_alpha.ALPHA_PINS:
+        try:
+            pin(mod)
+        except Exception:
+            return
+    pytest.fail(f"mutant {name} passed every pin")
+
+
+SRC_BETA = os.path.join(ORACLE_DIR, "beta64.py")
+BETA_MUTANTS = {
+    "beta_term_dropped": ("A[:, j] += (-S if upper else S) * beta[:, e]", "A[:, j] += 0.0 * beta[:, e]"),
+    "beta_term_sign_flipped": ("A[:, j] += (-S if upper else S) * beta[:, e]", "A[:, j] += (S if upper else -S) * beta[:, e]"),
+    "beta_grad_sign_flipped": ("gb[:, e] = (-S if upper else S) * D[:, j]", "gb[:, e] = (S if upper else -S) * D[:, j]"),
+    "beta_not_projected": ('bl = adam("bl", bl, gbl, 1.0, lr_beta, 0.0, np.inf)', 'bl = adam("bl", bl, gbl, 1.0, lr_beta, -np.inf, np.inf)'),
+    "beta_split_sign_ignored": ("(ids[int(r)], int(j), -1.0 if sg > 0 else 1.0)", "(ids[int(r)], int(j), 1.0)"),
+    "bab_branches_same_neuron": ("nxt = next((o for o in order if o not in used), None)", "nxt = order[0] if order else None"),
+    "bab_keeps_verified": ("if np.all(r.lb > 0.0):\n                pruned += 1", "if False:\n                pruned += 1"),
+}
+
+
+def _beta_mutant(old, new):
+    src = open(SRC_BETA).read()
+    assert src.count(old) >= 1, f"mutation anchor missing: {old!r}"
+    mod = types.ModuleType("beta_mutant")
+    sys.modules["beta_mutant"] = mod
+    exec(compile(src.replace(old, new), "beta_mutant", "exec"), mod.__dict__)
+    return mod
+
+
+@pytest.mark.parametrize("name", sorted(BETA_MUTANTS))
+def test_beta_mutant_is_caught(name):
+    mod = _beta_mutant(*BETA_MUTANTS[name])
+    for pin in pins_beta.BETA_PINS:
         try:
             pin(mod)
         except Exception:

@@ -3,8 +3,8 @@ sandwiches, library convolutions, soundness, finite differences).  CPU only."""
 import pytest
 
 import oracle
-from oracle import alpha64
-from tests import pins, pins_alpha
+from oracle import alpha64, beta64
+from tests import pins, pins_alpha, pins_beta
 
 
 @pytest.mark.parametrize("pin", pins.ALL_PINS, ids=lambda p: p.__name__)
@@ -15,3 +15,8 @@ def test_pin(pin):
 @pytest.mark.parametrize("pin", pins_alpha.ALPHA_PINS, ids=lambda p: p.__name__)
 def test_alpha_pin(pin):
     pin(alpha64)
+
+
+@pytest.mark.parametrize("pin", pins_beta.BETA_PINS, ids=lambda p: p.__name__)
+def test_beta_pin(pin):
+    pin(beta64)
