@@ -78,6 +78,7 @@ typedef struct {
  *   neuron[...]                flat index into that ReLU's tensor;
  *   sign[...]                  +1: the pre-activation is fixed to z >= 0 (active),
  *                              -1: fixed to z <= 0 (inactive).
+ * A split slot with relu_id -1 is unused (skipped).
  * A domain's intermediate bounds are the root pass's, with each split neuron's interval
  * clamped (l <- max(l, 0) for +1, u <- min(u, 0) for -1).  A domain whose clamped interval
  * is empty (l > u) is infeasible and gets lb = +inf, ub = -inf (not an error).  A domain
@@ -208,6 +209,60 @@ vcr_status vcr_alpha_crown_bounds(vcr_ctx *ctx, const float *x0, int32_t B, floa
 
 /* Number of ReLU neurons over all ReLU nodes of the loaded network (n_total above). */
 int64_t vcr_relu_neurons(const vcr_ctx *ctx);
+
+/* beta-CROWN on branch-and-bound subdomains (paper, Sec. 2.1, Alpha-Beta-CROWN): every split
+ * g <= 0 (g = -z for an active split, g = z for an inactive one) enters the bound of its
+ * subdomain with a multiplier beta >= 0 (f + beta g for a lower bound, f - beta g for an upper
+ * one), one per (split, specification bound); the multipliers and the lower slopes alpha
+ * (as in vcr_alpha_crown_bounds) are optimised jointly by projected Adam steps, and each bound
+ * is the best one evaluated (the first evaluation is CROWN's, as vcr_crown_bounds with the
+ * same splits).  Intermediate bounds: the root's full CROWN, with each split neuron's interval
+ * clamped.  Networks of dense and relu nodes. */
+typedef struct {
+  int32_t iters;            /* optimisation steps after the first evaluation (>= 0) */
+  float lr_alpha, lr_beta;  /* Adam step sizes (> 0) */
+  float beta1, beta2;       /* Adam moment decays, in [0, 1) */
+  float adam_eps;           /* Adam denominator guard (> 0) */
+  float *lb_hist, *ub_hist; /* device [iters + 1][n_domains][m] each, or NULL */
+} vcr_beta_opts;
+
+/* x0 (1, n0) and C (1, m, n_out) as in vcr_crown_bounds with splits; lb, ub (n_domains, m).
+ * A split slot with relu_id -1 is unused (subdomains of different depths in one array). */
+vcr_status vcr_beta_crown_bounds(vcr_ctx *ctx, const float *x0, float eps, const float *C, int32_t m,
+                                 const vcr_splits *splits, const vcr_beta_opts *opts,
+                                 float *lb, float *ub);
+
+/* Fixed-batch branch-and-bound (paper, Sec. 2.1 complete verification; Sec. 3.4.4: a fixed
+ * number of subdomains per round, no early stop) on the property C f(x) > 0 for every row of
+ * C over the eps-ball around x0.  The root is bounded by alpha-CROWN; unverified subdomains
+ * wait first-in first-out; each round takes up to `batch` of them, splits each on the first
+ * neuron of the priority order that it has not split yet into an active and an inactive
+ * child, bounds the children with beta-CROWN and keeps those with a non-positive lower bound
+ * (infeasible children are dropped).  Verified when no subdomain is left; otherwise unknown
+ * after max_rounds, or when a subdomain has no neuron left to split. */
+typedef struct {
+  int32_t batch;            /* subdomains split per round (>= 1) */
+  int32_t max_rounds;       /* >= 0 */
+  vcr_beta_opts bound;      /* bounding of the root and of every subdomain (hist ignored) */
+  const int32_t *order_relu;    /* host [order_len]: split priority (ReLU node position,  */
+  const int32_t *order_neuron;  /* neuron), or NULL: the root's unstable neurons by        */
+  int32_t order_len;            /* decreasing chord intercept -u l / (u - l)               */
+} vcr_bab_opts;
+
+typedef struct {
+  int32_t verified;         /* 1: the property holds on the whole ball */
+  int32_t rounds;           /* rounds run */
+  int64_t evaluated;        /* subdomains bounded (the root not counted) */
+  int64_t remaining;        /* unverified subdomains left */
+  float root_min_lb;        /* smallest lower bound of the root (alpha-CROWN) */
+  float worst_lb;           /* smallest lower bound over the remaining subdomains (+inf if none) */
+} vcr_bab_result;
+
+/* x0, C device as above (one input).  round_log: host [max_rounds][4] or NULL, per round
+ * (subdomains taken, children bounded, children verified, subdomains left).  Synchronises
+ * once per round. */
+vcr_status vcr_bab_verify(vcr_ctx *ctx, const float *x0, float eps, const float *C, int32_t m,
+                          const vcr_bab_opts *opts, vcr_bab_result *result, int64_t *round_log);
 
 /* Pre-activation bounds of ReLU node `relu_id` (0-based among ReLU nodes) from the last
  * CROWN call, for every input: l, u device (B, numel).  Queued on the stream. */

@@ -127,18 +127,66 @@ hipError_t launch_alpha_adam(const AlphaLayer &l, int32_t rows, int32_t rows_per
   return hipGetLastError();
 }
 
-__global__ void k_alpha_final(const float *best_val, int32_t units, int32_t m, float *lb, float *ub) {
+__global__ void k_alpha_final(const float *best_val, int32_t units, int32_t m, const int32_t *unit_flags, float *lb,
+                              float *ub) {
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= (int64_t)units * m) return;
   const int64_t u = idx / m;
   const int64_t q = idx - u * m;
-  lb[idx] = best_val[u * 2 * m + q];
-  ub[idx] = -best_val[u * 2 * m + m + q];
+  float l = best_val[u * 2 * m + q], h = -best_val[u * 2 * m + m + q];
+  const int32_t f = unit_flags ? unit_flags[u] : 0;
+  if (f == 1) {
+    l = INFINITY;
+    h = -INFINITY;
+  } else if (f == 2) {
+    l = h = NAN;
+  }
+  lb[idx] = l;
+  ub[idx] = h;
 }
 
-hipError_t launch_alpha_final(const float *best_val, int32_t units, int32_t m, float *lb, float *ub, hipStream_t s) {
+hipError_t launch_alpha_final(const float *best_val, int32_t units, int32_t m, const int32_t *unit_flags, float *lb,
+                              float *ub, hipStream_t s) {
   const int64_t n = (int64_t)units * m;
-  hipLaunchKernelGGL(k_alpha_final, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, best_val, units, m, lb, ub);
+  hipLaunchKernelGGL(k_alpha_final, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, best_val, units, m,
+                     unit_flags, lb, ub);
+  return hipGetLastError();
+}
+
+__global__ void k_beta_init(BetaState b, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  b.beta[i] = 0.f;
+  b.mom[i] = 0.f;
+  b.vel[i] = 0.f;
+  b.grad[i] = 0.f;
+}
+
+hipError_t launch_beta_init(const BetaState &b, int32_t rows_pad, hipStream_t s) {
+  const int64_t n = (int64_t)rows_pad * b.S;
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_beta_init, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, b, n);
+  return hipGetLastError();
+}
+
+__global__ void k_beta_adam(BetaState b, int64_t n, float lr, float beta1, float beta2, float eps, float c1,
+                            float c2) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const float g = b.grad[i];   // 0 for unused slots (never written)
+  const float mo = beta1 * b.mom[i] + (1.f - beta1) * g;
+  const float ve = beta2 * b.vel[i] + (1.f - beta2) * g * g;
+  b.mom[i] = mo;
+  b.vel[i] = ve;
+  b.beta[i] = fmaxf(b.beta[i] + lr * (mo * c1) / (sqrtf(ve * c2) + eps), 0.f);
+}
+
+hipError_t launch_beta_adam(const BetaState &b, int32_t rows, float lr, float beta1, float beta2, float eps,
+                            float c1, float c2, hipStream_t s) {
+  const int64_t n = (int64_t)rows * b.S;
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_beta_adam, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, b, n, lr, beta1, beta2, eps, c1,
+                     c2);
   return hipGetLastError();
 }
 

@@ -24,6 +24,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <deque>
 #include <string>
 #include <vector>
 
@@ -280,6 +281,7 @@ void vcr_destroy(vcr_ctx *c) {
     free_layers(c);
     free_ws(c);
     if (c->d_counters) (void)hipFree(c->d_counters);
+    if (c->bab_buf) (void)hipFree(c->bab_buf);
     for (auto e : c->ev_pool) (void)hipEventDestroy(e);
     if (c->gexec) (void)hipGraphExecDestroy(c->gexec);
     if (c->cap_stream) (void)hipStreamDestroy(c->cap_stream);
@@ -455,6 +457,8 @@ struct CallBufs {
   float *pre0, *best_val;
   int32_t *flag;
   float *tmp_c, *tmp_r;   // ReLU'd IBP inputs of large layers
+  // beta-CROWN multipliers of the split entries [rows][S] and their Adam state
+  float *mul, *mul_mom, *mul_vel, *mul_grad;
 };
 
 vcr_status check_common(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m,
@@ -579,6 +583,13 @@ void carve(const vcr_ctx *c, Workspace &w, const Plan &p, int32_t S, CallBufs *b
     bf->pre0 = take<float>(w, (size_t)ra * ld0);
     bf->best_val = take<float>(w, (size_t)ra);
     bf->flag = take<int32_t>(w, (size_t)ra);
+    bf->mul = bf->mul_mom = bf->mul_vel = bf->mul_grad = nullptr;
+    if (p.D > 0 && S > 0) {
+      bf->mul = take<float>(w, (size_t)ra * S);
+      bf->mul_mom = take<float>(w, (size_t)ra * S);
+      bf->mul_vel = take<float>(w, (size_t)ra * S);
+      bf->mul_grad = take<float>(w, (size_t)ra * S);
+    }
   }
   bf->A[0] = take<float>(w, (size_t)mp * std::max<int64_t>(ldmax, 1));
   bf->A[1] = take<float>(w, (size_t)mp * std::max<int64_t>(ldmax, 1));
@@ -665,64 +676,88 @@ vcr_status run_chain(vcr_ctx *c, CallBufs &bf, int top, int32_t M, int32_t rows_
 struct AlphaCall {
   vcr_alpha_opts o;
   int64_t n_total;
+  float lr_beta = 0.f;   // subdomains (beta-CROWN): step size of the multipliers
 };
 
-// alpha-CROWN final pass over every input chunk (after the intermediate bounds are fixed):
-// evaluate the bounds with the current slopes (backward chain with per-row slopes, keeping
-// the coefficients before each relaxation), keep each row's best, then the gradient pass
-// (the relaxed network forward from each row's box vertex) and one Adam step.
-vcr_status alpha_spec(vcr_ctx *c, CallBufs &bf, const Plan &p, const AlphaCall &ac, int32_t B, int32_t m,
-                      float *lb, float *ub, uint64_t *flops, int32_t *chunks) {
+// alpha-CROWN final pass (after the intermediate bounds are fixed) over every chunk of units:
+// inputs, or subdomains of the root input (beta-CROWN: each split adds a multiplier).  Each
+// step evaluates the bounds with the current slopes and multipliers (backward chain with
+// per-row slopes and split terms, keeping the coefficients before each relaxation), keeps
+// each row's best, then runs the gradient pass (the relaxed network forward from each row's
+// box vertex) and one projected Adam step on both.
+vcr_status alpha_spec(vcr_ctx *c, CallBufs &bf, const Plan &p, const AlphaCall &ac, int32_t units, int32_t m,
+                      int32_t S, float *lb, float *ub, uint64_t *flops, int32_t *chunks) {
   const int L = (int)c->layers.size();
   const int R = L - 1;
+  const bool dom = p.D > 0;   // subdomains of one root input (shared relaxation, split table)
   const DenseLayer &WL = c->layers[L - 1];
   const int64_t ld0 = ld_of(c->n0);
   hipStream_t s = c->stream;
   const vcr_alpha_opts &o = ac.o;
-  for (int32_t u0 = 0; u0 < B; u0 += p.chunk_units) {
-    const int32_t uc = std::min(p.chunk_units, B - u0);
+  const int Rn = (int)c->relu_n.size();
+  for (int32_t u0 = 0; u0 < units; u0 += p.chunk_units) {
+    const int32_t uc = std::min(p.chunk_units, units - u0);
     const int32_t rpu = 2 * m;
     const int32_t M = rpu * uc;
     const int32_t M_pad = (int32_t)rows_pad(M);
+    // per-unit parameters (inputs) or the root's for every row (subdomains)
+    const int32_t prpu = dom ? M_pad : rpu;
+    const int64_t pu0 = dom ? 0 : u0;
+    const int32_t pun = dom ? 1 : uc;
+    SplitTable tab{};
+    BetaState bs{bf.mul, bf.mul_mom, bf.mul_vel, bf.mul_grad, S};
+    if (dom) {
+      tab.off = bf.off + (int64_t)u0 * (Rn + 1);
+      tab.ent_n = bf.ent_n + (int64_t)u0 * S;
+      tab.ent_p = bf.ent_p + (int64_t)u0 * S;
+      tab.R = Rn;
+      tab.S = S;
+      tab.D = uc;
+      tab.rows_per_domain = rpu;
+      tab.beta = S > 0 ? bf.mul : nullptr;
+      HIP_TRY(c, launch_beta_init(bs, M_pad, s));
+    }
     std::vector<AlphaLayer> al = bf.al;
     for (int r = 0; r < R; ++r) {
-      al[r].P = bf.P[r] + (int64_t)u0 * al[r].ld;
+      al[r].P = bf.P[r] + pu0 * al[r].ld;
       HIP_TRY(c, launch_alpha_init(al[r], o.alpha_init ? o.alpha_init + (int64_t)u0 * rpu * ac.n_total : nullptr,
-                                   ac.n_total, M, M_pad, rpu, s));
+                                   ac.n_total, M, M_pad, prpu, s));
     }
     for (int32_t t = 0; t <= o.iters; ++t) {
       // evaluate
       InitArgs ia{};
-      ia.src = bf.CW + (int64_t)u0 * m * WL.ld_in;
+      ia.src = bf.CW + (dom ? 0 : (int64_t)u0 * m * WL.ld_in);
       ia.ld_src = WL.ld_in;
       ia.n_src = m;
-      ia.per_unit_src = 1;
-      ia.src_bias = bf.Cb + (int64_t)u0 * m;
+      ia.per_unit_src = dom ? 0 : 1;
+      ia.src_bias = bf.Cb + (dom ? 0 : (int64_t)u0 * m);
       ia.n_cols = WL.n_in;
       ia.ldo = WL.ld_in;
       ia.M = M;
       ia.units = uc;
       ia.P = al[R - 1].P;
       ia.ldp = WL.ld_in;
-      ia.param_per_unit = 1;
+      ia.param_per_unit = dom ? 0 : 1;
       ia.relu_index = R - 1;
+      ia.splits = tab;
       ia.out = bf.A[0];
       ia.beta = bf.beta;
       ia.alpha = al[R - 1].alpha;
       ia.ld_alpha = al[R - 1].ld;
       ia.pre = al[R - 1].pre;
       HIP_TRY(c, launch_init_rows(ia, s));
-      vcr_status st = run_chain(c, bf, L - 1, M, rpu, uc, u0, 1, SplitTable{}, flops, true);
+      vcr_status st = run_chain(c, bf, L - 1, M, rpu, uc, dom ? 0 : u0, dom ? 0 : 1, tab, flops, true);
       if (st != VCR_OK) return st;
       HIP_TRY(c, launch_alpha_best(bf.beta, bf.cpart, (int32_t)(ld0 / PART_COLS), M_pad, M, m, t == 0, bf.best_val,
-                                   bf.flag, o.lb_hist ? o.lb_hist + ((int64_t)t * B + u0) * m : nullptr,
-                                   o.ub_hist ? o.ub_hist + ((int64_t)t * B + u0) * m : nullptr, s));
+                                   bf.flag, o.lb_hist ? o.lb_hist + ((int64_t)t * units + u0) * m : nullptr,
+                                   o.ub_hist ? o.ub_hist + ((int64_t)t * units + u0) * m : nullptr, s));
       for (int r = 0; r < R; ++r) HIP_TRY(c, launch_alpha_keep(al[r], bf.flag, M, s));
       const bool step = t < o.iters;
       if (!step && !o.grad_out) break;
       // gradient: E_0 = the row's box vertex, then E_k = line_k(W_k E_{k-1} + b_k)
-      HIP_TRY(c, launch_alpha_vertex(bf.pre0, ld0, bf.c0 + (int64_t)u0 * ld0, bf.r0 + (int64_t)u0 * ld0, M_pad, rpu,
-                                     uc, bf.A[0], s));
+      HIP_TRY(c, launch_alpha_vertex(bf.pre0, ld0, bf.c0 + pu0 * ld0, bf.r0 + pu0 * ld0, M_pad, prpu, pun, bf.A[0], s));
+      SplitTable ftab = tab;
+      ftab.grad_beta = dom && S > 0 ? bf.mul_grad : nullptr;
       for (int k = 1; k <= R; ++k) {
         const DenseLayer &W = c->layers[k - 1];
         GemmArgs g{};
@@ -739,8 +774,10 @@ vcr_status alpha_spec(vcr_ctx *c, CallBufs &bf, const Plan &p, const AlphaCall &
         g.ldo = W.ld_out;
         g.P = al[k - 1].P;
         g.ldp = W.ld_out;
-        g.rows_per_unit = rpu;
-        g.n_units = uc;
+        g.rows_per_unit = prpu;
+        g.n_units = pun;
+        g.relu_index = k - 1;
+        g.splits = ftab;
         g.alpha = al[k - 1].alpha;
         g.ld_alpha = al[k - 1].ld;
         g.pre = al[k - 1].pre;
@@ -755,9 +792,12 @@ vcr_status alpha_spec(vcr_ctx *c, CallBufs &bf, const Plan &p, const AlphaCall &
       const double c1 = 1.0 / (1.0 - std::pow((double)o.beta1, (double)(t + 1)));
       const double c2 = 1.0 / (1.0 - std::pow((double)o.beta2, (double)(t + 1)));
       for (int r = 0; r < R; ++r)
-        HIP_TRY(c, launch_alpha_adam(al[r], M, rpu, o.lr, o.beta1, o.beta2, o.adam_eps, (float)c1, (float)c2, s));
+        HIP_TRY(c, launch_alpha_adam(al[r], M, prpu, o.lr, o.beta1, o.beta2, o.adam_eps, (float)c1, (float)c2, s));
+      if (dom && S > 0)
+        HIP_TRY(c, launch_beta_adam(bs, M, ac.lr_beta, o.beta1, o.beta2, o.adam_eps, (float)c1, (float)c2, s));
     }
-    HIP_TRY(c, launch_alpha_final(bf.best_val, uc, m, lb + (int64_t)u0 * m, ub + (int64_t)u0 * m, s));
+    HIP_TRY(c, launch_alpha_final(bf.best_val, uc, m, dom ? bf.flags + u0 : nullptr, lb + (int64_t)u0 * m,
+                                  ub + (int64_t)u0 * m, s));
     if (o.alpha_out || o.grad_out)
       for (int r = 0; r < R; ++r)
         HIP_TRY(c, launch_alpha_out(al[r], M, m, ac.n_total,
@@ -881,7 +921,7 @@ vcr_status crown_impl(vcr_ctx *c, const float *x0, int32_t B, float eps, const f
   }
   const int32_t units = D > 0 ? D : B;
   if (ac) {
-    st = alpha_spec(c, bf, p, *ac, B, m, lb, ub, &flops, &chunks);
+    st = alpha_spec(c, bf, p, *ac, units, m, S, lb, ub, &flops, &chunks);
     if (st != VCR_OK) return st;
   } else if (L == 1) {
     HIP_TRY(c, launch_spec_direct(bf.CW, WL.ld_in, bf.Cb, B, m, WL.n_in, bf.c0, bf.r0, ld0, 0, lb, ub, s));
@@ -1084,6 +1124,247 @@ vcr_status vcr_alpha_crown_bounds(vcr_ctx *c, const float *x0, int32_t B, float 
   for (int32_t n : c->relu_n) ac.n_total += n;
   if ((int64_t)B * 2 * m * ac.n_total > ((int64_t)1 << 40)) return fail(c, VCR_ERR_SHAPE, "alpha tensors too large");
   return after_call(c, crown_impl(c, x0, B, eps, C, m, nullptr, lb, ub, &ac), t0);
+}
+
+namespace {
+
+vcr_status check_splits(vcr_ctx *c, const vcr_splits *splits, int32_t m) {
+  if (splits->n_domains <= 0 || splits->per_domain < 0 || splits->per_domain > 64)
+    return fail(c, VCR_ERR_ARG, "bad split sizes (n_domains > 0, 0 <= per_domain <= 64)");
+  if (splits->per_domain > 0 && (!splits->relu_id || !splits->neuron || !splits->sign))
+    return fail(c, VCR_ERR_ARG, "null split array");
+  if (c->relu_n.empty()) return fail(c, VCR_ERR_ARG, "splits need at least one ReLU");
+  if ((int64_t)splits->n_domains * m > (int64_t)1 << 30) return fail(c, VCR_ERR_SHAPE, "n_domains * m too large");
+  return VCR_OK;
+}
+
+vcr_status check_beta_opts(vcr_ctx *c, const vcr_beta_opts *o) {
+  if (!o) return fail(c, VCR_ERR_ARG, "null beta options");
+  if (o->iters < 0 || o->iters > 1000000) return fail(c, VCR_ERR_ARG, "iters must be in [0, 1e6]");
+  if (!(o->lr_alpha > 0.f) || !std::isfinite(o->lr_alpha) || !(o->lr_beta > 0.f) || !std::isfinite(o->lr_beta))
+    return fail(c, VCR_ERR_ARG, "lr_alpha and lr_beta must be finite and > 0");
+  if (!(o->beta1 >= 0.f && o->beta1 < 1.f) || !(o->beta2 >= 0.f && o->beta2 < 1.f))
+    return fail(c, VCR_ERR_ARG, "beta1 and beta2 must be in [0, 1)");
+  if (!(o->adam_eps > 0.f) || !std::isfinite(o->adam_eps)) return fail(c, VCR_ERR_ARG, "adam_eps must be finite and > 0");
+  if ((o->lb_hist == nullptr) != (o->ub_hist == nullptr)) return fail(c, VCR_ERR_ARG, "lb_hist and ub_hist go together");
+  return VCR_OK;
+}
+
+AlphaCall alpha_call_of(const vcr_ctx *c, const vcr_beta_opts &b, bool hist) {
+  AlphaCall ac{};
+  ac.o.iters = b.iters;
+  ac.o.lr = b.lr_alpha;
+  ac.o.beta1 = b.beta1;
+  ac.o.beta2 = b.beta2;
+  ac.o.adam_eps = b.adam_eps;
+  if (hist) {
+    ac.o.lb_hist = b.lb_hist;
+    ac.o.ub_hist = b.ub_hist;
+  }
+  for (int32_t n : c->relu_n) ac.n_total += n;
+  ac.lr_beta = b.lr_beta;
+  return ac;
+}
+
+// device memory of one branch-and-bound round (split arrays, bounds), grown on demand
+vcr_status bab_reserve(vcr_ctx *c, size_t bytes) {
+  if (c->bab_cap >= bytes) return VCR_OK;
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  if (c->bab_buf) HIP_TRY(c, hipFree(c->bab_buf));
+  c->bab_buf = nullptr;
+  c->bab_cap = 0;
+  HIP_TRY(c, hipMalloc(&c->bab_buf, bytes));
+  c->bab_cap = bytes;
+  return VCR_OK;
+}
+
+struct Split {
+  int32_t r, j, sg;
+};
+
+}  // namespace
+
+vcr_status vcr_beta_crown_bounds(vcr_ctx *c, const float *x0, float eps, const float *C, int32_t m,
+                                 const vcr_splits *splits, const vcr_beta_opts *opts, float *lb, float *ub) {
+  if (!c) return VCR_ERR_ARG;
+  const auto t0 = std::chrono::steady_clock::now();
+  vcr_status st = check_common(c, x0, 1, eps, C, m, lb, ub);
+  if (st != VCR_OK) return st;
+  if (c->graph) return fail(c, VCR_ERR_UNSUPPORTED, "beta-CROWN is built for networks of dense and relu nodes");
+  if (!splits) return fail(c, VCR_ERR_ARG, "null splits");
+  st = check_splits(c, splits, m);
+  if (st != VCR_OK) return st;
+  st = check_beta_opts(c, opts);
+  if (st != VCR_OK) return st;
+  AlphaCall ac = alpha_call_of(c, *opts, true);
+  return after_call(c, crown_impl(c, x0, 1, eps, C, m, splits, lb, ub, &ac), t0);
+}
+
+vcr_status vcr_bab_verify(vcr_ctx *c, const float *x0, float eps, const float *C, int32_t m, const vcr_bab_opts *opts,
+                          vcr_bab_result *res, int64_t *round_log) {
+  if (!c) return VCR_ERR_ARG;
+  const auto t0 = std::chrono::steady_clock::now();
+  if (!opts || !res) return fail(c, VCR_ERR_ARG, "null options or result");
+  if (!c->loaded) return fail(c, VCR_ERR_STATE, "no network loaded");
+  if (c->graph) return fail(c, VCR_ERR_UNSUPPORTED, "branch and bound is built for networks of dense and relu nodes");
+  if (c->relu_n.empty()) return fail(c, VCR_ERR_ARG, "branch and bound needs at least one ReLU");
+  if (opts->batch < 1 || opts->max_rounds < 0) return fail(c, VCR_ERR_ARG, "batch must be >= 1, max_rounds >= 0");
+  if (m <= 0 || !x0 || !C) return fail(c, VCR_ERR_ARG, "bad property");
+  vcr_status st = check_beta_opts(c, &opts->bound);
+  if (st != VCR_OK) return st;
+  const int R = (int)c->relu_n.size();
+  if (opts->order_len < 0 || (opts->order_len > 0 && (!opts->order_relu || !opts->order_neuron)))
+    return fail(c, VCR_ERR_ARG, "bad split order");
+  for (int32_t k = 0; k < opts->order_len; ++k)
+    if (opts->order_relu[k] < 0 || opts->order_relu[k] >= R || opts->order_neuron[k] < 0 ||
+        opts->order_neuron[k] >= c->relu_n[opts->order_relu[k]])
+      return fail(c, VCR_ERR_ARG, "split order entry %d out of range", k);
+  if (c->device < 0) return fail(c, VCR_ERR_STATE, "validation-only context: no device work");
+  HIP_TRY(c, hipSetDevice(c->device));
+  hipStream_t s = c->stream;
+  *res = vcr_bab_result{};
+  const AlphaCall ac = alpha_call_of(c, opts->bound, false);
+
+  // root: alpha-CROWN
+  st = bab_reserve(c, sizeof(float) * 2 * (size_t)m);
+  if (st != VCR_OK) return st;
+  float *d_lb = static_cast<float *>(c->bab_buf), *d_ub = d_lb + m;
+  st = crown_impl(c, x0, 1, eps, C, m, nullptr, d_lb, d_ub, &ac);
+  if (st != VCR_OK) return st;
+  std::vector<float> h_lb(m);
+  HIP_TRY(c, hipMemcpyAsync(h_lb.data(), d_lb, sizeof(float) * m, hipMemcpyDeviceToHost, s));
+  // the split order: given, or the root's unstable neurons by decreasing chord intercept
+  std::vector<std::pair<int32_t, int32_t>> order;
+  if (opts->order_len > 0) {
+    for (int32_t k = 0; k < opts->order_len; ++k) order.emplace_back(opts->order_relu[k], opts->order_neuron[k]);
+  } else {
+    struct Cand {
+      double score;
+      int32_t r, j;
+    };
+    std::vector<Cand> cand;
+    for (int r = 0; r < R; ++r) {
+      const int32_t n = c->relu_n[r];
+      std::vector<float> l(n), u(n);
+      HIP_TRY(c, hipMemcpyAsync(l.data(), c->lastL[r], sizeof(float) * n, hipMemcpyDeviceToHost, s));
+      HIP_TRY(c, hipMemcpyAsync(u.data(), c->lastU[r], sizeof(float) * n, hipMemcpyDeviceToHost, s));
+      HIP_TRY(c, hipStreamSynchronize(s));
+      for (int32_t j = 0; j < n; ++j)
+        if (l[j] < 0.f && u[j] > 0.f) cand.push_back({-(double)u[j] * (double)l[j] / ((double)u[j] - (double)l[j]), r, j});
+    }
+    std::stable_sort(cand.begin(), cand.end(), [](const Cand &a, const Cand &b) { return a.score > b.score; });
+    for (const Cand &k : cand) order.emplace_back(k.r, k.j);
+  }
+  HIP_TRY(c, hipStreamSynchronize(s));
+  float root_min = INFINITY;
+  for (float v : h_lb) root_min = std::min(root_min, v);
+  res->root_min_lb = root_min;
+  bool all_pos = true;
+  for (float v : h_lb) all_pos = all_pos && v > 0.f;
+  if (all_pos) {
+    res->verified = 1;
+    res->worst_lb = INFINITY;
+    c->ms_last = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+    return VCR_OK;
+  }
+  std::deque<std::vector<Split>> queue;
+  std::deque<float> queue_lb;
+  queue.emplace_back();
+  queue_lb.push_back(root_min);
+  for (int32_t rnd = 0; rnd < opts->max_rounds && !queue.empty(); ++rnd) {
+    const size_t take = std::min<size_t>((size_t)opts->batch, queue.size());
+    std::vector<std::vector<Split>> kids;
+    bool stuck = false;
+    for (size_t k = 0; k < take; ++k) {
+      std::vector<Split> dom = std::move(queue.front());
+      const float dlb = queue_lb.front();
+      queue.pop_front();
+      queue_lb.pop_front();
+      const std::pair<int32_t, int32_t> *nxt = nullptr;
+      for (const auto &o : order) {
+        bool used = false;
+        for (const Split &q : dom) used = used || (q.r == o.first && q.j == o.second);
+        if (!used) {
+          nxt = &o;
+          break;
+        }
+      }
+      if (!nxt) {   // nothing left to split: stays unverified
+        stuck = true;
+        queue.push_back(std::move(dom));
+        queue_lb.push_back(dlb);
+        continue;
+      }
+      for (int sg : {1, -1}) {
+        std::vector<Split> ch = dom;
+        ch.push_back({nxt->first, nxt->second, sg});
+        kids.push_back(std::move(ch));
+      }
+    }
+    int64_t pruned = 0;
+    if (!kids.empty()) {
+      const int32_t D = (int32_t)kids.size();
+      int32_t S = 0;
+      for (const auto &k : kids) S = std::max<int32_t>(S, (int32_t)k.size());
+      std::vector<int32_t> hr((size_t)D * S, -1), hn((size_t)D * S, 0);
+      std::vector<int8_t> hs((size_t)D * S, 1);
+      for (int32_t d = 0; d < D; ++d)
+        for (size_t e = 0; e < kids[d].size(); ++e) {
+          hr[(size_t)d * S + e] = kids[d][e].r;
+          hn[(size_t)d * S + e] = kids[d][e].j;
+          hs[(size_t)d * S + e] = (int8_t)kids[d][e].sg;
+        }
+      const size_t nb = (size_t)D * S;
+      const size_t off_n = al(sizeof(int32_t) * nb), off_s = off_n + al(sizeof(int32_t) * nb);
+      const size_t off_lb = off_s + al(nb), off_ub = off_lb + al(sizeof(float) * D * m);
+      st = bab_reserve(c, off_ub + al(sizeof(float) * D * m));
+      if (st != VCR_OK) return st;
+      char *base = static_cast<char *>(c->bab_buf);
+      int32_t *d_r = reinterpret_cast<int32_t *>(base), *d_n = reinterpret_cast<int32_t *>(base + off_n);
+      int8_t *d_s = reinterpret_cast<int8_t *>(base + off_s);
+      float *k_lb = reinterpret_cast<float *>(base + off_lb), *k_ub = reinterpret_cast<float *>(base + off_ub);
+      HIP_TRY(c, hipMemcpyAsync(d_r, hr.data(), sizeof(int32_t) * nb, hipMemcpyHostToDevice, s));
+      HIP_TRY(c, hipMemcpyAsync(d_n, hn.data(), sizeof(int32_t) * nb, hipMemcpyHostToDevice, s));
+      HIP_TRY(c, hipMemcpyAsync(d_s, hs.data(), nb, hipMemcpyHostToDevice, s));
+      vcr_splits sp{D, S, d_r, d_n, d_s};
+      st = crown_impl(c, x0, 1, eps, C, m, &sp, k_lb, k_ub, &ac);
+      if (st != VCR_OK) return st;
+      std::vector<float> kl((size_t)D * m);
+      HIP_TRY(c, hipMemcpyAsync(kl.data(), k_lb, sizeof(float) * D * m, hipMemcpyDeviceToHost, s));
+      HIP_TRY(c, hipStreamSynchronize(s));
+      for (int32_t d = 0; d < D; ++d) {
+        bool ok = true;
+        float mn = INFINITY;
+        for (int32_t q = 0; q < m; ++q) {
+          const float v = kl[(size_t)d * m + q];
+          if (std::isnan(v)) return fail(c, VCR_ERR_DEVICE, "internal: NaN bound of a subdomain");
+          ok = ok && v > 0.f;
+          mn = std::min(mn, v);
+        }
+        if (ok) {
+          ++pruned;
+        } else {
+          queue.push_back(std::move(kids[d]));
+          queue_lb.push_back(mn);
+        }
+      }
+      res->evaluated += D;
+    }
+    res->rounds = rnd + 1;
+    if (round_log) {
+      round_log[4 * rnd + 0] = (int64_t)take;
+      round_log[4 * rnd + 1] = (int64_t)kids.size();
+      round_log[4 * rnd + 2] = pruned;
+      round_log[4 * rnd + 3] = (int64_t)queue.size();
+    }
+    if (stuck && kids.empty()) break;
+  }
+  res->remaining = (int64_t)queue.size();
+  res->verified = queue.empty() ? 1 : 0;
+  res->worst_lb = INFINITY;
+  for (float v : queue_lb) res->worst_lb = std::min(res->worst_lb, v);
+  c->ms_last = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+  return VCR_OK;
 }
 
 int64_t vcr_relu_neurons(const vcr_ctx *c) {

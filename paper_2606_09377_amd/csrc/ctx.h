@@ -63,6 +63,10 @@ struct vcr_ctx {
   int32_t last_B = 0;
   std::vector<float *> lastL, lastU;
   int32_t *d_counters = nullptr;    // [64] unstable counts + [1] invalid domains
+  // branch-and-bound loop: device split arrays and bounds of one round (outside the
+  // workspace, which every bounding call carves anew)
+  void *bab_buf = nullptr;
+  size_t bab_cap = 0;
   bool last_had_splits = false;
   double ms_last = 0.0;
   uint64_t flops_last = 0;

@@ -236,7 +236,8 @@ hipError_t launch_layer_from_ibp(const float *c, const float *r, int64_t ld, int
 // (d ? -1 : 1) * src_bias[i]; the ReLU just below is relaxed with the lower rule and its
 // constants (relaxation intercepts and the bias of the dense layer below) are added.  One
 // wavefront per row; padding rows are zero.
-__device__ __forceinline__ float4 init_override(const SplitTable &st, int d, int relu, int col, float4 prm) {
+__device__ __forceinline__ float4 init_override(const SplitTable &st, int d, int relu, int col, float4 prm,
+                                                int *ent, float *sterm) {
   const int e0 = st.off[d * (st.R + 1) + relu];
   const int e1 = st.off[d * (st.R + 1) + relu + 1];
   for (int e = e0; e < e1; ++e) {
@@ -245,6 +246,8 @@ __device__ __forceinline__ float4 init_override(const SplitTable &st, int d, int
       prm.x = q.x;
       prm.y = q.y;
       prm.z = q.z;
+      *ent = e;
+      *sterm = q.w;
     }
   }
   return prm;
@@ -281,11 +284,14 @@ __global__ __launch_bounds__(256) void k_init_rows(const InitArgs a, int32_t M_p
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       float4 prm = P[c + e];
-      if (has_splits) prm = init_override(a.splits, u, a.relu_index, (int)(c + e), prm);
+      int ent = -1;
+      float sterm = 0.f;
+      if (has_splits) prm = init_override(a.splits, u, a.relu_index, (int)(c + e), prm, &ent, &sterm);
       const float x = sgn * wv[e];
       float lam = prm.x;
       if (a.alpha && prm.z > 0.f) lam = a.alpha[row * a.ld_alpha + c + e];
-      const float ap = x > 0.f ? x * lam : x * prm.y;
+      float ap = x > 0.f ? x * lam : x * prm.y;
+      if (ent >= 0 && a.splits.beta) ap += a.splits.beta[row * a.splits.S + ent] * sterm;
       acc += fminf(x, 0.f) * prm.z + ap * prm.w;
       ov[e] = ap;
     }
@@ -486,6 +492,7 @@ __global__ void k_split_prepare(const SplitPrepArgs a) {
     const int r = a.relu_id[(int64_t)d * a.S + k];
     const int j = a.neuron[(int64_t)d * a.S + k];
     const int sg = a.sign[(int64_t)d * a.S + k];
+    if (r == -1) continue;   // an unused slot
     if (r < 0 || r >= a.R || (sg != 1 && sg != -1)) {
       invalid = true;
       break;
@@ -530,7 +537,13 @@ __global__ void k_split_prepare(const SplitPrepArgs a) {
       u = fminf(u, 0.f);
     if (l > u) infeasible = true;
     a.ent_n[(int64_t)d * a.S + k] = en[k];
-    a.ent_p[(int64_t)d * a.S + k] = relax_params(l, u, 0.f);
+    float4 q = relax_params(l, u, 0.f);
+    q.w = es[k] > 0 ? -1.f : 1.f;   // sign of the split's Lagrangian term
+    a.ent_p[(int64_t)d * a.S + k] = q;
+  }
+  for (int k = cnt; k < a.S; ++k) {   // unused slots (never matched: off[] ends at cnt)
+    a.ent_n[(int64_t)d * a.S + k] = -1;
+    a.ent_p[(int64_t)d * a.S + k] = make_float4(0.f, 0.f, 0.f, 0.f);
   }
   a.flags[d] = infeasible ? 1 : 0;
 }

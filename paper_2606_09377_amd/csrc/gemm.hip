@@ -60,7 +60,10 @@ __device__ __forceinline__ void map_tile(int bid, int G, int n_mt, int n_nt, int
   nt = idx / gm;
 }
 
-__device__ __forceinline__ float4 split_override(const SplitTable &st, int row, int relu, int n, float4 prm) {
+// The split entry of (the row's domain, relu, neuron n), if any: its relaxation replaces
+// (lam, s, t); *ent receives the entry index and *sterm its Lagrangian sign.
+__device__ __forceinline__ float4 split_override(const SplitTable &st, int row, int relu, int n, float4 prm,
+                                                 int *ent = nullptr, float *sterm = nullptr) {
   int d = row / st.rows_per_domain;
   d = d < st.D ? d : st.D - 1;
   const int e0 = st.off[d * (st.R + 1) + relu];
@@ -71,6 +74,10 @@ __device__ __forceinline__ float4 split_override(const SplitTable &st, int row, 
       prm.x = q.x;
       prm.y = q.y;
       prm.z = q.z;
+      if (ent) {
+        *ent = e;
+        *sterm = q.w;
+      }
     }
   }
   return prm;
@@ -234,10 +241,14 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm(const GemmArgs p) {
             u = u < p.n_units ? u : p.n_units - 1;
             prm = p.P[(int64_t)u * p.ldp + n];
           }
+          int ent = -1;
+          float sterm = 0.f;
+          if (has_splits) prm = split_override(p.splits, row, p.relu_index, n, prm, &ent, &sterm);
           const bool unst = prm.z > 0.f;
           const float lam = unst ? alpha_t[off] : prm.x;
           const float an = pre_t[off];
           const float D = acc[bi][bj][v] + prm.w;
+          if (ent >= 0 && p.splits.grad_beta) p.splits.grad_beta[(int64_t)row * p.splits.S + ent] = sterm * D;
           const float E = an > 0.f ? lam * D : prm.y * D + (an < 0.f ? prm.z : 0.f);
           out_t[off] = E;
           grad_t[off] = (unst && an > 0.f) ? an * D : 0.f;
@@ -259,13 +270,23 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm(const GemmArgs p) {
             u = u < p.n_units ? u : p.n_units - 1;
             prm = p.P[(int64_t)u * p.ldp + n];
           }
-          if (has_splits) prm = split_override(p.splits, row, p.relu_index, n, prm);
+          int ent = -1;
+          float sterm = 0.f;
+          if (has_splits) {
+            if constexpr (AL)
+              prm = split_override(p.splits, row, p.relu_index, n, prm, &ent, &sterm);
+            else
+              prm = split_override(p.splits, row, p.relu_index, n, prm);
+          }
           const float a = acc[bi][bj][v];
           float lam = prm.x;
           if constexpr (AL) {
             if (alpha_t && prm.z > 0.f) lam = alpha_t[off];
           }
-          const float ap = a > 0.f ? a * lam : a * prm.y;
+          float ap = a > 0.f ? a * lam : a * prm.y;
+          if constexpr (AL) {
+            if (ent >= 0 && p.splits.beta) ap += p.splits.beta[(int64_t)row * p.splits.S + ent] * sterm;
+          }
           out_t[off] = ap;
           if constexpr (AL) {
             if (pre_t) pre_t[off] = a;

@@ -21,9 +21,15 @@ inline int64_t rows_pad(int64_t m) { return (m + BM - 1) / BM * BM; }
 struct SplitTable {
   const int32_t *off = nullptr;   // [D][R+1] start of each ReLU's entries in ent_*
   const int32_t *ent_n = nullptr; // [D][S] neuron of each entry (sorted by ReLU)
-  const float4 *ent_p = nullptr;  // [D][S] (lam, s, t, 0) after the split is applied
+  const float4 *ent_p = nullptr;  // [D][S] (lam, s, t, S) after the split is applied; S = -1 for
+                                  // an active split (z >= 0), +1 for an inactive one (z <= 0)
   int32_t R = 0, S = 0, D = 0;
   int32_t rows_per_domain = 0;
+  // beta-CROWN (optional): per-row multipliers of the entries, beta[row * S + e] >= 0; the
+  // term beta S z of each split is added to the coefficient of z; in the forward epilogue
+  // grad_beta[row * S + e] receives S z at the row's vertex
+  const float *beta = nullptr;
+  float *grad_beta = nullptr;
 };
 
 enum EpiMode : int32_t { EPI_RELAX = 0, EPI_CONCRETIZE = 1, EPI_FORWARD = 2, EPI_AFFINE = 3 };
@@ -163,8 +169,19 @@ hipError_t launch_alpha_keep(const AlphaLayer &l, const int32_t *flag, int32_t r
 // one projected Adam step (ascent) at unstable neurons; c1 = 1 / (1 - beta1^t), c2 = 1 / (1 - beta2^t)
 hipError_t launch_alpha_adam(const AlphaLayer &l, int32_t rows, int32_t rows_per_unit, float lr, float beta1,
                              float beta2, float eps, float c1, float c2, hipStream_t s);
-// lb / ub from the best row values
-hipError_t launch_alpha_final(const float *best_val, int32_t units, int32_t m, float *lb, float *ub, hipStream_t s);
+// lb / ub from the best row values; with unit_flags (subdomains): 1 infeasible -> lb = +inf,
+// ub = -inf; 2 invalid splits -> NaN
+hipError_t launch_alpha_final(const float *best_val, int32_t units, int32_t m, const int32_t *unit_flags, float *lb,
+                              float *ub, hipStream_t s);
+// beta-CROWN multipliers [M_pad][S] with their Adam moments and gradient
+struct BetaState {
+  float *beta, *mom, *vel, *grad;
+  int32_t S;
+};
+hipError_t launch_beta_init(const BetaState &b, int32_t rows_pad, hipStream_t s);
+// one projected Adam step (ascent) on the multipliers of real split entries: beta >= 0
+hipError_t launch_beta_adam(const BetaState &b, int32_t rows, float lr, float beta1, float beta2, float eps,
+                            float c1, float c2, hipStream_t s);
 // compact outputs: slopes of the best bound and the last gradient (d ub / d alpha for the
 // upper rows, so the sign of the negated rows is undone)
 hipError_t launch_alpha_out(const AlphaLayer &l, int32_t rows, int32_t m, int64_t n_total, float *alpha_out,

@@ -53,6 +53,22 @@ class VcrAlphaOpts(ctypes.Structure):
                 ("ub_hist", ctypes.c_void_p)]
 
 
+class VcrBetaOpts(ctypes.Structure):
+    _fields_ = [("iters", ctypes.c_int32), ("lr_alpha", ctypes.c_float), ("lr_beta", ctypes.c_float),
+                ("beta1", ctypes.c_float), ("beta2", ctypes.c_float), ("adam_eps", ctypes.c_float),
+                ("lb_hist", ctypes.c_void_p), ("ub_hist", ctypes.c_void_p)]
+
+
+class VcrBabOpts(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("max_rounds", ctypes.c_int32), ("bound", VcrBetaOpts),
+                ("order_relu", ctypes.c_void_p), ("order_neuron", ctypes.c_void_p), ("order_len", ctypes.c_int32)]
+
+
+class VcrBabResult(ctypes.Structure):
+    _fields_ = [("verified", ctypes.c_int32), ("rounds", ctypes.c_int32), ("evaluated", ctypes.c_int64),
+                ("remaining", ctypes.c_int64), ("root_min_lb", ctypes.c_float), ("worst_lb", ctypes.c_float)]
+
+
 class VcrError(RuntimeError):
     def __init__(self, status, msg):
         super().__init__(f"{STATUS_NAMES[status] if 0 <= status < 7 else status}: {msg}")
@@ -86,6 +102,9 @@ def load_library(path: str = LIB_PATH):
         "vcr_get_stats": ([P, ctypes.POINTER(VcrStats)], I32),
         "vcr_alpha_crown_bounds": ([P, P, I32, F32, P, I32, ctypes.POINTER(VcrAlphaOpts), P, P], I32),
         "vcr_relu_neurons": ([P], ctypes.c_int64),
+        "vcr_beta_crown_bounds": ([P, P, F32, P, I32, ctypes.POINTER(VcrSplits), ctypes.POINTER(VcrBetaOpts), P, P],
+                                  I32),
+        "vcr_bab_verify": ([P, P, F32, P, I32, ctypes.POINTER(VcrBabOpts), ctypes.POINTER(VcrBabResult), P], I32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -247,6 +266,62 @@ class Ctx:
         self._check(self.lib.vcr_alpha_crown_bounds(self.h, _ptr(x0), B, ctypes.c_float(float(eps)), _ptr(C), m,
                                                     ctypes.byref(o), _ptr(lb), _ptr(ub)))
         return lb, ub, extra
+
+    def beta_crown_bounds(self, x0, eps, C, splits, iters=20, lr_alpha=0.1, lr_beta=0.05, beta1=0.9, beta2=0.999,
+                          adam_eps=1e-8, want_hist=False):
+        """beta-CROWN bounds of subdomains of one input: x0 (1, n0), C (1, m, n_out) CUDA
+        tensors, splits (relu_id, neuron, sign) (D, S) CUDA tensors (relu_id -1: unused slot).
+        Returns (lb, ub, extra) with lb, ub (D, m); extra "lb_hist", "ub_hist" (iters + 1, D, m)."""
+        import torch
+        m = C.shape[1]
+        _check_tensor(x0, (1, None))
+        _check_tensor(C, (1, m, None))
+        rid, neu, sgn = splits
+        for t, dt in ((rid, torch.int32), (neu, torch.int32), (sgn, torch.int8)):
+            if t.dtype != dt or not t.is_contiguous() or t.shape != rid.shape:
+                raise ValueError("splits must be contiguous (D, S) int32, int32, int8 tensors")
+        D = rid.shape[0]
+        dev = x0.device
+        lb = torch.empty((D, m), dtype=torch.float32, device=dev)
+        ub = torch.empty((D, m), dtype=torch.float32, device=dev)
+        o = VcrBetaOpts(int(iters), float(lr_alpha), float(lr_beta), float(beta1), float(beta2), float(adam_eps),
+                        None, None)
+        extra = {}
+        if want_hist:
+            extra["lb_hist"] = torch.empty((iters + 1, D, m), dtype=torch.float32, device=dev)
+            extra["ub_hist"] = torch.empty((iters + 1, D, m), dtype=torch.float32, device=dev)
+            o.lb_hist, o.ub_hist = extra["lb_hist"].data_ptr(), extra["ub_hist"].data_ptr()
+        sp = VcrSplits(D, rid.shape[1], rid.data_ptr(), neu.data_ptr(), sgn.data_ptr())
+        self._stream_sync()
+        self._check(self.lib.vcr_beta_crown_bounds(self.h, _ptr(x0), ctypes.c_float(float(eps)), _ptr(C), m,
+                                                   ctypes.byref(sp), ctypes.byref(o), _ptr(lb), _ptr(ub)))
+        return lb, ub, extra
+
+    def bab_verify(self, x0, eps, C, batch=512, max_rounds=10, iters=20, lr_alpha=0.1, lr_beta=0.05, beta1=0.9,
+                   beta2=0.999, adam_eps=1e-8, order=None):
+        """Fixed-batch branch and bound on C f(x) > 0 (x0 (1, n0), C (1, m, n_out) CUDA tensors).
+        order: optional [(relu position, neuron), ...] split priority.  Returns a dict with the
+        result fields and "log": per round (taken, bounded, verified, left)."""
+        m = C.shape[1]
+        _check_tensor(x0, (1, None))
+        _check_tensor(C, (1, m, None))
+        bo = VcrBetaOpts(int(iters), float(lr_alpha), float(lr_beta), float(beta1), float(beta2), float(adam_eps),
+                         None, None)
+        keep = []
+        o = VcrBabOpts(int(batch), int(max_rounds), bo, None, None, 0)
+        if order is not None:
+            orr = np.ascontiguousarray([int(a) for a, _ in order], dtype=np.int32)
+            orn = np.ascontiguousarray([int(b) for _, b in order], dtype=np.int32)
+            keep += [orr, orn]
+            o.order_relu, o.order_neuron, o.order_len = orr.ctypes.data, orn.ctypes.data, len(orr)
+        log = np.zeros((max(int(max_rounds), 1), 4), dtype=np.int64)
+        res = VcrBabResult()
+        self._stream_sync()
+        self._check(self.lib.vcr_bab_verify(self.h, _ptr(x0), ctypes.c_float(float(eps)), _ptr(C), m, ctypes.byref(o),
+                                            ctypes.byref(res), log.ctypes.data))
+        return {"verified": bool(res.verified), "rounds": res.rounds, "evaluated": int(res.evaluated),
+                "remaining": int(res.remaining), "root_min_lb": res.root_min_lb, "worst_lb": res.worst_lb,
+                "log": [tuple(int(v) for v in r) for r in log[:res.rounds]]}
 
     def ibp_bounds(self, x0, eps, C):
         import torch
