@@ -138,6 +138,96 @@ def cpu_baseline_bab(wl, sp, budget_s):
                       f"domain time scaled to all domains", "cpu_count": os.cpu_count()}
 
 
+BAB_ROUNDS, BAB_ITERS = 10, 20
+
+
+def cpu_baseline_bab_loop(wl, batch, budget_s):
+    """The oracle's beta-CROWN on the subdomains the loop bounds first (the same loop, with
+    the oracle's own split order), until the time budget is used; subdomains per second."""
+    import threadpoolctl
+    import oracle
+    from oracle import beta64
+    root = oracle.crown(wl.net, wl.x0[0], wl.eps, wl.C[0])
+    order = beta64.default_order(wl.net, root)
+    t0 = time.perf_counter()
+    n, frontier = 0, [()]
+    while frontier and time.perf_counter() - t0 < budget_s:
+        kids = []
+        for dom in frontier[:batch]:
+            used = {(r, j) for r, j, _ in dom}
+            nxt = next(o for o in order if o not in used)
+            kids += [dom + ((nxt[0], nxt[1], 1),), dom + ((nxt[0], nxt[1], -1),)]
+        frontier = []
+        for k in kids:
+            r = beta64.beta_crown(wl.net, root, wl.C[0], list(k), iters=BAB_ITERS)
+            n += 1
+            if not np.all(r.lb > 0.0):
+                frontier.append(k)
+            if time.perf_counter() - t0 >= budget_s:
+                break
+    dt = time.perf_counter() - t0
+    threads = max((p.get("num_threads", 1) for p in threadpoolctl.threadpool_info()), default=1)
+    return {"value": n / dt, "unit": "domains/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"beta-CROWN ({BAB_ITERS} steps) on the first {n} subdomains of the same loop, {dt:.1f} s",
+            "cpu_count": os.cpu_count()}
+
+
+def bench_bab_loop(args):
+    import torch
+    from paper_2606_09377_amd import Ctx
+    from paper_2606_09377_amd.vcrown import OPT_TIME_GEMM
+    from workloads import make_workload
+    if not args.workload.startswith("bab_"):
+        print("--bab-loop runs on a bab_ workload (its root input and property)", file=sys.stderr)
+        sys.exit(2)
+    wl = make_workload(args.workload)
+    ctx = Ctx(0)
+    ctx.load_net(wl.net)
+    x0 = torch.from_numpy(wl.x0).cuda()
+    C = torch.from_numpy(wl.C).cuda()
+
+    def step():
+        return ctx.bab_verify(x0, wl.eps, C, batch=args.bab_loop, max_rounds=BAB_ROUNDS, iters=BAB_ITERS)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ctx.set_option(OPT_TIME_GEMM, 1)
+    t0 = time.perf_counter()
+    results = [step() for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    st = ctx.stats()
+    ctx.set_option(OPT_TIME_GEMM, 0)
+    res = results[-1]
+    assert all(r == res for r in results), "the loop is deterministic"
+    domains = res["evaluated"] * args.steps
+    launches, gms, gfl = st["timed_gemm_launches"], st["timed_gemm_ms"], st["timed_gemm_flops"]
+    achieved = gfl / (gms / 1e3) / 1e12 if gms > 0 else None
+    rec = {
+        "metric": "CROWN bound evals/sec (inputs or BaB domains) at 1 GPU; % fp32 MFMA peak",
+        "value": domains / dt,
+        "unit": "domains/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": dt / args.steps * 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": args.workload, "mode": "branch-and-bound loop", "batch": args.bab_loop,
+                   "rounds": BAB_ROUNDS, "eps": float(wl.eps), "spec_rows": int(wl.C.shape[1]),
+                   "method": f"alpha-CROWN root, beta-CROWN subdomains ({BAB_ITERS} joint Adam steps)"},
+        "roofline": {"bound": "mfma", "kernel": KERNEL_DESC["k_gemm"], "achieved": achieved,
+                     "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / PEAK_FP32_MFMA_TFLOPS if achieved else None,
+                     "traffic": traffic_for("k_gemm", args.workload), "launches_timed": launches,
+                     "avg_launch_ms": gms / launches if launches else None,
+                     "flops_per_launch": gfl / launches if launches else None,
+                     "share_of_step": gms / 1e3 / dt if launches else None},
+        "bab": {k: res[k] for k in ("verified", "rounds", "evaluated", "remaining", "root_min_lb", "worst_lb", "log")},
+    }
+    if args.cpu_budget > 0:
+        rec["cpu_baseline"] = cpu_baseline_bab_loop(wl, args.bab_loop, args.cpu_budget)
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -147,6 +237,9 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time (0: skip)")
     ap.add_argument("--alpha-iters", type=int, default=0,
                     help="alpha-CROWN with this many Adam steps on the final pass (MLPs; 0: CROWN)")
+    ap.add_argument("--bab-loop", type=int, default=0, metavar="BATCH",
+                    help="run the fixed-batch branch-and-bound loop (10 rounds, beta-CROWN bounds) with this batch "
+                         "on the bab_ workload's root input; value = subdomains bounded per second")
     ap.add_argument("--graph", action="store_true",
                     help="replay the call as a recorded HIP graph (the roofline then comes from a "
                          "second timed pass without the graph)")
@@ -168,6 +261,8 @@ def main():
         print(f"bench.py measures one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus})",
               file=sys.stderr)
         sys.exit(2)
+    if args.bab_loop:
+        return bench_bab_loop(args)
 
     if args.alpha_iters and not args.workload.startswith("mlp"):
         print("--alpha-iters runs on the MLP workloads (alpha-CROWN is built for dense/relu networks)",
