@@ -83,6 +83,183 @@ __device__ __forceinline__ float4 split_override(const SplitTable &st, int row, 
   return prm;
 }
 
+// Epilogue of one wave: MB blocks of 32 rows from tile-relative row wrow of the tile at m0
+// (tile_rows high), 64 columns from col0 (one partial sum per row and 64 columns, so every
+// tiling gives the same bits), accumulators acc[MB][2].
+template <bool FWD, bool AL, bool AFF, int MB>
+__device__ __forceinline__ void gemm_epilogue(const GemmArgs &p, f32x16 (&acc)[MB][2], int m0, int wrow, int col0,
+                                              int lane, int tile_rows) {
+  const int r32 = lane & 31;
+  // 32x32 accumulator layout: lane holds column (lane % 32) and rows
+  // 8 (v / 4) + 4 (lane / 32) + (v % 4), v = 0..15.
+  const int half = lane >> 5;
+  const bool uniform_unit = (p.rows_per_unit % tile_rows) == 0;
+  int unit_tile = m0 / p.rows_per_unit;
+  unit_tile = unit_tile < p.n_units ? unit_tile : p.n_units - 1;
+  const bool has_splits = p.splits.D > 0;
+
+  // Stores and row-wise loads address the tile from a wave-uniform base with 32-bit lane
+  // offsets (every row-indexed array of one launch shares the pitch ld).
+  const int64_t ld = p.mode == EPI_CONCRETIZE ? p.ld_pre : p.ldo;
+  const int64_t tbase = (int64_t)m0 * ld;
+  float *const out_t = p.mode == EPI_CONCRETIZE ? nullptr : p.out + tbase;
+  float *const pre_t = p.pre ? p.pre + tbase : nullptr;
+  const float *const alpha_t = p.alpha ? p.alpha + tbase : nullptr;
+  float *const grad_t = p.grad ? p.grad + tbase : nullptr;
+  const int ld32 = (int)ld;
+
+  float rp[MB][16];
+#pragma unroll
+  for (int i = 0; i < MB; ++i)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) rp[i][v] = 0.f;
+
+  if constexpr (AFF) {
+    // plain affine map (the IBP step on the matrix cores): out = A Bt^T (+ bias)
+#pragma unroll
+    for (int bj = 0; bj < 2; ++bj) {
+      const int n = col0 + bj * 32 + r32;
+      const float bn = p.bias ? p.bias[n] : 0.f;
+#pragma unroll
+      for (int bi = 0; bi < MB; ++bi)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int lr = wrow + bi * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
+          out_t[lr * ld32 + n] = acc[bi][bj][v] + bn;
+        }
+    }
+    return;
+  }
+#pragma unroll
+  for (int bj = 0; bj < 2; ++bj) {
+    const int n = col0 + bj * 32 + r32;
+    if constexpr (FWD) {
+      // the relaxed network evaluated forward: D = W_k E + b_k, then the line of ReLU k that
+      // the backward pass chose for this row (by the sign of its coefficient)
+      float4 prm_tile = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (uniform_unit) prm_tile = p.P[(int64_t)unit_tile * p.ldp + n];
+#pragma unroll
+      for (int bi = 0; bi < MB; ++bi) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int lr = wrow + bi * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
+          const int row = m0 + lr;
+          const int off = lr * ld32 + n;
+          float4 prm = prm_tile;
+          if (!uniform_unit) {
+            int u = row / p.rows_per_unit;
+            u = u < p.n_units ? u : p.n_units - 1;
+            prm = p.P[(int64_t)u * p.ldp + n];
+          }
+          int ent = -1;
+          float sterm = 0.f;
+          if (has_splits) prm = split_override(p.splits, row, p.relu_index, n, prm, &ent, &sterm);
+          const bool unst = prm.z > 0.f;
+          const float lam = unst ? alpha_t[off] : prm.x;
+          const float an = pre_t[off];
+          const float D = acc[bi][bj][v] + prm.w;
+          if (ent >= 0 && p.splits.grad_beta) p.splits.grad_beta[(int64_t)row * p.splits.S + ent] = sterm * D;
+          const float E = an > 0.f ? lam * D : prm.y * D + (an < 0.f ? prm.z : 0.f);
+          out_t[off] = E;
+          grad_t[off] = (unst && an > 0.f) ? an * D : 0.f;
+        }
+      }
+    } else if (p.mode == EPI_RELAX) {
+      float4 prm_tile = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (uniform_unit) prm_tile = p.P[(int64_t)unit_tile * p.ldp + n];
+#pragma unroll
+      for (int bi = 0; bi < MB; ++bi) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int lr = wrow + bi * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
+          const int row = m0 + lr;
+          const int off = lr * ld32 + n;
+          float4 prm = prm_tile;
+          if (!uniform_unit) {
+            int u = row / p.rows_per_unit;
+            u = u < p.n_units ? u : p.n_units - 1;
+            prm = p.P[(int64_t)u * p.ldp + n];
+          }
+          int ent = -1;
+          float sterm = 0.f;
+          if (has_splits) {
+            if constexpr (AL)
+              prm = split_override(p.splits, row, p.relu_index, n, prm, &ent, &sterm);
+            else
+              prm = split_override(p.splits, row, p.relu_index, n, prm);
+          }
+          const float a = acc[bi][bj][v];
+          float lam = prm.x;
+          if constexpr (AL) {
+            if (alpha_t && prm.z > 0.f) lam = alpha_t[off];
+          }
+          float ap = a > 0.f ? a * lam : a * prm.y;
+          if constexpr (AL) {
+            if (ent >= 0 && p.splits.beta) ap += p.splits.beta[(int64_t)row * p.splits.S + ent] * sterm;
+          }
+          out_t[off] = ap;
+          if constexpr (AL) {
+            if (pre_t) pre_t[off] = a;
+          }
+          rp[bi][v] += fminf(a, 0.f) * prm.z + ap * prm.w;
+        }
+      }
+    } else {
+      float c_tile = 0.f, r_tile = 0.f;
+      if (uniform_unit) {
+        c_tile = p.c0[(int64_t)unit_tile * p.ldc + n];
+        r_tile = p.r0[(int64_t)unit_tile * p.ldc + n];
+      }
+#pragma unroll
+      for (int bi = 0; bi < MB; ++bi) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int lr = wrow + bi * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
+          const int row = m0 + lr;
+          float c = c_tile, r = r_tile;
+          if (!uniform_unit) {
+            int u = row / p.rows_per_unit;
+            u = u < p.n_units ? u : p.n_units - 1;
+            c = p.c0[(int64_t)u * p.ldc + n];
+            r = p.r0[(int64_t)u * p.ldc + n];
+          }
+          const float a = acc[bi][bj][v];
+          if constexpr (AL) {
+            if (pre_t) pre_t[lr * ld32 + n] = a;
+          }
+          rp[bi][v] += a * c - fabsf(a) * r;
+        }
+      }
+    }
+  }
+
+  if constexpr (FWD) return;
+  // fixed butterfly over the 32 lanes that share rows
+#pragma unroll
+  for (int bi = 0; bi < MB; ++bi) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      float x = rp[bi][v];
+      x += __shfl_xor(x, 16);
+      x += __shfl_xor(x, 8);
+      x += __shfl_xor(x, 4);
+      x += __shfl_xor(x, 2);
+      x += __shfl_xor(x, 1);
+      rp[bi][v] = x;
+    }
+  }
+  if (r32 == 0) {
+    float *dst = p.part + (int64_t)(col0 / PART_COLS) * p.M_pad;
+#pragma unroll
+    for (int bi = 0; bi < MB; ++bi)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = m0 + wrow + bi * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
+        dst[row] = rp[bi][v];
+      }
+  }
+}
+
 // Instantiations: FWD selects the forward epilogue (alpha-CROWN's gradient pass); otherwise the
 // relax and concretize epilogues share one kernel and the mode is read at run time (this keeps
 // the register allocation of the relax epilogue spill-free).  AL adds the alpha-CROWN extras
@@ -180,174 +357,70 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm(const GemmArgs p) {
   }
 
   // ---- epilogue ---------------------------------------------------------------------
-  // 32x32 accumulator layout: lane holds column (lane % 32) and rows
-  // 8 (v / 4) + 4 (lane / 32) + (v % 4), v = 0..15.
-  const int half = lane >> 5;
-  const bool uniform_unit = (p.rows_per_unit % BM) == 0;
-  int unit_tile = m0 / p.rows_per_unit;
-  unit_tile = unit_tile < p.n_units ? unit_tile : p.n_units - 1;
-  const bool has_splits = p.splits.D > 0;
+  gemm_epilogue<FWD, AL, AFF, 2>(p, acc, m0, wm * 64, n0 + wn * 64, lane, BM);
+}
 
-  // Stores and row-wise loads address the tile from a wave-uniform base with 32-bit lane
-  // offsets (every row-indexed array of one launch shares the pitch ld).
-  const int64_t ld = p.mode == EPI_CONCRETIZE ? p.ld_pre : p.ldo;
-  const int64_t tbase = (int64_t)m0 * ld;
-  float *const out_t = p.mode == EPI_CONCRETIZE ? nullptr : p.out + tbase;
-  float *const pre_t = p.pre ? p.pre + tbase : nullptr;
-  const float *const alpha_t = p.alpha ? p.alpha + tbase : nullptr;
-  float *const grad_t = p.grad ? p.grad + tbase : nullptr;
-  const int ld32 = (int)ld;
+// Small launches (few row tiles): one wave per workgroup owns a 32 x 64 tile and reads its
+// MFMA operands straight from global memory (no LDS, no barriers), next K tile prefetched in
+// registers.  Each lane takes the same 16 consecutive k of its row per K tile as in k_gemm, and
+// each accumulator sees the same MFMA sequence, so both kernels give the same bits.
+constexpr int SM_BM = 32, SM_BN = 64;
+constexpr int64_t SMALL_GRID = 512;   // 128 x 128 tiles below which the small kernel runs
 
-  float rp[2][16];
+template <bool FWD, bool AL, bool AFF = false>
+__global__ __launch_bounds__(64) void k_gemm_small(const GemmArgs p) {
+  const int lane = threadIdx.x;
+  const int n_mt = p.M_pad / SM_BM, n_nt = p.N_pad / SM_BN;
+  int mt, nt;
+  map_tile(blockIdx.x, n_mt * n_nt, n_mt, n_nt, mt, nt);
+  const int m0 = mt * SM_BM, n0 = nt * SM_BN;
+  const int r32 = lane & 31, kq = (lane >> 5) * 16;
+  const float *Ag = p.A + (int64_t)(m0 + r32) * p.lda + kq;
+  const float *Bg0 = p.Bt + (int64_t)(n0 + r32) * p.ldb + kq;
+  const float *Bg1 = Bg0 + 32 * p.ldb;
+  f32x16 acc[1][2];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int j = 0; j < 2; ++j)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) rp[i][v] = 0.f;
-
-  if constexpr (AFF) {
-    // plain affine map (the IBP step on the matrix cores): out = A Bt^T (+ bias)
+    for (int v = 0; v < 16; ++v) acc[0][j][v] = 0.f;
+  f32x4 a[4], b0[4], b1[4];
+  auto load = [&](int k0, f32x4 *ra, f32x4 *rb0, f32x4 *rb1) {
 #pragma unroll
-    for (int bj = 0; bj < 2; ++bj) {
-      const int n = n0 + wn * 64 + bj * 32 + r32;
-      const float bn = p.bias ? p.bias[n] : 0.f;
-#pragma unroll
-      for (int bi = 0; bi < 2; ++bi)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int lr = wm * 64 + bi * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
-          out_t[lr * ld32 + n] = acc[bi][bj][v] + bn;
-        }
-    }
-    return;
-  }
-#pragma unroll
-  for (int bj = 0; bj < 2; ++bj) {
-    const int n = n0 + wn * 64 + bj * 32 + r32;
-    if constexpr (FWD) {
-      // the relaxed network evaluated forward: D = W_k E + b_k, then the line of ReLU k that
-      // the backward pass chose for this row (by the sign of its coefficient)
-      float4 prm_tile = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (uniform_unit) prm_tile = p.P[(int64_t)unit_tile * p.ldp + n];
-#pragma unroll
-      for (int bi = 0; bi < 2; ++bi) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int lr = wm * 64 + bi * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
-          const int row = m0 + lr;
-          const int off = lr * ld32 + n;
-          float4 prm = prm_tile;
-          if (!uniform_unit) {
-            int u = row / p.rows_per_unit;
-            u = u < p.n_units ? u : p.n_units - 1;
-            prm = p.P[(int64_t)u * p.ldp + n];
-          }
-          int ent = -1;
-          float sterm = 0.f;
-          if (has_splits) prm = split_override(p.splits, row, p.relu_index, n, prm, &ent, &sterm);
-          const bool unst = prm.z > 0.f;
-          const float lam = unst ? alpha_t[off] : prm.x;
-          const float an = pre_t[off];
-          const float D = acc[bi][bj][v] + prm.w;
-          if (ent >= 0 && p.splits.grad_beta) p.splits.grad_beta[(int64_t)row * p.splits.S + ent] = sterm * D;
-          const float E = an > 0.f ? lam * D : prm.y * D + (an < 0.f ? prm.z : 0.f);
-          out_t[off] = E;
-          grad_t[off] = (unst && an > 0.f) ? an * D : 0.f;
-        }
-      }
-    } else if (p.mode == EPI_RELAX) {
-      float4 prm_tile = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (uniform_unit) prm_tile = p.P[(int64_t)unit_tile * p.ldp + n];
-#pragma unroll
-      for (int bi = 0; bi < 2; ++bi) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int lr = wm * 64 + bi * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
-          const int row = m0 + lr;
-          const int off = lr * ld32 + n;
-          float4 prm = prm_tile;
-          if (!uniform_unit) {
-            int u = row / p.rows_per_unit;
-            u = u < p.n_units ? u : p.n_units - 1;
-            prm = p.P[(int64_t)u * p.ldp + n];
-          }
-          int ent = -1;
-          float sterm = 0.f;
-          if (has_splits) {
-            if constexpr (AL)
-              prm = split_override(p.splits, row, p.relu_index, n, prm, &ent, &sterm);
-            else
-              prm = split_override(p.splits, row, p.relu_index, n, prm);
-          }
-          const float a = acc[bi][bj][v];
-          float lam = prm.x;
-          if constexpr (AL) {
-            if (alpha_t && prm.z > 0.f) lam = alpha_t[off];
-          }
-          float ap = a > 0.f ? a * lam : a * prm.y;
-          if constexpr (AL) {
-            if (ent >= 0 && p.splits.beta) ap += p.splits.beta[(int64_t)row * p.splits.S + ent] * sterm;
-          }
-          out_t[off] = ap;
-          if constexpr (AL) {
-            if (pre_t) pre_t[off] = a;
-          }
-          rp[bi][v] += fminf(a, 0.f) * prm.z + ap * prm.w;
-        }
-      }
-    } else {
-      float c_tile = 0.f, r_tile = 0.f;
-      if (uniform_unit) {
-        c_tile = p.c0[(int64_t)unit_tile * p.ldc + n];
-        r_tile = p.r0[(int64_t)unit_tile * p.ldc + n];
-      }
-#pragma unroll
-      for (int bi = 0; bi < 2; ++bi) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int lr = wm * 64 + bi * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
-          const int row = m0 + lr;
-          float c = c_tile, r = r_tile;
-          if (!uniform_unit) {
-            int u = row / p.rows_per_unit;
-            u = u < p.n_units ? u : p.n_units - 1;
-            c = p.c0[(int64_t)u * p.ldc + n];
-            r = p.r0[(int64_t)u * p.ldc + n];
-          }
-          const float a = acc[bi][bj][v];
-          if constexpr (AL) {
-            if (pre_t) pre_t[lr * ld32 + n] = a;
-          }
-          rp[bi][v] += a * c - fabsf(a) * r;
+    for (int h = 0; h < 4; ++h) {
+      ra[h] = *reinterpret_cast<const f32x4 *>(Ag + k0 + 4 * h);
+      rb0[h] = *reinterpret_cast<const f32x4 *>(Bg0 + k0 + 4 * h);
+      rb1[h] = *reinterpret_cast<const f32x4 *>(Bg1 + k0 + 4 * h);
+      if constexpr (AFF) {
+        if (p.abs_b) {
+          rb0[h] = __builtin_elementwise_abs(rb0[h]);
+          rb1[h] = __builtin_elementwise_abs(rb1[h]);
         }
       }
     }
-  }
-
-  if constexpr (FWD) return;
-  // fixed butterfly over the 32 lanes that share rows
+  };
+  load(0, a, b0, b1);
+  const int KT = p.K / BK;
+  for (int kt = 0; kt < KT; ++kt) {
+    f32x4 na[4], nb0[4], nb1[4];
+    const bool more = kt + 1 < KT;
+    if (more) load((kt + 1) * BK, na, nb0, nb1);
 #pragma unroll
-  for (int bi = 0; bi < 2; ++bi) {
+    for (int h = 0; h < 4; ++h)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      float x = rp[bi][v];
-      x += __shfl_xor(x, 16);
-      x += __shfl_xor(x, 8);
-      x += __shfl_xor(x, 4);
-      x += __shfl_xor(x, 2);
-      x += __shfl_xor(x, 1);
-      rp[bi][v] = x;
+      for (int e = 0; e < 4; ++e) {
+        acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[h][e], b0[h][e], acc[0][0], 0, 0, 0);
+        acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[h][e], b1[h][e], acc[0][1], 0, 0, 0);
+      }
+    if (more) {
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        a[h] = na[h];
+        b0[h] = nb0[h];
+        b1[h] = nb1[h];
+      }
     }
   }
-  if (r32 == 0) {
-    float *dst = p.part + (int64_t)(nt * 2 + wn) * p.M_pad;
-#pragma unroll
-    for (int bi = 0; bi < 2; ++bi)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = m0 + wm * 64 + bi * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
-        dst[row] = rp[bi][v];
-      }
-  }
+  gemm_epilogue<FWD, AL, AFF, 1>(p, acc, m0, 0, n0, lane, SM_BM);
 }
 
 hipError_t launch_gemm(const GemmArgs &a, hipStream_t s) {
@@ -364,13 +437,27 @@ hipError_t launch_gemm(const GemmArgs &a, hipStream_t s) {
   const int64_t grid = (int64_t)(a.M_pad / BM) * (a.N_pad / BN);
   if (grid > 0x7fffffff) return hipErrorInvalidValue;
   const bool al = a.alpha || a.pre;
+  if (a.mode != EPI_RELAX && a.mode != EPI_CONCRETIZE && a.mode != EPI_FORWARD && a.mode != EPI_AFFINE)
+    return hipErrorInvalidValue;
+  if (grid < SMALL_GRID) {
+    // too few 128 x 128 tiles to fill the chip: 32 x 64 tiles, one wave each (same bits)
+    const int64_t sg = (int64_t)(a.M_pad / SM_BM) * (a.N_pad / SM_BN);
+    const dim3 g((unsigned)sg), t(64);
+    if (a.mode == EPI_AFFINE)
+      hipLaunchKernelGGL((k_gemm_small<false, false, true>), g, t, 0, s, a);
+    else if (a.mode == EPI_FORWARD)
+      hipLaunchKernelGGL((k_gemm_small<true, true>), g, t, 0, s, a);
+    else if (al)
+      hipLaunchKernelGGL((k_gemm_small<false, true>), g, t, 0, s, a);
+    else
+      hipLaunchKernelGGL((k_gemm_small<false, false>), g, t, 0, s, a);
+    return hipGetLastError();
+  }
   const dim3 g((unsigned)grid), t(NTHREADS);
   if (a.mode == EPI_AFFINE)
     hipLaunchKernelGGL((k_gemm<false, false, true>), g, t, 0, s, a);
   else if (a.mode == EPI_FORWARD)
     hipLaunchKernelGGL((k_gemm<true, true>), g, t, 0, s, a);
-  else if (a.mode != EPI_RELAX && a.mode != EPI_CONCRETIZE)
-    return hipErrorInvalidValue;
   else if (al)
     hipLaunchKernelGGL((k_gemm<false, true>), g, t, 0, s, a);
   else
