@@ -11,16 +11,18 @@ struct FastDiv {
 };
 FastDiv make_fastdiv(uint32_t d);
 
-// One output-parity class of a transposed convolution.  With stride 2 an output position
-// (u, w) of the destination window only receives the taps whose (ky, kx) have the parity of
-// (u + delta, w + delta), so the GEMM runs as four classes, each with only its own taps (4, 2,
-// 2 and 1 of the 9); with stride 1 there is one class with all 9.  Positions of a class:
-// u = u0 + stride iy, w = w0 + stride ix; taps: (ky0 + kstep ty, kx0 + kstep tx).
+// One class of output positions of a transposed convolution: the positions of the
+// destination window that receive the same set of taps.  With stride 2 a position (u, w)
+// only receives the taps whose (ky, kx) have the parity of (u + delta, w + delta); at the
+// window's border ring, taps whose source falls outside the source window are missing too.
+// Each class runs as a GEMM over its own taps only, so no all-zero K tile is computed (the
+// executed flops are the algorithmic ones).  Positions: u = u0 + ustep iy, w = w0 + wstep ix
+// (ustep = stride unless ny = 1); taps (ky0 + kys ty, kx0 + kxs tx).
 struct ConvClass {
   int32_t blk0;              // first workgroup of the class (classes are consecutive)
   int32_t M;                 // GEMM rows of the class: R ny nx
-  int32_t ny, nx, u0, w0;
-  int32_t nty, ntx, ky0, kx0, kstep;
+  int32_t ny, nx, u0, w0, ustep, wstep;
+  int32_t nty, ntx, ky0, kx0, kys, kxs;
   FastDiv div_yx, div_x;
 };
 

@@ -25,6 +25,9 @@
 // and reduces the constants over the tile's columns into one partial per GEMM row.
 #include "conv.h"
 
+#include <algorithm>
+#include <vector>
+
 namespace vcr {
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -97,7 +100,7 @@ __global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
     const int t = k0 / p.C_out;
     const int co0 = k0 - t * p.C_out;
     const int ty = t / cl.ntx, tx = t - ty * cl.ntx;
-    const int ky = cl.ky0 + cl.kstep * ty, kx = cl.kx0 + cl.kstep * tx;
+    const int ky = cl.ky0 + cl.kys * ty, kx = cl.kx0 + cl.kxs * tx;
     const int dy = (cl.u0 + p.delta - ky) >> sh, dx = (cl.w0 + p.delta - kx) >> sh;   // exact
     const int co = co0 + lcol;
 #pragma unroll
@@ -188,8 +191,8 @@ __global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
         const uint32_t r = valid ? fdiv((uint32_t)m, cl.div_yx) : 0u;
         const uint32_t pos = valid ? (uint32_t)m - r * (uint32_t)nyx : 0u;
         const uint32_t iy = fdiv(pos, cl.div_x);
-        const int u = cl.u0 + ((int)iy << sh);
-        const int w = cl.w0 + ((int)(pos - iy * (uint32_t)cl.nx) << sh);
+        const int u = cl.u0 + (int)iy * cl.ustep;
+        const int w = cl.w0 + (int)(pos - iy * (uint32_t)cl.nx) * cl.wstep;
         const int4 an = rowsp[r];   // (unit, anchor y, anchor x, -)
         const int gy = p.dense ? u : an.y * p.scale - p.h_in + u;
         const int gx = p.dense ? w : an.z * p.scale - p.h_in + w;
@@ -250,12 +253,49 @@ __global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
   }
 }
 
-// Fills the parity classes for BM-row tiles; returns the number of workgroups (or -1).
-static int64_t convt_classes(ConvTArgs &a, int BM, int BN) {
+// Classes of one axis: positions u of the destination window with the same taps ky, as an
+// arithmetic progression of positions and of taps.
+struct AxisClass {
+  int u0, ustep, n, k0, ks, nk;
+};
+
+static bool axis_classes(int S_in, int S_out, int stride, int delta, std::vector<AxisClass> &out) {
+  out.clear();
+  std::vector<AxisClass> open;   // classes that can still grow
+  for (int u = 0; u < S_in; ++u) {
+    int taps[3], nt = 0;
+    for (int ky = 0; ky < 3; ++ky) {
+      const int q = u + delta - ky;
+      if (q < 0 || q % stride) continue;
+      if (q / stride < S_out) taps[nt++] = ky;
+    }
+    if (nt == 0) return false;   // a position no tap reaches (not produced by these shapes)
+    const int ks = nt > 1 ? taps[1] - taps[0] : 1;
+    for (int i = 2; i < nt; ++i)
+      if (taps[i] - taps[i - 1] != ks) return false;
+    bool joined = false;
+    for (AxisClass &c : open) {   // same taps, next position of the progression
+      if (c.k0 == taps[0] && c.nk == nt && c.ks == ks && u == c.u0 + stride * c.n) {
+        ++c.n;
+        joined = true;
+        break;
+      }
+    }
+    if (!joined) open.push_back({u, stride, 1, taps[0], ks, nt});
+  }
+  out = open;
+  return true;
+}
+
+// Fills the classes for BM-row tiles (up to 4 per launch, from class `first`); returns the
+// number of workgroups (or -1) and the number of classes in all.
+static int64_t convt_classes(ConvTArgs &a, int BM, int BN, const std::vector<AxisClass> &cu,
+                             const std::vector<AxisClass> &cw, int first) {
   if (a.C_out % 32 || a.R <= 0 || a.N_pad % BN || a.N_pad <= 0 || (a.stride != 1 && a.stride != 2)) return -1;
   if ((int64_t)a.R * a.S_in * a.S_in > a.M_pad) return -1;
   const int n_nt = a.N_pad / BN;
-  a.n_cls = a.stride == 2 ? 4 : 1;
+  const int total = (int)(cu.size() * cw.size());
+  a.n_cls = std::min(4, total - first);
   int64_t blk = 0;
   for (int c = 0; c < 4; ++c) {
     ConvClass &k = a.cls[c];
@@ -264,24 +304,19 @@ static int64_t convt_classes(ConvTArgs &a, int BM, int BN) {
       k.blk0 = 0x7fffffff;
       continue;
     }
-    if (a.stride == 1) {
-      k.u0 = k.w0 = 0;
-      k.ny = k.nx = a.S_in;
-      k.nty = k.ntx = 3;
-      k.ky0 = k.kx0 = 0;
-      k.kstep = 1;
-    } else {
-      const int py = c & 1, px = c >> 1;   // parity of u + delta, w + delta
-      k.u0 = (py - a.delta) & 1;
-      k.w0 = (px - a.delta) & 1;
-      k.ny = (a.S_in - k.u0 + 1) / 2;
-      k.nx = (a.S_in - k.w0 + 1) / 2;
-      k.ky0 = py;
-      k.kx0 = px;
-      k.nty = py ? 1 : 2;
-      k.ntx = px ? 1 : 2;
-      k.kstep = 2;
-    }
+    const AxisClass &yu = cu[(first + c) / cw.size()], &xw = cw[(first + c) % cw.size()];
+    k.u0 = yu.u0;
+    k.ustep = yu.ustep;
+    k.ny = yu.n;
+    k.ky0 = yu.k0;
+    k.kys = yu.ks;
+    k.nty = yu.nk;
+    k.w0 = xw.u0;
+    k.wstep = xw.ustep;
+    k.nx = xw.n;
+    k.kx0 = xw.k0;
+    k.kxs = xw.ks;
+    k.ntx = xw.nk;
     const int64_t M = (int64_t)a.R * k.ny * k.nx;
     if (M >= ((int64_t)1 << 31)) return -1;
     k.M = (int32_t)M;
@@ -294,17 +329,27 @@ static int64_t convt_classes(ConvTArgs &a, int BM, int BN) {
 }
 
 hipError_t launch_convt(const ConvTArgs &a0, hipStream_t s) {
-  ConvTArgs a = a0;
-  if (a.N_pad % 128 == 0) {   // 128 x 128 tiles, 2 x 2 waves of 64 x 64
-    const int64_t blk = convt_classes(a, 128, 128);
-    if (blk < 0) return hipErrorInvalidValue;
-    if (blk > 0) hipLaunchKernelGGL((k_convt<128, 128, 16, 2, 2, 3>), dim3((unsigned)blk), dim3(256), 0, s, a);
-  } else {                    // 256 x 64 tiles, 4 x 1 waves of 64 x 64
-    const int64_t blk = convt_classes(a, 256, 64);
-    if (blk < 0) return hipErrorInvalidValue;
-    if (blk > 0) hipLaunchKernelGGL((k_convt<256, 64, 16, 4, 1, 3>), dim3((unsigned)blk), dim3(256), 0, s, a);
+  std::vector<AxisClass> cu, cw;
+  if (!axis_classes(a0.S_in, a0.S_out, a0.stride, a0.delta, cu) || !cu.size()) return hipErrorInvalidValue;
+  for (const AxisClass &c : cu)   // the gather's row offset assumes ustep = stride for n > 1
+    if (c.n > 1 && c.ustep != a0.stride) return hipErrorInvalidValue;
+  cw = cu;   // square windows
+  const int total = (int)(cu.size() * cw.size());
+  for (int first = 0; first < total; first += 4) {
+    ConvTArgs a = a0;
+    if (a.N_pad % 128 == 0) {   // 128 x 128 tiles, 2 x 2 waves of 64 x 64
+      const int64_t blk = convt_classes(a, 128, 128, cu, cw, first);
+      if (blk < 0) return hipErrorInvalidValue;
+      if (blk > 0) hipLaunchKernelGGL((k_convt<128, 128, 16, 2, 2, 3>), dim3((unsigned)blk), dim3(256), 0, s, a);
+    } else {                    // 256 x 64 tiles, 4 x 1 waves of 64 x 64
+      const int64_t blk = convt_classes(a, 256, 64, cu, cw, first);
+      if (blk < 0) return hipErrorInvalidValue;
+      if (blk > 0) hipLaunchKernelGGL((k_convt<256, 64, 16, 4, 1, 3>), dim3((unsigned)blk), dim3(256), 0, s, a);
+    }
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
   }
-  return hipGetLastError();
+  return hipSuccess;
 }
 
 // ------------------------------------------------------------------------------------
