@@ -136,6 +136,11 @@ typedef struct {
   double timed_conv_ms;
   uint64_t timed_conv_flops;
   uint64_t net_bytes;               /* device memory holding the loaded network's weights */
+  /* the dense GEMM launches too small to fill the chip, which run a small-tile kernel (not
+   * included in timed_gemm_*) */
+  uint64_t timed_small_launches;
+  double timed_small_ms;
+  uint64_t timed_small_flops;
 } vcr_stats;
 
 /* ABI version compiled into the library (VCR_ABI_VERSION). */

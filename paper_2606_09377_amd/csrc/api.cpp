@@ -323,7 +323,7 @@ vcr_status vcr_set_option(vcr_ctx *c, int32_t key, double v) {
       c->time_gemm = v != 0.0;
       c->ev_used = 0;
       c->pending.clear();
-      for (int k = 0; k < 2; ++k) {
+      for (int k = 0; k < 3; ++k) {
         c->timed_launches[k] = c->timed_flops[k] = 0;
         c->timed_ms[k] = 0.0;
       }
@@ -512,13 +512,13 @@ vcr_status ibp_layer(vcr_ctx *c, const DenseLayer &W, const float *cin, const fl
   g.bias = W.b;
   const uint64_t gf = 2ull * (uint64_t)B * (uint64_t)W.n_out * (uint64_t)W.n_in;
   if (flops) *flops += 2 * gf;
-  vcr_status st = timed_launch(c, s, 0, gf, [&] { return launch_gemm(g, s); });
+  vcr_status st = TIMED_GEMM(c, s, gf, g);
   if (st != VCR_OK) return st;
   g.A = rin;
   g.out = rout;
   g.bias = nullptr;
   g.abs_b = 1;
-  return timed_launch(c, s, 0, gf, [&] { return launch_gemm(g, s); });
+  return TIMED_GEMM(c, s, gf, g);
 }
 
 bool any_ibp_relu_on_mfma(const vcr_ctx *c) {
@@ -661,7 +661,7 @@ vcr_status run_chain(vcr_ctx *c, CallBufs &bf, int top, int32_t M, int32_t rows_
     }
     const uint64_t gf = 2ull * (uint64_t)M * (uint64_t)W.n_out * (uint64_t)W.n_in;
     {
-      const vcr_status st = timed_launch(c, c->stream, 0, gf, [&] { return launch_gemm(g, c->stream); });
+      const vcr_status st = TIMED_GEMM(c, c->stream, gf, g);
       if (st != VCR_OK) return st;
     }
     *flops += gf;
@@ -784,7 +784,7 @@ vcr_status alpha_spec(vcr_ctx *c, CallBufs &bf, const Plan &p, const AlphaCall &
         g.ld_pre = al[k - 1].ld;
         g.grad = al[k - 1].grad;
         const uint64_t gf = 2ull * (uint64_t)M * (uint64_t)W.n_out * (uint64_t)W.n_in;
-        st = timed_launch(c, s, 0, gf, [&] { return launch_gemm(g, s); });
+        st = TIMED_GEMM(c, s, gf, g);
         if (st != VCR_OK) return st;
         *flops += gf;
       }
@@ -1426,6 +1426,9 @@ vcr_status vcr_get_stats(vcr_ctx *c, vcr_stats *out) {
   out->timed_conv_launches = c->timed_launches[1];
   out->timed_conv_ms = c->timed_ms[1];
   out->timed_conv_flops = c->timed_flops[1];
+  out->timed_small_launches = c->timed_launches[2];
+  out->timed_small_ms = c->timed_ms[2];
+  out->timed_small_flops = c->timed_flops[2];
   if (c->lastL.empty()) return VCR_OK;
   int32_t *cnt = c->d_counters;
   const int R = std::min<int>((int)c->lastL.size(), 64);

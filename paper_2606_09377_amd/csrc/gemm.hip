@@ -423,6 +423,10 @@ __global__ __launch_bounds__(64) void k_gemm_small(const GemmArgs p) {
   gemm_epilogue<FWD, AL, AFF, 1>(p, acc, m0, 0, n0, lane, SM_BM);
 }
 
+bool gemm_is_small(const GemmArgs &a) {
+  return a.M_pad > 0 && a.N_pad > 0 && (int64_t)(a.M_pad / BM) * (a.N_pad / BN) < SMALL_GRID;
+}
+
 hipError_t launch_gemm(const GemmArgs &a, hipStream_t s) {
   if (a.M_pad % BM || a.N_pad % BN || a.K % BK || a.K <= 0 || a.M_pad <= 0 || a.N_pad <= 0)
     return hipErrorInvalidValue;

@@ -851,7 +851,7 @@ vcr_status run_pass(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &pp, int 
         if (st.dst.row_stride != nd.ld_in) return fail(c, VCR_ERR_UNSUPPORTED, "internal: dense output width mismatch");
         const uint64_t df = 2ull * (uint64_t)R * (uint64_t)nd.numel * (uint64_t)g->nodes[nd.in0].numel;
         {
-          const vcr_status st2 = timed_launch(c, s, 0, df, [&] { return launch_gemm(ga, s); });
+          const vcr_status st2 = TIMED_GEMM(c, s, df, ga);
           if (st2 != VCR_OK) return st2;
         }
         HIP_TRY(c, launch_rowsum_win(bf.beta, bf.part, (int32_t)(nd.ld_in / PART_COLS), ga.M_pad, R, 1, s));

@@ -43,7 +43,8 @@ class VcrStats(ctypes.Structure):
                 ("timed_gemm_launches", ctypes.c_uint64), ("timed_gemm_ms", ctypes.c_double),
                 ("timed_gemm_flops", ctypes.c_uint64), ("timed_conv_launches", ctypes.c_uint64),
                 ("timed_conv_ms", ctypes.c_double), ("timed_conv_flops", ctypes.c_uint64),
-                ("net_bytes", ctypes.c_uint64)]
+                ("net_bytes", ctypes.c_uint64), ("timed_small_launches", ctypes.c_uint64),
+                ("timed_small_ms", ctypes.c_double), ("timed_small_flops", ctypes.c_uint64)]
 
 
 class VcrAlphaOpts(ctypes.Structure):
@@ -359,7 +360,8 @@ class Ctx:
                 "timed_gemm_launches": int(s.timed_gemm_launches), "timed_gemm_ms": s.timed_gemm_ms,
                 "timed_gemm_flops": int(s.timed_gemm_flops), "timed_conv_launches": int(s.timed_conv_launches),
                 "timed_conv_ms": s.timed_conv_ms, "timed_conv_flops": int(s.timed_conv_flops),
-                "net_bytes": int(s.net_bytes)}
+                "net_bytes": int(s.net_bytes), "timed_small_launches": int(s.timed_small_launches),
+                "timed_small_ms": s.timed_small_ms, "timed_small_flops": int(s.timed_small_flops)}
 
 
 def _relu_sizes(net):
