@@ -52,6 +52,12 @@ struct ConvTArgs {
   ConvClass cls[4];
 };
 hipError_t launch_convt(const ConvTArgs &a, hipStream_t s);
+// The transposed convolution runs as classes of output positions (the taps that reach them),
+// four per dispatch: the number of dispatches (or -1 for unsupported shapes), dispatch `part`
+// alone, and its flops (2 per multiply-add of a position and a tap that reaches it).
+int convt_launches(const ConvTArgs &a);
+hipError_t launch_convt_part(const ConvTArgs &a, int part, hipStream_t s);
+uint64_t convt_part_flops(const ConvTArgs &a, int part);
 
 struct StemArgs {
   const float *A;

@@ -328,25 +328,56 @@ static int64_t convt_classes(ConvTArgs &a, int BM, int BN, const std::vector<Axi
   return blk > 0x7fffffff ? -1 : blk;
 }
 
-hipError_t launch_convt(const ConvTArgs &a0, hipStream_t s) {
-  std::vector<AxisClass> cu, cw;
-  if (!axis_classes(a0.S_in, a0.S_out, a0.stride, a0.delta, cu) || !cu.size()) return hipErrorInvalidValue;
+static bool convt_axes(const ConvTArgs &a, std::vector<AxisClass> &cu) {
+  if (!axis_classes(a.S_in, a.S_out, a.stride, a.delta, cu) || cu.empty()) return false;
   for (const AxisClass &c : cu)   // the gather's row offset assumes ustep = stride for n > 1
-    if (c.n > 1 && c.ustep != a0.stride) return hipErrorInvalidValue;
-  cw = cu;   // square windows
+    if (c.n > 1 && c.ustep != a.stride) return false;
+  return true;
+}
+
+uint64_t convt_part_flops(const ConvTArgs &a0, int part) {
+  std::vector<AxisClass> cu;
+  if (!convt_axes(a0, cu)) return 0;
+  ConvTArgs a = a0;
+  if (convt_classes(a, 256, 64, cu, cu, 4 * part) < 0) return 0;   // class sizes do not depend on the tile
+  uint64_t f = 0;   // every position times the taps that reach it: the necessary multiply-adds
+  for (int c = 0; c < a.n_cls; ++c)
+    f += 2ull * (uint64_t)a.cls[c].M * (uint64_t)(a.cls[c].nty * a.cls[c].ntx) * (uint64_t)a.C_out * (uint64_t)a.C_in;
+  return f;
+}
+
+int convt_launches(const ConvTArgs &a) {
+  std::vector<AxisClass> cu;
+  if (!convt_axes(a, cu)) return -1;
+  return ((int)(cu.size() * cu.size()) + 3) / 4;
+}
+
+hipError_t launch_convt_part(const ConvTArgs &a0, int part, hipStream_t s) {
+  std::vector<AxisClass> cu;
+  if (!convt_axes(a0, cu)) return hipErrorInvalidValue;
+  const std::vector<AxisClass> &cw = cu;   // square windows
   const int total = (int)(cu.size() * cw.size());
-  for (int first = 0; first < total; first += 4) {
-    ConvTArgs a = a0;
-    if (a.N_pad % 128 == 0) {   // 128 x 128 tiles, 2 x 2 waves of 64 x 64
-      const int64_t blk = convt_classes(a, 128, 128, cu, cw, first);
-      if (blk < 0) return hipErrorInvalidValue;
-      if (blk > 0) hipLaunchKernelGGL((k_convt<128, 128, 16, 2, 2, 3>), dim3((unsigned)blk), dim3(256), 0, s, a);
-    } else {                    // 256 x 64 tiles, 4 x 1 waves of 64 x 64
-      const int64_t blk = convt_classes(a, 256, 64, cu, cw, first);
-      if (blk < 0) return hipErrorInvalidValue;
-      if (blk > 0) hipLaunchKernelGGL((k_convt<256, 64, 16, 4, 1, 3>), dim3((unsigned)blk), dim3(256), 0, s, a);
-    }
-    const hipError_t e = hipGetLastError();
+  const int first = 4 * part;
+  if (first < 0 || first >= total) return hipErrorInvalidValue;
+  ConvTArgs a = a0;
+  int64_t blk;
+  if (a.N_pad % 128 == 0) {   // 128 x 128 tiles, 2 x 2 waves of 64 x 64
+    blk = convt_classes(a, 128, 128, cu, cw, first);
+    if (blk < 0) return hipErrorInvalidValue;
+    if (blk > 0) hipLaunchKernelGGL((k_convt<128, 128, 16, 2, 2, 3>), dim3((unsigned)blk), dim3(256), 0, s, a);
+  } else {                    // 256 x 64 tiles, 4 x 1 waves of 64 x 64
+    blk = convt_classes(a, 256, 64, cu, cw, first);
+    if (blk < 0) return hipErrorInvalidValue;
+    if (blk > 0) hipLaunchKernelGGL((k_convt<256, 64, 16, 4, 1, 3>), dim3((unsigned)blk), dim3(256), 0, s, a);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_convt(const ConvTArgs &a, hipStream_t s) {
+  const int n = convt_launches(a);
+  if (n < 0) return hipErrorInvalidValue;
+  for (int k = 0; k < n; ++k) {
+    const hipError_t e = launch_convt_part(a, k, s);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;

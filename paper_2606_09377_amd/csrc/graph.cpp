@@ -785,13 +785,15 @@ vcr_status run_pass(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &pp, int 
         a.bias = st.bias_off >= 0 ? g->bias_arena + st.bias_off : nullptr;
         a.out = slot(st.dst);
         a.part = bf.part;
-        const uint64_t cf = 2ull * (uint64_t)R * a.S_out * a.S_out * 9ull * (uint64_t)nd.C * (uint64_t)nd.Ci;
-        {
-          const vcr_status st2 = timed_launch(c, s, 1, cf, [&] { return launch_convt(a, s); });
+        const int parts = convt_launches(a);
+        if (parts < 0) return fail(c, VCR_ERR_UNSUPPORTED, "internal: transposed convolution shape");
+        for (int k = 0; k < parts; ++k) {
+          const uint64_t cf = convt_part_flops(a, k);
+          const vcr_status st2 = timed_launch(c, s, 1, cf, [&] { return launch_convt_part(a, k, s); });
           if (st2 != VCR_OK) return st2;
+          *flops += cf;
         }
         HIP_TRY(c, launch_rowsum_win(bf.beta, bf.part, a.N_pad / 64, a.M_pad, R, a.S_in * a.S_in, s));
-        *flops += cf;
         break;
       }
       case ST_STEM: {
