@@ -143,3 +143,54 @@ def test_planner_chunks_under_a_workspace_cap(vc):
     # subdomains: 4096 domains x 18 rows in one chunk
     ctx.load_net(wl.net)
     assert ctx.workspace_bytes(1, 9, 4096) >= 2 * 4096 * 18 * 1024 * 4
+
+
+def test_alpha_beta_bab_argument_validation(vc):
+    """alpha-CROWN, beta-CROWN and the branch-and-bound loop check their options before any
+    device work (a validation-only context then reports VCR_ERR_STATE)."""
+    ctx = vc.Ctx(-1)
+    wl = random_mlp(3, [20, 30, 30, 5], 1, 0.1)
+    ctx.load_net(wl.net)
+    lib = ctx.lib
+    assert lib.vcr_relu_neurons(ctx.h) == 60
+    x, C, lb, ub = _buf(20), _buf(4 * 5), _buf(4), _buf(4)
+    p = lambda a: ctypes.c_void_p(a.ctypes.data)  # noqa: E731
+
+    def alpha(**kw):
+        o = vc.VcrAlphaOpts(kw.get("iters", 5), kw.get("lr", 0.1), kw.get("b1", 0.9), kw.get("b2", 0.999),
+                            kw.get("eps", 1e-8), None, None, None, kw.get("lh"), kw.get("uh"))
+        return lib.vcr_alpha_crown_bounds(ctx.h, p(x), 1, ctypes.c_float(0.1), p(C), 4, ctypes.byref(o), p(lb), p(ub))
+
+    assert alpha() == vc.VCR_ERR_STATE
+    for kw in ({"iters": -1}, {"lr": 0.0}, {"lr": float("inf")}, {"b1": 1.0}, {"b2": -0.1}, {"eps": 0.0},
+               {"lh": lb.ctypes.data}):
+        assert alpha(**kw) == vc.VCR_ERR_ARG, kw
+    assert lib.vcr_alpha_crown_bounds(ctx.h, p(x), 1, ctypes.c_float(0.1), p(C), 4, None, p(lb), p(ub)) == vc.VCR_ERR_ARG
+
+    rid, neu, sg = _buf(8, np.int32), _buf(8, np.int32), _buf(8, np.int8)
+    sp = vc.VcrSplits(4, 2, rid.ctypes.data, neu.ctypes.data, sg.ctypes.data)
+
+    def beta(splits=sp, **kw):
+        o = vc.VcrBetaOpts(kw.get("iters", 5), kw.get("la", 0.1), kw.get("lb", 0.05), 0.9, 0.999, 1e-8, None, None)
+        s = ctypes.byref(splits) if splits is not None else None
+        return lib.vcr_beta_crown_bounds(ctx.h, p(x), ctypes.c_float(0.1), p(C), 4, s, ctypes.byref(o), p(lb), p(ub))
+
+    assert beta() == vc.VCR_ERR_STATE
+    assert beta(splits=None) == vc.VCR_ERR_ARG
+    assert beta(la=0.0) == vc.VCR_ERR_ARG and beta(lb=-1.0) == vc.VCR_ERR_ARG and beta(iters=-2) == vc.VCR_ERR_ARG
+    assert beta(splits=vc.VcrSplits(0, 2, rid.ctypes.data, neu.ctypes.data, sg.ctypes.data)) == vc.VCR_ERR_ARG
+
+    def bab(batch=4, rounds=3, order=None):
+        bo = vc.VcrBetaOpts(5, 0.1, 0.05, 0.9, 0.999, 1e-8, None, None)
+        o = vc.VcrBabOpts(batch, rounds, bo, None, None, 0)
+        keep = None
+        if order is not None:
+            keep = (np.array([a for a, _ in order], np.int32), np.array([b for _, b in order], np.int32))
+            o.order_relu, o.order_neuron, o.order_len = keep[0].ctypes.data, keep[1].ctypes.data, len(order)
+        res = vc.VcrBabResult()
+        return lib.vcr_bab_verify(ctx.h, p(x), ctypes.c_float(0.1), p(C), 4, ctypes.byref(o), ctypes.byref(res), None)
+
+    assert bab() == vc.VCR_ERR_STATE
+    assert bab(order=[(0, 3), (1, 29)]) == vc.VCR_ERR_STATE
+    assert bab(batch=0) == vc.VCR_ERR_ARG and bab(rounds=-1) == vc.VCR_ERR_ARG
+    assert bab(order=[(2, 0)]) == vc.VCR_ERR_ARG and bab(order=[(1, 30)]) == vc.VCR_ERR_ARG
