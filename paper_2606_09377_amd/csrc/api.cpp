@@ -1126,6 +1126,8 @@ vcr_status vcr_alpha_crown_bounds(vcr_ctx *c, const float *x0, int32_t B, float 
   return after_call(c, crown_impl(c, x0, B, eps, C, m, nullptr, lb, ub, &ac), t0);
 }
 
+}  // extern "C"
+
 namespace {
 
 vcr_status check_splits(vcr_ctx *c, const vcr_splits *splits, int32_t m) {
@@ -1183,6 +1185,8 @@ struct Split {
 };
 
 }  // namespace
+
+extern "C" {
 
 vcr_status vcr_beta_crown_bounds(vcr_ctx *c, const float *x0, float eps, const float *C, int32_t m,
                                  const vcr_splits *splits, const vcr_beta_opts *opts, float *lb, float *ub) {

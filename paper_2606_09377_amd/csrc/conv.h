@@ -65,8 +65,9 @@ struct StemArgs {
   int32_t S_out, C_out;
   const float *W;          // [C_out][C_in][3][3]
   int32_t C_in, S_in, H_in, stride, delta;
-  int32_t R, cc;           // rows, channels staged per LDS pass (chosen by launch_stem)
-  int32_t rpw, lg_cc;      // rows per workgroup, log2(cc) (chosen by launch_stem)
+  int32_t R;               // rows
+  int32_t rpw, strip, n_strips;  // rows per workgroup, destination rows per strip, strips
+                                 // per row (chosen by launch_stem)
   const int4 *rows;
   int32_t dense, scale, h_in;
   const float *c0, *r0;    // box centre / radius, CHW per unit

@@ -52,6 +52,9 @@ __device__ __forceinline__ int lds_swz(int row) {
   return (row / RPG) & (CPR - 1);
 }
 
+// Source of the zeros that taps outside the source window load
+__device__ __attribute__((aligned(16))) const float g_zero4[4] = {0.f, 0.f, 0.f, 0.f};
+
 template <int BM, int BN, int BK, int WM, int WN, int MINB>
 __global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
   static_assert(BK == 16 || BK == 32, "LDS swizzle assumes 4 or 8 chunks per row");
@@ -95,10 +98,13 @@ __global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
   }
   const float *Bg = p.Bt + (int64_t)(n0 + lrow) * p.ldb + lcol;
   f32x4 ra[QA], rb[QB];
+  // K order: channel block outer, tap inner, so the shifted re-reads of one source block
+  // follow each other within a few K tiles (they hit the caches instead of HBM)
+  const int ntap = cl.nty * cl.ntx;
   auto gload = [&](int kt) {
-    const int k0 = kt * BK;
-    const int t = k0 / p.C_out;
-    const int co0 = k0 - t * p.C_out;
+    const int cb = kt / ntap;
+    const int t = kt - cb * ntap;
+    const int co0 = cb * BK;
     const int ty = t / cl.ntx, tx = t - ty * cl.ntx;
     const int ky = cl.ky0 + cl.kys * ty, kx = cl.kx0 + cl.kxs * tx;
     const int dy = (cl.u0 + p.delta - ky) >> sh, dx = (cl.w0 + p.delta - kx) >> sh;   // exact
@@ -107,10 +113,10 @@ __global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
     for (int q = 0; q < QA; ++q) {
       const int yy = ys[q] + dy, xx = xs[q] + dx;
       const bool ok = (unsigned)yy < (unsigned)p.S_out && (unsigned)xx < (unsigned)p.S_out;
-      const int off = ok ? (yy * p.S_out + xx) * p.C_out + co : lcol;
-      const f32x4 v = *reinterpret_cast<const f32x4 *>(a_row[q] + off);
-      const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-      ra[q] = ok ? v : z;
+      // positions outside the source window read a zero block: no select on the loaded
+      // value, so the wait for the load moves past the MFMAs to the LDS store
+      const float *src = ok ? a_row[q] + (yy * p.S_out + xx) * p.C_out + co : g_zero4;
+      ra[q] = *reinterpret_cast<const f32x4 *>(src);
     }
     const int kb = (3 * ky + kx) * p.C_out + co0;
 #pragma unroll
@@ -384,159 +390,170 @@ hipError_t launch_convt(const ConvTArgs &a, hipStream_t s) {
 }
 
 // ------------------------------------------------------------------------------------
-// Transposed stem convolution onto the network input (few input channels, so VALU), fused
-// with the concretization: for every input-window position (r, u, w) and channel ci,
-//   a = sum_{tap, co} A_out[r][u'][w'][co] W[co][ci][ky][kx]
+// Transposed stem convolution onto the network input (at most 4 input channels), fused with
+// the concretization.  With few input channels the contraction is regrouped so that the
+// matrix cores see a useful N: per source position s of a coefficient row
+//   G[s][ci * 9 + tap] = sum_co A_out[r][s][co] W[co][ci][tap]        (GEMM, N = 9 C_in, K = C_out)
+// and every input-window position (u, w) then gathers the taps that reach it,
+//   a[ci] = sum over taps (ky, kx) reaching (u, w) of G[s(u, w, ky, kx)][ci * 9 + 3 ky + kx]
 //   part[(r, u, w)] = sum_ci a c[unit][ci][gy][gx] - |a| r[unit][ci][gy][gx]   (inside the image)
-// One workgroup per coefficient row; the row's source window is staged through LDS
-// channel-major (odd row pitch, so neighbouring positions hit neighbouring banks) in channel
-// chunks, together with the chunk's weights, which every lane reads at the same address.
-template <int CIN, int MAXP>
-__global__ __launch_bounds__(256, MAXP >= 4 ? 3 : 4) void k_stem(const StemArgs p) {
-  // LDS: rpw rows x cc channels x pitch; cell S_out^2 of every channel row is a zero that
-  // invalid taps read, so the inner loop has no branches
-  extern __shared__ float lds[];
-  const int S_out2 = p.S_out * p.S_out;
-  const int pitch = (S_out2 + 1) | 1;
+// W's own layout [co][ci][3][3] is the B operand [K][N].  A workgroup takes several whole
+// rows (small windows) or a strip of destination rows of one row (large windows); the
+// source positions' G stays in LDS between the two phases.
+template <int CIN>
+__global__ __launch_bounds__(256, 2) void k_stem(const StemArgs p) {
+  constexpr int NB = CIN * 9 > 32 ? 2 : 1;   // 32-column MFMA blocks of N
+  constexpr int GP = 32 * NB + 1;            // G row pitch (odd: the gather reads hit distinct banks)
+  constexpr int NW = CIN * 9;
+  extern __shared__ __attribute__((aligned(16))) float lds[];
+  const int WTP = p.C_out + 4;               // transposed weights, k contiguous
+  float *wt = lds;                           // [32 NB][WTP]
+  float *G = lds + 32 * NB * WTP;            // [source positions][GP]
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int rg = blockIdx.x / p.n_strips, st = blockIdx.x - rg * p.n_strips;
+  const int r0 = rg * p.rpw;
+  const int rows = min(p.rpw, p.R - r0);
+  const int u_lo = st * p.strip, u_hi = min(p.S_in, u_lo + p.strip);
+  // source rows reached from destination rows [u_lo, u_hi): y = (u + delta - ky) / stride
+  const int lo_num = max(0, u_lo + p.delta - 2);
+  const int y_lo = (lo_num + p.stride - 1) / p.stride;
+  const int y_hi = min(p.S_out - 1, (u_hi - 1 + p.delta) / p.stride);
+  const int n_row_src = (y_hi >= y_lo ? y_hi - y_lo + 1 : 0) * p.S_out;
+  const int n_src = rows * n_row_src;
+
+  for (int i = tid; i < 32 * NB * p.C_out; i += 256) {
+    const int n = i / p.C_out, k = i - n * p.C_out;
+    wt[n * WTP + k] = n < NW ? p.W[(int64_t)k * NW + n] : 0.f;
+  }
+  __syncthreads();
+
+  // ---- G = A_src W: each wave takes 32-position blocks; lane (r32, half) feeds the MFMAs
+  // with 16 consecutive k of its position per 32-k chunk, identically for both operands
+  const int r32 = lane & 31, half = lane >> 5;
+  const int n_blk = (n_src + 31) / 32;
+  const int KC = p.C_out / 32;
+  for (int blk = wave; blk < n_blk; blk += 4) {
+    // positions past the last one repeat it: their G rows are never gathered
+    const int pi = min(blk * 32 + r32, n_src - 1);
+    const int rl = pi / n_row_src, sp = pi - rl * n_row_src;
+    const float *src = p.A + (int64_t)(r0 + rl) * p.row_stride_out +
+                       ((int64_t)y_lo * p.S_out + sp) * p.C_out + half * 16;
+    f32x16 acc[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[j][v] = 0.f;
+    f32x4 a[4];
+#pragma unroll
+    for (int h = 0; h < 4; ++h) a[h] = *reinterpret_cast<const f32x4 *>(src + 4 * h);
+    for (int kc = 0; kc < KC; ++kc) {
+      f32x4 an[4];
+      if (kc + 1 < KC) {
+#pragma unroll
+        for (int h = 0; h < 4; ++h) an[h] = *reinterpret_cast<const f32x4 *>(src + (kc + 1) * 32 + 4 * h);
+      }
+      f32x4 b[NB][4];
+#pragma unroll
+      for (int j = 0; j < NB; ++j)
+#pragma unroll
+        for (int h = 0; h < 4; ++h)
+          b[j][h] = *reinterpret_cast<const f32x4 *>(wt + (32 * j + r32) * WTP + kc * 32 + half * 16 + 4 * h);
+#pragma unroll
+      for (int h = 0; h < 4; ++h)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+          for (int j = 0; j < NB; ++j) acc[j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[h][e], b[j][h][e], acc[j], 0, 0, 0);
+      if (kc + 1 < KC) {
+#pragma unroll
+        for (int h = 0; h < 4; ++h) a[h] = an[h];
+      }
+    }
+    // lane holds rows 8 g + 4 half + t (v = 4 g + t) of column 32 j + r32
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v)
+        G[(blk * 32 + (v >> 2) * 8 + half * 4 + (v & 3)) * GP + 32 * j + r32] = acc[j][v];
+  }
+  __syncthreads();
+
+  // ---- gather the taps of every destination position and concretize
+  const int nu = u_hi - u_lo;
+  const int per_rl = nu * p.S_in;
   const int S_in2 = p.S_in * p.S_in;
-  const int r0 = blockIdx.x * p.rpw;
-  constexpr int WP = (CIN * 9 + 3) & ~3;
-  float *wlds = lds + ((p.rpw * p.cc * pitch + 3) & ~3);   // after the rows
-  const float *__restrict__ Wg = p.W;
-  float acc[MAXP][CIN];
-  int sidx[MAXP][9];
-  int lbase[MAXP];
-  int rloc[MAXP], ppos[MAXP];
-  bool live[MAXP];
-#pragma unroll
-  for (int k = 0; k < MAXP; ++k) {
-    const int j = threadIdx.x + k * 256;
-    const int rl = j / S_in2, pos = j - (j / S_in2) * S_in2;
-    rloc[k] = rl;
-    ppos[k] = pos;
-    const bool row_ok = rl < p.rpw && r0 + rl < p.R;
-    const int4 an = row_ok ? p.rows[r0 + rl] : make_int4(0, 0, 0, 0);
-    const int u = pos / p.S_in, w = pos - (pos / p.S_in) * p.S_in;
-    const int gy = p.dense ? u : an.y * p.scale - p.h_in + u;
-    const int gx = p.dense ? w : an.z * p.scale - p.h_in + w;
-    live[k] = row_ok && gy >= 0 && gx >= 0 && gy < p.H_in && gx < p.H_in;
-    lbase[k] = (row_ok ? rl : 0) * p.cc * pitch;
-#pragma unroll
-    for (int tap = 0; tap < 9; ++tap) {
-      const int ky = tap / 3, kx = tap % 3;
-      int yy = u + p.delta - ky, xx = w + p.delta - kx;
-      bool ok = live[k];
-      if (p.stride == 2) {
-        ok = ok && ((yy | xx) & 1) == 0;
-        yy >>= 1;
-        xx >>= 1;
-      }
-      ok = ok && yy >= 0 && xx >= 0 && yy < p.S_out && xx < p.S_out;
-      sidx[k][tap] = ok ? yy * p.S_out + xx : S_out2;
-    }
-#pragma unroll
-    for (int ci = 0; ci < CIN; ++ci) acc[k][ci] = 0.f;
-  }
-  // zero cells (staging never writes them)
-  for (int i = threadIdx.x; i < p.rpw * p.cc; i += 256) lds[i * pitch + S_out2] = 0.f;
-  const int per_row = S_out2 * p.cc;
-  for (int c0 = 0; c0 < p.C_out; c0 += p.cc) {
-    __syncthreads();
-    // stage cc channels of each row: four independent loads in flight per thread
-    for (int rl = 0; rl < p.rpw && r0 + rl < p.R; ++rl) {
-      const float *src = p.A + (int64_t)(r0 + rl) * p.row_stride_out + c0;
-      float *dst = lds + rl * p.cc * pitch;
-      for (int e0 = threadIdx.x; e0 < per_row; e0 += 1024) {
-        float v[4];
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          const int e = e0 + 256 * k;
-          v[k] = e < per_row ? src[(e >> p.lg_cc) * p.C_out + (e & (p.cc - 1))] : 0.f;
-        }
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          const int e = e0 + 256 * k;
-          if (e < per_row) dst[(e & (p.cc - 1)) * pitch + (e >> p.lg_cc)] = v[k];
-        }
-      }
-    }
-    // the chunk's weights, WP floats per channel (wave-uniform reads, broadcast from LDS)
-    for (int i = threadIdx.x; i < p.cc * CIN * 9; i += 256) {
-      const int c = i / (CIN * 9), q = i - c * (CIN * 9);
-      wlds[c * WP + q] = Wg[(int64_t)(c0 + c) * CIN * 9 + q];
-    }
-    __syncthreads();
-    for (int c = 0; c < p.cc; ++c) {
-      float wv[WP];
-#pragma unroll
-      for (int q = 0; q < WP; q += 4) *reinterpret_cast<float4 *>(&wv[q]) = *reinterpret_cast<const float4 *>(&wlds[c * WP + q]);
-#pragma unroll
-      for (int tap = 0; tap < 9; ++tap) {
-#pragma unroll
-        for (int k = 0; k < MAXP; ++k) {
-          const float a = lds[lbase[k] + c * pitch + sidx[k][tap]];
-#pragma unroll
-          for (int ci = 0; ci < CIN; ++ci) acc[k][ci] += a * wv[ci * 9 + tap];
-        }
-      }
-    }
-  }
-#pragma unroll
-  for (int k = 0; k < MAXP; ++k) {
-    const int rl = rloc[k], pos = ppos[k];
-    if (rl >= p.rpw || r0 + rl >= p.R) continue;
+  for (int d = tid; d < rows * per_rl; d += 256) {
+    const int rl = d / per_rl, rem = d - rl * per_rl;
+    const int uu = rem / p.S_in;
+    const int u = u_lo + uu, w = rem - uu * p.S_in;
     const int4 an = p.rows[r0 + rl];
-    const int u = pos / p.S_in, w = pos - (pos / p.S_in) * p.S_in;
     const int gy = p.dense ? u : an.y * p.scale - p.h_in + u;
     const int gx = p.dense ? w : an.z * p.scale - p.h_in + w;
     float part = 0.f;
-    if (live[k]) {
+    if (gy >= 0 && gx >= 0 && gy < p.H_in && gx < p.H_in) {
+      float a[CIN];
+#pragma unroll
+      for (int ci = 0; ci < CIN; ++ci) a[ci] = 0.f;
+#pragma unroll
+      for (int ky = 0; ky < 3; ++ky) {
+        int yy = u + p.delta - ky;
+        if (yy < 0 || (yy & (p.stride - 1))) continue;
+        yy /= p.stride;
+        if (yy >= p.S_out) continue;
+#pragma unroll
+        for (int kx = 0; kx < 3; ++kx) {
+          int xx = w + p.delta - kx;
+          if (xx < 0 || (xx & (p.stride - 1))) continue;
+          xx /= p.stride;
+          if (xx >= p.S_out) continue;
+          const float *g = G + (rl * n_row_src + (yy - y_lo) * p.S_out + xx) * GP + 3 * ky + kx;
+#pragma unroll
+          for (int ci = 0; ci < CIN; ++ci) a[ci] += g[9 * ci];
+        }
+      }
 #pragma unroll
       for (int ci = 0; ci < CIN; ++ci) {
         const int64_t bi = (int64_t)an.x * p.ld_box + ((int64_t)ci * p.H_in + gy) * p.H_in + gx;
-        const float a = acc[k][ci];
-        part += a * p.c0[bi] - fabsf(a) * p.r0[bi];
+        part += a[ci] * p.c0[bi] - fabsf(a[ci]) * p.r0[bi];
       }
     }
-    p.part[(int64_t)(r0 + rl) * S_in2 + pos] = part;
+    p.part[(int64_t)(r0 + rl) * S_in2 + u * p.S_in + w] = part;
   }
 }
 
 template <int CIN>
 hipError_t launch_stem_t(StemArgs a, hipStream_t s) {
-  const int S_in2 = a.S_in * a.S_in;
-  const int pitch = (a.S_out * a.S_out + 1) | 1;
-  // slots per thread and rows per workgroup with the best lane use
-  int best_p = 0, best_r = 0;
-  double best_u = 0.0;
-  for (int mp : {1, 2, 4}) {
-    const int rpw = 256 * mp / S_in2;
-    if (rpw < 1) continue;
-    const double util = (double)rpw * S_in2 / (256.0 * mp);
-    if (util > best_u + 1e-9) {
-      best_u = util;
-      best_p = mp;
-      best_r = rpw;
+  constexpr int NB = CIN * 9 > 32 ? 2 : 1;
+  constexpr int GP = 32 * NB + 1;
+  if (a.C_out <= 0 || a.C_out % 32 || a.R <= 0 || (a.stride != 1 && a.stride != 2) || a.S_out <= 0 || a.S_in <= 0)
+    return hipErrorInvalidValue;
+  const int64_t wt_floats = 32 * NB * (int64_t)(a.C_out + 4);
+  const int64_t src_max = ((16384 - wt_floats) / GP) & ~(int64_t)31;   // 64 KB of LDS per workgroup
+  if (src_max < 32) return hipErrorInvalidValue;
+  auto src_positions = [&](int u_lo, int u_hi) {   // the kernel's source-row range, times S_out
+    const int y_lo = (std::max(0, u_lo + a.delta - 2) + a.stride - 1) / a.stride;
+    const int y_hi = std::min(a.S_out - 1, (u_hi - 1 + a.delta) / a.stride);
+    return (int64_t)(y_hi >= y_lo ? y_hi - y_lo + 1 : 0) * a.S_out;
+  };
+  const int64_t full = src_positions(0, a.S_in);
+  if (full <= src_max) {   // whole rows
+    a.rpw = (int32_t)std::max<int64_t>(1, src_max / std::max<int64_t>(full, 1));
+    a.strip = a.S_in;
+  } else {                 // one row, strips of destination rows
+    a.rpw = 1;
+    a.strip = 0;
+    for (int h = a.S_in; h >= 1 && !a.strip; --h) {
+      bool fits = true;
+      for (int u0 = 0; u0 < a.S_in && fits; u0 += h) fits = src_positions(u0, std::min(a.S_in, u0 + h)) <= src_max;
+      if (fits) a.strip = h;
     }
+    if (!a.strip) return hipErrorInvalidValue;
   }
-  if (!best_p) return hipErrorInvalidValue;
-  a.rpw = best_r;
-  constexpr int WP = (CIN * 9 + 3) & ~3;
-  // LDS floats: the rows' channel chunk plus the chunk's weights, within 64 KB
-  auto lds_floats = [&](int cc) { return (((int64_t)a.rpw * cc * pitch + 3) & ~(int64_t)3) + (int64_t)cc * WP; };
-  a.cc = a.C_out;
-  while (a.cc > 1 && (lds_floats(a.cc) > 16384 || a.C_out % a.cc)) a.cc /= 2;
-  if (lds_floats(a.cc) > 16384 || (a.cc & (a.cc - 1))) return hipErrorInvalidValue;
-  a.lg_cc = 0;
-  while ((1 << a.lg_cc) < a.cc) ++a.lg_cc;
-  const size_t lds = sizeof(float) * (size_t)lds_floats(a.cc);
-  const unsigned grid = (unsigned)((a.R + a.rpw - 1) / a.rpw);
-  if (best_p == 1)
-    hipLaunchKernelGGL((k_stem<CIN, 1>), dim3(grid), dim3(256), lds, s, a);
-  else if (best_p == 2)
-    hipLaunchKernelGGL((k_stem<CIN, 2>), dim3(grid), dim3(256), lds, s, a);
-  else
-    hipLaunchKernelGGL((k_stem<CIN, 4>), dim3(grid), dim3(256), lds, s, a);
+  a.n_strips = (a.S_in + a.strip - 1) / a.strip;
+  const int64_t grid = ((int64_t)a.R + a.rpw - 1) / a.rpw * a.n_strips;
+  if (grid > 0x7fffffff) return hipErrorInvalidValue;
+  const size_t lds = sizeof(float) * (size_t)(wt_floats + src_max * GP);
+  hipLaunchKernelGGL((k_stem<CIN>), dim3((unsigned)grid), dim3(256), lds, s, a);
   return hipGetLastError();
 }
 
@@ -600,23 +617,33 @@ hipError_t launch_init_conv(const ConvInitArgs &a, hipStream_t s) {
   return hipGetLastError();
 }
 
-// beta[r] += sum_{q < per_row} sum_p part[p][r * per_row + q]   (fixed order)
+// Constant terms of a pass: beta[r] += sum over the row's positions and the column parts.
+// G = 2^lg lanes share a row (lane j sums positions j, j + G, ... over all parts), then add
+// their sums by a fixed butterfly: consecutive lanes read consecutive positions.
 __global__ void k_rowsum_win(float *beta, const float *part, int32_t n_parts, int64_t M_pad, int64_t R,
-                             int32_t per_row) {
-  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (r >= R) return;
+                             int32_t per_row, int32_t lg) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t r = t >> lg;
+  const int G = 1 << lg, j = (int)(t & (G - 1));
   float s = 0.f;
-  for (int q = 0; q < per_row; ++q) {
-    const int64_t m = r * per_row + q;
-    for (int p = 0; p < n_parts; ++p) s += part[p * M_pad + m];
+  if (r < R) {
+    for (int q = j; q < per_row; q += G) {
+      const int64_t m = r * per_row + q;
+      for (int p = 0; p < n_parts; ++p) s += part[p * M_pad + m];
+    }
   }
-  beta[r] += s;
+  for (int o = G >> 1; o > 0; o >>= 1) s += __shfl_xor(s, o);   // every lane takes part
+  if (r < R && j == 0) beta[r] += s;
 }
 
 hipError_t launch_rowsum_win(float *beta, const float *part, int32_t n_parts, int64_t M_pad, int64_t R,
                              int32_t per_row, hipStream_t s) {
-  hipLaunchKernelGGL(k_rowsum_win, dim3((unsigned)((R + 255) / 256)), dim3(256), 0, s, beta, part, n_parts,
-                     M_pad, R, per_row);
+  if (R <= 0) return hipSuccess;
+  int lg = 0;
+  while (lg < 6 && (2 << lg) <= per_row) ++lg;
+  const int64_t n = R << lg;
+  hipLaunchKernelGGL(k_rowsum_win, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, beta, part, n_parts, M_pad, R,
+                     per_row, lg);
   return hipGetLastError();
 }
 

@@ -50,6 +50,46 @@ def conv_chain(seed, batch=2, eps=0.02):
     return Workload("convchain", net, x0, np.float32(eps), margin_spec(net, x0))
 
 
+def stem_net(seed, cin, stride, hw, second=True, batch=1, eps=0.02):
+    """conv(cin -> 32, stride) -> ReLU [-> conv 32 -> 32 -> ReLU] -> flatten -> dense 12 -> ReLU
+    -> dense 4, on cin x hw x hw: the first convolution's transposed step (onto the input) in
+    its other shapes: 1, 2 and 4 input channels (4 needs two 32-column blocks), stride 2, and
+    whole-image rows larger than one workgroup's source buffer (split into strips)."""
+    rng = np.random.default_rng(seed)
+
+    def cw(co, ci):
+        return ((rng.standard_normal((co, ci, 3, 3)) * np.sqrt(2 / (ci * 9))).astype(np.float32),
+                (rng.standard_normal(co) * 0.05).astype(np.float32))
+
+    W0, b0 = cw(32, cin)
+    nodes = [Node("conv2d", -1, W=W0, b=b0, stride=stride, pad=1), Node("relu", 0)]
+    h = (hw - 1) // stride + 1
+    if second:
+        W1, b1 = cw(32, 32)
+        nodes += [Node("conv2d", 1, W=W1, b=b1, stride=1, pad=1), Node("relu", 2)]
+    nf = 32 * h * h
+    Wd = (rng.standard_normal((12, nf)) * np.sqrt(2 / nf)).astype(np.float32)
+    bd = (rng.standard_normal(12) * 0.05).astype(np.float32)
+    Wo = (rng.standard_normal((4, 12)) * np.sqrt(2 / 12)).astype(np.float32)
+    bo = (rng.standard_normal(4) * 0.05).astype(np.float32)
+    k = len(nodes)
+    nodes += [Node("flatten", k - 1), Node("dense", k, W=Wd, b=bd), Node("relu", k + 1),
+              Node("dense", k + 2, W=Wo, b=bo)]
+    net = Net((cin, hw, hw), nodes)
+    x0 = rng.random((batch, net.n_in)).astype(np.float32)
+    return Workload(f"stem{cin}s{stride}x{hw}", net, x0, np.float32(eps), margin_spec(net, x0))
+
+
+@pytest.mark.parametrize("cin,stride,hw,second", [(1, 2, 10, True), (2, 1, 8, True), (4, 2, 12, True),
+                                                  (4, 1, 16, False), (3, 1, 24, False)])
+def test_stem_shapes_all_bounds(cin, stride, hw, second):
+    wl = stem_net(305, cin, stride, hw, second)
+    log("case", wl.name)
+    ctx = gpu_ctx(wl.net)
+    lb, ub, layers = gpu_crown(ctx, wl)
+    check_input(wl.net, wl.x0[0], wl.eps, wl.C[0], lb[0], ub[0], [(l[0], u[0]) for l, u in layers], what=wl.name)
+
+
 @pytest.mark.parametrize("make", [lambda: small_resnet(301), lambda: conv_chain(302)], ids=["resnet8", "convchain"])
 def test_small_conv_nets_all_bounds(make):
     wl = make()
