@@ -53,9 +53,143 @@ __device__ __forceinline__ int lds_swz(int row) {
 }
 
 // Source of the zeros that taps outside the source window load
-__device__ __attribute__((aligned(16))) const float g_zero4[4] = {0.f, 0.f, 0.f, 0.f};
+__device__ __attribute__((aligned(16))) float g_zero4[4] = {0.f, 0.f, 0.f, 0.f};   // never written
 
-template <int BM, int BN, int BK, int WM, int WN, int MINB>
+// Epilogue shared by the transposed-convolution kernels: relaxation (or identity), residual,
+// constant terms per GEMM row for the tile m0.. of class cl, columns n0..; acc holds the
+// MB x NB 32 x 32 MFMA blocks of wave (wm, wn); scratch is >= 24 BM bytes of free LDS.
+template <int BM, int BN, int WM, int WN, bool RELU>
+__device__ __forceinline__ void convt_epilogue(const ConvTArgs &p, const ConvClass &cl,
+                                               const f32x16 (&acc)[BM / WM / 32][BN / WN / 32], int m0, int n0,
+                                               int nt, float *scratch) {
+  constexpr int MB = BM / WM / 32, NB = BN / WN / 32;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN, r32 = lane & 31;
+  const int nyx = cl.ny * cl.nx;
+  // Row information of the tile's BM GEMM rows is computed once, one row per thread, into
+  // LDS (the operand buffers are free after the main loop's last barrier).  A lane holds 16
+  // rows of each 32 x 32 block as 4 groups of 4 consecutive rows; the relaxation parameters
+  // and residual terms of the next group are loaded while the current group is relaxed and
+  // stored, so the epilogue waits on global memory about once instead of once per group.
+  static_assert(BM <= 256, "one row per thread");
+  int64_t *s_ob = reinterpret_cast<int64_t *>(scratch);      // output offset
+  int64_t *s_rb = s_ob + BM;                                 // residual offset, or -1
+  int *s_pb = reinterpret_cast<int *>(s_rb + BM);            // parameter offset, -1 outside the image
+  int *s_mo = s_pb + BM;                                     // partial-sum index, -1 past M
+  const int S_in2 = p.S_in * p.S_in;
+  const float4 *__restrict__ Pp = p.P_pos;
+  const float *__restrict__ resp = p.res;
+  float *__restrict__ outp = p.out;
+  if (tid < BM) {
+    const int m = m0 + tid;
+    const bool valid = m < cl.M;
+    const uint32_t r = valid ? fdiv((uint32_t)m, cl.div_yx) : 0u;
+    const uint32_t pos = valid ? (uint32_t)m - r * (uint32_t)nyx : 0u;
+    const uint32_t iy = fdiv(pos, cl.div_x);
+    const int u = cl.u0 + (int)iy * cl.ustep;
+    const int w = cl.w0 + (int)(pos - iy * (uint32_t)cl.nx) * cl.wstep;
+    const int4 an = p.rows[r];   // (unit, anchor y, anchor x, -)
+    const int gy = p.dense ? u : an.y * p.scale - p.h_in + u;
+    const int gx = p.dense ? w : an.z * p.scale - p.h_in + w;
+    const bool inside = valid && gy >= 0 && gx >= 0 && gy < p.H_in && gx < p.H_in;
+    const int du = u - p.res_off, dw = w - p.res_off;
+    s_mo[tid] = valid ? (int)r * S_in2 + u * p.S_in + w : -1;
+    s_ob[tid] = (int64_t)r * p.row_stride_in + ((int64_t)u * p.S_in + w) * p.C_in;
+    s_pb[tid] = inside ? ((an.x * p.H_in + gy) * p.H_in + gx) * p.C_in : -1;
+    s_rb[tid] = inside && resp && du >= 0 && dw >= 0 && du < p.res_S && dw < p.res_S
+                    ? (int64_t)r * p.res_row_stride + ((int64_t)du * p.res_S + dw) * p.C_in
+                    : -1;
+  }
+  __syncthreads();
+
+  const int half = lane >> 5;
+  const int lrow0 = wm * (BM / WM) + half * 4;   // + 32 i + 8 g + t
+  int ncol[NB];
+  float bn[NB];   // no ReLU at this node: identity, constant term a b[n]
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    ncol[j] = n0 + wn * (BN / WN) + j * 32 + r32;
+    bn[j] = (!RELU && ncol[j] < p.C_in) ? p.bias[ncol[j]] : 0.f;
+  }
+  // Parameters of group q = 4 i + g into buffer b, one group ahead of their use.  Lanes with
+  // nothing to load (outside the image, past C_in) read element 0, a finite parameter that
+  // meets a zero coefficient: no select on a loaded value, 32-bit offsets from one base.
+  constexpr int NG = MB * 4;
+  float4 prm[2][NB][4];
+  auto fetch = [&](int q, int b) {
+    const int lr = lrow0 + (q >> 2) * 32 + (q & 3) * 8;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int pb = s_pb[lr + t];
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        const uint32_t off = (ncol[j] < p.C_in && pb >= 0) ? (uint32_t)(pb + ncol[j]) : 0u;
+        if constexpr (RELU) prm[b][j][t] = Pp[off];
+      }
+    }
+  };
+  fetch(0, 0);
+  float rp[16];
+#pragma unroll
+  for (int q = 0; q < NG; ++q) {
+    const int i = q >> 2, g = q & 3, b = q & 1;
+    const int lr = lrow0 + i * 32 + g * 8;
+    float rv[NB][4];   // residual terms of this group, loaded before the next group's parameters
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int64_t rb = s_rb[lr + t];
+#pragma unroll
+      for (int j = 0; j < NB; ++j)
+        rv[j][t] = resp ? *((ncol[j] < p.C_in && rb >= 0) ? resp + rb + ncol[j] : g_zero4) : 0.f;
+    }
+    if (q + 1 < NG) fetch(q + 1, b ^ 1);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int pb = s_pb[lr + t], mo = s_mo[lr + t];
+      const int64_t ob = s_ob[lr + t];
+      float x = 0.f;
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        const float a = acc[i][j][g * 4 + t] + rv[j][t];
+        float ap = 0.f;
+        if (pb >= 0) {   // inside the image: relax (or identity) and constant terms
+          if constexpr (RELU) {
+            ap = a > 0.f ? a * prm[b][j][t].x : a * prm[b][j][t].y;
+            x += fminf(a, 0.f) * prm[b][j][t].z + ap * prm[b][j][t].w;
+          } else {
+            ap = a;
+            x += a * bn[j];
+          }
+        }
+        if (mo >= 0 && ncol[j] < p.C_in) outp[ob + ncol[j]] = ap;
+      }
+      rp[g * 4 + t] = x;
+    }
+    if (g == 3) {   // the lane's 16 rows of block i: reduce over the 32 columns, one partial each
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        float x = rp[v];
+        x += __shfl_xor(x, 16);
+        x += __shfl_xor(x, 8);
+        x += __shfl_xor(x, 4);
+        x += __shfl_xor(x, 2);
+        x += __shfl_xor(x, 1);
+        rp[v] = x;
+      }
+      if (r32 == 0) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int mo = s_mo[lrow0 + i * 32 + (v >> 2) * 8 + (v & 3)];
+          if (mo >= 0) p.part[(int64_t)(nt * WN + wn) * p.M_pad + mo] = rp[v];
+        }
+      }
+    }
+  }
+}
+
+// RELU: the destination node feeds a ReLU (relaxation parameters P_pos), else the identity
+// with a per-channel constant (bias).
+template <int BM, int BN, int BK, int WM, int WN, int MINB, bool RELU>
 __global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
   static_assert(BK == 16 || BK == 32, "LDS swizzle assumes 4 or 8 chunks per row");
   constexpr int CPR = BK / 4;                 // 16-byte chunks per tile row
@@ -171,92 +305,9 @@ __global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
     __syncthreads();
   }
 
-  // ---- epilogue ----------------------------------------------------------------------
-  // A lane holds 16 rows of each 32 x 32 block, as 4 groups of 4 consecutive GEMM rows.  Per
-  // group, every global load (row anchors, then relaxation parameters and residual terms for
-  // all of the lane's columns) is issued before the group's first store.
-  const int half = lane >> 5;
-  const int S_in2 = p.S_in * p.S_in;
-  const float4 *__restrict__ Pp = p.P_pos;
-  const float *__restrict__ resp = p.res;
-  const float *__restrict__ biasp = p.bias;
-  const int4 *__restrict__ rowsp = p.rows;
-  float *__restrict__ outp = p.out;
-#pragma unroll
-  for (int i = 0; i < MB; ++i) {
-    float rp[16];
-    int mo[16];
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      int pb[4];
-      int64_t ob[4], rb[4];
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const int m = m0 + wm * (BM / WM) + i * 32 + g * 8 + half * 4 + t;
-        const bool valid = m < cl.M;
-        const uint32_t r = valid ? fdiv((uint32_t)m, cl.div_yx) : 0u;
-        const uint32_t pos = valid ? (uint32_t)m - r * (uint32_t)nyx : 0u;
-        const uint32_t iy = fdiv(pos, cl.div_x);
-        const int u = cl.u0 + (int)iy * cl.ustep;
-        const int w = cl.w0 + (int)(pos - iy * (uint32_t)cl.nx) * cl.wstep;
-        const int4 an = rowsp[r];   // (unit, anchor y, anchor x, -)
-        const int gy = p.dense ? u : an.y * p.scale - p.h_in + u;
-        const int gx = p.dense ? w : an.z * p.scale - p.h_in + w;
-        const bool inside = valid && gy >= 0 && gx >= 0 && gy < p.H_in && gx < p.H_in;
-        const int du = u - p.res_off, dw = w - p.res_off;
-        mo[g * 4 + t] = valid ? (int)r * S_in2 + u * p.S_in + w : -1;
-        ob[t] = (int64_t)r * p.row_stride_in + ((int64_t)u * p.S_in + w) * p.C_in;
-        pb[t] = inside ? ((an.x * p.H_in + gy) * p.H_in + gx) * p.C_in : -1;
-        rb[t] = inside && resp && du >= 0 && dw >= 0 && du < p.res_S && dw < p.res_S
-                    ? (int64_t)r * p.res_row_stride + ((int64_t)du * p.res_S + dw) * p.C_in
-                    : -1;
-      }
-      float4 prm[NB][4];
-      float rv[NB][4];
-#pragma unroll
-      for (int j = 0; j < NB; ++j) {
-        const int n = n0 + wn * (BN / WN) + j * 32 + r32;
-        const bool nok = n < p.C_in;
-        const float bn = (!Pp && nok) ? biasp[n] : 0.f;
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          prm[j][t] = (Pp && nok && pb[t] >= 0) ? Pp[pb[t] + n] : make_float4(1.f, 1.f, 0.f, bn);
-          rv[j][t] = (nok && rb[t] >= 0) ? resp[rb[t] + n] : 0.f;
-        }
-      }
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        float x = 0.f;
-#pragma unroll
-        for (int j = 0; j < NB; ++j) {
-          const int n = n0 + wn * (BN / WN) + j * 32 + r32;
-          const float a = acc[i][j][g * 4 + t] + rv[j][t];
-          float ap = 0.f;
-          if (pb[t] >= 0) {   // inside the image: relax (or identity) and constant terms
-            ap = a > 0.f ? a * prm[j][t].x : a * prm[j][t].y;
-            x += fminf(a, 0.f) * prm[j][t].z + ap * prm[j][t].w;
-          }
-          if (mo[g * 4 + t] >= 0 && n < p.C_in) outp[ob[t] + n] = ap;
-        }
-        rp[g * 4 + t] = x;
-      }
-    }
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      float x = rp[v];
-      x += __shfl_xor(x, 16);
-      x += __shfl_xor(x, 8);
-      x += __shfl_xor(x, 4);
-      x += __shfl_xor(x, 2);
-      x += __shfl_xor(x, 1);
-      rp[v] = x;
-    }
-    if (r32 == 0) {
-#pragma unroll
-      for (int v = 0; v < 16; ++v)
-        if (mo[v] >= 0) p.part[(int64_t)(nt * WN + wn) * p.M_pad + mo[v]] = rp[v];
-    }
-  }
+  // ---- epilogue (the operand buffers are free after the main loop's last barrier) ----
+  static_assert(24 * BM <= (int)sizeof(As), "epilogue row information must fit the A buffers");
+  convt_epilogue<BM, BN, WM, WN, RELU>(p, cl, acc, m0, n0, nt, &As[0][0]);
 }
 
 // Classes of one axis: positions u of the destination window with the same taps ky, as an
@@ -293,15 +344,57 @@ static bool axis_classes(int S_in, int S_out, int stride, int delta, std::vector
   return true;
 }
 
-// Fills the classes for BM-row tiles (up to 4 per launch, from class `first`); returns the
-// number of workgroups (or -1) and the number of classes in all.
-static int64_t convt_classes(ConvTArgs &a, int BM, int BN, const std::vector<AxisClass> &cu,
-                             const std::vector<AxisClass> &cw, int first) {
-  if (a.C_out % 32 || a.R <= 0 || a.N_pad % BN || a.N_pad <= 0 || (a.stride != 1 && a.stride != 2)) return -1;
-  if ((int64_t)a.R * a.S_in * a.S_in > a.M_pad) return -1;
+// The classes of a transposed convolution (axis classes of rows times those of columns) and
+// their dispatches, up to four consecutive classes each.
+struct ConvtDispatch {
+  std::vector<int> cls;   // indices into the class list
+};
+
+static bool convt_axes(const ConvTArgs &a, std::vector<AxisClass> &cu) {
+  if (!axis_classes(a.S_in, a.S_out, a.stride, a.delta, cu) || cu.empty()) return false;
+  for (const AxisClass &c : cu)   // the gather's row offset assumes ustep = stride for n > 1
+    if (c.n > 1 && c.ustep != a.stride) return false;
+  return true;
+}
+
+static ConvClass class_geometry(const std::vector<AxisClass> &cu, int idx) {
+  const AxisClass &yu = cu[idx / cu.size()], &xw = cu[idx % cu.size()];   // square windows
+  ConvClass k{};
+  k.u0 = yu.u0;
+  k.ustep = yu.ustep;
+  k.ny = yu.n;
+  k.ky0 = yu.k0;
+  k.kys = yu.ks;
+  k.nty = yu.nk;
+  k.w0 = xw.u0;
+  k.wstep = xw.ustep;
+  k.nx = xw.n;
+  k.kx0 = xw.k0;
+  k.kxs = xw.ks;
+  k.ntx = xw.nk;
+  return k;
+}
+
+static bool convt_plan(const ConvTArgs &a, std::vector<AxisClass> &cu, std::vector<ConvtDispatch> &plan) {
+  plan.clear();
+  if (a.C_out % 32 || a.R <= 0 || a.N_pad <= 0 || (a.stride != 1 && a.stride != 2)) return false;
+  if ((int64_t)a.R * a.S_in * a.S_in > a.M_pad) return false;
+  if (!convt_axes(a, cu)) return false;
+  const int total = (int)(cu.size() * cu.size());
+  for (int f = 0; f < total; f += 4) {
+    ConvtDispatch d;
+    for (int idx = f; idx < std::min(total, f + 4); ++idx) d.cls.push_back(idx);
+    plan.push_back(d);
+  }
+  return true;
+}
+
+// Fills a.cls for dispatch d with BM-row tiles and n_nt column tiles; returns the number of
+// workgroups (or -1).
+static int64_t convt_fill(ConvTArgs &a, const std::vector<AxisClass> &cu, const ConvtDispatch &d, int BM, int BN) {
+  if (a.N_pad % BN) return -1;
   const int n_nt = a.N_pad / BN;
-  const int total = (int)(cu.size() * cw.size());
-  a.n_cls = std::min(4, total - first);
+  a.n_cls = (int)d.cls.size();
   int64_t blk = 0;
   for (int c = 0; c < 4; ++c) {
     ConvClass &k = a.cls[c];
@@ -310,19 +403,7 @@ static int64_t convt_classes(ConvTArgs &a, int BM, int BN, const std::vector<Axi
       k.blk0 = 0x7fffffff;
       continue;
     }
-    const AxisClass &yu = cu[(first + c) / cw.size()], &xw = cw[(first + c) % cw.size()];
-    k.u0 = yu.u0;
-    k.ustep = yu.ustep;
-    k.ny = yu.n;
-    k.ky0 = yu.k0;
-    k.kys = yu.ks;
-    k.nty = yu.nk;
-    k.w0 = xw.u0;
-    k.wstep = xw.ustep;
-    k.nx = xw.n;
-    k.kx0 = xw.k0;
-    k.kxs = xw.ks;
-    k.ntx = xw.nk;
+    k = class_geometry(cu, d.cls[c]);
     const int64_t M = (int64_t)a.R * k.ny * k.nx;
     if (M >= ((int64_t)1 << 31)) return -1;
     k.M = (int32_t)M;
@@ -334,47 +415,45 @@ static int64_t convt_classes(ConvTArgs &a, int BM, int BN, const std::vector<Axi
   return blk > 0x7fffffff ? -1 : blk;
 }
 
-static bool convt_axes(const ConvTArgs &a, std::vector<AxisClass> &cu) {
-  if (!axis_classes(a.S_in, a.S_out, a.stride, a.delta, cu) || cu.empty()) return false;
-  for (const AxisClass &c : cu)   // the gather's row offset assumes ustep = stride for n > 1
-    if (c.n > 1 && c.ustep != a.stride) return false;
-  return true;
-}
-
-uint64_t convt_part_flops(const ConvTArgs &a0, int part) {
+uint64_t convt_part_flops(const ConvTArgs &a, int part) {
   std::vector<AxisClass> cu;
-  if (!convt_axes(a0, cu)) return 0;
-  ConvTArgs a = a0;
-  if (convt_classes(a, 256, 64, cu, cu, 4 * part) < 0) return 0;   // class sizes do not depend on the tile
+  std::vector<ConvtDispatch> plan;
+  if (!convt_plan(a, cu, plan) || part < 0 || part >= (int)plan.size()) return 0;
   uint64_t f = 0;   // every position times the taps that reach it: the necessary multiply-adds
-  for (int c = 0; c < a.n_cls; ++c)
-    f += 2ull * (uint64_t)a.cls[c].M * (uint64_t)(a.cls[c].nty * a.cls[c].ntx) * (uint64_t)a.C_out * (uint64_t)a.C_in;
+  for (int idx : plan[part].cls) {
+    const ConvClass k = class_geometry(cu, idx);
+    f += 2ull * (uint64_t)a.R * (uint64_t)(k.ny * k.nx) * (uint64_t)(k.nty * k.ntx) * (uint64_t)a.C_out *
+         (uint64_t)a.C_in;
+  }
   return f;
 }
 
 int convt_launches(const ConvTArgs &a) {
   std::vector<AxisClass> cu;
-  if (!convt_axes(a, cu)) return -1;
-  return ((int)(cu.size() * cu.size()) + 3) / 4;
+  std::vector<ConvtDispatch> plan;
+  return convt_plan(a, cu, plan) ? (int)plan.size() : -1;
 }
 
 hipError_t launch_convt_part(const ConvTArgs &a0, int part, hipStream_t s) {
   std::vector<AxisClass> cu;
-  if (!convt_axes(a0, cu)) return hipErrorInvalidValue;
-  const std::vector<AxisClass> &cw = cu;   // square windows
-  const int total = (int)(cu.size() * cw.size());
-  const int first = 4 * part;
-  if (first < 0 || first >= total) return hipErrorInvalidValue;
+  std::vector<ConvtDispatch> plan;
+  if (!convt_plan(a0, cu, plan) || part < 0 || part >= (int)plan.size()) return hipErrorInvalidValue;
+  const ConvtDispatch &d = plan[part];
   ConvTArgs a = a0;
-  int64_t blk;
   if (a.N_pad % 128 == 0) {   // 128 x 128 tiles, 2 x 2 waves of 64 x 64
-    blk = convt_classes(a, 128, 128, cu, cw, first);
+    const int64_t blk = convt_fill(a, cu, d, 128, 128);
     if (blk < 0) return hipErrorInvalidValue;
-    if (blk > 0) hipLaunchKernelGGL((k_convt<128, 128, 16, 2, 2, 3>), dim3((unsigned)blk), dim3(256), 0, s, a);
-  } else {                    // 256 x 64 tiles, 4 x 1 waves of 64 x 64
-    blk = convt_classes(a, 256, 64, cu, cw, first);
+    if (blk > 0 && a.P_pos)
+      hipLaunchKernelGGL((k_convt<128, 128, 16, 2, 2, 3, true>), dim3((unsigned)blk), dim3(256), 0, s, a);
+    else if (blk > 0)
+      hipLaunchKernelGGL((k_convt<128, 128, 16, 2, 2, 3, false>), dim3((unsigned)blk), dim3(256), 0, s, a);
+  } else {                           // 256 x 64 tiles, 4 x 1 waves of 64 x 64
+    const int64_t blk = convt_fill(a, cu, d, 256, 64);
     if (blk < 0) return hipErrorInvalidValue;
-    if (blk > 0) hipLaunchKernelGGL((k_convt<256, 64, 16, 4, 1, 3>), dim3((unsigned)blk), dim3(256), 0, s, a);
+    if (blk > 0 && a.P_pos)
+      hipLaunchKernelGGL((k_convt<256, 64, 16, 4, 1, 3, true>), dim3((unsigned)blk), dim3(256), 0, s, a);
+    else if (blk > 0)
+      hipLaunchKernelGGL((k_convt<256, 64, 16, 4, 1, 3, false>), dim3((unsigned)blk), dim3(256), 0, s, a);
   }
   return hipGetLastError();
 }
