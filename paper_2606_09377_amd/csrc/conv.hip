@@ -479,8 +479,10 @@ hipError_t launch_convt(const ConvTArgs &a, hipStream_t s) {
 // W's own layout [co][ci][3][3] is the B operand [K][N].  A workgroup takes several whole
 // rows (small windows) or a strip of destination rows of one row (large windows); the
 // source positions' G stays in LDS between the two phases.
+constexpr int STEM_LDS_FLOATS = 10752;
+
 template <int CIN>
-__global__ __launch_bounds__(256, 2) void k_stem(const StemArgs p) {
+__global__ __launch_bounds__(256, 3) void k_stem(const StemArgs p) {
   constexpr int NB = CIN * 9 > 32 ? 2 : 1;   // 32-column MFMA blocks of N
   constexpr int GP = 32 * NB + 1;            // G row pitch (odd: the gather reads hit distinct banks)
   constexpr int NW = CIN * 9;
@@ -506,30 +508,41 @@ __global__ __launch_bounds__(256, 2) void k_stem(const StemArgs p) {
   }
   __syncthreads();
 
-  // ---- G = A_src W: each wave takes 32-position blocks; lane (r32, half) feeds the MFMAs
-  // with 16 consecutive k of its position per 32-k chunk, identically for both operands
+  // ---- G = A_src W: each wave takes 32-position blocks, two at a time (blocks b and b + 4,
+  // both blocks' loads in flight together); lane (r32, half) feeds the MFMAs with 16
+  // consecutive k of its position per 32-k chunk, identically for both operands
   const int r32 = lane & 31, half = lane >> 5;
   const int n_blk = (n_src + 31) / 32;
   const int KC = p.C_out / 32;
-  for (int blk = wave; blk < n_blk; blk += 4) {
-    // positions past the last one repeat it: their G rows are never gathered
-    const int pi = min(blk * 32 + r32, n_src - 1);
-    const int rl = pi / n_row_src, sp = pi - rl * n_row_src;
-    const float *src = p.A + (int64_t)(r0 + rl) * p.row_stride_out +
-                       ((int64_t)y_lo * p.S_out + sp) * p.C_out + half * 16;
-    f32x16 acc[NB];
+  for (int b0 = wave; b0 < n_blk; b0 += 8) {
+    const bool two = b0 + 4 < n_blk;   // wave-uniform
+    const float *src[2];
 #pragma unroll
-    for (int j = 0; j < NB; ++j)
+    for (int q = 0; q < 2; ++q) {
+      // positions past the last one repeat it: their G rows are never gathered
+      const int pi = min((b0 + 4 * q) * 32 + r32, n_src - 1);
+      const int rl = pi / n_row_src, sp = pi - rl * n_row_src;
+      src[q] = p.A + (int64_t)(r0 + rl) * p.row_stride_out + ((int64_t)y_lo * p.S_out + sp) * p.C_out + half * 16;
+    }
+    f32x16 acc[2][NB];
 #pragma unroll
-      for (int v = 0; v < 16; ++v) acc[j][v] = 0.f;
-    f32x4 a[4];
+    for (int q = 0; q < 2; ++q)
 #pragma unroll
-    for (int h = 0; h < 4; ++h) a[h] = *reinterpret_cast<const f32x4 *>(src + 4 * h);
+      for (int j = 0; j < NB; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[q][j][v] = 0.f;
+    f32x4 a[2][4];
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+#pragma unroll
+      for (int h = 0; h < 4; ++h) a[q][h] = *reinterpret_cast<const f32x4 *>(src[q] + 4 * h);
     for (int kc = 0; kc < KC; ++kc) {
-      f32x4 an[4];
+      f32x4 an[2][4];
       if (kc + 1 < KC) {
 #pragma unroll
-        for (int h = 0; h < 4; ++h) an[h] = *reinterpret_cast<const f32x4 *>(src + (kc + 1) * 32 + 4 * h);
+        for (int q = 0; q < 2; ++q)
+#pragma unroll
+          for (int h = 0; h < 4; ++h) an[q][h] = *reinterpret_cast<const f32x4 *>(src[q] + (kc + 1) * 32 + 4 * h);
       }
       f32x4 b[NB][4];
 #pragma unroll
@@ -542,18 +555,27 @@ __global__ __launch_bounds__(256, 2) void k_stem(const StemArgs p) {
 #pragma unroll
         for (int e = 0; e < 4; ++e)
 #pragma unroll
-          for (int j = 0; j < NB; ++j) acc[j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[h][e], b[j][h][e], acc[j], 0, 0, 0);
+          for (int q = 0; q < 2; ++q)
+#pragma unroll
+            for (int j = 0; j < NB; ++j)
+              acc[q][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[q][h][e], b[j][h][e], acc[q][j], 0, 0, 0);
       if (kc + 1 < KC) {
 #pragma unroll
-        for (int h = 0; h < 4; ++h) a[h] = an[h];
+        for (int q = 0; q < 2; ++q)
+#pragma unroll
+          for (int h = 0; h < 4; ++h) a[q][h] = an[q][h];
       }
     }
     // lane holds rows 8 g + 4 half + t (v = 4 g + t) of column 32 j + r32
 #pragma unroll
-    for (int j = 0; j < NB; ++j)
+    for (int q = 0; q < 2; ++q) {
+      if (q == 1 && !two) break;
 #pragma unroll
-      for (int v = 0; v < 16; ++v)
-        G[(blk * 32 + (v >> 2) * 8 + half * 4 + (v & 3)) * GP + 32 * j + r32] = acc[j][v];
+      for (int j = 0; j < NB; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          G[((b0 + 4 * q) * 32 + (v >> 2) * 8 + half * 4 + (v & 3)) * GP + 32 * j + r32] = acc[q][j][v];
+    }
   }
   __syncthreads();
 
@@ -607,7 +629,9 @@ hipError_t launch_stem_t(StemArgs a, hipStream_t s) {
   if (a.C_out <= 0 || a.C_out % 32 || a.R <= 0 || (a.stride != 1 && a.stride != 2) || a.S_out <= 0 || a.S_in <= 0)
     return hipErrorInvalidValue;
   const int64_t wt_floats = 32 * NB * (int64_t)(a.C_out + 4);
-  const int64_t src_max = ((16384 - wt_floats) / GP) & ~(int64_t)31;   // 64 KB of LDS per workgroup
+  // 42 KB of LDS per workgroup (three workgroups per CU), 64 KB for wide weights
+  int64_t src_max = ((STEM_LDS_FLOATS - wt_floats) / GP) & ~(int64_t)31;
+  if (src_max < 64) src_max = ((16384 - wt_floats) / GP) & ~(int64_t)31;
   if (src_max < 32) return hipErrorInvalidValue;
   auto src_positions = [&](int u_lo, int u_hi) {   // the kernel's source-row range, times S_out
     const int y_lo = (std::max(0, u_lo + a.delta - 2) + a.stride - 1) / a.stride;
