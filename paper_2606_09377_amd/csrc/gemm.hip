@@ -86,9 +86,22 @@ __device__ __forceinline__ float4 split_override(const SplitTable &st, int row, 
 // Epilogue of one wave: MB blocks of 32 rows from tile-relative row wrow of the tile at m0
 // (tile_rows high), 64 columns from col0 (one partial sum per row and 64 columns, so every
 // tiling gives the same bits), accumulators acc[MB][2].
-template <bool FWD, bool AL, bool AFF, int MB>
-__device__ __forceinline__ void gemm_epilogue(const GemmArgs &p, f32x16 (&acc)[MB][2], int m0, int wrow, int col0,
-                                              int lane, int tile_rows) {
+//
+// NBJ = 1: the wave holds only column block bj1 (0 or 1) of the 64; the two waves of the
+// workgroup combine their row sums through xpart (LDS, 16 x 64 floats) in the order a wave
+// holding both blocks uses, so the bits do not change.
+//
+// The arrays the epilogue reads and writes arrive as restrict-qualified parameters of the body,
+// so the compiler may issue the loads of later rows before the stores of earlier ones.
+template <bool FWD, bool AL, bool AFF, int MB, int NBJ>
+__device__ __forceinline__ void gemm_epilogue_body(const GemmArgs &p, f32x16 (&acc)[MB][NBJ], int m0, int wrow,
+                                                   int col0, int lane, int tile_rows, int bj1, float *xpart,
+                                                   const float4 *__restrict__ Pp, const float *__restrict__ c0p,
+                                                   const float *__restrict__ r0p, const float *__restrict__ alpha_t,
+                                                   float *__restrict__ pre_t, float *__restrict__ out_t,
+                                                   float *__restrict__ grad_t, const float *__restrict__ sbeta,
+                                                   float *__restrict__ gbeta, const float *__restrict__ biasp,
+                                                   float *__restrict__ partp) {
   const int r32 = lane & 31;
   // 32x32 accumulator layout: lane holds column (lane % 32) and rows
   // 8 (v / 4) + 4 (lane / 32) + (v % 4), v = 0..15.
@@ -98,15 +111,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &p, f32x16 (&acc)[M
   unit_tile = unit_tile < p.n_units ? unit_tile : p.n_units - 1;
   const bool has_splits = p.splits.D > 0;
 
-  // Stores and row-wise loads address the tile from a wave-uniform base with 32-bit lane
-  // offsets (every row-indexed array of one launch shares the pitch ld).
-  const int64_t ld = p.mode == EPI_CONCRETIZE ? p.ld_pre : p.ldo;
-  const int64_t tbase = (int64_t)m0 * ld;
-  float *const out_t = p.mode == EPI_CONCRETIZE ? nullptr : p.out + tbase;
-  float *const pre_t = p.pre ? p.pre + tbase : nullptr;
-  const float *const alpha_t = p.alpha ? p.alpha + tbase : nullptr;
-  float *const grad_t = p.grad ? p.grad + tbase : nullptr;
-  const int ld32 = (int)ld;
+  const int ld32 = (int)(p.mode == EPI_CONCRETIZE ? p.ld_pre : p.ldo);
 
   float rp[MB][16];
 #pragma unroll
@@ -117,27 +122,29 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &p, f32x16 (&acc)[M
   if constexpr (AFF) {
     // plain affine map (the IBP step on the matrix cores): out = A Bt^T (+ bias)
 #pragma unroll
-    for (int bj = 0; bj < 2; ++bj) {
+    for (int jj = 0; jj < NBJ; ++jj) {
+      const int bj = NBJ == 2 ? jj : bj1;
       const int n = col0 + bj * 32 + r32;
-      const float bn = p.bias ? p.bias[n] : 0.f;
+      const float bn = biasp ? biasp[n] : 0.f;
 #pragma unroll
       for (int bi = 0; bi < MB; ++bi)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int lr = wrow + bi * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
-          out_t[lr * ld32 + n] = acc[bi][bj][v] + bn;
+          out_t[lr * ld32 + n] = acc[bi][jj][v] + bn;
         }
     }
     return;
   }
 #pragma unroll
-  for (int bj = 0; bj < 2; ++bj) {
+  for (int jj = 0; jj < NBJ; ++jj) {
+    const int bj = NBJ == 2 ? jj : bj1;
     const int n = col0 + bj * 32 + r32;
     if constexpr (FWD) {
       // the relaxed network evaluated forward: D = W_k E + b_k, then the line of ReLU k that
       // the backward pass chose for this row (by the sign of its coefficient)
       float4 prm_tile = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (uniform_unit) prm_tile = p.P[(int64_t)unit_tile * p.ldp + n];
+      if (uniform_unit) prm_tile = Pp[(int64_t)unit_tile * p.ldp + n];
 #pragma unroll
       for (int bi = 0; bi < MB; ++bi) {
 #pragma unroll
@@ -149,16 +156,17 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &p, f32x16 (&acc)[M
           if (!uniform_unit) {
             int u = row / p.rows_per_unit;
             u = u < p.n_units ? u : p.n_units - 1;
-            prm = p.P[(int64_t)u * p.ldp + n];
+            prm = Pp[(int64_t)u * p.ldp + n];
           }
           int ent = -1;
           float sterm = 0.f;
           if (has_splits) prm = split_override(p.splits, row, p.relu_index, n, prm, &ent, &sterm);
           const bool unst = prm.z > 0.f;
-          const float lam = unst ? alpha_t[off] : prm.x;
+          const float al = alpha_t[off];   // loaded for every row: no load waits on prm
+          const float lam = unst ? al : prm.x;
           const float an = pre_t[off];
-          const float D = acc[bi][bj][v] + prm.w;
-          if (ent >= 0 && p.splits.grad_beta) p.splits.grad_beta[(int64_t)row * p.splits.S + ent] = sterm * D;
+          const float D = acc[bi][jj][v] + prm.w;
+          if (ent >= 0 && gbeta) gbeta[(int64_t)row * p.splits.S + ent] = sterm * D;
           const float E = an > 0.f ? lam * D : prm.y * D + (an < 0.f ? prm.z : 0.f);
           out_t[off] = E;
           grad_t[off] = (unst && an > 0.f) ? an * D : 0.f;
@@ -166,7 +174,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &p, f32x16 (&acc)[M
       }
     } else if (p.mode == EPI_RELAX) {
       float4 prm_tile = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (uniform_unit) prm_tile = p.P[(int64_t)unit_tile * p.ldp + n];
+      if (uniform_unit) prm_tile = Pp[(int64_t)unit_tile * p.ldp + n];
 #pragma unroll
       for (int bi = 0; bi < MB; ++bi) {
 #pragma unroll
@@ -178,7 +186,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &p, f32x16 (&acc)[M
           if (!uniform_unit) {
             int u = row / p.rows_per_unit;
             u = u < p.n_units ? u : p.n_units - 1;
-            prm = p.P[(int64_t)u * p.ldp + n];
+            prm = Pp[(int64_t)u * p.ldp + n];
           }
           int ent = -1;
           float sterm = 0.f;
@@ -188,14 +196,17 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &p, f32x16 (&acc)[M
             else
               prm = split_override(p.splits, row, p.relu_index, n, prm);
           }
-          const float a = acc[bi][bj][v];
+          const float a = acc[bi][jj][v];
           float lam = prm.x;
           if constexpr (AL) {
-            if (alpha_t && prm.z > 0.f) lam = alpha_t[off];
+            if (alpha_t) {
+              const float al = alpha_t[off];
+              lam = prm.z > 0.f ? al : lam;
+            }
           }
           float ap = a > 0.f ? a * lam : a * prm.y;
           if constexpr (AL) {
-            if (ent >= 0 && p.splits.beta) ap += p.splits.beta[(int64_t)row * p.splits.S + ent] * sterm;
+            if (ent >= 0 && sbeta) ap += sbeta[(int64_t)row * p.splits.S + ent] * sterm;
           }
           out_t[off] = ap;
           if constexpr (AL) {
@@ -207,8 +218,8 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &p, f32x16 (&acc)[M
     } else {
       float c_tile = 0.f, r_tile = 0.f;
       if (uniform_unit) {
-        c_tile = p.c0[(int64_t)unit_tile * p.ldc + n];
-        r_tile = p.r0[(int64_t)unit_tile * p.ldc + n];
+        c_tile = c0p[(int64_t)unit_tile * p.ldc + n];
+        r_tile = r0p[(int64_t)unit_tile * p.ldc + n];
       }
 #pragma unroll
       for (int bi = 0; bi < MB; ++bi) {
@@ -220,10 +231,10 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &p, f32x16 (&acc)[M
           if (!uniform_unit) {
             int u = row / p.rows_per_unit;
             u = u < p.n_units ? u : p.n_units - 1;
-            c = p.c0[(int64_t)u * p.ldc + n];
-            r = p.r0[(int64_t)u * p.ldc + n];
+            c = c0p[(int64_t)u * p.ldc + n];
+            r = r0p[(int64_t)u * p.ldc + n];
           }
-          const float a = acc[bi][bj][v];
+          const float a = acc[bi][jj][v];
           if constexpr (AL) {
             if (pre_t) pre_t[lr * ld32 + n] = a;
           }
@@ -234,6 +245,16 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &p, f32x16 (&acc)[M
   }
 
   if constexpr (FWD) return;
+  if constexpr (NBJ == 1) {
+    if (bj1 == 1) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) xpart[v * 64 + lane] = rp[0][v];
+    }
+    __syncthreads();
+    if (bj1 == 1) return;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) rp[0][v] += xpart[v * 64 + lane];
+  }
   // fixed butterfly over the 32 lanes that share rows
 #pragma unroll
   for (int bi = 0; bi < MB; ++bi) {
@@ -249,7 +270,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &p, f32x16 (&acc)[M
     }
   }
   if (r32 == 0) {
-    float *dst = p.part + (int64_t)(col0 / PART_COLS) * p.M_pad;
+    float *dst = partp + (int64_t)(col0 / PART_COLS) * p.M_pad;
 #pragma unroll
     for (int bi = 0; bi < MB; ++bi)
 #pragma unroll
@@ -258,6 +279,19 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &p, f32x16 (&acc)[M
         dst[row] = rp[bi][v];
       }
   }
+}
+
+// Stores and row-wise loads address the tile from a wave-uniform base with 32-bit lane offsets
+// (every row-indexed array of one launch shares the pitch ld).
+template <bool FWD, bool AL, bool AFF, int MB, int NBJ = 2>
+__device__ __forceinline__ void gemm_epilogue(const GemmArgs &p, f32x16 (&acc)[MB][NBJ], int m0, int wrow, int col0,
+                                              int lane, int tile_rows, int bj1 = 0, float *xpart = nullptr) {
+  const int64_t ld = p.mode == EPI_CONCRETIZE ? p.ld_pre : p.ldo;
+  const int64_t tbase = (int64_t)m0 * ld;
+  gemm_epilogue_body<FWD, AL, AFF, MB, NBJ>(
+      p, acc, m0, wrow, col0, lane, tile_rows, bj1, xpart, p.P, p.c0, p.r0, p.alpha ? p.alpha + tbase : nullptr,
+      p.pre ? p.pre + tbase : nullptr, p.mode == EPI_CONCRETIZE ? nullptr : p.out + tbase,
+      p.grad ? p.grad + tbase : nullptr, p.splits.beta, p.splits.grad_beta, p.bias, p.part);
 }
 
 // Instantiations: FWD selects the forward epilogue (alpha-CROWN's gradient pass); otherwise the
@@ -360,67 +394,58 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm(const GemmArgs p) {
   gemm_epilogue<FWD, AL, AFF, 2>(p, acc, m0, wm * 64, n0 + wn * 64, lane, BM);
 }
 
-// Small launches (few row tiles): one wave per workgroup owns a 32 x 64 tile and reads its
-// MFMA operands straight from global memory (no LDS, no barriers), next K tile prefetched in
-// registers.  Each lane takes the same 16 consecutive k of its row per K tile as in k_gemm, and
-// each accumulator sees the same MFMA sequence, so both kernels give the same bits.
+// Small launches (few row tiles): a workgroup of two waves owns a 32 x 64 tile, each wave one
+// 32-column block, and reads its MFMA operands straight from global memory (no LDS operand
+// staging), two K tiles prefetched in registers.  Each lane takes the same 16 consecutive k of
+// its row per K tile as in k_gemm, each accumulator sees the same MFMA sequence, and the row
+// sums of the two blocks are added in k_gemm's order, so both kernels give the same bits.
 constexpr int SM_BM = 32, SM_BN = 64;
 constexpr int64_t SMALL_GRID = 512;   // 128 x 128 tiles below which the small kernel runs
 
 template <bool FWD, bool AL, bool AFF = false>
-__global__ __launch_bounds__(64) void k_gemm_small(const GemmArgs p) {
-  const int lane = threadIdx.x;
+__global__ __launch_bounds__(128) void k_gemm_small(const GemmArgs p) {
+  __shared__ float xpart[16 * 64];
+  const int lane = threadIdx.x & 63, bj = threadIdx.x >> 6;
   const int n_mt = p.M_pad / SM_BM, n_nt = p.N_pad / SM_BN;
   int mt, nt;
   map_tile(blockIdx.x, n_mt * n_nt, n_mt, n_nt, mt, nt);
   const int m0 = mt * SM_BM, n0 = nt * SM_BN;
   const int r32 = lane & 31, kq = (lane >> 5) * 16;
   const float *Ag = p.A + (int64_t)(m0 + r32) * p.lda + kq;
-  const float *Bg0 = p.Bt + (int64_t)(n0 + r32) * p.ldb + kq;
-  const float *Bg1 = Bg0 + 32 * p.ldb;
-  f32x16 acc[1][2];
+  const float *Bg = p.Bt + (int64_t)(n0 + bj * 32 + r32) * p.ldb + kq;
+  f32x16 acc[1][1];
 #pragma unroll
-  for (int j = 0; j < 2; ++j)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) acc[0][j][v] = 0.f;
-  f32x4 a[4], b0[4], b1[4];
-  auto load = [&](int k0, f32x4 *ra, f32x4 *rb0, f32x4 *rb1) {
+  for (int v = 0; v < 16; ++v) acc[0][0][v] = 0.f;
+  f32x4 a[4], b[4], a1[4], b1[4], a2[4], b2[4];
+  auto load = [&](int k0, f32x4 *ra, f32x4 *rb) {
 #pragma unroll
     for (int h = 0; h < 4; ++h) {
       ra[h] = *reinterpret_cast<const f32x4 *>(Ag + k0 + 4 * h);
-      rb0[h] = *reinterpret_cast<const f32x4 *>(Bg0 + k0 + 4 * h);
-      rb1[h] = *reinterpret_cast<const f32x4 *>(Bg1 + k0 + 4 * h);
+      rb[h] = *reinterpret_cast<const f32x4 *>(Bg + k0 + 4 * h);
       if constexpr (AFF) {
-        if (p.abs_b) {
-          rb0[h] = __builtin_elementwise_abs(rb0[h]);
-          rb1[h] = __builtin_elementwise_abs(rb1[h]);
-        }
+        if (p.abs_b) rb[h] = __builtin_elementwise_abs(rb[h]);
       }
     }
   };
-  load(0, a, b0, b1);
   const int KT = p.K / BK;
+  load(0, a, b);
+  if (KT > 1) load(BK, a1, b1);
   for (int kt = 0; kt < KT; ++kt) {
-    f32x4 na[4], nb0[4], nb1[4];
-    const bool more = kt + 1 < KT;
-    if (more) load((kt + 1) * BK, na, nb0, nb1);
+    if (kt + 2 < KT) load((kt + 2) * BK, a2, b2);
 #pragma unroll
     for (int h = 0; h < 4; ++h)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[h][e], b0[h][e], acc[0][0], 0, 0, 0);
-        acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[h][e], b1[h][e], acc[0][1], 0, 0, 0);
-      }
-    if (more) {
+      for (int e = 0; e < 4; ++e)
+        acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[h][e], b[h][e], acc[0][0], 0, 0, 0);
 #pragma unroll
-      for (int h = 0; h < 4; ++h) {
-        a[h] = na[h];
-        b0[h] = nb0[h];
-        b1[h] = nb1[h];
-      }
+    for (int h = 0; h < 4; ++h) {
+      a[h] = a1[h];
+      b[h] = b1[h];
+      a1[h] = a2[h];
+      b1[h] = b2[h];
     }
   }
-  gemm_epilogue<FWD, AL, AFF, 1>(p, acc, m0, 0, n0, lane, SM_BM);
+  gemm_epilogue<FWD, AL, AFF, 1, 1>(p, acc, m0, 0, n0, lane, SM_BM, bj, xpart);
 }
 
 bool gemm_is_small(const GemmArgs &a) {
@@ -446,7 +471,7 @@ hipError_t launch_gemm(const GemmArgs &a, hipStream_t s) {
   if (grid < SMALL_GRID) {
     // too few 128 x 128 tiles to fill the chip: 32 x 64 tiles, one wave each (same bits)
     const int64_t sg = (int64_t)(a.M_pad / SM_BM) * (a.N_pad / SM_BN);
-    const dim3 g((unsigned)sg), t(64);
+    const dim3 g((unsigned)sg), t(128);
     if (a.mode == EPI_AFFINE)
       hipLaunchKernelGGL((k_gemm_small<false, false, true>), g, t, 0, s, a);
     else if (a.mode == EPI_FORWARD)
