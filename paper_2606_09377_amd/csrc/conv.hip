@@ -66,12 +66,12 @@ __device__ __forceinline__ void convt_epilogue(const ConvTArgs &p, const ConvCla
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN, r32 = lane & 31;
   const int nyx = cl.ny * cl.nx;
-  // Row information of the tile's BM GEMM rows is computed once, one row per thread, into
+  // Row information of the tile's BM GEMM rows is computed once, a row per thread, into
   // LDS (the operand buffers are free after the main loop's last barrier).  A lane holds 16
   // rows of each 32 x 32 block as 4 groups of 4 consecutive rows; the relaxation parameters
   // and residual terms of the next group are loaded while the current group is relaxed and
   // stored, so the epilogue waits on global memory about once instead of once per group.
-  static_assert(BM <= 256, "one row per thread");
+  static_assert(BM % 256 == 0 || BM < 256, "rows are spread over the 256 threads");
   int64_t *s_ob = reinterpret_cast<int64_t *>(scratch);      // output offset
   int64_t *s_rb = s_ob + BM;                                 // residual offset, or -1
   int *s_pb = reinterpret_cast<int *>(s_rb + BM);            // parameter offset, -1 outside the image
@@ -80,8 +80,8 @@ __device__ __forceinline__ void convt_epilogue(const ConvTArgs &p, const ConvCla
   const float4 *__restrict__ Pp = p.P_pos;
   const float *__restrict__ resp = p.res;
   float *__restrict__ outp = p.out;
-  if (tid < BM) {
-    const int m = m0 + tid;
+  for (int tr = tid; tr < BM; tr += 256) {
+    const int m = m0 + tr;
     const bool valid = m < cl.M;
     const uint32_t r = valid ? fdiv((uint32_t)m, cl.div_yx) : 0u;
     const uint32_t pos = valid ? (uint32_t)m - r * (uint32_t)nyx : 0u;
@@ -93,10 +93,10 @@ __device__ __forceinline__ void convt_epilogue(const ConvTArgs &p, const ConvCla
     const int gx = p.dense ? w : an.z * p.scale - p.h_in + w;
     const bool inside = valid && gy >= 0 && gx >= 0 && gy < p.H_in && gx < p.H_in;
     const int du = u - p.res_off, dw = w - p.res_off;
-    s_mo[tid] = valid ? (int)r * S_in2 + u * p.S_in + w : -1;
-    s_ob[tid] = (int64_t)r * p.row_stride_in + ((int64_t)u * p.S_in + w) * p.C_in;
-    s_pb[tid] = inside ? ((an.x * p.H_in + gy) * p.H_in + gx) * p.C_in : -1;
-    s_rb[tid] = inside && resp && du >= 0 && dw >= 0 && du < p.res_S && dw < p.res_S
+    s_mo[tr] = valid ? (int)r * S_in2 + u * p.S_in + w : -1;
+    s_ob[tr] = (int64_t)r * p.row_stride_in + ((int64_t)u * p.S_in + w) * p.C_in;
+    s_pb[tr] = inside ? ((an.x * p.H_in + gy) * p.H_in + gx) * p.C_in : -1;
+    s_rb[tr] = inside && resp && du >= 0 && dw >= 0 && du < p.res_S && dw < p.res_S
                     ? (int64_t)r * p.res_row_stride + ((int64_t)du * p.res_S + dw) * p.C_in
                     : -1;
   }
@@ -480,6 +480,8 @@ hipError_t launch_convt(const ConvTArgs &a, hipStream_t s) {
 // rows (small windows) or a strip of destination rows of one row (large windows); the
 // source positions' G stays in LDS between the two phases.
 constexpr int STEM_LDS_FLOATS = 10752;
+// destination positions per thread (fewer with four input channels: register budget)
+constexpr int stem_dpt(int cin) { return cin == 4 ? 2 : 4; }
 
 template <int CIN>
 __global__ __launch_bounds__(256, 3) void k_stem(const StemArgs p) {
@@ -501,6 +503,37 @@ __global__ __launch_bounds__(256, 3) void k_stem(const StemArgs p) {
   const int y_hi = min(p.S_out - 1, (u_hi - 1 + p.delta) / p.stride);
   const int n_row_src = (y_hi >= y_lo ? y_hi - y_lo + 1 : 0) * p.S_out;
   const int n_src = rows * n_row_src;
+
+  // destination positions of this thread (at most stem_dpt): their box terms are loaded
+  // before the GEMM phase, so the loads complete under it
+  const int nu = u_hi - u_lo;
+  const int per_rl = nu * p.S_in;
+  constexpr int STEM_DPT = stem_dpt(CIN);
+  const int n_dst = rows * per_rl;   // <= 256 STEM_DPT (launch_stem)
+  bool live[STEM_DPT];
+  float bc[STEM_DPT][CIN], br[STEM_DPT][CIN];
+#pragma unroll
+  for (int q = 0; q < STEM_DPT; ++q) {
+    const int d = tid + 256 * q;
+    live[q] = false;
+    if (d < n_dst) {
+      const int rl = d / per_rl, rem = d - rl * per_rl;
+      const int uu = rem / p.S_in;
+      const int u = u_lo + uu, w = rem - uu * p.S_in;
+      const int4 an = p.rows[r0 + rl];
+      const int gy = p.dense ? u : an.y * p.scale - p.h_in + u;
+      const int gx = p.dense ? w : an.z * p.scale - p.h_in + w;
+      live[q] = gy >= 0 && gx >= 0 && gy < p.H_in && gx < p.H_in;
+      if (live[q]) {
+#pragma unroll
+        for (int ci = 0; ci < CIN; ++ci) {
+          const int64_t bi = (int64_t)an.x * p.ld_box + ((int64_t)ci * p.H_in + gy) * p.H_in + gx;
+          bc[q][ci] = p.c0[bi];
+          br[q][ci] = p.r0[bi];
+        }
+      }
+    }
+  }
 
   for (int i = tid; i < 32 * NB * p.C_out; i += 256) {
     const int n = i / p.C_out, k = i - n * p.C_out;
@@ -580,18 +613,16 @@ __global__ __launch_bounds__(256, 3) void k_stem(const StemArgs p) {
   __syncthreads();
 
   // ---- gather the taps of every destination position and concretize
-  const int nu = u_hi - u_lo;
-  const int per_rl = nu * p.S_in;
   const int S_in2 = p.S_in * p.S_in;
-  for (int d = tid; d < rows * per_rl; d += 256) {
+#pragma unroll
+  for (int q = 0; q < STEM_DPT; ++q) {
+    const int d = tid + 256 * q;
+    if (d >= n_dst) break;
     const int rl = d / per_rl, rem = d - rl * per_rl;
     const int uu = rem / p.S_in;
     const int u = u_lo + uu, w = rem - uu * p.S_in;
-    const int4 an = p.rows[r0 + rl];
-    const int gy = p.dense ? u : an.y * p.scale - p.h_in + u;
-    const int gx = p.dense ? w : an.z * p.scale - p.h_in + w;
     float part = 0.f;
-    if (gy >= 0 && gx >= 0 && gy < p.H_in && gx < p.H_in) {
+    if (live[q]) {   // inside the image
       float a[CIN];
 #pragma unroll
       for (int ci = 0; ci < CIN; ++ci) a[ci] = 0.f;
@@ -613,10 +644,7 @@ __global__ __launch_bounds__(256, 3) void k_stem(const StemArgs p) {
         }
       }
 #pragma unroll
-      for (int ci = 0; ci < CIN; ++ci) {
-        const int64_t bi = (int64_t)an.x * p.ld_box + ((int64_t)ci * p.H_in + gy) * p.H_in + gx;
-        part += a[ci] * p.c0[bi] - fabsf(a[ci]) * p.r0[bi];
-      }
+      for (int ci = 0; ci < CIN; ++ci) part += a[ci] * bc[q][ci] - fabsf(a[ci]) * br[q][ci];
     }
     p.part[(int64_t)(r0 + rl) * S_in2 + u * p.S_in + w] = part;
   }
@@ -639,13 +667,14 @@ hipError_t launch_stem_t(StemArgs a, hipStream_t s) {
     return (int64_t)(y_hi >= y_lo ? y_hi - y_lo + 1 : 0) * a.S_out;
   };
   const int64_t full = src_positions(0, a.S_in);
-  if (full <= src_max) {   // whole rows
-    a.rpw = (int32_t)std::max<int64_t>(1, src_max / std::max<int64_t>(full, 1));
+  const int64_t dst_max = 256 * stem_dpt(CIN), S_in2 = (int64_t)a.S_in * a.S_in;
+  if (full <= src_max && S_in2 <= dst_max) {   // whole rows
+    a.rpw = (int32_t)std::max<int64_t>(1, std::min(src_max / std::max<int64_t>(full, 1), dst_max / S_in2));
     a.strip = a.S_in;
-  } else {                 // one row, strips of destination rows
+  } else {                                     // one row, strips of destination rows
     a.rpw = 1;
     a.strip = 0;
-    for (int h = a.S_in; h >= 1 && !a.strip; --h) {
+    for (int h = std::min<int64_t>(a.S_in, dst_max / a.S_in); h >= 1 && !a.strip; --h) {
       bool fits = true;
       for (int u0 = 0; u0 < a.S_in && fits; u0 += h) fits = src_positions(u0, std::min(a.S_in, u0 + h)) <= src_max;
       if (fits) a.strip = h;
