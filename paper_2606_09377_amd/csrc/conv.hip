@@ -480,8 +480,9 @@ hipError_t launch_convt(const ConvTArgs &a, hipStream_t s) {
 // rows (small windows) or a strip of destination rows of one row (large windows); the
 // source positions' G stays in LDS between the two phases.
 constexpr int STEM_LDS_FLOATS = 10752;
+constexpr int64_t STEM_GRID = 4096;   // workgroups; each takes every gridDim-th work item
 // destination positions per thread (fewer with four input channels: register budget)
-constexpr int stem_dpt(int cin) { return cin == 4 ? 2 : 4; }
+constexpr int stem_dpt(int cin) { return cin == 4 ? 1 : 4; }
 
 template <int CIN>
 __global__ __launch_bounds__(256, 3) void k_stem(const StemArgs p) {
@@ -493,160 +494,165 @@ __global__ __launch_bounds__(256, 3) void k_stem(const StemArgs p) {
   float *wt = lds;                           // [32 NB][WTP]
   float *G = lds + 32 * NB * WTP;            // [source positions][GP]
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int rg = blockIdx.x / p.n_strips, st = blockIdx.x - rg * p.n_strips;
-  const int r0 = rg * p.rpw;
-  const int rows = min(p.rpw, p.R - r0);
-  const int u_lo = st * p.strip, u_hi = min(p.S_in, u_lo + p.strip);
-  // source rows reached from destination rows [u_lo, u_hi): y = (u + delta - ky) / stride
-  const int lo_num = max(0, u_lo + p.delta - 2);
-  const int y_lo = (lo_num + p.stride - 1) / p.stride;
-  const int y_hi = min(p.S_out - 1, (u_hi - 1 + p.delta) / p.stride);
-  const int n_row_src = (y_hi >= y_lo ? y_hi - y_lo + 1 : 0) * p.S_out;
-  const int n_src = rows * n_row_src;
-
-  // destination positions of this thread (at most stem_dpt): their box terms are loaded
-  // before the GEMM phase, so the loads complete under it
-  const int nu = u_hi - u_lo;
-  const int per_rl = nu * p.S_in;
-  constexpr int STEM_DPT = stem_dpt(CIN);
-  const int n_dst = rows * per_rl;   // <= 256 STEM_DPT (launch_stem)
-  bool live[STEM_DPT];
-  float bc[STEM_DPT][CIN], br[STEM_DPT][CIN];
-#pragma unroll
-  for (int q = 0; q < STEM_DPT; ++q) {
-    const int d = tid + 256 * q;
-    live[q] = false;
-    if (d < n_dst) {
-      const int rl = d / per_rl, rem = d - rl * per_rl;
-      const int uu = rem / p.S_in;
-      const int u = u_lo + uu, w = rem - uu * p.S_in;
-      const int4 an = p.rows[r0 + rl];
-      const int gy = p.dense ? u : an.y * p.scale - p.h_in + u;
-      const int gx = p.dense ? w : an.z * p.scale - p.h_in + w;
-      live[q] = gy >= 0 && gx >= 0 && gy < p.H_in && gx < p.H_in;
-      if (live[q]) {
-#pragma unroll
-        for (int ci = 0; ci < CIN; ++ci) {
-          const int64_t bi = (int64_t)an.x * p.ld_box + ((int64_t)ci * p.H_in + gy) * p.H_in + gx;
-          bc[q][ci] = p.c0[bi];
-          br[q][ci] = p.r0[bi];
-        }
-      }
-    }
-  }
-
   for (int i = tid; i < 32 * NB * p.C_out; i += 256) {
     const int n = i / p.C_out, k = i - n * p.C_out;
     wt[n * WTP + k] = n < NW ? p.W[(int64_t)k * NW + n] : 0.f;
   }
   __syncthreads();
+  // work items (row groups x strips), the weights staged once for all of them
+  const int n_items = (p.R + p.rpw - 1) / p.rpw * p.n_strips;
+  for (int item = blockIdx.x; item < n_items; item += gridDim.x) {
+    const int rg = item / p.n_strips, st = item - rg * p.n_strips;
+    const int r0 = rg * p.rpw;
+    const int rows = min(p.rpw, p.R - r0);
+    const int u_lo = st * p.strip, u_hi = min(p.S_in, u_lo + p.strip);
+    // source rows reached from destination rows [u_lo, u_hi): y = (u + delta - ky) / stride
+    const int lo_num = max(0, u_lo + p.delta - 2);
+    const int y_lo = (lo_num + p.stride - 1) / p.stride;
+    const int y_hi = min(p.S_out - 1, (u_hi - 1 + p.delta) / p.stride);
+    const int n_row_src = (y_hi >= y_lo ? y_hi - y_lo + 1 : 0) * p.S_out;
+    const int n_src = rows * n_row_src;
 
-  // ---- G = A_src W: each wave takes 32-position blocks, two at a time (blocks b and b + 4,
-  // both blocks' loads in flight together); lane (r32, half) feeds the MFMAs with 16
-  // consecutive k of its position per 32-k chunk, identically for both operands
-  const int r32 = lane & 31, half = lane >> 5;
-  const int n_blk = (n_src + 31) / 32;
-  const int KC = p.C_out / 32;
-  for (int b0 = wave; b0 < n_blk; b0 += 8) {
-    const bool two = b0 + 4 < n_blk;   // wave-uniform
-    const float *src[2];
+    // destination positions of this thread (at most stem_dpt): their box terms are loaded
+    // before the GEMM phase, so the loads complete under it
+    const int nu = u_hi - u_lo;
+    const int per_rl = nu * p.S_in;
+    constexpr int STEM_DPT = stem_dpt(CIN);
+    const int n_dst = rows * per_rl;   // <= 256 STEM_DPT (launch_stem)
+    bool live[STEM_DPT];
+    float bc[STEM_DPT][CIN], br[STEM_DPT][CIN];
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      // positions past the last one repeat it: their G rows are never gathered
-      const int pi = min((b0 + 4 * q) * 32 + r32, n_src - 1);
-      const int rl = pi / n_row_src, sp = pi - rl * n_row_src;
-      src[q] = p.A + (int64_t)(r0 + rl) * p.row_stride_out + ((int64_t)y_lo * p.S_out + sp) * p.C_out + half * 16;
-    }
-    f32x16 acc[2][NB];
+    for (int q = 0; q < STEM_DPT; ++q) {
+      const int d = tid + 256 * q;
+      live[q] = false;
+      if (d < n_dst) {
+        const int rl = d / per_rl, rem = d - rl * per_rl;
+        const int uu = rem / p.S_in;
+        const int u = u_lo + uu, w = rem - uu * p.S_in;
+        const int4 an = p.rows[r0 + rl];
+        const int gy = p.dense ? u : an.y * p.scale - p.h_in + u;
+        const int gx = p.dense ? w : an.z * p.scale - p.h_in + w;
+        live[q] = gy >= 0 && gx >= 0 && gy < p.H_in && gx < p.H_in;
+        if (live[q]) {
 #pragma unroll
-    for (int q = 0; q < 2; ++q)
-#pragma unroll
-      for (int j = 0; j < NB; ++j)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) acc[q][j][v] = 0.f;
-    f32x4 a[2][4];
-#pragma unroll
-    for (int q = 0; q < 2; ++q)
-#pragma unroll
-      for (int h = 0; h < 4; ++h) a[q][h] = *reinterpret_cast<const f32x4 *>(src[q] + 4 * h);
-    for (int kc = 0; kc < KC; ++kc) {
-      f32x4 an[2][4];
-      if (kc + 1 < KC) {
-#pragma unroll
-        for (int q = 0; q < 2; ++q)
-#pragma unroll
-          for (int h = 0; h < 4; ++h) an[q][h] = *reinterpret_cast<const f32x4 *>(src[q] + (kc + 1) * 32 + 4 * h);
+          for (int ci = 0; ci < CIN; ++ci) {
+            const int64_t bi = (int64_t)an.x * p.ld_box + ((int64_t)ci * p.H_in + gy) * p.H_in + gx;
+            bc[q][ci] = p.c0[bi];
+            br[q][ci] = p.r0[bi];
+          }
+        }
       }
-      f32x4 b[NB][4];
+    }
+
+
+    // ---- G = A_src W: each wave takes 32-position blocks, two at a time (blocks b and b + 4,
+    // both blocks' loads in flight together); lane (r32, half) feeds the MFMAs with 16
+    // consecutive k of its position per 32-k chunk, identically for both operands
+    const int r32 = lane & 31, half = lane >> 5;
+    const int n_blk = (n_src + 31) / 32;
+    const int KC = p.C_out / 32;
+    for (int b0 = wave; b0 < n_blk; b0 += 8) {
+      const bool two = b0 + 4 < n_blk;   // wave-uniform
+      const float *src[2];
 #pragma unroll
-      for (int j = 0; j < NB; ++j)
+      for (int q = 0; q < 2; ++q) {
+        // positions past the last one repeat it: their G rows are never gathered
+        const int pi = min((b0 + 4 * q) * 32 + r32, n_src - 1);
+        const int rl = pi / n_row_src, sp = pi - rl * n_row_src;
+        src[q] = p.A + (int64_t)(r0 + rl) * p.row_stride_out + ((int64_t)y_lo * p.S_out + sp) * p.C_out + half * 16;
+      }
+      f32x16 acc[2][NB];
 #pragma unroll
-        for (int h = 0; h < 4; ++h)
-          b[j][h] = *reinterpret_cast<const f32x4 *>(wt + (32 * j + r32) * WTP + kc * 32 + half * 16 + 4 * h);
+      for (int q = 0; q < 2; ++q)
 #pragma unroll
-      for (int h = 0; h < 4; ++h)
+        for (int j = 0; j < NB; ++j)
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
+          for (int v = 0; v < 16; ++v) acc[q][j][v] = 0.f;
+      f32x4 a[2][4];
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+#pragma unroll
+        for (int h = 0; h < 4; ++h) a[q][h] = *reinterpret_cast<const f32x4 *>(src[q] + 4 * h);
+      for (int kc = 0; kc < KC; ++kc) {
+        f32x4 an[2][4];
+        if (kc + 1 < KC) {
 #pragma unroll
           for (int q = 0; q < 2; ++q)
 #pragma unroll
-            for (int j = 0; j < NB; ++j)
-              acc[q][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[q][h][e], b[j][h][e], acc[q][j], 0, 0, 0);
-      if (kc + 1 < KC) {
+            for (int h = 0; h < 4; ++h) an[q][h] = *reinterpret_cast<const f32x4 *>(src[q] + (kc + 1) * 32 + 4 * h);
+        }
+        f32x4 b[NB][4];
 #pragma unroll
-        for (int q = 0; q < 2; ++q)
+        for (int j = 0; j < NB; ++j)
 #pragma unroll
-          for (int h = 0; h < 4; ++h) a[q][h] = an[q][h];
-      }
-    }
-    // lane holds rows 8 g + 4 half + t (v = 4 g + t) of column 32 j + r32
+          for (int h = 0; h < 4; ++h)
+            b[j][h] = *reinterpret_cast<const f32x4 *>(wt + (32 * j + r32) * WTP + kc * 32 + half * 16 + 4 * h);
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      if (q == 1 && !two) break;
+        for (int h = 0; h < 4; ++h)
 #pragma unroll
-      for (int j = 0; j < NB; ++j)
+          for (int e = 0; e < 4; ++e)
 #pragma unroll
-        for (int v = 0; v < 16; ++v)
-          G[((b0 + 4 * q) * 32 + (v >> 2) * 8 + half * 4 + (v & 3)) * GP + 32 * j + r32] = acc[q][j][v];
-    }
-  }
-  __syncthreads();
-
-  // ---- gather the taps of every destination position and concretize
-  const int S_in2 = p.S_in * p.S_in;
+            for (int q = 0; q < 2; ++q)
 #pragma unroll
-  for (int q = 0; q < STEM_DPT; ++q) {
-    const int d = tid + 256 * q;
-    if (d >= n_dst) break;
-    const int rl = d / per_rl, rem = d - rl * per_rl;
-    const int uu = rem / p.S_in;
-    const int u = u_lo + uu, w = rem - uu * p.S_in;
-    float part = 0.f;
-    if (live[q]) {   // inside the image
-      float a[CIN];
+              for (int j = 0; j < NB; ++j)
+                acc[q][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[q][h][e], b[j][h][e], acc[q][j], 0, 0, 0);
+        if (kc + 1 < KC) {
 #pragma unroll
-      for (int ci = 0; ci < CIN; ++ci) a[ci] = 0.f;
+          for (int q = 0; q < 2; ++q)
 #pragma unroll
-      for (int ky = 0; ky < 3; ++ky) {
-        int yy = u + p.delta - ky;
-        if (yy < 0 || (yy & (p.stride - 1))) continue;
-        yy /= p.stride;
-        if (yy >= p.S_out) continue;
-#pragma unroll
-        for (int kx = 0; kx < 3; ++kx) {
-          int xx = w + p.delta - kx;
-          if (xx < 0 || (xx & (p.stride - 1))) continue;
-          xx /= p.stride;
-          if (xx >= p.S_out) continue;
-          const float *g = G + (rl * n_row_src + (yy - y_lo) * p.S_out + xx) * GP + 3 * ky + kx;
-#pragma unroll
-          for (int ci = 0; ci < CIN; ++ci) a[ci] += g[9 * ci];
+            for (int h = 0; h < 4; ++h) a[q][h] = an[q][h];
         }
       }
+      // lane holds rows 8 g + 4 half + t (v = 4 g + t) of column 32 j + r32
 #pragma unroll
-      for (int ci = 0; ci < CIN; ++ci) part += a[ci] * bc[q][ci] - fabsf(a[ci]) * br[q][ci];
+      for (int q = 0; q < 2; ++q) {
+        if (q == 1 && !two) break;
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+#pragma unroll
+          for (int v = 0; v < 16; ++v)
+            G[((b0 + 4 * q) * 32 + (v >> 2) * 8 + half * 4 + (v & 3)) * GP + 32 * j + r32] = acc[q][j][v];
+      }
     }
-    p.part[(int64_t)(r0 + rl) * S_in2 + u * p.S_in + w] = part;
+    __syncthreads();
+
+    // ---- gather the taps of every destination position and concretize
+    const int S_in2 = p.S_in * p.S_in;
+#pragma unroll
+    for (int q = 0; q < STEM_DPT; ++q) {
+      const int d = tid + 256 * q;
+      if (d >= n_dst) break;
+      const int rl = d / per_rl, rem = d - rl * per_rl;
+      const int uu = rem / p.S_in;
+      const int u = u_lo + uu, w = rem - uu * p.S_in;
+      float part = 0.f;
+      if (live[q]) {   // inside the image
+        float a[CIN];
+#pragma unroll
+        for (int ci = 0; ci < CIN; ++ci) a[ci] = 0.f;
+#pragma unroll
+        for (int ky = 0; ky < 3; ++ky) {
+          int yy = u + p.delta - ky;
+          if (yy < 0 || (yy & (p.stride - 1))) continue;
+          yy /= p.stride;
+          if (yy >= p.S_out) continue;
+#pragma unroll
+          for (int kx = 0; kx < 3; ++kx) {
+            int xx = w + p.delta - kx;
+            if (xx < 0 || (xx & (p.stride - 1))) continue;
+            xx /= p.stride;
+            if (xx >= p.S_out) continue;
+            const float *g = G + (rl * n_row_src + (yy - y_lo) * p.S_out + xx) * GP + 3 * ky + kx;
+#pragma unroll
+            for (int ci = 0; ci < CIN; ++ci) a[ci] += g[9 * ci];
+          }
+        }
+#pragma unroll
+        for (int ci = 0; ci < CIN; ++ci) part += a[ci] * bc[q][ci] - fabsf(a[ci]) * br[q][ci];
+      }
+      p.part[(int64_t)(r0 + rl) * S_in2 + u * p.S_in + w] = part;
+    }
+    __syncthreads();   // G is rewritten by the next item
   }
 }
 
@@ -682,8 +688,9 @@ hipError_t launch_stem_t(StemArgs a, hipStream_t s) {
     if (!a.strip) return hipErrorInvalidValue;
   }
   a.n_strips = (a.S_in + a.strip - 1) / a.strip;
-  const int64_t grid = ((int64_t)a.R + a.rpw - 1) / a.rpw * a.n_strips;
-  if (grid > 0x7fffffff) return hipErrorInvalidValue;
+  const int64_t items = ((int64_t)a.R + a.rpw - 1) / a.rpw * a.n_strips;
+  if (items > 0x7fffffff) return hipErrorInvalidValue;
+  const int64_t grid = std::min<int64_t>(items, STEM_GRID);
   const size_t lds = sizeof(float) * (size_t)(wt_floats + src_max * GP);
   hipLaunchKernelGGL((k_stem<CIN>), dim3((unsigned)grid), dim3(256), lds, s, a);
   return hipGetLastError();
