@@ -13,8 +13,9 @@
 // The transposed convolution of one row is an implicit GEMM:
 //   out[(r, u, w), ci] = sum_{tap=(ky,kx), co} A_out[r][u'][w'][co] * W[co][ci][ky][kx]
 //   u' = (u + delta - ky) / stride (only when divisible and inside the source window)
-// with M = rows x S_in^2, N = C_in, K = 9 C_out (with stride 2, split by output parity into
-// four GEMMs over their own taps only).  The weights are repacked at load time as
+// with M = rows x S_in^2, N = C_in, K = 9 C_out, run per class of output positions (the
+// positions that the same taps reach: stride parity and the window's border ring) over that
+// class's taps only.  The weights are repacked at load time as
 // Bt[ci][tap * C_out + co] (K-contiguous).  The epilogue applies, per output element at
 // global position (gy, gx):
 //   outside the image          -> 0
