@@ -51,7 +51,7 @@ typedef enum {
   VCR_ERR_STATE = 3,        /* call out of order (e.g. bounds before vcr_load_net) */
   VCR_ERR_OOM = 4,          /* device allocation failed or exceeds the workspace cap */
   VCR_ERR_DEVICE = 5,       /* HIP runtime error (including an earlier asynchronous fault) */
-  VCR_ERR_UNSUPPORTED = 6   /* valid request this build does not implement */
+  VCR_ERR_UNSUPPORTED = 6   /* valid request the library does not implement */
 } vcr_status;
 
 /* Node kinds of a feed-forward network given in topological order. */

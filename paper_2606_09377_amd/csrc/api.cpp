@@ -198,11 +198,12 @@ vcr_status validate_net(vcr_ctx *c, const vcr_node *nodes, int32_t n, const int3
   return VCR_OK;
 }
 
-// The GPU path handles the MLP chain dense (relu dense)*; returns UNSUPPORTED otherwise.
+// The dense path handles the MLP chain dense (relu dense)*; UNSUPPORTED otherwise (the caller
+// then loads the network on the graph path).
 vcr_status check_chain(vcr_ctx *c, const vcr_node *nodes, int32_t n, const int32_t in_chw[3],
                        const std::vector<std::vector<int64_t>> &sh) {
   if (in_chw[1] != 1 || in_chw[2] != 1)
-    return fail(c, VCR_ERR_UNSUPPORTED, "this build bounds MLPs on flat inputs only (got a %dx%dx%d input)",
+    return fail(c, VCR_ERR_UNSUPPORTED, "the dense path takes flat inputs only (got a %dx%dx%d input)",
                 in_chw[0], in_chw[1], in_chw[2]);
   (void)sh;
   for (int32_t i = 0; i < n; ++i) {
@@ -211,11 +212,11 @@ vcr_status check_chain(vcr_ctx *c, const vcr_node *nodes, int32_t n, const int32
     if (want_dense) {
       if (nd.op != VCR_DENSE || nd.in0 != i - 1)
         return fail(c, VCR_ERR_UNSUPPORTED,
-                    "node %d: this build bounds chains dense (relu dense)* only (conv/add/flatten are not built)", i);
+                    "node %d: the dense path takes chains dense (relu dense)* only", i);
     } else {
       if (nd.op != VCR_RELU || nd.in0 != i - 1)
         return fail(c, VCR_ERR_UNSUPPORTED,
-                    "node %d: this build bounds chains dense (relu dense)* only", i);
+                    "node %d: the dense path takes chains dense (relu dense)* only", i);
     }
   }
   return VCR_OK;

@@ -41,6 +41,10 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int LDS_LD = BK + 4;
+constexpr int TPR = BK / 4;             // staging threads per tile row (one 16-byte chunk each)
+constexpr int RPP = 256 / TPR;          // tile rows per staging pass
+constexpr int SQ = 128 / RPP;           // staging passes per 128-row tile
+constexpr int GEMM_MINB = BK == 32 ? 2 : 3;   // workgroups per CU the registers are sized for
 constexpr int NTHREADS = 256;
 constexpr int GROUP_M = 8;
 
@@ -299,7 +303,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &p, f32x16 (&acc)[M
 // the register allocation of the relax epilogue spill-free).  AL adds the alpha-CROWN extras
 // (per-row slopes, stored coefficients) to the backward epilogues.
 template <bool FWD, bool AL, bool AFF = false>
-__global__ __launch_bounds__(NTHREADS, 2) void k_gemm(const GemmArgs p) {
+__global__ __launch_bounds__(NTHREADS, GEMM_MINB) void k_gemm(const GemmArgs p) {
   __shared__ __attribute__((aligned(16))) float As[2][BM * LDS_LD];
   __shared__ __attribute__((aligned(16))) float Bs[2][BN * LDS_LD];
 
@@ -312,12 +316,12 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm(const GemmArgs p) {
   map_tile(blockIdx.x, n_mt * n_nt, n_mt, n_nt, mt, nt);
   const int m0 = mt * BM, n0 = nt * BN;
 
-  // global -> register staging: thread t moves rows t/8 + 32q, columns 4(t%8)..+3
-  const int lrow = tid >> 3, lcol = (tid & 7) << 2;
+  // global -> register staging: thread t moves rows t/TPR + RPP q, columns 4(t%TPR)..+3
+  const int lrow = tid / TPR, lcol = (tid % TPR) * 4;
   const float *Ag = p.A + (int64_t)(m0 + lrow) * p.lda + lcol;
   const float *Bg = p.Bt + (int64_t)(n0 + lrow) * p.ldb + lcol;
-  const int64_t a_step = 32 * p.lda, b_step = 32 * p.ldb;
-  f32x4 ra[4], rb[4];
+  const int64_t a_step = RPP * p.lda, b_step = RPP * p.ldb;
+  f32x4 ra[SQ], rb[SQ];
 
   f32x16 acc[2][2];
 #pragma unroll
@@ -329,7 +333,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm(const GemmArgs p) {
 
   const int KT = p.K / BK;
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
+  for (int q = 0; q < SQ; ++q) {
     ra[q] = *reinterpret_cast<const f32x4 *>(Ag + q * a_step);
     rb[q] = *reinterpret_cast<const f32x4 *>(Bg + q * b_step);
     if constexpr (AFF) {
@@ -337,14 +341,14 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm(const GemmArgs p) {
     }
   }
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    *reinterpret_cast<f32x4 *>(&As[0][(lrow + 32 * q) * LDS_LD + lcol]) = ra[q];
-    *reinterpret_cast<f32x4 *>(&Bs[0][(lrow + 32 * q) * LDS_LD + lcol]) = rb[q];
+  for (int q = 0; q < SQ; ++q) {
+    *reinterpret_cast<f32x4 *>(&As[0][(lrow + RPP * q) * LDS_LD + lcol]) = ra[q];
+    *reinterpret_cast<f32x4 *>(&Bs[0][(lrow + RPP * q) * LDS_LD + lcol]) = rb[q];
   }
   __syncthreads();
 
   const int r32 = lane & 31;
-  const int kq = (lane >> 5) * 16;
+  const int kq = (lane >> 5) * (BK / 2);
   const int a_off0 = (wm * 64 + r32) * LDS_LD + kq;
   const int a_off1 = a_off0 + 32 * LDS_LD;
   const int b_off0 = (wn * 64 + r32) * LDS_LD + kq;
@@ -356,7 +360,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm(const GemmArgs p) {
     if (more) {
       const int k0 = (kt + 1) * BK;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
+      for (int q = 0; q < SQ; ++q) {
         ra[q] = *reinterpret_cast<const f32x4 *>(Ag + q * a_step + k0);
         rb[q] = *reinterpret_cast<const f32x4 *>(Bg + q * b_step + k0);
         if constexpr (AFF) {
@@ -367,7 +371,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm(const GemmArgs p) {
     const float *as = As[cur];
     const float *bs = Bs[cur];
 #pragma unroll
-    for (int h = 0; h < 4; ++h) {
+    for (int h = 0; h < BK / 8; ++h) {
       const f32x4 a0 = *reinterpret_cast<const f32x4 *>(as + a_off0 + 4 * h);
       const f32x4 a1 = *reinterpret_cast<const f32x4 *>(as + a_off1 + 4 * h);
       const f32x4 b0 = *reinterpret_cast<const f32x4 *>(bs + b_off0 + 4 * h);
@@ -382,9 +386,9 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_gemm(const GemmArgs p) {
     }
     if (more) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        *reinterpret_cast<f32x4 *>(&As[cur ^ 1][(lrow + 32 * q) * LDS_LD + lcol]) = ra[q];
-        *reinterpret_cast<f32x4 *>(&Bs[cur ^ 1][(lrow + 32 * q) * LDS_LD + lcol]) = rb[q];
+      for (int q = 0; q < SQ; ++q) {
+        *reinterpret_cast<f32x4 *>(&As[cur ^ 1][(lrow + RPP * q) * LDS_LD + lcol]) = ra[q];
+        *reinterpret_cast<f32x4 *>(&Bs[cur ^ 1][(lrow + RPP * q) * LDS_LD + lcol]) = rb[q];
       }
     }
     __syncthreads();
@@ -410,16 +414,16 @@ __global__ __launch_bounds__(128) void k_gemm_small(const GemmArgs p) {
   int mt, nt;
   map_tile(blockIdx.x, n_mt * n_nt, n_mt, n_nt, mt, nt);
   const int m0 = mt * SM_BM, n0 = nt * SM_BN;
-  const int r32 = lane & 31, kq = (lane >> 5) * 16;
+  const int r32 = lane & 31, kq = (lane >> 5) * (BK / 2);
   const float *Ag = p.A + (int64_t)(m0 + r32) * p.lda + kq;
   const float *Bg = p.Bt + (int64_t)(n0 + bj * 32 + r32) * p.ldb + kq;
   f32x16 acc[1][1];
 #pragma unroll
   for (int v = 0; v < 16; ++v) acc[0][0][v] = 0.f;
-  f32x4 a[4], b[4], a1[4], b1[4], a2[4], b2[4];
+  f32x4 a[BK / 8], b[BK / 8], a1[BK / 8], b1[BK / 8], a2[BK / 8], b2[BK / 8];
   auto load = [&](int k0, f32x4 *ra, f32x4 *rb) {
 #pragma unroll
-    for (int h = 0; h < 4; ++h) {
+    for (int h = 0; h < BK / 8; ++h) {
       ra[h] = *reinterpret_cast<const f32x4 *>(Ag + k0 + 4 * h);
       rb[h] = *reinterpret_cast<const f32x4 *>(Bg + k0 + 4 * h);
       if constexpr (AFF) {
@@ -433,12 +437,12 @@ __global__ __launch_bounds__(128) void k_gemm_small(const GemmArgs p) {
   for (int kt = 0; kt < KT; ++kt) {
     if (kt + 2 < KT) load((kt + 2) * BK, a2, b2);
 #pragma unroll
-    for (int h = 0; h < 4; ++h)
+    for (int h = 0; h < BK / 8; ++h)
 #pragma unroll
       for (int e = 0; e < 4; ++e)
         acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[h][e], b[h][e], acc[0][0], 0, 0, 0);
 #pragma unroll
-    for (int h = 0; h < 4; ++h) {
+    for (int h = 0; h < BK / 8; ++h) {
       a[h] = a1[h];
       b[h] = b1[h];
       a1[h] = a2[h];
