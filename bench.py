@@ -25,10 +25,11 @@ sys.path.insert(0, ROOT)
 
 PEAK_FP32_MFMA_TFLOPS = 157.3   # MI355X dense fp32 matrix peak
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
-KERNEL_SOURCES = {"k_gemm": "gemm.hip", "k_convt": "conv.hip", "k_gemm_small": "gemm.hip"}
+KERNEL_SOURCES = {"k_gemm": "gemm.hip", "k_convt": "conv.hip", "k_gemm_small": "gemm.hip", "k_gemm_mid": "gemm.hip"}
 KERNEL_DESC = {"k_gemm": "k_gemm (dense A.W step, fp32 v_mfma_f32_32x32x2f32)",
                "k_convt": "k_convt (transposed-conv implicit GEMM, fp32 v_mfma_f32_32x32x2f32)",
-               "k_gemm_small": "k_gemm_small (dense A.W step on 32x64 tiles, fp32 v_mfma_f32_32x32x2f32)"}
+               "k_gemm_small": "k_gemm_small (dense A.W step on 32x64 tiles, fp32 v_mfma_f32_32x32x2f32)",
+               "k_gemm_mid": "k_gemm_mid (dense A.W step on 64x64 tiles, fp32 v_mfma_f32_32x32x2f32)"}
 
 
 def source_hash(kernel):
@@ -203,9 +204,9 @@ def bench_bab_loop(args):
     res = results[-1]
     assert all(r == res for r in results), "the loop is deterministic"
     domains = res["evaluated"] * args.steps
-    launches = st["timed_gemm_launches"] + st["timed_small_launches"]
-    gms = st["timed_gemm_ms"] + st["timed_small_ms"]
-    gfl = st["timed_gemm_flops"] + st["timed_small_flops"]
+    launches = st["timed_gemm_launches"] + st["timed_small_launches"] + st["timed_mid_launches"]
+    gms = st["timed_gemm_ms"] + st["timed_small_ms"] + st["timed_mid_ms"]
+    gfl = st["timed_gemm_flops"] + st["timed_small_flops"] + st["timed_mid_flops"]
     achieved = gfl / (gms / 1e3) / 1e12 if gms > 0 else None
     rec = {
         "metric": "CROWN bound evals/sec (inputs or BaB domains) at 1 GPU; % fp32 MFMA peak",
@@ -344,7 +345,8 @@ def main():
     value = units * args.steps / dt
     timed = {"k_gemm": (st["timed_gemm_launches"], st["timed_gemm_ms"], st["timed_gemm_flops"]),
              "k_convt": (st["timed_conv_launches"], st["timed_conv_ms"], st["timed_conv_flops"]),
-             "k_gemm_small": (st["timed_small_launches"], st["timed_small_ms"], st["timed_small_flops"])}
+             "k_gemm_small": (st["timed_small_launches"], st["timed_small_ms"], st["timed_small_flops"]),
+             "k_gemm_mid": (st["timed_mid_launches"], st["timed_mid_ms"], st["timed_mid_flops"])}
 
     def roofline(kernel):
         launches, ms, fl = timed[kernel]

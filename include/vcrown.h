@@ -40,7 +40,7 @@
 extern "C" {
 #endif
 
-#define VCR_ABI_VERSION 1
+#define VCR_ABI_VERSION 2   /* 2: vcr_stats gained timed_mid_* */
 
 typedef struct vcr_ctx vcr_ctx;
 
@@ -141,6 +141,11 @@ typedef struct {
   uint64_t timed_small_launches;
   double timed_small_ms;
   uint64_t timed_small_flops;
+  /* the dense GEMM launches of middle size (too few 128 x 128 tiles, enough 64 x 64 ones),
+   * which run a 64 x 64 tile kernel (not included in the two above) */
+  uint64_t timed_mid_launches;
+  double timed_mid_ms;
+  uint64_t timed_mid_flops;
 } vcr_stats;
 
 /* ABI version compiled into the library (VCR_ABI_VERSION). */

@@ -324,7 +324,7 @@ vcr_status vcr_set_option(vcr_ctx *c, int32_t key, double v) {
       c->time_gemm = v != 0.0;
       c->ev_used = 0;
       c->pending.clear();
-      for (int k = 0; k < 3; ++k) {
+      for (int k = 0; k < 4; ++k) {
         c->timed_launches[k] = c->timed_flops[k] = 0;
         c->timed_ms[k] = 0.0;
       }
@@ -1434,6 +1434,9 @@ vcr_status vcr_get_stats(vcr_ctx *c, vcr_stats *out) {
   out->timed_small_launches = c->timed_launches[2];
   out->timed_small_ms = c->timed_ms[2];
   out->timed_small_flops = c->timed_flops[2];
+  out->timed_mid_launches = c->timed_launches[3];
+  out->timed_mid_ms = c->timed_ms[3];
+  out->timed_mid_flops = c->timed_flops[3];
   if (c->lastL.empty()) return VCR_OK;
   int32_t *cnt = c->d_counters;
   const int R = std::min<int>((int)c->lastL.size(), 64);

@@ -80,12 +80,12 @@ struct vcr_ctx {
   hipGraphExec_t gexec = nullptr;
   std::vector<uint64_t> gkey;
   // timing of the GEMM launches (VCR_OPT_TIME_GEMM); kind 0 = dense k_gemm, 1 = conv k_convt,
-  // 2 = dense k_gemm_small
+  // 2 = dense k_gemm_small, 3 = dense k_gemm_mid
   int32_t time_gemm = 0;
   std::vector<hipEvent_t> ev_pool;      // pairs: start, stop
   size_t ev_used = 0;                   // events recorded but not yet read
-  uint64_t timed_launches[3] = {0, 0, 0}, timed_flops[3] = {0, 0, 0};
-  double timed_ms[3] = {0.0, 0.0, 0.0};
+  uint64_t timed_launches[4] = {0, 0, 0, 0}, timed_flops[4] = {0, 0, 0, 0};
+  double timed_ms[4] = {0.0, 0.0, 0.0, 0.0};
   std::vector<std::pair<uint64_t, int>> pending;  // (flops, kind) of each recorded pair
 };
 
@@ -105,9 +105,9 @@ inline vcr_status fail(vcr_ctx *c, vcr_status st, const char *fmt, ...) {
     if (e_ != hipSuccess) return fail((c), VCR_ERR_DEVICE, "%s: %s", #expr, hipGetErrorString(e_)); \
   } while (0)
 
-// A dense GEMM launch timed under the kernel it runs (k_gemm or k_gemm_small).
+// A dense GEMM launch timed under the kernel it runs (k_gemm, k_gemm_small or k_gemm_mid).
 #define TIMED_GEMM(c, s, flops, args)                                                            \
-  timed_launch((c), (s), vcr::gemm_is_small(args) ? 2 : 0, (flops), [&] { return vcr::launch_gemm((args), (s)); })
+  timed_launch((c), (s), vcr::gemm_kind(args), (flops), [&] { return vcr::launch_gemm((args), (s)); })
 
 // Reads every recorded timing pair into the sums (waits for the last one).
 vcr_status timing_fold(vcr_ctx *c);

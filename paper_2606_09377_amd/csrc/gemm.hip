@@ -452,8 +452,80 @@ __global__ __launch_bounds__(128) void k_gemm_small(const GemmArgs p) {
   gemm_epilogue<FWD, AL, AFF, 1, 1>(p, acc, m0, 0, n0, lane, SM_BM, bj, xpart);
 }
 
-bool gemm_is_small(const GemmArgs &a) {
-  return a.M_pad > 0 && a.N_pad > 0 && (int64_t)(a.M_pad / BM) * (a.N_pad / BN) < SMALL_GRID;
+// Mid-size launches (too few 128 x 128 tiles, enough 64 x 64 ones): 64 x 64 tiles staged
+// through double-buffered LDS like k_gemm, four waves of 32 x 32.  Each accumulator sees
+// k_gemm's MFMA sequence and the two column waves of a row block add their row sums in
+// k_gemm's order (through LDS), so the bits are k_gemm's; the operands cross the L2 half as
+// often as in the small-tile kernel.
+constexpr int MD_BM = 64, MD_BN = 64;
+constexpr int64_t MID_GRID = 256;   // 64 x 64 tiles from which the mid-size kernel runs
+
+template <bool FWD, bool AL, bool AFF = false>
+__global__ __launch_bounds__(256) void k_gemm_mid(const GemmArgs p) {
+  __shared__ __attribute__((aligned(16))) float As[2][MD_BM * LDS_LD];
+  __shared__ __attribute__((aligned(16))) float Bs[2][MD_BN * LDS_LD];
+  __shared__ float xpart[2][16 * 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int n_mt = p.M_pad / MD_BM, n_nt = p.N_pad / MD_BN;
+  int mt, nt;
+  map_tile(blockIdx.x, n_mt * n_nt, n_mt, n_nt, mt, nt);
+  const int m0 = mt * MD_BM, n0 = nt * MD_BN;
+
+  // global -> register staging: thread t moves rows t/TPR + RPP q of both operand tiles
+  constexpr int MQ = MD_BM / RPP;
+  const int lrow = tid / TPR, lcol = (tid % TPR) * 4;
+  const float *Ag = p.A + (int64_t)(m0 + lrow) * p.lda + lcol;
+  const float *Bg = p.Bt + (int64_t)(n0 + lrow) * p.ldb + lcol;
+  const int64_t a_step = RPP * p.lda, b_step = RPP * p.ldb;
+  f32x4 ra[MQ], rb[MQ];
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int q = 0; q < MQ; ++q) {
+      ra[q] = *reinterpret_cast<const f32x4 *>(Ag + q * a_step + k0);
+      rb[q] = *reinterpret_cast<const f32x4 *>(Bg + q * b_step + k0);
+      if constexpr (AFF) {
+        if (p.abs_b) rb[q] = __builtin_elementwise_abs(rb[q]);
+      }
+    }
+  };
+  auto lstore = [&](int buf) {
+#pragma unroll
+    for (int q = 0; q < MQ; ++q) {
+      *reinterpret_cast<f32x4 *>(&As[buf][(lrow + RPP * q) * LDS_LD + lcol]) = ra[q];
+      *reinterpret_cast<f32x4 *>(&Bs[buf][(lrow + RPP * q) * LDS_LD + lcol]) = rb[q];
+    }
+  };
+
+  f32x16 acc[1][1];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) acc[0][0][v] = 0.f;
+  const int KT = p.K / BK;
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  const int r32 = lane & 31, kq = (lane >> 5) * (BK / 2);
+  const int a_off = (wm * 32 + r32) * LDS_LD + kq, b_off = (wn * 32 + r32) * LDS_LD + kq;
+  for (int kt = 0; kt < KT; ++kt) {
+    const int cur = kt & 1;
+    const bool more = kt + 1 < KT;
+    if (more) gload((kt + 1) * BK);
+#pragma unroll
+    for (int h = 0; h < BK / 8; ++h) {
+      const f32x4 a = *reinterpret_cast<const f32x4 *>(As[cur] + a_off + 4 * h);
+      const f32x4 b = *reinterpret_cast<const f32x4 *>(Bs[cur] + b_off + 4 * h);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[e], b[e], acc[0][0], 0, 0, 0);
+    }
+    if (more) lstore(cur ^ 1);
+    __syncthreads();
+  }
+  gemm_epilogue<FWD, AL, AFF, 1, 1>(p, acc, m0, wm * 32, n0, lane, MD_BM, wn, xpart[wm]);
+}
+
+int gemm_kind(const GemmArgs &a) {
+  if (a.M_pad <= 0 || a.N_pad <= 0 || (int64_t)(a.M_pad / BM) * (a.N_pad / BN) >= SMALL_GRID) return 0;
+  return (int64_t)(a.M_pad / MD_BM) * (a.N_pad / MD_BN) >= MID_GRID ? 3 : 2;
 }
 
 hipError_t launch_gemm(const GemmArgs &a, hipStream_t s) {
@@ -472,8 +544,22 @@ hipError_t launch_gemm(const GemmArgs &a, hipStream_t s) {
   const bool al = a.alpha || a.pre;
   if (a.mode != EPI_RELAX && a.mode != EPI_CONCRETIZE && a.mode != EPI_FORWARD && a.mode != EPI_AFFINE)
     return hipErrorInvalidValue;
+  const int64_t mid = (int64_t)(a.M_pad / MD_BM) * (a.N_pad / MD_BN);
+  if (grid < SMALL_GRID && mid >= MID_GRID) {   // gemm_kind 3
+    // too few 128 x 128 tiles to fill the chip, enough of 64 x 64 (same bits)
+    const dim3 g((unsigned)mid), t(256);
+    if (a.mode == EPI_AFFINE)
+      hipLaunchKernelGGL((k_gemm_mid<false, false, true>), g, t, 0, s, a);
+    else if (a.mode == EPI_FORWARD)
+      hipLaunchKernelGGL((k_gemm_mid<true, true>), g, t, 0, s, a);
+    else if (al)
+      hipLaunchKernelGGL((k_gemm_mid<false, true>), g, t, 0, s, a);
+    else
+      hipLaunchKernelGGL((k_gemm_mid<false, false>), g, t, 0, s, a);
+    return hipGetLastError();
+  }
   if (grid < SMALL_GRID) {
-    // too few 128 x 128 tiles to fill the chip: 32 x 64 tiles, one wave each (same bits)
+    // too few tiles of either size: 32 x 64 tiles, two waves each (same bits)
     const int64_t sg = (int64_t)(a.M_pad / SM_BM) * (a.N_pad / SM_BN);
     const dim3 g((unsigned)sg), t(128);
     if (a.mode == EPI_AFFINE)

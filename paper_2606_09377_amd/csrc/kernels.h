@@ -77,8 +77,8 @@ struct GemmArgs {
 };
 
 hipError_t launch_gemm(const GemmArgs &a, hipStream_t s);
-// true when launch_gemm runs the small-tile kernel for these arguments
-bool gemm_is_small(const GemmArgs &a);
+// The kernel launch_gemm runs for these arguments: 0 k_gemm, 2 k_gemm_small, 3 k_gemm_mid.
+int gemm_kind(const GemmArgs &a);
 
 // ---- bandwidth-bound kernels -------------------------------------------------------
 hipError_t launch_fill(float *p, int64_t n, float v, hipStream_t s);

@@ -14,6 +14,7 @@ import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "lib", "libvcrown.so")
+ABI_VERSION = 2   # VCR_ABI_VERSION of include/vcrown.h this binding is written for
 HEADER = os.path.join(os.path.dirname(HERE), "include", "vcrown.h")
 
 VCR_OK, VCR_ERR_ARG, VCR_ERR_SHAPE, VCR_ERR_STATE, VCR_ERR_OOM, VCR_ERR_DEVICE, VCR_ERR_UNSUPPORTED = range(7)
@@ -44,7 +45,9 @@ class VcrStats(ctypes.Structure):
                 ("timed_gemm_flops", ctypes.c_uint64), ("timed_conv_launches", ctypes.c_uint64),
                 ("timed_conv_ms", ctypes.c_double), ("timed_conv_flops", ctypes.c_uint64),
                 ("net_bytes", ctypes.c_uint64), ("timed_small_launches", ctypes.c_uint64),
-                ("timed_small_ms", ctypes.c_double), ("timed_small_flops", ctypes.c_uint64)]
+                ("timed_small_ms", ctypes.c_double), ("timed_small_flops", ctypes.c_uint64),
+                ("timed_mid_launches", ctypes.c_uint64), ("timed_mid_ms", ctypes.c_double),
+                ("timed_mid_flops", ctypes.c_uint64)]
 
 
 class VcrAlphaOpts(ctypes.Structure):
@@ -111,6 +114,9 @@ def load_library(path: str = LIB_PATH):
         fn = getattr(lib, name)
         fn.argtypes = args
         fn.restype = res
+    if lib.vcr_abi_version() != ABI_VERSION:
+        raise RuntimeError(f"{path} has ABI version {lib.vcr_abi_version()}, this binding expects {ABI_VERSION}: "
+                           "rebuild the library")
     _lib = lib
     return lib
 
@@ -361,7 +367,9 @@ class Ctx:
                 "timed_gemm_flops": int(s.timed_gemm_flops), "timed_conv_launches": int(s.timed_conv_launches),
                 "timed_conv_ms": s.timed_conv_ms, "timed_conv_flops": int(s.timed_conv_flops),
                 "net_bytes": int(s.net_bytes), "timed_small_launches": int(s.timed_small_launches),
-                "timed_small_ms": s.timed_small_ms, "timed_small_flops": int(s.timed_small_flops)}
+                "timed_small_ms": s.timed_small_ms, "timed_small_flops": int(s.timed_small_flops),
+                "timed_mid_launches": int(s.timed_mid_launches), "timed_mid_ms": s.timed_mid_ms,
+                "timed_mid_flops": int(s.timed_mid_flops)}
 
 
 def _relu_sizes(net):
