@@ -370,12 +370,23 @@ __global__ __launch_bounds__(NTHREADS, GEMM_MINB) void k_gemm(const GemmArgs p) 
     }
     const float *as = As[cur];
     const float *bs = Bs[cur];
+    // all operand reads of the K tile first (the scheduler then spreads them over the MFMAs
+    // instead of stalling half-way through the tile), then the next tile's global loads
+    f32x4 A0[BK / 8], A1[BK / 8], B0[BK / 8], B1[BK / 8];
 #pragma unroll
     for (int h = 0; h < BK / 8; ++h) {
-      const f32x4 a0 = *reinterpret_cast<const f32x4 *>(as + a_off0 + 4 * h);
-      const f32x4 a1 = *reinterpret_cast<const f32x4 *>(as + a_off1 + 4 * h);
-      const f32x4 b0 = *reinterpret_cast<const f32x4 *>(bs + b_off0 + 4 * h);
-      const f32x4 b1 = *reinterpret_cast<const f32x4 *>(bs + b_off1 + 4 * h);
+      A0[h] = *reinterpret_cast<const f32x4 *>(as + a_off0 + 4 * h);
+      A1[h] = *reinterpret_cast<const f32x4 *>(as + a_off1 + 4 * h);
+      B0[h] = *reinterpret_cast<const f32x4 *>(bs + b_off0 + 4 * h);
+      B1[h] = *reinterpret_cast<const f32x4 *>(bs + b_off1 + 4 * h);
+    }
+    // scheduling groups (masks: 0x100 LDS reads, 0x020 global reads, 0x008 MFMA)
+    __builtin_amdgcn_sched_group_barrier(0x100, 4 * (BK / 8), 0);
+    __builtin_amdgcn_sched_group_barrier(0x020, 2 * SQ, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 16 * (BK / 8), 0);
+#pragma unroll
+    for (int h = 0; h < BK / 8; ++h) {
+      const f32x4 a0 = A0[h], a1 = A1[h], b0 = B0[h], b1 = B1[h];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0[e], b0[e], acc[0][0], 0, 0, 0);
