@@ -87,6 +87,61 @@ __device__ __forceinline__ float4 split_override(const SplitTable &st, int row, 
   return prm;
 }
 
+// Split lookups of one tile through LDS: flags[d - d0][n - n0] is the entry index of
+// (domain d, neuron n) at this ReLU, or -1.  All threads of the workgroup build it once, so
+// the per-element lookup is one LDS read instead of a walk over the domain's entries in
+// global memory.  Tiles spanning more than SPLIT_ND domains keep the global walk.
+constexpr int SPLIT_ND = 16;
+struct TileSplits {
+  const signed char *flags;   // null: look up in global memory
+  int d0, n0, cols;
+};
+
+__device__ __forceinline__ TileSplits tile_splits_build(const SplitTable &st, int relu, int m0, int tile_rows,
+                                                        int n0, int cols, signed char *lds) {
+  TileSplits t{nullptr, 0, n0, cols};
+  if (st.D <= 0 || !lds) return t;   // uniform over the workgroup
+  const int d0 = min(m0 / st.rows_per_domain, st.D - 1);
+  const int d1 = min((m0 + tile_rows - 1) / st.rows_per_domain, st.D - 1);
+  const int nd = d1 - d0 + 1;
+  if (nd > SPLIT_ND) return t;
+  for (int i = threadIdx.x; i < nd * cols; i += blockDim.x) lds[i] = -1;
+  __syncthreads();
+  for (int i = threadIdx.x; i < nd * st.S; i += blockDim.x) {
+    const int dl = i / st.S, e = i - dl * st.S, d = d0 + dl;
+    const int e0 = st.off[d * (st.R + 1) + relu], e1 = st.off[d * (st.R + 1) + relu + 1];
+    if (e >= e0 && e < e1) {
+      const int n = st.ent_n[d * st.S + e];
+      if (n >= n0 && n < n0 + cols) lds[dl * cols + (n - n0)] = (signed char)e;
+    }
+  }
+  __syncthreads();
+  t.flags = lds;
+  t.d0 = d0;
+  return t;
+}
+
+// split_override through the tile's table when there is one (the same entry, so the same
+// parameters)
+__device__ __forceinline__ float4 split_lookup(const SplitTable &st, const TileSplits &t, int row, int relu, int n,
+                                               float4 prm, int *ent = nullptr, float *sterm = nullptr) {
+  if (!t.flags) return split_override(st, row, relu, n, prm, ent, sterm);
+  int d = row / st.rows_per_domain;
+  d = d < st.D ? d : st.D - 1;
+  const int e = t.flags[(d - t.d0) * t.cols + (n - t.n0)];
+  if (e >= 0) {
+    const float4 q = st.ent_p[d * st.S + e];
+    prm.x = q.x;
+    prm.y = q.y;
+    prm.z = q.z;
+    if (ent) {
+      *ent = e;
+      *sterm = q.w;
+    }
+  }
+  return prm;
+}
+
 // Epilogue of one wave: MB blocks of 32 rows from tile-relative row wrow of the tile at m0
 // (tile_rows high), 64 columns from col0 (one partial sum per row and 64 columns, so every
 // tiling gives the same bits), accumulators acc[MB][2].
@@ -105,7 +160,7 @@ __device__ __forceinline__ void gemm_epilogue_body(const GemmArgs &p, f32x16 (&a
                                                    float *__restrict__ pre_t, float *__restrict__ out_t,
                                                    float *__restrict__ grad_t, const float *__restrict__ sbeta,
                                                    float *__restrict__ gbeta, const float *__restrict__ biasp,
-                                                   float *__restrict__ partp) {
+                                                   float *__restrict__ partp, const TileSplits &ts) {
   const int r32 = lane & 31;
   // 32x32 accumulator layout: lane holds column (lane % 32) and rows
   // 8 (v / 4) + 4 (lane / 32) + (v % 4), v = 0..15.
@@ -164,7 +219,7 @@ __device__ __forceinline__ void gemm_epilogue_body(const GemmArgs &p, f32x16 (&a
           }
           int ent = -1;
           float sterm = 0.f;
-          if (has_splits) prm = split_override(p.splits, row, p.relu_index, n, prm, &ent, &sterm);
+          if (has_splits) prm = split_lookup(p.splits, ts, row, p.relu_index, n, prm, &ent, &sterm);
           const bool unst = prm.z > 0.f;
           const float al = alpha_t[off];   // loaded for every row: no load waits on prm
           const float lam = unst ? al : prm.x;
@@ -196,9 +251,9 @@ __device__ __forceinline__ void gemm_epilogue_body(const GemmArgs &p, f32x16 (&a
           float sterm = 0.f;
           if (has_splits) {
             if constexpr (AL)
-              prm = split_override(p.splits, row, p.relu_index, n, prm, &ent, &sterm);
+              prm = split_lookup(p.splits, ts, row, p.relu_index, n, prm, &ent, &sterm);
             else
-              prm = split_override(p.splits, row, p.relu_index, n, prm);
+              prm = split_lookup(p.splits, ts, row, p.relu_index, n, prm);
           }
           const float a = acc[bi][jj][v];
           float lam = prm.x;
@@ -287,15 +342,20 @@ __device__ __forceinline__ void gemm_epilogue_body(const GemmArgs &p, f32x16 (&a
 
 // Stores and row-wise loads address the tile from a wave-uniform base with 32-bit lane offsets
 // (every row-indexed array of one launch shares the pitch ld).
+// tn0, tcols: the workgroup tile's first column and width; sflag: free LDS for the tile's
+// split table (SPLIT_ND x tcols bytes), or null.  Every thread of the workgroup calls this.
 template <bool FWD, bool AL, bool AFF, int MB, int NBJ = 2>
 __device__ __forceinline__ void gemm_epilogue(const GemmArgs &p, f32x16 (&acc)[MB][NBJ], int m0, int wrow, int col0,
-                                              int lane, int tile_rows, int bj1 = 0, float *xpart = nullptr) {
+                                              int lane, int tile_rows, int bj1, float *xpart, int tn0, int tcols,
+                                              signed char *sflag) {
   const int64_t ld = p.mode == EPI_CONCRETIZE ? p.ld_pre : p.ldo;
   const int64_t tbase = (int64_t)m0 * ld;
+  TileSplits ts{nullptr, 0, tn0, tcols};
+  if (!AFF && p.mode != EPI_CONCRETIZE) ts = tile_splits_build(p.splits, p.relu_index, m0, tile_rows, tn0, tcols, sflag);
   gemm_epilogue_body<FWD, AL, AFF, MB, NBJ>(
       p, acc, m0, wrow, col0, lane, tile_rows, bj1, xpart, p.P, p.c0, p.r0, p.alpha ? p.alpha + tbase : nullptr,
       p.pre ? p.pre + tbase : nullptr, p.mode == EPI_CONCRETIZE ? nullptr : p.out + tbase,
-      p.grad ? p.grad + tbase : nullptr, p.splits.beta, p.splits.grad_beta, p.bias, p.part);
+      p.grad ? p.grad + tbase : nullptr, p.splits.beta, p.splits.grad_beta, p.bias, p.part, ts);
 }
 
 // Instantiations: FWD selects the forward epilogue (alpha-CROWN's gradient pass); otherwise the
@@ -406,7 +466,8 @@ __global__ __launch_bounds__(NTHREADS, GEMM_MINB) void k_gemm(const GemmArgs p) 
   }
 
   // ---- epilogue ---------------------------------------------------------------------
-  gemm_epilogue<FWD, AL, AFF, 2>(p, acc, m0, wm * 64, n0 + wn * 64, lane, BM);
+  gemm_epilogue<FWD, AL, AFF, 2>(p, acc, m0, wm * 64, n0 + wn * 64, lane, BM, 0, nullptr, n0, BN,
+                                 reinterpret_cast<signed char *>(&As[0][0]));
 }
 
 // Small launches (few row tiles): a workgroup of two waves owns a 32 x 64 tile, each wave one
@@ -420,6 +481,7 @@ constexpr int64_t SMALL_GRID = 512;   // 128 x 128 tiles below which the small k
 template <bool FWD, bool AL, bool AFF = false>
 __global__ __launch_bounds__(128) void k_gemm_small(const GemmArgs p) {
   __shared__ float xpart[16 * 64];
+  __shared__ signed char sflag[SPLIT_ND * SM_BN];
   const int lane = threadIdx.x & 63, bj = threadIdx.x >> 6;
   const int n_mt = p.M_pad / SM_BM, n_nt = p.N_pad / SM_BN;
   int mt, nt;
@@ -460,7 +522,7 @@ __global__ __launch_bounds__(128) void k_gemm_small(const GemmArgs p) {
       b1[h] = b2[h];
     }
   }
-  gemm_epilogue<FWD, AL, AFF, 1, 1>(p, acc, m0, 0, n0, lane, SM_BM, bj, xpart);
+  gemm_epilogue<FWD, AL, AFF, 1, 1>(p, acc, m0, 0, n0, lane, SM_BM, bj, xpart, n0, SM_BN, sflag);
 }
 
 // Mid-size launches (too few 128 x 128 tiles, enough 64 x 64 ones): 64 x 64 tiles staged
@@ -531,7 +593,8 @@ __global__ __launch_bounds__(256) void k_gemm_mid(const GemmArgs p) {
     if (more) lstore(cur ^ 1);
     __syncthreads();
   }
-  gemm_epilogue<FWD, AL, AFF, 1, 1>(p, acc, m0, wm * 32, n0, lane, MD_BM, wn, xpart[wm]);
+  gemm_epilogue<FWD, AL, AFF, 1, 1>(p, acc, m0, wm * 32, n0, lane, MD_BM, wn, xpart[wm], n0, MD_BN,
+                                    reinterpret_cast<signed char *>(&As[0][0]));
 }
 
 int gemm_kind(const GemmArgs &a) {
