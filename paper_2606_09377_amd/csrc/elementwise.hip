@@ -117,75 +117,58 @@ hipError_t launch_box(const float *x0, int32_t B, int32_t n0, int64_t ld0, float
 // ------------------------------------------------------------------------------------
 // IBP through a dense layer in centre/radius form: c' = W c + b, r' = |W| r, which is the
 // interval step W+ l + W- u + b, W+ u + W- l + b with l = c - r, u = c + r.  With relu_in
-// the input is first passed through ReLU: [max(l, 0), max(u, 0)].  One workgroup owns 32
-// output neurons x 16 inputs and streams W once through LDS in 64-wide K chunks.
-constexpr int IBP_TO = 32, IBP_TB = 16, IBP_KC = 64;
+// the input is first passed through ReLU: [max(l, 0), max(u, 0)].  One wave per output
+// neuron and tile of up to IBP_TB inputs: the lanes stride over K (the weight row is read
+// once, coalesced), then a fixed butterfly, so the summation order does not depend on the
+// batch; every output has its own wave, which keeps small batches parallel too.
+constexpr int IBP_TB = 16;
 
 __global__ __launch_bounds__(256) void k_ibp_dense(const float *Wp, int64_t ldw, const float *bias,
                                                    int32_t n_out, int32_t n_in, const float *cin,
                                                    const float *rin, int64_t ld_in, int32_t relu_in,
                                                    float *cout, float *rout, int64_t ld_out, int32_t B) {
-  __shared__ float Ws[IBP_TO][IBP_KC + 1];
-  __shared__ float Cs[IBP_TB][IBP_KC + 1];
-  __shared__ float Rs[IBP_TB][IBP_KC + 1];
-  const int tid = threadIdx.x;
-  const int o_loc = tid >> 3, bq = tid & 7;
-  const int64_t o = (int64_t)blockIdx.x * IBP_TO + o_loc;
+  const int lane = threadIdx.x & 63;
+  const int64_t o = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int b0 = blockIdx.y * IBP_TB;
-  float c_a = 0.f, r_a = 0.f, c_b = 0.f, r_b = 0.f;
-  for (int64_t k0 = 0; k0 < n_in; k0 += IBP_KC) {
-    {  // W tile: 32 rows x 64, 8 floats per thread
-      const int wr = tid >> 3, wc = (tid & 7) * 8;
-      const int64_t go = (int64_t)blockIdx.x * IBP_TO + wr;
+  if (o >= ld_out) return;   // wave-uniform
+  const int nb = min(IBP_TB, B - b0);
+  float ac[IBP_TB], ar[IBP_TB];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int64_t k = k0 + wc + e;
-        Ws[wr][wc + e] = (go < n_out && k < ld_in) ? Wp[go * ldw + k] : 0.f;
-      }
-    }
-    {  // input tile: 16 inputs x 64, 4 floats per thread
-      const int ib = tid >> 4, ic = (tid & 15) * 4;
-      const int gb = b0 + ib;
+  for (int b = 0; b < IBP_TB; ++b) ac[b] = ar[b] = 0.f;
+  if (o < n_out) {
+    const float *wrow = Wp + o * ldw;
+#pragma unroll 1
+    for (int64_t k = lane; k < n_in; k += 64) {
+      const float w = wrow[k], aw = fabsf(w);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int64_t k = k0 + ic + e;
-        float c = 0.f, r = 0.f;
-        if (gb < B && k < ld_in) {
-          c = cin[(int64_t)gb * ld_in + k];
-          r = rin[(int64_t)gb * ld_in + k];
+      for (int b = 0; b < IBP_TB; ++b) {
+        if (b < nb) {
+          float c = cin[(int64_t)(b0 + b) * ld_in + k], r = rin[(int64_t)(b0 + b) * ld_in + k];
           if (relu_in) {
             const float lo = fmaxf(c - r, 0.f), hi = fmaxf(c + r, 0.f);
             c = (lo + hi) * 0.5f;
             r = (hi - lo) * 0.5f;
           }
+          ac[b] += w * c;
+          ar[b] += aw * r;
         }
-        Cs[ib][ic + e] = c;
-        Rs[ib][ic + e] = r;
       }
     }
-    __syncthreads();
-#pragma unroll 8
-    for (int kk = 0; kk < IBP_KC; ++kk) {
-      const float w = Ws[o_loc][kk];
-      const float aw = fabsf(w);
-      c_a += w * Cs[bq][kk];
-      r_a += aw * Rs[bq][kk];
-      c_b += w * Cs[bq + 8][kk];
-      r_b += aw * Rs[bq + 8][kk];
-    }
-    __syncthreads();
   }
-  if (o < ld_out) {
+#pragma unroll
+  for (int b = 0; b < IBP_TB; ++b) {
+    ac[b] = wave_sum(ac[b]);   // every lane takes part
+    ar[b] = wave_sum(ar[b]);
+  }
+  if (lane == 0) {
     const bool real = o < n_out;
     const float bo = real ? bias[o] : 0.f;
-    const int ba = b0 + bq, bb = b0 + bq + 8;
-    if (ba < B) {
-      cout[(int64_t)ba * ld_out + o] = real ? c_a + bo : 0.f;
-      rout[(int64_t)ba * ld_out + o] = real ? r_a : 0.f;
-    }
-    if (bb < B) {
-      cout[(int64_t)bb * ld_out + o] = real ? c_b + bo : 0.f;
-      rout[(int64_t)bb * ld_out + o] = real ? r_b : 0.f;
+#pragma unroll
+    for (int b = 0; b < IBP_TB; ++b) {
+      if (b < nb) {
+        cout[(int64_t)(b0 + b) * ld_out + o] = real ? ac[b] + bo : 0.f;
+        rout[(int64_t)(b0 + b) * ld_out + o] = real ? ar[b] : 0.f;
+      }
     }
   }
 }
@@ -194,7 +177,7 @@ hipError_t launch_ibp_dense(const float *Wp, int64_t ldw, const float *b, int32_
                             const float *cin, const float *rin, int64_t ld_in, int32_t relu_in,
                             float *cout, float *rout, int64_t ld_out, int32_t B, hipStream_t s) {
   (void)n_in;
-  dim3 grid((unsigned)((ld_out + IBP_TO - 1) / IBP_TO), (unsigned)((B + IBP_TB - 1) / IBP_TB));
+  dim3 grid((unsigned)((ld_out + 3) / 4), (unsigned)((B + IBP_TB - 1) / IBP_TB));
   hipLaunchKernelGGL(k_ibp_dense, grid, dim3(256), 0, s, Wp, ldw, b, n_out, (int32_t)ld_in, cin, rin, ld_in,
                      relu_in, cout, rout, ld_out, B);
   return hipGetLastError();
