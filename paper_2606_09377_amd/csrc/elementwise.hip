@@ -117,68 +117,116 @@ hipError_t launch_box(const float *x0, int32_t B, int32_t n0, int64_t ld0, float
 // ------------------------------------------------------------------------------------
 // IBP through a dense layer in centre/radius form: c' = W c + b, r' = |W| r, which is the
 // interval step W+ l + W- u + b, W+ u + W- l + b with l = c - r, u = c + r.  With relu_in
-// the input is first passed through ReLU: [max(l, 0), max(u, 0)].  One wave per output
-// neuron and tile of up to IBP_TB inputs: the lanes stride over K (the weight row is read
-// once, coalesced), then a fixed butterfly, so the summation order does not depend on the
-// batch; every output has its own wave, which keeps small batches parallel too.
-constexpr int IBP_TB = 16;
+// the input is first passed through ReLU: [max(l, 0), max(u, 0)].
+// Both products run on the matrix cores (v_mfma_f32_16x16x4f32, operands straight from global
+// memory).  A workgroup owns a block of 16 inputs x 16 outputs, so even one input spreads over
+// n_out / 16 compute units; its IBP_KS waves split K into contiguous runs of whole 32-wide K
+// tiles (many short runs in flight hide the memory latency), and their partial sums are added
+// in wave order through LDS.  The K split depends on n_in only, so an input's bounds do not
+// depend on the batch it is in.  Per K tile lane l supplies the 8 consecutive k at 8 (l / 16);
+// the loads of the next two tiles are in flight while a tile is multiplied.
+typedef float ibp_f32x4 __attribute__((ext_vector_type(4)));
+constexpr int IBP_KS = 16;
 
-__global__ __launch_bounds__(256) void k_ibp_dense(const float *Wp, int64_t ldw, const float *bias,
-                                                   int32_t n_out, int32_t n_in, const float *cin,
-                                                   const float *rin, int64_t ld_in, int32_t relu_in,
-                                                   float *cout, float *rout, int64_t ld_out, int32_t B) {
-  const int lane = threadIdx.x & 63;
-  const int64_t o = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int b0 = blockIdx.y * IBP_TB;
-  if (o >= ld_out) return;   // wave-uniform
-  const int nb = min(IBP_TB, B - b0);
-  float ac[IBP_TB], ar[IBP_TB];
+__global__ __launch_bounds__(64 * IBP_KS) void k_ibp_dense(const float *Wp, int64_t ldw, const float *bias,
+                                                           int32_t n_out, int32_t n_in, const float *cin,
+                                                           const float *rin, int64_t ld_in, int32_t relu_in,
+                                                           float *cout, float *rout, int64_t ld_out, int32_t B) {
+  __shared__ float red[IBP_KS][2][4][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, kg = lane >> 4;
+  const int o0 = blockIdx.x * 16, b0 = blockIdx.y * 16;
+  const int n_kt = (n_in + 31) / 32;
+  const int per = (n_kt + IBP_KS - 1) / IBP_KS;
+  const int t0 = wave * per, t1 = min(n_kt, t0 + per);
+  const bool bval = b0 + r16 < B;
+  const float *crow = cin + (int64_t)(bval ? b0 + r16 : 0) * ld_in;
+  const float *rrow = rin + (int64_t)(bval ? b0 + r16 : 0) * ld_in;
+  // columns past n_out compute on the last real row and are stored as zeros (Wp may hold only
+  // n_out rows)
+  const float *wrow = Wp + (int64_t)min(o0 + r16, n_out - 1) * ldw;
+  ibp_f32x4 accc = {0.f, 0.f, 0.f, 0.f}, accr = {0.f, 0.f, 0.f, 0.f};
+  // two K tiles in flight: slot 0 holds the even tiles of the run, slot 1 the odd ones
+  float4 nc[2][2], nr[2][2], nw[2][2];
+  auto load = [&](int t, float4 (&bc)[2], float4 (&br)[2], float4 (&bw)[2]) {
+    const int kb = t * 32 + kg * 8;
 #pragma unroll
-  for (int b = 0; b < IBP_TB; ++b) ac[b] = ar[b] = 0.f;
-  if (o < n_out) {
-    const float *wrow = Wp + o * ldw;
+    for (int j = 0; j < 2; ++j) {
+      bw[j] = *reinterpret_cast<const float4 *>(wrow + kb + 4 * j);
+      bc[j] = bval ? *reinterpret_cast<const float4 *>(crow + kb + 4 * j) : make_float4(0.f, 0.f, 0.f, 0.f);
+      br[j] = bval ? *reinterpret_cast<const float4 *>(rrow + kb + 4 * j) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  };
+  auto step = [&](int t, float4 (&bc)[2], float4 (&br)[2], float4 (&bw)[2]) {
+    const int kb = t * 32 + kg * 8;
+    float c[8], r[8], w[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const bool in = kb + j < n_in;   // past n_in: zero, whatever the padding holds
+      const float4 c4 = bc[j / 4], r4 = br[j / 4], w4 = bw[j / 4];
+      const float cs = (j & 3) == 0 ? c4.x : (j & 3) == 1 ? c4.y : (j & 3) == 2 ? c4.z : c4.w;
+      const float rs = (j & 3) == 0 ? r4.x : (j & 3) == 1 ? r4.y : (j & 3) == 2 ? r4.z : r4.w;
+      const float ws = (j & 3) == 0 ? w4.x : (j & 3) == 1 ? w4.y : (j & 3) == 2 ? w4.z : w4.w;
+      float cj = in ? cs : 0.f, rj = in ? rs : 0.f;
+      if (relu_in) {
+        const float lo = fmaxf(cj - rj, 0.f), hi = fmaxf(cj + rj, 0.f);
+        cj = (lo + hi) * 0.5f;
+        rj = (hi - lo) * 0.5f;
+      }
+      c[j] = cj;
+      r[j] = rj;
+      w[j] = in ? ws : 0.f;
+    }
+    if (t + 2 < t1) load(t + 2, bc, br, bw);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      accc = __builtin_amdgcn_mfma_f32_16x16x4f32(c[j], w[j], accc, 0, 0, 0);
+      accr = __builtin_amdgcn_mfma_f32_16x16x4f32(r[j], fabsf(w[j]), accr, 0, 0, 0);
+    }
+  };
+  if (t0 < t1) load(t0, nc[0], nr[0], nw[0]);
+  if (t0 + 1 < t1) load(t0 + 1, nc[1], nr[1], nw[1]);
+  for (int t = t0; t < t1; t += 2) {
+    step(t, nc[0], nr[0], nw[0]);
+    if (t + 1 < t1) step(t + 1, nc[1], nr[1], nw[1]);
+  }
+  if (wave > 0) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      red[wave][0][v][lane] = accc[v];
+      red[wave][1][v][lane] = accr[v];
+    }
+  }
+  __syncthreads();
+  if (wave != 0) return;
 #pragma unroll 1
-    for (int64_t k = lane; k < n_in; k += 64) {
-      const float w = wrow[k], aw = fabsf(w);
+  for (int w = 1; w < IBP_KS; ++w)
 #pragma unroll
-      for (int b = 0; b < IBP_TB; ++b) {
-        if (b < nb) {
-          float c = cin[(int64_t)(b0 + b) * ld_in + k], r = rin[(int64_t)(b0 + b) * ld_in + k];
-          if (relu_in) {
-            const float lo = fmaxf(c - r, 0.f), hi = fmaxf(c + r, 0.f);
-            c = (lo + hi) * 0.5f;
-            r = (hi - lo) * 0.5f;
-          }
-          ac[b] += w * c;
-          ar[b] += aw * r;
-        }
-      }
+    for (int v = 0; v < 4; ++v) {
+      accc[v] += red[w][0][v][lane];
+      accr[v] += red[w][1][v][lane];
     }
-  }
+  // entry v of a lane: input b0 + 4 (lane / 16) + v, output o0 + lane % 16
+  const int o = o0 + r16;
+  const bool real = o < n_out;
+  const float bo = real ? bias[o] : 0.f;
 #pragma unroll
-  for (int b = 0; b < IBP_TB; ++b) {
-    ac[b] = wave_sum(ac[b]);   // every lane takes part
-    ar[b] = wave_sum(ar[b]);
-  }
-  if (lane == 0) {
-    const bool real = o < n_out;
-    const float bo = real ? bias[o] : 0.f;
-#pragma unroll
-    for (int b = 0; b < IBP_TB; ++b) {
-      if (b < nb) {
-        cout[(int64_t)(b0 + b) * ld_out + o] = real ? ac[b] + bo : 0.f;
-        rout[(int64_t)(b0 + b) * ld_out + o] = real ? ar[b] : 0.f;
-      }
-    }
+  for (int v = 0; v < 4; ++v) {
+    const int b = b0 + 4 * kg + v;
+    if (b >= B) continue;
+    cout[(int64_t)b * ld_out + o] = real ? accc[v] + bo : 0.f;
+    rout[(int64_t)b * ld_out + o] = real ? accr[v] : 0.f;
   }
 }
 
 hipError_t launch_ibp_dense(const float *Wp, int64_t ldw, const float *b, int32_t n_out, int32_t n_in,
                             const float *cin, const float *rin, int64_t ld_in, int32_t relu_in,
                             float *cout, float *rout, int64_t ld_out, int32_t B, hipStream_t s) {
-  (void)n_in;
-  dim3 grid((unsigned)((ld_out + 3) / 4), (unsigned)((B + IBP_TB - 1) / IBP_TB));
-  hipLaunchKernelGGL(k_ibp_dense, grid, dim3(256), 0, s, Wp, ldw, b, n_out, (int32_t)ld_in, cin, rin, ld_in,
+  // whole K tiles are read from every row: both pitches must cover them
+  const int64_t k_pad = (int64_t)(n_in + 31) / 32 * 32;
+  if (ld_out % 16 || ldw < k_pad || ld_in < k_pad || ldw % 4 || ld_in % 4) return hipErrorInvalidValue;
+  dim3 grid((unsigned)(ld_out / 16), (unsigned)((B + 15) / 16));
+  hipLaunchKernelGGL(k_ibp_dense, grid, dim3(64 * IBP_KS), 0, s, Wp, ldw, b, n_out, n_in, cin, rin, ld_in,
                      relu_in, cout, rout, ld_out, B);
   return hipGetLastError();
 }
@@ -217,8 +265,8 @@ hipError_t launch_layer_from_ibp(const float *c, const float *r, int64_t ld, int
 // First rows of a backward pass.  Row (unit u, direction d, i) starts as
 // (d ? -1 : 1) * src[i, :] (a weight row W_k[i] or a spec row (C W_L)[i]) with constant
 // (d ? -1 : 1) * src_bias[i]; the ReLU just below is relaxed with the lower rule and its
-// constants (relaxation intercepts and the bias of the dense layer below) are added.  One
-// wavefront per row; padding rows are zero.
+// constants (relaxation intercepts and the bias of the dense layer below) are added.
+// Padding rows are zero.
 __device__ __forceinline__ float4 init_override(const SplitTable &st, int d, int relu, int col, float4 prm,
                                                 int *ent, float *sterm) {
   const int e0 = st.off[d * (st.R + 1) + relu];
@@ -236,60 +284,127 @@ __device__ __forceinline__ float4 init_override(const SplitTable &st, int d, int
   return prm;
 }
 
-__global__ __launch_bounds__(256) void k_init_rows(const InitArgs a, int32_t M_pad) {
-  const int lane = threadIdx.x & 63;
-  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= M_pad) return;
-  float *orow = a.out + row * a.ldo;
-  if (row >= a.M) {
-    for (int64_t c = (int64_t)lane * 4; c < a.ldo; c += 256) {
-      *reinterpret_cast<float4 *>(orow + c) = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (a.pre) *reinterpret_cast<float4 *>(a.pre + row * a.ldo + c) = make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-    if (lane == 0) a.beta[row] = 0.f;
-    return;
-  }
-  const int rpu = 2 * a.n_src;
-  const int u = (int)(row / rpu);
-  const int r2 = (int)(row - (int64_t)u * rpu);
-  const int dir = r2 >= a.n_src;
-  const int i = r2 - dir * a.n_src;
-  const float sgn = dir ? -1.f : 1.f;
-  const int64_t srow = a.per_unit_src ? (int64_t)u * a.n_src + i : i;
-  const float *src = a.src + srow * a.ld_src;
-  const float4 *P = a.P + (a.param_per_unit ? (int64_t)u * a.ldp : 0);
-  const bool has_splits = a.splits.D > 0;
-  float acc = 0.f;
-  for (int64_t c = (int64_t)lane * 4; c < a.ldo; c += 256) {
-    const float4 w = *reinterpret_cast<const float4 *>(src + c);
-    const float wv[4] = {w.x, w.y, w.z, w.w};
-    float ov[4];
+// The kernel only writes: each wavefront owns IR consecutive rows and walks the columns in
+// blocks of 256 NCH.  A lane keeps the relaxation parameters of its 4 NCH columns of the block
+// in registers while it writes those columns of all its rows (reloading them only where the
+// unit changes), so the parameters are read once per row group instead of once per row.  Each
+// lane adds its columns in ascending order (carrying its running sum across column blocks in
+// LDS), whatever IR and NCH are, so the row constants have the same bits for every launch shape.
+// PLAIN: no split table, no per-row slopes and no copy of the unrelaxed rows (fewer registers).
+template <int NCH, int IR, bool PLAIN>
+__global__ __launch_bounds__(256) void k_init_rows(const InitArgs a) {
+  __shared__ float carry[4][IR][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int32_t row0 = ((int32_t)blockIdx.x * 4 + wave) * IR;
+  const int32_t rpu = 2 * a.n_src;
+  const bool has_splits = !PLAIN && a.splits.D > 0;
+  const float *alpha = PLAIN ? nullptr : a.alpha;
+  float *pre = PLAIN ? nullptr : a.pre;
+  for (int64_t cb = 0; cb < a.ldo; cb += 256 * NCH) {
+    const bool first = cb == 0, last = cb + 256 * NCH >= a.ldo;
+    float4 prm[NCH][4];
+    int32_t held = -1;
+#pragma unroll 1
+    for (int r = 0; r < IR; ++r) {
+      const int32_t row = row0 + r;
+      float *orow = a.out + (int64_t)row * a.ldo + cb + lane * 4;
+      float *prow = pre ? pre + (int64_t)row * a.ldo + cb + lane * 4 : nullptr;
+      if (row >= a.M) {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      float4 prm = P[c + e];
-      int ent = -1;
-      float sterm = 0.f;
-      if (has_splits) prm = init_override(a.splits, u, a.relu_index, (int)(c + e), prm, &ent, &sterm);
-      const float x = sgn * wv[e];
-      float lam = prm.x;
-      if (a.alpha && prm.z > 0.f) lam = a.alpha[row * a.ld_alpha + c + e];
-      float ap = x > 0.f ? x * lam : x * prm.y;
-      if (ent >= 0 && a.splits.beta) ap += a.splits.beta[row * a.splits.S + ent] * sterm;
-      acc += fminf(x, 0.f) * prm.z + ap * prm.w;
-      ov[e] = ap;
+        for (int j = 0; j < NCH; ++j) {
+          if (cb + j * 256 + lane * 4 >= a.ldo) continue;
+          *reinterpret_cast<float4 *>(orow + j * 256) = make_float4(0.f, 0.f, 0.f, 0.f);
+          if (prow) *reinterpret_cast<float4 *>(prow + j * 256) = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+        if (last && lane == 0) a.beta[row] = 0.f;
+        continue;
+      }
+      const int32_t u = row / rpu;
+      const int32_t r2 = row - u * rpu;
+      const int dir = r2 >= a.n_src;
+      const int32_t i = r2 - dir * a.n_src;
+      const float sgn = dir ? -1.f : 1.f;
+      const int64_t srow = a.per_unit_src ? (int64_t)u * a.n_src + i : i;
+      const int32_t pu = a.param_per_unit ? u : 0;
+      if (pu != held) {
+        const float4 *P = a.P + (int64_t)pu * a.ldp + cb + lane * 4;
+#pragma unroll
+        for (int j = 0; j < NCH; ++j)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            prm[j][e] = cb + j * 256 + lane * 4 < a.ldo ? P[j * 256 + e] : make_float4(0.f, 0.f, 0.f, 0.f);
+        held = pu;
+      }
+      const float *src = a.src + srow * a.ld_src + cb + lane * 4;
+      float4 w[NCH];
+#pragma unroll
+      for (int j = 0; j < NCH; ++j)
+        w[j] = cb + j * 256 + lane * 4 < a.ldo ? *reinterpret_cast<const float4 *>(src + j * 256)
+                                              : make_float4(0.f, 0.f, 0.f, 0.f);
+      float acc = first ? 0.f : carry[wave][r][lane];
+#pragma unroll
+      for (int j = 0; j < NCH; ++j) {
+        const int64_t c = cb + j * 256 + lane * 4;
+        if (c >= a.ldo) continue;
+        const float wv[4] = {w[j].x, w[j].y, w[j].z, w[j].w};
+        float ov[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          float4 q = prm[j][e];
+          int ent = -1;
+          float sterm = 0.f;
+          if (has_splits) q = init_override(a.splits, u, a.relu_index, (int)(c + e), q, &ent, &sterm);
+          const float x = sgn * wv[e];
+          float lam = q.x;
+          if (alpha && q.z > 0.f) lam = alpha[(int64_t)row * a.ld_alpha + c + e];
+          float ap = x > 0.f ? x * lam : x * q.y;
+          if (ent >= 0 && a.splits.beta) ap += a.splits.beta[(int64_t)row * a.splits.S + ent] * sterm;
+          acc += fminf(x, 0.f) * q.z + ap * q.w;
+          ov[e] = ap;
+        }
+        *reinterpret_cast<float4 *>(orow + j * 256) = make_float4(ov[0], ov[1], ov[2], ov[3]);
+        if (prow)
+          *reinterpret_cast<float4 *>(prow + j * 256) =
+              make_float4(sgn * wv[0], sgn * wv[1], sgn * wv[2], sgn * wv[3]);
+      }
+      if (!last) {
+        carry[wave][r][lane] = acc;  // each lane only ever touches its own slot
+        continue;
+      }
+      acc = wave_sum(acc);
+      if (lane == 0) a.beta[row] = sgn * a.src_bias[srow] + acc;
     }
-    *reinterpret_cast<float4 *>(orow + c) = make_float4(ov[0], ov[1], ov[2], ov[3]);
-    if (a.pre)
-      *reinterpret_cast<float4 *>(a.pre + row * a.ldo + c) = make_float4(sgn * wv[0], sgn * wv[1], sgn * wv[2], sgn * wv[3]);
   }
-  acc = wave_sum(acc);
-  if (lane == 0) a.beta[row] = sgn * a.src_bias[srow] + acc;
+}
+
+template <int NCH, int IR>
+static void launch_init_rows_t(const InitArgs &a, int32_t M_pad, hipStream_t s) {
+  const dim3 grid((unsigned)(M_pad / (4 * IR)));
+  if (a.splits.D == 0 && !a.alpha && !a.pre)
+    hipLaunchKernelGGL((k_init_rows<NCH, IR, true>), grid, dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL((k_init_rows<NCH, IR, false>), grid, dim3(256), 0, s, a);
+}
+
+template <int NCH>
+static void launch_init_rows_n(const InitArgs &a, int32_t M_pad, hipStream_t s) {
+  if (M_pad >= 32768)
+    launch_init_rows_t<NCH, 16>(a, M_pad, s);
+  else if (M_pad >= 4096)
+    launch_init_rows_t<NCH, 4>(a, M_pad, s);
+  else
+    launch_init_rows_t<NCH, 1>(a, M_pad, s);
 }
 
 hipError_t launch_init_rows(const InitArgs &a, hipStream_t s) {
   if (a.ldo % 4) return hipErrorInvalidValue;
-  const int32_t M_pad = (int32_t)rows_pad(a.M);
-  hipLaunchKernelGGL(k_init_rows, dim3((unsigned)((M_pad + 3) / 4)), dim3(256), 0, s, a, M_pad);
+  const int32_t M_pad = (int32_t)rows_pad(a.M);  // a multiple of 128: every row group is whole
+  if (a.ldo <= 256)
+    launch_init_rows_n<1>(a, M_pad, s);
+  else if (a.ldo <= 512)
+    launch_init_rows_n<2>(a, M_pad, s);
+  else
+    launch_init_rows_n<4>(a, M_pad, s);
   return hipGetLastError();
 }
 

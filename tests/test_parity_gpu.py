@@ -92,6 +92,23 @@ def test_ibp_bounds():
             assert_close(ub[b], iu, "ibp ub")
 
 
+def test_ibp_bounds_several_tiles():
+    """IBP where the batch spans several input tiles (ragged last tile), the outputs several
+    64-wide groups, and K splits unevenly over the workgroup's waves; checked against the
+    oracle and for batch invariance (bit for bit against the inputs alone)."""
+    wl = random_mlp(108, [300, 200, 130, 7], 19, 0.05)
+    ctx = gpu_ctx(wl.net)
+    lb, ub = ctx.ibp_bounds(to_dev(wl.x0), wl.eps, to_dev(wl.C))
+    lb, ub = lb.cpu().numpy(), ub.cpu().numpy()
+    for b in range(19):
+        il, iu = oracle.ibp_spec_bounds(wl.net, wl.x0[b], wl.eps, wl.C[b])
+        assert_close(lb[b], il, "ibp lb")
+        assert_close(ub[b], iu, "ibp ub")
+    for b in (0, 17):
+        l1, u1 = ctx.ibp_bounds(to_dev(wl.x0[b:b + 1]), wl.eps, to_dev(wl.C[b:b + 1]))
+        assert np.array_equal(l1.cpu().numpy()[0], lb[b]) and np.array_equal(u1.cpu().numpy()[0], ub[b])
+
+
 def test_eps_zero_is_a_point():
     wl = random_mlp(107, [50, 130, 140, 6], 3, 0.0)
     ctx = gpu_ctx(wl.net)
