@@ -86,6 +86,8 @@ hipError_t launch_transpose_pad(const float *W, int32_t rows, int32_t cols, floa
                                 int64_t rows_t, hipStream_t s);
 hipError_t launch_box(const float *x0, int32_t B, int32_t n0, int64_t ld0, float eps, int32_t clip_on,
                       float clip_lo, float clip_hi, float *c0, float *r0, hipStream_t s);
+// Wp: the weights, n_out rows of pitch ldw (>= n_in rounded up to 32, zero padded); cin, rin:
+// [B][ld_in]; cout, rout: [B][ld_out], ld_out a multiple of 16
 hipError_t launch_ibp_dense(const float *Wp, int64_t ldw, const float *b, int32_t n_out, int32_t n_in,
                             const float *cin, const float *rin, int64_t ld_in, int32_t relu_in,
                             float *cout, float *rout, int64_t ld_out, int32_t B, hipStream_t s);
