@@ -87,43 +87,64 @@ hipError_t launch_alpha_best(const float *beta, const float *cpart, int32_t n_pa
   return hipGetLastError();
 }
 
-__global__ void k_alpha_keep(AlphaLayer l, const int32_t *flag, int32_t rows) {
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (int64_t)rows * l.ld) return;
-  const int64_t row = idx / l.ld;
-  if (flag[row]) l.best[idx] = l.alpha[idx];
+// The slope-state kernels run one thread per 4 consecutive columns of a row (ld is a multiple
+// of 128), workgroups of 256 threads covering 1024 columns of one row.
+constexpr int ALPHA_COLS_PER_BLOCK = 1024;
+
+// best <- alpha on the rows whose bound improved (flag)
+__global__ void k_alpha_keep(AlphaLayer l, const int32_t *flag, int32_t blocks_per_row) {
+  const int32_t row = blockIdx.x / blocks_per_row;
+  const int64_t n0 = (int64_t)(blockIdx.x - row * blocks_per_row) * ALPHA_COLS_PER_BLOCK + threadIdx.x * 4;
+  if (n0 >= l.ld || !flag[row]) return;
+  const int64_t idx = (int64_t)row * l.ld + n0;
+  *reinterpret_cast<float4 *>(l.best + idx) = *reinterpret_cast<const float4 *>(l.alpha + idx);
 }
 
 hipError_t launch_alpha_keep(const AlphaLayer &l, const int32_t *flag, int32_t rows, hipStream_t s) {
-  const int64_t n = (int64_t)rows * l.ld;
-  hipLaunchKernelGGL(k_alpha_keep, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, l, flag, rows);
+  if (l.ld % 4) return hipErrorInvalidValue;
+  const int32_t bpr = (int32_t)((l.ld + ALPHA_COLS_PER_BLOCK - 1) / ALPHA_COLS_PER_BLOCK);
+  hipLaunchKernelGGL(k_alpha_keep, dim3((unsigned)((int64_t)rows * bpr)), dim3(256), 0, s, l, flag, bpr);
   return hipGetLastError();
 }
 
-// Adam (bias-corrected moments) then projection onto [0, 1], at unstable neurons only
-__global__ void k_alpha_adam(AlphaLayer l, int32_t rows, int32_t rows_per_unit, float lr, float beta1, float beta2,
-                             float eps, float c1, float c2) {
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (int64_t)rows * l.ld) return;
-  const int64_t row = idx / l.ld;
-  const int64_t n = idx - row * l.ld;
-  if (n >= l.n) return;
-  const int64_t u = row / rows_per_unit;
-  if (!(l.P[u * l.ld + n].z > 0.f)) return;
-  const float g = l.grad[idx];
-  const float mo = beta1 * l.mom[idx] + (1.f - beta1) * g;
-  const float ve = beta2 * l.vel[idx] + (1.f - beta2) * g * g;
-  l.mom[idx] = mo;
-  l.vel[idx] = ve;
-  const float a = l.alpha[idx] + lr * (mo * c1) / (sqrtf(ve * c2) + eps);
-  l.alpha[idx] = fminf(fmaxf(a, 0.f), 1.f);
+// Adam (bias-corrected moments) then projection onto [0, 1], at unstable neurons only.  With
+// flag, the rows whose bound improved first keep their current slopes in best (the keep step
+// folded into the same pass over the state).
+__global__ void k_alpha_adam(AlphaLayer l, const int32_t *flag, int32_t blocks_per_row, int32_t rows_per_unit,
+                             float lr, float beta1, float beta2, float eps, float c1, float c2) {
+  const int32_t row = blockIdx.x / blocks_per_row;
+  const int64_t n0 = (int64_t)(blockIdx.x - row * blocks_per_row) * ALPHA_COLS_PER_BLOCK + threadIdx.x * 4;
+  if (n0 >= l.ld) return;
+  const int64_t idx = (int64_t)row * l.ld + n0;
+  float4 a4 = *reinterpret_cast<const float4 *>(l.alpha + idx);
+  if (flag && flag[row]) *reinterpret_cast<float4 *>(l.best + idx) = a4;
+  if (n0 >= l.n) return;
+  const int32_t u = row / rows_per_unit;
+  const float4 *P = l.P + (int64_t)u * l.ld + n0;
+  const float4 g4 = *reinterpret_cast<const float4 *>(l.grad + idx);
+  float4 m4 = *reinterpret_cast<const float4 *>(l.mom + idx);
+  float4 v4 = *reinterpret_cast<const float4 *>(l.vel + idx);
+  float a[4] = {a4.x, a4.y, a4.z, a4.w}, g[4] = {g4.x, g4.y, g4.z, g4.w};
+  float mo[4] = {m4.x, m4.y, m4.z, m4.w}, ve[4] = {v4.x, v4.y, v4.z, v4.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    if (n0 + e >= l.n || !(P[e].z > 0.f)) continue;   // padding or a stable neuron: unchanged
+    mo[e] = beta1 * mo[e] + (1.f - beta1) * g[e];
+    ve[e] = beta2 * ve[e] + (1.f - beta2) * g[e] * g[e];
+    const float t = a[e] + lr * (mo[e] * c1) / (sqrtf(ve[e] * c2) + eps);
+    a[e] = fminf(fmaxf(t, 0.f), 1.f);
+  }
+  *reinterpret_cast<float4 *>(l.mom + idx) = make_float4(mo[0], mo[1], mo[2], mo[3]);
+  *reinterpret_cast<float4 *>(l.vel + idx) = make_float4(ve[0], ve[1], ve[2], ve[3]);
+  *reinterpret_cast<float4 *>(l.alpha + idx) = make_float4(a[0], a[1], a[2], a[3]);
 }
 
-hipError_t launch_alpha_adam(const AlphaLayer &l, int32_t rows, int32_t rows_per_unit, float lr, float beta1,
-                             float beta2, float eps, float c1, float c2, hipStream_t s) {
-  const int64_t n = (int64_t)rows * l.ld;
-  hipLaunchKernelGGL(k_alpha_adam, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, l, rows, rows_per_unit, lr,
-                     beta1, beta2, eps, c1, c2);
+hipError_t launch_alpha_adam(const AlphaLayer &l, const int32_t *flag, int32_t rows, int32_t rows_per_unit, float lr,
+                             float beta1, float beta2, float eps, float c1, float c2, hipStream_t s) {
+  if (l.ld % 4) return hipErrorInvalidValue;
+  const int32_t bpr = (int32_t)((l.ld + ALPHA_COLS_PER_BLOCK - 1) / ALPHA_COLS_PER_BLOCK);
+  hipLaunchKernelGGL(k_alpha_adam, dim3((unsigned)((int64_t)rows * bpr)), dim3(256), 0, s, l, flag, bpr,
+                     rows_per_unit, lr, beta1, beta2, eps, c1, c2);
   return hipGetLastError();
 }
 

@@ -752,8 +752,11 @@ vcr_status alpha_spec(vcr_ctx *c, CallBufs &bf, const Plan &p, const AlphaCall &
       HIP_TRY(c, launch_alpha_best(bf.beta, bf.cpart, (int32_t)(ld0 / PART_COLS), M_pad, M, m, t == 0, bf.best_val,
                                    bf.flag, o.lb_hist ? o.lb_hist + ((int64_t)t * units + u0) * m : nullptr,
                                    o.ub_hist ? o.ub_hist + ((int64_t)t * units + u0) * m : nullptr, s));
-      for (int r = 0; r < R; ++r) HIP_TRY(c, launch_alpha_keep(al[r], bf.flag, M, s));
       const bool step = t < o.iters;
+      // rows that improved keep their slopes: here after the last evaluation, otherwise inside
+      // the Adam step below (the gradient pass leaves the slopes unchanged)
+      if (!step)
+        for (int r = 0; r < R; ++r) HIP_TRY(c, launch_alpha_keep(al[r], bf.flag, M, s));
       if (!step && !o.grad_out) break;
       // gradient: E_0 = the row's box vertex, then E_k = line_k(W_k E_{k-1} + b_k)
       HIP_TRY(c, launch_alpha_vertex(bf.pre0, ld0, bf.c0 + pu0 * ld0, bf.r0 + pu0 * ld0, M_pad, prpu, pun, bf.A[0], s));
@@ -793,7 +796,8 @@ vcr_status alpha_spec(vcr_ctx *c, CallBufs &bf, const Plan &p, const AlphaCall &
       const double c1 = 1.0 / (1.0 - std::pow((double)o.beta1, (double)(t + 1)));
       const double c2 = 1.0 / (1.0 - std::pow((double)o.beta2, (double)(t + 1)));
       for (int r = 0; r < R; ++r)
-        HIP_TRY(c, launch_alpha_adam(al[r], M, prpu, o.lr, o.beta1, o.beta2, o.adam_eps, (float)c1, (float)c2, s));
+        HIP_TRY(c, launch_alpha_adam(al[r], bf.flag, M, prpu, o.lr, o.beta1, o.beta2, o.adam_eps, (float)c1,
+                                     (float)c2, s));
       if (dom && S > 0)
         HIP_TRY(c, launch_beta_adam(bs, M, ac.lr_beta, o.beta1, o.beta2, o.adam_eps, (float)c1, (float)c2, s));
     }

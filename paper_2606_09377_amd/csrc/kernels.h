@@ -170,9 +170,10 @@ hipError_t launch_alpha_best(const float *beta, const float *cpart, int32_t n_pa
                              float *hist_ub, hipStream_t s);
 // best <- alpha where the row improved
 hipError_t launch_alpha_keep(const AlphaLayer &l, const int32_t *flag, int32_t rows, hipStream_t s);
-// one projected Adam step (ascent) at unstable neurons; c1 = 1 / (1 - beta1^t), c2 = 1 / (1 - beta2^t)
-hipError_t launch_alpha_adam(const AlphaLayer &l, int32_t rows, int32_t rows_per_unit, float lr, float beta1,
-                             float beta2, float eps, float c1, float c2, hipStream_t s);
+// one projected Adam step (ascent) at unstable neurons; c1 = 1 / (1 - beta1^t), c2 = 1 / (1 - beta2^t);
+// with flag, first the keep step above on the same rows
+hipError_t launch_alpha_adam(const AlphaLayer &l, const int32_t *flag, int32_t rows, int32_t rows_per_unit, float lr,
+                             float beta1, float beta2, float eps, float c1, float c2, hipStream_t s);
 // lb / ub from the best row values; with unit_flags (subdomains): 1 infeasible -> lb = +inf,
 // ub = -inf; 2 invalid splits -> NaN
 hipError_t launch_alpha_final(const float *best_val, int32_t units, int32_t m, const int32_t *unit_flags, float *lb,
