@@ -525,13 +525,18 @@ __global__ __launch_bounds__(128) void k_gemm_small(const GemmArgs p) {
   gemm_epilogue<FWD, AL, AFF, 1, 1>(p, acc, m0, 0, n0, lane, SM_BM, bj, xpart, n0, SM_BN, sflag);
 }
 
-// Mid-size launches (too few 128 x 128 tiles, enough 64 x 64 ones): 64 x 64 tiles staged
+// Mid-size launches (fewer than MID_MAX_GRID 128 x 128 tiles, at least MID_GRID 64 x 64 ones):
+// 64 x 64 tiles staged
 // through double-buffered LDS like k_gemm, four waves of 32 x 32.  Each accumulator sees
 // k_gemm's MFMA sequence and the two column waves of a row block add their row sums in
 // k_gemm's order (through LDS), so the bits are k_gemm's; the operands cross the L2 half as
 // often as in the small-tile kernel.
 constexpr int MD_BM = 64, MD_BN = 64;
 constexpr int64_t MID_GRID = 256;   // 64 x 64 tiles from which the mid-size kernel runs
+// 128 x 128 tiles up to which it runs instead of k_gemm: between one and three rounds of the
+// 512 k_gemm workgroups that fit the chip, the last round of k_gemm leaves most compute units
+// idle (576 tiles: a round of 64), while four times as many 64 x 64 tiles fill it evenly
+constexpr int64_t MID_MAX_GRID = 1536;
 
 template <bool FWD, bool AL, bool AFF = false>
 __global__ __launch_bounds__(256) void k_gemm_mid(const GemmArgs p) {
@@ -598,8 +603,11 @@ __global__ __launch_bounds__(256) void k_gemm_mid(const GemmArgs p) {
 }
 
 int gemm_kind(const GemmArgs &a) {
-  if (a.M_pad <= 0 || a.N_pad <= 0 || (int64_t)(a.M_pad / BM) * (a.N_pad / BN) >= SMALL_GRID) return 0;
-  return (int64_t)(a.M_pad / MD_BM) * (a.N_pad / MD_BN) >= MID_GRID ? 3 : 2;
+  if (a.M_pad <= 0 || a.N_pad <= 0) return 0;
+  const int64_t grid = (int64_t)(a.M_pad / BM) * (a.N_pad / BN);
+  const int64_t mid = (int64_t)(a.M_pad / MD_BM) * (a.N_pad / MD_BN);
+  if (grid < MID_MAX_GRID && mid >= MID_GRID) return 3;
+  return grid < SMALL_GRID ? 2 : 0;
 }
 
 hipError_t launch_gemm(const GemmArgs &a, hipStream_t s) {
@@ -619,7 +627,7 @@ hipError_t launch_gemm(const GemmArgs &a, hipStream_t s) {
   if (a.mode != EPI_RELAX && a.mode != EPI_CONCRETIZE && a.mode != EPI_FORWARD && a.mode != EPI_AFFINE)
     return hipErrorInvalidValue;
   const int64_t mid = (int64_t)(a.M_pad / MD_BM) * (a.N_pad / MD_BN);
-  if (grid < SMALL_GRID && mid >= MID_GRID) {   // gemm_kind 3
+  if (grid < MID_MAX_GRID && mid >= MID_GRID) {   // gemm_kind 3
     // too few 128 x 128 tiles to fill the chip, enough of 64 x 64 (same bits)
     const dim3 g((unsigned)mid), t(256);
     if (a.mode == EPI_AFFINE)
