@@ -291,6 +291,7 @@ __device__ __forceinline__ float4 init_override(const SplitTable &st, int d, int
 // lane adds its columns in ascending order (carrying its running sum across column blocks in
 // LDS), whatever IR and NCH are, so the row constants have the same bits for every launch shape.
 // PLAIN: no split table, no per-row slopes and no copy of the unrelaxed rows (fewer registers).
+constexpr int INIT_ENT = 8;
 template <int NCH, int IR, bool PLAIN>
 __global__ __launch_bounds__(256) void k_init_rows(const InitArgs a) {
   __shared__ float carry[4][IR][64];
@@ -341,22 +342,49 @@ __global__ __launch_bounds__(256) void k_init_rows(const InitArgs a) {
       for (int j = 0; j < NCH; ++j)
         w[j] = cb + j * 256 + lane * 4 < a.ldo ? *reinterpret_cast<const float4 *>(src + j * 256)
                                               : make_float4(0.f, 0.f, 0.f, 0.f);
+      // the row's split entries at this ReLU, read once per row (the unit is wave-uniform);
+      // more than INIT_ENT of them take the general per-element lookup
+      int e0 = 0, ne = 0, ecol[INIT_ENT];
+      if (has_splits) {
+        e0 = a.splits.off[u * (a.splits.R + 1) + a.relu_index];
+        ne = a.splits.off[u * (a.splits.R + 1) + a.relu_index + 1] - e0;
+#pragma unroll
+        for (int k = 0; k < INIT_ENT; ++k) ecol[k] = k < ne ? a.splits.ent_n[u * a.splits.S + e0 + k] : -1;
+      }
       float acc = first ? 0.f : carry[wave][r][lane];
 #pragma unroll
       for (int j = 0; j < NCH; ++j) {
         const int64_t c = cb + j * 256 + lane * 4;
         if (c >= a.ldo) continue;
         const float wv[4] = {w[j].x, w[j].y, w[j].z, w[j].w};
+        float4 al4 = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (alpha) al4 = *reinterpret_cast<const float4 *>(alpha + (int64_t)row * a.ld_alpha + c);
+        const float alv[4] = {al4.x, al4.y, al4.z, al4.w};
         float ov[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           float4 q = prm[j][e];
           int ent = -1;
           float sterm = 0.f;
-          if (has_splits) q = init_override(a.splits, u, a.relu_index, (int)(c + e), q, &ent, &sterm);
+          if (has_splits) {
+            if (ne <= INIT_ENT) {
+#pragma unroll
+              for (int k = 0; k < INIT_ENT; ++k)
+                if (ecol[k] == (int)(c + e)) {   // the last match wins, as in init_override
+                  const float4 o = a.splits.ent_p[u * a.splits.S + e0 + k];
+                  q.x = o.x;
+                  q.y = o.y;
+                  q.z = o.z;
+                  ent = e0 + k;
+                  sterm = o.w;
+                }
+            } else {
+              q = init_override(a.splits, u, a.relu_index, (int)(c + e), q, &ent, &sterm);
+            }
+          }
           const float x = sgn * wv[e];
           float lam = q.x;
-          if (alpha && q.z > 0.f) lam = alpha[(int64_t)row * a.ld_alpha + c + e];
+          if (alpha && q.z > 0.f) lam = alv[e];
           float ap = x > 0.f ? x * lam : x * q.y;
           if (ent >= 0 && a.splits.beta) ap += a.splits.beta[(int64_t)row * a.splits.S + ent] * sterm;
           acc += fminf(x, 0.f) * q.z + ap * q.w;
