@@ -45,11 +45,13 @@ __device__ __forceinline__ uint32_t fdiv(uint32_t n, FastDiv d) {
 // double-buffered LDS.  A K tile never straddles two taps (C_out is a multiple of 32).
 //
 // LDS rows hold BK floats unpadded, as BK / 4 16-byte chunks; chunk c of tile row q sits at
-// chunk c ^ swz(q).  The tile stores (BK / 4 threads per row) and the MFMA operand reads (8
-// consecutive rows at one chunk per 8 lanes) then both touch 8 distinct 4-bank groups.
+// chunk c ^ swz(q).  A 16-byte LDS access serves 16 lanes per cycle over the 64 banks, so the
+// swizzle spreads 16 consecutive rows at one chunk (the MFMA operand reads) over 16 distinct
+// 4-bank groups; the tile stores (BK / 4 threads per row) cover whole rows and are spread
+// already.  (Rows whose offsets coincide modulo the 64 banks get different chunk positions.)
 template <int BK>
 __device__ __forceinline__ int lds_swz(int row) {
-  constexpr int CPR = BK / 4, RPG = 8 / CPR;
+  constexpr int CPR = BK / 4, RPG = 16 / CPR;
   return (row / RPG) & (CPR - 1);
 }
 
