@@ -235,12 +235,22 @@ __global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
   }
   const float *Bg = p.Bt + (int64_t)(n0 + lrow) * p.ldb + lcol;
   f32x4 ra[QA], rb[QB];
-  // K order: channel block outer, tap inner, so the shifted re-reads of one source block
-  // follow each other within a few K tiles (they hit the caches instead of HBM)
+  // K order: pairs of channel blocks outer, tap, then the block of the pair: the shifted
+  // re-reads of one source block follow each other within a few K tiles (they hit the caches
+  // instead of HBM), and the two halves of a 128-byte line (32 channels) are read by
+  // consecutive K tiles (the second from L1)
   const int ntap = cl.nty * cl.ntx;
+  const bool pairs = (p.C_out / BK) % 2 == 0;
   auto gload = [&](int kt) {
-    const int cb = kt / ntap;
-    const int t = kt - cb * ntap;
+    int cb, t;
+    if (pairs) {
+      const int grp = kt / (2 * ntap), rem = kt - grp * 2 * ntap;
+      t = rem >> 1;
+      cb = grp * 2 + (rem & 1);
+    } else {
+      cb = kt / ntap;
+      t = kt - cb * ntap;
+    }
     const int co0 = cb * BK;
     const int ty = t / cl.ntx, tx = t - ty * cl.ntx;
     const int ky = cl.ky0 + cl.kys * ty, kx = cl.kx0 + cl.kxs * tx;
