@@ -292,6 +292,7 @@ __device__ __forceinline__ float4 init_override(const SplitTable &st, int d, int
 // LDS), whatever IR and NCH are, so the row constants have the same bits for every launch shape.
 // PLAIN: no split table, no per-row slopes and no copy of the unrelaxed rows (fewer registers).
 constexpr int INIT_ENT = 8;
+typedef float nt_f32x4 __attribute__((ext_vector_type(4)));
 template <int NCH, int IR, bool PLAIN>
 __global__ __launch_bounds__(256) void k_init_rows(const InitArgs a) {
   __shared__ float carry[4][IR][64];
@@ -390,10 +391,12 @@ __global__ __launch_bounds__(256) void k_init_rows(const InitArgs a) {
           acc += fminf(x, 0.f) * q.z + ap * q.w;
           ov[e] = ap;
         }
-        *reinterpret_cast<float4 *>(orow + j * 256) = make_float4(ov[0], ov[1], ov[2], ov[3]);
+        // streaming stores: the rows are read back only by the next GEMM, long after
+        __builtin_nontemporal_store(nt_f32x4{ov[0], ov[1], ov[2], ov[3]},
+                                    reinterpret_cast<nt_f32x4 *>(orow + j * 256));
         if (prow)
-          *reinterpret_cast<float4 *>(prow + j * 256) =
-              make_float4(sgn * wv[0], sgn * wv[1], sgn * wv[2], sgn * wv[3]);
+          __builtin_nontemporal_store(nt_f32x4{sgn * wv[0], sgn * wv[1], sgn * wv[2], sgn * wv[3]},
+                                      reinterpret_cast<nt_f32x4 *>(prow + j * 256));
       }
       if (!last) {
         carry[wave][r][lane] = acc;  // each lane only ever touches its own slot
