@@ -77,7 +77,7 @@ struct StemArgs {
 hipError_t launch_stem(const StemArgs &a, hipStream_t s);
 
 struct ConvInitArgs {
-  const float *W;          // start convolution [C_src][C_in][3][3]
+  const float *W;          // start convolution, taps outer: [C_src][3][3][C_in]
   const float *b;          // its bias
   int32_t C_src, H_src;    // start node shape (C_src, H_src, H_src)
   int32_t C_in, H_in;      // the convolution's input node

@@ -723,49 +723,57 @@ hipError_t launch_stem(const StemArgs &a, hipStream_t s) {
 // First rows of a pass that starts at a 3x3 convolution's output neurons: row (unit, dir,
 // c0, i, j) is (dir ? -1 : 1) W[c0][ci][u][w] on the convolution's input window around
 // (stride i, stride j), zero outside the image; relaxed (or identity) like the GEMM
-// epilogue; beta = (dir ? -1 : 1) b[c0] + the window's constant terms.  One wave per row.
+// epilogue; beta = (dir ? -1 : 1) b[c0] + the window's constant terms.  Each wave takes
+// INIT_CONV_RPW consecutive rows; the weights come tap-major ([c0][u][w][ci]), so the lanes' channel
+// loads are contiguous.
+constexpr int INIT_CONV_RPW = 4;   // rows per wave
+
 __global__ __launch_bounds__(256) void k_init_conv(const ConvInitArgs a) {
   const int lane = threadIdx.x & 63;
-  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (r >= a.R) return;
-  const int4 an = a.rows[r];
   const int n_src = a.C_src * a.H_src * a.H_src;
-  const int q = (int)(r % (2 * n_src));
-  const int dir = q >= n_src;
-  const int nq = q - dir * n_src;
-  const int c0 = nq / (a.H_src * a.H_src);
-  const float sg = dir ? -1.f : 1.f;
   const int S = a.S;   // kernel window (3)
-  float *orow = a.out + r * (int64_t)S * S * a.C_in;
-  float acc = 0.f;
-  for (int e = lane; e < S * S * a.C_in; e += 64) {
-    const int pos = e / a.C_in, ci = e - pos * a.C_in;
-    const int u = pos / S, w = pos - u * S;
-    const int gy = an.y * a.scale - a.h + u, gx = an.z * a.scale - a.h + w;
-    float ap = 0.f;
-    if (gy >= 0 && gx >= 0 && gy < a.H_in && gx < a.H_in) {
-      const float x = sg * a.W[(((int64_t)c0 * a.C_in + ci) * 3 + u) * 3 + w];
-      float4 prm;
-      if (a.P_pos)
-        prm = a.P_pos[(((int64_t)an.x * a.H_in + gy) * a.H_in + gx) * a.C_in + ci];
-      else
-        prm = make_float4(1.f, 1.f, 0.f, a.bias_next[ci]);
-      ap = x > 0.f ? x * prm.x : x * prm.y;
-      acc += fminf(x, 0.f) * prm.z + ap * prm.w;
-    }
-    orow[e] = ap;
+  for (int k = 0; k < INIT_CONV_RPW; ++k) {
+    const int64_t r = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * INIT_CONV_RPW + k;
+    if (r >= a.R) return;   // wave-uniform
+    const int4 an = a.rows[r];
+    const int q = (int)(r % (2 * n_src));
+    const int dir = q >= n_src;
+    const int nq = q - dir * n_src;
+    const int c0 = nq / (a.H_src * a.H_src);
+    const float sg = dir ? -1.f : 1.f;
+    float *orow = a.out + r * (int64_t)S * S * a.C_in;
+    float acc = 0.f;
+    // window positions outer (their image bounds are wave-uniform), channels across the lanes
+    for (int u = 0; u < S; ++u)
+      for (int w = 0; w < S; ++w) {
+        const int gy = an.y * a.scale - a.h + u, gx = an.z * a.scale - a.h + w;
+        const bool in = gy >= 0 && gx >= 0 && gy < a.H_in && gx < a.H_in;
+        const float4 *P = a.P_pos ? a.P_pos + (((int64_t)an.x * a.H_in + gy) * a.H_in + gx) * a.C_in : nullptr;
+        float *o = orow + (int64_t)(u * S + w) * a.C_in;
+        for (int ci = lane; ci < a.C_in; ci += 64) {
+          float ap = 0.f;
+          if (in) {
+            const float x = sg * a.W[((int64_t)c0 * 9 + u * 3 + w) * a.C_in + ci];
+            const float4 prm = P ? P[ci] : make_float4(1.f, 1.f, 0.f, a.bias_next[ci]);
+            ap = x > 0.f ? x * prm.x : x * prm.y;
+            acc += fminf(x, 0.f) * prm.z + ap * prm.w;
+          }
+          __builtin_nontemporal_store(ap, o + ci);   // read back only by the next GEMM
+        }
+      }
+    acc += __shfl_xor(acc, 32);
+    acc += __shfl_xor(acc, 16);
+    acc += __shfl_xor(acc, 8);
+    acc += __shfl_xor(acc, 4);
+    acc += __shfl_xor(acc, 2);
+    acc += __shfl_xor(acc, 1);
+    if (lane == 0) a.beta[r] = sg * a.b[c0] + acc;
   }
-  acc += __shfl_xor(acc, 32);
-  acc += __shfl_xor(acc, 16);
-  acc += __shfl_xor(acc, 8);
-  acc += __shfl_xor(acc, 4);
-  acc += __shfl_xor(acc, 2);
-  acc += __shfl_xor(acc, 1);
-  if (lane == 0) a.beta[r] = sg * a.b[c0] + acc;
 }
 
 hipError_t launch_init_conv(const ConvInitArgs &a, hipStream_t s) {
-  hipLaunchKernelGGL(k_init_conv, dim3((unsigned)((a.R + 3) / 4)), dim3(256), 0, s, a);
+  const int64_t waves = (a.R + INIT_CONV_RPW - 1) / INIT_CONV_RPW;
+  hipLaunchKernelGGL(k_init_conv, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
@@ -781,7 +789,8 @@ __global__ void k_rowsum_win(float *beta, const float *part, int32_t n_parts, in
   if (r < R) {
     for (int q = j; q < per_row; q += G) {
       const int64_t m = r * per_row + q;
-      for (int p = 0; p < n_parts; ++p) s += part[p * M_pad + m];
+#pragma unroll 4
+      for (int p = 0; p < n_parts; ++p) s += part[p * M_pad + m];   // loads issued ahead of the adds
     }
   }
   for (int o = G >> 1; o > 0; o >>= 1) s += __shfl_xor(s, o);   // every lane takes part

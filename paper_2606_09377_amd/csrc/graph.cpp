@@ -24,6 +24,7 @@
 #include <cstring>
 #include <functional>
 #include <map>
+#include <vector>
 
 #include "conv.h"
 #include "ctx.h"
@@ -44,6 +45,7 @@ struct GNode {
   float *Bt = nullptr;         // conv [Ci_pad][9 Co]; dense [ld(in)][ld(out)] (HWC order if hwc_in)
   float *Wp = nullptr;         // dense [out][ld(in)] original column order (IBP, spec fold)
   float *Wh = nullptr;         // dense [out][ld(in)] HWC column order when hwc_in (init rows)
+  float *Wk = nullptr;         // conv [Co][3][3][Ci]: channels contiguous per tap (init rows)
   float *b = nullptr;          // bias, zero padded to ld(out) for dense
   std::vector<float> hb;       // host copy of the bias
   int Ci_pad = 0;
@@ -102,7 +104,7 @@ struct GraphNet {
 void destroy_graph(GraphNet *g) {
   if (!g) return;
   for (auto &n : g->nodes) {
-    for (float *p : {n.W, n.Bt, n.Wp, n.Wh, n.b})
+    for (float *p : {n.W, n.Bt, n.Wp, n.Wh, n.Wk, n.b})
       if (p) (void)hipFree(p);
   }
   if (g->bias_arena) (void)hipFree(g->bias_arena);
@@ -571,6 +573,15 @@ vcr_status graph_load(vcr_ctx *c, const vcr_node *nodes, int32_t n, const int32_
       HIP_TRY(c, hipMalloc(&gn.W, wn * 4));
       c->net_bytes += wn * 4;
       HIP_TRY(c, hipMemcpy(gn.W, d.W, wn * 4, hipMemcpyHostToDevice));
+      {
+        std::vector<float> wk(wn);
+        for (int co = 0; co < Co; ++co)
+          for (int ci = 0; ci < Ci; ++ci)
+            for (int t = 0; t < 9; ++t) wk[((size_t)co * 9 + t) * Ci + ci] = d.W[((size_t)co * Ci + ci) * 9 + t];
+        HIP_TRY(c, hipMalloc(&gn.Wk, wn * 4));
+        c->net_bytes += wn * 4;
+        HIP_TRY(c, hipMemcpy(gn.Wk, wk.data(), wn * 4, hipMemcpyHostToDevice));
+      }
       HIP_TRY(c, hipMalloc(&gn.b, (size_t)Co * 4));
       c->net_bytes += (size_t)Co * 4;
       HIP_TRY(c, hipMemcpy(gn.b, d.b, (size_t)Co * 4, hipMemcpyHostToDevice));
@@ -701,7 +712,7 @@ vcr_status run_pass(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &pp, int 
     switch (st.kind) {
       case ST_INIT_CONV: {
         ConvInitArgs a{};
-        a.W = nd.W;
+        a.W = nd.Wk;
         a.b = nd.b;
         a.C_src = nd.C;
         a.H_src = nd.H;
