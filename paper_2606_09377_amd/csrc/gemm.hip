@@ -472,7 +472,7 @@ __global__ __launch_bounds__(NTHREADS, GEMM_MINB) void k_gemm(const GemmArgs p) 
 
 // Small launches (few row tiles): a workgroup of two waves owns a 32 x 64 tile, each wave one
 // 32-column block, and reads its MFMA operands straight from global memory (no LDS operand
-// staging), two K tiles prefetched in registers.  Each lane takes the same 16 consecutive k of
+// staging), four K tiles prefetched in registers.  Each lane takes the same 16 consecutive k of
 // its row per K tile as in k_gemm, each accumulator sees the same MFMA sequence, and the row
 // sums of the two blocks are added in k_gemm's order, so both kernels give the same bits.
 constexpr int SM_BM = 32, SM_BN = 64;
@@ -493,7 +493,9 @@ __global__ __launch_bounds__(128) void k_gemm_small(const GemmArgs p) {
   f32x16 acc[1][1];
 #pragma unroll
   for (int v = 0; v < 16; ++v) acc[0][0][v] = 0.f;
-  f32x4 a[BK / 8], b[BK / 8], a1[BK / 8], b1[BK / 8], a2[BK / 8], b2[BK / 8];
+  // four K tiles of loads in flight: a lone wave per tile has no other way to hide the latency
+  f32x4 a[BK / 8], b[BK / 8], a1[BK / 8], b1[BK / 8], a2[BK / 8], b2[BK / 8], a3[BK / 8], b3[BK / 8], a4[BK / 8],
+      b4[BK / 8];
   auto load = [&](int k0, f32x4 *ra, f32x4 *rb) {
 #pragma unroll
     for (int h = 0; h < BK / 8; ++h) {
@@ -507,8 +509,10 @@ __global__ __launch_bounds__(128) void k_gemm_small(const GemmArgs p) {
   const int KT = p.K / BK;
   load(0, a, b);
   if (KT > 1) load(BK, a1, b1);
+  if (KT > 2) load(2 * BK, a2, b2);
+  if (KT > 3) load(3 * BK, a3, b3);
   for (int kt = 0; kt < KT; ++kt) {
-    if (kt + 2 < KT) load((kt + 2) * BK, a2, b2);
+    if (kt + 4 < KT) load((kt + 4) * BK, a4, b4);
 #pragma unroll
     for (int h = 0; h < BK / 8; ++h)
 #pragma unroll
@@ -520,6 +524,10 @@ __global__ __launch_bounds__(128) void k_gemm_small(const GemmArgs p) {
       b[h] = b1[h];
       a1[h] = a2[h];
       b1[h] = b2[h];
+      a2[h] = a3[h];
+      b2[h] = b3[h];
+      a3[h] = a4[h];
+      b3[h] = b4[h];
     }
   }
   gemm_epilogue<FWD, AL, AFF, 1, 1>(p, acc, m0, 0, n0, lane, SM_BM, bj, xpart, n0, SM_BN, sflag);
