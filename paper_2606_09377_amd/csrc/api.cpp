@@ -897,12 +897,21 @@ vcr_status crown_impl(vcr_ctx *c, const float *x0, int32_t B, float eps, const f
   HIP_TRY(c, launch_spec_cw(C, Bs, m, WL.n_out, WL.Wp, WL.ld_in, WL.b, WL.n_in, bf.CW, WL.ld_in, bf.Cb, s));
   SplitTable tab{};
   if (D > 0) {
+    // the per-ReLU bound pointers for the split preparation: as a kernel argument when they
+    // fit one (no wait), else copied from a host array that must outlive the copy
     std::vector<const float *> hp(2 * R);
     for (int r = 0; r < R; ++r) {
       hp[r] = bf.Lb[r];
       hp[R + r] = bf.Ub[r];
     }
-    HIP_TRY(c, hipMemcpyAsync(bf.Lptr, hp.data(), sizeof(void *) * 2 * R, hipMemcpyHostToDevice, s));
+    const bool by_arg = 2 * R <= PTR_TABLE_MAX;
+    if (by_arg) {
+      PtrTable pt{};
+      for (int i = 0; i < 2 * R; ++i) pt.p[i] = hp[i];
+      HIP_TRY(c, launch_store_ptrs(pt, 2 * R, bf.Lptr, s));
+    } else {
+      HIP_TRY(c, hipMemcpyAsync(bf.Lptr, hp.data(), sizeof(void *) * 2 * R, hipMemcpyHostToDevice, s));
+    }
     HIP_TRY(c, hipMemcpyAsync(bf.relu_n, c->relu_n.data(), sizeof(int32_t) * R, hipMemcpyHostToDevice, s));
     HIP_TRY(c, launch_fill(reinterpret_cast<float *>(c->d_counters), 80, 0.f, s));
     SplitPrepArgs sp{};
@@ -921,8 +930,7 @@ vcr_status crown_impl(vcr_ctx *c, const float *x0, int32_t B, float eps, const f
     sp.flags = bf.flags;
     sp.n_invalid = c->d_counters + 64;
     HIP_TRY(c, launch_split_prepare(sp, s));
-    // the host-side pointer array must outlive the async copy
-    HIP_TRY(c, hipStreamSynchronize(s));
+    if (!by_arg) HIP_TRY(c, hipStreamSynchronize(s));   // hp must outlive its copy
   }
   const int32_t units = D > 0 ? D : B;
   if (ac) {

@@ -56,6 +56,18 @@ hipError_t launch_copy(float *dst, const float *src, int64_t n, hipStream_t s) {
   return hipGetLastError();
 }
 
+__global__ void k_store_ptrs(const PtrTable t, int32_t n, const float **dst) {
+  const int i = threadIdx.x;
+  if (i < n) dst[i] = t.p[i];
+}
+
+hipError_t launch_store_ptrs(const PtrTable &t, int32_t n, const float **dst, hipStream_t s) {
+  if (n < 0 || n > PTR_TABLE_MAX) return hipErrorInvalidValue;
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_store_ptrs, dim3(1), dim3(PTR_TABLE_MAX), 0, s, t, n, dst);
+  return hipGetLastError();
+}
+
 // Wt[j][i] = W[i][j] for i < rows, j < cols, zero elsewhere; Wt is rows_t x ldt.
 // With rows == 0 the same kernel zero-pads a plain copy (see launch_transpose_pad).
 __global__ void k_transpose_pad(const float *W, int32_t rows, int32_t cols, float *Wt, int64_t ldt,

@@ -147,6 +147,13 @@ struct SplitPrepArgs {
 hipError_t launch_split_prepare(const SplitPrepArgs &a, hipStream_t s);
 hipError_t launch_count_unstable(const float *L, const float *U, int64_t n, int32_t *count, hipStream_t s);
 hipError_t launch_copy(float *dst, const float *src, int64_t n, hipStream_t s);
+// dst[i] = ptrs[i] for i < n <= PTR_TABLE_MAX, the table travelling as a kernel argument (no
+// host buffer has to outlive the launch)
+constexpr int PTR_TABLE_MAX = 128;
+struct PtrTable {
+  const float *p[PTR_TABLE_MAX];
+};
+hipError_t launch_store_ptrs(const PtrTable &t, int32_t n, const float **dst, hipStream_t s);
 
 // ---- alpha-CROWN (alpha.hip) --------------------------------------------------------
 // Rows are (unit, q), q < 2m: q < m the lower bound of spec row q, q >= m the negated upper
