@@ -541,10 +541,12 @@ __global__ __launch_bounds__(128) void k_gemm_small(const GemmArgs p) {
 // often as in the small-tile kernel.
 constexpr int MD_BM = 64, MD_BN = 64;
 constexpr int64_t MID_GRID = 256;   // 64 x 64 tiles from which the mid-size kernel runs
-// 128 x 128 tiles up to which it runs instead of k_gemm: between one and three rounds of the
-// 512 k_gemm workgroups that fit the chip, the last round of k_gemm leaves most compute units
-// idle (576 tiles: a round of 64), while four times as many 64 x 64 tiles fill it evenly
+// It also runs instead of k_gemm below MID_MAX_GRID 128 x 128 tiles when the last of k_gemm's
+// rounds of 512 workgroups (what fits the chip) would be at most half full (576 tiles: a
+// second round of 64): four times as many 64 x 64 tiles fill the chip evenly.  Whole or
+// nearly whole rounds stay on k_gemm, which is faster per tile.
 constexpr int64_t MID_MAX_GRID = 1536;
+constexpr int64_t GEMM_ROUND = 512;
 
 template <bool FWD, bool AL, bool AFF = false>
 __global__ __launch_bounds__(256) void k_gemm_mid(const GemmArgs p) {
@@ -614,7 +616,9 @@ int gemm_kind(const GemmArgs &a) {
   if (a.M_pad <= 0 || a.N_pad <= 0) return 0;
   const int64_t grid = (int64_t)(a.M_pad / BM) * (a.N_pad / BN);
   const int64_t mid = (int64_t)(a.M_pad / MD_BM) * (a.N_pad / MD_BN);
-  if (grid < MID_MAX_GRID && mid >= MID_GRID) return 3;
+  const int64_t last = grid % GEMM_ROUND;
+  const bool ragged = grid < MID_MAX_GRID && last > 0 && last <= GEMM_ROUND / 2;
+  if ((grid < SMALL_GRID || ragged) && mid >= MID_GRID) return 3;
   return grid < SMALL_GRID ? 2 : 0;
 }
 
@@ -635,7 +639,7 @@ hipError_t launch_gemm(const GemmArgs &a, hipStream_t s) {
   if (a.mode != EPI_RELAX && a.mode != EPI_CONCRETIZE && a.mode != EPI_FORWARD && a.mode != EPI_AFFINE)
     return hipErrorInvalidValue;
   const int64_t mid = (int64_t)(a.M_pad / MD_BM) * (a.N_pad / MD_BN);
-  if (grid < MID_MAX_GRID && mid >= MID_GRID) {   // gemm_kind 3
+  if (gemm_kind(a) == 3) {
     // too few 128 x 128 tiles to fill the chip, enough of 64 x 64 (same bits)
     const dim3 g((unsigned)mid), t(256);
     if (a.mode == EPI_AFFINE)
