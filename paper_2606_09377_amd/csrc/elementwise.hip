@@ -296,7 +296,7 @@ __device__ __forceinline__ float4 init_override(const SplitTable &st, int d, int
   return prm;
 }
 
-// The kernel only writes: each wavefront owns IR consecutive rows and walks the columns in
+// A write-bound kernel: each wavefront owns IR consecutive rows and walks the columns in
 // blocks of 256 NCH.  A lane keeps the relaxation parameters of its 4 NCH columns of the block
 // in registers while it writes those columns of all its rows (reloading them only where the
 // unit changes), so the parameters are read once per row group instead of once per row.  Each
