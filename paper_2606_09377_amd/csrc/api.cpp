@@ -283,6 +283,7 @@ void vcr_destroy(vcr_ctx *c) {
     free_ws(c);
     if (c->d_counters) (void)hipFree(c->d_counters);
     if (c->bab_buf) (void)hipFree(c->bab_buf);
+    if (c->root_cache) (void)hipFree(c->root_cache);
     for (auto e : c->ev_pool) (void)hipEventDestroy(e);
     if (c->gexec) (void)hipGraphExecDestroy(c->gexec);
     if (c->cap_stream) (void)hipStreamDestroy(c->cap_stream);
@@ -844,9 +845,32 @@ vcr_status crown_impl(vcr_ctx *c, const float *x0, int32_t B, float eps, const f
   hipStream_t s = c->stream;
   const int64_t ld0 = ld_of(c->n0);
 
+  // the root steps 1-3 of a branch-and-bound round: copied from the loop's first round
+  const bool use_cache = D > 0 && c->bab_reuse && c->root_cached;
+  const bool fill_cache = D > 0 && c->bab_reuse && !c->root_cached;
+  size_t cache_floats = 0;
+  for (int r = 0; r < R && D > 0; ++r) cache_floats += 2 * (size_t)c->relu_n[r] + 4 * (size_t)c->layers[r].ld_out;
+  auto cache_copy = [&](bool to_cache) -> vcr_status {
+    size_t o = 0;
+    for (int r = 0; r < R; ++r) {
+      const int64_t n = c->relu_n[r], np = 4 * c->layers[r].ld_out;
+      float *cl = c->root_cache + o, *cu = cl + n, *cp = cu + n;
+      float *pp = reinterpret_cast<float *>(bf.P[r]);
+      HIP_TRY(c, launch_copy(to_cache ? cl : bf.Lb[r], to_cache ? bf.Lb[r] : cl, n, s));
+      HIP_TRY(c, launch_copy(to_cache ? cu : bf.Ub[r], to_cache ? bf.Ub[r] : cu, n, s));
+      HIP_TRY(c, launch_copy(to_cache ? cp : pp, to_cache ? pp : cp, np, s));
+      o += 2 * n + np;
+    }
+    return VCR_OK;
+  };
+
   // 1. box and IBP
   HIP_TRY(c, launch_box(x0, B, c->n0, ld0, eps, c->clip_on, c->clip_lo, c->clip_hi, bf.c0, bf.r0, s));
-  for (int k = 0; k < L - 1; ++k) {
+  if (use_cache) {
+    st = cache_copy(false);
+    if (st != VCR_OK) return st;
+  }
+  for (int k = 0; k < L - 1 && !use_cache; ++k) {
     const DenseLayer &W = c->layers[k];
     const float *cin = k == 0 ? bf.c0 : bf.ibp_c[k - 1];
     const float *rin = k == 0 ? bf.r0 : bf.ibp_r[k - 1];
@@ -854,11 +878,11 @@ vcr_status crown_impl(vcr_ctx *c, const float *x0, int32_t B, float eps, const f
     if (st != VCR_OK) return st;
   }
   // 2. first ReLU
-  if (L >= 2)
+  if (L >= 2 && !use_cache)
     HIP_TRY(c, launch_layer_from_ibp(bf.ibp_c[0], bf.ibp_r[0], c->layers[0].ld_out, c->layers[0].n_out, B,
                                      c->layers[0].b, bf.Lb[0], bf.Ub[0], bf.P[0], c->layers[0].ld_out, s));
   // 3. ReLU k >= 2 (layer index k: z_k = layers[k-1]); relu r = k-1
-  for (int k = 2; k <= L - 1; ++k) {
+  for (int k = 2; k <= L - 1 && !use_cache; ++k) {
     const DenseLayer &Wk = c->layers[k - 1];
     const int32_t n = Wk.n_out;
     for (int32_t b0 = 0; b0 < B; b0 += p.chunk_in) {
@@ -890,6 +914,19 @@ vcr_status crown_impl(vcr_ctx *c, const float *x0, int32_t B, float eps, const f
                                        bf.P[k - 1] + (int64_t)b0 * Wk.ld_out, Wk.ld_out, s));
       ++chunks;
     }
+  }
+  if (fill_cache) {
+    if (c->root_cache_cap < cache_floats) {
+      HIP_TRY(c, hipStreamSynchronize(s));
+      if (c->root_cache) HIP_TRY(c, hipFree(c->root_cache));
+      c->root_cache = nullptr;
+      c->root_cache_cap = 0;
+      HIP_TRY(c, hipMalloc(&c->root_cache, sizeof(float) * cache_floats));
+      c->root_cache_cap = cache_floats;
+    }
+    st = cache_copy(true);
+    if (st != VCR_OK) return st;
+    c->root_cached = true;
   }
   // 4. spec pass
   const DenseLayer &WL = c->layers[L - 1];
@@ -1288,6 +1325,12 @@ vcr_status vcr_bab_verify(vcr_ctx *c, const float *x0, float eps, const float *C
   std::deque<float> queue_lb;
   queue.emplace_back();
   queue_lb.push_back(root_min);
+  // every round bounds subdomains of the same root: its steps 1-3 run in the first round only
+  struct ReuseScope {
+    vcr_ctx *c;
+    explicit ReuseScope(vcr_ctx *cc) : c(cc) { c->bab_reuse = true; c->root_cached = false; }
+    ~ReuseScope() { c->bab_reuse = false; c->root_cached = false; }
+  } reuse_scope(c);
   for (int32_t rnd = 0; rnd < opts->max_rounds && !queue.empty(); ++rnd) {
     const size_t take = std::min<size_t>((size_t)opts->batch, queue.size());
     std::vector<std::vector<Split>> kids;

@@ -67,6 +67,12 @@ struct vcr_ctx {
   // workspace, which every bounding call carves anew)
   void *bab_buf = nullptr;
   size_t bab_cap = 0;
+  // the root's intermediate bounds and relaxation (one input), kept by the loop's first
+  // subdomain call and copied back by the later rounds instead of being recomputed (the
+  // rounds share the root input)
+  bool bab_reuse = false, root_cached = false;
+  float *root_cache = nullptr;
+  size_t root_cache_cap = 0;
   bool last_had_splits = false;
   double ms_last = 0.0;
   uint64_t flops_last = 0;
