@@ -277,25 +277,10 @@ hipError_t launch_layer_from_ibp(const float *c, const float *r, int64_t ld, int
 // First rows of a backward pass.  Row (unit u, direction d, i) starts as
 // (d ? -1 : 1) * src[i, :] (a weight row W_k[i] or a spec row (C W_L)[i]) with constant
 // (d ? -1 : 1) * src_bias[i]; the ReLU just below is relaxed with the lower rule and its
-// constants (relaxation intercepts and the bias of the dense layer below) are added.
-// Padding rows are zero.
-__device__ __forceinline__ float4 init_override(const SplitTable &st, int d, int relu, int col, float4 prm,
-                                                int *ent, float *sterm) {
-  const int e0 = st.off[d * (st.R + 1) + relu];
-  const int e1 = st.off[d * (st.R + 1) + relu + 1];
-  for (int e = e0; e < e1; ++e) {
-    if (st.ent_n[d * st.S + e] == col) {
-      const float4 q = st.ent_p[d * st.S + e];
-      prm.x = q.x;
-      prm.y = q.y;
-      prm.z = q.z;
-      *ent = e;
-      *sterm = q.w;
-    }
-  }
-  return prm;
-}
-
+// constants (relaxation intercepts and the bias of the dense layer below) are added; a split
+// neuron takes its fixed relaxation from the unit's split entries (the last entry of a column
+// wins).  Padding rows are zero.
+//
 // A write-bound kernel: each wavefront owns IR consecutive rows and walks the columns in
 // blocks of 256 NCH.  A lane keeps the relaxation parameters of its 4 NCH columns of the block
 // in registers while it writes those columns of all its rows (reloading them only where the
@@ -303,7 +288,6 @@ __device__ __forceinline__ float4 init_override(const SplitTable &st, int d, int
 // lane adds its columns in ascending order (carrying its running sum across column blocks in
 // LDS), whatever IR and NCH are, so the row constants have the same bits for every launch shape.
 // PLAIN: no split table, no per-row slopes and no copy of the unrelaxed rows (fewer registers).
-constexpr int INIT_ENT = 8;
 typedef float nt_f32x4 __attribute__((ext_vector_type(4)));
 template <int NCH, int IR, bool PLAIN>
 __global__ __launch_bounds__(256) void k_init_rows(const InitArgs a) {
@@ -318,6 +302,10 @@ __global__ __launch_bounds__(256) void k_init_rows(const InitArgs a) {
     const bool first = cb == 0, last = cb + 256 * NCH >= a.ldo;
     float4 prm[NCH][4];
     int32_t held = -1;
+    // the unit's split entries at this ReLU (the unit is wave-uniform), folded into prm when
+    // the unit changes; smask marks this lane's split columns of the block (bit 4 j + e)
+    int e0 = 0, ne = 0;
+    uint32_t smask = 0;
 #pragma unroll 1
     for (int r = 0; r < IR; ++r) {
       const int32_t row = row0 + r;
@@ -340,14 +328,36 @@ __global__ __launch_bounds__(256) void k_init_rows(const InitArgs a) {
       const float sgn = dir ? -1.f : 1.f;
       const int64_t srow = a.per_unit_src ? (int64_t)u * a.n_src + i : i;
       const int32_t pu = a.param_per_unit ? u : 0;
-      if (pu != held) {
+      const int32_t key = has_splits ? u : pu;   // split units carry their own overrides
+      if (key != held) {
         const float4 *P = a.P + (int64_t)pu * a.ldp + cb + lane * 4;
 #pragma unroll
         for (int j = 0; j < NCH; ++j)
 #pragma unroll
           for (int e = 0; e < 4; ++e)
             prm[j][e] = cb + j * 256 + lane * 4 < a.ldo ? P[j * 256 + e] : make_float4(0.f, 0.f, 0.f, 0.f);
-        held = pu;
+        if (has_splits) {
+          smask = 0;
+          e0 = a.splits.off[u * (a.splits.R + 1) + a.relu_index];
+          ne = a.splits.off[u * (a.splits.R + 1) + a.relu_index + 1] - e0;
+          for (int k = 0; k < ne; ++k) {   // in order: the last entry of a column wins
+            const int64_t o = a.splits.ent_n[u * a.splits.S + e0 + k] - (cb + lane * 4);
+            if (o < 0 || o >= 256 * NCH || (o & 255) >= 4) continue;   // not this lane's column
+            const float4 ov = a.splits.ent_p[u * a.splits.S + e0 + k];
+            const int jo = (int)(o >> 8), eo = (int)(o & 3);
+#pragma unroll
+            for (int j = 0; j < NCH; ++j)
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                if (j == jo && e == eo) {
+                  prm[j][e].x = ov.x;
+                  prm[j][e].y = ov.y;
+                  prm[j][e].z = ov.z;
+                }
+            smask |= 1u << (4 * jo + eo);
+          }
+        }
+        held = key;
       }
       const float *src = a.src + srow * a.ld_src + cb + lane * 4;
       float4 w[NCH];
@@ -355,15 +365,6 @@ __global__ __launch_bounds__(256) void k_init_rows(const InitArgs a) {
       for (int j = 0; j < NCH; ++j)
         w[j] = cb + j * 256 + lane * 4 < a.ldo ? *reinterpret_cast<const float4 *>(src + j * 256)
                                               : make_float4(0.f, 0.f, 0.f, 0.f);
-      // the row's split entries at this ReLU, read once per row (the unit is wave-uniform);
-      // more than INIT_ENT of them take the general per-element lookup
-      int e0 = 0, ne = 0, ecol[INIT_ENT];
-      if (has_splits) {
-        e0 = a.splits.off[u * (a.splits.R + 1) + a.relu_index];
-        ne = a.splits.off[u * (a.splits.R + 1) + a.relu_index + 1] - e0;
-#pragma unroll
-        for (int k = 0; k < INIT_ENT; ++k) ecol[k] = k < ne ? a.splits.ent_n[u * a.splits.S + e0 + k] : -1;
-      }
       float acc = first ? 0.f : carry[wave][r][lane];
 #pragma unroll
       for (int j = 0; j < NCH; ++j) {
@@ -379,21 +380,13 @@ __global__ __launch_bounds__(256) void k_init_rows(const InitArgs a) {
           float4 q = prm[j][e];
           int ent = -1;
           float sterm = 0.f;
-          if (has_splits) {
-            if (ne <= INIT_ENT) {
-#pragma unroll
-              for (int k = 0; k < INIT_ENT; ++k)
-                if (ecol[k] == (int)(c + e)) {   // the last match wins, as in init_override
-                  const float4 o = a.splits.ent_p[u * a.splits.S + e0 + k];
-                  q.x = o.x;
-                  q.y = o.y;
-                  q.z = o.z;
-                  ent = e0 + k;
-                  sterm = o.w;
-                }
-            } else {
-              q = init_override(a.splits, u, a.relu_index, (int)(c + e), q, &ent, &sterm);
-            }
+          if (has_splits && a.splits.beta && ((smask >> (4 * j + e)) & 1u)) {
+            // a split column (rare): its entry for the beta term, the last match as above
+            for (int k = 0; k < ne; ++k)
+              if (a.splits.ent_n[u * a.splits.S + e0 + k] == (int)(c + e)) {
+                ent = e0 + k;
+                sterm = a.splits.ent_p[u * a.splits.S + e0 + k].w;
+              }
           }
           const float x = sgn * wv[e];
           float lam = q.x;
