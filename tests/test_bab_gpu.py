@@ -94,3 +94,27 @@ def test_bab_edge_cases():
     ctx.set_option(OPT_SYNC_CHECK, 1)
     with pytest.raises(VcrError):
         gpu_crown(ctx, wl, splits=splits)
+
+
+def test_bab_many_splits_per_layer():
+    """Forty splits per domain, most of them at one ReLU layer (many per column block and per
+    lane), against the oracle on every domain."""
+    wl = random_mlp(202, [60, 140, 300, 5], 1, 0.05)
+    root = oracle.crown(wl.net, wl.x0[0], wl.eps, wl.C[0])
+    pool = oracle.unstable_pool(wl.net, root)
+    first, last = pool[pool[:, 0] == 0], pool[pool[:, 0] == 1]
+    assert len(first) >= 12 and len(last) >= 40
+    rng = np.random.default_rng(23)
+    a = draw_splits(rng, last, 256, 40)
+    b1, b2 = draw_splits(rng, last, 256, 28), draw_splits(rng, first, 256, 12)
+    splits = Splits(np.concatenate([a.relu_id, np.concatenate([b1.relu_id, b2.relu_id], 1)]),
+                    np.concatenate([a.neuron, np.concatenate([b1.neuron, b2.neuron], 1)]),
+                    np.concatenate([a.sign, np.concatenate([b1.sign, b2.sign], 1)]))
+    ctx = gpu_ctx(wl.net)
+    log("gpu run 512 domains, 40 splits each")
+    lb, ub, _ = gpu_crown(ctx, wl, splits=splits)
+    assert ctx.stats()["invalid_domains"] == 0
+    LB, UB = oracle.crown_domains(wl.net, root, wl.C[0], splits, domains=list(range(512)))
+    for d in range(512):
+        assert_close(lb[d], LB[d], f"domain {d} lb")
+        assert_close(ub[d], UB[d], f"domain {d} ub")

@@ -132,3 +132,36 @@ def test_bab_default_order_is_intercept_order():
     order = [(r, j) for _, r, j in sorted(cand, key=lambda t: t[0])]
     b = ctx.bab_verify(to_dev(wl.x0), wl.eps, to_dev(wl.C), batch=4, max_rounds=5, iters=10, order=order)
     assert a == b
+
+
+def test_beta_deep_domains_one_layer():
+    """Subdomains with 12 to 24 splits, most at one ReLU layer (many split columns per lane):
+    every evaluation of five Adam steps against the oracle."""
+    import torch
+    wl, root = _case()
+    ctx = gpu_ctx(wl.net)
+    order = beta64.default_order(wl.net, root)
+    layer1 = [o for o in order if o[0] == 1]
+    assert len(layer1) >= 24
+    rng = np.random.default_rng(29)
+    doms = []
+    for depth in (12, 16, 20, 24):
+        pick = rng.choice(len(layer1), size=depth, replace=False)
+        doms.append([(layer1[p][0], layer1[p][1], int(rng.choice([-1, 1]))) for p in pick])
+    doms.append(doms[0] + [(order[0][0], order[0][1], 1)] if order[0][0] != 1 else doms[0][:6])
+    T = 5
+    lb, ub, ex = ctx.beta_crown_bounds(to_dev(wl.x0), wl.eps, to_dev(wl.C), _split_tensors(doms, 25), iters=T,
+                                       want_hist=True)
+    torch.cuda.synchronize()
+    lb, ub = lb.cpu().numpy(), ub.cpu().numpy()
+    lh, uh = ex["lb_hist"].cpu().numpy(), ex["ub_hist"].cpu().numpy()
+    for d, dom in enumerate(doms):
+        r = beta64.beta_crown(wl.net, root, wl.C[0], dom, iters=T)
+        if not r.feasible:
+            assert np.all(np.isposinf(lb[d])) and np.all(np.isneginf(ub[d]))
+            continue
+        for t in range(T + 1):
+            assert_close(lh[t, d], r.lb_hist[t], f"domain {d} evaluation {t} lb")
+            assert_close(uh[t, d], r.ub_hist[t], f"domain {d} evaluation {t} ub")
+        assert_close(lb[d], r.lb, f"domain {d} lb")
+        assert_close(ub[d], r.ub, f"domain {d} ub")
