@@ -110,6 +110,7 @@ hipError_t launch_alpha_keep(const AlphaLayer &l, const int32_t *flag, int32_t r
 // Adam (bias-corrected moments) then projection onto [0, 1], at unstable neurons only.  With
 // flag, the rows whose bound improved first keep their current slopes in best (the keep step
 // folded into the same pass over the state).
+typedef float adam_f32x4 __attribute__((ext_vector_type(4)));
 __global__ void k_alpha_adam(AlphaLayer l, const int32_t *flag, int32_t blocks_per_row, int32_t rows_per_unit,
                              float lr, float beta1, float beta2, float eps, float c1, float c2) {
   const int32_t row = blockIdx.x / blocks_per_row;
@@ -121,11 +122,12 @@ __global__ void k_alpha_adam(AlphaLayer l, const int32_t *flag, int32_t blocks_p
   if (n0 >= l.n) return;
   const int32_t u = row / rows_per_unit;
   const float4 *P = l.P + (int64_t)u * l.ld + n0;
-  const float4 g4 = *reinterpret_cast<const float4 *>(l.grad + idx);
-  float4 m4 = *reinterpret_cast<const float4 *>(l.mom + idx);
-  float4 v4 = *reinterpret_cast<const float4 *>(l.vel + idx);
-  float a[4] = {a4.x, a4.y, a4.z, a4.w}, g[4] = {g4.x, g4.y, g4.z, g4.w};
-  float mo[4] = {m4.x, m4.y, m4.z, m4.w}, ve[4] = {v4.x, v4.y, v4.z, v4.w};
+  // the gradient and the moments are touched once per step: streamed past the caches
+  const adam_f32x4 g4 = __builtin_nontemporal_load(reinterpret_cast<const adam_f32x4 *>(l.grad + idx));
+  const adam_f32x4 m4 = __builtin_nontemporal_load(reinterpret_cast<const adam_f32x4 *>(l.mom + idx));
+  const adam_f32x4 v4 = __builtin_nontemporal_load(reinterpret_cast<const adam_f32x4 *>(l.vel + idx));
+  float a[4] = {a4.x, a4.y, a4.z, a4.w}, g[4] = {g4[0], g4[1], g4[2], g4[3]};
+  float mo[4] = {m4[0], m4[1], m4[2], m4[3]}, ve[4] = {v4[0], v4[1], v4[2], v4[3]};
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     if (n0 + e >= l.n || !(P[e].z > 0.f)) continue;   // padding or a stable neuron: unchanged
@@ -134,8 +136,8 @@ __global__ void k_alpha_adam(AlphaLayer l, const int32_t *flag, int32_t blocks_p
     const float t = a[e] + lr * (mo[e] * c1) / (sqrtf(ve[e] * c2) + eps);
     a[e] = fminf(fmaxf(t, 0.f), 1.f);
   }
-  *reinterpret_cast<float4 *>(l.mom + idx) = make_float4(mo[0], mo[1], mo[2], mo[3]);
-  *reinterpret_cast<float4 *>(l.vel + idx) = make_float4(ve[0], ve[1], ve[2], ve[3]);
+  __builtin_nontemporal_store(adam_f32x4{mo[0], mo[1], mo[2], mo[3]}, reinterpret_cast<adam_f32x4 *>(l.mom + idx));
+  __builtin_nontemporal_store(adam_f32x4{ve[0], ve[1], ve[2], ve[3]}, reinterpret_cast<adam_f32x4 *>(l.vel + idx));
   *reinterpret_cast<float4 *>(l.alpha + idx) = make_float4(a[0], a[1], a[2], a[3]);
 }
 
