@@ -8,7 +8,12 @@ Calls only the fp64 oracle (oracle/) on the seeded workloads (workloads/).
     oracle's row-block computation for one hidden layer;
   * bab_mlp784x1024x6_splits.npz: the branch-and-bound subdomains of that workload, drawn
     from the oracle root pass's unstable neurons (the draw continues the workload's seeded
-    generator, so it equals what the tests draw at run time).
+    generator, so it equals what the tests draw at run time);
+  * <workload>_alpha.npz: the alpha-CROWN oracle's run (every evaluation's bounds and the
+    best ones) on the listed inputs, from CROWN's own slopes;
+  * <workload>_corners.npz: for the listed inputs, the box vertices where each spec row's
+    final linear bounds are attained (x_i = lo_i where the oracle's lower-bound coefficient
+    on x_i is positive, else hi_i; the mirror image for the upper bound), as sign bits.
 
   python tests/golden/make_goldens.py [name ...]     (name "bab" for the split file)
 """
@@ -30,6 +35,17 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 GOLDENS = {
     "mlp3072x8192x4": [0, 15],
     "resnet3x16x16": [0, 1],
+    "resnet3x8x8": [0, 1],
+}
+
+# alpha-CROWN runs: {workload: (inputs, Adam steps)}
+ALPHA = {
+    "mlp3072x8192x4": ([0], 5),
+}
+
+# A-guided box vertices: {workload: inputs}
+CORNERS = {
+    "mlp3072x8192x4": [0, 15],
 }
 
 # full-size workloads whose bounds are stored for sampled neurons (with every neuron their
@@ -39,12 +55,24 @@ SAMPLED = {
 }
 
 
+def tie_count(r, tie=1e-5):
+    """Neurons whose adaptive lower slope sits on its tie u = -l (either slope would be a
+    correct result there; a stored result must have none)."""
+    n = 0
+    for i in r.layer_l:
+        l, u = r.layer_l[i], r.layer_u[i]
+        n += int(np.sum((l < 0) & (u > 0) & (np.abs(u + l) <= tie * (u - l))))
+    return n
+
+
 def make(name, inputs):
     wl = make_workload(name)
     out = {"inputs": np.array(inputs)}
     for b in inputs:
         t = time.time()
         r = oracle.crown(wl.net, wl.x0[b], wl.eps, wl.C[b])
+        if tie_count(r):
+            raise SystemExit(f"{name} input {b}: {tie_count(r)} neurons on the slope tie; pick another seed")
         out[f"lb_{b}"] = r.lb
         out[f"ub_{b}"] = r.ub
         for i in r.layer_l:
@@ -101,6 +129,36 @@ def make_one_hidden(name, inputs, n_sample):
     print("wrote", path)
 
 
+def make_alpha(name, inputs, iters):
+    from oracle import alpha64
+    wl = make_workload(name)
+    out = {"inputs": np.array(inputs), "iters": np.array(iters)}
+    for b in inputs:
+        t = time.time()
+        r = alpha64.alpha_crown(wl.net, wl.x0[b], wl.eps, wl.C[b], iters=iters)
+        out[f"lb_{b}"], out[f"ub_{b}"] = r.lb, r.ub
+        out[f"lb_hist_{b}"], out[f"ub_hist_{b}"] = r.lb_hist, r.ub_hist
+        print(f"{name} alpha input {b}: {time.time() - t:.1f} s", flush=True)
+    path = os.path.join(HERE, f"{name}_alpha.npz")
+    np.savez_compressed(path, **out)
+    print("wrote", path)
+
+
+def make_corners(name, inputs):
+    wl = make_workload(name)
+    out = {"inputs": np.array(inputs)}
+    for b in inputs:
+        t = time.time()
+        r = oracle.crown(wl.net, wl.x0[b], wl.eps, wl.C[b], keep_A=True)
+        # lower bound: attained at lo where the coefficient is positive; upper: at hi there
+        out[f"lower_at_lo_{b}"] = np.packbits(r.A_lower > 0, axis=1)
+        out[f"upper_at_hi_{b}"] = np.packbits(r.A_upper > 0, axis=1)
+        print(f"{name} corners input {b}: {time.time() - t:.1f} s", flush=True)
+    path = os.path.join(HERE, f"{name}_corners.npz")
+    np.savez_compressed(path, **out)
+    print("wrote", path)
+
+
 def make_bab_splits():
     from workloads import draw_splits
     wl = make_workload("bab_mlp784x1024x6")
@@ -113,9 +171,14 @@ def make_bab_splits():
 
 
 if __name__ == "__main__":
-    names = sys.argv[1:] or list(GOLDENS) + ["bab"] + [f"{k}_sampled" for k in SAMPLED] + list(ONE_HIDDEN)
+    names = sys.argv[1:] or (list(GOLDENS) + ["bab"] + [f"{k}_sampled" for k in SAMPLED] + list(ONE_HIDDEN)
+                             + [f"{k}_alpha" for k in ALPHA] + [f"{k}_corners" for k in CORNERS])
     for n in names:
-        if n in ONE_HIDDEN:
+        if n.endswith("_alpha"):
+            make_alpha(n[:-len("_alpha")], *ALPHA[n[:-len("_alpha")]])
+        elif n.endswith("_corners"):
+            make_corners(n[:-len("_corners")], CORNERS[n[:-len("_corners")]])
+        elif n in ONE_HIDDEN:
             make_one_hidden(n, *ONE_HIDDEN[n])
         elif n == "bab":
             make_bab_splits()

@@ -10,7 +10,7 @@ import numpy as np
 import pytest
 
 import oracle
-from tests.gpu_util import assert_close, check_input, gpu_crown, gpu_ctx, log, to_dev
+from tests.gpu_util import assert_classes, assert_close, check_input, gpu_crown, gpu_ctx, log, to_dev
 from workloads import Net, Node, Workload, make_workload
 from workloads.gen import margin_spec, resnet_net
 
@@ -164,6 +164,33 @@ def test_resnet3x16x16_all_bounds_golden():
         for r, i in enumerate(relu_ids):
             assert_close(layers[r][0][b], g[f"l_{b}_{i}"], f"input {b} relu {r} l")
             assert_close(layers[r][1][b], g[f"u_{b}_{i}"], f"input {b} relu {r} u")
+
+
+def test_resnet3x8x8_full_width_all_bounds_golden():
+    """The full ResNet's channel widths (64 and 128), FC 512 and 100 classes on a 3x8x8
+    image: every intermediate bound of all four ReLU layers, every ReLU class and all 99
+    spec rows of both inputs against the stored oracle results.  Its 128-channel
+    convolutions run the transposed convolution on 128 x 128 tiles (with and without the
+    ReLU relaxation in the epilogue) in the FC 512 and spec passes."""
+    g = np.load(os.path.join(GOLDEN, "resnet3x8x8.npz"))
+    wl = make_workload("resnet3x8x8")
+    assert wl.net.nodes[-1].W.shape == (100, 512)
+    ctx = gpu_ctx(wl.net)
+    lb, ub, layers = gpu_crown(ctx, wl)
+    relu_ids = [i for i, nd in enumerate(wl.net.nodes) if nd.op == "relu"]
+    assert len(relu_ids) == 4
+    for b in g["inputs"]:
+        assert_close(lb[b], g[f"lb_{b}"], f"input {b} lb")
+        assert_close(ub[b], g[f"ub_{b}"], f"input {b} ub")
+        for r, i in enumerate(relu_ids):
+            rl, ru = g[f"l_{b}_{i}"], g[f"u_{b}_{i}"]
+            assert_close(layers[r][0][b], rl, f"input {b} relu {r} l")
+            assert_close(layers[r][1][b], ru, f"input {b} relu {r} u")
+            assert_classes(layers[r][0][b], layers[r][1][b], rl, ru, f"input {b} relu {r}")
+            log("input", b, "relu", r, "unstable (oracle)", int(np.sum((rl < 0) & (ru > 0))))
+    # one input alone gives its batch row bit for bit
+    lb1, ub1, _ = gpu_crown(ctx, wl, inputs=[1])
+    assert np.array_equal(lb1[0], lb[1]) and np.array_equal(ub1[0], ub[1])
 
 
 def test_resnet3x32x32_full_size():

@@ -296,6 +296,10 @@ WORKLOADS = {
     # the oracle to compute every bound)
     "resnet3x16x16": dict(kind="resnet", seed=41, batch=2, eps=2.0 / 255.0,
                           arch=dict(in_chw=(3, 16, 16), c1=32, c2=64, fc=64, n_out=10)),
+    # the full ResNet's channel widths (64 / 128), FC 512 and 100 classes on a 3x8x8 image,
+    # small enough for the oracle to compute every bound
+    "resnet3x8x8": dict(kind="resnet", seed=42, batch=2, eps=2.0 / 255.0,
+                        arch=dict(in_chw=(3, 8, 8), c1=64, c2=128, fc=512, n_out=100)),
 }
 
 
