@@ -175,3 +175,38 @@ def test_alpha_rejects_conv_nets_and_bad_options():
     for kw in ({"lr": 0.0}, {"beta1": 1.0}, {"iters": -1}, {"adam_eps": 0.0}):
         with pytest.raises(VcrError, match="ARG"):
             ctx.alpha_crown_bounds(to_dev(wl.x0), wl.eps, to_dev(wl.C), **kw)
+
+
+def test_alpha_mlp3072x8192x4_bench_size():
+    """The wide MLP (8192-wide layers, 99 spec rows), 16 inputs, 5 Adam steps: the batch runs
+    its spec-pass steps on the 128 x 128 tile kernel with the alpha-CROWN epilogues, one
+    input alone on the 64 x 64 and 32 x 64 tile kernels.  The input alone equals its batch
+    row bit for bit at every evaluation, and input 0 matches the stored oracle run (every
+    evaluation and the best bounds)."""
+    import os
+    import torch
+    from paper_2606_09377_amd.vcrown import OPT_TIME_GEMM
+    g = np.load(os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "mlp3072x8192x4_alpha.npz"))
+    T = int(g["iters"])
+    wl = make_workload("mlp3072x8192x4")
+    ctx = gpu_ctx(wl.net)
+    log("alpha B=16 T", T)
+    lb, ub, ex = ctx.alpha_crown_bounds(to_dev(wl.x0), wl.eps, to_dev(wl.C), iters=T, want_hist=True)
+    torch.cuda.synchronize()
+    lb, ub = lb.cpu().numpy(), ub.cpu().numpy()
+    lh, uh = ex["lb_hist"].cpu().numpy(), ex["ub_hist"].cpu().numpy()
+    ctx.set_option(OPT_TIME_GEMM, 1)
+    log("alpha B=1")
+    lb1, ub1, ex1 = ctx.alpha_crown_bounds(to_dev(wl.x0[:1]), wl.eps, to_dev(wl.C[:1]), iters=T, want_hist=True)
+    torch.cuda.synchronize()
+    assert ctx.stats()["timed_mid_launches"] > 0   # the single input's spec-pass steps
+    assert np.array_equal(lb1.cpu().numpy()[0], lb[0]) and np.array_equal(ub1.cpu().numpy()[0], ub[0])
+    assert np.array_equal(ex1["lb_hist"].cpu().numpy()[:, 0], lh[:, 0])
+    assert np.array_equal(ex1["ub_hist"].cpu().numpy()[:, 0], uh[:, 0])
+    for b in g["inputs"]:
+        for t in range(T + 1):
+            assert_close(lh[t, b], g[f"lb_hist_{b}"][t], f"input {b} evaluation {t} lb")
+            assert_close(uh[t, b], g[f"ub_hist_{b}"][t], f"input {b} evaluation {t} ub")
+        assert_close(lb[b], g[f"lb_{b}"], f"input {b} best lb")
+        assert_close(ub[b], g[f"ub_{b}"], f"input {b} best ub")
+        log("input", b, "mean lb gain over CROWN", float(np.mean(g[f"lb_{b}"] - g[f"lb_hist_{b}"][0])))

@@ -165,3 +165,48 @@ def test_beta_deep_domains_one_layer():
             assert_close(uh[t, d], r.ub_hist[t], f"domain {d} evaluation {t} ub")
         assert_close(lb[d], r.lb, f"domain {d} lb")
         assert_close(ub[d], r.ub, f"domain {d} ub")
+
+
+def test_beta_bench_size_batches():
+    """beta-CROWN on the 784-1024x6 MLP's stored subdomains (8 splits each) at the sizes the
+    branch-and-bound bench runs: 512 subdomains (9216 rows, the 64 x 64 tile kernel with
+    split multipliers in its epilogues) and 4096 (73728 rows, the 128 x 128 tile kernel).
+    Every evaluation of 5 joint Adam steps on 16 sampled subdomains of each call against the
+    oracle; the 512 subdomains are the first of the 4096, and their bounds agree bit for bit
+    between the two calls."""
+    import os
+    import torch
+    from paper_2606_09377_amd.vcrown import OPT_TIME_GEMM
+    from workloads import make_workload
+    wl = make_workload("bab_mlp784x1024x6")
+    sp = np.load(os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "bab_mlp784x1024x6_splits.npz"))
+    root = oracle.crown(wl.net, wl.x0[0], wl.eps, wl.C[0])
+    ctx = gpu_ctx(wl.net)
+    T = 5
+    rng = np.random.default_rng(17)
+    res = {}
+    for D in (512, 4096):
+        tens = tuple(to_dev(np.ascontiguousarray(sp[k][:D])) for k in ("relu_id", "neuron", "sign"))
+        ctx.set_option(OPT_TIME_GEMM, 1)
+        log("beta D", D)
+        lb, ub, ex = ctx.beta_crown_bounds(to_dev(wl.x0), wl.eps, to_dev(wl.C), tens, iters=T, want_hist=True)
+        torch.cuda.synchronize()
+        # the root pass (2048 rows) never reaches the 128 x 128 tile kernel; the spec pass of
+        # 4096 subdomains does, that of 512 does not
+        n_big = ctx.stats()["timed_gemm_launches"]
+        assert (n_big > 0) if D == 4096 else (n_big == 0), (D, n_big)
+        lb, ub = lb.cpu().numpy(), ub.cpu().numpy()
+        lh, uh = ex["lb_hist"].cpu().numpy(), ex["ub_hist"].cpu().numpy()
+        res[D] = (lb, ub)
+        for d in sorted(rng.choice(D, 16, replace=False)):
+            dom = [(int(sp["relu_id"][d, e]), int(sp["neuron"][d, e]), int(sp["sign"][d, e])) for e in range(8)]
+            r = beta64.beta_crown(wl.net, root, wl.C[0], dom, iters=T)
+            if not r.feasible:
+                assert np.all(np.isposinf(lb[d])) and np.all(np.isneginf(ub[d]))
+                continue
+            for t in range(T + 1):
+                assert_close(lh[t, d], r.lb_hist[t], f"D={D} domain {d} evaluation {t} lb")
+                assert_close(uh[t, d], r.ub_hist[t], f"D={D} domain {d} evaluation {t} ub")
+            assert_close(lb[d], r.lb, f"D={D} domain {d} lb")
+            assert_close(ub[d], r.ub, f"D={D} domain {d} ub")
+    assert np.array_equal(res[512][0], res[4096][0][:512]) and np.array_equal(res[512][1], res[4096][1][:512])
