@@ -84,6 +84,8 @@ typedef struct {
  * is empty (l > u) is infeasible and gets lb = +inf, ub = -inf (not an error).  A domain
  * with an out-of-range entry, a sign other than +-1 or a neuron repeated gets NaN bounds and
  * is counted in vcr_stats.invalid_domains. */
+#define VCR_MAX_SPLITS 64   /* split slots per subdomain (per_domain <= VCR_MAX_SPLITS) */
+
 typedef struct {
   int32_t n_domains, per_domain;
   const int32_t *relu_id;
@@ -105,12 +107,33 @@ enum {
                                        transposed-convolution) with HIP events
                                        on the context's stream; vcr_get_stats reports their summed
                                        duration.  Setting the option (either value) resets the sums. */
-  VCR_OPT_GRAPH = 8                 /* 1: vcr_crown_bounds without splits records its kernel launches
+  VCR_OPT_GRAPH = 8,                /* 1: vcr_crown_bounds without splits records its kernel launches
                                        into a HIP graph (captured on a private stream after one
                                        ordinary call with the same arguments) and, while the
                                        arguments, options, network and workspace stay the same,
                                        replays the graph on the context's stream instead of
                                        launching kernel by kernel.  Ignored while TIME_GEMM is on. */
+  VCR_OPT_CHECK_FINITE = 9,         /* 1: every bounds call first scans x0 and C on the device for NaN
+                                       and infinite values and fails with VCR_ERR_ARG (nothing else
+                                       queued, outputs untouched) if it finds any; the scan
+                                       synchronises the stream.  0 (default): no scan, and a
+                                       non-finite input gives undefined bounds (Sec. 1.1 defines the
+                                       input set for finite centres only). */
+  VCR_OPT_LAMBDA_RULE = 10          /* lower slope lambda of unstable ReLU neurons (Sec. 2.1 only
+                                       requires lambda in [0, 1], every value being sound):
+                                       VCR_LAMBDA_ADAPTIVE (default), VCR_LAMBDA_ZERO, VCR_LAMBDA_ONE,
+                                       VCR_LAMBDA_SAME_SLOPE.  Applies to every ReLU layer, to split
+                                       neurons' relaxations and to alpha-CROWN's initial slopes. */
+};
+
+/* Values of VCR_OPT_LAMBDA_RULE.  For an unstable neuron (l < 0 < u) with upper line slope
+ * s = u / (u - l): ADAPTIVE takes lambda = 1 if u > -l else 0 (a tie gives 0); ZERO 0; ONE 1;
+ * SAME_SLOPE lambda = s. */
+enum {
+  VCR_LAMBDA_ADAPTIVE = 0,
+  VCR_LAMBDA_ZERO = 1,
+  VCR_LAMBDA_ONE = 2,
+  VCR_LAMBDA_SAME_SLOPE = 3
 };
 
 typedef struct {
@@ -220,7 +243,7 @@ vcr_status vcr_alpha_crown_bounds(vcr_ctx *ctx, const float *x0, int32_t B, floa
 /* Number of ReLU neurons over all ReLU nodes of the loaded network (n_total above). */
 int64_t vcr_relu_neurons(const vcr_ctx *ctx);
 
-/* beta-CROWN on branch-and-bound subdomains (paper, Sec. 2.1, Alpha-Beta-CROWN): every split
+/* beta-CROWN on branch-and-bound subdomains (paper, Sec. 2.2, the alpha-beta-CROWN verifier): every split
  * g <= 0 (g = -z for an active split, g = z for an inactive one) enters the bound of its
  * subdomain with a multiplier beta >= 0 (f + beta g for a lower bound, f - beta g for an upper
  * one), one per (split, specification bound); the multipliers and the lower slopes alpha
@@ -242,8 +265,8 @@ vcr_status vcr_beta_crown_bounds(vcr_ctx *ctx, const float *x0, float eps, const
                                  const vcr_splits *splits, const vcr_beta_opts *opts,
                                  float *lb, float *ub);
 
-/* Fixed-batch branch-and-bound (paper, Sec. 2.1 complete verification; Sec. 3.4.4: a fixed
- * number of subdomains per round, no early stop) on the property C f(x) > 0 for every row of
+/* Fixed-batch branch-and-bound (paper, Sec. 2.1 complete verification; Sec. 2.2; Sec. 3.4.4: a
+ * fixed number of subdomains per round, no early stop) on the property C f(x) > 0 for every row of
  * C over the eps-ball around x0.  The root is bounded by alpha-CROWN; unverified subdomains
  * wait first-in first-out; each round takes up to `batch` of them, splits each on the first
  * neuron of the priority order that it has not split yet into an active and an inactive
@@ -252,7 +275,8 @@ vcr_status vcr_beta_crown_bounds(vcr_ctx *ctx, const float *x0, float eps, const
  * after max_rounds, or when a subdomain has no neuron left to split. */
 typedef struct {
   int32_t batch;            /* subdomains split per round (>= 1) */
-  int32_t max_rounds;       /* >= 0 */
+  int32_t max_rounds;       /* in [0, VCR_MAX_SPLITS]: a subdomain gains one split per round
+                               and holds at most VCR_MAX_SPLITS (VCR_ERR_ARG otherwise) */
   vcr_beta_opts bound;      /* bounding of the root and of every subdomain (hist ignored) */
   const int32_t *order_relu;    /* host [order_len]: split priority (ReLU node position,  */
   const int32_t *order_neuron;  /* neuron), or NULL: the root's unstable neurons by        */

@@ -6,7 +6,7 @@ leg may import this module.  It shares no code with the GPU library.
 
 What it computes (section numbers are the paper's).  Branch-and-bound (Sec. 2.1, complete
 verification) splits ReLU neurons into an active (z >= 0) and an inactive (z <= 0) case and
-bounds every subdomain.  beta-CROWN (Sec. 2.1, Alpha-Beta-CROWN) puts each split constraint
+bounds every subdomain.  beta-CROWN (Sec. 2.2, Alpha-Beta-CROWN) puts each split constraint
 into the bound propagation with a Lagrange multiplier beta >= 0: writing a split as g <= 0
 (g = -z for an active split, g = z for an inactive one), the minimum of f over the
 subdomain is at least the minimum over the whole box of f + beta g, and the maximum at most

@@ -41,6 +41,7 @@ vcr_status graph_crown(vcr_ctx *c, const float *x0, int32_t B, float eps, const 
 vcr_status graph_ibp(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m, float *lb,
                      float *ub);
 size_t graph_workspace_bytes(vcr_ctx *c, int32_t B, int32_t m);
+vcr_status graph_plan(vcr_ctx *c, int32_t B, int32_t m, int *chunk_out, size_t *bytes_out);
 }  // namespace vcr
 
 namespace {
@@ -313,6 +314,12 @@ vcr_status vcr_set_option(vcr_ctx *c, int32_t key, double v) {
       c->ws_cap = (uint64_t)v;
       break;
     case VCR_OPT_SYNC_CHECK: c->sync_check = v != 0.0; break;
+    case VCR_OPT_CHECK_FINITE: c->check_finite = v != 0.0; break;
+    case VCR_OPT_LAMBDA_RULE:
+      if (v != VCR_LAMBDA_ADAPTIVE && v != VCR_LAMBDA_ZERO && v != VCR_LAMBDA_ONE && v != VCR_LAMBDA_SAME_SLOPE)
+        return fail(c, VCR_ERR_ARG, "lambda rule %g is not one of VCR_LAMBDA_*", v);
+      c->lambda_rule = (int32_t)v;
+      break;
     case VCR_OPT_GRAPH:
       c->use_graph = v != 0.0;
       if (!c->use_graph && c->gexec) {
@@ -345,6 +352,7 @@ vcr_status vcr_load_net(vcr_ctx *c, const vcr_node *nodes, int32_t n, const int3
   std::vector<std::vector<int64_t>> sh;
   vcr_status st = validate_net(c, nodes, n, in_chw, &sh);
   if (st != VCR_OK) return st;
+  c->n_out = nodes[n - 1].out_features;
   // dense weight shapes must match their inputs
   for (int32_t i = 0; i < n; ++i) {
     if (nodes[i].op != VCR_DENSE) continue;
@@ -474,6 +482,22 @@ vcr_status check_common(vcr_ctx *c, const float *x0, int32_t B, float eps, const
     return fail(c, VCR_ERR_ARG, "tensor pointers must be 16-byte aligned");
   if ((int64_t)B * m > (int64_t)1 << 30) return fail(c, VCR_ERR_SHAPE, "B * m too large");
   if (c->clip_on && !(c->clip_lo <= c->clip_hi)) return fail(c, VCR_ERR_ARG, "clip_lo > clip_hi");
+  return VCR_OK;
+}
+
+// VCR_OPT_CHECK_FINITE: count the non-finite values of x0 (B x n0) and C (B x m x n_out) on
+// the device before anything else is queued (synchronises).
+vcr_status check_finite_inputs(vcr_ctx *c, const float *x0, int32_t B, const float *C, int32_t m) {
+  if (!c->check_finite || c->device < 0) return VCR_OK;
+  HIP_TRY(c, hipSetDevice(c->device));
+  int32_t *cnt = c->d_counters + 65;
+  HIP_TRY(c, launch_fill(reinterpret_cast<float *>(cnt), 1, 0.f, c->stream));
+  HIP_TRY(c, launch_count_nonfinite(x0, (int64_t)B * c->n0, cnt, c->stream));
+  HIP_TRY(c, launch_count_nonfinite(C, (int64_t)B * m * c->n_out, cnt, c->stream));
+  int32_t host = 0;
+  HIP_TRY(c, hipMemcpyAsync(&host, cnt, sizeof(int32_t), hipMemcpyDeviceToHost, c->stream));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  if (host > 0) return fail(c, VCR_ERR_ARG, "x0 or C holds %d non-finite value(s)", host);
   return VCR_OK;
 }
 
@@ -880,7 +904,7 @@ vcr_status crown_impl(vcr_ctx *c, const float *x0, int32_t B, float eps, const f
   // 2. first ReLU
   if (L >= 2 && !use_cache)
     HIP_TRY(c, launch_layer_from_ibp(bf.ibp_c[0], bf.ibp_r[0], c->layers[0].ld_out, c->layers[0].n_out, B,
-                                     c->layers[0].b, bf.Lb[0], bf.Ub[0], bf.P[0], c->layers[0].ld_out, s));
+                                     c->layers[0].b, bf.Lb[0], bf.Ub[0], bf.P[0], c->layers[0].ld_out, c->lambda_rule, s));
   // 3. ReLU k >= 2 (layer index k: z_k = layers[k-1]); relu r = k-1
   for (int k = 2; k <= L - 1 && !use_cache; ++k) {
     const DenseLayer &Wk = c->layers[k - 1];
@@ -911,7 +935,7 @@ vcr_status crown_impl(vcr_ctx *c, const float *x0, int32_t B, float eps, const f
                                        bf.ibp_c[k - 1] + (int64_t)b0 * Wk.ld_out,
                                        bf.ibp_r[k - 1] + (int64_t)b0 * Wk.ld_out, Wk.ld_out, c->intersect, Wk.b,
                                        bf.Lb[k - 1] + (int64_t)b0 * n, bf.Ub[k - 1] + (int64_t)b0 * n,
-                                       bf.P[k - 1] + (int64_t)b0 * Wk.ld_out, Wk.ld_out, s));
+                                       bf.P[k - 1] + (int64_t)b0 * Wk.ld_out, Wk.ld_out, c->lambda_rule, s));
       ++chunks;
     }
   }
@@ -966,6 +990,7 @@ vcr_status crown_impl(vcr_ctx *c, const float *x0, int32_t B, float eps, const f
     sp.ent_p = bf.ent_p;
     sp.flags = bf.flags;
     sp.n_invalid = c->d_counters + 64;
+    sp.lam_rule = c->lambda_rule;
     HIP_TRY(c, launch_split_prepare(sp, s));
     if (!by_arg) HIP_TRY(c, hipStreamSynchronize(s));   // hp must outlive its copy
   }
@@ -1050,13 +1075,15 @@ vcr_status vcr_crown_bounds(vcr_ctx *c, const float *x0, int32_t B, float eps, c
   if (st != VCR_OK) return st;
   if (splits) {
     if (B != 1) return fail(c, VCR_ERR_ARG, "splits need exactly one root input (B = 1)");
-    if (splits->n_domains <= 0 || splits->per_domain < 0 || splits->per_domain > 64)
+    if (splits->n_domains <= 0 || splits->per_domain < 0 || splits->per_domain > VCR_MAX_SPLITS)
       return fail(c, VCR_ERR_ARG, "bad split sizes (n_domains > 0, 0 <= per_domain <= 64)");
     if (splits->per_domain > 0 && (!splits->relu_id || !splits->neuron || !splits->sign))
       return fail(c, VCR_ERR_ARG, "null split array");
     if (c->relu_n.empty()) return fail(c, VCR_ERR_ARG, "splits need at least one ReLU");
     if ((int64_t)splits->n_domains * m > (int64_t)1 << 30) return fail(c, VCR_ERR_SHAPE, "n_domains * m too large");
   }
+  st = check_finite_inputs(c, x0, B, C, m);
+  if (st != VCR_OK) return st;
   auto run = [&]() {
     return c->graph ? graph_crown(c, x0, B, eps, C, m, splits, lb, ub) : crown_impl(c, x0, B, eps, C, m, splits, lb, ub);
   };
@@ -1066,7 +1093,8 @@ vcr_status vcr_crown_bounds(vcr_ctx *c, const float *x0, int32_t B, float eps, c
                                (uint64_t)(uintptr_t)C, (uint64_t)m, (uint64_t)(uintptr_t)lb, (uint64_t)(uintptr_t)ub,
                                (uint64_t)c->clip_on, (uint64_t)*reinterpret_cast<const uint32_t *>(&c->clip_lo),
                                (uint64_t)*reinterpret_cast<const uint32_t *>(&c->clip_hi), (uint64_t)c->intersect,
-                               c->ws_cap, c->net_epoch, (uint64_t)(uintptr_t)c->ws.base, (uint64_t)c->ws.cap};
+                               c->ws_cap, c->net_epoch, (uint64_t)(uintptr_t)c->ws.base, (uint64_t)c->ws.cap,
+                               (uint64_t)c->lambda_rule};
   if (c->gexec && key == c->gkey) {
     HIP_TRY(c, hipSetDevice(c->device));
     HIP_TRY(c, hipGraphLaunch(c->gexec, c->stream));
@@ -1116,6 +1144,8 @@ vcr_status vcr_ibp_bounds(vcr_ctx *c, const float *x0, int32_t B, float eps, con
   vcr_status st = check_common(c, x0, B, eps, C, m, lb, ub);
   if (st != VCR_OK) return st;
   if (c->device < 0) return fail(c, VCR_ERR_STATE, "validation-only context: no device work");
+  st = check_finite_inputs(c, x0, B, C, m);
+  if (st != VCR_OK) return st;
   if (c->graph) return after_call(c, graph_ibp(c, x0, B, eps, C, m, lb, ub), t0);
   HIP_TRY(c, hipSetDevice(c->device));
   const int L = (int)c->layers.size();
@@ -1173,6 +1203,8 @@ vcr_status vcr_alpha_crown_bounds(vcr_ctx *c, const float *x0, int32_t B, float 
   AlphaCall ac{o, 0};
   for (int32_t n : c->relu_n) ac.n_total += n;
   if ((int64_t)B * 2 * m * ac.n_total > ((int64_t)1 << 40)) return fail(c, VCR_ERR_SHAPE, "alpha tensors too large");
+  st = check_finite_inputs(c, x0, B, C, m);
+  if (st != VCR_OK) return st;
   return after_call(c, crown_impl(c, x0, B, eps, C, m, nullptr, lb, ub, &ac), t0);
 }
 
@@ -1181,7 +1213,7 @@ vcr_status vcr_alpha_crown_bounds(vcr_ctx *c, const float *x0, int32_t B, float 
 namespace {
 
 vcr_status check_splits(vcr_ctx *c, const vcr_splits *splits, int32_t m) {
-  if (splits->n_domains <= 0 || splits->per_domain < 0 || splits->per_domain > 64)
+  if (splits->n_domains <= 0 || splits->per_domain < 0 || splits->per_domain > VCR_MAX_SPLITS)
     return fail(c, VCR_ERR_ARG, "bad split sizes (n_domains > 0, 0 <= per_domain <= 64)");
   if (splits->per_domain > 0 && (!splits->relu_id || !splits->neuron || !splits->sign))
     return fail(c, VCR_ERR_ARG, "null split array");
@@ -1250,6 +1282,8 @@ vcr_status vcr_beta_crown_bounds(vcr_ctx *c, const float *x0, float eps, const f
   if (st != VCR_OK) return st;
   st = check_beta_opts(c, opts);
   if (st != VCR_OK) return st;
+  st = check_finite_inputs(c, x0, 1, C, m);
+  if (st != VCR_OK) return st;
   AlphaCall ac = alpha_call_of(c, *opts, true);
   return after_call(c, crown_impl(c, x0, 1, eps, C, m, splits, lb, ub, &ac), t0);
 }
@@ -1263,7 +1297,13 @@ vcr_status vcr_bab_verify(vcr_ctx *c, const float *x0, float eps, const float *C
   if (c->graph) return fail(c, VCR_ERR_UNSUPPORTED, "branch and bound is built for networks of dense and relu nodes");
   if (c->relu_n.empty()) return fail(c, VCR_ERR_ARG, "branch and bound needs at least one ReLU");
   if (opts->batch < 1 || opts->max_rounds < 0) return fail(c, VCR_ERR_ARG, "batch must be >= 1, max_rounds >= 0");
+  // a subdomain gains one split per round, and the split table holds VCR_MAX_SPLITS
+  if (opts->max_rounds > VCR_MAX_SPLITS)
+    return fail(c, VCR_ERR_ARG, "max_rounds %d exceeds %d: a subdomain would hold more splits than the table",
+                opts->max_rounds, VCR_MAX_SPLITS);
   if (m <= 0 || !x0 || !C) return fail(c, VCR_ERR_ARG, "bad property");
+  if (!(eps >= 0.f) || !std::isfinite(eps)) return fail(c, VCR_ERR_ARG, "eps must be finite and >= 0");
+  if (!aligned16(x0) || !aligned16(C)) return fail(c, VCR_ERR_ARG, "tensor pointers must be 16-byte aligned");
   vcr_status st = check_beta_opts(c, &opts->bound);
   if (st != VCR_OK) return st;
   const int R = (int)c->relu_n.size();
@@ -1274,6 +1314,8 @@ vcr_status vcr_bab_verify(vcr_ctx *c, const float *x0, float eps, const float *C
         opts->order_neuron[k] >= c->relu_n[opts->order_relu[k]])
       return fail(c, VCR_ERR_ARG, "split order entry %d out of range", k);
   if (c->device < 0) return fail(c, VCR_ERR_STATE, "validation-only context: no device work");
+  st = check_finite_inputs(c, x0, 1, C, m);
+  if (st != VCR_OK) return st;
   HIP_TRY(c, hipSetDevice(c->device));
   hipStream_t s = c->stream;
   *res = vcr_bab_result{};

@@ -96,10 +96,10 @@ hipError_t launch_row_table(int4 *rows, int64_t R, int32_t rows_per_unit, int32_
                             int32_t windowed, int32_t unit0, hipStream_t s);
 hipError_t launch_finalize_conv(const float *beta, int32_t B, int32_t C, int32_t H, const float *ibp_c,
                                 const float *ibp_r, int64_t ld_ibp, int32_t intersect, const float *bias_next,
-                                float *L, float *U, float4 *P, hipStream_t s);
+                                float *L, float *U, float4 *P, int32_t lam_rule, hipStream_t s);
 hipError_t launch_conv_layer_from_ibp(const float *ibp_c, const float *ibp_r, int64_t ld_ibp, int32_t B, int32_t C,
                                       int32_t H, const float *bias_next, float *L, float *U, float4 *P,
-                                      hipStream_t s);
+                                      int32_t lam_rule, hipStream_t s);
 hipError_t launch_ibp_conv(const float *W, const float *bias, int32_t Co, int32_t Ci, int32_t Hin, int32_t Hout,
                            int32_t stride, int32_t pad, const float *cin, const float *rin, int64_t ld_in,
                            float *cout, float *rout, int64_t ld_out, int32_t B, hipStream_t s);

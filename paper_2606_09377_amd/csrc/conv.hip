@@ -25,6 +25,7 @@
 //                                 identity (1, 1, 0, b[ci]) when the node is not a ReLU
 // and reduces the constants over the tile's columns into one partial per GEMM row.
 #include "conv.h"
+#include "relax.h"
 
 #include <algorithm>
 #include <vector>
@@ -838,7 +839,7 @@ hipError_t launch_row_table(int4 *rows, int64_t R, int32_t rows_per_unit, int32_
 // relaxation is stored channels-last [b][y][x][c] for the windowed epilogues above.
 __global__ void k_finalize_conv(const float *beta, int32_t B, int32_t C, int32_t H, const float *ibp_c,
                                 const float *ibp_r, int64_t ld_ibp, int32_t intersect, const float *bias_next,
-                                float *L, float *U, float4 *P) {
+                                float *L, float *U, float4 *P, int32_t rule) {
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t n = (int64_t)C * H * H;
   if (idx >= B * n) return;
@@ -853,30 +854,24 @@ __global__ void k_finalize_conv(const float *beta, int32_t B, int32_t C, int32_t
   L[idx] = l;
   U[idx] = u;
   const int c = (int)(q / (H * H)), hw = (int)(q % (H * H));
-  float4 prm;
-  if (u <= 0.f) prm = make_float4(0.f, 0.f, 0.f, 0.f);
-  else if (l >= 0.f) prm = make_float4(1.f, 1.f, 0.f, 0.f);
-  else {
-    const float s = u / (u - l);
-    prm = make_float4(u > -l ? 1.f : 0.f, s, -s * l, 0.f);
-  }
-  prm.w = bias_next ? bias_next[c] : 0.f;
+  const float4 prm = relax_params(l, u, bias_next ? bias_next[c] : 0.f, rule);
   P[(b * H * H + hw) * C + c] = prm;
 }
 
 hipError_t launch_finalize_conv(const float *beta, int32_t B, int32_t C, int32_t H, const float *ibp_c,
                                 const float *ibp_r, int64_t ld_ibp, int32_t intersect, const float *bias_next,
-                                float *L, float *U, float4 *P, hipStream_t s) {
+                                float *L, float *U, float4 *P, int32_t lam_rule, hipStream_t s) {
   const int64_t tot = (int64_t)B * C * H * H;
   hipLaunchKernelGGL(k_finalize_conv, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, beta, B, C, H, ibp_c,
-                     ibp_r, ld_ibp, intersect, bias_next, L, U, P);
+                     ibp_r, ld_ibp, intersect, bias_next, L, U, P, lam_rule);
   return hipGetLastError();
 }
 
 // A ReLU layer whose input is one convolution of the network input: its exact range over
 // the box is the IBP interval [c - r, c + r]; relaxation stored channels-last.
 __global__ void k_conv_layer_from_ibp(const float *ibp_c, const float *ibp_r, int64_t ld_ibp, int32_t B, int32_t C,
-                                      int32_t H, const float *bias_next, float *L, float *U, float4 *P) {
+                                      int32_t H, const float *bias_next, float *L, float *U, float4 *P,
+                                      int32_t rule) {
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t n = (int64_t)C * H * H;
   if (idx >= B * n) return;
@@ -886,23 +881,16 @@ __global__ void k_conv_layer_from_ibp(const float *ibp_c, const float *ibp_r, in
   L[idx] = l;
   U[idx] = u;
   const int c = (int)(q / (H * H)), hw = (int)(q % (H * H));
-  float4 prm;
-  if (u <= 0.f) prm = make_float4(0.f, 0.f, 0.f, 0.f);
-  else if (l >= 0.f) prm = make_float4(1.f, 1.f, 0.f, 0.f);
-  else {
-    const float s = u / (u - l);
-    prm = make_float4(u > -l ? 1.f : 0.f, s, -s * l, 0.f);
-  }
-  prm.w = bias_next[c];
+  const float4 prm = relax_params(l, u, bias_next[c], rule);
   P[(b * H * H + hw) * C + c] = prm;
 }
 
 hipError_t launch_conv_layer_from_ibp(const float *ibp_c, const float *ibp_r, int64_t ld_ibp, int32_t B, int32_t C,
                                       int32_t H, const float *bias_next, float *L, float *U, float4 *P,
-                                      hipStream_t s) {
+                                      int32_t lam_rule, hipStream_t s) {
   const int64_t tot = (int64_t)B * C * H * H;
   hipLaunchKernelGGL(k_conv_layer_from_ibp, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, ibp_c, ibp_r,
-                     ld_ibp, B, C, H, bias_next, L, U, P);
+                     ld_ibp, B, C, H, bias_next, L, U, P, lam_rule);
   return hipGetLastError();
 }
 

@@ -49,12 +49,14 @@ struct vcr_ctx {
   int32_t intersect = 1;
   uint64_t ws_cap = 0;
   int32_t sync_check = 0;
+  int32_t check_finite = 0;
+  int32_t lambda_rule = 0;          // VCR_OPT_LAMBDA_RULE (relax.h)
   // network
   bool loaded = false;
   int32_t n0 = 0;
   std::vector<DenseLayer> layers;   // the MLP chain
   std::vector<int32_t> relu_n;      // neurons per ReLU node
-  std::vector<vcr_node> node_desc;  // validated node list (weights not retained)
+  int32_t n_out = 0;                // outputs of the loaded network (the last dense node)
   // workspace
   Workspace ws;
   uint64_t peak_ws = 0;
@@ -62,7 +64,7 @@ struct vcr_ctx {
   // last call
   int32_t last_B = 0;
   std::vector<float *> lastL, lastU;
-  int32_t *d_counters = nullptr;    // [64] unstable counts + [1] invalid domains
+  int32_t *d_counters = nullptr;    // [0, 64) unstable counts, [64] invalid domains, [65] non-finite inputs
   // branch-and-bound loop: device split arrays and bounds of one round (outside the
   // workspace, which every bounding call carves anew)
   void *bab_buf = nullptr;
@@ -160,3 +162,4 @@ T *take(vcr_ctx *c, size_t count) {
 }
 
 vcr_status ensure_ws(vcr_ctx *c, size_t bytes);
+

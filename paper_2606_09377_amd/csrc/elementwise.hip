@@ -3,24 +3,15 @@
 // pass, the fixed-order row reductions that finish a bound, and the split table of
 // branch-and-bound subdomains.
 //
-// Relaxation parameters of a ReLU on [l, u] are packed as float4 (lam, s, t, b):
-//   u <= 0 : (0, 0, 0)  inactive;   l >= 0 : (1, 1, 0)  active;
-//   else   : s = u / (u - l), t = -s l, lam = 1 if u > -l else 0;
-// and b is the bias of the dense layer that produces the ReLU's input, which the
+// Relaxation parameters of a ReLU on [l, u] are packed as float4 (lam, s, t, b) (relax.h),
+// b being the bias of the dense layer that produces the ReLU's input, which the
 // backward pass adds next.  All reductions run in a fixed order (sequential or a fixed
 // butterfly), so every bound is reproducible bit for bit and independent of batching.
 #include "kernels.h"
+#include "relax.h"
+#include "../../include/vcrown.h"
 
 namespace vcr {
-
-__device__ __forceinline__ float4 relax_params(float l, float u, float bias) {
-  if (u <= 0.f) return make_float4(0.f, 0.f, 0.f, bias);
-  if (l >= 0.f) return make_float4(1.f, 1.f, 0.f, bias);
-  const float s = u / (u - l);
-  const float t = -s * l;
-  const float lam = (u > -l) ? 1.f : 0.f;
-  return make_float4(lam, s, t, bias);
-}
 
 __device__ __forceinline__ float wave_sum(float x) {
   // fixed butterfly over the 64 lanes of a wavefront
@@ -247,7 +238,7 @@ hipError_t launch_ibp_dense(const float *Wp, int64_t ldw, const float *b, int32_
 // First ReLU layer: its pre-activation is one affine map of the input, whose exact range
 // over the box is the IBP interval [c - r, c + r].
 __global__ void k_layer_from_ibp(const float *c, const float *r, int64_t ld, int32_t n, int32_t B,
-                                 const float *bias, float *L, float *U, float4 *P, int64_t ldp) {
+                                 const float *bias, float *L, float *U, float4 *P, int64_t ldp, int32_t rule) {
   // one thread per (input, column) of P, padding columns included (they get zeros)
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= (int64_t)B * ldp) return;
@@ -260,16 +251,16 @@ __global__ void k_layer_from_ibp(const float *c, const float *r, int64_t ld, int
   const float l = cc - rr, u = cc + rr;
   L[b * n + i] = l;
   U[b * n + i] = u;
-  P[idx] = relax_params(l, u, bias[i]);
+  P[idx] = relax_params(l, u, bias[i], rule);
 }
 
 hipError_t launch_layer_from_ibp(const float *c, const float *r, int64_t ld, int32_t n, int32_t B,
                                  const float *bias, float *L, float *U, float4 *P, int64_t ldp,
-                                 hipStream_t s) {
+                                 int32_t lam_rule, hipStream_t s) {
   if (ldp < n) return hipErrorInvalidValue;
   const int64_t tot = (int64_t)B * ldp;
   hipLaunchKernelGGL(k_layer_from_ibp, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, c, r, ld, n, B,
-                     bias, L, U, P, ldp);
+                     bias, L, U, P, ldp, lam_rule);
   return hipGetLastError();
 }
 
@@ -467,7 +458,7 @@ hipError_t launch_rowsum(float *beta, const float *part, int32_t n_parts, int32_
 __global__ void k_finalize_layer(const float *beta, const float *cpart, int32_t n_parts, int32_t M_pad,
                                  int32_t B, int32_t n, const float *ibp_c, const float *ibp_r, int64_t ld_ibp,
                                  int32_t intersect, const float *bias_next, float *L, float *U, float4 *P,
-                                 int64_t ldp) {
+                                 int64_t ldp, int32_t rule) {
   // one thread per (input, column) of P, padding columns included (they get zeros)
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= (int64_t)B * ldp) return;
@@ -491,17 +482,17 @@ __global__ void k_finalize_layer(const float *beta, const float *cpart, int32_t 
   }
   L[b * n + i] = l;
   U[b * n + i] = u;
-  P[idx] = relax_params(l, u, bias_next[i]);
+  P[idx] = relax_params(l, u, bias_next[i], rule);
 }
 
 hipError_t launch_finalize_layer(const float *beta, const float *cpart, int32_t n_parts, int32_t M_pad,
                                  int32_t B, int32_t n, const float *ibp_c, const float *ibp_r,
                                  int64_t ld_ibp, int32_t intersect, const float *bias_next,
-                                 float *L, float *U, float4 *P, int64_t ldp, hipStream_t s) {
+                                 float *L, float *U, float4 *P, int64_t ldp, int32_t lam_rule, hipStream_t s) {
   if (ldp < n) return hipErrorInvalidValue;
   const int64_t tot = (int64_t)B * ldp;
   hipLaunchKernelGGL(k_finalize_layer, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, beta, cpart,
-                     n_parts, M_pad, B, n, ibp_c, ibp_r, ld_ibp, intersect, bias_next, L, U, P, ldp);
+                     n_parts, M_pad, B, n, ibp_c, ibp_r, ld_ibp, intersect, bias_next, L, U, P, ldp, lam_rule);
   return hipGetLastError();
 }
 
@@ -614,7 +605,7 @@ hipError_t launch_finalize_spec(const float *beta, const float *cpart, int32_t n
 // One thread per domain validates its entries, clamps each split neuron's root interval
 // (active: l <- max(l, 0); inactive: u <- min(u, 0)), marks the domain infeasible if an
 // interval becomes empty, and stores the entries sorted by ReLU with their relaxation.
-constexpr int MAX_SPLITS = 64;
+constexpr int MAX_SPLITS = VCR_MAX_SPLITS;   // split slots per subdomain (the ABI limit)
 
 __global__ void k_split_prepare(const SplitPrepArgs a) {
   const int d = blockIdx.x * blockDim.x + threadIdx.x;
@@ -671,7 +662,7 @@ __global__ void k_split_prepare(const SplitPrepArgs a) {
       u = fminf(u, 0.f);
     if (l > u) infeasible = true;
     a.ent_n[(int64_t)d * a.S + k] = en[k];
-    float4 q = relax_params(l, u, 0.f);
+    float4 q = relax_params(l, u, 0.f, a.lam_rule);
     q.w = es[k] > 0 ? -1.f : 1.f;   // sign of the split's Lagrangian term
     a.ent_p[(int64_t)d * a.S + k] = q;
   }
@@ -704,6 +695,27 @@ __global__ void k_count_unstable(const float *L, const float *U, int64_t n, int3
 hipError_t launch_count_unstable(const float *L, const float *U, int64_t n, int32_t *count, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_count_unstable, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, L, U, n, count);
+  return hipGetLastError();
+}
+
+// Non-finite values (NaN, +-inf) among n floats, added to *count (the VCR_OPT_CHECK_FINITE
+// scan of a call's inputs).  One atomic per workgroup that found any.
+__global__ void k_count_nonfinite(const float *p, int64_t n, int32_t *count) {
+  __shared__ int32_t blk;
+  if (threadIdx.x == 0) blk = 0;
+  __syncthreads();
+  int32_t mine = 0;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    mine += isfinite(p[i]) ? 0 : 1;
+  if (mine) atomicAdd(&blk, mine);
+  __syncthreads();
+  if (threadIdx.x == 0 && blk) atomicAdd(count, blk);
+}
+
+hipError_t launch_count_nonfinite(const float *p, int64_t n, int32_t *count, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int64_t blocks = std::min<int64_t>((n + 255) / 256, 4096);
+  hipLaunchKernelGGL(k_count_nonfinite, dim3((unsigned)blocks), dim3(256), 0, s, p, n, count);
   return hipGetLastError();
 }
 

@@ -878,13 +878,10 @@ vcr_status run_pass(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &pp, int 
 
 }  // namespace
 
-vcr_status graph_crown(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m,
-                       const vcr_splits *splits, float *lb, float *ub) {
+// Inputs per chunk and workspace bytes of a CROWN call of B inputs: the whole batch, halved
+// until the plan fits the workspace cap (VCR_ERR_OOM when one input does not).
+vcr_status graph_plan(vcr_ctx *c, int32_t B, int32_t m, int *chunk_out, size_t *bytes_out) {
   GraphNet *g = c->graph;
-  if (splits) return fail(c, VCR_ERR_UNSUPPORTED, "subdomain splits are built for MLPs only");
-  const int nn = (int)g->nodes.size();
-  const GNode &out = g->nodes[nn - 1];
-  // plan the chunking
   int chunk = B;
   Workspace probe;
   GBufs tmp;
@@ -899,6 +896,21 @@ vcr_status graph_crown(vcr_ctx *c, const float *x0, int32_t B, float eps, const 
       return fail(c, VCR_ERR_OOM, "workspace cap %llu bytes is below the minimum plan (%llu bytes)",
                   (unsigned long long)c->ws_cap, (unsigned long long)need);
   }
+  *chunk_out = chunk;
+  *bytes_out = need;
+  return VCR_OK;
+}
+
+vcr_status graph_crown(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m,
+                       const vcr_splits *splits, float *lb, float *ub) {
+  GraphNet *g = c->graph;
+  if (splits) return fail(c, VCR_ERR_UNSUPPORTED, "subdomain splits are built for MLPs only");
+  const int nn = (int)g->nodes.size();
+  const GNode &out = g->nodes[nn - 1];
+  int chunk = B;
+  size_t need = 0;
+  vcr_status st = graph_plan(c, B, m, &chunk, &need);
+  if (st != VCR_OK) return st;
   if (c->device < 0) {
     c->chunks_last = (int)g->passes.size() * ((B + chunk - 1) / chunk);
     return fail(c, VCR_ERR_STATE, "validation-only context: no device work");
@@ -906,7 +918,7 @@ vcr_status graph_crown(vcr_ctx *c, const float *x0, int32_t B, float eps, const 
   HIP_TRY(c, hipSetDevice(c->device));
   c->lastL.clear();
   c->lastU.clear();
-  vcr_status st = ensure_ws(c, need);
+  st = ensure_ws(c, need);
   if (st != VCR_OK) return st;
   GBufs bf;
   carve_graph(c, g, c->ws, B, m, chunk, &bf);
@@ -926,10 +938,10 @@ vcr_status graph_crown(vcr_ctx *c, const float *x0, int32_t B, float eps, const 
       const int64_t ldz = ld_of(z.numel);
       if (!z.flat)
         HIP_TRY(c, launch_conv_layer_from_ibp(bf.ic[pp.start], bf.ir[pp.start], ldz, B, z.C, z.H, z.b, bf.L[ri],
-                                              bf.U[ri], bf.P[ri], s));
+                                              bf.U[ri], bf.P[ri], c->lambda_rule, s));
       else
         HIP_TRY(c, launch_layer_from_ibp(bf.ic[pp.start], bf.ir[pp.start], ldz, (int32_t)z.numel, B, z.b, bf.L[ri],
-                                         bf.U[ri], bf.P[ri], ldz, s));
+                                         bf.U[ri], bf.P[ri], ldz, c->lambda_rule, s));
       continue;
     }
     for (int u0 = 0; u0 < B; u0 += chunk) {
@@ -945,12 +957,12 @@ vcr_status graph_crown(vcr_ctx *c, const float *x0, int32_t B, float eps, const 
           HIP_TRY(c, launch_finalize_conv(bf.beta, units, z.C, z.H, bf.ic[pp.start] + (int64_t)u0 * ldz,
                                           bf.ir[pp.start] + (int64_t)u0 * ldz, ldz, c->intersect,
                                           z.b, bf.L[ri] + (int64_t)u0 * z.numel, bf.U[ri] + (int64_t)u0 * z.numel,
-                                          bf.P[ri] + (int64_t)u0 * z.numel, s));
+                                          bf.P[ri] + (int64_t)u0 * z.numel, c->lambda_rule, s));
         } else {
           HIP_TRY(c, launch_finalize_layer(bf.beta, nullptr, 0, 0, units, (int32_t)z.numel,
                                            bf.ic[pp.start] + (int64_t)u0 * ldz, bf.ir[pp.start] + (int64_t)u0 * ldz,
                                            ldz, c->intersect, z.b, bf.L[ri] + (int64_t)u0 * z.numel,
-                                           bf.U[ri] + (int64_t)u0 * z.numel, bf.P[ri] + (int64_t)u0 * ldz, ldz, s));
+                                           bf.U[ri] + (int64_t)u0 * z.numel, bf.P[ri] + (int64_t)u0 * ldz, ldz, c->lambda_rule, s));
         }
       } else {
         HIP_TRY(c, launch_finalize_spec(bf.beta, nullptr, 0, 0, units, m, nullptr, lb + (int64_t)u0 * m,

@@ -91,9 +91,10 @@ hipError_t launch_box(const float *x0, int32_t B, int32_t n0, int64_t ld0, float
 hipError_t launch_ibp_dense(const float *Wp, int64_t ldw, const float *b, int32_t n_out, int32_t n_in,
                             const float *cin, const float *rin, int64_t ld_in, int32_t relu_in,
                             float *cout, float *rout, int64_t ld_out, int32_t B, hipStream_t s);
+// lam_rule: the lower-slope rule of unstable neurons (VCR_OPT_LAMBDA_RULE values, relax.h)
 hipError_t launch_layer_from_ibp(const float *c, const float *r, int64_t ld, int32_t n, int32_t B,
                                  const float *bias, float *L, float *U, float4 *P, int64_t ldp,
-                                 hipStream_t s);
+                                 int32_t lam_rule, hipStream_t s);
 struct InitArgs {
   const float *src;      // source rows (W_k, or C W_L per input)
   int64_t ld_src;
@@ -121,7 +122,7 @@ hipError_t launch_rowsum(float *beta, const float *part, int32_t n_parts, int32_
 hipError_t launch_finalize_layer(const float *beta, const float *cpart, int32_t n_parts, int32_t M_pad,
                                  int32_t B, int32_t n, const float *ibp_c, const float *ibp_r,
                                  int64_t ld_ibp, int32_t intersect, const float *bias_next,
-                                 float *L, float *U, float4 *P, int64_t ldp, hipStream_t s);
+                                 float *L, float *U, float4 *P, int64_t ldp, int32_t lam_rule, hipStream_t s);
 hipError_t launch_spec_cw(const float *C, int32_t B, int32_t m, int32_t n_out, const float *Wp,
                           int64_t ldw, const float *b, int32_t n_in, float *CW, int64_t ld_cw,
                           float *Cb, hipStream_t s);
@@ -143,9 +144,11 @@ struct SplitPrepArgs {
   float4 *ent_p;             // [D][S]
   int32_t *flags;            // [D] 0 ok, 1 infeasible, 2 invalid
   int32_t *n_invalid;        // one counter
+  int32_t lam_rule;          // lower-slope rule of unstable neurons (relax.h)
 };
 hipError_t launch_split_prepare(const SplitPrepArgs &a, hipStream_t s);
 hipError_t launch_count_unstable(const float *L, const float *U, int64_t n, int32_t *count, hipStream_t s);
+hipError_t launch_count_nonfinite(const float *p, int64_t n, int32_t *count, hipStream_t s);
 hipError_t launch_copy(float *dst, const float *src, int64_t n, hipStream_t s);
 // dst[i] = ptrs[i] for i < n <= PTR_TABLE_MAX, the table travelling as a kernel argument (no
 // host buffer has to outlive the launch)

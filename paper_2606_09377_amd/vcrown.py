@@ -21,7 +21,10 @@ VCR_OK, VCR_ERR_ARG, VCR_ERR_SHAPE, VCR_ERR_STATE, VCR_ERR_OOM, VCR_ERR_DEVICE, 
 STATUS_NAMES = ["OK", "ERR_ARG", "ERR_SHAPE", "ERR_STATE", "ERR_OOM", "ERR_DEVICE", "ERR_UNSUPPORTED"]
 OPS = {"dense": 0, "conv2d": 1, "relu": 2, "add": 3, "flatten": 4}
 (OPT_CLIP_ENABLE, OPT_CLIP_LO, OPT_CLIP_HI, OPT_INTERSECT_IBP, OPT_WORKSPACE_CAP_BYTES, OPT_SYNC_CHECK,
- OPT_TIME_GEMM, OPT_GRAPH) = range(1, 9)
+ OPT_TIME_GEMM, OPT_GRAPH, OPT_CHECK_FINITE, OPT_LAMBDA_RULE) = range(1, 11)
+# values of OPT_LAMBDA_RULE (the lower slope of unstable ReLU neurons)
+LAMBDA_RULES = {"adaptive": 0, "zero": 1, "one": 2, "same_slope": 3}
+MAX_SPLITS = 64   # VCR_MAX_SPLITS
 
 
 class VcrNode(ctypes.Structure):

@@ -194,3 +194,37 @@ def test_alpha_beta_bab_argument_validation(vc):
     assert bab(order=[(0, 3), (1, 29)]) == vc.VCR_ERR_STATE
     assert bab(batch=0) == vc.VCR_ERR_ARG and bab(rounds=-1) == vc.VCR_ERR_ARG
     assert bab(order=[(2, 0)]) == vc.VCR_ERR_ARG and bab(order=[(1, 30)]) == vc.VCR_ERR_ARG
+
+
+def test_option_values_and_round_limit(vc):
+    """The lambda rule takes the four VCR_LAMBDA_* values only; CHECK_FINITE is a flag; the
+    branch-and-bound loop rejects more rounds than a subdomain has split slots (one split
+    per round) before any device work."""
+    ctx = vc.Ctx(-1)
+    wl = random_mlp(3, [20, 30, 30, 5], 1, 0.1)
+    ctx.load_net(wl.net)
+    for v in vc.LAMBDA_RULES.values():
+        ctx.set_option(vc.OPT_LAMBDA_RULE, v)
+    for v in (-1, 4, 0.5):
+        with pytest.raises(vc.VcrError) as e:
+            ctx.set_option(vc.OPT_LAMBDA_RULE, v)
+        assert e.value.status == vc.VCR_ERR_ARG
+    ctx.set_option(vc.OPT_CHECK_FINITE, 1)
+    ctx.set_option(vc.OPT_CHECK_FINITE, 0)
+    lib = ctx.lib
+    x, C = _buf(20), _buf(4 * 5)
+    p = lambda a: ctypes.c_void_p(a.ctypes.data)  # noqa: E731
+
+    def bab(rounds):
+        bo = vc.VcrBetaOpts(5, 0.1, 0.05, 0.9, 0.999, 1e-8, None, None)
+        o = vc.VcrBabOpts(4, rounds, bo, None, None, 0)
+        res = vc.VcrBabResult()
+        return lib.vcr_bab_verify(ctx.h, p(x), ctypes.c_float(0.1), p(C), 4, ctypes.byref(o), ctypes.byref(res), None)
+
+    assert bab(vc.MAX_SPLITS) == vc.VCR_ERR_STATE
+    assert bab(vc.MAX_SPLITS + 1) == vc.VCR_ERR_ARG
+    assert "max_rounds" in lib.vcr_last_error(ctx.h).decode()
+    # per_domain beyond the split slots
+    rid, neu, sg = _buf(4 * 65, np.int32), _buf(4 * 65, np.int32), _buf(4 * 65, np.int8)
+    sp = vc.VcrSplits(4, vc.MAX_SPLITS + 1, rid.ctypes.data, neu.ctypes.data, sg.ctypes.data)
+    assert _call(vc, ctx, 1, 0.1, 4, 20, 5, splits=sp) == vc.VCR_ERR_ARG
