@@ -2,8 +2,9 @@
 
 A step is one vcr_crown_bounds call over one batch of seeded synthetic inputs that are
 already resident in HBM: the IBP pass, every intermediate layer's backward A-matrix pass,
-the ReLU relaxations and the final spec pass.  Default workload: the 784-1024x6-10 ReLU
-MLP, 64 inputs, eps = 0.015, 9 margin rows per input.
+the ReLU relaxations and the final spec pass.  Default workload: the wide ReLU MLP
+3072-8192x4-100 (the width of the paper's Table 4 at h = 8192), 16 inputs, eps = 2/255,
+99 margin rows per input, with its 8192 x 8192 A matrices held whole (146.6 TFLOP per call).
 
 Prints one JSON line with the throughput (inputs/s), the dominant kernel's roofline
 (the backward-step fp32 MFMA GEMM, timed with HIP events on the stream it runs on) and the
@@ -51,10 +52,31 @@ def traffic_for(kernel, workload):
     return None if w is None else w.get("bytes_per_launch")
 
 
+def host_info():
+    """The host the oracle runs on: CPU model, logical CPUs and numpy's BLAS thread pools."""
+    import threadpoolctl
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    pools = [{k: p.get(k) for k in ("user_api", "internal_api", "num_threads", "version", "threading_layer")}
+             for p in threadpoolctl.threadpool_info()]
+    return {"cpu_model": model, "cpu_count": os.cpu_count(), "threadpool_info": pools}
+
+
+def _threads():
+    import threadpoolctl
+    return int(max((p.get("num_threads", 1) for p in threadpoolctl.threadpool_info()), default=1))
+
+
 def cpu_baseline(wl, budget_s, alpha_iters=0):
     """The fp64 oracle, as it stands, on the first inputs of the same batch until the time
     budget is used (at least one input); with alpha_iters the alpha-CROWN oracle."""
-    import threadpoolctl
     import oracle
     from oracle import alpha64
     t0 = time.perf_counter()
@@ -71,38 +93,54 @@ def cpu_baseline(wl, budget_s, alpha_iters=0):
         if time.perf_counter() - t0 >= budget_s:
             break
     dt = time.perf_counter() - t0
-    threads = max((p.get("num_threads", 1) for p in threadpoolctl.threadpool_info()), default=1)
-    return {"value": n / dt, "unit": "inputs/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"first {n} of the {wl.x0.shape[0]} inputs of the same batch, {dt:.1f} s",
-            "cpu_count": os.cpu_count()}
+    return {"value": n / dt, "unit": "inputs/s", "cores": _threads(), "kind": "oracle",
+            "sample": f"first {n} of the {wl.x0.shape[0]} inputs of the same batch, {dt:.1f} s", **host_info()}
 
 
-def cpu_baseline_sampled(wl, budget_s):
-    """The fp64 oracle takes hours per input of the full ResNet, so its time per input is
-    estimated from a timed sample: for every ReLU layer and for the spec rows, one chunk of
-    rows goes through the oracle's backward pass and concretization (lower and upper), and
-    the per-row time is scaled to the layer's row count.  The cost of a row does not depend
-    on the relaxation values, so the sample uses the IBP bounds' relaxation."""
-    import threadpoolctl
+def cpu_baseline_sampled(wl, budget_s, chunk):
+    """One input of the wide MLP or the full ResNet takes the fp64 oracle minutes to hours,
+    so its time per input is estimated from a timed sample of the oracle's own steps on
+    input 0: the box, the IBP pass and a first ReLU on an affine map of the input run whole;
+    for every other ReLU layer and for the spec rows, chunks of `chunk` rows go through the
+    oracle's backward pass and concretization (lower and upper), as the oracle processes
+    them, until that layer's share of the budget is used, and the per-row time is scaled to
+    the layer's row count.  The cost of a row does not depend on the relaxation values, so
+    the sample uses the IBP bounds' relaxation."""
     import oracle
     net = wl.net
     shapes = oracle.node_shapes(net)
+    t0 = time.perf_counter()
     lo, hi = oracle.input_box(wl.x0[0], wl.eps, wl.clip)
     IL, IU = oracle.ibp(net, lo, hi)
     relus = [i for i, nd in enumerate(net.nodes) if nd.op == "relu"]
     relax = {i: oracle.relu_relaxation(IL[net.nodes[i].in0].reshape(-1), IU[net.nodes[i].in0].reshape(-1))
              for i in relus}
-    per_layer = max(budget_s / (len(relus) + 1), 0.5)
-    total, parts = 0.0, []
+    total = time.perf_counter() - t0
+    parts = [f"box and IBP {total:.1f} s"]
     starts = [(net.nodes[i].in0, int(np.prod(shapes[net.nodes[i].in0]))) for i in relus]
     starts.append((len(net.nodes) - 1, wl.C.shape[1]))
+    per_layer = max(budget_s / len(starts), 0.5)
     for k, (z, n_rows) in enumerate(starts):
         n = int(np.prod(shapes[z]))
+        nd = net.nodes[z]
         t0 = time.perf_counter()
+        if k < len(relus) and nd.op == "dense" and nd.in0 == -1:
+            # the oracle bounds an affine map of the input directly from W, b
+            W, b = nd.W.astype(np.float64), nd.b.astype(np.float64)
+            oracle.concretize(W, b, lo, hi, False)
+            oracle.concretize(W, b, lo, hi, True)
+            dt = time.perf_counter() - t0
+            total += dt
+            parts.append(f"node {z} (affine map of the input) whole in {dt:.1f} s")
+            continue
         done = 0
-        while done < min(n_rows, 256) and (done == 0 or time.perf_counter() - t0 < per_layer):
-            rows = min(16, n_rows - done)
-            A = wl.C[0][done:done + rows].astype(np.float64) if k == len(relus) else np.eye(n)[done:done + rows]
+        while done < n_rows and (done == 0 or time.perf_counter() - t0 < per_layer):
+            rows = min(chunk, n_rows - done)
+            if k == len(relus):
+                A = wl.C[0][done:done + rows].astype(np.float64)
+            else:
+                A = np.zeros((rows, n))
+                A[np.arange(rows), np.arange(done, done + rows)] = 1.0
             zero = np.zeros(rows)
             for up in (False, True):
                 Ax, bx = oracle.backward(net, shapes, relax, z, A, zero, upper=up)
@@ -111,16 +149,14 @@ def cpu_baseline_sampled(wl, budget_s):
         dt = time.perf_counter() - t0
         total += dt / done * n_rows
         parts.append(f"{done}/{n_rows} rows of node {z} in {dt:.1f} s")
-    threads = max((p.get("num_threads", 1) for p in threadpoolctl.threadpool_info()), default=1)
-    return {"value": 1.0 / total, "unit": "inputs/s", "cores": int(threads), "kind": "oracle",
-            "sample": "estimated from timed row chunks of input 0, scaled to each layer's rows: " + "; ".join(parts)
-                      + f"; {total:.0f} s per input", "cpu_count": os.cpu_count()}
+    return {"value": 1.0 / total, "unit": "inputs/s", "cores": _threads(), "kind": "oracle",
+            "sample": f"estimated from timed steps of input 0 ({chunk}-row chunks), scaled to each layer's rows: "
+                      + "; ".join(parts) + f"; {total:.0f} s per input", **host_info()}
 
 
 def cpu_baseline_bab(wl, sp, budget_s):
     """The fp64 oracle on the same subdomains: its root pass, then domains until the time
     budget is used; reported as domains/s of the domain evaluations plus the root pass."""
-    import threadpoolctl
     import oracle
     from workloads import Splits
     splits = Splits(sp["relu_id"], sp["neuron"], sp["sign"])
@@ -134,11 +170,15 @@ def cpu_baseline_bab(wl, sp, budget_s):
         n += 16
     t_dom = time.perf_counter() - t1
     total = t_root + t_dom * splits.n_domains / n
-    threads = max((p.get("num_threads", 1) for p in threadpoolctl.threadpool_info()), default=1)
-    return {"value": splits.n_domains / total, "unit": "domains/s", "cores": int(threads), "kind": "oracle",
+    return {"value": splits.n_domains / total, "unit": "domains/s", "cores": _threads(), "kind": "oracle",
             "sample": f"root pass ({t_root:.1f} s) + first {n} of {splits.n_domains} domains ({t_dom:.1f} s), "
-                      f"domain time scaled to all domains", "cpu_count": os.cpu_count()}
+                      f"domain time scaled to all domains", **host_info()}
 
+
+# workloads whose oracle time per input is estimated from a timed sample (row chunk size):
+# the oracle's own 256-row chunks for the wide MLP, 16 rows of the ResNet's dense coefficient
+# tensors (up to 65536 columns per row)
+SAMPLED_BASELINE = {"mlp3072x8192x4": 256, "resnet3x32x32": 16}
 
 BAB_ROUNDS, BAB_ITERS = 10, 20
 
@@ -146,7 +186,6 @@ BAB_ROUNDS, BAB_ITERS = 10, 20
 def cpu_baseline_bab_loop(wl, batch, budget_s):
     """The oracle's beta-CROWN on the subdomains the loop bounds first (the same loop, with
     the oracle's own split order), until the time budget is used; subdomains per second."""
-    import threadpoolctl
     import oracle
     from oracle import beta64
     root = oracle.crown(wl.net, wl.x0[0], wl.eps, wl.C[0])
@@ -168,10 +207,9 @@ def cpu_baseline_bab_loop(wl, batch, budget_s):
             if time.perf_counter() - t0 >= budget_s:
                 break
     dt = time.perf_counter() - t0
-    threads = max((p.get("num_threads", 1) for p in threadpoolctl.threadpool_info()), default=1)
-    return {"value": n / dt, "unit": "domains/s", "cores": int(threads), "kind": "oracle",
+    return {"value": n / dt, "unit": "domains/s", "cores": _threads(), "kind": "oracle",
             "sample": f"beta-CROWN ({BAB_ITERS} steps) on the first {n} subdomains of the same loop, {dt:.1f} s",
-            "cpu_count": os.cpu_count()}
+            **host_info()}
 
 
 def bench_bab_loop(args):
@@ -238,7 +276,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="mlp784x1024x6")
+    ap.add_argument("--workload", default="mlp3072x8192x4")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time (0: skip)")
     ap.add_argument("--alpha-iters", type=int, default=0,
                     help="alpha-CROWN with this many Adam steps on the final pass (MLPs; 0: CROWN)")
@@ -391,8 +429,8 @@ def main():
     if other:
         rec["roofline_other"] = [roofline(k) for k in other]
     rec.update(extra)
-    if args.cpu_budget > 0 and args.workload.startswith("resnet3x32x32"):
-        rec["cpu_baseline"] = cpu_baseline_sampled(wl, args.cpu_budget)
+    if args.cpu_budget > 0 and args.workload in SAMPLED_BASELINE:
+        rec["cpu_baseline"] = cpu_baseline_sampled(wl, args.cpu_budget, SAMPLED_BASELINE[args.workload])
     elif args.cpu_budget > 0 and splits is None:
         rec["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget, args.alpha_iters)
     elif args.cpu_budget > 0:
