@@ -40,7 +40,7 @@
 extern "C" {
 #endif
 
-#define VCR_ABI_VERSION 2   /* 2: vcr_stats gained timed_mid_* */
+#define VCR_ABI_VERSION 3   /* 2: vcr_stats gained timed_mid_*; 3: vcr_crown_bounds_noalloc */
 
 typedef struct vcr_ctx vcr_ctx;
 
@@ -297,6 +297,23 @@ typedef struct {
  * once per round. */
 vcr_status vcr_bab_verify(vcr_ctx *ctx, const float *x0, float eps, const float *C, int32_t m,
                           const vcr_bab_opts *opts, vcr_bab_result *result, int64_t *round_log);
+
+/* Allocation-free variant of vcr_crown_bounds without splits, for callers that cannot
+ * allocate device memory during a call (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments, results and errors as
+ * vcr_crown_bounds(ctx, x0, B, eps, C, m, NULL, lb, ub), bit for bit; the call allocates
+ * nothing: its workspace is a fixed device array of VCR_NOALLOC_SCRATCH_BYTES per GPU (held
+ * from the library's first use on that GPU until the process ends), shared by every context
+ * on that GPU.  Inputs are processed in chunks that fit the scratch (and the workspace cap
+ * option, if smaller); a call whose single input does not fit fails with VCR_ERR_OOM before
+ * queueing work (for example the 3072-8192x4 MLP, or convolutional networks beyond a few
+ * channels at small images).  The call clears the part of the scratch it uses before use.
+ * Calls that overlap on one GPU (other streams, threads or contexts) race on the scratch;
+ * vcr_get_layer_bounds after this call reads the scratch and is valid until the next call of
+ * this entry point on the same GPU.  VCR_OPT_TIME_GEMM and VCR_OPT_GRAPH do not apply. */
+#define VCR_NOALLOC_SCRATCH_BYTES ((uint64_t)256 << 20)
+vcr_status vcr_crown_bounds_noalloc(vcr_ctx *ctx, const float *x0, int32_t B, float eps, const float *C, int32_t m,
+                                    float *lb, float *ub);
 
 /* Pre-activation bounds of ReLU node `relu_id` (0-based among ReLU nodes) from the last
  * CROWN call, for every input: l, u device (B, numel).  Queued on the stream. */

@@ -11,7 +11,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB_DIR = os.path.join(HERE, "lib")
 LIB = os.path.join(LIB_DIR, "libvcrown.so")
-SOURCES = ["gemm.hip", "elementwise.hip", "conv.hip", "alpha.hip", "api.cpp", "graph.cpp"]
+SOURCES = ["gemm.hip", "elementwise.hip", "conv.hip", "alpha.hip", "noalloc.hip", "api.cpp", "graph.cpp"]
 ARCH = "gfx950"
 
 

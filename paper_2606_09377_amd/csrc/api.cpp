@@ -267,6 +267,11 @@ vcr_status vcr_create(int32_t hip_device, vcr_ctx **out) {
       delete c;
       return VCR_ERR_OOM;
     }
+    if (vcr::noalloc_setup(c) != VCR_OK) {
+      (void)hipFree(c->d_counters);
+      delete c;
+      return VCR_ERR_DEVICE;
+    }
   } else if (hip_device != -1) {
     delete c;
     return VCR_ERR_ARG;
@@ -1136,6 +1141,64 @@ vcr_status vcr_crown_bounds(vcr_ctx *c, const float *x0, int32_t B, float eps, c
   c->gkey = key;
   return after_call(c, VCR_OK, t0);
 }
+
+}  // extern "C"
+
+// vcr_crown_bounds (no splits) with the workspace replaced by [base, base + bytes), which the
+// caller owns: the plan is chunked to fit it (VCR_ERR_OOM when even one input does not), the
+// bytes the plan uses are cleared by a fill kernel (the A buffers' padding is read by the
+// GEMMs), and nothing is allocated: no workspace growth, no timing events (TIME_GEMM is
+// ignored for the call), no graph capture.  The context's own workspace is left as it was.
+vcr_status vcr::crown_bounds_in(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m,
+                                float *lb, float *ub, char *base, size_t bytes) {
+  const auto t0 = std::chrono::steady_clock::now();
+  vcr_status st = check_common(c, x0, B, eps, C, m, lb, ub);
+  if (st != VCR_OK) return st;
+  if (c->device < 0) return fail(c, VCR_ERR_STATE, "validation-only context: no device work");
+  if (!base || bytes == 0) return fail(c, VCR_ERR_STATE, "no scratch memory on this device");
+  st = check_finite_inputs(c, x0, B, C, m);
+  if (st != VCR_OK) return st;
+  HIP_TRY(c, hipSetDevice(c->device));
+  // plan under the scratch size (or the user's cap, if smaller): the same plan the call makes
+  const uint64_t user_cap = c->ws_cap;
+  const uint64_t cap = user_cap > 0 ? std::min<uint64_t>(user_cap, bytes) : bytes;
+  c->ws_cap = cap;
+  size_t need = 0;
+  if (c->graph) {
+    int chunk = 0;
+    st = graph_plan(c, B, m, &chunk, &need);
+  } else {
+    Plan p;
+    st = make_plan(c, B, m, 0, 0, &p);
+    need = p.bytes;
+  }
+  c->ws_cap = user_cap;
+  if (st != VCR_OK)
+    return fail(c, VCR_ERR_OOM, "the call does not fit the %llu-byte scratch even one input at a time (%s)",
+                (unsigned long long)cap, c->err.c_str());
+  const Workspace own = c->ws;
+  const int32_t timing = c->time_gemm;
+  c->ws = Workspace{base, cap, 0};
+  c->ws_cap = cap;
+  c->time_gemm = 0;
+  struct Restore {
+    vcr_ctx *c;
+    Workspace own;
+    uint64_t cap;
+    int32_t timing;
+    ~Restore() {
+      c->ws = own;
+      c->ws_cap = cap;
+      c->time_gemm = timing;
+    }
+  } restore{c, own, user_cap, timing};
+  // the scratch keeps the last call's contents: clear what this call's plan uses
+  HIP_TRY(c, launch_fill(reinterpret_cast<float *>(base), (int64_t)(need / 4), 0.f, c->stream));
+  st = c->graph ? graph_crown(c, x0, B, eps, C, m, nullptr, lb, ub) : crown_impl(c, x0, B, eps, C, m, nullptr, lb, ub);
+  return after_call(c, st, t0);
+}
+
+extern "C" {
 
 vcr_status vcr_ibp_bounds(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m,
                           float *lb, float *ub) {

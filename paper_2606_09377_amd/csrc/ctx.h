@@ -95,6 +95,10 @@ struct vcr_ctx {
   uint64_t timed_launches[4] = {0, 0, 0, 0}, timed_flops[4] = {0, 0, 0, 0};
   double timed_ms[4] = {0.0, 0.0, 0.0, 0.0};
   std::vector<std::pair<uint64_t, int>> pending;  // (flops, kind) of each recorded pair
+  // the device's allocation-free scratch (vcr_crown_bounds_noalloc): its device address on
+  // this context's device, resolved at vcr_create, and its size
+  char *scratch = nullptr;
+  size_t scratch_bytes = 0;
 };
 
 inline vcr_status fail(vcr_ctx *c, vcr_status st, const char *fmt, ...) {
@@ -163,3 +167,12 @@ T *take(vcr_ctx *c, size_t count) {
 
 vcr_status ensure_ws(vcr_ctx *c, size_t bytes);
 
+namespace vcr {
+// Resolves the device address of the allocation-free scratch on c's device (current) into
+// c->scratch / c->scratch_bytes (noalloc.hip).
+vcr_status noalloc_setup(vcr_ctx *c);
+// vcr_crown_bounds without splits, run in the caller-given device memory [base, base + bytes)
+// instead of the context's workspace: no device allocation (api.cpp).
+vcr_status crown_bounds_in(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m, float *lb,
+                           float *ub, char *base, size_t bytes);
+}  // namespace vcr

@@ -14,7 +14,7 @@ import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "lib", "libvcrown.so")
-ABI_VERSION = 2   # VCR_ABI_VERSION of include/vcrown.h this binding is written for
+ABI_VERSION = 3   # VCR_ABI_VERSION of include/vcrown.h this binding is written for
 HEADER = os.path.join(os.path.dirname(HERE), "include", "vcrown.h")
 
 VCR_OK, VCR_ERR_ARG, VCR_ERR_SHAPE, VCR_ERR_STATE, VCR_ERR_OOM, VCR_ERR_DEVICE, VCR_ERR_UNSUPPORTED = range(7)
@@ -112,6 +112,7 @@ def load_library(path: str = LIB_PATH):
         "vcr_beta_crown_bounds": ([P, P, F32, P, I32, ctypes.POINTER(VcrSplits), ctypes.POINTER(VcrBetaOpts), P, P],
                                   I32),
         "vcr_bab_verify": ([P, P, F32, P, I32, ctypes.POINTER(VcrBabOpts), ctypes.POINTER(VcrBabResult), P], I32),
+        "vcr_crown_bounds_noalloc": ([P, P, I32, F32, P, I32, P, P], I32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -234,6 +235,21 @@ class Ctx:
             sp = ctypes.byref(sp)
         self._check(self.lib.vcr_crown_bounds(self.h, _ptr(x0), B, ctypes.c_float(float(eps)), _ptr(C), m, sp,
                                               _ptr(lb), _ptr(ub)))
+        return lb, ub
+
+    def crown_bounds_noalloc(self, x0, eps, C, out):
+        """CROWN bounds on C f(x) (no splits) through the allocation-free entry point: the
+        call runs in the library's fixed per-GPU scratch.  out = (lb, ub), caller-allocated
+        (B, m) float32 CUDA tensors."""
+        B, m = C.shape[0], C.shape[1]
+        lb, ub = out
+        _check_tensor(x0, (B, None))
+        _check_tensor(C, (B, m, None))
+        _check_tensor(lb, (B, m))
+        _check_tensor(ub, (B, m))
+        self._stream_sync()
+        self._check(self.lib.vcr_crown_bounds_noalloc(self.h, _ptr(x0), B, ctypes.c_float(float(eps)), _ptr(C), m,
+                                                      _ptr(lb), _ptr(ub)))
         return lb, ub
 
     def alpha_crown_bounds(self, x0, eps, C, iters=20, lr=0.1, beta1=0.9, beta2=0.999, adam_eps=1e-8,

@@ -32,7 +32,7 @@ def test_exports_every_header_symbol(vc):
     lib = vc.load_library()
     for s in syms:
         assert hasattr(lib, s)
-    assert lib.vcr_abi_version() == vc.ABI_VERSION == 2
+    assert lib.vcr_abi_version() == vc.ABI_VERSION == 3
 
 
 def _buf(n, dtype=np.float32):
