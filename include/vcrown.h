@@ -188,6 +188,11 @@ vcr_status vcr_set_stream(vcr_ctx *ctx, void *hip_stream);
 
 vcr_status vcr_set_option(vcr_ctx *ctx, int32_t key, double value);
 
+/* Size limits checked by vcr_load_net (VCR_ERR_SHAPE beyond them): elements of the input or
+ * of any node's output, and weights of one dense or convolution layer (kernels up to 64 x 64). */
+#define VCR_MAX_NODE_ELEMENTS ((int64_t)1 << 30)
+#define VCR_MAX_LAYER_WEIGHTS ((int64_t)1 << 32)
+
 /* Load (copy) a network.  nodes[0..n) in topological order; the last node is the output and
  * must be VCR_DENSE.  in_chw is the input shape (C, H, W); for a flat input use
  * (n0, 1, 1).  Weight pointers are host memory and are not retained.  Replaces any

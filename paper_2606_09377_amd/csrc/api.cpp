@@ -148,6 +148,8 @@ vcr_status validate_net(vcr_ctx *c, const vcr_node *nodes, int32_t n, const int3
                         std::vector<std::vector<int64_t>> *shapes_out) {
   if (!nodes || n <= 0 || !in_chw) return fail(c, VCR_ERR_ARG, "empty network");
   if (in_chw[0] <= 0 || in_chw[1] <= 0 || in_chw[2] <= 0) return fail(c, VCR_ERR_SHAPE, "bad input shape");
+  if ((int64_t)in_chw[0] * in_chw[1] * in_chw[2] > VCR_MAX_NODE_ELEMENTS)
+    return fail(c, VCR_ERR_SHAPE, "the input exceeds the limit of %lld elements", (long long)VCR_MAX_NODE_ELEMENTS);
   std::vector<std::vector<int64_t>> sh;
   const std::vector<int64_t> in_shape = {in_chw[0], in_chw[1], in_chw[2]};
   auto shape_of = [&](int32_t i) -> const std::vector<int64_t> & { return i == -1 ? in_shape : sh[i]; };
@@ -159,7 +161,7 @@ vcr_status validate_net(vcr_ctx *c, const vcr_node *nodes, int32_t n, const int3
   for (int32_t i = 0; i < n; ++i) {
     const vcr_node &nd = nodes[i];
     if (nd.in0 < -1 || nd.in0 >= i) return fail(c, VCR_ERR_ARG, "node %d: in0=%d is not an earlier node", i, nd.in0);
-    const auto &s = shape_of(nd.in0);
+    const std::vector<int64_t> s = shape_of(nd.in0);   // a copy: sh grows below
     switch (nd.op) {
       case VCR_DENSE: {
         if (!nd.W || !nd.b) return fail(c, VCR_ERR_ARG, "node %d: dense without weights", i);
@@ -192,7 +194,17 @@ vcr_status validate_net(vcr_ctx *c, const vcr_node *nodes, int32_t n, const int3
       default:
         return fail(c, VCR_ERR_ARG, "node %d: unknown op %d", i, nd.op);
     }
-    (void)numel;
+    // size limits: kernel index arithmetic is 32-bit within a row and 64-bit across rows
+    if (numel(sh.back()) > VCR_MAX_NODE_ELEMENTS)
+      return fail(c, VCR_ERR_SHAPE, "node %d: %lld elements exceed the limit of %lld", i, (long long)numel(sh.back()),
+                  (long long)VCR_MAX_NODE_ELEMENTS);
+    const int64_t weights = nd.op == VCR_DENSE    ? (int64_t)nd.out_features * numel(s)
+                            : nd.op == VCR_CONV2D ? (int64_t)nd.out_ch * s[0] * nd.kh * nd.kw
+                                                  : 0;
+    if ((nd.op == VCR_DENSE || nd.op == VCR_CONV2D) &&
+        (nd.out_features > VCR_MAX_NODE_ELEMENTS || nd.kh > 64 || nd.kw > 64 || weights > VCR_MAX_LAYER_WEIGHTS))
+      return fail(c, VCR_ERR_SHAPE, "node %d: %lld weights exceed the limit of %lld", i, (long long)weights,
+                  (long long)VCR_MAX_LAYER_WEIGHTS);
   }
   if (nodes[n - 1].op != VCR_DENSE) return fail(c, VCR_ERR_ARG, "the output node must be dense");
   *shapes_out = sh;
@@ -584,7 +596,7 @@ void carve(const vcr_ctx *c, Workspace &w, const Plan &p, int32_t S, CallBufs *b
     bf->ent_p = take<float4>(w, (size_t)p.D * S);
     bf->flags = take<int32_t>(w, p.D);
     bf->Lptr = take<const float *>(w, 2 * R);
-    bf->Uptr = bf->Lptr + R;
+    bf->Uptr = bf->Lptr ? bf->Lptr + R : nullptr;   // null while only counting bytes
     bf->relu_n = take<int32_t>(w, R);
   }
   const int64_t rpi = max_inter_rows_per_input(c);
