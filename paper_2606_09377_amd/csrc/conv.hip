@@ -359,7 +359,10 @@ static bool axis_classes(int S_in, int S_out, int stride, int delta, std::vector
 }
 
 // The classes of a transposed convolution (axis classes of rows times those of columns) and
-// their dispatches, up to four consecutive classes each.
+// their dispatches, up to four consecutive classes each.  (One dispatch of all classes, the
+// longest first, measured 1.7% slower on the ResNet: a border-ring tile gathers a position or
+// two from each of its 256 rows' windows, and mixing them with the interior tiles of other
+// rows costs L2 locality.)
 struct ConvtDispatch {
   std::vector<int> cls;   // indices into the class list
 };
@@ -724,56 +727,87 @@ hipError_t launch_stem(const StemArgs &a, hipStream_t s) {
 // First rows of a pass that starts at a 3x3 convolution's output neurons: row (unit, dir,
 // c0, i, j) is (dir ? -1 : 1) W[c0][ci][u][w] on the convolution's input window around
 // (stride i, stride j), zero outside the image; relaxed (or identity) like the GEMM
-// epilogue; beta = (dir ? -1 : 1) b[c0] + the window's constant terms.  Each wave takes
-// INIT_CONV_RPW consecutive rows; the weights come tap-major ([c0][u][w][ci]), so the lanes' channel
-// loads are contiguous.
-constexpr int INIT_CONV_RPW = 4;   // rows per wave
+// epilogue; beta = (dir ? -1 : 1) b[c0] + the window's constant terms.  Rows are ordered
+// (unit, dir, c0, position); the 2 INIT_CONV_G rows of one unit and position with start
+// channels c0 in one group of INIT_CONV_G (both directions) share their window and so their
+// relaxation parameters, which are the bulk of the reads: a wave takes those rows, loads each
+// parameter once for all of them, and writes each row with the lanes across the channels
+// (weights tap-major, [c0][u][w][ci]: contiguous channel loads).  A row's constant is summed
+// positions outer, a lane's channels inner, then a fixed butterfly.
+constexpr int INIT_CONV_G = 4;   // start channels per wave (8 rows)
 
 __global__ __launch_bounds__(256) void k_init_conv(const ConvInitArgs a) {
   const int lane = threadIdx.x & 63;
-  const int n_src = a.C_src * a.H_src * a.H_src;
-  const int S = a.S;   // kernel window (3)
-  for (int k = 0; k < INIT_CONV_RPW; ++k) {
-    const int64_t r = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * INIT_CONV_RPW + k;
-    if (r >= a.R) return;   // wave-uniform
-    const int4 an = a.rows[r];
-    const int q = (int)(r % (2 * n_src));
-    const int dir = q >= n_src;
-    const int nq = q - dir * n_src;
-    const int c0 = nq / (a.H_src * a.H_src);
-    const float sg = dir ? -1.f : 1.f;
-    float *orow = a.out + r * (int64_t)S * S * a.C_in;
-    float acc = 0.f;
-    // window positions outer (their image bounds are wave-uniform), channels across the lanes
-    for (int u = 0; u < S; ++u)
-      for (int w = 0; w < S; ++w) {
-        const int gy = an.y * a.scale - a.h + u, gx = an.z * a.scale - a.h + w;
-        const bool in = gy >= 0 && gx >= 0 && gy < a.H_in && gx < a.H_in;
-        const float4 *P = a.P_pos ? a.P_pos + (((int64_t)an.x * a.H_in + gy) * a.H_in + gx) * a.C_in : nullptr;
-        float *o = orow + (int64_t)(u * S + w) * a.C_in;
-        for (int ci = lane; ci < a.C_in; ci += 64) {
-          float ap = 0.f;
-          if (in) {
-            const float x = sg * a.W[((int64_t)c0 * 9 + u * 3 + w) * a.C_in + ci];
-            const float4 prm = P ? P[ci] : make_float4(1.f, 1.f, 0.f, a.bias_next[ci]);
-            ap = x > 0.f ? x * prm.x : x * prm.y;
-            acc += fminf(x, 0.f) * prm.z + ap * prm.w;
+  const int HW = a.H_src * a.H_src;
+  const int64_t n_src = (int64_t)a.C_src * HW;
+  const int n_grp = a.C_src / INIT_CONV_G;
+  const int64_t wv = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int64_t units = a.R / (2 * n_src);
+  if (wv >= units * n_grp * HW) return;   // wave-uniform
+  const int64_t ug = wv / HW;
+  const int pos = (int)(wv - ug * HW);
+  const int64_t ul = ug / n_grp;
+  const int cg = (int)(ug - ul * n_grp);
+  const int64_t r0 = ul * 2 * n_src + (int64_t)cg * INIT_CONV_G * HW + pos;   // dir 0, first c0 of the group
+  const int4 an = a.rows[r0];   // the same unit and anchor for all the wave's rows
+  const int S = a.S;
+  const int64_t row_len = (int64_t)S * S * a.C_in;
+  float acc[2][INIT_CONV_G];
+#pragma unroll
+  for (int d = 0; d < 2; ++d)
+#pragma unroll
+    for (int e = 0; e < INIT_CONV_G; ++e) acc[d][e] = 0.f;
+  for (int u = 0; u < S; ++u)
+    for (int w = 0; w < S; ++w) {
+      const int gy = an.y * a.scale - a.h + u, gx = an.z * a.scale - a.h + w;
+      const bool in = gy >= 0 && gx >= 0 && gy < a.H_in && gx < a.H_in;
+      const float4 *P = a.P_pos ? a.P_pos + (((int64_t)an.x * a.H_in + gy) * a.H_in + gx) * a.C_in : nullptr;
+      const int64_t po = (int64_t)(u * S + w) * a.C_in;
+      for (int ci = lane; ci < a.C_in; ci += 64) {
+        float4 prm = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (in) prm = P ? P[ci] : make_float4(1.f, 1.f, 0.f, a.bias_next[ci]);
+#pragma unroll
+        for (int e = 0; e < INIT_CONV_G; ++e) {
+          const int c0 = cg * INIT_CONV_G + e;
+          const float wt = in ? a.W[((int64_t)c0 * 9 + u * 3 + w) * a.C_in + ci] : 0.f;
+#pragma unroll
+          for (int d = 0; d < 2; ++d) {
+            const float x = d ? -wt : wt;
+            float ap = 0.f;
+            if (in) {
+              ap = x > 0.f ? x * prm.x : x * prm.y;
+              acc[d][e] += fminf(x, 0.f) * prm.z + ap * prm.w;
+            }
+            const int64_t r = r0 + d * n_src + (int64_t)e * HW;
+            __builtin_nontemporal_store(ap, a.out + r * row_len + po + ci);   // read back only by the next GEMM
           }
-          __builtin_nontemporal_store(ap, o + ci);   // read back only by the next GEMM
         }
       }
-    acc += __shfl_xor(acc, 32);
-    acc += __shfl_xor(acc, 16);
-    acc += __shfl_xor(acc, 8);
-    acc += __shfl_xor(acc, 4);
-    acc += __shfl_xor(acc, 2);
-    acc += __shfl_xor(acc, 1);
-    if (lane == 0) a.beta[r] = sg * a.b[c0] + acc;
-  }
+    }
+#pragma unroll
+  for (int d = 0; d < 2; ++d)
+#pragma unroll
+    for (int e = 0; e < INIT_CONV_G; ++e) {
+      float x = acc[d][e];
+      x += __shfl_xor(x, 32);
+      x += __shfl_xor(x, 16);
+      x += __shfl_xor(x, 8);
+      x += __shfl_xor(x, 4);
+      x += __shfl_xor(x, 2);
+      x += __shfl_xor(x, 1);
+      if (lane == 0) {
+        const int c0 = cg * INIT_CONV_G + e;
+        a.beta[r0 + d * n_src + (int64_t)e * HW] = (d ? -1.f : 1.f) * a.b[c0] + x;
+      }
+    }
 }
 
 hipError_t launch_init_conv(const ConvInitArgs &a, hipStream_t s) {
-  const int64_t waves = (a.R + INIT_CONV_RPW - 1) / INIT_CONV_RPW;
+  const int64_t n_src = (int64_t)a.C_src * a.H_src * a.H_src;
+  // whole units of 2 n_src rows, start channels in groups, a 3 x 3 window
+  if (a.C_src % INIT_CONV_G || a.S != 3 || n_src <= 0 || a.R % (2 * n_src)) return hipErrorInvalidValue;
+  const int64_t waves = a.R / 2 / INIT_CONV_G;
+  if ((waves + 3) / 4 > 0x7fffffff) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_init_conv, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
@@ -896,43 +930,91 @@ hipError_t launch_conv_layer_from_ibp(const float *ibp_c, const float *ibp_r, in
 
 // ------------------------------------------------------------------------------------
 // IBP of a convolution in centre/radius form, c' = conv(W, c) + b, r' = conv(|W|, r), over
-// CHW tensors.  One thread per output element.
-__global__ void k_ibp_conv(const float *W, const float *bias, int32_t Co, int32_t Ci, int32_t Hin, int32_t Hout,
-                           int32_t stride, int32_t pad, const float *cin, const float *rin, int64_t ld_in,
-                           float *cout, float *rout, int64_t ld_out, int32_t B) {
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t per = (int64_t)Co * Hout * Hout;
-  if (idx >= B * per) return;
-  const int64_t b = idx / per, q = idx - b * per;
-  const int co = (int)(q / (Hout * Hout)), hw = (int)(q % (Hout * Hout));
-  const int oy = hw / Hout, ox = hw % Hout;
-  float c = 0.f, r = 0.f;
-  for (int ci = 0; ci < Ci; ++ci) {
-    const float *wp = W + ((int64_t)co * Ci + ci) * 9;
-    const float *cp = cin + b * ld_in + (int64_t)ci * Hin * Hin;
-    const float *rq = rin + b * ld_in + (int64_t)ci * Hin * Hin;
-    for (int ky = 0; ky < 3; ++ky) {
-      const int iy = oy * stride - pad + ky;
-      if (iy < 0 || iy >= Hin) continue;
-      for (int kx = 0; kx < 3; ++kx) {
-        const int ix = ox * stride - pad + kx;
-        if (ix < 0 || ix >= Hin) continue;
-        const float w = wp[ky * 3 + kx];
-        c += w * cp[iy * Hin + ix];
-        r += fabsf(w) * rq[iy * Hin + ix];
+// CHW tensors, as an implicit GEMM on the matrix cores: out[co][pos] = sum_k W[co][k] x[k][pos]
+// with k = (ci, ky, kx) (the weights' own K-contiguous order) and x[k][pos] the input value
+// the tap reaches (0 in the padding).  A workgroup of 4 waves owns 32 output channels x 32
+// output positions of one input: each wave takes a quarter of K (v_mfma_f32_32x32x2f32, the
+// weights as the A operand, the gathered input as the B operand, so a lane's 32 consecutive
+// positions are coalesced), and the four partial tiles are added in wave order through LDS,
+// so every output has one fixed summation order (independent of the batch).
+constexpr int IBPC_WAVES = 4;
+
+__global__ __launch_bounds__(64 * IBPC_WAVES) void k_ibp_conv(const float *W, const float *bias, int32_t Co,
+                                                             int32_t Ci, int32_t Hin, int32_t Hout, int32_t stride,
+                                                             int32_t pad, const float *cin, const float *rin,
+                                                             int64_t ld_in, float *cout, float *rout, int64_t ld_out) {
+  __shared__ float red[IBPC_WAVES][32][64];   // per wave: 16 centre + 16 radius values per lane
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int P = Hout * Hout, K = Ci * 9;
+  const int n_pt = (P + 31) / 32;
+  const int b = blockIdx.x / n_pt, p0 = (blockIdx.x - b * n_pt) * 32;
+  const int co0 = blockIdx.y * 32;
+  const int l32 = lane & 31, kh = lane >> 5;
+  // this lane's weight row (A operand) and output position (B operand)
+  const int co = co0 + l32;
+  const float *wrow = W + (int64_t)(co < Co ? co : 0) * K;
+  const int pos = p0 + l32;
+  const int oy = pos / Hout, ox = pos - oy * Hout;
+  const int y0 = oy * stride - pad, x0 = ox * stride - pad;
+  const bool pos_ok = pos < P, co_ok = co < Co;
+  const float *cb = cin + (int64_t)b * ld_in, *rb = rin + (int64_t)b * ld_in;
+  // this wave's quarter of K, in steps of 2 (one MFMA each for the centre and the radius)
+  const int steps = (K + 1) / 2, per = (steps + IBPC_WAVES - 1) / IBPC_WAVES;
+  const int s0 = wave * per, s1 = min(steps, s0 + per);
+  f32x16 ac, ar;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) ac[v] = ar[v] = 0.f;
+  for (int st = s0; st < s1; ++st) {
+    const int k = 2 * st + kh;
+    float w = 0.f, xc = 0.f, xr = 0.f;
+    if (k < K) {
+      w = co_ok ? wrow[k] : 0.f;
+      const int ci = k / 9, tap = k - ci * 9;
+      const int ky = tap / 3, kx = tap - ky * 3;
+      const int iy = y0 + ky, ix = x0 + kx;
+      if (pos_ok && (unsigned)iy < (unsigned)Hin && (unsigned)ix < (unsigned)Hin) {
+        const int64_t o = ((int64_t)ci * Hin + iy) * Hin + ix;
+        xc = cb[o];
+        xr = rb[o];
       }
     }
+    ac = __builtin_amdgcn_mfma_f32_32x32x2f32(w, xc, ac, 0, 0, 0);
+    ar = __builtin_amdgcn_mfma_f32_32x32x2f32(fabsf(w), xr, ar, 0, 0, 0);
   }
-  cout[b * ld_out + q] = c + bias[co];
-  rout[b * ld_out + q] = r;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    red[wave][v][lane] = ac[v];
+    red[wave][16 + v][lane] = ar[v];
+  }
+  __syncthreads();
+  // thread t adds value v = 8 (t / 64) .. + 8 of lane t % 64 over the waves, in wave order;
+  // lane l's value v is output channel 8 (v / 4) + 4 (l / 32) + v % 4 of the tile at position l % 32
+  const int t = threadIdx.x, tl = t & 63, vq = t >> 6;
+  const int op = p0 + (tl & 31);
+  for (int j = 0; j < 8; ++j) {
+    const int v = vq * 8 + j;   // 0..31: centre 0..15, radius 16..31
+    float x = 0.f;
+#pragma unroll
+    for (int w = 0; w < IBPC_WAVES; ++w) x += red[w][v][tl];
+    const int vv = v & 15;
+    const int oc = co0 + 8 * (vv >> 2) + 4 * (tl >> 5) + (vv & 3);
+    if (oc < Co && op < P) {
+      if (v < 16)
+        cout[(int64_t)b * ld_out + (int64_t)oc * P + op] = x + bias[oc];
+      else
+        rout[(int64_t)b * ld_out + (int64_t)oc * P + op] = x;
+    }
+  }
 }
 
 hipError_t launch_ibp_conv(const float *W, const float *bias, int32_t Co, int32_t Ci, int32_t Hin, int32_t Hout,
                            int32_t stride, int32_t pad, const float *cin, const float *rin, int64_t ld_in,
                            float *cout, float *rout, int64_t ld_out, int32_t B, hipStream_t s) {
-  const int64_t tot = (int64_t)B * Co * Hout * Hout;
-  hipLaunchKernelGGL(k_ibp_conv, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, W, bias, Co, Ci, Hin, Hout,
-                     stride, pad, cin, rin, ld_in, cout, rout, ld_out, B);
+  const int64_t n_pt = ((int64_t)Hout * Hout + 31) / 32;
+  if (B <= 0 || B * n_pt > 0x7fffffff) return hipErrorInvalidValue;
+  dim3 grid((unsigned)(B * n_pt), (unsigned)((Co + 31) / 32));
+  hipLaunchKernelGGL(k_ibp_conv, grid, dim3(64 * IBPC_WAVES), 0, s, W, bias, Co, Ci, Hin, Hout, stride, pad, cin, rin,
+                     ld_in, cout, rout, ld_out);
   return hipGetLastError();
 }
 
