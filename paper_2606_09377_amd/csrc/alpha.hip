@@ -107,21 +107,22 @@ hipError_t launch_alpha_keep(const AlphaLayer &l, const int32_t *flag, int32_t r
   return hipGetLastError();
 }
 
-// Adam (bias-corrected moments) then projection onto [0, 1], at unstable neurons only.  With
-// flag, the rows whose bound improved first keep their current slopes in best (the keep step
-// folded into the same pass over the state).
+// Adam (bias-corrected moments) then projection onto [0, 1].  Only unstable neurons move:
+// the gradient pass writes a zero gradient at every other column (stable neurons, split
+// neurons made stable), whose moments therefore stay zero and whose step is exactly 0, and
+// their slopes start at lambda in {0, 1}, which the projection keeps; so no relaxation
+// parameter is read here and the result is the same as skipping those columns.  With flag, the rows whose bound improved first
+// keep their current slopes in best (the keep step folded into the same pass over the state).
 typedef float adam_f32x4 __attribute__((ext_vector_type(4)));
-__global__ void k_alpha_adam(AlphaLayer l, const int32_t *flag, int32_t blocks_per_row, int32_t rows_per_unit,
-                             float lr, float beta1, float beta2, float eps, float c1, float c2) {
+__global__ void k_alpha_adam(AlphaLayer l, const int32_t *flag, int32_t blocks_per_row, float lr, float beta1,
+                             float beta2, float eps, float c1, float c2) {
   const int32_t row = blockIdx.x / blocks_per_row;
   const int64_t n0 = (int64_t)(blockIdx.x - row * blocks_per_row) * ALPHA_COLS_PER_BLOCK + threadIdx.x * 4;
   if (n0 >= l.ld) return;
   const int64_t idx = (int64_t)row * l.ld + n0;
-  float4 a4 = *reinterpret_cast<const float4 *>(l.alpha + idx);
+  const float4 a4 = *reinterpret_cast<const float4 *>(l.alpha + idx);
   if (flag && flag[row]) *reinterpret_cast<float4 *>(l.best + idx) = a4;
   if (n0 >= l.n) return;
-  const int32_t u = row / rows_per_unit;
-  const float4 *P = l.P + (int64_t)u * l.ld + n0;
   // the gradient and the moments are touched once per step: streamed past the caches
   const adam_f32x4 g4 = __builtin_nontemporal_load(reinterpret_cast<const adam_f32x4 *>(l.grad + idx));
   const adam_f32x4 m4 = __builtin_nontemporal_load(reinterpret_cast<const adam_f32x4 *>(l.mom + idx));
@@ -130,7 +131,7 @@ __global__ void k_alpha_adam(AlphaLayer l, const int32_t *flag, int32_t blocks_p
   float mo[4] = {m4[0], m4[1], m4[2], m4[3]}, ve[4] = {v4[0], v4[1], v4[2], v4[3]};
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    if (n0 + e >= l.n || !(P[e].z > 0.f)) continue;   // padding or a stable neuron: unchanged
+    if (n0 + e >= l.n) continue;   // padding
     mo[e] = beta1 * mo[e] + (1.f - beta1) * g[e];
     ve[e] = beta2 * ve[e] + (1.f - beta2) * g[e] * g[e];
     const float t = a[e] + lr * (mo[e] * c1) / (sqrtf(ve[e] * c2) + eps);
@@ -145,8 +146,9 @@ hipError_t launch_alpha_adam(const AlphaLayer &l, const int32_t *flag, int32_t r
                              float beta1, float beta2, float eps, float c1, float c2, hipStream_t s) {
   if (l.ld % 4) return hipErrorInvalidValue;
   const int32_t bpr = (int32_t)((l.ld + ALPHA_COLS_PER_BLOCK - 1) / ALPHA_COLS_PER_BLOCK);
-  hipLaunchKernelGGL(k_alpha_adam, dim3((unsigned)((int64_t)rows * bpr)), dim3(256), 0, s, l, flag, bpr,
-                     rows_per_unit, lr, beta1, beta2, eps, c1, c2);
+  (void)rows_per_unit;   // the relaxation parameters are not needed (see k_alpha_adam)
+  hipLaunchKernelGGL(k_alpha_adam, dim3((unsigned)((int64_t)rows * bpr)), dim3(256), 0, s, l, flag, bpr, lr, beta1,
+                     beta2, eps, c1, c2);
   return hipGetLastError();
 }
 
