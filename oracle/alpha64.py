@@ -30,8 +30,11 @@ coefficient a_j on that ReLU's output is positive (0 otherwise), where D_j is th
 pre-activation z_j obtained by evaluating the network forward from x* with every ReLU
 replaced by the line its coefficient's sign selected (alpha z where a > 0, s z + t where
 a < 0, s z where a = 0).  The upper bound is the mirror image (alpha where a < 0, the
-maximising vertex).  Networks: chains of dense, conv2d, relu and flatten nodes (each node
-reads the one before it).
+maximising vertex).  Networks: dense, conv2d, relu, add and flatten nodes in topological
+order (residual blocks included): the backward pass sums the coefficients that reach a node
+along every path, and the forward evaluation adds both inputs of an add, so the same
+argument holds (the coefficient on h_j is the derivative of the relaxed network's linear
+function with respect to h_j).
 """
 from __future__ import annotations
 
@@ -48,10 +51,10 @@ def relu_ids(net):
 
 def _check_chain(net):
     for i, nd in enumerate(net.nodes):
-        if nd.op not in ("dense", "conv2d", "relu", "flatten"):
+        if nd.op not in ("dense", "conv2d", "relu", "add", "flatten"):
             raise ValueError(f"alpha-CROWN oracle: unsupported node {nd.op}")
-        if nd.in0 != i - 1:
-            raise ValueError("alpha-CROWN oracle: the network must be a chain")
+        if not (-1 <= nd.in0 < i) or (nd.op == "add" and not (-1 <= nd.in1 < i)):
+            raise ValueError("alpha-CROWN oracle: nodes must be in topological order")
 
 
 def unstable_mask(root, i):
@@ -72,23 +75,33 @@ def initial_alpha(net, root, m):
 def _pass(net, shapes, root, C, alpha, upper):
     """Backward pass from the output with A = C and per-row lower slopes `alpha`.
 
-    Returns the bound of every row, the coefficients on the input and, for every ReLU, the
-    coefficient rows on its output before relaxation."""
+    Nodes are visited in reverse order; the coefficients that reach a node along several
+    paths (the two inputs of an add) are summed before the node is expanded.  Returns the
+    bound of every row, the coefficients on the input and, for every ReLU, the coefficient
+    rows on its output before relaxation."""
     A = np.asarray(C, np.float64)
     rows = A.shape[0]
     bias = np.zeros(rows)
     pre = {}
+    acc = {len(net.nodes) - 1: A}
+
+    def add_to(node, X):
+        acc[node] = acc[node] + X if node in acc else X
+
     for i in range(len(net.nodes) - 1, -1, -1):
+        if i not in acc:
+            continue
+        A = acc.pop(i)
         nd = net.nodes[i]
         if nd.op == "dense":
             bias = bias + A @ cr._f64(nd.b)
-            A = A @ cr._f64(nd.W)
+            add_to(nd.in0, A @ cr._f64(nd.W))
         elif nd.op == "conv2d":
             co, ho, wo = shapes[i]
             in_shape = tuple(net.in_shape) if nd.in0 == -1 else shapes[nd.in0]
             A4 = A.reshape(rows, co, ho, wo)
             bias = bias + A4.sum(axis=(2, 3)) @ cr._f64(nd.b)
-            A = cr.conv2d_transpose(A4, cr._f64(nd.W), nd.stride, nd.pad, in_shape[1:]).reshape(rows, -1)
+            add_to(nd.in0, cr.conv2d_transpose(A4, cr._f64(nd.W), nd.stride, nd.pad, in_shape[1:]).reshape(rows, -1))
         elif nd.op == "relu":
             lam0, s, t = (v.reshape(-1) for v in root.relax[i])
             lam = np.where(unstable_mask(root, i).reshape(-1)[None, :], alpha[i], lam0[None, :])
@@ -96,32 +109,41 @@ def _pass(net, shapes, root, C, alpha, upper):
             Ap, An = np.maximum(A, 0.0), np.minimum(A, 0.0)
             if not upper:
                 bias = bias + An @ t
-                A = Ap * lam + An * s
+                add_to(nd.in0, Ap * lam + An * s)
             else:
                 bias = bias + Ap @ t
-                A = Ap * s + An * lam
-        # flatten: coefficients keep their (C, H, W) order
+                add_to(nd.in0, Ap * s + An * lam)
+        elif nd.op == "add":
+            add_to(nd.in0, A)
+            add_to(nd.in1, A)
+        elif nd.op == "flatten":
+            # coefficients keep their (C, H, W) order
+            add_to(nd.in0, A)
+    A = acc.pop(-1) if -1 in acc else np.zeros((rows, int(np.prod(net.in_shape))))
     lo, hi = root.box
     return cr.concretize(A, bias, lo, hi, upper), A, pre
 
 
 def _gradient(net, shapes, root, A_x, pre, alpha, upper):
-    """d bound / d alpha for every ReLU (see the module docstring)."""
+    """d bound / d alpha for every ReLU (see the module docstring): the relaxed network
+    evaluated forward, node by node, from the attaining box vertex."""
     lo, hi = root.box
     c, r = (lo + hi) / 2.0, (hi - lo) / 2.0
     sgn = np.sign(A_x)
-    v = c[None, :] + sgn * r[None, :] if upper else c[None, :] - sgn * r[None, :]
-    rows = v.shape[0]
+    x = c[None, :] + sgn * r[None, :] if upper else c[None, :] - sgn * r[None, :]
+    rows = x.shape[0]
+    val = {}
     grad = {}
+    get = lambda i: x if i == -1 else val[i]  # noqa: E731
     for i, nd in enumerate(net.nodes):
+        v = get(nd.in0)
         if nd.op == "dense":
-            v = v.reshape(rows, -1) @ cr._f64(nd.W).T + cr._f64(nd.b)
+            val[i] = v.reshape(rows, -1) @ cr._f64(nd.W).T + cr._f64(nd.b)
         elif nd.op == "conv2d":
             in_shape = tuple(net.in_shape) if nd.in0 == -1 else shapes[nd.in0]
             x4 = v.reshape((rows,) + tuple(in_shape))
-            v = np.stack([cr.conv2d(x4[k], cr._f64(nd.W), nd.stride, nd.pad) for k in range(rows)])
-            v = v + cr._f64(nd.b)[None, :, None, None]
-            v = v.reshape(rows, -1)
+            y = np.stack([cr.conv2d(x4[k], cr._f64(nd.W), nd.stride, nd.pad) for k in range(rows)])
+            val[i] = (y + cr._f64(nd.b)[None, :, None, None]).reshape(rows, -1)
         elif nd.op == "relu":
             lam0, s, t = (q.reshape(-1) for q in root.relax[i])
             unst = unstable_mask(root, i).reshape(-1)[None, :]
@@ -133,9 +155,11 @@ def _gradient(net, shapes, root, A_x, pre, alpha, upper):
             else:
                 on_lam, on_chord_t = a < 0.0, a > 0.0
             grad[i] = np.where(unst & on_lam, a * D, 0.0)
-            v = np.where(on_lam, lam * D, s[None, :] * D + np.where(on_chord_t, t[None, :], 0.0))
+            val[i] = np.where(on_lam, lam * D, s[None, :] * D + np.where(on_chord_t, t[None, :], 0.0))
+        elif nd.op == "add":
+            val[i] = v.reshape(rows, -1) + get(nd.in1).reshape(rows, -1)
         elif nd.op == "flatten":
-            v = v.reshape(rows, -1)
+            val[i] = v.reshape(rows, -1)
     return grad
 
 

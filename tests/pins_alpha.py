@@ -10,15 +10,18 @@ formulas:
     the lower slopes can be exchanged), solved by scipy; with more layers every alpha bound
     lies between CROWN's and the LP's;
   * every alpha in [0, 1] gives bounds that contain sampled outputs, box corners and dense
-    grids of 2-input networks.
+    grids of 2-input networks;
+  * the same on networks with residual additions (convolutional and dense): CROWN's slopes
+    give CROWN, finite differences, soundness, and with one ReLU layer in a dense residual
+    block y = x + W2 ReLU(W1 x + b1) the optimised bound reaches the triangle LP's optimum.
 """
 from __future__ import annotations
 
 import numpy as np
 
 from oracle import crown64 as cr
-from tests.pins import box_of, spec_values
-from workloads import random_mlp
+from tests.pins import box_of, spec_values, tiny_resnet
+from workloads import Net, Node, margin_spec, random_mlp
 
 
 def _random_alpha(A, net, root, m, rng):
@@ -209,5 +212,140 @@ def pin_alpha_history(A):
             assert np.all((v >= 0.0) & (v <= 1.0))
 
 
+def _residual_dense(seed, n0=4, hid=10, n_out=3):
+    """x -> y = x + W2 ReLU(W1 x + b1) + b2 -> f = W3 y + b3: one ReLU layer with a skip."""
+    rng = np.random.default_rng(seed)
+    W1 = (rng.standard_normal((hid, n0)) * np.sqrt(2 / n0)).astype(np.float32)
+    b1 = (rng.standard_normal(hid) * 0.3).astype(np.float32)
+    W2 = (rng.standard_normal((n0, hid)) * np.sqrt(2 / hid)).astype(np.float32)
+    b2 = (rng.standard_normal(n0) * 0.1).astype(np.float32)
+    W3 = (rng.standard_normal((n_out, n0)) * np.sqrt(2 / n0)).astype(np.float32)
+    b3 = (rng.standard_normal(n_out) * 0.1).astype(np.float32)
+    nodes = [Node("dense", -1, W=W1, b=b1), Node("relu", 0), Node("dense", 1, W=W2, b=b2),
+             Node("flatten", -1), Node("add", 3, 2), Node("dense", 4, W=W3, b=b3)]
+    net = Net((n0,), nodes)
+    x0 = rng.random((1, n0)).astype(np.float32)
+    return net, x0, margin_spec(net, x0)
+
+
+def _residual_cases():
+    out = []
+    for seed in (81, 82):
+        net = tiny_resnet(seed)
+        rng = np.random.default_rng(seed + 100)
+        x0 = rng.random((1, int(np.prod(net.in_shape)))).astype(np.float32)
+        out.append((net, x0[0], np.float32(0.08), margin_spec(net, x0)[0]))
+    net, x0, C = _residual_dense(83)
+    out.append((net, x0[0], np.float32(0.25), C[0]))
+    return out
+
+
+def residual_lp(net, root, C, upper):
+    """min (or max) of C f(x) over the box for the dense residual block of _residual_dense,
+    with the unstable ReLUs replaced by their triangles; variables x, z = W1 x + b1, h."""
+    from scipy.optimize import linprog
+    W1, b1 = net.nodes[0].W.astype(np.float64), net.nodes[0].b.astype(np.float64)
+    W2, b2 = net.nodes[2].W.astype(np.float64), net.nodes[2].b.astype(np.float64)
+    W3, b3 = net.nodes[5].W.astype(np.float64), net.nodes[5].b.astype(np.float64)
+    lo, hi = root.box
+    n0, hid = lo.size, W1.shape[0]
+    l, u = root.layer_l[1], root.layer_u[1]
+    nv = n0 + 2 * hid
+    A_eq, b_eq, A_ub, b_ub = [], [], [], []
+    for j in range(hid):
+        row = np.zeros(nv)
+        row[n0 + j] = 1.0
+        row[:n0] = -W1[j]
+        A_eq.append(row); b_eq.append(b1[j])
+        ez = np.zeros(nv); ez[n0 + j] = 1.0
+        eh = np.zeros(nv); eh[n0 + hid + j] = 1.0
+        if u[j] <= 0:
+            A_eq.append(eh); b_eq.append(0.0)
+        elif l[j] >= 0:
+            A_eq.append(eh - ez); b_eq.append(0.0)
+        else:
+            A_ub.append(ez - eh); b_ub.append(0.0)
+            A_ub.append(-eh); b_ub.append(0.0)
+            s_ = u[j] / (u[j] - l[j])
+            A_ub.append(eh - s_ * ez); b_ub.append(-s_ * l[j])
+    bounds = [(lo[i], hi[i]) for i in range(n0)] + [(l[j], u[j]) for j in range(hid)] + [(None, None)] * hid
+    out = []
+    for c in np.asarray(C, np.float64):
+        g = c @ W3                      # c f = g (x + W2 h + b2) + c b3
+        obj = np.zeros(nv)
+        obj[:n0] = g
+        obj[n0 + hid:] = g @ W2
+        res = linprog(-obj if upper else obj, A_ub=np.array(A_ub) if A_ub else None,
+                      b_ub=np.array(b_ub) if b_ub else None, A_eq=np.array(A_eq), b_eq=np.array(b_eq),
+                      bounds=bounds, method="highs")
+        assert res.status == 0, res.message
+        out.append((-res.fun if upper else res.fun) + g @ b2 + c @ b3)
+    return np.array(out)
+
+
+def pin_alpha_residual_nets(A):
+    """Residual networks (a conv net with a residual block, a dense residual block): CROWN's
+    slopes reproduce CROWN; the gradient matches central finite differences; random and
+    optimised slopes stay sound on sampled points and box corners."""
+    rng = np.random.default_rng(9)
+    for net, x0, eps, C in _residual_cases():
+        m = C.shape[0]
+        for rule in ("adaptive", "zero", "one"):
+            ref = cr.crown(net, x0, eps, C, lambda_rule=rule)
+            al, au = A.initial_alpha(net, ref, m)
+            lb, ub, _, _ = A.alpha_bound(net, ref, C, al, au)
+            np.testing.assert_allclose(lb, ref.lb, rtol=1e-12, atol=1e-12)
+            np.testing.assert_allclose(ub, ref.ub, rtol=1e-12, atol=1e-12)
+        root = cr.crown(net, x0, eps, C)
+        al, au = _random_alpha(A, net, root, m, rng)
+        lb, ub, gl, gu = A.alpha_bound(net, root, C, al, au)
+        n_checked = 0
+        for i in al:
+            unst = np.flatnonzero(A.unstable_mask(root, i).reshape(-1))
+            for j in rng.choice(unst, size=min(4, unst.size), replace=False) if unst.size else []:
+                for q in range(min(m, 3)):
+                    for which in ("l", "u"):
+                        h = 1e-6
+                        a0 = al if which == "l" else au
+                        plus = {k: v.copy() for k, v in a0.items()}
+                        minus = {k: v.copy() for k, v in a0.items()}
+                        plus[i][q, j] += h
+                        minus[i][q, j] -= h
+                        k = 0 if which == "l" else 1
+                        args_p = (plus, au) if which == "l" else (al, plus)
+                        args_m = (minus, au) if which == "l" else (al, minus)
+                        fd = (A.alpha_bound(net, root, C, *args_p)[k][q] - A.alpha_bound(net, root, C, *args_m)[k][q]) / (2 * h)
+                        g = (gl if which == "l" else gu)[i][q, j]
+                        assert abs(fd - g) <= 1e-6 * (1.0 + abs(g)), (i, j, q, which, fd, g)
+                        n_checked += 1
+        assert n_checked >= 12
+        lo, hi = box_of(x0, eps, (0.0, 1.0))
+        X = np.concatenate([lo + (hi - lo) * rng.random((3000, lo.size)), np.where(rng.random((1000, lo.size)) < 0.5, lo, hi)])
+        Y = spec_values(net, C, X)
+        r = A.alpha_crown(net, x0, eps, C, iters=20, root=root)
+        assert np.all(r.lb >= root.lb) and np.all(r.ub <= root.ub)
+        for a_l, a_u in (_random_alpha(A, net, root, m, rng), (r.alpha_l, r.alpha_u)):
+            lb, ub, _, _ = A.alpha_bound(net, root, C, a_l, a_u)
+            assert np.all(Y >= lb[None, :] - 1e-9 * (1 + np.abs(Y)))
+            assert np.all(Y <= ub[None, :] + 1e-9 * (1 + np.abs(Y)))
+
+
+def pin_alpha_residual_lp(A):
+    """A dense residual block with one ReLU layer: the optimised bound reaches the triangle
+    LP's optimum (minimax over the slopes) and never passes it."""
+    for seed in (84, 85, 87):   # cases where CROWN leaves a gap to the LP
+        net, x0, C = _residual_dense(seed, n0=4, hid=12)
+        r = A.alpha_crown(net, x0[0], np.float32(0.3), C[0], iters=300, lr=0.05)
+        lp_lo = residual_lp(net, r.root, C[0], upper=False)
+        lp_hi = residual_lp(net, r.root, C[0], upper=True)
+        assert np.all(r.lb <= lp_lo + 1e-7 * (1 + np.abs(lp_lo)))
+        assert np.all(r.ub >= lp_hi - 1e-7 * (1 + np.abs(lp_hi)))
+        gap0_l, gap_l = lp_lo - r.root.lb, lp_lo - r.lb
+        gap0_u, gap_u = r.root.ub - lp_hi, r.ub - lp_hi
+        assert np.all(gap_l <= 1e-3 * (1 + np.abs(lp_lo)) + 0.02 * gap0_l), (seed, gap_l, gap0_l)
+        assert np.all(gap_u <= 1e-3 * (1 + np.abs(lp_hi)) + 0.02 * gap0_u), (seed, gap_u, gap0_u)
+        assert np.any(gap0_l > 1e-3), "the case should leave CROWN a gap to close"
+
+
 ALPHA_PINS = [pin_alpha_reduces_to_crown, pin_alpha_gradient_fd, pin_alpha_lp, pin_alpha_sound,
-              pin_alpha_history]
+              pin_alpha_history, pin_alpha_residual_nets, pin_alpha_residual_lp]

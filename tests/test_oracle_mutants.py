@@ -76,6 +76,12 @@ ALPHA_MUTANTS = {
                             "a[i] + sign * lr * mhat / (np.sqrt(vhat) + adam_eps)"),
     "alpha_upper_ascends": ('(("l", al, gl, 1.0), ("u", au, gu, -1.0))', '(("l", al, gl, 1.0), ("u", au, gu, 1.0))'),
     "alpha_best_not_kept": ("best_l = np.where(better_l, lb, best_l)", "best_l = lb"),
+    # residual networks: one input of an add dropped in the backward pass, or in the forward
+    # evaluation of the gradient
+    "alpha_pass_add_drops_branch": ("            add_to(nd.in0, A)\n            add_to(nd.in1, A)",
+                                    "            add_to(nd.in0, A)"),
+    "alpha_grad_add_drops_skip": ("val[i] = v.reshape(rows, -1) + get(nd.in1).reshape(rows, -1)",
+                                  "val[i] = v.reshape(rows, -1)"),
 }
 
 
