@@ -97,7 +97,7 @@ def cpu_baseline(wl, budget_s, alpha_iters=0):
             "sample": f"first {n} of the {wl.x0.shape[0]} inputs of the same batch, {dt:.1f} s", **host_info()}
 
 
-def cpu_baseline_sampled(wl, budget_s, chunk):
+def cpu_baseline_sampled(wl, budget_s, chunk, alpha_iters=0):
     """One input of the wide MLP or the full ResNet takes the fp64 oracle minutes to hours,
     so its time per input is estimated from a timed sample of the oracle's own steps on
     input 0: the box, the IBP pass and a first ReLU on an affine map of the input run whole;
@@ -105,7 +105,9 @@ def cpu_baseline_sampled(wl, budget_s, chunk):
     oracle's backward pass and concretization (lower and upper), as the oracle processes
     them, until that layer's share of the budget is used, and the per-row time is scaled to
     the layer's row count.  The cost of a row does not depend on the relaxation values, so
-    the sample uses the IBP bounds' relaxation."""
+    the sample uses the IBP bounds' relaxation.  With alpha_iters, the alpha-CROWN oracle's
+    evaluation (both bounds and their gradients) of a chunk of spec rows is timed as well and
+    scaled to all spec rows and the alpha_iters + 1 evaluations."""
     import oracle
     net = wl.net
     shapes = oracle.node_shapes(net)
@@ -149,6 +151,20 @@ def cpu_baseline_sampled(wl, budget_s, chunk):
         dt = time.perf_counter() - t0
         total += dt / done * n_rows
         parts.append(f"{done}/{n_rows} rows of node {z} in {dt:.1f} s")
+    if alpha_iters:
+        from types import SimpleNamespace
+        from oracle import alpha64
+        root = SimpleNamespace(relax={i: tuple(v.reshape(shapes[i]) for v in relax[i]) for i in relus},
+                               layer_l={i: IL[net.nodes[i].in0] for i in relus},
+                               layer_u={i: IU[net.nodes[i].in0] for i in relus}, box=(lo, hi))
+        rows = min(chunk, wl.C.shape[1])
+        al, au = alpha64.initial_alpha(net, root, rows)
+        t0 = time.perf_counter()
+        alpha64.alpha_bound(net, root, wl.C[0][:rows], al, au)
+        dt = time.perf_counter() - t0
+        total += dt / rows * wl.C.shape[1] * (alpha_iters + 1)
+        parts.append(f"one alpha-CROWN evaluation with gradients of {rows}/{wl.C.shape[1]} spec rows in {dt:.1f} s, "
+                     f"scaled to {alpha_iters + 1} evaluations")
     return {"value": 1.0 / total, "unit": "inputs/s", "cores": _threads(), "kind": "oracle",
             "sample": f"estimated from timed steps of input 0 ({chunk}-row chunks), scaled to each layer's rows: "
                       + "; ".join(parts) + f"; {total:.0f} s per input", **host_info()}
@@ -279,7 +295,7 @@ def main():
     ap.add_argument("--workload", default="mlp3072x8192x4")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time (0: skip)")
     ap.add_argument("--alpha-iters", type=int, default=0,
-                    help="alpha-CROWN with this many Adam steps on the final pass (MLPs; 0: CROWN)")
+                    help="alpha-CROWN with this many Adam steps on the final pass (0: CROWN)")
     ap.add_argument("--bab-loop", type=int, default=0, metavar="BATCH",
                     help="run the fixed-batch branch-and-bound loop (10 rounds, beta-CROWN bounds) with this batch "
                          "on the bab_ workload's root input; value = subdomains bounded per second")
@@ -307,9 +323,8 @@ def main():
     if args.bab_loop:
         return bench_bab_loop(args)
 
-    if args.alpha_iters and not args.workload.startswith("mlp"):
-        print("--alpha-iters runs on the MLP workloads (alpha-CROWN is built for dense/relu networks)",
-              file=sys.stderr)
+    if args.alpha_iters and (args.workload.startswith("bab_") or args.workload.startswith("exp1_")):
+        print("--alpha-iters runs on the input-batch workloads (MLPs and ResNets)", file=sys.stderr)
         sys.exit(2)
     import torch
     from paper_2606_09377_amd import Ctx
@@ -430,7 +445,8 @@ def main():
         rec["roofline_other"] = [roofline(k) for k in other]
     rec.update(extra)
     if args.cpu_budget > 0 and args.workload in SAMPLED_BASELINE:
-        rec["cpu_baseline"] = cpu_baseline_sampled(wl, args.cpu_budget, SAMPLED_BASELINE[args.workload])
+        rec["cpu_baseline"] = cpu_baseline_sampled(wl, args.cpu_budget, SAMPLED_BASELINE[args.workload],
+                                                   args.alpha_iters)
     elif args.cpu_budget > 0 and splits is None:
         rec["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget, args.alpha_iters)
     elif args.cpu_budget > 0:

@@ -221,8 +221,9 @@ vcr_status vcr_crown_bounds(vcr_ctx *ctx, const float *x0, int32_t B, float eps,
  *
  * Slope arrays use the compact layout [B][2m][n_total]: row q < m holds the slopes of the
  * lower bound of specification row q, row m + q those of its upper bound; the columns are
- * the neurons of every ReLU node in node order (n_total = sum of their sizes).  Entries of
- * neurons that are not unstable are ignored on input and report the fixed slope on output. */
+ * the neurons of every ReLU node in node order (n_total = sum of their sizes), each node's
+ * neurons in its own (C, H, W) order.  Entries of neurons that are not unstable are ignored
+ * on input and report the fixed slope on output. */
 typedef struct {
   int32_t iters;            /* optimisation steps after the first evaluation (>= 0) */
   float lr;                 /* Adam step size (> 0) */
@@ -239,8 +240,11 @@ typedef struct {
  * vcr_crown_bounds, IBP-intersected when that option is on); the final pass is evaluated
  * iters + 1 times, with projected Adam steps on the slopes in between (ascent on every
  * lower bound, descent on every upper bound), and each bound is the best one evaluated.
- * Networks of dense and relu nodes only (VCR_ERR_UNSUPPORTED otherwise); x0, C, lb, ub as
- * in vcr_crown_bounds without splits.  All arrays are caller-owned device memory. */
+ * Every network vcr_crown_bounds takes: dense/relu chains, and convolutional networks with
+ * residual additions and flatten (VCR_ERR_UNSUPPORTED, with the reason in vcr_last_error,
+ * for a ReLU whose input is not a convolution or dense node, or an add of the network
+ * input); x0, C, lb, ub as in vcr_crown_bounds without splits.  All arrays are caller-owned
+ * device memory. */
 vcr_status vcr_alpha_crown_bounds(vcr_ctx *ctx, const float *x0, int32_t B, float eps,
                                   const float *C, int32_t m, const vcr_alpha_opts *opts,
                                   float *lb, float *ub);

@@ -8,6 +8,13 @@
 
 namespace vcr {
 
+// column of neuron n (this layer's order) in the compact per-row layout
+__device__ __forceinline__ int64_t compact_col(const AlphaLayer &l, int64_t n) {
+  if (l.hwc_C == 0) return n;
+  const int64_t pos = n / l.hwc_C;
+  return (n - pos * l.hwc_C) * l.hwc_HW + pos;
+}
+
 __global__ void k_alpha_init(AlphaLayer l, const float *alpha_init, int64_t n_total, int32_t rows, int32_t rows_pad,
                              int32_t rows_per_unit) {
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -18,8 +25,8 @@ __global__ void k_alpha_init(AlphaLayer l, const float *alpha_init, int64_t n_to
   if (row < rows && n < l.n) {
     // unstable neurons (t > 0) take the given slope, the others keep their fixed one
     const int64_t u = row / rows_per_unit;
-    const float4 prm = l.P[u * l.ld + n];
-    a = (alpha_init && prm.z > 0.f) ? alpha_init[row * n_total + l.col0 + n] : prm.x;
+    const float4 prm = l.P[u * l.ldp + n];
+    a = (alpha_init && prm.z > 0.f) ? alpha_init[row * n_total + l.col0 + compact_col(l, n)] : prm.x;
   }
   l.alpha[idx] = a;
   l.best[idx] = a;
@@ -222,7 +229,7 @@ __global__ void k_alpha_out(AlphaLayer l, int32_t rows, int32_t m, int64_t n_tot
   const int64_t row = idx / l.n;
   const int64_t n = idx - row * l.n;
   const int64_t q = row % (2 * m);
-  const int64_t src = row * l.ld + n, dst = row * n_total + l.col0 + n;
+  const int64_t src = row * l.ld + n, dst = row * n_total + l.col0 + compact_col(l, n);
   if (alpha_out) alpha_out[dst] = l.best[src];
   if (grad_out) grad_out[dst] = q < m ? l.grad[src] : -l.grad[src];
 }

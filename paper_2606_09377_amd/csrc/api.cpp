@@ -40,8 +40,10 @@ vcr_status graph_crown(vcr_ctx *c, const float *x0, int32_t B, float eps, const 
                        const vcr_splits *splits, float *lb, float *ub);
 vcr_status graph_ibp(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m, float *lb,
                      float *ub);
-size_t graph_workspace_bytes(vcr_ctx *c, int32_t B, int32_t m);
-vcr_status graph_plan(vcr_ctx *c, int32_t B, int32_t m, int *chunk_out, size_t *bytes_out);
+vcr_status graph_alpha(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m,
+                       const vcr_alpha_opts &o, int64_t n_total, float *lb, float *ub);
+size_t graph_workspace_bytes(vcr_ctx *c, int32_t B, int32_t m, bool alpha);
+vcr_status graph_plan(vcr_ctx *c, int32_t B, int32_t m, int *chunk_out, size_t *bytes_out, bool alpha);
 }  // namespace vcr
 
 namespace {
@@ -612,6 +614,7 @@ void carve(const vcr_ctx *c, Workspace &w, const Plan &p, int32_t S, CallBufs *b
     for (int k = 0; k < L - 1; ++k) {
       AlphaLayer a{};
       a.ld = c->layers[k].ld_out;
+      a.ldp = a.ld;
       a.n = c->layers[k].n_out;
       a.col0 = col0;
       col0 += a.n;
@@ -1178,7 +1181,7 @@ vcr_status vcr::crown_bounds_in(vcr_ctx *c, const float *x0, int32_t B, float ep
   size_t need = 0;
   if (c->graph) {
     int chunk = 0;
-    st = graph_plan(c, B, m, &chunk, &need);
+    st = graph_plan(c, B, m, &chunk, &need, false);
   } else {
     Plan p;
     st = make_plan(c, B, m, 0, 0, &p);
@@ -1266,7 +1269,6 @@ vcr_status vcr_alpha_crown_bounds(vcr_ctx *c, const float *x0, int32_t B, float 
   vcr_status st = check_common(c, x0, B, eps, C, m, lb, ub);
   if (st != VCR_OK) return st;
   if (!opts) return fail(c, VCR_ERR_ARG, "null alpha options");
-  if (c->graph) return fail(c, VCR_ERR_UNSUPPORTED, "alpha-CROWN is built for networks of dense and relu nodes");
   if (c->relu_n.empty()) return fail(c, VCR_ERR_ARG, "alpha-CROWN needs at least one ReLU");
   const vcr_alpha_opts &o = *opts;
   if (o.iters < 0 || o.iters > 1000000) return fail(c, VCR_ERR_ARG, "iters must be in [0, 1e6]");
@@ -1280,6 +1282,7 @@ vcr_status vcr_alpha_crown_bounds(vcr_ctx *c, const float *x0, int32_t B, float 
   if ((int64_t)B * 2 * m * ac.n_total > ((int64_t)1 << 40)) return fail(c, VCR_ERR_SHAPE, "alpha tensors too large");
   st = check_finite_inputs(c, x0, B, C, m);
   if (st != VCR_OK) return st;
+  if (c->graph) return after_call(c, graph_alpha(c, x0, B, eps, C, m, o, ac.n_total, lb, ub), t0);
   return after_call(c, crown_impl(c, x0, B, eps, C, m, nullptr, lb, ub, &ac), t0);
 }
 
@@ -1568,7 +1571,7 @@ vcr_status vcr_workspace_bytes(vcr_ctx *c, int32_t B, int32_t m, int32_t n_domai
   if (B <= 0 || m <= 0 || n_domains < 0) return fail(c, VCR_ERR_ARG, "bad sizes");
   if (c->graph) {
     if (n_domains > 0) return fail(c, VCR_ERR_UNSUPPORTED, "subdomain splits are built for MLPs only");
-    *bytes = graph_workspace_bytes(c, B, m);
+    *bytes = graph_workspace_bytes(c, B, m, false);
     return VCR_OK;
   }
   const uint64_t cap = c->ws_cap;

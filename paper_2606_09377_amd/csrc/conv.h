@@ -47,6 +47,10 @@ struct ConvTArgs {
   const float *bias;         // identity: constant per channel
   float *out;                // [R][S_in][S_in][C_in]
   float *part;               // [N_pad / 64][M_pad]
+  // alpha-CROWN (dense windows with a ReLU only): per-row lower slopes at unstable neurons,
+  // and the coefficients before relaxation, both laid out like out
+  const float *alpha;
+  float *pre;
   // filled by launch_convt
   int32_t n_cls;
   ConvClass cls[4];
@@ -73,6 +77,10 @@ struct StemArgs {
   const float *c0, *r0;    // box centre / radius, CHW per unit
   int64_t ld_box;          // floats per unit in c0 / r0
   float *part;             // [R][S_in^2]
+  // optional (dense windows): the box vertex where each row's linear function is smallest,
+  // c - sign(a) r per input neuron (the centre where a = 0), channels-last [R][ld_vtx]
+  float *vtx;
+  int64_t ld_vtx;
 };
 hipError_t launch_stem(const StemArgs &a, hipStream_t s);
 
@@ -90,6 +98,32 @@ struct ConvInitArgs {
   float *beta;
 };
 hipError_t launch_init_conv(const ConvInitArgs &a, hipStream_t s);
+
+// Forward 3x3 convolution (pad 1) of `rows` channels-last images, the gradient pass of
+// alpha-CROWN: out = conv(in) + bias (+ res), or with a ReLU line: the line of that ReLU the
+// backward pass chose for the row (by the sign of the coefficient `pre` it recorded), and the
+// slope gradient pre * D at unstable neurons whose coefficient is positive (else 0).
+struct FwdConvArgs {
+  const float *in;         // [rows][in_rs]: (Hi, Hi, Ci) channels-last
+  int64_t in_rs;
+  int32_t Ci, Hi;
+  const float *Wk;         // [Co][3][3][Ci]
+  const float *bias;       // [Co]
+  int32_t Co, Ho, stride;
+  int32_t rows;
+  const float *res;        // optional [rows][res_rs], (Ho, Ho, Co): added to D
+  int64_t res_rs;
+  const float4 *P;         // optional ReLU parameters [units][Ho][Ho][Co]
+  int32_t rows_per_unit, units;
+  const float *alpha, *pre;  // [rows][out_rs] with P
+  float *grad;               // [rows][out_rs] with P
+  float *out;              // [rows][out_rs], (Ho, Ho, Co)
+  int64_t out_rs;
+};
+hipError_t launch_fwd_conv(const FwdConvArgs &a, hipStream_t s);
+// out = x + y over rows of n values (the add node in the gradient pass)
+hipError_t launch_fwd_add(const float *x, int64_t xs, const float *y, int64_t ys, float *out, int64_t os,
+                          int32_t rows, int64_t n, hipStream_t s);
 hipError_t launch_rowsum_win(float *beta, const float *part, int32_t n_parts, int64_t M_pad, int64_t R,
                              int32_t per_row, hipStream_t s);
 hipError_t launch_row_table(int4 *rows, int64_t R, int32_t rows_per_unit, int32_t C, int32_t H, int32_t W,

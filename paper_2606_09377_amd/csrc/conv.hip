@@ -62,7 +62,7 @@ __device__ __attribute__((aligned(16))) float g_zero4[4] = {0.f, 0.f, 0.f, 0.f};
 // Epilogue shared by the transposed-convolution kernels: relaxation (or identity), residual,
 // constant terms per GEMM row for the tile m0.. of class cl, columns n0..; acc holds the
 // MB x NB 32 x 32 MFMA blocks of wave (wm, wn); scratch is >= 24 BM bytes of free LDS.
-template <int BM, int BN, int WM, int WN, bool RELU>
+template <int BM, int BN, int WM, int WN, bool RELU, bool AL>
 __device__ __forceinline__ void convt_epilogue(const ConvTArgs &p, const ConvClass &cl,
                                                const f32x16 (&acc)[BM / WM / 32][BN / WN / 32], int m0, int n0,
                                                int nt, float *scratch) {
@@ -84,6 +84,8 @@ __device__ __forceinline__ void convt_epilogue(const ConvTArgs &p, const ConvCla
   const float4 *__restrict__ Pp = p.P_pos;
   const float *__restrict__ resp = p.res;
   float *__restrict__ outp = p.out;
+  const float *__restrict__ alp = p.alpha;
+  float *__restrict__ prep = p.pre;
   for (int tr = tid; tr < BM; tr += 256) {
     const int m = m0 + tr;
     const bool valid = m < cl.M;
@@ -155,17 +157,26 @@ __device__ __forceinline__ void convt_epilogue(const ConvTArgs &p, const ConvCla
 #pragma unroll
       for (int j = 0; j < NB; ++j) {
         const float a = acc[i][j][g * 4 + t] + rv[j][t];
+        const bool store = mo >= 0 && ncol[j] < p.C_in;
         float ap = 0.f;
         if (pb >= 0) {   // inside the image: relax (or identity) and constant terms
           if constexpr (RELU) {
-            ap = a > 0.f ? a * prm[b][j][t].x : a * prm[b][j][t].y;
+            float lam = prm[b][j][t].x;
+            if constexpr (AL) {   // alpha-CROWN: the row's own slope at unstable neurons
+              const float al = store ? alp[ob + ncol[j]] : 0.f;
+              lam = prm[b][j][t].z > 0.f ? al : lam;
+            }
+            ap = a > 0.f ? a * lam : a * prm[b][j][t].y;
             x += fminf(a, 0.f) * prm[b][j][t].z + ap * prm[b][j][t].w;
           } else {
             ap = a;
             x += a * bn[j];
           }
         }
-        if (mo >= 0 && ncol[j] < p.C_in) outp[ob + ncol[j]] = ap;
+        if (store) {
+          outp[ob + ncol[j]] = ap;
+          if constexpr (AL) prep[ob + ncol[j]] = a;
+        }
       }
       rp[g * 4 + t] = x;
     }
@@ -192,8 +203,9 @@ __device__ __forceinline__ void convt_epilogue(const ConvTArgs &p, const ConvCla
 }
 
 // RELU: the destination node feeds a ReLU (relaxation parameters P_pos), else the identity
-// with a per-channel constant (bias).
-template <int BM, int BN, int BK, int WM, int WN, int MINB, bool RELU>
+// with a per-channel constant (bias).  AL (with RELU, dense windows): alpha-CROWN's per-row
+// slopes and the record of the coefficients before relaxation.
+template <int BM, int BN, int BK, int WM, int WN, int MINB, bool RELU, bool AL = false>
 __global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
   static_assert(BK == 16 || BK == 32, "LDS swizzle assumes 4 or 8 chunks per row");
   constexpr int CPR = BK / 4;                 // 16-byte chunks per tile row
@@ -321,7 +333,7 @@ __global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
 
   // ---- epilogue (the operand buffers are free after the main loop's last barrier) ----
   static_assert(24 * BM <= (int)sizeof(As), "epilogue row information must fit the A buffers");
-  convt_epilogue<BM, BN, WM, WN, RELU>(p, cl, acc, m0, n0, nt, &As[0][0]);
+  convt_epilogue<BM, BN, WM, WN, RELU, AL>(p, cl, acc, m0, n0, nt, &As[0][0]);
 }
 
 // Classes of one axis: positions u of the destination window with the same taps ky, as an
@@ -457,17 +469,23 @@ hipError_t launch_convt_part(const ConvTArgs &a0, int part, hipStream_t s) {
   if (!convt_plan(a0, cu, plan) || part < 0 || part >= (int)plan.size()) return hipErrorInvalidValue;
   const ConvtDispatch &d = plan[part];
   ConvTArgs a = a0;
+  const bool al = a.alpha || a.pre;
+  if (al && (!a.alpha || !a.pre || !a.P_pos || !a.dense)) return hipErrorInvalidValue;
   if (a.N_pad % 128 == 0) {   // 128 x 128 tiles, 2 x 2 waves of 64 x 64
     const int64_t blk = convt_fill(a, cu, d, 128, 128);
     if (blk < 0) return hipErrorInvalidValue;
-    if (blk > 0 && a.P_pos)
+    if (blk > 0 && al)
+      hipLaunchKernelGGL((k_convt<128, 128, 16, 2, 2, 2, true, true>), dim3((unsigned)blk), dim3(256), 0, s, a);
+    else if (blk > 0 && a.P_pos)
       hipLaunchKernelGGL((k_convt<128, 128, 16, 2, 2, 3, true>), dim3((unsigned)blk), dim3(256), 0, s, a);
     else if (blk > 0)
       hipLaunchKernelGGL((k_convt<128, 128, 16, 2, 2, 3, false>), dim3((unsigned)blk), dim3(256), 0, s, a);
   } else {                           // 256 x 64 tiles, 4 x 1 waves of 64 x 64
     const int64_t blk = convt_fill(a, cu, d, 256, 64);
     if (blk < 0) return hipErrorInvalidValue;
-    if (blk > 0 && a.P_pos)
+    if (blk > 0 && al)
+      hipLaunchKernelGGL((k_convt<256, 64, 16, 4, 1, 2, true, true>), dim3((unsigned)blk), dim3(256), 0, s, a);
+    else if (blk > 0 && a.P_pos)
       hipLaunchKernelGGL((k_convt<256, 64, 16, 4, 1, 3, true>), dim3((unsigned)blk), dim3(256), 0, s, a);
     else if (blk > 0)
       hipLaunchKernelGGL((k_convt<256, 64, 16, 4, 1, 3, false>), dim3((unsigned)blk), dim3(256), 0, s, a);
@@ -666,6 +684,12 @@ __global__ __launch_bounds__(256, 3) void k_stem(const StemArgs p) {
         }
 #pragma unroll
         for (int ci = 0; ci < CIN; ++ci) part += a[ci] * bc[q][ci] - fabsf(a[ci]) * br[q][ci];
+        if (p.vtx) {   // dense windows: (u, w) is the image position
+          float *v = p.vtx + (int64_t)(r0 + rl) * p.ld_vtx + (u * p.H_in + w) * CIN;
+#pragma unroll
+          for (int ci = 0; ci < CIN; ++ci)
+            v[ci] = a[ci] > 0.f ? bc[q][ci] - br[q][ci] : (a[ci] < 0.f ? bc[q][ci] + br[q][ci] : bc[q][ci]);
+        }
       }
       p.part[(int64_t)(r0 + rl) * S_in2 + u * p.S_in + w] = part;
     }
@@ -678,6 +702,8 @@ hipError_t launch_stem_t(StemArgs a, hipStream_t s) {
   constexpr int NB = CIN * 9 > 32 ? 2 : 1;
   constexpr int GP = 32 * NB + 1;
   if (a.C_out <= 0 || a.C_out % 32 || a.R <= 0 || (a.stride != 1 && a.stride != 2) || a.S_out <= 0 || a.S_in <= 0)
+    return hipErrorInvalidValue;
+  if (a.vtx && (!a.dense || a.S_in != a.H_in || a.ld_vtx < (int64_t)a.H_in * a.H_in * CIN))
     return hipErrorInvalidValue;
   const int64_t wt_floats = 32 * NB * (int64_t)(a.C_out + 4);
   // 42 KB of LDS per workgroup (three workgroups per CU), 64 KB for wide weights
@@ -1112,6 +1138,242 @@ FastDiv make_fastdiv(uint32_t d) {
     f.shift = 0;
   }
   return f;
+}
+
+
+// ------------------------------------------------------------------------------------
+// Forward 3x3 convolution (pad 1, stride 1 or 2) of channels-last images: alpha-CROWN's
+// gradient pass evaluates the relaxed network forward from each coefficient row's box vertex
+// (every row is one image).  Implicit GEMM with M = rows x Ho^2 output positions, N = Co,
+// K = 9 Ci (tap outer, 16 input channels per K tile), the same LDS tiling and MFMA blocking
+// as the transposed convolution above; inputs with at most 4 channels (the network input)
+// take a plain per-output kernel instead.
+
+// One output element: D = acc + bias (+ residual), then the identity or the ReLU line
+// selected by the recorded coefficient's sign (lam D where it is positive, s D + t where it
+// is negative, s D where it is 0), with the slope gradient at unstable neurons.
+__device__ __forceinline__ void fwd_store(const FwdConvArgs &p, int64_t r, int32_t pos, int32_t n, float acc) {
+  float D = acc + p.bias[n];
+  const int64_t q = (int64_t)pos * p.Co + n;
+  if (p.res) D += p.res[r * p.res_rs + q];
+  const int64_t off = r * p.out_rs + q;
+  if (p.P) {
+    int64_t u = r / p.rows_per_unit;
+    u = u < p.units ? u : p.units - 1;
+    const float4 prm = p.P[u * ((int64_t)p.Ho * p.Ho * p.Co) + q];
+    const bool unst = prm.z > 0.f;
+    const float lam = unst ? p.alpha[off] : prm.x;
+    const float an = p.pre[off];
+    p.out[off] = an > 0.f ? lam * D : prm.y * D + (an < 0.f ? prm.z : 0.f);
+    p.grad[off] = (unst && an > 0.f) ? an * D : 0.f;
+  } else {
+    p.out[off] = D;
+  }
+}
+
+template <int BM, int BN, int WM, int WN>
+__global__ __launch_bounds__(256, 2) void k_fwd_conv(const FwdConvArgs p, FastDiv div_pos) {
+  constexpr int BK = 16, CPR = BK / 4, TPR = CPR, RPP = 256 / TPR;
+  constexpr int MB = BM / WM / 32, NB = BN / WN / 32;
+  constexpr int QA = BM / RPP, QB = BN / RPP;
+  __shared__ __attribute__((aligned(16))) float As[2][BM * BK];
+  __shared__ __attribute__((aligned(16))) float Bs[2][BN * BK];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int n_nt = (p.Co + BN - 1) / BN;
+  const int mt = blockIdx.x / n_nt, nt = blockIdx.x - mt * n_nt;
+  const int m0 = mt * BM, n0 = nt * BN;
+  const int HW = p.Ho * p.Ho;
+  const uint32_t Mtot = (uint32_t)p.rows * (uint32_t)HW;
+
+  const int lrow = tid / TPR, lcol = (tid % TPR) * 4;
+  const int scol = ((tid % TPR) ^ lds_swz<BK>(lrow)) * 4;
+  const float *a_row[QA];
+  int yi0[QA], xi0[QA];
+#pragma unroll
+  for (int q = 0; q < QA; ++q) {
+    const uint32_t m = (uint32_t)(m0 + lrow + RPP * q);
+    const bool valid = m < Mtot;
+    const uint32_t r = valid ? fdiv(m, div_pos) : 0u;
+    const int pos = (int)(m - r * (uint32_t)HW);
+    const int yo = pos / p.Ho, xo = pos - yo * p.Ho;
+    a_row[q] = p.in + (int64_t)r * p.in_rs;
+    yi0[q] = valid ? yo * p.stride - 1 : -(1 << 20);   // an invalid row reads zeros only
+    xi0[q] = xo * p.stride - 1;
+  }
+  const float *b_row[QB];
+#pragma unroll
+  for (int q = 0; q < QB; ++q) {
+    const int co = n0 + lrow + RPP * q;
+    b_row[q] = co < p.Co ? p.Wk + (int64_t)co * 9 * p.Ci + lcol : nullptr;
+  }
+  const int cpt = p.Ci / BK;   // K tiles per tap
+  f32x4 ra[QA], rb[QB];
+  auto gload = [&](int kt) {
+    const int t = kt / cpt, c0 = (kt - t * cpt) * BK;
+    const int ky = t / 3, kx = t - ky * 3;
+#pragma unroll
+    for (int q = 0; q < QA; ++q) {
+      const int yy = yi0[q] + ky, xx = xi0[q] + kx;
+      const bool ok = (unsigned)yy < (unsigned)p.Hi && (unsigned)xx < (unsigned)p.Hi;
+      const float *src = ok ? a_row[q] + ((int64_t)yy * p.Hi + xx) * p.Ci + c0 + lcol : g_zero4;
+      ra[q] = *reinterpret_cast<const f32x4 *>(src);
+    }
+#pragma unroll
+    for (int q = 0; q < QB; ++q) {
+      const float *src = b_row[q] ? b_row[q] + t * p.Ci + c0 : g_zero4;
+      rb[q] = *reinterpret_cast<const f32x4 *>(src);
+    }
+  };
+  auto lstore = [&](int buf) {
+#pragma unroll
+    for (int q = 0; q < QA; ++q) *reinterpret_cast<f32x4 *>(&As[buf][(lrow + RPP * q) * BK + scol]) = ra[q];
+#pragma unroll
+    for (int q = 0; q < QB; ++q) *reinterpret_cast<f32x4 *>(&Bs[buf][(lrow + RPP * q) * BK + scol]) = rb[q];
+  };
+  f32x16 acc[MB][NB];
+#pragma unroll
+  for (int i = 0; i < MB; ++i)
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+  const int KT = 9 * cpt;
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  const int r32 = lane & 31, sw = lds_swz<BK>(r32);
+  int roff[CPR / 2];
+#pragma unroll
+  for (int h = 0; h < CPR / 2; ++h) roff[h] = ((((lane >> 5) * (CPR / 2)) + h) ^ sw) * 4;
+  for (int kt = 0; kt < KT; ++kt) {
+    const int cur = kt & 1;
+    const bool more = kt + 1 < KT;
+    if (more) gload(kt + 1);
+    const float *as = As[cur] + (wm * (BM / WM) + r32) * BK;
+    const float *bs = Bs[cur] + (wn * (BN / WN) + r32) * BK;
+#pragma unroll
+    for (int h = 0; h < CPR / 2; ++h) {
+      f32x4 a[MB], b[NB];
+#pragma unroll
+      for (int i = 0; i < MB; ++i) a[i] = *reinterpret_cast<const f32x4 *>(as + i * 32 * BK + roff[h]);
+#pragma unroll
+      for (int j = 0; j < NB; ++j) b[j] = *reinterpret_cast<const f32x4 *>(bs + j * 32 * BK + roff[h]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+#pragma unroll
+        for (int i = 0; i < MB; ++i)
+#pragma unroll
+          for (int j = 0; j < NB; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][e], b[j][e], acc[i][j], 0, 0, 0);
+    }
+    if (more) lstore(cur ^ 1);
+    __syncthreads();
+  }
+  // epilogue: row and position of every tile row once, through the free A buffer
+  int *s_r = reinterpret_cast<int *>(&As[0][0]);
+  int *s_pos = s_r + BM;
+  for (int tr = tid; tr < BM; tr += 256) {
+    const uint32_t m = (uint32_t)(m0 + tr);
+    const uint32_t r = m < Mtot ? fdiv(m, div_pos) : 0u;
+    s_r[tr] = m < Mtot ? (int)r : -1;
+    s_pos[tr] = (int)(m - r * (uint32_t)HW);
+  }
+  __syncthreads();
+  const int half = lane >> 5;
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const int n = n0 + wn * (BN / WN) + j * 32 + r32;
+    if (n >= p.Co) continue;
+#pragma unroll
+    for (int i = 0; i < MB; ++i)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int lr = wm * (BM / WM) + i * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
+        const int r = s_r[lr];
+        if (r >= 0) fwd_store(p, r, s_pos[lr], n, acc[i][j][v]);
+      }
+  }
+}
+
+// inputs with CIN <= 4 channels: one thread per output element, channels fastest
+template <int CIN>
+__global__ void k_fwd_conv_small(const FwdConvArgs p) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int HW = p.Ho * p.Ho;
+  if (idx >= (int64_t)p.rows * HW * p.Co) return;
+  const int n = (int)(idx % p.Co);
+  const int64_t rp = idx / p.Co;
+  const int64_t r = rp / HW;
+  const int pos = (int)(rp - r * HW);
+  const int yo = pos / p.Ho, xo = pos - yo * p.Ho;
+  const float *x = p.in + r * p.in_rs;
+  const float *w = p.Wk + (int64_t)n * 9 * CIN;
+  float acc = 0.f;
+#pragma unroll
+  for (int ky = 0; ky < 3; ++ky) {
+    const int yy = yo * p.stride - 1 + ky;
+    if ((unsigned)yy >= (unsigned)p.Hi) continue;
+#pragma unroll
+    for (int kx = 0; kx < 3; ++kx) {
+      const int xx = xo * p.stride - 1 + kx;
+      if ((unsigned)xx >= (unsigned)p.Hi) continue;
+      const float *xs = x + ((int64_t)yy * p.Hi + xx) * CIN;
+#pragma unroll
+      for (int ci = 0; ci < CIN; ++ci) acc += xs[ci] * w[(ky * 3 + kx) * CIN + ci];
+    }
+  }
+  fwd_store(p, r, pos, n, acc);
+}
+
+hipError_t launch_fwd_conv(const FwdConvArgs &a, hipStream_t s) {
+  if (a.rows <= 0 || a.Co <= 0 || a.Ci <= 0 || a.Hi <= 0 || (a.stride != 1 && a.stride != 2) ||
+      a.Ho != (a.Hi - 1) / a.stride + 1 || !a.in || !a.Wk || !a.bias || !a.out)
+    return hipErrorInvalidValue;
+  if (a.P && (!a.alpha || !a.pre || !a.grad || a.rows_per_unit <= 0 || a.units <= 0 || a.res))
+    return hipErrorInvalidValue;
+  const int64_t HW = (int64_t)a.Ho * a.Ho;
+  if (a.out_rs < HW * a.Co || a.in_rs < (int64_t)a.Hi * a.Hi * a.Ci || (a.res && a.res_rs < HW * a.Co))
+    return hipErrorInvalidValue;
+  if (a.Ci <= 4) {
+    const int64_t n = (int64_t)a.rows * HW * a.Co;
+    const unsigned grid = (unsigned)((n + 255) / 256);
+    switch (a.Ci) {
+      case 1: hipLaunchKernelGGL(k_fwd_conv_small<1>, dim3(grid), dim3(256), 0, s, a); break;
+      case 2: hipLaunchKernelGGL(k_fwd_conv_small<2>, dim3(grid), dim3(256), 0, s, a); break;
+      case 3: hipLaunchKernelGGL(k_fwd_conv_small<3>, dim3(grid), dim3(256), 0, s, a); break;
+      default: hipLaunchKernelGGL(k_fwd_conv_small<4>, dim3(grid), dim3(256), 0, s, a); break;
+    }
+    return hipGetLastError();
+  }
+  if (a.Ci % 16 || a.in_rs % 4) return hipErrorInvalidValue;   // 16-byte operand loads
+  const int64_t M = (int64_t)a.rows * HW;
+  if (M >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+  const FastDiv dp = make_fastdiv((uint32_t)HW);
+  if (a.Co % 128 == 0) {
+    const int64_t blk = (M + 127) / 128 * (a.Co / 128);
+    hipLaunchKernelGGL((k_fwd_conv<128, 128, 2, 2>), dim3((unsigned)blk), dim3(256), 0, s, a, dp);
+  } else {
+    const int64_t blk = (M + 255) / 256 * ((a.Co + 63) / 64);
+    hipLaunchKernelGGL((k_fwd_conv<256, 64, 4, 1>), dim3((unsigned)blk), dim3(256), 0, s, a, dp);
+  }
+  return hipGetLastError();
+}
+
+__global__ void k_fwd_add(const float *x, int64_t xs, const float *y, int64_t ys, float *out, int64_t os,
+                          int32_t rows, int64_t n) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)rows * n) return;
+  const int64_t r = idx / n, i = idx - r * n;
+  out[r * os + i] = x[r * xs + i] + y[r * ys + i];
+}
+
+hipError_t launch_fwd_add(const float *x, int64_t xs, const float *y, int64_t ys, float *out, int64_t os,
+                          int32_t rows, int64_t n, hipStream_t s) {
+  if (rows <= 0 || n <= 0) return hipSuccess;
+  const int64_t tot = (int64_t)rows * n;
+  hipLaunchKernelGGL(k_fwd_add, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, x, xs, y, ys, out, os, rows, n);
+  return hipGetLastError();
 }
 
 }  // namespace vcr

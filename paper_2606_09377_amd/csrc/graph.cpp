@@ -89,6 +89,19 @@ struct PassPlan {
   int64_t rows_per_unit_mult = 0;      // rows per unit = 2 * this (numel or m)
 };
 
+// One step of alpha-CROWN's gradient pass: the relaxed network evaluated forward on every
+// coefficient row, each row its own image (the box vertex where the row's bound is attained).
+enum FwdKind { FW_CONV, FW_DENSE, FW_ADD };
+
+struct FwdStep {
+  FwdKind kind;
+  int node = -1;               // node evaluated
+  int in = -1;                 // node whose values it reads (-1: the input vertex)
+  int res = -1;                // second summand (FW_CONV: a residual fused into the epilogue)
+  int out = -1;                // node whose values it writes: node, the ReLU it feeds, or the add
+  int relu = -1;               // ReLU index whose line (and slope gradient) is applied, or -1
+};
+
 }  // namespace
 
 struct GraphNet {
@@ -99,6 +112,13 @@ struct GraphNet {
   std::vector<PassPlan> passes;  // one per ReLU (in order) + the spec pass last
   float *bias_arena = nullptr;
   float4 *param_arena = nullptr;
+  // alpha-CROWN on the spec pass (empty alpha_why: supported)
+  std::string alpha_why;
+  std::vector<int64_t> alpha_ld;          // per ReLU index: floats per row of its slope state
+  std::vector<FwdStep> fwd;               // gradient pass
+  std::vector<int> val_slot;              // per node: slot of its forward values, or -1
+  std::vector<int64_t> val_rs;            // per node: floats per row of its forward values
+  std::vector<int64_t> fwd_slot_floats;   // floats per row of every slot
 };
 
 void destroy_graph(GraphNet *g) {
@@ -395,6 +415,112 @@ struct Planner {
   }
 };
 
+// ---- alpha-CROWN plan -----------------------------------------------------------------------
+// The slope state of every ReLU is laid out like the coefficient rows that the spec pass
+// relaxes through it, so the relaxation, the recorded coefficients and the gradient pass all
+// share one row layout.  The gradient pass evaluates nodes in order up to the last ReLU,
+// fusing each ReLU line into the convolution or dense node below it and each add into the
+// convolution that produces its later summand; value buffers are reused once their last
+// reader has run.  Returns an empty string, or why the net has no alpha-CROWN plan.
+std::string plan_alpha(GraphNet *g) {
+  const int nn = (int)g->nodes.size();
+  const int R = (int)g->relus.size();
+  const PassPlan &sp = g->passes.back();
+  g->alpha_ld.assign(R, 0);
+  for (const Step &st : sp.steps) {
+    if (st.relu < 0) continue;
+    if (st.kind == ST_CONVT && !st.dst.dense) return "windowed rows in the spec pass";
+    g->alpha_ld[g->nodes[st.relu].relu_index] = st.dst.row_stride;
+  }
+  for (int r = 0; r < R; ++r)
+    if (g->alpha_ld[r] <= 0 || g->alpha_ld[r] % 4) return "a ReLU the spec pass does not relax";
+  auto src = [&](int v) { return v >= 0 && g->nodes[v].op == VCR_FLATTEN ? g->nodes[v].in0 : v; };
+  g->val_rs.assign(nn, 0);
+  for (int i = 0; i < nn; ++i) {
+    const GNode &n = g->nodes[i];
+    g->val_rs[i] = n.op == VCR_RELU ? g->alpha_ld[n.relu_index] : ld_of(n.numel);
+  }
+  const int last = g->relus.back();
+  std::vector<char> written(nn, 0), fused_add(nn, 0);
+  g->fwd.clear();
+  for (int i = 0; i < last; ++i) {
+    const GNode &nd = g->nodes[i];
+    if (nd.op == VCR_FLATTEN) continue;
+    if (nd.op == VCR_RELU) {
+      if (!written[i]) return "a ReLU whose input is not a convolution or dense node";
+      continue;
+    }
+    if (nd.op == VCR_ADD) {
+      if (fused_add[i]) continue;
+      FwdStep f;
+      f.kind = FW_ADD;
+      f.node = i;
+      f.in = src(nd.in0);
+      f.res = src(nd.in1);
+      f.out = i;
+      if (f.in < 0 || f.res < 0) return "an add of the network input";
+      g->fwd.push_back(f);
+      written[i] = 1;
+      continue;
+    }
+    FwdStep f;
+    f.kind = nd.op == VCR_CONV2D ? FW_CONV : FW_DENSE;
+    f.node = i;
+    f.in = src(nd.in0);
+    f.out = i;
+    if (nd.cons.size() == 1) {
+      const int cn = nd.cons[0];
+      const GNode &c = g->nodes[cn];
+      if (c.op == VCR_RELU) {
+        f.out = cn;
+        f.relu = c.relu_index;
+      } else if (c.op == VCR_ADD && f.kind == FW_CONV) {
+        const int other = c.in0 == i ? c.in1 : c.in0;
+        if (other >= 0 && other < i && written[src(other)] && !g->nodes[other].flat) {
+          f.res = src(other);
+          f.out = cn;
+          fused_add[cn] = 1;
+        }
+      }
+    }
+    if (f.kind == FW_DENSE) {
+      if (f.in < 0) return "a dense node on the network input";
+      if (g->val_rs[f.in] != nd.ld_in) return "dense input rows of another width";
+      if (f.relu >= 0 && g->alpha_ld[f.relu] != nd.ld_out) return "dense ReLU rows of another width";
+    }
+    if (f.kind == FW_CONV && f.in >= 0 && g->nodes[f.in].flat) return "a convolution of a flat node";
+    g->fwd.push_back(f);
+    written[f.out] = 1;
+  }
+  for (int r : g->relus)
+    if (!written[r]) return "a ReLU whose input is not a convolution or dense node";
+  // value slots: a step's output never shares a slot with its inputs
+  std::vector<int> last_use(nn, -1);
+  for (int k = 0; k < (int)g->fwd.size(); ++k)
+    for (int v : {g->fwd[k].in, g->fwd[k].res})
+      if (v >= 0) last_use[v] = k;
+  g->val_slot.assign(nn, -1);
+  g->fwd_slot_floats.clear();
+  std::vector<char> busy;
+  for (int k = 0; k < (int)g->fwd.size(); ++k) {
+    const int o = g->fwd[k].out;
+    int sl = -1;
+    for (size_t j = 0; j < busy.size() && sl < 0; ++j)
+      if (!busy[j]) sl = (int)j;
+    if (sl < 0) {
+      sl = (int)busy.size();
+      busy.push_back(0);
+      g->fwd_slot_floats.push_back(0);
+    }
+    busy[sl] = 1;
+    g->fwd_slot_floats[sl] = std::max(g->fwd_slot_floats[sl], g->val_rs[o]);
+    g->val_slot[o] = sl;
+    for (int v : {g->fwd[k].in, g->fwd[k].res})
+      if (v >= 0 && last_use[v] == k) busy[g->val_slot[v]] = 0;
+  }
+  return std::string();
+}
+
 // ---- call-time buffers ------------------------------------------------------------------
 struct GBufs {
   float *c0 = nullptr, *r0 = nullptr;
@@ -405,6 +531,13 @@ struct GBufs {
   std::vector<float *> slots;
   float *beta = nullptr, *part = nullptr;
   int4 *rows = nullptr;
+  // alpha-CROWN: slope state per ReLU, best row bounds, improvement flags, the rows' box
+  // vertices and the gradient pass's value slots
+  std::vector<AlphaLayer> al;
+  float *best_val = nullptr;
+  int32_t *flag = nullptr;
+  float *vtx = nullptr;
+  std::vector<float *> fslots;
 };
 
 struct GPlanSize {
@@ -437,7 +570,8 @@ int64_t max_part_per_row(const GraphNet *g) {
   return best;
 }
 
-size_t carve_graph(const vcr_ctx *c, const GraphNet *g, Workspace &w, int B, int m, int chunk, GBufs *bf) {
+size_t carve_graph(const vcr_ctx *c, const GraphNet *g, Workspace &w, int B, int m, int chunk, GBufs *bf,
+                   bool alpha = false) {
   const int nn = (int)g->nodes.size();
   const int64_t ld0 = ld_of(g->n0);
   bf->c0 = take<float>(w, (size_t)B * ld0);
@@ -481,6 +615,29 @@ size_t carve_graph(const vcr_ctx *c, const GraphNet *g, Workspace &w, int B, int
   bf->beta = take<float>(w, (size_t)rows_pad(rows));
   bf->part = take<float>(w, (size_t)((rows + 128) * max_part_per_row(g)));
   bf->rows = take<int4>(w, (size_t)rows);
+  bf->al.clear();
+  bf->fslots.clear();
+  if (alpha) {
+    const int64_t ra = rows_pad(2 * (int64_t)m * chunk);
+    int32_t col0 = 0;
+    for (size_t r = 0; r < g->relus.size(); ++r) {
+      const GNode &n = g->nodes[g->relus[r]];
+      AlphaLayer a{};
+      a.ld = g->alpha_ld[r];
+      a.ldp = n.flat ? ld_of(n.numel) : n.numel;   // the layout of P above
+      a.n = (int32_t)n.numel;
+      a.col0 = col0;
+      a.hwc_C = n.flat ? 0 : n.C;
+      a.hwc_HW = n.flat ? 0 : n.H * n.H;
+      col0 += a.n;
+      for (float **q : {&a.alpha, &a.mom, &a.vel, &a.best, &a.grad, &a.pre}) *q = take<float>(w, (size_t)ra * a.ld);
+      bf->al.push_back(a);
+    }
+    bf->best_val = take<float>(w, (size_t)ra);
+    bf->flag = take<int32_t>(w, (size_t)ra);
+    bf->vtx = take<float>(w, (size_t)ra * ld_of(g->n0));
+    for (int64_t f : g->fwd_slot_floats) bf->fslots.push_back(take<float>(w, (size_t)(ra * f)));
+  }
   (void)c;
   return w.used;
 }
@@ -594,19 +751,22 @@ vcr_status graph_load(vcr_ctx *c, const vcr_node *nodes, int32_t n, const int32_
       float *staging = nullptr;
       HIP_TRY(c, hipMalloc(&staging, (size_t)nout * nin * 4));
       HIP_TRY(c, hipMemcpy(staging, d.W, (size_t)nout * nin * 4, hipMemcpyHostToDevice));
-      HIP_TRY(c, hipMalloc(&gn.Wp, (size_t)nout * gn.ld_in * 4));
-      c->net_bytes += (size_t)nout * gn.ld_in * 4;
+      // Wp and Wh have zero rows up to ld(out): the gradient pass runs them as GEMM operands
+      HIP_TRY(c, hipMalloc(&gn.Wp, (size_t)gn.ld_out * gn.ld_in * 4));
+      c->net_bytes += (size_t)gn.ld_out * gn.ld_in * 4;
       HIP_TRY(c, hipMalloc(&gn.Bt, (size_t)gn.ld_in * gn.ld_out * 4));
       c->net_bytes += (size_t)gn.ld_in * gn.ld_out * 4;
       // Wp = W with zero-padded rows (via the transposed copy)
       HIP_TRY(c, launch_transpose_pad(staging, (int32_t)nout, (int32_t)nin, gn.Bt, gn.ld_out, gn.ld_in, s));
-      HIP_TRY(c, launch_transpose_pad(gn.Bt, (int32_t)gn.ld_in, (int32_t)gn.ld_out, gn.Wp, gn.ld_in, nout, s));
+      HIP_TRY(c, launch_transpose_pad(gn.Bt, (int32_t)gn.ld_in, (int32_t)gn.ld_out, gn.Wp, gn.ld_in, gn.ld_out, s));
       if (gn.hwc_in) {
         const GNode &fl = g->nodes[d.in0];
         const GNode &cv = g->nodes[fl.in0];
-        HIP_TRY(c, hipMalloc(&gn.Wh, (size_t)nout * gn.ld_in * 4));
-        c->net_bytes += (size_t)nout * gn.ld_in * 4;
+        HIP_TRY(c, hipMalloc(&gn.Wh, (size_t)gn.ld_out * gn.ld_in * 4));
+        c->net_bytes += (size_t)gn.ld_out * gn.ld_in * 4;
         HIP_TRY(c, launch_permute_hwc(staging, (int32_t)nout, cv.C, cv.H * cv.H, gn.Wh, gn.ld_in, s));
+        if (gn.ld_out > nout)
+          HIP_TRY(c, launch_fill(gn.Wh + (size_t)nout * gn.ld_in, (gn.ld_out - nout) * gn.ld_in, 0.f, s));
         HIP_TRY(c, launch_transpose_pad(gn.Wh, (int32_t)nout, (int32_t)gn.ld_in, gn.Bt, gn.ld_out, gn.ld_in, s));
       }
       HIP_TRY(c, hipMalloc(&gn.b, (size_t)gn.ld_out * 4));
@@ -634,6 +794,7 @@ vcr_status graph_load(vcr_ctx *c, const vcr_node *nodes, int32_t n, const int32_
     if (!pl.plan(pp)) return fail(c, VCR_ERR_UNSUPPORTED, "spec pass: %s", pl.why.c_str());
     g->passes.push_back(pp);
   }
+  g->alpha_why = g->relus.empty() ? std::string("no ReLU") : plan_alpha(g);
   // the first ReLU's input must be reachable from the box by one pass like the others:
   // every pass ends at the stem (checked by the planner)
   if (dev && !pl.host_bias.empty()) {
@@ -698,9 +859,11 @@ vcr_status run_ibp(vcr_ctx *c, GraphNet *g, GBufs &bf, int B) {
 float4 *relu_P(GraphNet *g, GBufs &bf, int relu_node) { return bf.P[g->nodes[relu_node].relu_index]; }
 
 // One pass over `units` units starting at absolute unit u0.  Leaves the row constants
-// (complete bounds) in bf.beta.
+// (complete bounds) in bf.beta.  With alpha (the spec pass of alpha-CROWN) every relaxation
+// takes the rows' slopes at unstable neurons and records the coefficients before it, and the
+// stem writes each row's box vertex.
 vcr_status run_pass(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &pp, int u0, int units, int m,
-                    uint64_t *flops) {
+                    uint64_t *flops, bool alpha = false) {
   hipStream_t s = c->stream;
   const GNode &start = g->nodes[pp.start];
   const int64_t rpu = pp.spec ? 2 * (int64_t)m : 2 * pp.rows_per_unit_mult;
@@ -759,6 +922,13 @@ vcr_status run_pass(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &pp, int 
         ia.out = slot(st.dst);
         ia.beta = bf.beta;
         if (ia.ldo != nd.ld_in) return fail(c, VCR_ERR_UNSUPPORTED, "internal: init row width mismatch");
+        if (alpha && st.relu >= 0) {
+          const AlphaLayer &l = bf.al[g->nodes[st.relu].relu_index];
+          if (l.ld != ia.ldo) return fail(c, VCR_ERR_UNSUPPORTED, "internal: slope row width mismatch");
+          ia.alpha = l.alpha;
+          ia.ld_alpha = l.ld;
+          ia.pre = l.pre;
+        }
         HIP_TRY(c, launch_init_rows(ia, s));
         break;
       }
@@ -796,6 +966,13 @@ vcr_status run_pass(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &pp, int 
         a.bias = st.bias_off >= 0 ? g->bias_arena + st.bias_off : nullptr;
         a.out = slot(st.dst);
         a.part = bf.part;
+        if (alpha && st.relu >= 0) {
+          const AlphaLayer &l = bf.al[g->nodes[st.relu].relu_index];
+          if (!st.dst.dense || l.ld != st.dst.row_stride)
+            return fail(c, VCR_ERR_UNSUPPORTED, "internal: slope row width mismatch");
+          a.alpha = l.alpha;
+          a.pre = l.pre;
+        }
         const int parts = convt_launches(a);
         if (parts < 0) return fail(c, VCR_ERR_UNSUPPORTED, "internal: transposed convolution shape");
         for (int k = 0; k < parts; ++k) {
@@ -829,6 +1006,10 @@ vcr_status run_pass(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &pp, int 
         a.r0 = bf.r0;
         a.ld_box = ld_of(g->n0);
         a.part = bf.part;
+        if (alpha) {
+          a.vtx = bf.vtx;
+          a.ld_vtx = ld_of(g->n0);
+        }
         HIP_TRY(c, launch_stem(a, s));
         HIP_TRY(c, launch_rowsum_win(bf.beta, bf.part, 1, 0, R, a.S_in * a.S_in, s));
         *flops += 2ull * (uint64_t)R * a.S_out * a.S_out * 9ull * (uint64_t)nd.C * (uint64_t)nd.Ci;
@@ -862,6 +1043,14 @@ vcr_status run_pass(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &pp, int 
         ga.relu_index = 0;
         ga.part = bf.part;
         if (st.dst.row_stride != nd.ld_in) return fail(c, VCR_ERR_UNSUPPORTED, "internal: dense output width mismatch");
+        if (alpha && st.relu >= 0) {
+          const AlphaLayer &l = bf.al[g->nodes[st.relu].relu_index];
+          if (l.ld != nd.ld_in) return fail(c, VCR_ERR_UNSUPPORTED, "internal: slope row width mismatch");
+          ga.alpha = l.alpha;
+          ga.ld_alpha = l.ld;
+          ga.pre = l.pre;
+          ga.ld_pre = l.ld;
+        }
         const uint64_t df = 2ull * (uint64_t)R * (uint64_t)nd.numel * (uint64_t)g->nodes[nd.in0].numel;
         {
           const vcr_status st2 = TIMED_GEMM(c, s, df, ga);
@@ -876,21 +1065,166 @@ vcr_status run_pass(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &pp, int 
   return VCR_OK;
 }
 
+// alpha-CROWN's gradient pass over the M rows of `units` units from unit u0: the relaxed
+// network evaluated forward from each row's box vertex (bf.vtx, written by the spec pass),
+// each ReLU replaced by the line the row's coefficient selected, which leaves the slope
+// gradients in bf.al[].grad.
+vcr_status run_forward(vcr_ctx *c, GraphNet *g, GBufs &bf, int u0, int units, int32_t M, int32_t rpu,
+                       uint64_t *flops) {
+  hipStream_t s = c->stream;
+  const int64_t ld0 = ld_of(g->n0);
+  auto val = [&](int v) { return v < 0 ? bf.vtx : bf.fslots[g->val_slot[v]]; };
+  auto rs = [&](int v) { return v < 0 ? ld0 : g->val_rs[v]; };
+  for (const FwdStep &f : g->fwd) {
+    const GNode &nd = g->nodes[f.node];
+    switch (f.kind) {
+      case FW_CONV: {
+        FwdConvArgs a{};
+        a.in = val(f.in);
+        a.in_rs = rs(f.in);
+        a.Ci = nd.Ci;
+        a.Hi = nd.Hi;
+        a.Wk = nd.Wk;
+        a.bias = nd.b;
+        a.Co = nd.C;
+        a.Ho = nd.H;
+        a.stride = nd.stride;
+        a.rows = M;
+        if (f.res >= 0) {
+          a.res = val(f.res);
+          a.res_rs = rs(f.res);
+        }
+        if (f.relu >= 0) {
+          const AlphaLayer &l = bf.al[f.relu];
+          a.P = bf.P[f.relu] + (int64_t)u0 * l.ldp;
+          a.rows_per_unit = rpu;
+          a.units = units;
+          a.alpha = l.alpha;
+          a.pre = l.pre;
+          a.grad = l.grad;
+        }
+        a.out = val(f.out);
+        a.out_rs = rs(f.out);
+        HIP_TRY(c, launch_fwd_conv(a, s));
+        *flops += 2ull * (uint64_t)M * (uint64_t)nd.numel * 9ull * (uint64_t)nd.Ci;
+        break;
+      }
+      case FW_DENSE: {
+        GemmArgs ga{};
+        ga.A = val(f.in);
+        ga.lda = nd.ld_in;
+        ga.Bt = nd.hwc_in ? nd.Wh : nd.Wp;
+        ga.ldb = nd.ld_in;
+        ga.M = M;
+        ga.M_pad = (int32_t)rows_pad(M);
+        ga.K = (int32_t)nd.ld_in;
+        ga.N_pad = (int32_t)nd.ld_out;
+        ga.out = val(f.out);
+        ga.ldo = nd.ld_out;
+        if (f.relu >= 0) {
+          const AlphaLayer &l = bf.al[f.relu];
+          ga.mode = EPI_FORWARD;
+          ga.P = bf.P[f.relu] + (int64_t)u0 * l.ldp;
+          ga.ldp = l.ldp;
+          ga.rows_per_unit = rpu;
+          ga.n_units = units;
+          ga.alpha = l.alpha;
+          ga.ld_alpha = l.ld;
+          ga.pre = l.pre;
+          ga.ld_pre = l.ld;
+          ga.grad = l.grad;
+        } else {
+          ga.mode = EPI_AFFINE;
+          ga.bias = nd.b;
+          ga.rows_per_unit = ga.M_pad;
+          ga.n_units = 1;
+        }
+        const uint64_t df = 2ull * (uint64_t)M * (uint64_t)nd.numel * (uint64_t)g->nodes[f.in].numel;
+        const vcr_status st = TIMED_GEMM(c, s, df, ga);
+        if (st != VCR_OK) return st;
+        *flops += df;
+        break;
+      }
+      case FW_ADD:
+        HIP_TRY(c, launch_fwd_add(val(f.in), rs(f.in), val(f.res), rs(f.res), val(f.out), rs(f.out), M, nd.numel, s));
+        break;
+    }
+  }
+  return VCR_OK;
+}
+
+struct GraphAlphaCall {
+  vcr_alpha_opts o;
+  int64_t n_total = 0;
+};
+
+// alpha-CROWN on the spec pass, per chunk of inputs: evaluate with the current slopes (the
+// spec pass with per-row slopes), keep each row's best bound, run the gradient pass and one
+// projected Adam step; T steps give T + 1 evaluations.  The slope kernels are the MLP path's.
+vcr_status alpha_spec_graph(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &pp, int B, int m, int chunk,
+                            const GraphAlphaCall &ac, float *lb, float *ub, uint64_t *flops, int *chunks) {
+  hipStream_t s = c->stream;
+  const vcr_alpha_opts &o = ac.o;
+  const int R = (int)g->relus.size();
+  const int32_t rpu = 2 * m;
+  for (int u0 = 0; u0 < B; u0 += chunk) {
+    const int units = std::min(chunk, B - u0);
+    const int32_t M = rpu * units;
+    const int32_t M_pad = (int32_t)rows_pad(M);
+    for (int r = 0; r < R; ++r) {
+      bf.al[r].P = bf.P[r] + (int64_t)u0 * bf.al[r].ldp;
+      HIP_TRY(c, launch_alpha_init(bf.al[r], o.alpha_init ? o.alpha_init + (int64_t)u0 * rpu * ac.n_total : nullptr,
+                                   ac.n_total, M, M_pad, rpu, s));
+    }
+    // value rows are read at their padded width: zero once, the padding is never written
+    for (size_t k = 0; k < bf.fslots.size(); ++k)
+      HIP_TRY(c, launch_fill(bf.fslots[k], (int64_t)M_pad * g->fwd_slot_floats[k], 0.f, s));
+    HIP_TRY(c, launch_fill(bf.vtx, (int64_t)M_pad * ld_of(g->n0), 0.f, s));
+    for (int32_t t = 0; t <= o.iters; ++t) {
+      vcr_status st = run_pass(c, g, bf, pp, u0, units, m, flops, true);
+      if (st != VCR_OK) return st;
+      HIP_TRY(c, launch_alpha_best(bf.beta, nullptr, 0, M_pad, M, m, t == 0, bf.best_val, bf.flag,
+                                   o.lb_hist ? o.lb_hist + ((int64_t)t * B + u0) * m : nullptr,
+                                   o.ub_hist ? o.ub_hist + ((int64_t)t * B + u0) * m : nullptr, s));
+      const bool step = t < o.iters;
+      if (!step)
+        for (int r = 0; r < R; ++r) HIP_TRY(c, launch_alpha_keep(bf.al[r], bf.flag, M, s));
+      if (!step && !o.grad_out) break;
+      st = run_forward(c, g, bf, u0, units, M, rpu, flops);
+      if (st != VCR_OK) return st;
+      if (!step) break;
+      const double c1 = 1.0 / (1.0 - std::pow((double)o.beta1, (double)(t + 1)));
+      const double c2 = 1.0 / (1.0 - std::pow((double)o.beta2, (double)(t + 1)));
+      for (int r = 0; r < R; ++r)
+        HIP_TRY(c, launch_alpha_adam(bf.al[r], bf.flag, M, rpu, o.lr, o.beta1, o.beta2, o.adam_eps, (float)c1,
+                                     (float)c2, s));
+    }
+    HIP_TRY(c, launch_alpha_final(bf.best_val, units, m, nullptr, lb + (int64_t)u0 * m, ub + (int64_t)u0 * m, s));
+    if (o.alpha_out || o.grad_out)
+      for (int r = 0; r < R; ++r)
+        HIP_TRY(c, launch_alpha_out(bf.al[r], M, m, ac.n_total,
+                                    o.alpha_out ? o.alpha_out + (int64_t)u0 * rpu * ac.n_total : nullptr,
+                                    o.grad_out ? o.grad_out + (int64_t)u0 * rpu * ac.n_total : nullptr, s));
+    ++*chunks;
+  }
+  return VCR_OK;
+}
+
 }  // namespace
 
 // Inputs per chunk and workspace bytes of a CROWN call of B inputs: the whole batch, halved
 // until the plan fits the workspace cap (VCR_ERR_OOM when one input does not).
-vcr_status graph_plan(vcr_ctx *c, int32_t B, int32_t m, int *chunk_out, size_t *bytes_out) {
+vcr_status graph_plan(vcr_ctx *c, int32_t B, int32_t m, int *chunk_out, size_t *bytes_out, bool alpha) {
   GraphNet *g = c->graph;
   int chunk = B;
   Workspace probe;
   GBufs tmp;
-  size_t need = carve_graph(c, g, probe, B, m, chunk, &tmp);
+  size_t need = carve_graph(c, g, probe, B, m, chunk, &tmp, alpha);
   if (c->ws_cap > 0) {
     while (need > c->ws_cap && chunk > 1) {
       chunk = (chunk + 1) / 2;
       Workspace pw;
-      need = carve_graph(c, g, pw, B, m, chunk, &tmp);
+      need = carve_graph(c, g, pw, B, m, chunk, &tmp, alpha);
     }
     if (need > c->ws_cap)
       return fail(c, VCR_ERR_OOM, "workspace cap %llu bytes is below the minimum plan (%llu bytes)",
@@ -901,15 +1235,16 @@ vcr_status graph_plan(vcr_ctx *c, int32_t B, int32_t m, int *chunk_out, size_t *
   return VCR_OK;
 }
 
-vcr_status graph_crown(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m,
-                       const vcr_splits *splits, float *lb, float *ub) {
+namespace {
+
+vcr_status graph_run(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m, float *lb,
+                     float *ub, const GraphAlphaCall *ac) {
   GraphNet *g = c->graph;
-  if (splits) return fail(c, VCR_ERR_UNSUPPORTED, "subdomain splits are built for MLPs only");
   const int nn = (int)g->nodes.size();
   const GNode &out = g->nodes[nn - 1];
   int chunk = B;
   size_t need = 0;
-  vcr_status st = graph_plan(c, B, m, &chunk, &need);
+  vcr_status st = graph_plan(c, B, m, &chunk, &need, ac != nullptr);
   if (st != VCR_OK) return st;
   if (c->device < 0) {
     c->chunks_last = (int)g->passes.size() * ((B + chunk - 1) / chunk);
@@ -921,7 +1256,7 @@ vcr_status graph_crown(vcr_ctx *c, const float *x0, int32_t B, float eps, const 
   st = ensure_ws(c, need);
   if (st != VCR_OK) return st;
   GBufs bf;
-  carve_graph(c, g, c->ws, B, m, chunk, &bf);
+  carve_graph(c, g, c->ws, B, m, chunk, &bf, ac != nullptr);
   hipStream_t s = c->stream;
   const int64_t ld0 = ld_of(g->n0);
   HIP_TRY(c, launch_box(x0, B, (int32_t)g->n0, ld0, eps, c->clip_on, c->clip_lo, c->clip_hi, bf.c0, bf.r0, s));
@@ -932,6 +1267,11 @@ vcr_status graph_crown(vcr_ctx *c, const float *x0, int32_t B, float eps, const 
   uint64_t flops = 0;
   int chunks = 0;
   for (const PassPlan &pp : g->passes) {
+    if (pp.spec && ac) {
+      st = alpha_spec_graph(c, g, bf, pp, B, m, chunk, *ac, lb, ub, &flops, &chunks);
+      if (st != VCR_OK) return st;
+      continue;
+    }
     if (pp.direct) {
       const GNode &z = g->nodes[pp.start];
       const int ri = g->nodes[pp.relu].relu_index;
@@ -979,6 +1319,24 @@ vcr_status graph_crown(vcr_ctx *c, const float *x0, int32_t B, float eps, const 
   return VCR_OK;
 }
 
+}  // namespace
+
+vcr_status graph_crown(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m,
+                       const vcr_splits *splits, float *lb, float *ub) {
+  if (splits) return fail(c, VCR_ERR_UNSUPPORTED, "subdomain splits are built for MLPs only");
+  return graph_run(c, x0, B, eps, C, m, lb, ub, nullptr);
+}
+
+vcr_status graph_alpha(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m,
+                       const vcr_alpha_opts &o, int64_t n_total, float *lb, float *ub) {
+  if (!c->graph->alpha_why.empty())
+    return fail(c, VCR_ERR_UNSUPPORTED, "alpha-CROWN on this network: %s", c->graph->alpha_why.c_str());
+  GraphAlphaCall ac;
+  ac.o = o;
+  ac.n_total = n_total;
+  return graph_run(c, x0, B, eps, C, m, lb, ub, &ac);
+}
+
 vcr_status graph_ibp(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m, float *lb,
                      float *ub) {
   GraphNet *g = c->graph;
@@ -1006,10 +1364,10 @@ vcr_status graph_ibp(vcr_ctx *c, const float *x0, int32_t B, float eps, const fl
   return VCR_OK;
 }
 
-size_t graph_workspace_bytes(vcr_ctx *c, int32_t B, int32_t m) {
+size_t graph_workspace_bytes(vcr_ctx *c, int32_t B, int32_t m, bool alpha) {
   Workspace probe;
   GBufs tmp;
-  return carve_graph(c, c->graph, probe, B, m, B, &tmp);
+  return carve_graph(c, c->graph, probe, B, m, B, &tmp, alpha && c->graph->alpha_why.empty());
 }
 
 }  // namespace vcr

@@ -163,9 +163,12 @@ hipError_t launch_store_ptrs(const PtrTable &t, int32_t n, const float **dst, hi
 // bound of spec row q - m; every row maximises its own lower bound.
 struct AlphaLayer {
   float *alpha, *mom, *vel, *best, *grad, *pre;   // [M_pad][ld] each
-  const float4 *P;                                // [units][ld] relaxation of this ReLU
-  int64_t ld;
+  const float4 *P;                                // [units][ldp] relaxation of this ReLU
+  int64_t ld, ldp;
   int32_t n, col0;                                // neurons, first column in the compact layout
+  // channels-last neurons (ReLUs on convolution outputs): neuron (y, x, c) is column
+  // (y W + x) C + c here and c H W + y W + x in the compact layout; 0 for flat neurons
+  int32_t hwc_C, hwc_HW;
 };
 // alpha <- alpha_init (compact [units][2m][n_total]) or lam (P.x); mom = vel = 0
 hipError_t launch_alpha_init(const AlphaLayer &l, const float *alpha_init, int64_t n_total, int32_t rows,

@@ -41,6 +41,7 @@ GOLDENS = {
 # alpha-CROWN runs: {workload: (inputs, Adam steps)}
 ALPHA = {
     "mlp3072x8192x4": ([0], 5),
+    "resnet3x8x8": ([0], 5),
 }
 
 # A-guided box vertices: {workload: inputs}

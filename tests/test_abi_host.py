@@ -69,6 +69,33 @@ def test_conv_networks_are_reported_unsupported(vc):
     assert e.value.status == vc.VCR_ERR_UNSUPPORTED
 
 
+def test_alpha_on_conv_networks_is_planned(vc):
+    """Residual and plain convolutional nets load in a validation-only context, and
+    alpha-CROWN on them gets past planning (the slope layout and the gradient pass) to the
+    device stage, VCR_ERR_STATE; bad options are still VCR_ERR_ARG."""
+    from tests.test_conv_gpu import conv_chain, small_resnet
+    for wl in (small_resnet(1), conv_chain(2)):
+        ctx = vc.Ctx(-1)
+        ctx.load_net(wl.net)
+        lib = ctx.lib
+        shapes = oracle_shapes(wl.net)
+        n_total = sum(int(np.prod(shapes[i])) for i, nd in enumerate(wl.net.nodes) if nd.op == "relu")
+        assert lib.vcr_relu_neurons(ctx.h) == n_total
+        B, m = wl.C.shape[0], wl.C.shape[1]
+        x, C, lb, ub = _buf(B * wl.net.n_in), _buf(wl.C.size), _buf(B * m), _buf(B * m)
+        p = lambda a: ctypes.c_void_p(a.ctypes.data)  # noqa: E731
+        for lr, want in ((0.1, vc.VCR_ERR_STATE), (0.0, vc.VCR_ERR_ARG)):
+            o = vc.VcrAlphaOpts(3, lr, 0.9, 0.999, 1e-8, None, None, None, None, None)
+            st = lib.vcr_alpha_crown_bounds(ctx.h, p(x), B, ctypes.c_float(0.01), p(C), m, ctypes.byref(o), p(lb),
+                                            p(ub))
+            assert st == want, (wl.name, lr, lib.vcr_last_error(ctx.h))
+
+
+def oracle_shapes(net):
+    from workloads.gen import node_shapes
+    return node_shapes(net)
+
+
 def _call(vc, ctx, B, eps, m, n0, n_out, splits=None, x0=None, C=None, lb=None, ub=None):
     lib = ctx.lib
     x0 = _buf(B * n0) if x0 is None else x0

@@ -163,18 +163,15 @@ def test_alpha_chunked_equals_whole():
     assert np.array_equal(lb.cpu().numpy(), lb2.cpu().numpy()) and np.array_equal(ub.cpu().numpy(), ub2.cpu().numpy())
 
 
-def test_alpha_rejects_conv_nets_and_bad_options():
+def test_alpha_rejects_bad_options():
+    """Bad options fail with VCR_ERR_ARG before any device work, on both network paths."""
     from paper_2606_09377_amd.vcrown import VcrError
     from tests.test_conv_gpu import small_resnet
-    wl = small_resnet(305)
-    ctx = gpu_ctx(wl.net)
-    with pytest.raises(VcrError, match="UNSUPPORTED"):
-        ctx.alpha_crown_bounds(to_dev(wl.x0), wl.eps, to_dev(wl.C), iters=1)
-    wl = small_case(seed=84, B=1)
-    ctx = gpu_ctx(wl.net)
-    for kw in ({"lr": 0.0}, {"beta1": 1.0}, {"iters": -1}, {"adam_eps": 0.0}):
-        with pytest.raises(VcrError, match="ARG"):
-            ctx.alpha_crown_bounds(to_dev(wl.x0), wl.eps, to_dev(wl.C), **kw)
+    for wl in (small_case(seed=84, B=1), small_resnet(305)):
+        ctx = gpu_ctx(wl.net)
+        for kw in ({"lr": 0.0}, {"beta1": 1.0}, {"iters": -1}, {"adam_eps": 0.0}):
+            with pytest.raises(VcrError, match="ARG"):
+                ctx.alpha_crown_bounds(to_dev(wl.x0), wl.eps, to_dev(wl.C), **kw)
 
 
 def test_alpha_mlp3072x8192x4_bench_size():
