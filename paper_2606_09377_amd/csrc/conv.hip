@@ -1151,16 +1151,14 @@ FastDiv make_fastdiv(uint32_t d) {
 
 // One output element: D = acc + bias (+ residual), then the identity or the ReLU line
 // selected by the recorded coefficient's sign (lam D where it is positive, s D + t where it
-// is negative, s D where it is 0), with the slope gradient at unstable neurons.
-__device__ __forceinline__ void fwd_store(const FwdConvArgs &p, int64_t r, int32_t pos, int32_t n, float acc) {
-  float D = acc + p.bias[n];
-  const int64_t q = (int64_t)pos * p.Co + n;
-  if (p.res) D += p.res[r * p.res_rs + q];
-  const int64_t off = r * p.out_rs + q;
+// is negative, s D where it is 0), with the slope gradient at unstable neurons.  ob, pb, rb:
+// the element's row offsets into out (and alpha, pre, grad), P and res, without the channel.
+__device__ __forceinline__ void fwd_apply(const FwdConvArgs &p, int64_t ob, int64_t pb, int64_t rb, int32_t n,
+                                          float D) {
+  if (p.res) D += p.res[rb + n];
+  const int64_t off = ob + n;
   if (p.P) {
-    int64_t u = r / p.rows_per_unit;
-    u = u < p.units ? u : p.units - 1;
-    const float4 prm = p.P[u * ((int64_t)p.Ho * p.Ho * p.Co) + q];
+    const float4 prm = p.P[pb + n];
     const bool unst = prm.z > 0.f;
     const float lam = unst ? p.alpha[off] : prm.x;
     const float an = p.pre[off];
@@ -1169,6 +1167,20 @@ __device__ __forceinline__ void fwd_store(const FwdConvArgs &p, int64_t r, int32
   } else {
     p.out[off] = D;
   }
+}
+
+// row offsets of coefficient row r at output position pos
+__device__ __forceinline__ void fwd_offsets(const FwdConvArgs &p, int64_t r, int32_t pos, int64_t *ob, int64_t *pb,
+                                            int64_t *rb) {
+  const int64_t q = (int64_t)pos * p.Co;
+  int64_t u = 0;
+  if (p.P) {
+    u = r / p.rows_per_unit;
+    u = u < p.units ? u : p.units - 1;
+  }
+  *ob = r * p.out_rs + q;
+  *pb = u * ((int64_t)p.Ho * p.Ho * p.Co) + q;
+  *rb = r * p.res_rs + q;
 }
 
 template <int BM, int BN, int WM, int WN>
@@ -1270,14 +1282,20 @@ __global__ __launch_bounds__(256, 2) void k_fwd_conv(const FwdConvArgs p, FastDi
     if (more) lstore(cur ^ 1);
     __syncthreads();
   }
-  // epilogue: row and position of every tile row once, through the free A buffer
-  int *s_r = reinterpret_cast<int *>(&As[0][0]);
-  int *s_pos = s_r + BM;
+  // epilogue: the offsets of every tile row once (a row per thread), through the free A
+  // buffer; -1 marks rows past the end
+  static_assert(24 * BM <= (int)sizeof(As), "row offsets must fit the A buffers");
+  int64_t *s_ob = reinterpret_cast<int64_t *>(&As[0][0]);
+  int64_t *s_pb = s_ob + BM;
+  int64_t *s_rb = s_pb + BM;
   for (int tr = tid; tr < BM; tr += 256) {
     const uint32_t m = (uint32_t)(m0 + tr);
-    const uint32_t r = m < Mtot ? fdiv(m, div_pos) : 0u;
-    s_r[tr] = m < Mtot ? (int)r : -1;
-    s_pos[tr] = (int)(m - r * (uint32_t)HW);
+    if (m < Mtot) {
+      const uint32_t r = fdiv(m, div_pos);
+      fwd_offsets(p, r, (int)(m - r * (uint32_t)HW), &s_ob[tr], &s_pb[tr], &s_rb[tr]);
+    } else {
+      s_ob[tr] = -1;
+    }
   }
   __syncthreads();
   const int half = lane >> 5;
@@ -1285,45 +1303,57 @@ __global__ __launch_bounds__(256, 2) void k_fwd_conv(const FwdConvArgs p, FastDi
   for (int j = 0; j < NB; ++j) {
     const int n = n0 + wn * (BN / WN) + j * 32 + r32;
     if (n >= p.Co) continue;
+    const float bn = p.bias[n];
 #pragma unroll
     for (int i = 0; i < MB; ++i)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int lr = wm * (BM / WM) + i * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
-        const int r = s_r[lr];
-        if (r >= 0) fwd_store(p, r, s_pos[lr], n, acc[i][j][v]);
+        const int64_t ob = s_ob[lr];
+        if (ob >= 0) fwd_apply(p, ob, s_pb[lr], s_rb[lr], n, acc[i][j][v] + bn);
       }
   }
 }
 
-// inputs with CIN <= 4 channels: one thread per output element, channels fastest
+// Inputs with CIN <= 4 channels (the network input): a thread per output element, channels
+// fastest, so the input loads of a wave are shared; the weights are staged in LDS channels
+// fastest, [tap][ci][Co].  Workgroups take FWD_SMALL_POS positions' worth of elements of one
+// row (blockIdx.x) and stride over the rows (blockIdx.y).
 template <int CIN>
-__global__ void k_fwd_conv_small(const FwdConvArgs p) {
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int HW = p.Ho * p.Ho;
-  if (idx >= (int64_t)p.rows * HW * p.Co) return;
-  const int n = (int)(idx % p.Co);
-  const int64_t rp = idx / p.Co;
-  const int64_t r = rp / HW;
-  const int pos = (int)(rp - r * HW);
-  const int yo = pos / p.Ho, xo = pos - yo * p.Ho;
-  const float *x = p.in + r * p.in_rs;
-  const float *w = p.Wk + (int64_t)n * 9 * CIN;
-  float acc = 0.f;
-#pragma unroll
-  for (int ky = 0; ky < 3; ++ky) {
-    const int yy = yo * p.stride - 1 + ky;
-    if ((unsigned)yy >= (unsigned)p.Hi) continue;
-#pragma unroll
-    for (int kx = 0; kx < 3; ++kx) {
-      const int xx = xo * p.stride - 1 + kx;
-      if ((unsigned)xx >= (unsigned)p.Hi) continue;
-      const float *xs = x + ((int64_t)yy * p.Hi + xx) * CIN;
-#pragma unroll
-      for (int ci = 0; ci < CIN; ++ci) acc += xs[ci] * w[(ky * 3 + kx) * CIN + ci];
-    }
+__global__ __launch_bounds__(256) void k_fwd_conv_small(const FwdConvArgs p) {
+  extern __shared__ float wl[];
+  const int tid = threadIdx.x;
+  for (int i = tid; i < 9 * CIN * p.Co; i += 256) {
+    const int co = i % p.Co, k = i / p.Co;   // k = tap * CIN + ci
+    wl[i] = p.Wk[(int64_t)co * 9 * CIN + k];
   }
-  fwd_store(p, r, pos, n, acc);
+  __syncthreads();
+  const int HW = p.Ho * p.Ho;
+  const int local = blockIdx.x * 256 + tid;
+  if (local >= HW * p.Co) return;
+  const int pos = local / p.Co, n = local - pos * p.Co;
+  const int yo = pos / p.Ho, xo = pos - yo * p.Ho;
+  const float bn = p.bias[n];
+  for (int64_t r = blockIdx.y; r < p.rows; r += gridDim.y) {
+    const float *x = p.in + r * p.in_rs;
+    float acc = 0.f;
+#pragma unroll
+    for (int ky = 0; ky < 3; ++ky) {
+      const int yy = yo * p.stride - 1 + ky;
+      if ((unsigned)yy >= (unsigned)p.Hi) continue;
+#pragma unroll
+      for (int kx = 0; kx < 3; ++kx) {
+        const int xx = xo * p.stride - 1 + kx;
+        if ((unsigned)xx >= (unsigned)p.Hi) continue;
+        const float *xs = x + (yy * p.Hi + xx) * CIN;
+#pragma unroll
+        for (int ci = 0; ci < CIN; ++ci) acc += xs[ci] * wl[((ky * 3 + kx) * CIN + ci) * p.Co + n];
+      }
+    }
+    int64_t ob, pb, rb;
+    fwd_offsets(p, r, pos, &ob, &pb, &rb);
+    fwd_apply(p, ob, pb, rb, n, acc + bn);
+  }
 }
 
 hipError_t launch_fwd_conv(const FwdConvArgs &a, hipStream_t s) {
@@ -1336,13 +1366,14 @@ hipError_t launch_fwd_conv(const FwdConvArgs &a, hipStream_t s) {
   if (a.out_rs < HW * a.Co || a.in_rs < (int64_t)a.Hi * a.Hi * a.Ci || (a.res && a.res_rs < HW * a.Co))
     return hipErrorInvalidValue;
   if (a.Ci <= 4) {
-    const int64_t n = (int64_t)a.rows * HW * a.Co;
-    const unsigned grid = (unsigned)((n + 255) / 256);
+    const size_t lds = sizeof(float) * 9 * (size_t)a.Ci * a.Co;
+    if (lds > 65536 || HW * a.Co >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)((HW * a.Co + 255) / 256), (unsigned)std::min<int64_t>(a.rows, 128));
     switch (a.Ci) {
-      case 1: hipLaunchKernelGGL(k_fwd_conv_small<1>, dim3(grid), dim3(256), 0, s, a); break;
-      case 2: hipLaunchKernelGGL(k_fwd_conv_small<2>, dim3(grid), dim3(256), 0, s, a); break;
-      case 3: hipLaunchKernelGGL(k_fwd_conv_small<3>, dim3(grid), dim3(256), 0, s, a); break;
-      default: hipLaunchKernelGGL(k_fwd_conv_small<4>, dim3(grid), dim3(256), 0, s, a); break;
+      case 1: hipLaunchKernelGGL(k_fwd_conv_small<1>, grid, dim3(256), lds, s, a); break;
+      case 2: hipLaunchKernelGGL(k_fwd_conv_small<2>, grid, dim3(256), lds, s, a); break;
+      case 3: hipLaunchKernelGGL(k_fwd_conv_small<3>, grid, dim3(256), lds, s, a); break;
+      default: hipLaunchKernelGGL(k_fwd_conv_small<4>, grid, dim3(256), lds, s, a); break;
     }
     return hipGetLastError();
   }
