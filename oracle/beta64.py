@@ -1,5 +1,5 @@
 """fp64 CPU oracle for beta-CROWN on branch-and-bound subdomains, and a fixed-batch
-branch-and-bound loop, on feed-forward ReLU chains.
+branch-and-bound loop, on feed-forward ReLU networks (dense, conv2d, add, flatten).
 
 TEST INFRASTRUCTURE ONLY.  Only the tests, the smoke check and the bench's CPU-baseline
 leg may import this module.  It shares no code with the GPU library.
@@ -48,8 +48,10 @@ def relu_ids(net):
 
 def _check_chain(net):
     for i, nd in enumerate(net.nodes):
-        if nd.op not in ("dense", "relu") or nd.in0 != i - 1:
-            raise ValueError("beta-CROWN oracle: dense/relu chains only")
+        if nd.op not in ("dense", "conv2d", "relu", "add", "flatten"):
+            raise ValueError(f"beta-CROWN oracle: unsupported node {nd.op}")
+        if not (-1 <= nd.in0 < i) or (nd.op == "add" and not (-1 <= nd.in1 < i)):
+            raise ValueError("beta-CROWN oracle: nodes must be in topological order")
 
 
 def domain_relaxation(net, root, splits):
@@ -68,16 +70,35 @@ def _terms(net, splits):
 
 
 def _pass(net, rel, unst, terms, box, C, alpha, beta, upper):
+    """Backward pass from the output with A = C, the rows' slopes and the split terms; the
+    coefficients reaching a node along several paths (an add's inputs) are summed before the
+    node is expanded.  Returns the bounds, the input coefficients and, per ReLU, the
+    coefficients on its output before relaxation."""
+    shapes = cr.node_shapes(net)
     A = np.asarray(C, np.float64)
     rows = A.shape[0]
     bias = np.zeros(rows)
     pre = {}
+    acc = {len(net.nodes) - 1: A}
+
+    def add_to(node, X):
+        acc[node] = acc[node] + X if node in acc else X
+
     for i in range(len(net.nodes) - 1, -1, -1):
+        if i not in acc:
+            continue
+        A = acc.pop(i)
         nd = net.nodes[i]
         if nd.op == "dense":
             bias = bias + A @ cr._f64(nd.b)
-            A = A @ cr._f64(nd.W)
-        else:
+            add_to(nd.in0, A @ cr._f64(nd.W))
+        elif nd.op == "conv2d":
+            co, ho, wo = shapes[i]
+            in_shape = tuple(net.in_shape) if nd.in0 == -1 else shapes[nd.in0]
+            A4 = A.reshape(rows, co, ho, wo)
+            bias = bias + A4.sum(axis=(2, 3)) @ cr._f64(nd.b)
+            add_to(nd.in0, cr.conv2d_transpose(A4, cr._f64(nd.W), nd.stride, nd.pad, in_shape[1:]).reshape(rows, -1))
+        elif nd.op == "relu":
             lam0, s, t = (v.reshape(-1) for v in rel[i])
             lam = np.where(unst[i][None, :], alpha[i], lam0[None, :])
             pre[i] = A.copy()
@@ -92,30 +113,53 @@ def _pass(net, rel, unst, terms, box, C, alpha, beta, upper):
             for e, (ri, j, S) in enumerate(terms):
                 if ri == i:
                     A[:, j] += (-S if upper else S) * beta[:, e]
+            add_to(nd.in0, A)
+        elif nd.op == "add":
+            add_to(nd.in0, A)
+            add_to(nd.in1, A)
+        elif nd.op == "flatten":
+            add_to(nd.in0, A)
+    A = acc.pop(-1) if -1 in acc else np.zeros((rows, int(np.prod(net.in_shape))))
     lo, hi = box
     return cr.concretize(A, bias, lo, hi, upper), A, pre
 
 
 def _gradient(net, rel, unst, terms, box, A_x, pre, alpha, upper):
+    """Gradients with respect to the slopes and the multipliers: the relaxed network
+    evaluated forward, node by node, from the attaining box vertex (the multiplier of a
+    split on z_j gets its sign term times z_j there)."""
+    shapes = cr.node_shapes(net)
     lo, hi = box
     c, r = (lo + hi) / 2.0, (hi - lo) / 2.0
     sgn = np.sign(A_x)
-    v = c[None, :] + sgn * r[None, :] if upper else c[None, :] - sgn * r[None, :]
-    rows = v.shape[0]
+    x = c[None, :] + sgn * r[None, :] if upper else c[None, :] - sgn * r[None, :]
+    rows = x.shape[0]
     ga, gb = {}, np.zeros((rows, len(terms)))
+    val = {}
+    get = lambda i: x if i == -1 else val[i]  # noqa: E731
     for i, nd in enumerate(net.nodes):
+        v = get(nd.in0)
         if nd.op == "dense":
-            v = v @ cr._f64(nd.W).T + cr._f64(nd.b)
-        else:
+            val[i] = v.reshape(rows, -1) @ cr._f64(nd.W).T + cr._f64(nd.b)
+        elif nd.op == "conv2d":
+            in_shape = tuple(net.in_shape) if nd.in0 == -1 else shapes[nd.in0]
+            x4 = v.reshape((rows,) + tuple(in_shape))
+            y = np.stack([cr.conv2d(x4[k], cr._f64(nd.W), nd.stride, nd.pad) for k in range(rows)])
+            val[i] = (y + cr._f64(nd.b)[None, :, None, None]).reshape(rows, -1)
+        elif nd.op == "relu":
             lam0, s, t = (q.reshape(-1) for q in rel[i])
             lam = np.where(unst[i][None, :], alpha[i], lam0[None, :])
-            a, D = pre[i], v
+            a, D = pre[i], v.reshape(rows, -1)
             for e, (ri, j, S) in enumerate(terms):
                 if ri == i:
                     gb[:, e] = (-S if upper else S) * D[:, j]
             on_lam, on_t = (a < 0.0, a > 0.0) if upper else (a > 0.0, a < 0.0)
             ga[i] = np.where(unst[i][None, :] & on_lam, a * D, 0.0)
-            v = np.where(on_lam, lam * D, s[None, :] * D + np.where(on_t, t[None, :], 0.0))
+            val[i] = np.where(on_lam, lam * D, s[None, :] * D + np.where(on_t, t[None, :], 0.0))
+        elif nd.op == "add":
+            val[i] = v.reshape(rows, -1) + get(nd.in1).reshape(rows, -1)
+        elif nd.op == "flatten":
+            val[i] = v.reshape(rows, -1)
     return ga, gb
 
 

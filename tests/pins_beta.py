@@ -13,7 +13,10 @@ formulas:
     points satisfying the split constraints;
   * the loop on 2-input networks: it verifies properties that a dense grid confirms with a
     margin, never verifies a property the grid refutes, every bound it computes contains
-    the grid points of its subdomain, and its bookkeeping is consistent.
+    the grid points of its subdomain, and its bookkeeping is consistent;
+  * the same on networks with residual additions (a convolutional net and a dense residual
+    block): beta = 0 gives the subdomain CROWN bounds, finite differences, soundness, and
+    with one ReLU layer the split-constrained triangle LP's optimum.
 """
 from __future__ import annotations
 
@@ -226,4 +229,111 @@ def pin_bab_on_grids(B):
     assert not res.verified and res.remaining > 0
 
 
-BETA_PINS = [pin_beta_zero_is_domain_crown, pin_beta_gradient_fd, pin_beta_lp, pin_beta_sound, pin_bab_on_grids]
+def _splits_of(doms, S):
+    pad = lambda d, k: [s[k] for s in d] + [d[0][k]] * (S - len(d))  # noqa: E731
+    return Splits(np.array([pad(d, 0) for d in doms], np.int32), np.array([pad(d, 1) for d in doms], np.int32),
+                  np.array([pad(d, 2) for d in doms], np.int8))
+
+
+def pin_beta_residual_nets(B):
+    """Residual networks (a conv net with a residual block, a dense residual block): with
+    beta = 0 and CROWN's slopes the subdomain CROWN bounds (an infeasible domain stays
+    infeasible); the multiplier and slope gradients match central finite differences; random
+    and optimised states stay sound on sampled points that satisfy the splits."""
+    from tests.pins_alpha import _residual_cases
+    rng = np.random.default_rng(21)
+    n_checked = 0
+    for net, x0, eps, C in _residual_cases():
+        root = cr.crown(net, x0, eps, C)
+        order = B.default_order(net, root)
+        m = C.shape[0]
+        ids = [i for i, nd in enumerate(net.nodes) if nd.op == "relu"]
+        act = [(r, int(np.flatnonzero(root.layer_l[i] > 0)[0])) for r, i in enumerate(ids) if np.any(root.layer_l[i] > 0)]
+        doms = _domains(order, rng, 4, 2) + ([[order[0] + (1,), act[0] + (-1,)]] if act else [])
+        LB, UB = cr.crown_domains(net, root, C, _splits_of(doms, 2))
+        lo, hi = box_of(x0, eps, (0.0, 1.0))
+        X = lo + (hi - lo) * rng.random((20000, lo.size))
+        for k, d in enumerate(doms):
+            dr = B.domain_relaxation(net, root, d)
+            if dr is None:
+                assert np.all(np.isposinf(LB[k])) and not B.beta_crown(net, root, C, d, iters=1).feasible
+                continue
+            al0 = {i: np.tile(dr[0][i][0].reshape(-1), (m, 1)) for i in dr[0]}
+            z = np.zeros((m, len(d)))
+            lb, ub = B.beta_bound(net, root, C, d, al0, al0, z, z)[:2]
+            np.testing.assert_allclose(lb, LB[k], rtol=1e-12, atol=1e-12)
+            np.testing.assert_allclose(ub, UB[k], rtol=1e-12, atol=1e-12)
+            al, au, bl, bu = _random_state(B, net, (root, d), m, rng)
+            out = B.beta_bound(net, root, C, d, al, au, bl, bu)
+            h = 1e-6
+            for e in range(len(d)):
+                for q in range(min(m, 3)):
+                    for which, base, g in (("l", bl, out[4]), ("u", bu, out[5])):
+                        p, mi = base.copy(), base.copy()
+                        p[q, e] += h
+                        mi[q, e] = max(mi[q, e] - h, 0.0)
+                        args = (lambda b: (b, bu)) if which == "l" else (lambda b: (bl, b))
+                        idx = 0 if which == "l" else 1
+                        fd = (B.beta_bound(net, root, C, d, al, au, *args(p))[idx][q] -
+                              B.beta_bound(net, root, C, d, al, au, *args(mi))[idx][q]) / (p[q, e] - mi[q, e])
+                        assert abs(fd - g[q, e]) <= 1e-6 * (1 + abs(g[q, e])), (d, e, q, which, fd, g[q, e])
+                        n_checked += 1
+            for i in al:
+                unst = np.flatnonzero(dr[1][i])
+                if not unst.size:
+                    continue
+                j = unst[0]
+                p = {kk: v.copy() for kk, v in al.items()}
+                mi = {kk: v.copy() for kk, v in al.items()}
+                p[i][0, j] += 1e-6
+                mi[i][0, j] -= 1e-6
+                fd = (B.beta_bound(net, root, C, d, p, au, bl, bu)[0][0] -
+                      B.beta_bound(net, root, C, d, mi, au, bl, bu)[0][0]) / 2e-6
+                assert abs(fd - out[2][i][0, j]) <= 1e-6 * (1 + abs(out[2][i][0, j]))
+            P = X[_in_domain(net, X, d)]
+            if len(P):
+                Y = spec_values(net, C, P)
+                r = B.beta_crown(net, root, C, d, iters=15)
+                for lb_, ub_ in (out[:2], (r.lb, r.ub)):
+                    assert np.all(Y >= lb_[None] - 1e-9 * (1 + np.abs(Y))) and np.all(Y <= ub_[None] + 1e-9 * (1 + np.abs(Y)))
+    assert n_checked >= 30
+
+
+def pin_beta_residual_lp(B):
+    """A dense residual block with one ReLU layer: on subdomains, optimised beta-CROWN reaches
+    the triangle LP with the split-clamped neuron intervals (a minimax identity over slopes
+    and multipliers) and never passes it."""
+    from tests.pins_alpha import _residual_dense, residual_lp
+    rng = np.random.default_rng(22)
+    n_done = 0
+    for seed in (84, 85, 87):
+        net, x0, C = _residual_dense(seed, n0=4, hid=12)
+        root = cr.crown(net, x0[0], np.float32(0.3), C[0])
+        order = B.default_order(net, root)
+        for d in _domains(order, rng, 3, 2):
+            if B.domain_relaxation(net, root, d) is None:
+                continue
+            clamped = cr.CrownResult(lb=None, ub=None, box=root.box)
+            clamped.layer_l = {i: v.copy() for i, v in root.layer_l.items()}
+            clamped.layer_u = {i: v.copy() for i, v in root.layer_u.items()}
+            for r, j, sg in d:
+                if sg > 0:
+                    clamped.layer_l[1][j] = max(clamped.layer_l[1][j], 0.0)
+                else:
+                    clamped.layer_u[1][j] = min(clamped.layer_u[1][j], 0.0)
+            try:
+                lp_lo = residual_lp(net, clamped, C[0], upper=False)
+                lp_hi = residual_lp(net, clamped, C[0], upper=True)
+            except AssertionError:   # the splits exclude every point of the box: no LP optimum
+                continue
+            r = B.beta_crown(net, root, C[0], d, iters=400, lr_alpha=0.05, lr_beta=0.5)
+            r0 = B.beta_crown(net, root, C[0], d, iters=0)
+            assert np.all(r.lb <= lp_lo + 1e-7 * (1 + np.abs(lp_lo))) and np.all(r.ub >= lp_hi - 1e-7 * (1 + np.abs(lp_hi)))
+            assert np.all(lp_lo - r.lb <= 1e-3 * (1 + np.abs(lp_lo)) + 0.03 * (lp_lo - r0.lb)), (seed, d, lp_lo, r.lb, r0.lb)
+            assert np.all(r.ub - lp_hi <= 1e-3 * (1 + np.abs(lp_hi)) + 0.03 * (r0.ub - lp_hi)), (seed, d, lp_hi, r.ub, r0.ub)
+            n_done += 1
+    assert n_done >= 4
+
+
+BETA_PINS = [pin_beta_zero_is_domain_crown, pin_beta_gradient_fd, pin_beta_lp, pin_beta_sound, pin_bab_on_grids,
+             pin_beta_residual_nets, pin_beta_residual_lp]

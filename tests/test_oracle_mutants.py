@@ -114,6 +114,12 @@ BETA_MUTANTS = {
     "beta_split_sign_ignored": ("(ids[int(r)], int(j), -1.0 if sg > 0 else 1.0)", "(ids[int(r)], int(j), 1.0)"),
     "bab_branches_same_neuron": ("nxt = next((o for o in order if o not in used), None)", "nxt = order[0] if order else None"),
     "bab_keeps_verified": ("if np.all(r.lb > 0.0):\n                pruned += 1", "if False:\n                pruned += 1"),
+    # residual networks: an add's coefficients reach one input only; the forward evaluation
+    # drops the skip connection
+    "beta_add_one_input": ("            add_to(nd.in0, A)\n            add_to(nd.in1, A)",
+                           "            add_to(nd.in0, A)"),
+    "beta_forward_drops_skip": ("val[i] = v.reshape(rows, -1) + get(nd.in1).reshape(rows, -1)",
+                                "val[i] = get(nd.in1).reshape(rows, -1)"),
 }
 
 
