@@ -75,7 +75,8 @@ typedef struct {
  * n_domains x per_domain entries each, DEVICE pointers, row-major by domain:
  *   relu_id[d*per_domain + k]  index of the ReLU node among the network's ReLU nodes, in
  *                              node order (0 = first ReLU);
- *   neuron[...]                flat index into that ReLU's tensor;
+ *   neuron[...]                flat index into that ReLU's tensor ((C, H, W) order for a
+ *                              ReLU on a convolution output);
  *   sign[...]                  +1: the pre-activation is fixed to z >= 0 (active),
  *                              -1: fixed to z <= 0 (inactive).
  * A split slot with relu_id -1 is unused (skipped).
@@ -259,7 +260,8 @@ int64_t vcr_relu_neurons(const vcr_ctx *ctx);
  * (as in vcr_alpha_crown_bounds) are optimised jointly by projected Adam steps, and each bound
  * is the best one evaluated (the first evaluation is CROWN's, as vcr_crown_bounds with the
  * same splits).  Intermediate bounds: the root's full CROWN, with each split neuron's interval
- * clamped.  Networks of dense and relu nodes. */
+ * clamped.  Every network vcr_crown_bounds takes (dense/relu chains and convolutional
+ * networks, as vcr_alpha_crown_bounds). */
 typedef struct {
   int32_t iters;            /* optimisation steps after the first evaluation (>= 0) */
   float lr_alpha, lr_beta;  /* Adam step sizes (> 0) */
@@ -281,7 +283,9 @@ vcr_status vcr_beta_crown_bounds(vcr_ctx *ctx, const float *x0, float eps, const
  * neuron of the priority order that it has not split yet into an active and an inactive
  * child, bounds the children with beta-CROWN and keeps those with a non-positive lower bound
  * (infeasible children are dropped).  Verified when no subdomain is left; otherwise unknown
- * after max_rounds, or when a subdomain has no neuron left to split. */
+ * after max_rounds, or when a subdomain has no neuron left to split.  On convolutional
+ * networks the root's intermediate passes run again in every round (on dense/relu chains the
+ * first round's are reused). */
 typedef struct {
   int32_t batch;            /* subdomains split per round (>= 1) */
   int32_t max_rounds;       /* in [0, VCR_MAX_SPLITS]: a subdomain gains one split per round

@@ -42,7 +42,9 @@ vcr_status graph_ibp(vcr_ctx *c, const float *x0, int32_t B, float eps, const fl
                      float *ub);
 vcr_status graph_alpha(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m,
                        const vcr_alpha_opts &o, int64_t n_total, float *lb, float *ub);
-size_t graph_workspace_bytes(vcr_ctx *c, int32_t B, int32_t m, bool alpha);
+vcr_status graph_beta(vcr_ctx *c, const float *x0, float eps, const float *C, int32_t m, const vcr_splits *splits,
+                      const vcr_alpha_opts &o, int64_t n_total, float lr_beta, float *lb, float *ub);
+size_t graph_workspace_bytes(vcr_ctx *c, int32_t B, int32_t m, int32_t D, int32_t S, bool alpha);
 vcr_status graph_plan(vcr_ctx *c, int32_t B, int32_t m, int *chunk_out, size_t *bytes_out, bool alpha);
 }  // namespace vcr
 
@@ -1354,7 +1356,6 @@ vcr_status vcr_beta_crown_bounds(vcr_ctx *c, const float *x0, float eps, const f
   const auto t0 = std::chrono::steady_clock::now();
   vcr_status st = check_common(c, x0, 1, eps, C, m, lb, ub);
   if (st != VCR_OK) return st;
-  if (c->graph) return fail(c, VCR_ERR_UNSUPPORTED, "beta-CROWN is built for networks of dense and relu nodes");
   if (!splits) return fail(c, VCR_ERR_ARG, "null splits");
   st = check_splits(c, splits, m);
   if (st != VCR_OK) return st;
@@ -1363,6 +1364,8 @@ vcr_status vcr_beta_crown_bounds(vcr_ctx *c, const float *x0, float eps, const f
   st = check_finite_inputs(c, x0, 1, C, m);
   if (st != VCR_OK) return st;
   AlphaCall ac = alpha_call_of(c, *opts, true);
+  if (c->graph)
+    return after_call(c, graph_beta(c, x0, eps, C, m, splits, ac.o, ac.n_total, ac.lr_beta, lb, ub), t0);
   return after_call(c, crown_impl(c, x0, 1, eps, C, m, splits, lb, ub, &ac), t0);
 }
 
@@ -1372,7 +1375,6 @@ vcr_status vcr_bab_verify(vcr_ctx *c, const float *x0, float eps, const float *C
   const auto t0 = std::chrono::steady_clock::now();
   if (!opts || !res) return fail(c, VCR_ERR_ARG, "null options or result");
   if (!c->loaded) return fail(c, VCR_ERR_STATE, "no network loaded");
-  if (c->graph) return fail(c, VCR_ERR_UNSUPPORTED, "branch and bound is built for networks of dense and relu nodes");
   if (c->relu_n.empty()) return fail(c, VCR_ERR_ARG, "branch and bound needs at least one ReLU");
   if (opts->batch < 1 || opts->max_rounds < 0) return fail(c, VCR_ERR_ARG, "batch must be >= 1, max_rounds >= 0");
   // a subdomain gains one split per round, and the split table holds VCR_MAX_SPLITS
@@ -1398,12 +1400,18 @@ vcr_status vcr_bab_verify(vcr_ctx *c, const float *x0, float eps, const float *C
   hipStream_t s = c->stream;
   *res = vcr_bab_result{};
   const AlphaCall ac = alpha_call_of(c, opts->bound, false);
+  // alpha-CROWN (no splits) or beta-CROWN (subdomains) on either network path
+  auto bound = [&](const vcr_splits *sp, float *l, float *u) -> vcr_status {
+    if (!c->graph) return crown_impl(c, x0, 1, eps, C, m, sp, l, u, &ac);
+    return sp ? graph_beta(c, x0, eps, C, m, sp, ac.o, ac.n_total, ac.lr_beta, l, u)
+              : graph_alpha(c, x0, 1, eps, C, m, ac.o, ac.n_total, l, u);
+  };
 
   // root: alpha-CROWN
   st = bab_reserve(c, sizeof(float) * 2 * (size_t)m);
   if (st != VCR_OK) return st;
   float *d_lb = static_cast<float *>(c->bab_buf), *d_ub = d_lb + m;
-  st = crown_impl(c, x0, 1, eps, C, m, nullptr, d_lb, d_ub, &ac);
+  st = bound(nullptr, d_lb, d_ub);
   if (st != VCR_OK) return st;
   std::vector<float> h_lb(m);
   HIP_TRY(c, hipMemcpyAsync(h_lb.data(), d_lb, sizeof(float) * m, hipMemcpyDeviceToHost, s));
@@ -1507,7 +1515,7 @@ vcr_status vcr_bab_verify(vcr_ctx *c, const float *x0, float eps, const float *C
       HIP_TRY(c, hipMemcpyAsync(d_n, hn.data(), sizeof(int32_t) * nb, hipMemcpyHostToDevice, s));
       HIP_TRY(c, hipMemcpyAsync(d_s, hs.data(), nb, hipMemcpyHostToDevice, s));
       vcr_splits sp{D, S, d_r, d_n, d_s};
-      st = crown_impl(c, x0, 1, eps, C, m, &sp, k_lb, k_ub, &ac);
+      st = bound(&sp, k_lb, k_ub);
       if (st != VCR_OK) return st;
       std::vector<float> kl((size_t)D * m);
       HIP_TRY(c, hipMemcpyAsync(kl.data(), k_lb, sizeof(float) * D * m, hipMemcpyDeviceToHost, s));
@@ -1570,8 +1578,7 @@ vcr_status vcr_workspace_bytes(vcr_ctx *c, int32_t B, int32_t m, int32_t n_domai
   if (!c->loaded) return fail(c, VCR_ERR_STATE, "no network loaded");
   if (B <= 0 || m <= 0 || n_domains < 0) return fail(c, VCR_ERR_ARG, "bad sizes");
   if (c->graph) {
-    if (n_domains > 0) return fail(c, VCR_ERR_UNSUPPORTED, "subdomain splits are built for MLPs only");
-    *bytes = graph_workspace_bytes(c, B, m, false);
+    *bytes = graph_workspace_bytes(c, B, m, n_domains, n_domains > 0 ? VCR_MAX_SPLITS : 0, false);
     return VCR_OK;
   }
   const uint64_t cap = c->ws_cap;

@@ -51,6 +51,11 @@ struct ConvTArgs {
   // and the coefficients before relaxation, both laid out like out
   const float *alpha;
   float *pre;
+  // branch-and-bound subdomains of one input (dense windows with a ReLU; every row belongs
+  // to unit 0, so a parameter's offset is its neuron's channels-last index): the split
+  // table of this ReLU (relu_index) and, with splits.beta, the multipliers' terms
+  SplitTable splits;
+  int32_t relu_index;
   // filled by launch_convt
   int32_t n_cls;
   ConvClass cls[4];
@@ -119,6 +124,10 @@ struct FwdConvArgs {
   float *grad;               // [rows][out_rs] with P
   float *out;              // [rows][out_rs], (Ho, Ho, Co)
   int64_t out_rs;
+  // with P, subdomains of one input (units = 1): the split table of this ReLU (relu_index);
+  // with splits.grad_beta, each split's multiplier gradient S z at the row's vertex
+  SplitTable splits;
+  int32_t relu_index;
 };
 hipError_t launch_fwd_conv(const FwdConvArgs &a, hipStream_t s);
 // out = x + y over rows of n values (the add node in the gradient pass)

@@ -26,6 +26,7 @@
 // and reduces the constants over the tile's columns into one partial per GEMM row.
 #include "conv.h"
 #include "relax.h"
+#include "splits.h"
 
 #include <algorithm>
 #include <vector>
@@ -62,7 +63,7 @@ __device__ __attribute__((aligned(16))) float g_zero4[4] = {0.f, 0.f, 0.f, 0.f};
 // Epilogue shared by the transposed-convolution kernels: relaxation (or identity), residual,
 // constant terms per GEMM row for the tile m0.. of class cl, columns n0..; acc holds the
 // MB x NB 32 x 32 MFMA blocks of wave (wm, wn); scratch is >= 24 BM bytes of free LDS.
-template <int BM, int BN, int WM, int WN, bool RELU, bool AL>
+template <int BM, int BN, int WM, int WN, bool RELU, bool AL, bool SPL>
 __device__ __forceinline__ void convt_epilogue(const ConvTArgs &p, const ConvClass &cl,
                                                const f32x16 (&acc)[BM / WM / 32][BN / WN / 32], int m0, int n0,
                                                int nt, float *scratch) {
@@ -80,6 +81,7 @@ __device__ __forceinline__ void convt_epilogue(const ConvTArgs &p, const ConvCla
   int64_t *s_rb = s_ob + BM;                                 // residual offset, or -1
   int *s_pb = reinterpret_cast<int *>(s_rb + BM);            // parameter offset, -1 outside the image
   int *s_mo = s_pb + BM;                                     // partial-sum index, -1 past M
+  int *s_rr = s_mo + BM;                                     // coefficient row (split lookups)
   const int S_in2 = p.S_in * p.S_in;
   const float4 *__restrict__ Pp = p.P_pos;
   const float *__restrict__ resp = p.res;
@@ -100,6 +102,7 @@ __device__ __forceinline__ void convt_epilogue(const ConvTArgs &p, const ConvCla
     const bool inside = valid && gy >= 0 && gx >= 0 && gy < p.H_in && gx < p.H_in;
     const int du = u - p.res_off, dw = w - p.res_off;
     s_mo[tr] = valid ? (int)r * S_in2 + u * p.S_in + w : -1;
+    s_rr[tr] = (int)r;
     s_ob[tr] = (int64_t)r * p.row_stride_in + ((int64_t)u * p.S_in + w) * p.C_in;
     s_pb[tr] = inside ? ((an.x * p.H_in + gy) * p.H_in + gx) * p.C_in : -1;
     s_rb[tr] = inside && resp && du >= 0 && dw >= 0 && du < p.res_S && dw < p.res_S
@@ -161,13 +164,22 @@ __device__ __forceinline__ void convt_epilogue(const ConvTArgs &p, const ConvCla
         float ap = 0.f;
         if (pb >= 0) {   // inside the image: relax (or identity) and constant terms
           if constexpr (RELU) {
-            float lam = prm[b][j][t].x;
+            float4 q = prm[b][j][t];
+            int ent = -1;
+            float sterm = 0.f;
+            if constexpr (SPL) {   // subdomains: a split neuron's clamped relaxation
+              if (store) q = split_override(p.splits, s_rr[lr + t], p.relu_index, pb + ncol[j], q, &ent, &sterm);
+            }
+            float lam = q.x;
             if constexpr (AL) {   // alpha-CROWN: the row's own slope at unstable neurons
               const float al = store ? alp[ob + ncol[j]] : 0.f;
-              lam = prm[b][j][t].z > 0.f ? al : lam;
+              lam = q.z > 0.f ? al : lam;
             }
-            ap = a > 0.f ? a * lam : a * prm[b][j][t].y;
-            x += fminf(a, 0.f) * prm[b][j][t].z + ap * prm[b][j][t].w;
+            ap = a > 0.f ? a * lam : a * q.y;
+            if constexpr (SPL) {   // beta-CROWN: the split's multiplier term
+              if (ent >= 0 && p.splits.beta) ap += p.splits.beta[(int64_t)s_rr[lr + t] * p.splits.S + ent] * sterm;
+            }
+            x += fminf(a, 0.f) * q.z + ap * q.w;
           } else {
             ap = a;
             x += a * bn[j];
@@ -205,7 +217,7 @@ __device__ __forceinline__ void convt_epilogue(const ConvTArgs &p, const ConvCla
 // RELU: the destination node feeds a ReLU (relaxation parameters P_pos), else the identity
 // with a per-channel constant (bias).  AL (with RELU, dense windows): alpha-CROWN's per-row
 // slopes and the record of the coefficients before relaxation.
-template <int BM, int BN, int BK, int WM, int WN, int MINB, bool RELU, bool AL = false>
+template <int BM, int BN, int BK, int WM, int WN, int MINB, bool RELU, bool AL = false, bool SPL = false>
 __global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
   static_assert(BK == 16 || BK == 32, "LDS swizzle assumes 4 or 8 chunks per row");
   constexpr int CPR = BK / 4;                 // 16-byte chunks per tile row
@@ -332,8 +344,8 @@ __global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
   }
 
   // ---- epilogue (the operand buffers are free after the main loop's last barrier) ----
-  static_assert(24 * BM <= (int)sizeof(As), "epilogue row information must fit the A buffers");
-  convt_epilogue<BM, BN, WM, WN, RELU, AL>(p, cl, acc, m0, n0, nt, &As[0][0]);
+  static_assert(28 * BM <= (int)sizeof(As), "epilogue row information must fit the A buffers");
+  convt_epilogue<BM, BN, WM, WN, RELU, AL, SPL>(p, cl, acc, m0, n0, nt, &As[0][0]);
 }
 
 // Classes of one axis: positions u of the destination window with the same taps ky, as an
@@ -470,12 +482,20 @@ hipError_t launch_convt_part(const ConvTArgs &a0, int part, hipStream_t s) {
   const ConvtDispatch &d = plan[part];
   ConvTArgs a = a0;
   const bool al = a.alpha || a.pre;
+  const bool spl = a.splits.D > 0;
   if (al && (!a.alpha || !a.pre || !a.P_pos || !a.dense)) return hipErrorInvalidValue;
+  if (spl && (!a.P_pos || !a.dense || a.splits.rows_per_domain <= 0)) return hipErrorInvalidValue;
+  const dim3 blk256(256);
   if (a.N_pad % 128 == 0) {   // 128 x 128 tiles, 2 x 2 waves of 64 x 64
     const int64_t blk = convt_fill(a, cu, d, 128, 128);
     if (blk < 0) return hipErrorInvalidValue;
-    if (blk > 0 && al)
-      hipLaunchKernelGGL((k_convt<128, 128, 16, 2, 2, 2, true, true>), dim3((unsigned)blk), dim3(256), 0, s, a);
+    const dim3 g((unsigned)blk);
+    if (blk > 0 && al && spl)
+      hipLaunchKernelGGL((k_convt<128, 128, 16, 2, 2, 2, true, true, true>), g, blk256, 0, s, a);
+    else if (blk > 0 && spl)
+      hipLaunchKernelGGL((k_convt<128, 128, 16, 2, 2, 2, true, false, true>), g, blk256, 0, s, a);
+    else if (blk > 0 && al)
+      hipLaunchKernelGGL((k_convt<128, 128, 16, 2, 2, 2, true, true>), g, blk256, 0, s, a);
     else if (blk > 0 && a.P_pos)
       hipLaunchKernelGGL((k_convt<128, 128, 16, 2, 2, 3, true>), dim3((unsigned)blk), dim3(256), 0, s, a);
     else if (blk > 0)
@@ -483,8 +503,13 @@ hipError_t launch_convt_part(const ConvTArgs &a0, int part, hipStream_t s) {
   } else {                           // 256 x 64 tiles, 4 x 1 waves of 64 x 64
     const int64_t blk = convt_fill(a, cu, d, 256, 64);
     if (blk < 0) return hipErrorInvalidValue;
-    if (blk > 0 && al)
-      hipLaunchKernelGGL((k_convt<256, 64, 16, 4, 1, 2, true, true>), dim3((unsigned)blk), dim3(256), 0, s, a);
+    const dim3 g((unsigned)blk);
+    if (blk > 0 && al && spl)
+      hipLaunchKernelGGL((k_convt<256, 64, 16, 4, 1, 2, true, true, true>), g, blk256, 0, s, a);
+    else if (blk > 0 && spl)
+      hipLaunchKernelGGL((k_convt<256, 64, 16, 4, 1, 2, true, false, true>), g, blk256, 0, s, a);
+    else if (blk > 0 && al)
+      hipLaunchKernelGGL((k_convt<256, 64, 16, 4, 1, 2, true, true>), g, blk256, 0, s, a);
     else if (blk > 0 && a.P_pos)
       hipLaunchKernelGGL((k_convt<256, 64, 16, 4, 1, 3, true>), dim3((unsigned)blk), dim3(256), 0, s, a);
     else if (blk > 0)
@@ -1153,12 +1178,18 @@ FastDiv make_fastdiv(uint32_t d) {
 // selected by the recorded coefficient's sign (lam D where it is positive, s D + t where it
 // is negative, s D where it is 0), with the slope gradient at unstable neurons.  ob, pb, rb:
 // the element's row offsets into out (and alpha, pre, grad), P and res, without the channel.
-__device__ __forceinline__ void fwd_apply(const FwdConvArgs &p, int64_t ob, int64_t pb, int64_t rb, int32_t n,
-                                          float D) {
+__device__ __forceinline__ void fwd_apply(const FwdConvArgs &p, int64_t r, int64_t ob, int64_t pb, int64_t rb,
+                                          int32_t n, float D) {
   if (p.res) D += p.res[rb + n];
   const int64_t off = ob + n;
   if (p.P) {
-    const float4 prm = p.P[pb + n];
+    float4 prm = p.P[pb + n];
+    if (p.splits.D > 0) {   // subdomains (unit 0 only: pb + n is the neuron's index)
+      int ent = -1;
+      float sterm = 0.f;
+      prm = split_override(p.splits, (int)r, p.relu_index, (int)(pb + n), prm, &ent, &sterm);
+      if (ent >= 0 && p.splits.grad_beta) p.splits.grad_beta[r * p.splits.S + ent] = sterm * D;
+    }
     const bool unst = prm.z > 0.f;
     const float lam = unst ? p.alpha[off] : prm.x;
     const float an = p.pre[off];
@@ -1284,15 +1315,17 @@ __global__ __launch_bounds__(256, 2) void k_fwd_conv(const FwdConvArgs p, FastDi
   }
   // epilogue: the offsets of every tile row once (a row per thread), through the free A
   // buffer; -1 marks rows past the end
-  static_assert(24 * BM <= (int)sizeof(As), "row offsets must fit the A buffers");
+  static_assert(28 * BM <= (int)sizeof(As), "row offsets must fit the A buffers");
   int64_t *s_ob = reinterpret_cast<int64_t *>(&As[0][0]);
   int64_t *s_pb = s_ob + BM;
   int64_t *s_rb = s_pb + BM;
+  int *s_r = reinterpret_cast<int *>(s_rb + BM);
   for (int tr = tid; tr < BM; tr += 256) {
     const uint32_t m = (uint32_t)(m0 + tr);
     if (m < Mtot) {
       const uint32_t r = fdiv(m, div_pos);
       fwd_offsets(p, r, (int)(m - r * (uint32_t)HW), &s_ob[tr], &s_pb[tr], &s_rb[tr]);
+      s_r[tr] = (int)r;
     } else {
       s_ob[tr] = -1;
     }
@@ -1310,7 +1343,7 @@ __global__ __launch_bounds__(256, 2) void k_fwd_conv(const FwdConvArgs p, FastDi
       for (int v = 0; v < 16; ++v) {
         const int lr = wm * (BM / WM) + i * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
         const int64_t ob = s_ob[lr];
-        if (ob >= 0) fwd_apply(p, ob, s_pb[lr], s_rb[lr], n, acc[i][j][v] + bn);
+        if (ob >= 0) fwd_apply(p, s_r[lr], ob, s_pb[lr], s_rb[lr], n, acc[i][j][v] + bn);
       }
   }
 }
@@ -1352,7 +1385,7 @@ __global__ __launch_bounds__(256) void k_fwd_conv_small(const FwdConvArgs p) {
     }
     int64_t ob, pb, rb;
     fwd_offsets(p, r, pos, &ob, &pb, &rb);
-    fwd_apply(p, ob, pb, rb, n, acc + bn);
+    fwd_apply(p, r, ob, pb, rb, n, acc + bn);
   }
 }
 
@@ -1362,6 +1395,7 @@ hipError_t launch_fwd_conv(const FwdConvArgs &a, hipStream_t s) {
     return hipErrorInvalidValue;
   if (a.P && (!a.alpha || !a.pre || !a.grad || a.rows_per_unit <= 0 || a.units <= 0 || a.res))
     return hipErrorInvalidValue;
+  if (a.splits.D > 0 && (!a.P || a.units != 1 || a.splits.rows_per_domain <= 0)) return hipErrorInvalidValue;
   const int64_t HW = (int64_t)a.Ho * a.Ho;
   if (a.out_rs < HW * a.Co || a.in_rs < (int64_t)a.Hi * a.Hi * a.Ci || (a.res && a.res_rs < HW * a.Co))
     return hipErrorInvalidValue;

@@ -661,7 +661,12 @@ __global__ void k_split_prepare(const SplitPrepArgs a) {
     else
       u = fminf(u, 0.f);
     if (l > u) infeasible = true;
-    a.ent_n[(int64_t)d * a.S + k] = en[k];
+    int jn = en[k];
+    if (a.hwc_C && a.hwc_C[er[k]] > 0) {   // (c, y, x) -> (y, x, c)
+      const int C = a.hwc_C[er[k]], HW = a.relu_n[er[k]] / C;
+      jn = (jn % HW) * C + jn / HW;
+    }
+    a.ent_n[(int64_t)d * a.S + k] = jn;
     float4 q = relax_params(l, u, 0.f, a.lam_rule);
     q.w = es[k] > 0 ? -1.f : 1.f;   // sign of the split's Lagrangian term
     a.ent_p[(int64_t)d * a.S + k] = q;

@@ -34,6 +34,7 @@
 // a lane group holds with a fixed butterfly, so results are deterministic and do not depend
 // on which other rows share the tile.
 #include "kernels.h"
+#include "splits.h"
 
 namespace vcr {
 
@@ -64,28 +65,6 @@ __device__ __forceinline__ void map_tile(int bid, int G, int n_mt, int n_nt, int
   nt = idx / gm;
 }
 
-// The split entry of (the row's domain, relu, neuron n), if any: its relaxation replaces
-// (lam, s, t); *ent receives the entry index and *sterm its Lagrangian sign.
-__device__ __forceinline__ float4 split_override(const SplitTable &st, int row, int relu, int n, float4 prm,
-                                                 int *ent = nullptr, float *sterm = nullptr) {
-  int d = row / st.rows_per_domain;
-  d = d < st.D ? d : st.D - 1;
-  const int e0 = st.off[d * (st.R + 1) + relu];
-  const int e1 = st.off[d * (st.R + 1) + relu + 1];
-  for (int e = e0; e < e1; ++e) {
-    if (st.ent_n[d * st.S + e] == n) {
-      const float4 q = st.ent_p[d * st.S + e];
-      prm.x = q.x;
-      prm.y = q.y;
-      prm.z = q.z;
-      if (ent) {
-        *ent = e;
-        *sterm = q.w;
-      }
-    }
-  }
-  return prm;
-}
 
 // Split lookups of one tile through LDS: flags[d - d0][n - n0] is the entry index of
 // (domain d, neuron n) at this ReLU, or -1.  All threads of the workgroup build it once, so

@@ -119,6 +119,9 @@ struct GraphNet {
   std::vector<int> val_slot;              // per node: slot of its forward values, or -1
   std::vector<int64_t> val_rs;            // per node: floats per row of its forward values
   std::vector<int64_t> fwd_slot_floats;   // floats per row of every slot
+  // device [2 R]: neurons of every ReLU node, then its channels (0 for flat nodes), for the
+  // split preparation of subdomains
+  int32_t *d_relu_info = nullptr;
 };
 
 void destroy_graph(GraphNet *g) {
@@ -129,6 +132,7 @@ void destroy_graph(GraphNet *g) {
   }
   if (g->bias_arena) (void)hipFree(g->bias_arena);
   if (g->param_arena) (void)hipFree(g->param_arena);
+  if (g->d_relu_info) (void)hipFree(g->d_relu_info);
   delete g;
 }
 
@@ -538,6 +542,19 @@ struct GBufs {
   int32_t *flag = nullptr;
   float *vtx = nullptr;
   std::vector<float *> fslots;
+  // subdomains: the split table, per-domain flags, the root's bound pointers for the split
+  // preparation, and (beta-CROWN) the multipliers with their Adam moments and gradient
+  int32_t *off = nullptr, *ent_n = nullptr, *flags = nullptr;
+  float4 *ent_p = nullptr;
+  const float **Lptr = nullptr;
+  float *mul = nullptr, *mul_mom = nullptr, *mul_vel = nullptr, *mul_grad = nullptr;
+};
+
+// Sizes of a call: B root inputs, m spec rows; ci inputs per chunk of the intermediate passes,
+// cs units per chunk of the spec pass (inputs, or subdomains when D > 0, with S splits each)
+struct GShape {
+  int B = 1, m = 1, ci = 1, cs = 1, D = 0, S = 0;
+  bool alpha = false;
 };
 
 struct GPlanSize {
@@ -570,8 +587,9 @@ int64_t max_part_per_row(const GraphNet *g) {
   return best;
 }
 
-size_t carve_graph(const vcr_ctx *c, const GraphNet *g, Workspace &w, int B, int m, int chunk, GBufs *bf,
-                   bool alpha = false) {
+size_t carve_graph(const vcr_ctx *c, const GraphNet *g, Workspace &w, const GShape &sh, GBufs *bf) {
+  const int B = sh.B, m = sh.m;
+  const bool alpha = sh.alpha;
   const int nn = (int)g->nodes.size();
   const int64_t ld0 = ld_of(g->n0);
   bf->c0 = take<float>(w, (size_t)B * ld0);
@@ -598,7 +616,7 @@ size_t carve_graph(const vcr_ctx *c, const GraphNet *g, Workspace &w, int B, int
   const GNode &out = g->nodes[nn - 1];
   bf->CW = take<float>(w, (size_t)B * m * out.ld_in);
   bf->Cb = take<float>(w, (size_t)B * m);
-  const int64_t rows = max_rows_per_unit(g, m) * chunk;
+  const int64_t rows = std::max(max_rows_per_unit(g, m) * sh.ci, 2 * (int64_t)m * sh.cs);
   size_t nslots = 0;
   for (auto &pp : g->passes) nslots = std::max(nslots, pp.slot_floats.size());
   bf->slots.assign(nslots, nullptr);
@@ -606,9 +624,9 @@ size_t carve_graph(const vcr_ctx *c, const GraphNet *g, Workspace &w, int B, int
     int64_t f = 0;
     for (auto &pp : g->passes) {
       if (s >= pp.slot_floats.size()) continue;
-      const int64_t rpu = pp.spec ? 2 * (int64_t)m : 2 * pp.rows_per_unit_mult;
+      const int64_t pr = pp.spec ? 2 * (int64_t)m * sh.cs : 2 * pp.rows_per_unit_mult * sh.ci;
       // whole GEMM row blocks: the dense GEMM reads and writes padding rows
-      f = std::max<int64_t>(f, pp.slot_floats[s] * rows_pad(rpu * chunk));
+      f = std::max<int64_t>(f, pp.slot_floats[s] * rows_pad(pr));
     }
     bf->slots[s] = take<float>(w, (size_t)f);
   }
@@ -617,8 +635,22 @@ size_t carve_graph(const vcr_ctx *c, const GraphNet *g, Workspace &w, int B, int
   bf->rows = take<int4>(w, (size_t)rows);
   bf->al.clear();
   bf->fslots.clear();
+  const int64_t ra = rows_pad(2 * (int64_t)m * sh.cs);
+  const int R = (int)g->relus.size();
+  bf->off = bf->ent_n = bf->flags = nullptr;
+  bf->ent_p = nullptr;
+  bf->Lptr = nullptr;
+  bf->mul = bf->mul_mom = bf->mul_vel = bf->mul_grad = nullptr;
+  if (sh.D > 0) {
+    bf->off = take<int32_t>(w, (size_t)sh.D * (R + 1));
+    bf->ent_n = take<int32_t>(w, (size_t)sh.D * std::max(sh.S, 1));
+    bf->ent_p = take<float4>(w, (size_t)sh.D * std::max(sh.S, 1));
+    bf->flags = take<int32_t>(w, (size_t)sh.D);
+    bf->Lptr = take<const float *>(w, (size_t)2 * R);
+    if (alpha && sh.S > 0)
+      for (float **q : {&bf->mul, &bf->mul_mom, &bf->mul_vel, &bf->mul_grad}) *q = take<float>(w, (size_t)ra * sh.S);
+  }
   if (alpha) {
-    const int64_t ra = rows_pad(2 * (int64_t)m * chunk);
     int32_t col0 = 0;
     for (size_t r = 0; r < g->relus.size(); ++r) {
       const GNode &n = g->nodes[g->relus[r]];
@@ -808,6 +840,14 @@ vcr_status graph_load(vcr_ctx *c, const vcr_node *nodes, int32_t n, const int32_
     HIP_TRY(c, hipMemcpy(g->param_arena, pl.host_params.data(), pl.host_params.size() * sizeof(float4),
                          hipMemcpyHostToDevice));
   }
+  if (dev && !g->relus.empty()) {
+    std::vector<int32_t> info;
+    for (int r : g->relus) info.push_back((int32_t)g->nodes[r].numel);
+    for (int r : g->relus) info.push_back(g->nodes[r].flat ? 0 : g->nodes[r].C);
+    HIP_TRY(c, hipMalloc(&g->d_relu_info, info.size() * sizeof(int32_t)));
+    c->net_bytes += info.size() * sizeof(int32_t);
+    HIP_TRY(c, hipMemcpy(g->d_relu_info, info.data(), info.size() * sizeof(int32_t), hipMemcpyHostToDevice));
+  }
   if (dev) HIP_TRY(c, hipDeviceSynchronize());
   destroy_graph(c->graph);
   c->graph = guard.release();
@@ -863,12 +903,22 @@ float4 *relu_P(GraphNet *g, GBufs &bf, int relu_node) { return bf.P[g->nodes[rel
 // takes the rows' slopes at unstable neurons and records the coefficients before it, and the
 // stem writes each row's box vertex.
 vcr_status run_pass(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &pp, int u0, int units, int m,
-                    uint64_t *flops, bool alpha = false) {
+                    uint64_t *flops, bool alpha = false, const SplitTable *tab = nullptr) {
   hipStream_t s = c->stream;
   const GNode &start = g->nodes[pp.start];
   const int64_t rpu = pp.spec ? 2 * (int64_t)m : 2 * pp.rows_per_unit_mult;
   const int64_t R = rpu * units;
-  HIP_TRY(c, launch_row_table(bf.rows, R, (int32_t)rpu, start.C, start.H, start.H, pp.windowed ? 1 : 0, u0, s));
+  // subdomains (tab, spec pass only): units are domains u0.. of one input, whose parameters,
+  // box and spec rows are unit 0's
+  const bool dom = tab != nullptr;
+  const int pu0 = dom ? 0 : u0;
+  if (dom) {
+    if (!pp.spec || R >= ((int64_t)1 << 31)) return fail(c, VCR_ERR_UNSUPPORTED, "internal: subdomain pass");
+    HIP_TRY(c, launch_row_table(bf.rows, R, (int32_t)R, start.C, start.H, start.H, 0, 0, s));
+  } else {
+    HIP_TRY(c, launch_row_table(bf.rows, R, (int32_t)rpu, start.C, start.H, start.H, pp.windowed ? 1 : 0, u0, s));
+  }
+  auto ridx = [&](int relu_node) { return g->nodes[relu_node].relu_index; };
   auto slot = [&](const Coef &k) { return bf.slots[k.slot]; };
   for (const Step &st : pp.steps) {
     const GNode &nd = g->nodes[st.node];
@@ -898,11 +948,11 @@ vcr_status run_pass(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &pp, int 
         InitArgs ia{};
         const bool spec = st.kind == ST_INIT_SPEC;
         const float *W = nd.hwc_in ? nd.Wh : nd.Wp;
-        ia.src = spec ? bf.CW + (int64_t)u0 * m * nd.ld_in : W;
+        ia.src = spec ? bf.CW + (int64_t)pu0 * m * nd.ld_in : W;
         ia.ld_src = nd.ld_in;
         ia.n_src = spec ? m : (int32_t)nd.numel;
-        ia.per_unit_src = spec ? 1 : 0;
-        ia.src_bias = spec ? bf.Cb + (int64_t)u0 * m : nd.b;
+        ia.per_unit_src = spec && !dom ? 1 : 0;
+        ia.src_bias = spec ? bf.Cb + (int64_t)pu0 * m : nd.b;
         ia.n_cols = (int32_t)g->nodes[st.dst.node].numel;
         ia.ldo = st.dst.row_stride;
         ia.M = (int32_t)R;
@@ -910,15 +960,18 @@ vcr_status run_pass(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &pp, int 
         if (st.relu >= 0) {
           // flat ReLU parameters have the padded row width per unit; channels-last ones numel
           const int64_t ldp = st.dst.flat ? st.dst.row_stride : g->nodes[st.dst.node].numel;
-          ia.P = relu_P(g, bf, st.relu) + (int64_t)u0 * ldp;
+          ia.P = relu_P(g, bf, st.relu) + (int64_t)pu0 * ldp;
           ia.ldp = ldp;
-          ia.param_per_unit = 1;
+          ia.param_per_unit = dom ? 0 : 1;
+          if (dom) {
+            ia.splits = *tab;
+            ia.relu_index = ridx(st.relu);
+          }
         } else {
           ia.P = g->param_arena + st.pid_off;
           ia.ldp = st.dst.row_stride;
           ia.param_per_unit = 0;
         }
-        ia.relu_index = 0;
         ia.out = slot(st.dst);
         ia.beta = bf.beta;
         if (ia.ldo != nd.ld_in) return fail(c, VCR_ERR_UNSUPPORTED, "internal: init row width mismatch");
@@ -972,6 +1025,10 @@ vcr_status run_pass(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &pp, int 
             return fail(c, VCR_ERR_UNSUPPORTED, "internal: slope row width mismatch");
           a.alpha = l.alpha;
           a.pre = l.pre;
+        }
+        if (dom && st.relu >= 0) {
+          a.splits = *tab;
+          a.relu_index = ridx(st.relu);
         }
         const int parts = convt_launches(a);
         if (parts < 0) return fail(c, VCR_ERR_UNSUPPORTED, "internal: transposed convolution shape");
@@ -1030,17 +1087,20 @@ vcr_status run_pass(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &pp, int 
         ga.ldo = nd.ld_in;
         if (st.relu >= 0) {
           const int64_t ldp = st.dst.flat ? nd.ld_in : g->nodes[st.dst.node].numel;
-          ga.P = relu_P(g, bf, st.relu) + (int64_t)u0 * ldp;
+          ga.P = relu_P(g, bf, st.relu) + (int64_t)pu0 * ldp;
           ga.ldp = ldp;
-          ga.rows_per_unit = (int32_t)rpu;
-          ga.n_units = units;
+          ga.rows_per_unit = dom ? ga.M_pad : (int32_t)rpu;
+          ga.n_units = dom ? 1 : units;
+          if (dom) {
+            ga.splits = *tab;
+            ga.relu_index = ridx(st.relu);
+          }
         } else {
           ga.P = g->param_arena + st.pid_off;
           ga.ldp = 0;
           ga.rows_per_unit = ga.M_pad;
           ga.n_units = 1;
         }
-        ga.relu_index = 0;
         ga.part = bf.part;
         if (st.dst.row_stride != nd.ld_in) return fail(c, VCR_ERR_UNSUPPORTED, "internal: dense output width mismatch");
         if (alpha && st.relu >= 0) {
@@ -1070,8 +1130,12 @@ vcr_status run_pass(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &pp, int 
 // each ReLU replaced by the line the row's coefficient selected, which leaves the slope
 // gradients in bf.al[].grad.
 vcr_status run_forward(vcr_ctx *c, GraphNet *g, GBufs &bf, int u0, int units, int32_t M, int32_t rpu,
-                       uint64_t *flops) {
+                       uint64_t *flops, const SplitTable *ftab = nullptr) {
   hipStream_t s = c->stream;
+  // subdomains: every row takes unit 0's relaxation, split neurons their own, and the
+  // multipliers' gradients are written where a split neuron's value is formed
+  const bool dom = ftab != nullptr;
+  if (dom) u0 = 0;
   const int64_t ld0 = ld_of(g->n0);
   auto val = [&](int v) { return v < 0 ? bf.vtx : bf.fslots[g->val_slot[v]]; };
   auto rs = [&](int v) { return v < 0 ? ld0 : g->val_rs[v]; };
@@ -1097,11 +1161,15 @@ vcr_status run_forward(vcr_ctx *c, GraphNet *g, GBufs &bf, int u0, int units, in
         if (f.relu >= 0) {
           const AlphaLayer &l = bf.al[f.relu];
           a.P = bf.P[f.relu] + (int64_t)u0 * l.ldp;
-          a.rows_per_unit = rpu;
-          a.units = units;
+          a.rows_per_unit = dom ? M : rpu;
+          a.units = dom ? 1 : units;
           a.alpha = l.alpha;
           a.pre = l.pre;
           a.grad = l.grad;
+          if (dom) {
+            a.splits = *ftab;
+            a.relu_index = f.relu;
+          }
         }
         a.out = val(f.out);
         a.out_rs = rs(f.out);
@@ -1126,8 +1194,12 @@ vcr_status run_forward(vcr_ctx *c, GraphNet *g, GBufs &bf, int u0, int units, in
           ga.mode = EPI_FORWARD;
           ga.P = bf.P[f.relu] + (int64_t)u0 * l.ldp;
           ga.ldp = l.ldp;
-          ga.rows_per_unit = rpu;
-          ga.n_units = units;
+          ga.rows_per_unit = dom ? ga.M_pad : rpu;
+          ga.n_units = dom ? 1 : units;
+          if (dom) {
+            ga.splits = *ftab;
+            ga.relu_index = f.relu;
+          }
           ga.alpha = l.alpha;
           ga.ld_alpha = l.ld;
           ga.pre = l.pre;
@@ -1156,50 +1228,85 @@ vcr_status run_forward(vcr_ctx *c, GraphNet *g, GBufs &bf, int u0, int units, in
 struct GraphAlphaCall {
   vcr_alpha_opts o;
   int64_t n_total = 0;
+  float lr_beta = 0.f;   // subdomains (beta-CROWN): step size of the multipliers
 };
 
-// alpha-CROWN on the spec pass, per chunk of inputs: evaluate with the current slopes (the
+// The split table of domains d0 .. d0 + dc - 1 (a slice of the one the split preparation
+// wrote for all domains); with S > 0 and beta, the multipliers of those rows.
+SplitTable domain_table(const GraphNet *g, const GBufs &bf, int d0, int dc, int m, int S, bool beta) {
+  const int R = (int)g->relus.size();
+  SplitTable t{};
+  t.off = bf.off + (int64_t)d0 * (R + 1);
+  t.ent_n = bf.ent_n + (int64_t)d0 * S;
+  t.ent_p = bf.ent_p + (int64_t)d0 * S;
+  t.R = R;
+  t.S = S;
+  t.D = dc;
+  t.rows_per_domain = 2 * m;
+  t.beta = beta && S > 0 ? bf.mul : nullptr;
+  return t;
+}
+
+// alpha-CROWN on the spec pass, per chunk of units: evaluate with the current slopes (the
 // spec pass with per-row slopes), keep each row's best bound, run the gradient pass and one
 // projected Adam step; T steps give T + 1 evaluations.  The slope kernels are the MLP path's.
-vcr_status alpha_spec_graph(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &pp, int B, int m, int chunk,
-                            const GraphAlphaCall &ac, float *lb, float *ub, uint64_t *flops, int *chunks) {
+// Units are inputs, or with D > 0 subdomains of the one input (beta-CROWN: the split
+// multipliers are optimised with the slopes, and infeasible domains report lb = +inf).
+vcr_status alpha_spec_graph(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &pp, int units_total, int m,
+                            int chunk, int D, int S, const GraphAlphaCall &ac, float *lb, float *ub, uint64_t *flops,
+                            int *chunks) {
   hipStream_t s = c->stream;
   const vcr_alpha_opts &o = ac.o;
   const int R = (int)g->relus.size();
   const int32_t rpu = 2 * m;
-  for (int u0 = 0; u0 < B; u0 += chunk) {
-    const int units = std::min(chunk, B - u0);
+  const bool dom = D > 0;
+  for (int u0 = 0; u0 < units_total; u0 += chunk) {
+    const int units = std::min(chunk, units_total - u0);
     const int32_t M = rpu * units;
     const int32_t M_pad = (int32_t)rows_pad(M);
+    // per-unit parameters (inputs) or the root's for every row (subdomains)
+    const int32_t prpu = dom ? M_pad : rpu;
+    const int64_t pu0 = dom ? 0 : u0;
     for (int r = 0; r < R; ++r) {
-      bf.al[r].P = bf.P[r] + (int64_t)u0 * bf.al[r].ldp;
+      bf.al[r].P = bf.P[r] + pu0 * bf.al[r].ldp;
       HIP_TRY(c, launch_alpha_init(bf.al[r], o.alpha_init ? o.alpha_init + (int64_t)u0 * rpu * ac.n_total : nullptr,
-                                   ac.n_total, M, M_pad, rpu, s));
+                                   ac.n_total, M, M_pad, prpu, s));
+    }
+    SplitTable tab{}, ftab{};
+    BetaState bs{bf.mul, bf.mul_mom, bf.mul_vel, bf.mul_grad, S};
+    if (dom) {
+      tab = domain_table(g, bf, u0, units, m, S, true);
+      ftab = tab;
+      ftab.grad_beta = S > 0 ? bf.mul_grad : nullptr;
+      if (S > 0) HIP_TRY(c, launch_beta_init(bs, M_pad, s));
     }
     // value rows are read at their padded width: zero once, the padding is never written
     for (size_t k = 0; k < bf.fslots.size(); ++k)
       HIP_TRY(c, launch_fill(bf.fslots[k], (int64_t)M_pad * g->fwd_slot_floats[k], 0.f, s));
     HIP_TRY(c, launch_fill(bf.vtx, (int64_t)M_pad * ld_of(g->n0), 0.f, s));
     for (int32_t t = 0; t <= o.iters; ++t) {
-      vcr_status st = run_pass(c, g, bf, pp, u0, units, m, flops, true);
+      vcr_status st = run_pass(c, g, bf, pp, u0, units, m, flops, true, dom ? &tab : nullptr);
       if (st != VCR_OK) return st;
       HIP_TRY(c, launch_alpha_best(bf.beta, nullptr, 0, M_pad, M, m, t == 0, bf.best_val, bf.flag,
-                                   o.lb_hist ? o.lb_hist + ((int64_t)t * B + u0) * m : nullptr,
-                                   o.ub_hist ? o.ub_hist + ((int64_t)t * B + u0) * m : nullptr, s));
+                                   o.lb_hist ? o.lb_hist + ((int64_t)t * units_total + u0) * m : nullptr,
+                                   o.ub_hist ? o.ub_hist + ((int64_t)t * units_total + u0) * m : nullptr, s));
       const bool step = t < o.iters;
       if (!step)
         for (int r = 0; r < R; ++r) HIP_TRY(c, launch_alpha_keep(bf.al[r], bf.flag, M, s));
       if (!step && !o.grad_out) break;
-      st = run_forward(c, g, bf, u0, units, M, rpu, flops);
+      st = run_forward(c, g, bf, u0, units, M, rpu, flops, dom ? &ftab : nullptr);
       if (st != VCR_OK) return st;
       if (!step) break;
       const double c1 = 1.0 / (1.0 - std::pow((double)o.beta1, (double)(t + 1)));
       const double c2 = 1.0 / (1.0 - std::pow((double)o.beta2, (double)(t + 1)));
       for (int r = 0; r < R; ++r)
-        HIP_TRY(c, launch_alpha_adam(bf.al[r], bf.flag, M, rpu, o.lr, o.beta1, o.beta2, o.adam_eps, (float)c1,
+        HIP_TRY(c, launch_alpha_adam(bf.al[r], bf.flag, M, prpu, o.lr, o.beta1, o.beta2, o.adam_eps, (float)c1,
                                      (float)c2, s));
+      if (dom && S > 0)
+        HIP_TRY(c, launch_beta_adam(bs, M, ac.lr_beta, o.beta1, o.beta2, o.adam_eps, (float)c1, (float)c2, s));
     }
-    HIP_TRY(c, launch_alpha_final(bf.best_val, units, m, nullptr, lb + (int64_t)u0 * m, ub + (int64_t)u0 * m, s));
+    HIP_TRY(c, launch_alpha_final(bf.best_val, units, m, dom ? bf.flags + u0 : nullptr, lb + (int64_t)u0 * m,
+                                  ub + (int64_t)u0 * m, s));
     if (o.alpha_out || o.grad_out)
       for (int r = 0; r < R; ++r)
         HIP_TRY(c, launch_alpha_out(bf.al[r], M, m, ac.n_total,
@@ -1212,42 +1319,106 @@ vcr_status alpha_spec_graph(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &
 
 }  // namespace
 
-// Inputs per chunk and workspace bytes of a CROWN call of B inputs: the whole batch, halved
-// until the plan fits the workspace cap (VCR_ERR_OOM when one input does not).
-vcr_status graph_plan(vcr_ctx *c, int32_t B, int32_t m, int *chunk_out, size_t *bytes_out, bool alpha) {
+namespace {
+
+// The call shape under the workspace cap: inputs (or subdomains) per chunk, halved from the
+// whole batch until the plan fits (VCR_ERR_OOM when one unit does not).  Subdomains share one
+// root input, whose intermediate passes run once.
+vcr_status plan_shape(vcr_ctx *c, GShape sh, GShape *out, size_t *bytes_out) {
   GraphNet *g = c->graph;
-  int chunk = B;
+  const int units = sh.D > 0 ? sh.D : sh.B;
+  sh.ci = sh.D > 0 ? 1 : units;
+  sh.cs = units;
   Workspace probe;
   GBufs tmp;
-  size_t need = carve_graph(c, g, probe, B, m, chunk, &tmp, alpha);
+  size_t need = carve_graph(c, g, probe, sh, &tmp);
   if (c->ws_cap > 0) {
-    while (need > c->ws_cap && chunk > 1) {
-      chunk = (chunk + 1) / 2;
+    while (need > c->ws_cap && sh.cs > 1) {
+      sh.cs = (sh.cs + 1) / 2;
+      if (sh.D == 0) sh.ci = sh.cs;
       Workspace pw;
-      need = carve_graph(c, g, pw, B, m, chunk, &tmp, alpha);
+      need = carve_graph(c, g, pw, sh, &tmp);
     }
     if (need > c->ws_cap)
       return fail(c, VCR_ERR_OOM, "workspace cap %llu bytes is below the minimum plan (%llu bytes)",
                   (unsigned long long)c->ws_cap, (unsigned long long)need);
   }
-  *chunk_out = chunk;
+  *out = sh;
   *bytes_out = need;
   return VCR_OK;
 }
 
+}  // namespace
+
+// Inputs per chunk and workspace bytes of a CROWN call of B inputs
+vcr_status graph_plan(vcr_ctx *c, int32_t B, int32_t m, int *chunk_out, size_t *bytes_out, bool alpha) {
+  GShape sh;
+  sh.B = B;
+  sh.m = m;
+  sh.alpha = alpha;
+  GShape out;
+  const vcr_status st = plan_shape(c, sh, &out, bytes_out);
+  if (st == VCR_OK) *chunk_out = out.cs;
+  return st;
+}
+
 namespace {
 
+// The split table of every subdomain from the root's bounds (in the workspace), written by
+// the split preparation; flags per domain, invalid ones counted in the context's counters.
+vcr_status prepare_splits(vcr_ctx *c, GraphNet *g, GBufs &bf, const vcr_splits *splits) {
+  hipStream_t s = c->stream;
+  const int R = (int)g->relus.size();
+  if (2 * R > PTR_TABLE_MAX) return fail(c, VCR_ERR_UNSUPPORTED, "subdomains need at most %d ReLU nodes", PTR_TABLE_MAX / 2);
+  PtrTable pt{};
+  for (int r = 0; r < R; ++r) {
+    pt.p[r] = bf.L[r];
+    pt.p[R + r] = bf.U[r];
+  }
+  HIP_TRY(c, launch_store_ptrs(pt, 2 * R, bf.Lptr, s));
+  HIP_TRY(c, launch_fill(reinterpret_cast<float *>(c->d_counters), 80, 0.f, s));
+  SplitPrepArgs sp{};
+  sp.relu_id = splits->relu_id;
+  sp.neuron = splits->neuron;
+  sp.sign = splits->sign;
+  sp.D = splits->n_domains;
+  sp.S = splits->per_domain;
+  sp.R = R;
+  sp.relu_n = g->d_relu_info;
+  sp.hwc_C = g->d_relu_info + R;
+  sp.L = bf.Lptr;
+  sp.U = bf.Lptr + R;
+  sp.off = bf.off;
+  sp.ent_n = bf.ent_n;
+  sp.ent_p = bf.ent_p;
+  sp.flags = bf.flags;
+  sp.n_invalid = c->d_counters + 64;
+  sp.lam_rule = c->lambda_rule;
+  HIP_TRY(c, launch_split_prepare(sp, s));
+  return VCR_OK;
+}
+
+// Full CROWN (intermediate passes of every ReLU layer, then the spec pass) on B inputs, or
+// with splits on subdomains of the one input (the root's intermediate bounds, each split
+// neuron's interval clamped), or with ac alpha-CROWN on the spec pass (with splits:
+// beta-CROWN).
 vcr_status graph_run(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m, float *lb,
-                     float *ub, const GraphAlphaCall *ac) {
+                     float *ub, const vcr_splits *splits, const GraphAlphaCall *ac) {
   GraphNet *g = c->graph;
   const int nn = (int)g->nodes.size();
   const GNode &out = g->nodes[nn - 1];
-  int chunk = B;
+  GShape sh;
+  sh.B = B;
+  sh.m = m;
+  sh.alpha = ac != nullptr;
+  sh.D = splits ? splits->n_domains : 0;
+  sh.S = splits ? splits->per_domain : 0;
   size_t need = 0;
-  vcr_status st = graph_plan(c, B, m, &chunk, &need, ac != nullptr);
+  vcr_status st = plan_shape(c, sh, &sh, &need);
   if (st != VCR_OK) return st;
+  const int units_total = sh.D > 0 ? sh.D : B;
   if (c->device < 0) {
-    c->chunks_last = (int)g->passes.size() * ((B + chunk - 1) / chunk);
+    c->chunks_last = ((int)g->passes.size() - 1) * ((B + sh.ci - 1) / sh.ci) + (units_total + sh.cs - 1) / sh.cs;
     return fail(c, VCR_ERR_STATE, "validation-only context: no device work");
   }
   HIP_TRY(c, hipSetDevice(c->device));
@@ -1256,7 +1427,7 @@ vcr_status graph_run(vcr_ctx *c, const float *x0, int32_t B, float eps, const fl
   st = ensure_ws(c, need);
   if (st != VCR_OK) return st;
   GBufs bf;
-  carve_graph(c, g, c->ws, B, m, chunk, &bf, ac != nullptr);
+  carve_graph(c, g, c->ws, sh, &bf);
   hipStream_t s = c->stream;
   const int64_t ld0 = ld_of(g->n0);
   HIP_TRY(c, launch_box(x0, B, (int32_t)g->n0, ld0, eps, c->clip_on, c->clip_lo, c->clip_hi, bf.c0, bf.r0, s));
@@ -1267,9 +1438,26 @@ vcr_status graph_run(vcr_ctx *c, const float *x0, int32_t B, float eps, const fl
   uint64_t flops = 0;
   int chunks = 0;
   for (const PassPlan &pp : g->passes) {
-    if (pp.spec && ac) {
-      st = alpha_spec_graph(c, g, bf, pp, B, m, chunk, *ac, lb, ub, &flops, &chunks);
-      if (st != VCR_OK) return st;
+    if (pp.spec) {
+      if (splits) {
+        st = prepare_splits(c, g, bf, splits);
+        if (st != VCR_OK) return st;
+      }
+      if (ac) {
+        st = alpha_spec_graph(c, g, bf, pp, units_total, m, sh.cs, sh.D, sh.S, *ac, lb, ub, &flops, &chunks);
+        if (st != VCR_OK) return st;
+        continue;
+      }
+      for (int u0 = 0; u0 < units_total; u0 += sh.cs) {
+        const int units = std::min(sh.cs, units_total - u0);
+        SplitTable tab{};
+        if (splits) tab = domain_table(g, bf, u0, units, m, sh.S, false);
+        st = run_pass(c, g, bf, pp, u0, units, m, &flops, false, splits ? &tab : nullptr);
+        if (st != VCR_OK) return st;
+        ++chunks;
+        HIP_TRY(c, launch_finalize_spec(bf.beta, nullptr, 0, 0, units, m, splits ? bf.flags + u0 : nullptr,
+                                        lb + (int64_t)u0 * m, ub + (int64_t)u0 * m, s));
+      }
       continue;
     }
     if (pp.direct) {
@@ -1284,36 +1472,32 @@ vcr_status graph_run(vcr_ctx *c, const float *x0, int32_t B, float eps, const fl
                                          bf.U[ri], bf.P[ri], ldz, c->lambda_rule, s));
       continue;
     }
-    for (int u0 = 0; u0 < B; u0 += chunk) {
-      const int units = std::min(chunk, B - u0);
+    for (int u0 = 0; u0 < B; u0 += sh.ci) {
+      const int units = std::min(sh.ci, B - u0);
       st = run_pass(c, g, bf, pp, u0, units, m, &flops);
       if (st != VCR_OK) return st;
       ++chunks;
-      if (!pp.spec) {
-        const GNode &z = g->nodes[pp.start];
-        const int ri = g->nodes[pp.relu].relu_index;
-        const int64_t ldz = ld_of(z.numel);
-        if (!z.flat) {
-          HIP_TRY(c, launch_finalize_conv(bf.beta, units, z.C, z.H, bf.ic[pp.start] + (int64_t)u0 * ldz,
-                                          bf.ir[pp.start] + (int64_t)u0 * ldz, ldz, c->intersect,
-                                          z.b, bf.L[ri] + (int64_t)u0 * z.numel, bf.U[ri] + (int64_t)u0 * z.numel,
-                                          bf.P[ri] + (int64_t)u0 * z.numel, c->lambda_rule, s));
-        } else {
-          HIP_TRY(c, launch_finalize_layer(bf.beta, nullptr, 0, 0, units, (int32_t)z.numel,
-                                           bf.ic[pp.start] + (int64_t)u0 * ldz, bf.ir[pp.start] + (int64_t)u0 * ldz,
-                                           ldz, c->intersect, z.b, bf.L[ri] + (int64_t)u0 * z.numel,
-                                           bf.U[ri] + (int64_t)u0 * z.numel, bf.P[ri] + (int64_t)u0 * ldz, ldz, c->lambda_rule, s));
-        }
+      const GNode &z = g->nodes[pp.start];
+      const int ri = g->nodes[pp.relu].relu_index;
+      const int64_t ldz = ld_of(z.numel);
+      if (!z.flat) {
+        HIP_TRY(c, launch_finalize_conv(bf.beta, units, z.C, z.H, bf.ic[pp.start] + (int64_t)u0 * ldz,
+                                        bf.ir[pp.start] + (int64_t)u0 * ldz, ldz, c->intersect,
+                                        z.b, bf.L[ri] + (int64_t)u0 * z.numel, bf.U[ri] + (int64_t)u0 * z.numel,
+                                        bf.P[ri] + (int64_t)u0 * z.numel, c->lambda_rule, s));
       } else {
-        HIP_TRY(c, launch_finalize_spec(bf.beta, nullptr, 0, 0, units, m, nullptr, lb + (int64_t)u0 * m,
-                                        ub + (int64_t)u0 * m, s));
+        HIP_TRY(c, launch_finalize_layer(bf.beta, nullptr, 0, 0, units, (int32_t)z.numel,
+                                         bf.ic[pp.start] + (int64_t)u0 * ldz, bf.ir[pp.start] + (int64_t)u0 * ldz,
+                                         ldz, c->intersect, z.b, bf.L[ri] + (int64_t)u0 * z.numel,
+                                         bf.U[ri] + (int64_t)u0 * z.numel, bf.P[ri] + (int64_t)u0 * ldz, ldz,
+                                         c->lambda_rule, s));
       }
     }
   }
   c->last_B = B;
   c->lastL.assign(bf.L.begin(), bf.L.end());
   c->lastU.assign(bf.U.begin(), bf.U.end());
-  c->last_had_splits = false;
+  c->last_had_splits = splits != nullptr;
   c->flops_last = flops;
   c->chunks_last = chunks;
   return VCR_OK;
@@ -1323,8 +1507,7 @@ vcr_status graph_run(vcr_ctx *c, const float *x0, int32_t B, float eps, const fl
 
 vcr_status graph_crown(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m,
                        const vcr_splits *splits, float *lb, float *ub) {
-  if (splits) return fail(c, VCR_ERR_UNSUPPORTED, "subdomain splits are built for MLPs only");
-  return graph_run(c, x0, B, eps, C, m, lb, ub, nullptr);
+  return graph_run(c, x0, B, eps, C, m, lb, ub, splits, nullptr);
 }
 
 vcr_status graph_alpha(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m,
@@ -1334,7 +1517,18 @@ vcr_status graph_alpha(vcr_ctx *c, const float *x0, int32_t B, float eps, const 
   GraphAlphaCall ac;
   ac.o = o;
   ac.n_total = n_total;
-  return graph_run(c, x0, B, eps, C, m, lb, ub, &ac);
+  return graph_run(c, x0, B, eps, C, m, lb, ub, nullptr, &ac);
+}
+
+vcr_status graph_beta(vcr_ctx *c, const float *x0, float eps, const float *C, int32_t m, const vcr_splits *splits,
+                      const vcr_alpha_opts &o, int64_t n_total, float lr_beta, float *lb, float *ub) {
+  if (!c->graph->alpha_why.empty())
+    return fail(c, VCR_ERR_UNSUPPORTED, "beta-CROWN on this network: %s", c->graph->alpha_why.c_str());
+  GraphAlphaCall ac;
+  ac.o = o;
+  ac.n_total = n_total;
+  ac.lr_beta = lr_beta;
+  return graph_run(c, x0, 1, eps, C, m, lb, ub, splits, &ac);
 }
 
 vcr_status graph_ibp(vcr_ctx *c, const float *x0, int32_t B, float eps, const float *C, int32_t m, float *lb,
@@ -1344,14 +1538,17 @@ vcr_status graph_ibp(vcr_ctx *c, const float *x0, int32_t B, float eps, const fl
   const GNode &out = g->nodes[nn - 1];
   Workspace probe;
   GBufs tmp;
-  const size_t need = carve_graph(c, g, probe, B, m, 1, &tmp);
+  GShape sh;
+  sh.B = B;
+  sh.m = m;
+  const size_t need = carve_graph(c, g, probe, sh, &tmp);
   HIP_TRY(c, hipSetDevice(c->device));
   c->lastL.clear();
   c->lastU.clear();
   vcr_status st = ensure_ws(c, need);
   if (st != VCR_OK) return st;
   GBufs bf;
-  carve_graph(c, g, c->ws, B, m, 1, &bf);
+  carve_graph(c, g, c->ws, sh, &bf);
   hipStream_t s = c->stream;
   HIP_TRY(c, launch_box(x0, B, (int32_t)g->n0, ld_of(g->n0), eps, c->clip_on, c->clip_lo, c->clip_hi, bf.c0, bf.r0, s));
   st = run_ibp(c, g, bf, B);
@@ -1364,10 +1561,18 @@ vcr_status graph_ibp(vcr_ctx *c, const float *x0, int32_t B, float eps, const fl
   return VCR_OK;
 }
 
-size_t graph_workspace_bytes(vcr_ctx *c, int32_t B, int32_t m, bool alpha) {
+size_t graph_workspace_bytes(vcr_ctx *c, int32_t B, int32_t m, int32_t D, int32_t S, bool alpha) {
   Workspace probe;
   GBufs tmp;
-  return carve_graph(c, c->graph, probe, B, m, B, &tmp, alpha && c->graph->alpha_why.empty());
+  GShape sh;
+  sh.B = D > 0 ? 1 : B;
+  sh.m = m;
+  sh.D = D;
+  sh.S = S;
+  sh.ci = D > 0 ? 1 : B;
+  sh.cs = D > 0 ? D : B;
+  sh.alpha = alpha && c->graph->alpha_why.empty();
+  return carve_graph(c, c->graph, probe, sh, &tmp);
 }
 
 }  // namespace vcr

@@ -145,6 +145,10 @@ struct SplitPrepArgs {
   int32_t *flags;            // [D] 0 ok, 1 infeasible, 2 invalid
   int32_t *n_invalid;        // one counter
   int32_t lam_rule;          // lower-slope rule of unstable neurons (relax.h)
+  // optional [R] (device): channels of a ReLU on a convolution output, 0 for flat ones.  The
+  // split neurons come in (C, H, W) order (as L and U are laid out); ent_n then holds their
+  // channels-last index, the one the convolution epilogues look up
+  const int32_t *hwc_C;
 };
 hipError_t launch_split_prepare(const SplitPrepArgs &a, hipStream_t s);
 hipError_t launch_count_unstable(const float *L, const float *U, int64_t n, int32_t *count, hipStream_t s);

@@ -72,7 +72,8 @@ def test_conv_networks_are_reported_unsupported(vc):
 def test_alpha_on_conv_networks_is_planned(vc):
     """Residual and plain convolutional nets load in a validation-only context, and
     alpha-CROWN on them gets past planning (the slope layout and the gradient pass) to the
-    device stage, VCR_ERR_STATE; bad options are still VCR_ERR_ARG."""
+    device stage, VCR_ERR_STATE; bad options are still VCR_ERR_ARG.  So do CROWN and
+    beta-CROWN on subdomains and the branch-and-bound loop."""
     from tests.test_conv_gpu import conv_chain, small_resnet
     for wl in (small_resnet(1), conv_chain(2)):
         ctx = vc.Ctx(-1)
@@ -89,6 +90,23 @@ def test_alpha_on_conv_networks_is_planned(vc):
             st = lib.vcr_alpha_crown_bounds(ctx.h, p(x), B, ctypes.c_float(0.01), p(C), m, ctypes.byref(o), p(lb),
                                             p(ub))
             assert st == want, (wl.name, lr, lib.vcr_last_error(ctx.h))
+        # subdomains of one input: CROWN, beta-CROWN and the loop are planned as well
+        D = 8
+        rid, neu, sg = _buf(D * 2, np.int32), _buf(D * 2, np.int32), _buf(D * 2, np.int8)
+        sp = vc.VcrSplits(D, 2, rid.ctypes.data, neu.ctypes.data, sg.ctypes.data)
+        dl, du = _buf(D * m), _buf(D * m)
+        st = lib.vcr_crown_bounds(ctx.h, p(x), 1, ctypes.c_float(0.01), p(C), m, ctypes.byref(sp), p(dl), p(du))
+        assert st == vc.VCR_ERR_STATE, (wl.name, lib.vcr_last_error(ctx.h))
+        bo = vc.VcrBetaOpts(3, 0.1, 0.05, 0.9, 0.999, 1e-8, None, None)
+        st = lib.vcr_beta_crown_bounds(ctx.h, p(x), ctypes.c_float(0.01), p(C), m, ctypes.byref(sp), ctypes.byref(bo),
+                                       p(dl), p(du))
+        assert st == vc.VCR_ERR_STATE, (wl.name, lib.vcr_last_error(ctx.h))
+        res = vc.VcrBabResult()
+        ob = vc.VcrBabOpts(4, 3, bo, None, None, 0)
+        st = lib.vcr_bab_verify(ctx.h, p(x), ctypes.c_float(0.01), p(C), m, ctypes.byref(ob), ctypes.byref(res), None)
+        assert st == vc.VCR_ERR_STATE, (wl.name, lib.vcr_last_error(ctx.h))
+        wsb = ctypes.c_uint64(0)
+        assert lib.vcr_workspace_bytes(ctx.h, 1, m, D, ctypes.byref(wsb)) == vc.VCR_OK and wsb.value > 0
 
 
 def oracle_shapes(net):
