@@ -215,7 +215,26 @@ void fixed_cases() {
   EXPECT(r.load(c) == VCR_OK);
   EXPECT(vcr_workspace_bytes(c, 2, 9, 0, &bytes) == VCR_OK && bytes > 0);
   EXPECT(crown(c, 2, 9, 3 * 64, 10, 0.01f, nullptr) == VCR_ERR_STATE);
-  EXPECT(crown(c, 1, 9, 3 * 64, 10, 0.01f, &sp) == VCR_ERR_UNSUPPORTED);
+  // subdomains of one input (CROWN, beta-CROWN) and the loop: planned, then no device work
+  EXPECT(crown(c, 1, 9, 3 * 64, 10, 0.01f, &sp) == VCR_ERR_STATE);
+  EXPECT(vcr_workspace_bytes(c, 1, 9, sp.n_domains, &bytes) == VCR_OK && bytes > 0);
+  {
+    Buf x(3 * 64), C(9 * 10), lb(9 * sp.n_domains), ub(9 * sp.n_domains);
+    vcr_beta_opts bo{};
+    bo.iters = 3;
+    bo.lr_alpha = 0.1f;
+    bo.lr_beta = 0.05f;
+    bo.beta1 = 0.9f;
+    bo.beta2 = 0.999f;
+    bo.adam_eps = 1e-8f;
+    EXPECT(vcr_beta_crown_bounds(c, x.p(), 0.02f, C.p(), 9, &sp, &bo, lb.p(), ub.p()) == VCR_ERR_STATE);
+    vcr_bab_opts bb{};
+    bb.batch = 4;
+    bb.max_rounds = 3;
+    bb.bound = bo;
+    vcr_bab_result res;
+    EXPECT(vcr_bab_verify(c, x.p(), 0.02f, C.p(), 9, &bb, &res, nullptr) == VCR_ERR_STATE);
+  }
   Net bad = resnet(8, 32, 64);
   bad.nodes[4].in1 = 5;   // not an earlier node
   EXPECT(bad.load(c) == VCR_ERR_ARG);
