@@ -233,14 +233,16 @@ def bench_bab_loop(args):
     from paper_2606_09377_amd import Ctx
     from paper_2606_09377_amd.vcrown import OPT_TIME_GEMM
     from workloads import make_workload
-    if not args.workload.startswith("bab_"):
-        print("--bab-loop runs on a bab_ workload (its root input and property)", file=sys.stderr)
+    conv = args.workload.startswith("resnet")
+    if not (args.workload.startswith("bab_") or conv):
+        print("--bab-loop runs on a bab_ workload (its root input and property) or on a ResNet's first input",
+              file=sys.stderr)
         sys.exit(2)
     wl = make_workload(args.workload)
     ctx = Ctx(0)
     ctx.load_net(wl.net)
-    x0 = torch.from_numpy(wl.x0).cuda()
-    C = torch.from_numpy(wl.C).cuda()
+    x0 = torch.from_numpy(wl.x0[:1]).cuda()
+    C = torch.from_numpy(wl.C[:1]).cuda()
 
     def step():
         return ctx.bab_verify(x0, wl.eps, C, batch=args.bab_loop, max_rounds=BAB_ROUNDS, iters=BAB_ITERS)
@@ -258,9 +260,10 @@ def bench_bab_loop(args):
     res = results[-1]
     assert all(r == res for r in results), "the loop is deterministic"
     domains = res["evaluated"] * args.steps
-    launches = st["timed_gemm_launches"] + st["timed_small_launches"] + st["timed_mid_launches"]
-    gms = st["timed_gemm_ms"] + st["timed_small_ms"] + st["timed_mid_ms"]
-    gfl = st["timed_gemm_flops"] + st["timed_small_flops"] + st["timed_mid_flops"]
+    kinds = ("conv",) if conv else ("gemm", "small", "mid")
+    launches = sum(st[f"timed_{k}_launches"] for k in kinds)
+    gms = sum(st[f"timed_{k}_ms"] for k in kinds)
+    gfl = sum(st[f"timed_{k}_flops"] for k in kinds)
     achieved = gfl / (gms / 1e3) / 1e12 if gms > 0 else None
     rec = {
         "metric": "CROWN bound evals/sec (inputs or BaB domains) at 1 GPU; % fp32 MFMA peak",
@@ -272,18 +275,22 @@ def bench_bab_loop(args):
         "config": {"workload": args.workload, "mode": "branch-and-bound loop", "batch": args.bab_loop,
                    "rounds": BAB_ROUNDS, "eps": float(wl.eps), "spec_rows": int(wl.C.shape[1]),
                    "method": f"alpha-CROWN root, beta-CROWN subdomains ({BAB_ITERS} joint Adam steps)"},
-        "roofline": {"bound": "mfma", "kernel": "k_gemm and k_gemm_small (dense A.W steps, fp32 MFMA)",
+        "roofline": {"bound": "mfma",
+                     "kernel": KERNEL_DESC["k_convt"] if conv else "k_gemm and k_gemm_small (dense A.W steps, fp32 MFMA)",
                      "achieved": achieved,
                      "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_FP32_MFMA_TFLOPS if achieved else None,
-                     "traffic": traffic_for("k_gemm", args.workload), "launches_timed": launches,
+                     "traffic": None if conv else traffic_for("k_gemm", args.workload), "launches_timed": launches,
                      "avg_launch_ms": gms / launches if launches else None,
                      "flops_per_launch": gfl / launches if launches else None,
                      "share_of_step": gms / 1e3 / dt if launches else None},
         "bab": {k: res[k] for k in ("verified", "rounds", "evaluated", "remaining", "root_min_lb", "worst_lb", "log")},
     }
-    if args.cpu_budget > 0:
+    if args.cpu_budget > 0 and not conv:
         rec["cpu_baseline"] = cpu_baseline_bab_loop(wl, args.bab_loop, args.cpu_budget)
+    elif conv:
+        rec["cpu_baseline"] = None
+        rec["cpu_baseline_note"] = "the oracle's root pass alone exceeds the CPU budget on this ResNet"
     print(json.dumps(rec), flush=True)
 
 
@@ -298,7 +305,8 @@ def main():
                     help="alpha-CROWN with this many Adam steps on the final pass (0: CROWN)")
     ap.add_argument("--bab-loop", type=int, default=0, metavar="BATCH",
                     help="run the fixed-batch branch-and-bound loop (10 rounds, beta-CROWN bounds) with this batch "
-                         "on the bab_ workload's root input; value = subdomains bounded per second")
+                         "on the bab_ workload's root input or a ResNet's first input; value = subdomains bounded "
+                         "per second")
     ap.add_argument("--graph", action="store_true",
                     help="replay the call as a recorded HIP graph (the roofline then comes from a "
                          "second timed pass without the graph)")
