@@ -48,7 +48,8 @@ struct ConvTArgs {
   float *out;                // [R][S_in][S_in][C_in]
   float *part;               // [N_pad / 64][M_pad]
   // alpha-CROWN (dense windows with a ReLU only): per-row lower slopes at unstable neurons,
-  // and the coefficients before relaxation, both laid out like out
+  // and the coefficients before relaxation (recorded at unstable neurons only), both laid
+  // out like out
   const float *alpha;
   float *pre;
   // branch-and-bound subdomains of one input (dense windows with a ReLU; every row belongs
@@ -120,8 +121,9 @@ struct FwdConvArgs {
   int64_t res_rs;
   const float4 *P;         // optional ReLU parameters [units][Ho][Ho][Co]
   int32_t rows_per_unit, units;
-  const float *alpha, *pre;  // [rows][out_rs] with P
-  float *grad;               // [rows][out_rs] with P
+  const float *alpha, *pre;  // [rows][out_rs] with P, read at unstable neurons only
+  float *grad;               // [rows][out_rs] with P, written at unstable neurons only (the
+                             // slope state starts at 0 and stable neurons keep it)
   float *out;              // [rows][out_rs], (Ho, Ho, Co)
   int64_t out_rs;
   // with P, subdomains of one input (units = 1): the split table of this ReLU (relu_index);

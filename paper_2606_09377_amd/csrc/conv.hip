@@ -171,9 +171,13 @@ __device__ __forceinline__ void convt_epilogue(const ConvTArgs &p, const ConvCla
               if (store) q = split_override(p.splits, s_rr[lr + t], p.relu_index, pb + ncol[j], q, &ent, &sterm);
             }
             float lam = q.x;
-            if constexpr (AL) {   // alpha-CROWN: the row's own slope at unstable neurons
-              const float al = store ? alp[ob + ncol[j]] : 0.f;
-              lam = q.z > 0.f ? al : lam;
+            if constexpr (AL) {   // alpha-CROWN: the row's own slope at unstable neurons, whose
+                                  // coefficients before relaxation are recorded (the gradient
+                                  // pass reads them there only)
+              if (store && q.z > 0.f) {
+                lam = alp[ob + ncol[j]];
+                prep[ob + ncol[j]] = a;
+              }
             }
             ap = a > 0.f ? a * lam : a * q.y;
             if constexpr (SPL) {   // beta-CROWN: the split's multiplier term
@@ -185,10 +189,7 @@ __device__ __forceinline__ void convt_epilogue(const ConvTArgs &p, const ConvCla
             x += a * bn[j];
           }
         }
-        if (store) {
-          outp[ob + ncol[j]] = ap;
-          if constexpr (AL) prep[ob + ncol[j]] = a;
-        }
+        if (store) outp[ob + ncol[j]] = ap;
       }
       rp[g * 4 + t] = x;
     }
@@ -1190,11 +1191,14 @@ __device__ __forceinline__ void fwd_apply(const FwdConvArgs &p, int64_t r, int64
       prm = split_override(p.splits, (int)r, p.relu_index, (int)(pb + n), prm, &ent, &sterm);
       if (ent >= 0 && p.splits.grad_beta) p.splits.grad_beta[r * p.splits.S + ent] = sterm * D;
     }
-    const bool unst = prm.z > 0.f;
-    const float lam = unst ? p.alpha[off] : prm.x;
-    const float an = p.pre[off];
-    p.out[off] = an > 0.f ? lam * D : prm.y * D + (an < 0.f ? prm.z : 0.f);
-    p.grad[off] = (unst && an > 0.f) ? an * D : 0.f;
+    if (prm.z > 0.f) {   // unstable: the line the recorded coefficient chose, and the gradient
+      const float an = p.pre[off];
+      p.out[off] = an > 0.f ? p.alpha[off] * D : prm.y * D + (an < 0.f ? prm.z : 0.f);
+      p.grad[off] = an > 0.f ? an * D : 0.f;
+    } else {   // stable (lam = s in {0, 1}, t = 0): every line is s D, and the gradient stays the
+               // 0 the slope state starts with, so neither the slope nor the coefficient is read
+      p.out[off] = prm.y * D;
+    }
   } else {
     p.out[off] = D;
   }
@@ -1251,9 +1255,22 @@ __global__ __launch_bounds__(256, 2) void k_fwd_conv(const FwdConvArgs p, FastDi
     b_row[q] = co < p.Co ? p.Wk + (int64_t)co * 9 * p.Ci + lcol : nullptr;
   }
   const int cpt = p.Ci / BK;   // K tiles per tap
+  // K order: pairs of 16-channel blocks (one 128-byte line of a position) outer, then the
+  // tap, then the block of the pair, so a tile's shifted re-reads of a line follow each
+  // other within a few K tiles (as in the transposed convolution)
+  const bool pairs = cpt % 2 == 0;
   f32x4 ra[QA], rb[QB];
   auto gload = [&](int kt) {
-    const int t = kt / cpt, c0 = (kt - t * cpt) * BK;
+    int t, cb;
+    if (pairs) {
+      const int grp = kt / 18, rem = kt - grp * 18;
+      t = rem >> 1;
+      cb = 2 * grp + (rem & 1);
+    } else {
+      cb = kt / 9;
+      t = kt - cb * 9;
+    }
+    const int c0 = cb * BK;
     const int ky = t / 3, kx = t - ky * 3;
 #pragma unroll
     for (int q = 0; q < QA; ++q) {

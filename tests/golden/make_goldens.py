@@ -44,6 +44,11 @@ ALPHA = {
     "resnet3x8x8": ([0], 5),
 }
 
+# beta-CROWN runs on subdomains of input 0: {workload: (domains, splits per domain, Adam steps)}
+BETA = {
+    "resnet3x8x8": (6, 3, 5),
+}
+
 # A-guided box vertices: {workload: inputs}
 CORNERS = {
     "mlp3072x8192x4": [0, 15],
@@ -145,6 +150,38 @@ def make_alpha(name, inputs, iters):
     print("wrote", path)
 
 
+def make_beta(name, n_dom, depth, iters):
+    """Subdomains of input 0 whose splits mix the ReLU layers (every split on a neuron the
+    root finds unstable, one per chosen layer, random signs), each run through the beta-CROWN
+    oracle: every evaluation's bounds."""
+    from oracle import beta64
+    wl = make_workload(name)
+    t = time.time()
+    root = oracle.crown(wl.net, wl.x0[0], wl.eps, wl.C[0])
+    print(f"{name} root: {time.time() - t:.1f} s", flush=True)
+    rng = np.random.default_rng(2026)
+    ids = beta64.relu_ids(wl.net)
+    unst = [np.flatnonzero((root.layer_l[i] < 0) & (root.layer_u[i] > 0)) for i in ids]
+    layers = [r for r in range(len(ids)) if unst[r].size]
+    rid = np.zeros((n_dom, depth), np.int32)
+    neu = np.zeros((n_dom, depth), np.int32)
+    sgn = np.zeros((n_dom, depth), np.int8)
+    out = {"iters": np.array(iters)}
+    for d in range(n_dom):
+        chosen = rng.choice(layers, size=depth, replace=False)
+        dom = [(int(r), int(rng.choice(unst[r])), int(rng.choice([-1, 1]))) for r in chosen]
+        rid[d], neu[d], sgn[d] = [x[0] for x in dom], [x[1] for x in dom], [x[2] for x in dom]
+        t = time.time()
+        r = beta64.beta_crown(wl.net, root, wl.C[0], dom, iters=iters)
+        out[f"feasible_{d}"] = np.array(r.feasible)
+        out[f"lb_hist_{d}"], out[f"ub_hist_{d}"] = r.lb_hist, r.ub_hist
+        print(f"{name} domain {d} {dom}: {time.time() - t:.1f} s", flush=True)
+    out["relu_id"], out["neuron"], out["sign"] = rid, neu, sgn
+    path = os.path.join(HERE, f"{name}_beta.npz")
+    np.savez_compressed(path, **out)
+    print("wrote", path)
+
+
 def make_corners(name, inputs):
     wl = make_workload(name)
     out = {"inputs": np.array(inputs)}
@@ -173,9 +210,12 @@ def make_bab_splits():
 
 if __name__ == "__main__":
     names = sys.argv[1:] or (list(GOLDENS) + ["bab"] + [f"{k}_sampled" for k in SAMPLED] + list(ONE_HIDDEN)
-                             + [f"{k}_alpha" for k in ALPHA] + [f"{k}_corners" for k in CORNERS])
+                             + [f"{k}_alpha" for k in ALPHA] + [f"{k}_corners" for k in CORNERS]
+                             + [f"{k}_beta" for k in BETA])
     for n in names:
-        if n.endswith("_alpha"):
+        if n.endswith("_beta"):
+            make_beta(n[:-len("_beta")], *BETA[n[:-len("_beta")]])
+        elif n.endswith("_alpha"):
             make_alpha(n[:-len("_alpha")], *ALPHA[n[:-len("_alpha")]])
         elif n.endswith("_corners"):
             make_corners(n[:-len("_corners")], CORNERS[n[:-len("_corners")]])

@@ -135,3 +135,40 @@ def test_conv_bab_loop_matches_oracle(which, eps, batch, rounds):
     assert got["verified"] == ref.verified
     assert got["rounds"] == ref.rounds and got["log"] == [tuple(x) for x in ref.log]
     assert got["evaluated"] == ref.evaluated and got["remaining"] == ref.remaining
+
+
+def test_beta_resnet3x8x8_full_width():
+    """The 3x8x8 ResNet at full width (64 and 128 channels, FC 512, 99 spec rows): six
+    subdomains of input 0 with splits across the convolutional and dense ReLU layers, five
+    joint Adam steps, against the stored oracle run evaluation by evaluation; the same six
+    domains inside a batch of 64 (the others their sign variants) give the same bits."""
+    import os
+    import torch
+    g = np.load(os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "resnet3x8x8_beta.npz"))
+    from workloads import make_workload
+    wl = make_workload("resnet3x8x8", batch=1)
+    T = int(g["iters"])
+    rid, neu, sgn = g["relu_id"], g["neuron"], g["sign"]
+    D0 = rid.shape[0]
+    ctx = gpu_ctx(wl.net)
+    sp = tuple(torch.from_numpy(np.ascontiguousarray(a)).cuda() for a in (rid, neu, sgn))
+    lb, ub, ex = ctx.beta_crown_bounds(to_dev(wl.x0), wl.eps, to_dev(wl.C), sp, iters=T, want_hist=True)
+    torch.cuda.synchronize()
+    lh, uh = ex["lb_hist"].cpu().numpy(), ex["ub_hist"].cpu().numpy()
+    for d in range(D0):
+        if not bool(g[f"feasible_{d}"]):
+            assert np.all(np.isposinf(lb[d].cpu().numpy()))
+            continue
+        for t in range(T + 1):
+            assert_close(lh[t, d], g[f"lb_hist_{d}"][t], f"domain {d} evaluation {t} lb")
+            assert_close(uh[t, d], g[f"ub_hist_{d}"][t], f"domain {d} evaluation {t} ub")
+    rng = np.random.default_rng(3)
+    reps = rng.integers(0, D0, 64 - D0)
+    big = [np.concatenate([a, a[reps]]) for a in (rid, neu, sgn)]
+    big[2][D0:] = np.where(rng.random(big[2][D0:].shape) < 0.5, -1, 1).astype(np.int8)
+    spb = tuple(torch.from_numpy(np.ascontiguousarray(a)).cuda() for a in big)
+    lb2, ub2, _ = ctx.beta_crown_bounds(to_dev(wl.x0), wl.eps, to_dev(wl.C), spb, iters=T)
+    torch.cuda.synchronize()
+    assert np.array_equal(lb2.cpu().numpy()[:D0], lb.cpu().numpy())
+    assert np.array_equal(ub2.cpu().numpy()[:D0], ub.cpu().numpy())
+    log("64-domain batch: lb range", float(lb2.min()), float(lb2[torch.isfinite(lb2)].max()))
