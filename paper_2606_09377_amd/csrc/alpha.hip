@@ -33,6 +33,7 @@ __global__ void k_alpha_init(AlphaLayer l, const float *alpha_init, int64_t n_to
   l.mom[idx] = 0.f;
   l.vel[idx] = 0.f;
   l.grad[idx] = 0.f;
+  l.pre[idx] = 0.f;   // coefficients a pass does not record (stable neurons) read as 0
 }
 
 hipError_t launch_alpha_init(const AlphaLayer &l, const float *alpha_init, int64_t n_total, int32_t rows,

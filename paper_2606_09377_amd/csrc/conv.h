@@ -121,9 +121,8 @@ struct FwdConvArgs {
   int64_t res_rs;
   const float4 *P;         // optional ReLU parameters [units][Ho][Ho][Co]
   int32_t rows_per_unit, units;
-  const float *alpha, *pre;  // [rows][out_rs] with P, read at unstable neurons only
-  float *grad;               // [rows][out_rs] with P, written at unstable neurons only (the
-                             // slope state starts at 0 and stable neurons keep it)
+  const float *alpha, *pre;  // [rows][out_rs] with P
+  float *grad;               // [rows][out_rs] with P
   float *out;              // [rows][out_rs], (Ho, Ho, Co)
   int64_t out_rs;
   // with P, subdomains of one input (units = 1): the split table of this ReLU (relu_index);

@@ -1191,14 +1191,13 @@ __device__ __forceinline__ void fwd_apply(const FwdConvArgs &p, int64_t r, int64
       prm = split_override(p.splits, (int)r, p.relu_index, (int)(pb + n), prm, &ent, &sterm);
       if (ent >= 0 && p.splits.grad_beta) p.splits.grad_beta[r * p.splits.S + ent] = sterm * D;
     }
-    if (prm.z > 0.f) {   // unstable: the line the recorded coefficient chose, and the gradient
-      const float an = p.pre[off];
-      p.out[off] = an > 0.f ? p.alpha[off] * D : prm.y * D + (an < 0.f ? prm.z : 0.f);
-      p.grad[off] = an > 0.f ? an * D : 0.f;
-    } else {   // stable (lam = s in {0, 1}, t = 0): every line is s D, and the gradient stays the
-               // 0 the slope state starts with, so neither the slope nor the coefficient is read
-      p.out[off] = prm.y * D;
-    }
+    // every load issued without waiting on the parameters (a stable neuron's lines all give
+    // s D whatever its recorded coefficient, which the spec pass leaves at 0 there)
+    const float al = p.alpha[off], an = p.pre[off];
+    const bool unst = prm.z > 0.f;
+    const float lam = unst ? al : prm.x;
+    p.out[off] = an > 0.f ? lam * D : prm.y * D + (an < 0.f ? prm.z : 0.f);
+    p.grad[off] = (unst && an > 0.f) ? an * D : 0.f;
   } else {
     p.out[off] = D;
   }

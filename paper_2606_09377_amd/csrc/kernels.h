@@ -174,7 +174,7 @@ struct AlphaLayer {
   // (y W + x) C + c here and c H W + y W + x in the compact layout; 0 for flat neurons
   int32_t hwc_C, hwc_HW;
 };
-// alpha <- alpha_init (compact [units][2m][n_total]) or lam (P.x); mom = vel = 0
+// alpha <- alpha_init (compact [units][2m][n_total]) or lam (P.x); mom = vel = grad = pre = 0
 hipError_t launch_alpha_init(const AlphaLayer &l, const float *alpha_init, int64_t n_total, int32_t rows,
                              int32_t rows_pad, int32_t rows_per_unit, hipStream_t s);
 // E0 = c - sign(pre0) r per row (the box vertex that attains the row's bound)
