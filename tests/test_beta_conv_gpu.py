@@ -172,3 +172,67 @@ def test_beta_resnet3x8x8_full_width():
     assert np.array_equal(lb2.cpu().numpy()[:D0], lb.cpu().numpy())
     assert np.array_equal(ub2.cpu().numpy()[:D0], ub.cpu().numpy())
     log("64-domain batch: lb range", float(lb2.min()), float(lb2[torch.isfinite(lb2)].max()))
+
+
+def test_conv_subdomain_edge_cases():
+    """Splits on convolutional ReLUs (neurons in (C, H, W) order): splits that restate a
+    stable neuron's state are bitwise no-ops, a contradicting split is infeasible, a neuron
+    out of range or repeated makes the domain invalid (NaN, counted), and a domain that agrees
+    with x0's own activation pattern contains f(x0)."""
+    from tests.pins import batch_forward, spec_values
+    from workloads import Splits
+    wl = _nets()[0]
+    net = wl.net
+    root = _root(wl)
+    ids = beta64.relu_ids(net)
+    l0, u0 = root.layer_l[ids[0]], root.layer_u[ids[0]]
+    act = np.flatnonzero(l0 > 1e-3)
+    ina = int(np.flatnonzero(u0 < -1e-3)[0])
+    l1, u1 = root.layer_l[ids[1]], root.layer_u[ids[1]]
+    unst = np.flatnonzero((l1 < -1e-3) & (u1 > 1e-3))
+    z = batch_forward(net, wl.x0[:1].astype(np.float64))
+    zin = z[net.nodes[ids[1]].in0].reshape(-1)
+    zsign = [1 if zin[j] >= 0 else -1 for j in unst[:3]]
+    n0 = l0.size
+    rid = np.array([[0, 0, 0], [0, 1, 1], [0, 1, 1], [1, 1, 1], [1, 1, 0]], np.int32)
+    neu = np.array([[act[0], ina, act[1]], [ina, unst[0], unst[1]], [act[0], n0 * 4, unst[0]],
+                    list(unst[:3]), [unst[0], unst[0], act[0]]], np.int32)
+    sgn = np.array([[1, -1, 1], [1, 1, -1], [1, 1, 1], zsign, [1, -1, 1]], np.int8)
+    ctx = gpu_ctx(net)
+    lb, ub, _ = gpu_crown(ctx, wl, splits=Splits(rid, neu, sgn))
+    assert ctx.stats()["invalid_domains"] == 2
+    lbr, ubr, _ = gpu_crown(ctx, wl)
+    assert np.array_equal(lb[0], lbr[0]) and np.array_equal(ub[0], ubr[0]), "stable splits must be no-ops"
+    assert np.all(lb[1] == np.inf) and np.all(ub[1] == -np.inf)
+    for d in (2, 4):
+        assert np.all(np.isnan(lb[d])) and np.all(np.isnan(ub[d])), d
+    y0 = spec_values(net, wl.C[0], wl.x0[:1].astype(np.float64))[0]
+    assert np.all(lb[3] <= y0 + 1e-4) and np.all(ub[3] >= y0 - 1e-4)
+    LB, UB = oracle.crown_domains(net, root, wl.C[0], Splits(rid[[3]], neu[[3]], sgn[[3]]))
+    assert_close(lb[3], LB[0], "domain 3 lb")
+    assert_close(ub[3], UB[0], "domain 3 ub")
+
+
+def test_conv_beta_chunked_equals_whole():
+    """beta-CROWN on 24 subdomains of a residual conv net: a workspace cap that splits the
+    domains into chunks gives the same bits."""
+    import torch
+    from paper_2606_09377_amd.vcrown import OPT_WORKSPACE_CAP_BYTES
+    wl = _nets()[0]
+    root = _root(wl)
+    order = beta64.default_order(wl.net, root)
+    rng = np.random.default_rng(12)
+    doms = []
+    for _ in range(24):
+        pick = rng.choice(len(order), size=3, replace=False)
+        doms.append([(order[p][0], order[p][1], int(rng.choice([-1, 1]))) for p in pick])
+    sp = _split_tensors(doms, 3)
+    ctx = gpu_ctx(wl.net)
+    lb, ub, _ = ctx.beta_crown_bounds(to_dev(wl.x0), wl.eps, to_dev(wl.C), sp, iters=3)
+    torch.cuda.synchronize()
+    st0 = ctx.stats()
+    ctx.set_option(OPT_WORKSPACE_CAP_BYTES, st0["peak_workspace_bytes"] - 1)
+    lb2, ub2, _ = ctx.beta_crown_bounds(to_dev(wl.x0), wl.eps, to_dev(wl.C), sp, iters=3)
+    torch.cuda.synchronize()
+    assert ctx.stats()["n_chunks_last_call"] > st0["n_chunks_last_call"]
+    assert np.array_equal(lb.cpu().numpy(), lb2.cpu().numpy()) and np.array_equal(ub.cpu().numpy(), ub2.cpu().numpy())
