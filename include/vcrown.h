@@ -283,9 +283,9 @@ vcr_status vcr_beta_crown_bounds(vcr_ctx *ctx, const float *x0, float eps, const
  * neuron of the priority order that it has not split yet into an active and an inactive
  * child, bounds the children with beta-CROWN and keeps those with a non-positive lower bound
  * (infeasible children are dropped).  Verified when no subdomain is left; otherwise unknown
- * after max_rounds, or when a subdomain has no neuron left to split.  On convolutional
- * networks the root's intermediate passes run again in every round (on dense/relu chains the
- * first round's are reused). */
+ * after max_rounds, or when a subdomain has no neuron left to split.  The root's
+ * intermediate bounds and relaxation are computed in the first round and reused in the later
+ * ones. */
 typedef struct {
   int32_t batch;            /* subdomains split per round (>= 1) */
   int32_t max_rounds;       /* in [0, VCR_MAX_SPLITS]: a subdomain gains one split per round

@@ -1430,14 +1430,61 @@ vcr_status graph_run(vcr_ctx *c, const float *x0, int32_t B, float eps, const fl
   carve_graph(c, g, c->ws, sh, &bf);
   hipStream_t s = c->stream;
   const int64_t ld0 = ld_of(g->n0);
-  HIP_TRY(c, launch_box(x0, B, (int32_t)g->n0, ld0, eps, c->clip_on, c->clip_lo, c->clip_hi, bf.c0, bf.r0, s));
-  st = run_ibp(c, g, bf, B);
-  if (st != VCR_OK) return st;
+  // the rounds of a branch-and-bound loop bound subdomains of one root: its box, bounds and
+  // relaxation (all the subdomain pass reads of it) are computed in the first round and
+  // copied back in the later ones
+  const bool use_cache = splits && c->bab_reuse && c->root_cached;
+  const bool fill_cache = splits && c->bab_reuse && !c->root_cached;
+  auto cache_copy = [&](bool to_cache) -> vcr_status {
+    size_t o = 0;
+    auto move = [&](float *ws_buf, size_t n) -> vcr_status {
+      float *cb = c->root_cache + o;
+      HIP_TRY(c, launch_copy(to_cache ? cb : ws_buf, to_cache ? ws_buf : cb, (int64_t)n, s));
+      o += n;
+      return VCR_OK;
+    };
+    vcr_status e = move(bf.c0, ld0);
+    if (e == VCR_OK) e = move(bf.r0, ld0);
+    for (size_t r = 0; r < g->relus.size() && e == VCR_OK; ++r) {
+      const GNode &n = g->nodes[g->relus[r]];
+      e = move(bf.L[r], n.numel);
+      if (e == VCR_OK) e = move(bf.U[r], n.numel);
+      if (e == VCR_OK) e = move(reinterpret_cast<float *>(bf.P[r]), 4 * (n.flat ? ld_of(n.numel) : n.numel));
+    }
+    return e;
+  };
+  size_t cache_floats = 2 * ld0;
+  for (int r : g->relus) {
+    const GNode &n = g->nodes[r];
+    cache_floats += 2 * n.numel + 4 * (n.flat ? ld_of(n.numel) : n.numel);
+  }
+  if (use_cache) {
+    st = cache_copy(false);
+    if (st != VCR_OK) return st;
+  } else {
+    HIP_TRY(c, launch_box(x0, B, (int32_t)g->n0, ld0, eps, c->clip_on, c->clip_lo, c->clip_hi, bf.c0, bf.r0, s));
+    st = run_ibp(c, g, bf, B);
+    if (st != VCR_OK) return st;
+  }
   HIP_TRY(c, launch_spec_cw(C, B, m, (int32_t)out.numel, out.hwc_in ? out.Wh : out.Wp, out.ld_in, out.b,
                             (int32_t)g->nodes[out.in0].numel, bf.CW, out.ld_in, bf.Cb, s));
   uint64_t flops = 0;
   int chunks = 0;
   for (const PassPlan &pp : g->passes) {
+    if (use_cache && !pp.spec) continue;
+    if (pp.spec && fill_cache) {
+      if (c->root_cache_cap < cache_floats) {
+        HIP_TRY(c, hipStreamSynchronize(s));
+        if (c->root_cache) HIP_TRY(c, hipFree(c->root_cache));
+        c->root_cache = nullptr;
+        c->root_cache_cap = 0;
+        HIP_TRY(c, hipMalloc(&c->root_cache, sizeof(float) * cache_floats));
+        c->root_cache_cap = cache_floats;
+      }
+      st = cache_copy(true);
+      if (st != VCR_OK) return st;
+      c->root_cached = true;
+    }
     if (pp.spec) {
       if (splits) {
         st = prepare_splits(c, g, bf, splits);
