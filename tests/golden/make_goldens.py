@@ -49,6 +49,11 @@ BETA = {
     "resnet3x8x8": (6, 3, 5),
 }
 
+# branch-and-bound loops on input 0: {workload: (eps, batch, rounds, Adam steps)}
+BAB = {
+    "resnet3x8x8": (1.6 / 255, 2, 3, 5),
+}
+
 # A-guided box vertices: {workload: inputs}
 CORNERS = {
     "mlp3072x8192x4": [0, 15],
@@ -182,6 +187,27 @@ def make_beta(name, n_dom, depth, iters):
     print("wrote", path)
 
 
+def make_bab(name, eps, batch, rounds, iters):
+    """The oracle's loop on input 0 at the given radius, with its default split order: the
+    order, the per-round log and the children's lower bounds."""
+    from oracle import beta64
+    wl = make_workload(name, batch=1, eps=np.float32(eps))
+    t = time.time()
+    root = oracle.crown(wl.net, wl.x0[0], wl.eps, wl.C[0])
+    order = beta64.default_order(wl.net, root)
+    r = beta64.bab(wl.net, wl.x0[0], wl.eps, wl.C[0], order=order, batch=batch, rounds=rounds, iters=iters, root=root)
+    lbs = np.array([lb for kids in r.children for _, lb in kids])
+    print(f"{name} loop: {time.time() - t:.1f} s, log {r.log}, closest bound to 0 "
+          f"{np.min(np.abs(lbs)) if lbs.size else None}", flush=True)
+    out = {"eps": np.array(eps, np.float32), "batch": np.array(batch), "rounds": np.array(rounds),
+           "iters": np.array(iters), "order": np.array(order, np.int32), "log": np.array(r.log, np.int64),
+           "verified": np.array(r.verified), "evaluated": np.array(r.evaluated), "remaining": np.array(r.remaining),
+           "children_lb": lbs}
+    path = os.path.join(HERE, f"{name}_bab.npz")
+    np.savez_compressed(path, **out)
+    print("wrote", path)
+
+
 def make_corners(name, inputs):
     wl = make_workload(name)
     out = {"inputs": np.array(inputs)}
@@ -211,9 +237,11 @@ def make_bab_splits():
 if __name__ == "__main__":
     names = sys.argv[1:] or (list(GOLDENS) + ["bab"] + [f"{k}_sampled" for k in SAMPLED] + list(ONE_HIDDEN)
                              + [f"{k}_alpha" for k in ALPHA] + [f"{k}_corners" for k in CORNERS]
-                             + [f"{k}_beta" for k in BETA])
+                             + [f"{k}_beta" for k in BETA] + [f"{k}_bab" for k in BAB])
     for n in names:
-        if n.endswith("_beta"):
+        if n.endswith("_bab"):
+            make_bab(n[:-len("_bab")], *BAB[n[:-len("_bab")]])
+        elif n.endswith("_beta"):
             make_beta(n[:-len("_beta")], *BETA[n[:-len("_beta")]])
         elif n.endswith("_alpha"):
             make_alpha(n[:-len("_alpha")], *ALPHA[n[:-len("_alpha")]])

@@ -236,3 +236,23 @@ def test_conv_beta_chunked_equals_whole():
     torch.cuda.synchronize()
     assert ctx.stats()["n_chunks_last_call"] > st0["n_chunks_last_call"]
     assert np.array_equal(lb.cpu().numpy(), lb2.cpu().numpy()) and np.array_equal(ub.cpu().numpy(), ub2.cpu().numpy())
+
+
+def test_bab_loop_resnet3x8x8_full_width():
+    """The loop on the full-width 3x8x8 ResNet's first input (99 spec rows) at a radius where
+    the root is not verified, with the oracle's split order: the same rounds, the same
+    children bounded and kept, as the stored oracle run (whose children's lower bounds all
+    stay farther than the parity tolerance from 0)."""
+    import os
+    from workloads import make_workload
+    g = np.load(os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "resnet3x8x8_bab.npz"))
+    assert float(np.min(np.abs(g["children_lb"]))) > 1e-3
+    wl = make_workload("resnet3x8x8", batch=1, eps=g["eps"])
+    order = [tuple(int(v) for v in o) for o in g["order"]]
+    ctx = gpu_ctx(wl.net)
+    got = ctx.bab_verify(to_dev(wl.x0), wl.eps, to_dev(wl.C), batch=int(g["batch"]), max_rounds=int(g["rounds"]),
+                         iters=int(g["iters"]), order=order)
+    log("oracle", g["log"].tolist(), "gpu", got["log"])
+    assert got["verified"] == bool(g["verified"])
+    assert got["log"] == [tuple(int(v) for v in x) for x in g["log"]]
+    assert got["evaluated"] == int(g["evaluated"]) and got["remaining"] == int(g["remaining"])
