@@ -1364,28 +1364,28 @@ __global__ __launch_bounds__(256, 2) void k_fwd_conv(const FwdConvArgs p, FastDi
   }
 }
 
-// Inputs with CIN <= 4 channels (the network input): a thread per output element, channels
-// fastest, so the input loads of a wave are shared; the weights are staged in LDS channels
-// fastest, [tap][ci][Co].  Workgroups take FWD_SMALL_POS positions' worth of elements of one
-// row (blockIdx.x) and stride over the rows (blockIdx.y).
+// Inputs with CIN <= 4 channels (the network input): a thread per output position and four
+// consecutive output channels (its 9 CIN inputs loaded once for the four), the weights staged
+// in LDS channels fastest, [tap][ci][Co], read as float4.  Workgroups take 256 such items of
+// one row (blockIdx.x) and stride over the rows (blockIdx.y).
 template <int CIN>
 __global__ __launch_bounds__(256) void k_fwd_conv_small(const FwdConvArgs p) {
-  extern __shared__ float wl[];
+  extern __shared__ __attribute__((aligned(16))) float wl[];
   const int tid = threadIdx.x;
   for (int i = tid; i < 9 * CIN * p.Co; i += 256) {
     const int co = i % p.Co, k = i / p.Co;   // k = tap * CIN + ci
     wl[i] = p.Wk[(int64_t)co * 9 * CIN + k];
   }
   __syncthreads();
-  const int HW = p.Ho * p.Ho;
+  const int HW = p.Ho * p.Ho, G = p.Co / 4;
   const int local = blockIdx.x * 256 + tid;
-  if (local >= HW * p.Co) return;
-  const int pos = local / p.Co, n = local - pos * p.Co;
+  if (local >= HW * G) return;
+  const int pos = local / G, n0 = 4 * (local - pos * G);
   const int yo = pos / p.Ho, xo = pos - yo * p.Ho;
-  const float bn = p.bias[n];
+  const float4 bn = *reinterpret_cast<const float4 *>(p.bias + n0);
   for (int64_t r = blockIdx.y; r < p.rows; r += gridDim.y) {
     const float *x = p.in + r * p.in_rs;
-    float acc = 0.f;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
     for (int ky = 0; ky < 3; ++ky) {
       const int yy = yo * p.stride - 1 + ky;
@@ -1396,12 +1396,22 @@ __global__ __launch_bounds__(256) void k_fwd_conv_small(const FwdConvArgs p) {
         if ((unsigned)xx >= (unsigned)p.Hi) continue;
         const float *xs = x + (yy * p.Hi + xx) * CIN;
 #pragma unroll
-        for (int ci = 0; ci < CIN; ++ci) acc += xs[ci] * wl[((ky * 3 + kx) * CIN + ci) * p.Co + n];
+        for (int ci = 0; ci < CIN; ++ci) {
+          const float xv = xs[ci];
+          const float4 w = *reinterpret_cast<const float4 *>(&wl[((ky * 3 + kx) * CIN + ci) * p.Co + n0]);
+          acc.x += xv * w.x;
+          acc.y += xv * w.y;
+          acc.z += xv * w.z;
+          acc.w += xv * w.w;
+        }
       }
     }
     int64_t ob, pb, rb;
     fwd_offsets(p, r, pos, &ob, &pb, &rb);
-    fwd_apply(p, r, ob, pb, rb, n, acc + bn);
+    fwd_apply(p, r, ob, pb, rb, n0, acc.x + bn.x);
+    fwd_apply(p, r, ob, pb, rb, n0 + 1, acc.y + bn.y);
+    fwd_apply(p, r, ob, pb, rb, n0 + 2, acc.z + bn.z);
+    fwd_apply(p, r, ob, pb, rb, n0 + 3, acc.w + bn.w);
   }
 }
 
@@ -1418,7 +1428,8 @@ hipError_t launch_fwd_conv(const FwdConvArgs &a, hipStream_t s) {
   if (a.Ci <= 4) {
     const size_t lds = sizeof(float) * 9 * (size_t)a.Ci * a.Co;
     if (lds > 65536 || HW * a.Co >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
-    const dim3 grid((unsigned)((HW * a.Co + 255) / 256), (unsigned)std::min<int64_t>(a.rows, 128));
+    if (a.Co % 4) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)((HW * (a.Co / 4) + 255) / 256), (unsigned)std::min<int64_t>(a.rows, 256));
     switch (a.Ci) {
       case 1: hipLaunchKernelGGL(k_fwd_conv_small<1>, grid, dim3(256), lds, s, a); break;
       case 2: hipLaunchKernelGGL(k_fwd_conv_small<2>, grid, dim3(256), lds, s, a); break;
