@@ -18,9 +18,18 @@ FastDiv make_fastdiv(uint32_t d);
 // Each class runs as a GEMM over its own taps only, so no all-zero K tile is computed (the
 // executed flops are the algorithmic ones).  Positions: u = u0 + ustep iy, w = w0 + wstep ix
 // (ustep = stride unless ny = 1); taps (ky0 + kys ty, kx0 + kxs tx).
+//
+// Windowed destinations are clipped to the image: a class then holds only the (row, position)
+// pairs whose destination lies inside the image, rows outer and positions (iy, ix) inner as
+// before.  Row r's anchor is (a_y, a_x) = ((r mod Ha^2) / Ha, r mod Ha); per anchor the inside
+// positions of an axis are an interval [lo(a), lo(a) + n(a)), so one cycle of Ha^2 rows holds
+// T = (sum_a n_y(a)) (sum_a n_x(a)) pairs and the kernel finds a pair's anchors by a search
+// over the prefix sums of n(a).
+constexpr int CONVT_CLIP_MAX = 64;   // anchors per axis (one wave builds the tables)
 struct ConvClass {
   int32_t blk0;              // first workgroup of the class (classes are consecutive)
-  int32_t M;                 // GEMM rows of the class: R ny nx
+  int32_t M;                 // GEMM rows of the class: R ny nx, or (R / Ha^2) T clipped
+  int32_t clip;              // 1: positions outside the image are left out (div_yx divides by T)
   int32_t ny, nx, u0, w0, ustep, wstep;
   int32_t nty, ntx, ky0, kx0, kys, kxs;
   FastDiv div_yx, div_x;
@@ -40,6 +49,14 @@ struct ConvTArgs {
   int32_t M_pad;             // partial-sum pitch (>= R S_in^2)
   const int4 *rows;          // per coefficient row: (unit, anchor y, anchor x, -)
   int32_t dense, scale, h_in;  // window origin = anchor * scale - h_in (dense: 0)
+  // windowed destinations: anchors per axis of the pass (rows in (cycle, a_y, a_x) order, the
+  // row table's anchors); with 0 < Ha <= CONVT_CLIP_MAX and R a multiple of Ha^2 only the
+  // window positions inside the image are computed and written (the others are never read:
+  // windowed sources are masked to the image, and the constant terms skip them)
+  int32_t Ha;
+  // windowed sources (src_scale > 0, in windowed passes: Ha > 0): the source window's origin
+  // is anchor * src_scale - src_h on an H_out image; source positions outside it read as zero
+  int32_t src_scale, src_h, H_out;
   const float *res;          // optional residual windows on the same node
   int64_t res_row_stride;
   int32_t res_S, res_off;
@@ -67,7 +84,11 @@ hipError_t launch_convt(const ConvTArgs &a, hipStream_t s);
 // alone, and its flops (2 per multiply-add of a position and a tap that reaches it).
 int convt_launches(const ConvTArgs &a);
 hipError_t launch_convt_part(const ConvTArgs &a, int part, hipStream_t s);
+// Algorithmic flops of dispatch `part`: 2 per multiply-add of a destination position and a tap
+// whose source position both lie inside the image (windowed rows clipped to the image).
 uint64_t convt_part_flops(const ConvTArgs &a, int part);
+// Whether the launch computes only the window positions inside the image
+bool convt_clipped(const ConvTArgs &a);
 
 struct StemArgs {
   const float *A;
@@ -80,6 +101,9 @@ struct StemArgs {
                                  // per row (chosen by launch_stem)
   const int4 *rows;
   int32_t dense, scale, h_in;
+  // windowed sources (src_scale > 0): source window origin anchor * src_scale - src_h on an
+  // H_src image; positions outside the image are not gathered
+  int32_t src_scale, src_h, H_src;
   const float *c0, *r0;    // box centre / radius, CHW per unit
   int64_t ld_box;          // floats per unit in c0 / r0
   float *part;             // [R][S_in^2]
@@ -134,8 +158,14 @@ hipError_t launch_fwd_conv(const FwdConvArgs &a, hipStream_t s);
 // out = x + y over rows of n values (the add node in the gradient pass)
 hipError_t launch_fwd_add(const float *x, int64_t xs, const float *y, int64_t ys, float *out, int64_t os,
                           int32_t rows, int64_t n, hipStream_t s);
+// Window positions of clipped rows (Ha > 0): row r's window of S x S positions at origin
+// anchor * scale - h, anchor ((r mod Ha^2) / Ha, r mod Ha); positions outside the H x H image
+// hold no partial sums.
+struct WinClip {
+  int32_t Ha = 0, scale = 1, h = 0, S = 0, H = 0;
+};
 hipError_t launch_rowsum_win(float *beta, const float *part, int32_t n_parts, int64_t M_pad, int64_t R,
-                             int32_t per_row, hipStream_t s);
+                             int32_t per_row, hipStream_t s, WinClip clip = WinClip{});
 hipError_t launch_row_table(int4 *rows, int64_t R, int32_t rows_per_unit, int32_t C, int32_t H, int32_t W,
                             int32_t windowed, int32_t unit0, hipStream_t s);
 hipError_t launch_finalize_conv(const float *beta, int32_t B, int32_t C, int32_t H, const float *ibp_c,

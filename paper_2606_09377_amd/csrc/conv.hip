@@ -8,14 +8,17 @@
 // window has half-size h around the row's anchor (i, j) (scaled to the node's resolution)
 // and grows by one per stride-1 3x3 convolution (2h + 1 through stride 2).  Rows of a
 // dense node (spec rows, fully connected neurons) use the whole image: origin 0, S = H.
-// Window positions outside the image are the convolution's zero padding and are kept at 0.
+// Window positions outside the image are the convolution's zero padding: the transposed
+// convolution computes and writes only the positions inside the image, and every reader of a
+// window (the next transposed convolution, the stem, the constant terms) takes the positions
+// outside it as zero without reading them.
 //
 // The transposed convolution of one row is an implicit GEMM:
 //   out[(r, u, w), ci] = sum_{tap=(ky,kx), co} A_out[r][u'][w'][co] * W[co][ci][ky][kx]
 //   u' = (u + delta - ky) / stride (only when divisible and inside the source window)
-// with M = rows x S_in^2, N = C_in, K = 9 C_out, run per class of output positions (the
-// positions that the same taps reach: stride parity and the window's border ring) over that
-// class's taps only.  The weights are repacked at load time as
+// with M = rows x S_in^2 (windowed rows: the positions inside the image), N = C_in,
+// K = 9 C_out, run per class of output positions (the positions that the same taps reach:
+// stride parity and the window's border ring) over that class's taps only.  The weights are repacked at load time as
 // Bt[ci][tap * C_out + co] (K-contiguous).  The epilogue applies, per output element at
 // global position (gy, gx):
 //   outside the image          -> 0
@@ -42,6 +45,78 @@ __device__ __forceinline__ uint32_t fdiv(uint32_t n, FastDiv d) {
   return (uint32_t)(t >> d.shift);
 }
 
+// floor(a / b) for b > 0 and any sign of a
+__host__ __device__ inline int floor_div(int a, int b) { return a >= 0 ? a / b : -((-a + b - 1) / b); }
+
+// Class positions i in [0, n) of one axis whose image coordinate o + u0 + ustep i lies in
+// [0, H): the interval [*lo, *hi) (empty: *lo == *hi)
+__host__ __device__ inline void clip_range(int o, int u0, int ustep, int n, int H, int *lo, int *hi) {
+  const int l = min(max(-floor_div(o + u0, ustep), 0), n);
+  const int h = min(max(floor_div(H - 1 - o - u0, ustep) + 1, 0), n);
+  *lo = l;
+  *hi = max(h, l);
+}
+
+// Tables of a clipped class, per anchor a < Ha: tab[0][a] = first inside position of the
+// y axis, tab[1][a] = inside y positions of the anchors before a (tab[1][Ha]: all of them),
+// tab[2], tab[3] the same for x.  Built by one wave (lane a), an inclusive scan across lanes.
+typedef int ClipTab[4][CONVT_CLIP_MAX + 1];
+__device__ __forceinline__ void clip_tables(const ConvTArgs &p, const ConvClass &cl, ClipTab &tab, int lane) {
+#pragma unroll
+  for (int ax = 0; ax < 2; ++ax) {
+    int lo = 0, hi = 0;
+    if (lane < p.Ha)
+      clip_range(lane * p.scale - p.h_in, ax ? cl.w0 : cl.u0, ax ? cl.wstep : cl.ustep, ax ? cl.nx : cl.ny, p.H_in,
+                 &lo, &hi);
+    int x = hi - lo;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(x, o);
+      if (lane >= o) x += y;
+    }
+    if (lane < p.Ha) {
+      tab[2 * ax][lane] = lo;
+      tab[2 * ax + 1][lane + 1] = x;
+    }
+    if (lane == 0) tab[2 * ax + 1][0] = 0;
+  }
+}
+
+// GEMM row m < cl.M of a class -> coefficient row r, class position (iy, ix) and, for
+// windowed rows (Ha > 0), the row's anchor index a_y Ha + a_x
+__device__ __forceinline__ void convt_row(const ConvTArgs &p, const ConvClass &cl, const ClipTab &tab, uint32_t m,
+                                          uint32_t *r, int *iy, int *ix, int *anc) {
+  if (cl.clip) {
+    const int Wx = tab[3][p.Ha];
+    const uint32_t cyc = fdiv(m, cl.div_yx);   // cycles of Ha^2 rows
+    int rem = (int)(m - cyc * (uint32_t)(tab[1][p.Ha] * Wx));
+    int ay = 0, ax = 0;
+#pragma unroll
+    for (int b = CONVT_CLIP_MAX / 2; b > 0; b >>= 1)   // last anchor with prefix * Wx <= rem
+      if (ay + b < p.Ha && tab[1][ay + b] * Wx <= rem) ay += b;
+    rem -= tab[1][ay] * Wx;
+    const int wy = tab[1][ay + 1] - tab[1][ay];
+#pragma unroll
+    for (int b = CONVT_CLIP_MAX / 2; b > 0; b >>= 1)
+      if (ax + b < p.Ha && wy * tab[3][ax + b] <= rem) ax += b;
+    rem -= wy * tab[3][ax];
+    const int wx = tab[3][ax + 1] - tab[3][ax];   // > 0: ax is the last anchor below rem
+    const int ky = rem / wx;
+    *anc = ay * p.Ha + ax;
+    *r = cyc * (uint32_t)(p.Ha * p.Ha) + (uint32_t)*anc;
+    *iy = tab[0][ay] + ky;
+    *ix = tab[2][ax] + rem - ky * wx;
+  } else {
+    const uint32_t rr = fdiv(m, cl.div_yx);
+    const uint32_t pos = m - rr * (uint32_t)(cl.ny * cl.nx);
+    const uint32_t y = fdiv(pos, cl.div_x);
+    *r = rr;
+    *iy = (int)y;
+    *ix = (int)(pos - y * (uint32_t)cl.nx);
+    *anc = p.Ha > 0 ? (int)(rr % (uint32_t)(p.Ha * p.Ha)) : 0;
+  }
+}
+
 // Tile shapes: BM x BN outputs per workgroup of 4 wave64 arranged WM x WN, each wave
 // owning (BM / WM) x (BN / WN) as 32 x 32 MFMA blocks; BK-deep K tiles through
 // double-buffered LDS.  A K tile never straddles two taps (C_out is a multiple of 32).
@@ -64,13 +139,12 @@ __device__ __attribute__((aligned(16))) float g_zero4[4] = {0.f, 0.f, 0.f, 0.f};
 // constant terms per GEMM row for the tile m0.. of class cl, columns n0..; acc holds the
 // MB x NB 32 x 32 MFMA blocks of wave (wm, wn); scratch is >= 24 BM bytes of free LDS.
 template <int BM, int BN, int WM, int WN, bool RELU, bool AL, bool SPL>
-__device__ __forceinline__ void convt_epilogue(const ConvTArgs &p, const ConvClass &cl,
+__device__ __forceinline__ void convt_epilogue(const ConvTArgs &p, const ConvClass &cl, const ClipTab &tab,
                                                const f32x16 (&acc)[BM / WM / 32][BN / WN / 32], int m0, int n0,
                                                int nt, float *scratch) {
   constexpr int MB = BM / WM / 32, NB = BN / WN / 32;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN, r32 = lane & 31;
-  const int nyx = cl.ny * cl.nx;
   // Row information of the tile's BM GEMM rows is computed once, a row per thread, into
   // LDS (the operand buffers are free after the main loop's last barrier).  A lane holds 16
   // rows of each 32 x 32 block as 4 groups of 4 consecutive rows; the relaxation parameters
@@ -91,11 +165,11 @@ __device__ __forceinline__ void convt_epilogue(const ConvTArgs &p, const ConvCla
   for (int tr = tid; tr < BM; tr += 256) {
     const int m = m0 + tr;
     const bool valid = m < cl.M;
-    const uint32_t r = valid ? fdiv((uint32_t)m, cl.div_yx) : 0u;
-    const uint32_t pos = valid ? (uint32_t)m - r * (uint32_t)nyx : 0u;
-    const uint32_t iy = fdiv(pos, cl.div_x);
-    const int u = cl.u0 + (int)iy * cl.ustep;
-    const int w = cl.w0 + (int)(pos - iy * (uint32_t)cl.nx) * cl.wstep;
+    uint32_t r = 0;
+    int iy = 0, ix = 0, anc = 0;
+    if (valid) convt_row(p, cl, tab, (uint32_t)m, &r, &iy, &ix, &anc);
+    const int u = cl.u0 + iy * cl.ustep;
+    const int w = cl.w0 + ix * cl.wstep;
     const int4 an = p.rows[r];   // (unit, anchor y, anchor x, -)
     const int gy = p.dense ? u : an.y * p.scale - p.h_in + u;
     const int gx = p.dense ? w : an.z * p.scale - p.h_in + w;
@@ -228,6 +302,7 @@ __global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
   constexpr int QA = BM / RPP, QB = BN / RPP;
   __shared__ __attribute__((aligned(16))) float As[2][BM * BK];
   __shared__ __attribute__((aligned(16))) float Bs[2][BN * BK];
+  __shared__ ClipTab tab;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
 
@@ -239,25 +314,41 @@ __global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
   const int lb = bid - cl.blk0;
   const int mt = lb / n_nt, nt = lb - mt * n_nt;
   const int m0 = mt * BM, n0 = nt * BN;
-  const int nyx = cl.ny * cl.nx;
   const int sh = p.stride == 2 ? 1 : 0;
+  if (cl.clip) {   // workgroup-uniform
+    if (wave == 0) clip_tables(p, cl, tab, lane);
+    __syncthreads();
+  }
 
   // Per tile row: its source row pointer and its class position (iy, ix).  Tap (ty, tx) of
-  // the class reads source position (iy + dy, ix + dx) with a wave-uniform shift (dy, dx).
+  // the class reads source position (iy + dy, ix + dx) with a wave-uniform shift (dy, dx);
+  // of a windowed source only the positions inside the image, [ylo, ylo + yl) x [xlo, xlo +
+  // xl) of the window, are read (the pointer and coordinates are taken relative to ylo, xlo).
   const int lrow = tid / TPR, lcol = (tid % TPR) * 4;
   const int scol = (((tid % TPR)) ^ lds_swz<BK>(lrow)) * 4;
   const float *a_row[QA];
-  int ys[QA], xs[QA];
+  int ys[QA], xs[QA], yl[QA], xl[QA];
 #pragma unroll
   for (int q = 0; q < QA; ++q) {
     const uint32_t m = (uint32_t)(m0 + lrow + RPP * q);
     const bool valid = m < (uint32_t)cl.M;
-    const uint32_t r = fdiv(m, cl.div_yx);
-    const uint32_t pos = m - r * (uint32_t)nyx;
-    const uint32_t iy = fdiv(pos, cl.div_x);
-    a_row[q] = p.A + (valid ? (int64_t)r * p.row_stride_out : 0);
-    ys[q] = valid ? (int)iy : -(1 << 20);   // an invalid row matches no tap
-    xs[q] = (int)(pos - iy * (uint32_t)cl.nx);
+    uint32_t r = 0;
+    int iy = 0, ix = 0, anc = 0;
+    if (valid) convt_row(p, cl, tab, m, &r, &iy, &ix, &anc);
+    int ylo = 0, xlo = 0, yn = p.S_out, xn = p.S_out;
+    if (p.src_scale > 0 && valid) {   // windowed source (Ha > 0): anchor from the row index
+      const int ay = anc / p.Ha, ax = anc - ay * p.Ha;
+      const int oy = ay * p.src_scale - p.src_h, ox = ax * p.src_scale - p.src_h;
+      ylo = max(0, -oy);
+      xlo = max(0, -ox);
+      yn = max(0, min(p.S_out, p.H_out - oy) - ylo);
+      xn = max(0, min(p.S_out, p.H_out - ox) - xlo);
+    }
+    a_row[q] = p.A + (valid ? (int64_t)r * p.row_stride_out + ((int64_t)ylo * p.S_out + xlo) * p.C_out : 0);
+    ys[q] = valid ? iy - ylo : -(1 << 20);   // an invalid row matches no tap
+    xs[q] = ix - xlo;
+    yl[q] = yn;
+    xl[q] = xn;
   }
   const float *Bg = p.Bt + (int64_t)(n0 + lrow) * p.ldb + lcol;
   f32x4 ra[QA], rb[QB];
@@ -285,9 +376,9 @@ __global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
 #pragma unroll
     for (int q = 0; q < QA; ++q) {
       const int yy = ys[q] + dy, xx = xs[q] + dx;
-      const bool ok = (unsigned)yy < (unsigned)p.S_out && (unsigned)xx < (unsigned)p.S_out;
-      // positions outside the source window read a zero block: no select on the loaded
-      // value, so the wait for the load moves past the MFMAs to the LDS store
+      const bool ok = (unsigned)yy < (unsigned)yl[q] && (unsigned)xx < (unsigned)xl[q];
+      // positions outside the source window or the image read a zero block: no select on
+      // the loaded value, so the wait for the load moves past the MFMAs to the LDS store
       const float *src = ok ? a_row[q] + (yy * p.S_out + xx) * p.C_out + co : g_zero4;
       ra[q] = *reinterpret_cast<const f32x4 *>(src);
     }
@@ -346,7 +437,7 @@ __global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
 
   // ---- epilogue (the operand buffers are free after the main loop's last barrier) ----
   static_assert(28 * BM <= (int)sizeof(As), "epilogue row information must fit the A buffers");
-  convt_epilogue<BM, BN, WM, WN, RELU, AL, SPL>(p, cl, acc, m0, n0, nt, &As[0][0]);
+  convt_epilogue<BM, BN, WM, WN, RELU, AL, SPL>(p, cl, tab, acc, m0, n0, nt, &As[0][0]);
 }
 
 // Classes of one axis: positions u of the destination window with the same taps ky, as an
@@ -417,10 +508,27 @@ static ConvClass class_geometry(const std::vector<AxisClass> &cu, int idx) {
   return k;
 }
 
+bool convt_clipped(const ConvTArgs &a) {
+  return !a.dense && a.Ha > 0 && a.Ha <= CONVT_CLIP_MAX && a.R % (a.Ha * a.Ha) == 0;
+}
+
+// Inside positions of one axis of a class, summed over the anchors (clipped classes)
+static int64_t clip_total(const ConvTArgs &a, int u0, int ustep, int n) {
+  int64_t t = 0;
+  for (int an = 0; an < a.Ha; ++an) {
+    int lo, hi;
+    clip_range(an * a.scale - a.h_in, u0, ustep, n, a.H_in, &lo, &hi);
+    t += hi - lo;
+  }
+  return t;
+}
+
 static bool convt_plan(const ConvTArgs &a, std::vector<AxisClass> &cu, std::vector<ConvtDispatch> &plan) {
   plan.clear();
   if (a.C_out % 32 || a.R <= 0 || a.N_pad <= 0 || (a.stride != 1 && a.stride != 2)) return false;
   if ((int64_t)a.R * a.S_in * a.S_in > a.M_pad) return false;
+  // windowed sources feed windows, in windowed passes (anchors from the row index)
+  if (a.src_scale > 0 && (a.H_out <= 0 || a.dense || a.Ha <= 0 || a.R % (a.Ha * a.Ha))) return false;
   if (!convt_axes(a, cu)) return false;
   const int total = (int)(cu.size() * cu.size());
   for (int f = 0; f < total; f += 4) {
@@ -446,10 +554,17 @@ static int64_t convt_fill(ConvTArgs &a, const std::vector<AxisClass> &cu, const 
       continue;
     }
     k = class_geometry(cu, d.cls[c]);
-    const int64_t M = (int64_t)a.R * k.ny * k.nx;
+    int64_t M = (int64_t)a.R * k.ny * k.nx;
+    uint32_t per = (uint32_t)(k.ny * k.nx);   // GEMM rows per coefficient row (clipped: per cycle)
+    if (convt_clipped(a)) {
+      const int64_t T = clip_total(a, k.u0, k.ustep, k.ny) * clip_total(a, k.w0, k.wstep, k.nx);
+      M = (int64_t)(a.R / (a.Ha * a.Ha)) * T;
+      per = (uint32_t)std::max<int64_t>(T, 1);
+      k.clip = 1;
+    }
     if (M >= ((int64_t)1 << 31)) return -1;
     k.M = (int32_t)M;
-    k.div_yx = make_fastdiv((uint32_t)(k.ny * k.nx));
+    k.div_yx = make_fastdiv(per);
     k.div_x = make_fastdiv((uint32_t)k.nx);
     k.blk0 = (int32_t)blk;
     blk += (M + BM - 1) / BM * n_nt;
@@ -462,10 +577,32 @@ uint64_t convt_part_flops(const ConvTArgs &a, int part) {
   std::vector<ConvtDispatch> plan;
   if (!convt_plan(a, cu, plan) || part < 0 || part >= (int)plan.size()) return 0;
   uint64_t f = 0;   // every position times the taps that reach it: the necessary multiply-adds
+  const bool win = !a.dense && a.Ha > 0 && a.R % (a.Ha * a.Ha) == 0;
+  const int sh = a.stride == 2 ? 1 : 0;
+  // windowed rows: per axis and anchor, the (position, tap) pairs whose destination and source
+  // both lie inside the image; a row's count is the product of its two axes'
+  auto axis_pairs = [&](int u0, int ustep, int n, int k0, int ks, int nk) {
+    int64_t t = 0;
+    for (int an = 0; an < a.Ha; ++an) {
+      int lo, hi;
+      clip_range(an * a.scale - a.h_in, u0, ustep, n, a.H_in, &lo, &hi);
+      const int os = an * a.src_scale - a.src_h;
+      for (int i = lo; i < hi; ++i)
+        for (int tk = 0; tk < nk; ++tk) {
+          const int ys = i + ((u0 + a.delta - (k0 + ks * tk)) >> sh);   // source window position
+          t += a.src_scale <= 0 || (os + ys >= 0 && os + ys < a.H_out);
+        }
+    }
+    return t;
+  };
   for (int idx : plan[part].cls) {
     const ConvClass k = class_geometry(cu, idx);
-    f += 2ull * (uint64_t)a.R * (uint64_t)(k.ny * k.nx) * (uint64_t)(k.nty * k.ntx) * (uint64_t)a.C_out *
-         (uint64_t)a.C_in;
+    if (win)
+      f += 2ull * (uint64_t)(a.R / (a.Ha * a.Ha)) * (uint64_t)axis_pairs(k.u0, k.ustep, k.ny, k.ky0, k.kys, k.nty) *
+           (uint64_t)axis_pairs(k.w0, k.wstep, k.nx, k.kx0, k.kxs, k.ntx) * (uint64_t)a.C_out * (uint64_t)a.C_in;
+    else
+      f += 2ull * (uint64_t)a.R * (uint64_t)(k.ny * k.nx) * (uint64_t)(k.nty * k.ntx) * (uint64_t)a.C_out *
+           (uint64_t)a.C_in;
   }
   return f;
 }
@@ -688,6 +825,16 @@ __global__ __launch_bounds__(256, 3) void k_stem(const StemArgs p) {
       const int u = u_lo + uu, w = rem - uu * p.S_in;
       float part = 0.f;
       if (live[q]) {   // inside the image
+        // source window positions inside the source image: [ylo, yhi) x [xlo, xhi)
+        int ylo = 0, yhi = p.S_out, xlo = 0, xhi = p.S_out;
+        if (p.src_scale > 0) {
+          const int4 an = p.rows[r0 + rl];
+          const int oy = an.y * p.src_scale - p.src_h, ox = an.z * p.src_scale - p.src_h;
+          ylo = max(0, -oy);
+          xlo = max(0, -ox);
+          yhi = min(p.S_out, p.H_src - oy);
+          xhi = min(p.S_out, p.H_src - ox);
+        }
         float a[CIN];
 #pragma unroll
         for (int ci = 0; ci < CIN; ++ci) a[ci] = 0.f;
@@ -696,13 +843,13 @@ __global__ __launch_bounds__(256, 3) void k_stem(const StemArgs p) {
           int yy = u + p.delta - ky;
           if (yy < 0 || (yy & (p.stride - 1))) continue;
           yy /= p.stride;
-          if (yy >= p.S_out) continue;
+          if (yy < ylo || yy >= yhi) continue;
 #pragma unroll
           for (int kx = 0; kx < 3; ++kx) {
             int xx = w + p.delta - kx;
             if (xx < 0 || (xx & (p.stride - 1))) continue;
             xx /= p.stride;
-            if (xx >= p.S_out) continue;
+            if (xx < xlo || xx >= xhi) continue;
             const float *g = G + (rl * n_row_src + (yy - y_lo) * p.S_out + xx) * GP + 3 * ky + kx;
 #pragma unroll
             for (int ci = 0; ci < CIN; ++ci) a[ci] += g[9 * ci];
@@ -731,6 +878,7 @@ hipError_t launch_stem_t(StemArgs a, hipStream_t s) {
     return hipErrorInvalidValue;
   if (a.vtx && (!a.dense || a.S_in != a.H_in || a.ld_vtx < (int64_t)a.H_in * a.H_in * CIN))
     return hipErrorInvalidValue;
+  if (a.src_scale > 0 && (a.dense || a.H_src <= 0)) return hipErrorInvalidValue;
   const int64_t wt_floats = 32 * NB * (int64_t)(a.C_out + 4);
   // 42 KB of LDS per workgroup (three workgroups per CU), 64 KB for wide weights
   int64_t src_max = ((STEM_LDS_FLOATS - wt_floats) / GP) & ~(int64_t)31;
@@ -868,13 +1016,23 @@ hipError_t launch_init_conv(const ConvInitArgs &a, hipStream_t s) {
 // G = 2^lg lanes share a row (lane j sums positions j, j + G, ... over all parts), then add
 // their sums by a fixed butterfly: consecutive lanes read consecutive positions.
 __global__ void k_rowsum_win(float *beta, const float *part, int32_t n_parts, int64_t M_pad, int64_t R,
-                             int32_t per_row, int32_t lg) {
+                             int32_t per_row, int32_t lg, WinClip cw) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t r = t >> lg;
   const int G = 1 << lg, j = (int)(t & (G - 1));
   float s = 0.f;
   if (r < R) {
+    int oy = 0, ox = 0;   // clipped rows: the window's origin in the image
+    if (cw.Ha > 0) {
+      const int an = (int)(r % (cw.Ha * cw.Ha));
+      oy = an / cw.Ha * cw.scale - cw.h;
+      ox = an % cw.Ha * cw.scale - cw.h;
+    }
     for (int q = j; q < per_row; q += G) {
+      if (cw.Ha > 0) {   // positions outside the image have no partial sums
+        const int u = q / cw.S, w = q - u * cw.S;
+        if ((unsigned)(oy + u) >= (unsigned)cw.H || (unsigned)(ox + w) >= (unsigned)cw.H) continue;
+      }
       const int64_t m = r * per_row + q;
 #pragma unroll 4
       for (int p = 0; p < n_parts; ++p) s += part[p * M_pad + m];   // loads issued ahead of the adds
@@ -885,13 +1043,15 @@ __global__ void k_rowsum_win(float *beta, const float *part, int32_t n_parts, in
 }
 
 hipError_t launch_rowsum_win(float *beta, const float *part, int32_t n_parts, int64_t M_pad, int64_t R,
-                             int32_t per_row, hipStream_t s) {
+                             int32_t per_row, hipStream_t s, WinClip clip) {
   if (R <= 0) return hipSuccess;
+  if (clip.Ha > 0 && (clip.S <= 0 || (int64_t)clip.S * clip.S != per_row || R % ((int64_t)clip.Ha * clip.Ha)))
+    return hipErrorInvalidValue;
   int lg = 0;
   while (lg < 6 && (2 << lg) <= per_row) ++lg;
   const int64_t n = R << lg;
   hipLaunchKernelGGL(k_rowsum_win, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, beta, part, n_parts, M_pad, R,
-                     per_row, lg);
+                     per_row, lg, clip);
   return hipGetLastError();
 }
 

@@ -1009,6 +1009,14 @@ vcr_status run_pass(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &pp, int 
         a.dense = st.dst.dense ? 1 : 0;
         a.scale = st.dst.scale;
         a.h_in = st.dst.h;
+        // windowed passes: rows (unit, direction, c, a_y, a_x) anchored on the start node's
+        // H x H grid, so row r's anchor is r mod H^2
+        a.Ha = pp.windowed && !dom && !st.dst.dense ? start.H : 0;
+        if (!st.src.dense) {
+          a.src_scale = st.src.scale;
+          a.src_h = st.src.h;
+          a.H_out = nd.H;
+        }
         if (st.has_res) {
           a.res = slot(st.res);
           a.res_row_stride = st.res.row_stride;
@@ -1038,7 +1046,9 @@ vcr_status run_pass(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &pp, int 
           if (st2 != VCR_OK) return st2;
           *flops += cf;
         }
-        HIP_TRY(c, launch_rowsum_win(bf.beta, bf.part, a.N_pad / 64, a.M_pad, R, a.S_in * a.S_in, s));
+        WinClip cw;
+        if (convt_clipped(a)) cw = WinClip{a.Ha, a.scale, a.h_in, a.S_in, a.H_in};
+        HIP_TRY(c, launch_rowsum_win(bf.beta, bf.part, a.N_pad / 64, a.M_pad, R, a.S_in * a.S_in, s, cw));
         break;
       }
       case ST_STEM: {
@@ -1059,6 +1069,11 @@ vcr_status run_pass(vcr_ctx *c, GraphNet *g, GBufs &bf, const PassPlan &pp, int 
         a.dense = st.src.dense ? 1 : 0;
         a.scale = st.dst.scale;
         a.h_in = st.dst.h;
+        if (!st.src.dense) {
+          a.src_scale = st.src.scale;
+          a.src_h = st.src.h;
+          a.H_src = nd.H;
+        }
         a.c0 = bf.c0;
         a.r0 = bf.r0;
         a.ld_box = ld_of(g->n0);
