@@ -135,6 +135,38 @@ __device__ __forceinline__ int lds_swz(int row) {
 // Source of the zeros that taps outside the source window load
 __device__ __attribute__((aligned(16))) float g_zero4[4] = {0.f, 0.f, 0.f, 0.f};   // never written
 
+// LDS stages of the transposed convolution's operand tiles
+constexpr int CONVT_NS = 2;
+
+// 16 bytes from global memory into LDS: lane i of the wave writes lds + 16 i (lds is
+// wave-uniform).  Issued as inline assembly so that the compiler neither waits on the
+// vector-memory counter before every LDS read of the loop nor counts these loads: the loop
+// waits for them itself (wait_vmcnt) before the barrier that publishes a stage.  M0 carries
+// the LDS address; the kernels that use this have no other use of M0 (clobbering a register
+// the compiler reserves draws a warning, silenced here).
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(const float *g, float *lds) {
+  const uint32_t l = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) float *)lds;
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(__builtin_amdgcn_readfirstlane(l)),
+               "v"(g)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// Workgroup barrier after this wave's LDS reads have completed, without the memory fences of
+// __syncthreads (which wait for every outstanding vector-memory load, the prefetched stages
+// included); the "memory" clobber keeps the compiler's LDS accesses on their side.
+__device__ __forceinline__ void barrier_only() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// s_waitcnt on the vector-memory counter alone (vmcnt <= N; gfx9 encoding: vmcnt in bits 3:0
+// and 15:14, expcnt and lgkmcnt left at their maxima)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
 // Epilogue shared by the transposed-convolution kernels: relaxation (or identity), residual,
 // constant terms per GEMM row for the tile m0.. of class cl, columns n0..; acc holds the
 // MB x NB 32 x 32 MFMA blocks of wave (wm, wn); scratch is >= 24 BM bytes of free LDS.
@@ -295,15 +327,17 @@ __device__ __forceinline__ void convt_epilogue(const ConvTArgs &p, const ConvCla
 template <int BM, int BN, int BK, int WM, int WN, int MINB, bool RELU, bool AL = false, bool SPL = false>
 __global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
   static_assert(BK == 16 || BK == 32, "LDS swizzle assumes 4 or 8 chunks per row");
+  static_assert(BN / WN == 64, "a wave's constant-term partial covers 64 columns (N_pad / 64 partials)");
   constexpr int CPR = BK / 4;                 // 16-byte chunks per tile row
   constexpr int MB = BM / WM / 32, NB = BN / WN / 32;
   constexpr int TPR = CPR;                    // threads per tile row (one chunk each)
   constexpr int RPP = 256 / TPR;              // tile rows per load pass
   constexpr int QA = BM / RPP, QB = BN / RPP;
-  __shared__ __attribute__((aligned(16))) float As[2][BM * BK];
-  __shared__ __attribute__((aligned(16))) float Bs[2][BN * BK];
+  __shared__ __attribute__((aligned(16))) float As[CONVT_NS][BM * BK];
+  __shared__ __attribute__((aligned(16))) float Bs[CONVT_NS][BN * BK];
   __shared__ ClipTab tab;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WN, wn = wave % WN;
 
   // parity class of this workgroup (wave-uniform selects, no indexed argument access)
@@ -324,8 +358,14 @@ __global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
   // the class reads source position (iy + dy, ix + dx) with a wave-uniform shift (dy, dx);
   // of a windowed source only the positions inside the image, [ylo, ylo + yl) x [xlo, xlo +
   // xl) of the window, are read (the pointer and coordinates are taken relative to ylo, xlo).
-  const int lrow = tid / TPR, lcol = (tid % TPR) * 4;
-  const int scol = (((tid % TPR)) ^ lds_swz<BK>(lrow)) * 4;
+  // The operand tiles go from global memory straight into LDS (global_load_lds_dwordx4: the
+  // 64 lanes of one load fill 1 KB of LDS in lane order, 64 / TPR whole tile rows).  Lane
+  // (row lrow, chunk slot tid % TPR) therefore loads the logical chunk that the swizzle puts
+  // into that slot: dcol = (slot ^ swz(lrow)) * 4 (the same for the rows lrow + RPP q).
+  const int lrow = tid / TPR;
+  const int dcol = (((tid % TPR)) ^ lds_swz<BK>(lrow)) * 4;
+  constexpr int WROWS = 64 / TPR;   // tile rows of one wave's load
+  static_assert(RPP % 16 == 0, "the swizzle (period 16 rows) repeats with the rows of a load pass");
   const float *a_row[QA];
   int ys[QA], xs[QA], yl[QA], xl[QA];
 #pragma unroll
@@ -350,15 +390,14 @@ __global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
     yl[q] = yn;
     xl[q] = xn;
   }
-  const float *Bg = p.Bt + (int64_t)(n0 + lrow) * p.ldb + lcol;
-  f32x4 ra[QA], rb[QB];
+  const float *Bg = p.Bt + (int64_t)(n0 + lrow) * p.ldb + dcol;
   // K order: pairs of channel blocks outer, tap, then the block of the pair: the shifted
   // re-reads of one source block follow each other within a few K tiles (they hit the caches
   // instead of HBM), and the two halves of a 128-byte line (32 channels) are read by
   // consecutive K tiles (the second from L1)
   const int ntap = cl.nty * cl.ntx;
   const bool pairs = (p.C_out / BK) % 2 == 0;
-  auto gload = [&](int kt) {
+  auto gload = [&](int kt, int buf) {
     int cb, t;
     if (pairs) {
       const int grp = kt / (2 * ntap), rem = kt - grp * 2 * ntap;
@@ -372,25 +411,19 @@ __global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
     const int ty = t / cl.ntx, tx = t - ty * cl.ntx;
     const int ky = cl.ky0 + cl.kys * ty, kx = cl.kx0 + cl.kxs * tx;
     const int dy = (cl.u0 + p.delta - ky) >> sh, dx = (cl.w0 + p.delta - kx) >> sh;   // exact
-    const int co = co0 + lcol;
+    const int co = co0 + dcol;
 #pragma unroll
     for (int q = 0; q < QA; ++q) {
       const int yy = ys[q] + dy, xx = xs[q] + dx;
       const bool ok = (unsigned)yy < (unsigned)yl[q] && (unsigned)xx < (unsigned)xl[q];
-      // positions outside the source window or the image read a zero block: no select on
-      // the loaded value, so the wait for the load moves past the MFMAs to the LDS store
+      // positions outside the source window or the image read a zero block
       const float *src = ok ? a_row[q] + (yy * p.S_out + xx) * p.C_out + co : g_zero4;
-      ra[q] = *reinterpret_cast<const f32x4 *>(src);
+      dma16(src, &As[buf][(wave * WROWS + RPP * q) * BK]);
     }
     const int kb = (3 * ky + kx) * p.C_out + co0;
 #pragma unroll
-    for (int q = 0; q < QB; ++q) rb[q] = *reinterpret_cast<const f32x4 *>(Bg + (int64_t)q * RPP * p.ldb + kb);
-  };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int q = 0; q < QA; ++q) *reinterpret_cast<f32x4 *>(&As[buf][(lrow + RPP * q) * BK + scol]) = ra[q];
-#pragma unroll
-    for (int q = 0; q < QB; ++q) *reinterpret_cast<f32x4 *>(&Bs[buf][(lrow + RPP * q) * BK + scol]) = rb[q];
+    for (int q = 0; q < QB; ++q)
+      dma16(Bg + (int64_t)q * RPP * p.ldb + kb, &Bs[buf][(wave * WROWS + RPP * q) * BK]);
   };
 
   f32x16 acc[MB][NB];
@@ -402,18 +435,23 @@ __global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
   const int KT = cl.nty * cl.ntx * p.C_out / BK;
-  gload(0);
-  lstore(0);
-  __syncthreads();
+  // CONVT_NS LDS stages: K tile kt + CONVT_NS - 1 is in flight while tile kt is multiplied
+  constexpr int LPT = QA + QB;   // loads per thread per K tile
+#pragma unroll
+  for (int st = 0; st < CONVT_NS - 1; ++st)
+    if (st < KT) gload(st, st);
   // operand reads: lane (r32, half) takes chunks half * CPR / 2 + h, h < CPR / 2, of row r32
   const int r32 = lane & 31, sw = lds_swz<BK>(r32);
   int roff[CPR / 2];
 #pragma unroll
   for (int h = 0; h < CPR / 2; ++h) roff[h] = ((((lane >> 5) * (CPR / 2)) + h) ^ sw) * 4;
   for (int kt = 0; kt < KT; ++kt) {
-    const int cur = kt & 1;
-    const bool more = kt + 1 < KT;
-    if (more) gload(kt + 1);
+    const int cur = kt % CONVT_NS;
+    // tile kt has landed once no more than the loads of the tiles after it are outstanding
+    if (kt + CONVT_NS - 2 < KT) wait_vmcnt<(CONVT_NS - 2) * LPT>();
+    else wait_vmcnt<0>();
+    barrier_only();   // every wave's part of tile kt is in LDS; stage (kt - 1) % NS is free
+    if (kt + CONVT_NS - 1 < KT) gload(kt + CONVT_NS - 1, (kt + CONVT_NS - 1) % CONVT_NS);
     const float *as = As[cur] + (wm * (BM / WM) + r32) * BK;
     const float *bs = Bs[cur] + (wn * (BN / WN) + r32) * BK;
 #pragma unroll
@@ -431,11 +469,10 @@ __global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
           for (int j = 0; j < NB; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][e], b[j][e], acc[i][j], 0, 0, 0);
     }
-    if (more) lstore(cur ^ 1);
-    __syncthreads();
   }
+  __syncthreads();   // every wave is done with the operand buffers, which the epilogue reuses
 
-  // ---- epilogue (the operand buffers are free after the main loop's last barrier) ----
+  // ---- epilogue ----
   static_assert(28 * BM <= (int)sizeof(As), "epilogue row information must fit the A buffers");
   convt_epilogue<BM, BN, WM, WN, RELU, AL, SPL>(p, cl, tab, acc, m0, n0, nt, &As[0][0]);
 }
