@@ -102,6 +102,21 @@ def test_small_conv_nets_all_bounds(make):
                     what=f"{wl.name} input {b}")
 
 
+@pytest.mark.parametrize("hw,c2", [(4, 64), (6, 128)])
+def test_windows_larger_than_the_image(hw, c2):
+    """Tiny images, where the coefficient windows outgrow the image (up to 15 x 15 windows on a
+    4 x 4 image): most window positions lie outside the image, and whole position classes
+    have no position inside it for any anchor; every bound of both inputs against the oracle."""
+    wl = small_resnet(331, hw=hw, c1=32, c2=c2, fc=16)
+    log("case", wl.name, "c2", c2)
+    ctx = gpu_ctx(wl.net)
+    lb, ub, layers = gpu_crown(ctx, wl)
+    for b in range(wl.x0.shape[0]):
+        log("oracle input", b)
+        check_input(wl.net, wl.x0[b], wl.eps, wl.C[b], lb[b], ub[b], [(l[b], u[b]) for l, u in layers],
+                    what=f"{wl.name} input {b}")
+
+
 def test_conv_ibp_bounds():
     wl = small_resnet(303)
     ctx = gpu_ctx(wl.net)
