@@ -29,6 +29,7 @@
 // and reduces the constants over the tile's columns into one partial per GEMM row.
 #include "conv.h"
 #include "relax.h"
+#include "lds_dma.h"
 #include "splits.h"
 
 #include <algorithm>
@@ -119,18 +120,8 @@ __device__ __forceinline__ void convt_row(const ConvTArgs &p, const ConvClass &c
 
 // Tile shapes: BM x BN outputs per workgroup of 4 wave64 arranged WM x WN, each wave
 // owning (BM / WM) x (BN / WN) as 32 x 32 MFMA blocks; BK-deep K tiles through
-// double-buffered LDS.  A K tile never straddles two taps (C_out is a multiple of 32).
-//
-// LDS rows hold BK floats unpadded, as BK / 4 16-byte chunks; chunk c of tile row q sits at
-// chunk c ^ swz(q).  A 16-byte LDS access serves 16 lanes per cycle over the 64 banks, so the
-// swizzle spreads 16 consecutive rows at one chunk (the MFMA operand reads) over 16 distinct
-// 4-bank groups; the tile stores (BK / 4 threads per row) cover whole rows and are spread
-// already.  (Rows whose offsets coincide modulo the 64 banks get different chunk positions.)
-template <int BK>
-__device__ __forceinline__ int lds_swz(int row) {
-  constexpr int CPR = BK / 4, RPG = 16 / CPR;
-  return (row / RPG) & (CPR - 1);
-}
+// double-buffered LDS (rows unpadded, chunks swizzled by lds_swz).  A K tile never straddles
+// two taps (C_out is a multiple of 32).
 
 // Source of the zeros that taps outside the source window load
 __device__ __attribute__((aligned(16))) float g_zero4[4] = {0.f, 0.f, 0.f, 0.f};   // never written
@@ -138,34 +129,7 @@ __device__ __attribute__((aligned(16))) float g_zero4[4] = {0.f, 0.f, 0.f, 0.f};
 // LDS stages of the transposed convolution's operand tiles
 constexpr int CONVT_NS = 2;
 
-// 16 bytes from global memory into LDS: lane i of the wave writes lds + 16 i (lds is
-// wave-uniform).  Issued as inline assembly so that the compiler neither waits on the
-// vector-memory counter before every LDS read of the loop nor counts these loads: the loop
-// waits for them itself (wait_vmcnt) before the barrier that publishes a stage.  M0 carries
-// the LDS address; the kernels that use this have no other use of M0 (clobbering a register
-// the compiler reserves draws a warning, silenced here).
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
-__device__ __forceinline__ void dma16(const float *g, float *lds) {
-  const uint32_t l = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) float *)lds;
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(__builtin_amdgcn_readfirstlane(l)),
-               "v"(g)
-               : "memory", "m0");
-}
-#pragma clang diagnostic pop
 
-// Workgroup barrier after this wave's LDS reads have completed, without the memory fences of
-// __syncthreads (which wait for every outstanding vector-memory load, the prefetched stages
-// included); the "memory" clobber keeps the compiler's LDS accesses on their side.
-__device__ __forceinline__ void barrier_only() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
-
-// s_waitcnt on the vector-memory counter alone (vmcnt <= N; gfx9 encoding: vmcnt in bits 3:0
-// and 15:14, expcnt and lgkmcnt left at their maxima)
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
-}
 
 // Epilogue shared by the transposed-convolution kernels: relaxation (or identity), residual,
 // constant terms per GEMM row for the tile m0.. of class cl, columns n0..; acc holds the

@@ -34,6 +34,7 @@
 // a lane group holds with a fixed butterfly, so results are deterministic and do not depend
 // on which other rows share the tile.
 #include "kernels.h"
+#include "lds_dma.h"
 #include "splits.h"
 
 namespace vcr {
@@ -343,24 +344,37 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &p, f32x16 (&acc)[M
 // (per-row slopes, stored coefficients) to the backward epilogues.
 template <bool FWD, bool AL, bool AFF = false>
 __global__ __launch_bounds__(NTHREADS, GEMM_MINB) void k_gemm(const GemmArgs p) {
-  __shared__ __attribute__((aligned(16))) float As[2][BM * LDS_LD];
-  __shared__ __attribute__((aligned(16))) float Bs[2][BN * LDS_LD];
+  __shared__ __attribute__((aligned(16))) float As[2][BM * BK];
+  __shared__ __attribute__((aligned(16))) float Bs[2][BN * BK];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
   const int n_mt = p.M_pad / BM, n_nt = p.N_pad / BN;
   int mt, nt;
   map_tile(blockIdx.x, n_mt * n_nt, n_mt, n_nt, mt, nt);
   const int m0 = mt * BM, n0 = nt * BN;
 
-  // global -> register staging: thread t moves rows t/TPR + RPP q, columns 4(t%TPR)..+3
-  const int lrow = tid / TPR, lcol = (tid % TPR) * 4;
-  const float *Ag = p.A + (int64_t)(m0 + lrow) * p.lda + lcol;
-  const float *Bg = p.Bt + (int64_t)(n0 + lrow) * p.ldb + lcol;
+  // Operand tiles go from global memory straight into LDS (rows unpadded, chunks swizzled by
+  // lds_swz): one load of a wave fills 64 / TPR whole rows, lane order, so lane (row lrow,
+  // chunk slot tid % TPR) fetches the logical chunk that the swizzle puts into its slot (the
+  // same for the rows lrow + RPP q, the swizzle repeating every 16 rows)
+  static_assert(RPP % 16 == 0, "rows of one load pass share the swizzle");
+  constexpr int WROWS = 64 / TPR;
+  const int lrow = tid / TPR;
+  const int dcol = ((tid % TPR) ^ lds_swz<BK>(lrow)) * 4;
+  const float *Ag = p.A + (int64_t)(m0 + lrow) * p.lda + dcol;
+  const float *Bg = p.Bt + (int64_t)(n0 + lrow) * p.ldb + dcol;
   const int64_t a_step = RPP * p.lda, b_step = RPP * p.ldb;
-  f32x4 ra[SQ], rb[SQ];
+  auto issue = [&](int kt, int buf) {
+    const int k0 = kt * BK;
+#pragma unroll
+    for (int q = 0; q < SQ; ++q) {
+      dma16(Ag + q * a_step + k0, &As[buf][(wave * WROWS + RPP * q) * BK]);
+      dma16(Bg + q * b_step + k0, &Bs[buf][(wave * WROWS + RPP * q) * BK]);
+    }
+  };
 
   f32x16 acc[2][2];
 #pragma unroll
@@ -370,58 +384,47 @@ __global__ __launch_bounds__(NTHREADS, GEMM_MINB) void k_gemm(const GemmArgs p) 
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
+  // lane (r32, half) reads the 16 consecutive k half * 16 .. + 15 of its row: logical chunks
+  // half * 4 + h, h < 4 (rows r32 and r32 + 32 of a 64-row block share the swizzle)
+  const int r32 = lane & 31, sw = lds_swz<BK>(r32);
+  int roff[BK / 8];
+#pragma unroll
+  for (int h = 0; h < BK / 8; ++h) roff[h] = ((((lane >> 5) * (BK / 8)) + h) ^ sw) * 4;
+  const int a_off0 = (wm * 64 + r32) * BK;
+  const int a_off1 = a_off0 + 32 * BK;
+  const int b_off0 = (wn * 64 + r32) * BK;
+  const int b_off1 = b_off0 + 32 * BK;
+
   const int KT = p.K / BK;
-#pragma unroll
-  for (int q = 0; q < SQ; ++q) {
-    ra[q] = *reinterpret_cast<const f32x4 *>(Ag + q * a_step);
-    rb[q] = *reinterpret_cast<const f32x4 *>(Bg + q * b_step);
-    if constexpr (AFF) {
-      if (p.abs_b) rb[q] = __builtin_elementwise_abs(rb[q]);
-    }
-  }
-#pragma unroll
-  for (int q = 0; q < SQ; ++q) {
-    *reinterpret_cast<f32x4 *>(&As[0][(lrow + RPP * q) * LDS_LD + lcol]) = ra[q];
-    *reinterpret_cast<f32x4 *>(&Bs[0][(lrow + RPP * q) * LDS_LD + lcol]) = rb[q];
-  }
-  __syncthreads();
-
-  const int r32 = lane & 31;
-  const int kq = (lane >> 5) * (BK / 2);
-  const int a_off0 = (wm * 64 + r32) * LDS_LD + kq;
-  const int a_off1 = a_off0 + 32 * LDS_LD;
-  const int b_off0 = (wn * 64 + r32) * LDS_LD + kq;
-  const int b_off1 = b_off0 + 32 * LDS_LD;
-
+  issue(0, 0);
   for (int kt = 0; kt < KT; ++kt) {
     const int cur = kt & 1;
-    const bool more = kt + 1 < KT;
-    if (more) {
-      const int k0 = (kt + 1) * BK;
-#pragma unroll
-      for (int q = 0; q < SQ; ++q) {
-        ra[q] = *reinterpret_cast<const f32x4 *>(Ag + q * a_step + k0);
-        rb[q] = *reinterpret_cast<const f32x4 *>(Bg + q * b_step + k0);
-        if constexpr (AFF) {
-          if (p.abs_b) rb[q] = __builtin_elementwise_abs(rb[q]);
-        }
-      }
-    }
+    wait_vmcnt<0>();
+    barrier_only();   // every wave's part of tile kt is in LDS; the other stage is free
+    if (kt + 1 < KT) issue(kt + 1, cur ^ 1);
     const float *as = As[cur];
     const float *bs = Bs[cur];
     // all operand reads of the K tile first (the scheduler then spreads them over the MFMAs
-    // instead of stalling half-way through the tile), then the next tile's global loads
+    // instead of stalling half-way through the tile)
     f32x4 A0[BK / 8], A1[BK / 8], B0[BK / 8], B1[BK / 8];
 #pragma unroll
     for (int h = 0; h < BK / 8; ++h) {
-      A0[h] = *reinterpret_cast<const f32x4 *>(as + a_off0 + 4 * h);
-      A1[h] = *reinterpret_cast<const f32x4 *>(as + a_off1 + 4 * h);
-      B0[h] = *reinterpret_cast<const f32x4 *>(bs + b_off0 + 4 * h);
-      B1[h] = *reinterpret_cast<const f32x4 *>(bs + b_off1 + 4 * h);
+      A0[h] = *reinterpret_cast<const f32x4 *>(as + a_off0 + roff[h]);
+      A1[h] = *reinterpret_cast<const f32x4 *>(as + a_off1 + roff[h]);
+      B0[h] = *reinterpret_cast<const f32x4 *>(bs + b_off0 + roff[h]);
+      B1[h] = *reinterpret_cast<const f32x4 *>(bs + b_off1 + roff[h]);
     }
-    // scheduling groups (masks: 0x100 LDS reads, 0x020 global reads, 0x008 MFMA)
+    if constexpr (AFF) {   // |W| for the radius term of an affine layer's interval
+      if (p.abs_b) {
+#pragma unroll
+        for (int h = 0; h < BK / 8; ++h) {
+          B0[h] = __builtin_elementwise_abs(B0[h]);
+          B1[h] = __builtin_elementwise_abs(B1[h]);
+        }
+      }
+    }
+    // scheduling groups (masks: 0x100 LDS reads, 0x008 MFMA)
     __builtin_amdgcn_sched_group_barrier(0x100, 4 * (BK / 8), 0);
-    __builtin_amdgcn_sched_group_barrier(0x020, 2 * SQ, 0);
     __builtin_amdgcn_sched_group_barrier(0x008, 16 * (BK / 8), 0);
 #pragma unroll
     for (int h = 0; h < BK / 8; ++h) {
@@ -434,15 +437,8 @@ __global__ __launch_bounds__(NTHREADS, GEMM_MINB) void k_gemm(const GemmArgs p) 
         acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[e], b1[e], acc[1][1], 0, 0, 0);
       }
     }
-    if (more) {
-#pragma unroll
-      for (int q = 0; q < SQ; ++q) {
-        *reinterpret_cast<f32x4 *>(&As[cur ^ 1][(lrow + RPP * q) * LDS_LD + lcol]) = ra[q];
-        *reinterpret_cast<f32x4 *>(&Bs[cur ^ 1][(lrow + RPP * q) * LDS_LD + lcol]) = rb[q];
-      }
-    }
-    __syncthreads();
   }
+  __syncthreads();   // every wave is done with the operand buffers, which the epilogue reuses
 
   // ---- epilogue ---------------------------------------------------------------------
   gemm_epilogue<FWD, AL, AFF, 2>(p, acc, m0, wm * 64, n0 + wn * 64, lane, BM, 0, nullptr, n0, BN,
