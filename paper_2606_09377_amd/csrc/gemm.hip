@@ -525,38 +525,32 @@ constexpr int64_t GEMM_ROUND = 512;
 
 template <bool FWD, bool AL, bool AFF = false>
 __global__ __launch_bounds__(256) void k_gemm_mid(const GemmArgs p) {
-  __shared__ __attribute__((aligned(16))) float As[2][MD_BM * LDS_LD];
-  __shared__ __attribute__((aligned(16))) float Bs[2][MD_BN * LDS_LD];
+  __shared__ __attribute__((aligned(16))) float As[2][MD_BM * BK];
+  __shared__ __attribute__((aligned(16))) float Bs[2][MD_BN * BK];
   __shared__ float xpart[2][16 * 64];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
   const int n_mt = p.M_pad / MD_BM, n_nt = p.N_pad / MD_BN;
   int mt, nt;
   map_tile(blockIdx.x, n_mt * n_nt, n_mt, n_nt, mt, nt);
   const int m0 = mt * MD_BM, n0 = nt * MD_BN;
 
-  // global -> register staging: thread t moves rows t/TPR + RPP q of both operand tiles
+  // operand tiles straight into LDS as in k_gemm (rows unpadded, chunks swizzled by lds_swz;
+  // lane (row lrow, chunk slot tid % TPR) fetches the chunk that lands in its slot)
   constexpr int MQ = MD_BM / RPP;
-  const int lrow = tid / TPR, lcol = (tid % TPR) * 4;
-  const float *Ag = p.A + (int64_t)(m0 + lrow) * p.lda + lcol;
-  const float *Bg = p.Bt + (int64_t)(n0 + lrow) * p.ldb + lcol;
+  constexpr int WROWS = 64 / TPR;
+  const int lrow = tid / TPR;
+  const int dcol = ((tid % TPR) ^ lds_swz<BK>(lrow)) * 4;
+  const float *Ag = p.A + (int64_t)(m0 + lrow) * p.lda + dcol;
+  const float *Bg = p.Bt + (int64_t)(n0 + lrow) * p.ldb + dcol;
   const int64_t a_step = RPP * p.lda, b_step = RPP * p.ldb;
-  f32x4 ra[MQ], rb[MQ];
-  auto gload = [&](int k0) {
+  auto issue = [&](int kt, int buf) {
+    const int k0 = kt * BK;
 #pragma unroll
     for (int q = 0; q < MQ; ++q) {
-      ra[q] = *reinterpret_cast<const f32x4 *>(Ag + q * a_step + k0);
-      rb[q] = *reinterpret_cast<const f32x4 *>(Bg + q * b_step + k0);
-      if constexpr (AFF) {
-        if (p.abs_b) rb[q] = __builtin_elementwise_abs(rb[q]);
-      }
-    }
-  };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int q = 0; q < MQ; ++q) {
-      *reinterpret_cast<f32x4 *>(&As[buf][(lrow + RPP * q) * LDS_LD + lcol]) = ra[q];
-      *reinterpret_cast<f32x4 *>(&Bs[buf][(lrow + RPP * q) * LDS_LD + lcol]) = rb[q];
+      dma16(Ag + q * a_step + k0, &As[buf][(wave * WROWS + RPP * q) * BK]);
+      dma16(Bg + q * b_step + k0, &Bs[buf][(wave * WROWS + RPP * q) * BK]);
     }
   };
 
@@ -564,25 +558,30 @@ __global__ __launch_bounds__(256) void k_gemm_mid(const GemmArgs p) {
 #pragma unroll
   for (int v = 0; v < 16; ++v) acc[0][0][v] = 0.f;
   const int KT = p.K / BK;
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  const int r32 = lane & 31, kq = (lane >> 5) * (BK / 2);
-  const int a_off = (wm * 32 + r32) * LDS_LD + kq, b_off = (wn * 32 + r32) * LDS_LD + kq;
+  // lane (r32, half) reads k half * 16 .. + 15 of its row (logical chunks half * 4 + h)
+  const int r32 = lane & 31, sw = lds_swz<BK>(r32);
+  int roff[BK / 8];
+#pragma unroll
+  for (int h = 0; h < BK / 8; ++h) roff[h] = ((((lane >> 5) * (BK / 8)) + h) ^ sw) * 4;
+  const int a_off = (wm * 32 + r32) * BK, b_off = (wn * 32 + r32) * BK;
+  issue(0, 0);
   for (int kt = 0; kt < KT; ++kt) {
     const int cur = kt & 1;
-    const bool more = kt + 1 < KT;
-    if (more) gload((kt + 1) * BK);
+    wait_vmcnt<0>();
+    barrier_only();   // every wave's part of tile kt is in LDS; the other stage is free
+    if (kt + 1 < KT) issue(kt + 1, cur ^ 1);
 #pragma unroll
     for (int h = 0; h < BK / 8; ++h) {
-      const f32x4 a = *reinterpret_cast<const f32x4 *>(As[cur] + a_off + 4 * h);
-      const f32x4 b = *reinterpret_cast<const f32x4 *>(Bs[cur] + b_off + 4 * h);
+      const f32x4 a = *reinterpret_cast<const f32x4 *>(As[cur] + a_off + roff[h]);
+      f32x4 b = *reinterpret_cast<const f32x4 *>(Bs[cur] + b_off + roff[h]);
+      if constexpr (AFF) {
+        if (p.abs_b) b = __builtin_elementwise_abs(b);
+      }
 #pragma unroll
       for (int e = 0; e < 4; ++e) acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[e], b[e], acc[0][0], 0, 0, 0);
     }
-    if (more) lstore(cur ^ 1);
-    __syncthreads();
   }
+  __syncthreads();   // every wave is done with the operand buffers, which the epilogue reuses
   gemm_epilogue<FWD, AL, AFF, 1, 1>(p, acc, m0, wm * 32, n0, lane, MD_BM, wn, xpart[wm], n0, MD_BN,
                                     reinterpret_cast<signed char *>(&As[0][0]));
 }
