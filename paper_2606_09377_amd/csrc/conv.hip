@@ -1385,7 +1385,8 @@ __global__ __launch_bounds__(256, 2) void k_fwd_conv(const FwdConvArgs p, FastDi
   constexpr int QA = BM / RPP, QB = BN / RPP;
   __shared__ __attribute__((aligned(16))) float As[2][BM * BK];
   __shared__ __attribute__((aligned(16))) float Bs[2][BN * BK];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WN, wn = wave % WN;
   const int n_nt = (p.Co + BN - 1) / BN;
   const int mt = blockIdx.x / n_nt, nt = blockIdx.x - mt * n_nt;
@@ -1393,8 +1394,12 @@ __global__ __launch_bounds__(256, 2) void k_fwd_conv(const FwdConvArgs p, FastDi
   const int HW = p.Ho * p.Ho;
   const uint32_t Mtot = (uint32_t)p.rows * (uint32_t)HW;
 
-  const int lrow = tid / TPR, lcol = (tid % TPR) * 4;
-  const int scol = ((tid % TPR) ^ lds_swz<BK>(lrow)) * 4;
+  // operand tiles straight into LDS (global_load_lds): lane (row lrow, chunk slot tid % TPR)
+  // fetches the logical chunk dcol that the swizzle puts into its slot
+  constexpr int WROWS = 64 / TPR;
+  static_assert(RPP % 16 == 0, "rows of one load pass share the swizzle");
+  const int lrow = tid / TPR;
+  const int dcol = ((tid % TPR) ^ lds_swz<BK>(lrow)) * 4;
   const float *a_row[QA];
   int yi0[QA], xi0[QA];
 #pragma unroll
@@ -1412,15 +1417,14 @@ __global__ __launch_bounds__(256, 2) void k_fwd_conv(const FwdConvArgs p, FastDi
 #pragma unroll
   for (int q = 0; q < QB; ++q) {
     const int co = n0 + lrow + RPP * q;
-    b_row[q] = co < p.Co ? p.Wk + (int64_t)co * 9 * p.Ci + lcol : nullptr;
+    b_row[q] = co < p.Co ? p.Wk + (int64_t)co * 9 * p.Ci + dcol : nullptr;
   }
   const int cpt = p.Ci / BK;   // K tiles per tap
   // K order: pairs of 16-channel blocks (one 128-byte line of a position) outer, then the
   // tap, then the block of the pair, so a tile's shifted re-reads of a line follow each
   // other within a few K tiles (as in the transposed convolution)
   const bool pairs = cpt % 2 == 0;
-  f32x4 ra[QA], rb[QB];
-  auto gload = [&](int kt) {
+  auto gload = [&](int kt, int buf) {
     int t, cb;
     if (pairs) {
       const int grp = kt / 18, rem = kt - grp * 18;
@@ -1436,20 +1440,14 @@ __global__ __launch_bounds__(256, 2) void k_fwd_conv(const FwdConvArgs p, FastDi
     for (int q = 0; q < QA; ++q) {
       const int yy = yi0[q] + ky, xx = xi0[q] + kx;
       const bool ok = (unsigned)yy < (unsigned)p.Hi && (unsigned)xx < (unsigned)p.Hi;
-      const float *src = ok ? a_row[q] + ((int64_t)yy * p.Hi + xx) * p.Ci + c0 + lcol : g_zero4;
-      ra[q] = *reinterpret_cast<const f32x4 *>(src);
+      const float *src = ok ? a_row[q] + ((int64_t)yy * p.Hi + xx) * p.Ci + c0 + dcol : g_zero4;
+      dma16(src, &As[buf][(wave * WROWS + RPP * q) * BK]);
     }
 #pragma unroll
     for (int q = 0; q < QB; ++q) {
       const float *src = b_row[q] ? b_row[q] + t * p.Ci + c0 : g_zero4;
-      rb[q] = *reinterpret_cast<const f32x4 *>(src);
+      dma16(src, &Bs[buf][(wave * WROWS + RPP * q) * BK]);
     }
-  };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int q = 0; q < QA; ++q) *reinterpret_cast<f32x4 *>(&As[buf][(lrow + RPP * q) * BK + scol]) = ra[q];
-#pragma unroll
-    for (int q = 0; q < QB; ++q) *reinterpret_cast<f32x4 *>(&Bs[buf][(lrow + RPP * q) * BK + scol]) = rb[q];
   };
   f32x16 acc[MB][NB];
 #pragma unroll
@@ -1459,17 +1457,16 @@ __global__ __launch_bounds__(256, 2) void k_fwd_conv(const FwdConvArgs p, FastDi
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
   const int KT = 9 * cpt;
-  gload(0);
-  lstore(0);
-  __syncthreads();
+  gload(0, 0);
   const int r32 = lane & 31, sw = lds_swz<BK>(r32);
   int roff[CPR / 2];
 #pragma unroll
   for (int h = 0; h < CPR / 2; ++h) roff[h] = ((((lane >> 5) * (CPR / 2)) + h) ^ sw) * 4;
   for (int kt = 0; kt < KT; ++kt) {
     const int cur = kt & 1;
-    const bool more = kt + 1 < KT;
-    if (more) gload(kt + 1);
+    wait_vmcnt<0>();
+    barrier_only();   // every wave's part of tile kt is in LDS; the other stage is free
+    if (kt + 1 < KT) gload(kt + 1, cur ^ 1);
     const float *as = As[cur] + (wm * (BM / WM) + r32) * BK;
     const float *bs = Bs[cur] + (wn * (BN / WN) + r32) * BK;
 #pragma unroll
@@ -1487,9 +1484,8 @@ __global__ __launch_bounds__(256, 2) void k_fwd_conv(const FwdConvArgs p, FastDi
           for (int j = 0; j < NB; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][e], b[j][e], acc[i][j], 0, 0, 0);
     }
-    if (more) lstore(cur ^ 1);
-    __syncthreads();
   }
+  __syncthreads();   // every wave is done with the operand buffers, which the epilogue reuses
   // epilogue: the offsets of every tile row once (a row per thread), through the free A
   // buffer; -1 marks rows past the end
   static_assert(28 * BM <= (int)sizeof(As), "row offsets must fit the A buffers");
