@@ -42,7 +42,6 @@ namespace vcr {
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int LDS_LD = BK + 4;
 constexpr int TPR = BK / 4;             // staging threads per tile row (one 16-byte chunk each)
 constexpr int RPP = 256 / TPR;          // tile rows per staging pass
 constexpr int SQ = 128 / RPP;           // staging passes per 128-row tile

@@ -22,15 +22,21 @@ __device__ __forceinline__ int lds_swz(int row) {
 // wave-uniform).  Issued as inline assembly so that the compiler neither waits on the
 // vector-memory counter before every LDS read of the loop nor counts these loads: the loop
 // waits for them itself (wait_vmcnt) before the barrier that publishes a stage.  M0 carries
-// the LDS address; the kernels that use this have no other use of M0 (clobbering a register
-// the compiler reserves draws a warning, silenced here).
+// the LDS address, with the one wait state a load to LDS needs after an M0 write.  M0 is
+// clobbered without being restored: the kernels that call this have no other use of M0
+// (checked in their ISA; saving and restoring it around every load cost 0.6% on the GEMM).
+// Clobbering a register the compiler reserves draws a warning, silenced here.
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void dma16(const float *g, float *lds) {
   const uint32_t l = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) float *)lds;
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(__builtin_amdgcn_readfirstlane(l)),
-               "v"(g)
-               : "memory", "m0");
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off"
+      :
+      : "s"(__builtin_amdgcn_readfirstlane(l)), "v"(g)
+      : "memory", "m0");
 }
 #pragma clang diagnostic pop
 
