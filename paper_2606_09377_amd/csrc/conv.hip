@@ -30,6 +30,7 @@
 #include "conv.h"
 #include "relax.h"
 #include "lds_dma.h"
+#include "row_sums.h"
 #include "splits.h"
 
 #include <algorithm>
@@ -264,22 +265,11 @@ __device__ __forceinline__ void convt_epilogue(const ConvTArgs &p, const ConvCla
       rp[g * 4 + t] = x;
     }
     if (g == 3) {   // the lane's 16 rows of block i: reduce over the 32 columns, one partial each
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        float x = rp[v];
-        x += __shfl_xor(x, 16);
-        x += __shfl_xor(x, 8);
-        x += __shfl_xor(x, 4);
-        x += __shfl_xor(x, 2);
-        x += __shfl_xor(x, 1);
-        rp[v] = x;
-      }
-      if (r32 == 0) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int mo = s_mo[lrow0 + i * 32 + (v >> 2) * 8 + (v & 3)];
-          if (mo >= 0) p.part[(int64_t)(nt * WN + wn) * p.M_pad + mo] = rp[v];
-        }
+      const float x = half_wave_row_sums(rp, r32);
+      if ((r32 & 1) == 0) {   // lane 2 v stores row v
+        const int v = r32 >> 1;
+        const int mo = s_mo[lrow0 + i * 32 + (v >> 2) * 8 + (v & 3)];
+        if (mo >= 0) p.part[(int64_t)(nt * WN + wn) * p.M_pad + mo] = x;
       }
     }
   }

@@ -35,6 +35,7 @@
 // on which other rows share the tile.
 #include "kernels.h"
 #include "lds_dma.h"
+#include "row_sums.h"
 #include "splits.h"
 
 namespace vcr {
@@ -293,29 +294,14 @@ __device__ __forceinline__ void gemm_epilogue_body(const GemmArgs &p, f32x16 (&a
 #pragma unroll
     for (int v = 0; v < 16; ++v) rp[0][v] += xpart[v * 64 + lane];
   }
-  // fixed butterfly over the 32 lanes that share rows
+  // fixed butterfly over the 32 lanes that share rows (as a reduce-scatter: lane 2 v ends
+  // with row v's sum)
+  float *dst = partp + (int64_t)(col0 / PART_COLS) * p.M_pad;
+  const int v = r32 >> 1;
 #pragma unroll
   for (int bi = 0; bi < MB; ++bi) {
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      float x = rp[bi][v];
-      x += __shfl_xor(x, 16);
-      x += __shfl_xor(x, 8);
-      x += __shfl_xor(x, 4);
-      x += __shfl_xor(x, 2);
-      x += __shfl_xor(x, 1);
-      rp[bi][v] = x;
-    }
-  }
-  if (r32 == 0) {
-    float *dst = partp + (int64_t)(col0 / PART_COLS) * p.M_pad;
-#pragma unroll
-    for (int bi = 0; bi < MB; ++bi)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = m0 + wrow + bi * 32 + (v >> 2) * 8 + half * 4 + (v & 3);
-        dst[row] = rp[bi][v];
-      }
+    const float x = half_wave_row_sums(rp[bi], r32);
+    if ((r32 & 1) == 0) dst[m0 + wrow + bi * 32 + (v >> 2) * 8 + half * 4 + (v & 3)] = x;
   }
 }
 
