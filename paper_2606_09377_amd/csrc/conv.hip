@@ -975,22 +975,19 @@ __global__ __launch_bounds__(256) void k_init_conv(const ConvInitArgs a) {
         }
       }
     }
+  // the eight rows' sums over the wave (lane 8 k ends with row k = INIT_CONV_G d + e)
+  static_assert(2 * INIT_CONV_G == 8, "one value per row of the wave's eight");
+  float rows8[8];
 #pragma unroll
   for (int d = 0; d < 2; ++d)
 #pragma unroll
-    for (int e = 0; e < INIT_CONV_G; ++e) {
-      float x = acc[d][e];
-      x += __shfl_xor(x, 32);
-      x += __shfl_xor(x, 16);
-      x += __shfl_xor(x, 8);
-      x += __shfl_xor(x, 4);
-      x += __shfl_xor(x, 2);
-      x += __shfl_xor(x, 1);
-      if (lane == 0) {
-        const int c0 = cg * INIT_CONV_G + e;
-        a.beta[r0 + d * n_src + (int64_t)e * HW] = (d ? -1.f : 1.f) * a.b[c0] + x;
-      }
-    }
+    for (int e = 0; e < INIT_CONV_G; ++e) rows8[d * INIT_CONV_G + e] = acc[d][e];
+  const float x = wave_sums8(rows8, lane);
+  if ((lane & 7) == 0) {
+    const int k = lane >> 3, d = k / INIT_CONV_G, e = k - d * INIT_CONV_G;
+    const int c0 = cg * INIT_CONV_G + e;
+    a.beta[r0 + d * n_src + (int64_t)e * HW] = (d ? -1.f : 1.f) * a.b[c0] + x;
+  }
 }
 
 hipError_t launch_init_conv(const ConvInitArgs &a, hipStream_t s) {

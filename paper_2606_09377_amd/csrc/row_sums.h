@@ -38,4 +38,28 @@ __device__ __forceinline__ float half_wave_row_sums(const float (&rp)[16], int r
   return x;
 }
 
+// Eight values per lane summed over the 64 lanes of a wave, as the same kind of
+// reduce-scatter over the butterfly x += shfl_xor(x, 32), (x, 16), ..., (x, 1): returns the
+// sum of value (lane >> 3) & 7, with the per-value butterfly's bits.
+__device__ __forceinline__ float wave_sums8(const float (&v)[8], int lane) {
+  const bool b5 = lane & 32, b4 = lane & 16, b3 = lane & 8;
+  float v4[4], v2[2];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const float send = b5 ? v[j] : v[j + 4], keep = b5 ? v[j + 4] : v[j];
+    v4[j] = keep + __shfl_xor(send, 32);
+  }
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const float send = b4 ? v4[j] : v4[j + 2], keep = b4 ? v4[j + 2] : v4[j];
+    v2[j] = keep + __shfl_xor(send, 16);
+  }
+  const float send = b3 ? v2[0] : v2[1], keep = b3 ? v2[1] : v2[0];
+  float x = keep + __shfl_xor(send, 8);
+  x += __shfl_xor(x, 4);
+  x += __shfl_xor(x, 2);
+  x += __shfl_xor(x, 1);
+  return x;
+}
+
 }  // namespace vcr
