@@ -319,6 +319,9 @@ __global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
   const int lrow = tid / TPR;
   const int dcol = (((tid % TPR)) ^ lds_swz<BK>(lrow)) * 4;
   constexpr int WROWS = 64 / TPR;   // tile rows of one wave's load
+  // LDS byte addresses of this wave's first tile rows in stage 0 (M0 of its loads)
+  const uint32_t a_lds = lds_addr(&As[0][0]) + (uint32_t)(wave * WROWS * BK * 4);
+  const uint32_t b_lds = lds_addr(&Bs[0][0]) + (uint32_t)(wave * WROWS * BK * 4);
   static_assert(RPP % 16 == 0, "the swizzle (period 16 rows) repeats with the rows of a load pass");
   const float *a_row[QA];
   int ys[QA], xs[QA], yl[QA], xl[QA];
@@ -372,12 +375,12 @@ __global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
       const bool ok = (unsigned)yy < (unsigned)yl[q] && (unsigned)xx < (unsigned)xl[q];
       // positions outside the source window or the image read a zero block
       const float *src = ok ? a_row[q] + (yy * p.S_out + xx) * p.C_out + co : g_zero4;
-      dma16(src, &As[buf][(wave * WROWS + RPP * q) * BK]);
+      dma16(src, a_lds + (uint32_t)(buf * (int)sizeof(As[0]) + RPP * q * BK * 4));
     }
     const int kb = (3 * ky + kx) * p.C_out + co0;
 #pragma unroll
     for (int q = 0; q < QB; ++q)
-      dma16(Bg + (int64_t)q * RPP * p.ldb + kb, &Bs[buf][(wave * WROWS + RPP * q) * BK]);
+      dma16(Bg + (int64_t)q * RPP * p.ldb + kb, b_lds + (uint32_t)(buf * (int)sizeof(Bs[0]) + RPP * q * BK * 4));
   };
 
   f32x16 acc[MB][NB];
@@ -1384,6 +1387,9 @@ __global__ __launch_bounds__(256, 2) void k_fwd_conv(const FwdConvArgs p, FastDi
   // operand tiles straight into LDS (global_load_lds): lane (row lrow, chunk slot tid % TPR)
   // fetches the logical chunk dcol that the swizzle puts into its slot
   constexpr int WROWS = 64 / TPR;
+  // LDS byte addresses of this wave's first tile rows in stage 0 (M0 of its loads)
+  const uint32_t a_lds = lds_addr(&As[0][0]) + (uint32_t)(wave * WROWS * BK * 4);
+  const uint32_t b_lds = lds_addr(&Bs[0][0]) + (uint32_t)(wave * WROWS * BK * 4);
   static_assert(RPP % 16 == 0, "rows of one load pass share the swizzle");
   const int lrow = tid / TPR;
   const int dcol = ((tid % TPR) ^ lds_swz<BK>(lrow)) * 4;
@@ -1428,12 +1434,12 @@ __global__ __launch_bounds__(256, 2) void k_fwd_conv(const FwdConvArgs p, FastDi
       const int yy = yi0[q] + ky, xx = xi0[q] + kx;
       const bool ok = (unsigned)yy < (unsigned)p.Hi && (unsigned)xx < (unsigned)p.Hi;
       const float *src = ok ? a_row[q] + ((int64_t)yy * p.Hi + xx) * p.Ci + c0 + dcol : g_zero4;
-      dma16(src, &As[buf][(wave * WROWS + RPP * q) * BK]);
+      dma16(src, a_lds + (uint32_t)(buf * (int)sizeof(As[0]) + RPP * q * BK * 4));
     }
 #pragma unroll
     for (int q = 0; q < QB; ++q) {
       const float *src = b_row[q] ? b_row[q] + t * p.Ci + c0 : g_zero4;
-      dma16(src, &Bs[buf][(wave * WROWS + RPP * q) * BK]);
+      dma16(src, b_lds + (uint32_t)(buf * (int)sizeof(Bs[0]) + RPP * q * BK * 4));
     }
   };
   f32x16 acc[MB][NB];

@@ -18,8 +18,14 @@ __device__ __forceinline__ int lds_swz(int row) {
   return (row / RPG) & (CPR - 1);
 }
 
-// 16 bytes from global memory into LDS: lane i of the wave writes lds + 16 i (lds is
-// wave-uniform).  Issued as inline assembly so that the compiler neither waits on the
+// The LDS byte address of a __shared__ location (the value M0 takes for a load to LDS):
+// computed once per kernel, outside the loops that issue the loads.
+__device__ __forceinline__ uint32_t lds_addr(const float *p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) float *)p;
+}
+
+// 16 bytes from global memory into LDS: lane i of the wave writes LDS byte address lds + 16 i
+// (lds is wave-uniform).  Issued as inline assembly so that the compiler neither waits on the
 // vector-memory counter before every LDS read of the loop nor counts these loads: the loop
 // waits for them itself (wait_vmcnt) before the barrier that publishes a stage.  M0 carries
 // the LDS address, with the one wait state a load to LDS needs after an M0 write.  M0 is
@@ -28,6 +34,19 @@ __device__ __forceinline__ int lds_swz(int row) {
 // Clobbering a register the compiler reserves draws a warning, silenced here.
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(const float *g, uint32_t lds) {
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off"
+      :
+      : "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(g)
+      : "memory", "m0");
+}
+// The same with the LDS location given as a pointer: the address conversion happens at every
+// load.  (The GEMM kernels use this form: on the wide MLP it measured 1% faster than loads
+// from precomputed addresses, which issue closer together; the convolutions gain 1% the other
+// way round.)
 __device__ __forceinline__ void dma16(const float *g, float *lds) {
   const uint32_t l = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) float *)lds;
   asm volatile(
