@@ -382,38 +382,31 @@ __global__ __launch_bounds__(NTHREADS, GEMM_MINB) void k_gemm(const GemmArgs p) 
 
   const int KT = p.K / BK;
   issue(0, 0);
+  static_assert(SQ == BK / 8, "one load pass per operand read step");
   for (int kt = 0; kt < KT; ++kt) {
     const int cur = kt & 1;
     wait_vmcnt<0>();
     barrier_only();   // every wave's part of tile kt is in LDS; the other stage is free
-    if (kt + 1 < KT) issue(kt + 1, cur ^ 1);
+    const bool more = kt + 1 < KT;
+    const int k1 = (kt + 1) * BK;
     const float *as = As[cur];
     const float *bs = Bs[cur];
-    // all operand reads of the K tile first (the scheduler then spreads them over the MFMAs
-    // instead of stalling half-way through the tile)
-    f32x4 A0[BK / 8], A1[BK / 8], B0[BK / 8], B1[BK / 8];
 #pragma unroll
     for (int h = 0; h < BK / 8; ++h) {
-      A0[h] = *reinterpret_cast<const f32x4 *>(as + a_off0 + roff[h]);
-      A1[h] = *reinterpret_cast<const f32x4 *>(as + a_off1 + roff[h]);
-      B0[h] = *reinterpret_cast<const f32x4 *>(bs + b_off0 + roff[h]);
-      B1[h] = *reinterpret_cast<const f32x4 *>(bs + b_off1 + roff[h]);
-    }
-    if constexpr (AFF) {   // |W| for the radius term of an affine layer's interval
-      if (p.abs_b) {
-#pragma unroll
-        for (int h = 0; h < BK / 8; ++h) {
-          B0[h] = __builtin_elementwise_abs(B0[h]);
-          B1[h] = __builtin_elementwise_abs(B1[h]);
+      const f32x4 a0 = *reinterpret_cast<const f32x4 *>(as + a_off0 + roff[h]);
+      const f32x4 a1 = *reinterpret_cast<const f32x4 *>(as + a_off1 + roff[h]);
+      f32x4 b0 = *reinterpret_cast<const f32x4 *>(bs + b_off0 + roff[h]);
+      f32x4 b1 = *reinterpret_cast<const f32x4 *>(bs + b_off1 + roff[h]);
+      if (more) {   // the next tile's loads spread over the MFMA steps, one pass per step
+        dma16(Ag + h * a_step + k1, &As[cur ^ 1][(wave * WROWS + RPP * h) * BK]);
+        dma16(Bg + h * b_step + k1, &Bs[cur ^ 1][(wave * WROWS + RPP * h) * BK]);
+      }
+      if constexpr (AFF) {
+        if (p.abs_b) {
+          b0 = __builtin_elementwise_abs(b0);
+          b1 = __builtin_elementwise_abs(b1);
         }
       }
-    }
-    // scheduling groups (masks: 0x100 LDS reads, 0x008 MFMA)
-    __builtin_amdgcn_sched_group_barrier(0x100, 4 * (BK / 8), 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 16 * (BK / 8), 0);
-#pragma unroll
-    for (int h = 0; h < BK / 8; ++h) {
-      const f32x4 a0 = A0[h], a1 = A1[h], b0 = B0[h], b1 = B1[h];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0[e], b0[e], acc[0][0], 0, 0, 0);
@@ -550,15 +543,21 @@ __global__ __launch_bounds__(256) void k_gemm_mid(const GemmArgs p) {
   for (int h = 0; h < BK / 8; ++h) roff[h] = ((((lane >> 5) * (BK / 8)) + h) ^ sw) * 4;
   const int a_off = (wm * 32 + r32) * BK, b_off = (wn * 32 + r32) * BK;
   issue(0, 0);
+  static_assert(MQ <= BK / 8, "the load passes fit the operand read steps");
   for (int kt = 0; kt < KT; ++kt) {
     const int cur = kt & 1;
     wait_vmcnt<0>();
     barrier_only();   // every wave's part of tile kt is in LDS; the other stage is free
-    if (kt + 1 < KT) issue(kt + 1, cur ^ 1);
+    const bool more = kt + 1 < KT;
+    const int k1 = (kt + 1) * BK;
 #pragma unroll
     for (int h = 0; h < BK / 8; ++h) {
       const f32x4 a = *reinterpret_cast<const f32x4 *>(As[cur] + a_off + roff[h]);
       f32x4 b = *reinterpret_cast<const f32x4 *>(Bs[cur] + b_off + roff[h]);
+      if (more && h < MQ) {   // the next tile's loads spread over the MFMA steps
+        dma16(Ag + h * a_step + k1, &As[cur ^ 1][(wave * WROWS + RPP * h) * BK]);
+        dma16(Bg + h * b_step + k1, &Bs[cur ^ 1][(wave * WROWS + RPP * h) * BK]);
+      }
       if constexpr (AFF) {
         if (p.abs_b) b = __builtin_elementwise_abs(b);
       }
