@@ -127,7 +127,8 @@ __device__ __forceinline__ void convt_row(const ConvTArgs &p, const ConvClass &c
 // Source of the zeros that taps outside the source window load
 __device__ __attribute__((aligned(16))) float g_zero4[4] = {0.f, 0.f, 0.f, 0.f};   // never written
 
-// LDS stages of the transposed convolution's operand tiles
+// LDS stages of the transposed convolution's operand tiles (three cost a workgroup per
+// compute unit on the 256 x 64 tiles and measured 9% slower)
 constexpr int CONVT_NS = 2;
 
 
@@ -392,11 +393,13 @@ __global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
   const int KT = cl.nty * cl.ntx * p.C_out / BK;
-  // CONVT_NS LDS stages: K tile kt + CONVT_NS - 1 is in flight while tile kt is multiplied
+  // two LDS stages: K tile kt + 1 is in flight while tile kt is multiplied.  Its loads go out
+  // right after the barrier that frees its stage, before this wave waits for tile kt's own
+  // loads (a second barrier then publishes tile kt): the gathers wait on the L2, and issuing
+  // them as early as possible is what counts here (issuing them after the operand reads, or
+  // spread over the MFMA steps, measured 5-8% slower)
   constexpr int LPT = QA + QB;   // loads per thread per K tile
-#pragma unroll
-  for (int st = 0; st < CONVT_NS - 1; ++st)
-    if (st < KT) gload(st, st);
+  gload(0, 0);
   // operand reads: lane (r32, half) takes chunks half * CPR / 2 + h, h < CPR / 2, of row r32
   const int r32 = lane & 31, sw = lds_swz<BK>(r32);
   int roff[CPR / 2];
@@ -404,11 +407,15 @@ __global__ __launch_bounds__(256, MINB) void k_convt(const ConvTArgs p) {
   for (int h = 0; h < CPR / 2; ++h) roff[h] = ((((lane >> 5) * (CPR / 2)) + h) ^ sw) * 4;
   for (int kt = 0; kt < KT; ++kt) {
     const int cur = kt % CONVT_NS;
-    // tile kt has landed once no more than the loads of the tiles after it are outstanding
-    if (kt + CONVT_NS - 2 < KT) wait_vmcnt<(CONVT_NS - 2) * LPT>();
-    else wait_vmcnt<0>();
-    barrier_only();   // every wave's part of tile kt is in LDS; stage (kt - 1) % NS is free
-    if (kt + CONVT_NS - 1 < KT) gload(kt + CONVT_NS - 1, (kt + CONVT_NS - 1) % CONVT_NS);
+    static_assert(CONVT_NS == 2, "two barriers per tile: the next tile's loads go out before this one has landed");
+    barrier_only();   // every wave is done with tile kt - 1: its stage is free
+    if (kt + 1 < KT) {
+      gload(kt + 1, cur ^ 1);
+      wait_vmcnt<LPT>();   // this wave's part of tile kt has landed
+    } else {
+      wait_vmcnt<0>();
+    }
+    barrier_only();   // every wave's part of tile kt is in LDS
     const float *as = As[cur] + (wm * (BM / WM) + r32) * BK;
     const float *bs = Bs[cur] + (wn * (BN / WN) + r32) * BK;
 #pragma unroll
@@ -1457,9 +1464,14 @@ __global__ __launch_bounds__(256, 2) void k_fwd_conv(const FwdConvArgs p, FastDi
   for (int h = 0; h < CPR / 2; ++h) roff[h] = ((((lane >> 5) * (CPR / 2)) + h) ^ sw) * 4;
   for (int kt = 0; kt < KT; ++kt) {
     const int cur = kt & 1;
-    wait_vmcnt<0>();
-    barrier_only();   // every wave's part of tile kt is in LDS; the other stage is free
-    if (kt + 1 < KT) gload(kt + 1, cur ^ 1);
+    barrier_only();   // every wave is done with tile kt - 1: its stage is free
+    if (kt + 1 < KT) {
+      gload(kt + 1, cur ^ 1);
+      wait_vmcnt<QA + QB>();   // this wave's part of tile kt has landed
+    } else {
+      wait_vmcnt<0>();
+    }
+    barrier_only();   // every wave's part of tile kt is in LDS
     const float *as = As[cur] + (wm * (BM / WM) + r32) * BK;
     const float *bs = Bs[cur] + (wn * (BN / WN) + r32) * BK;
 #pragma unroll
