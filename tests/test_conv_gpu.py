@@ -102,13 +102,15 @@ def test_small_conv_nets_all_bounds(make):
                     what=f"{wl.name} input {b}")
 
 
-@pytest.mark.parametrize("hw,c2", [(4, 64), (6, 128)])
-def test_windows_larger_than_the_image(hw, c2):
+@pytest.mark.parametrize("hw,c1,c2", [(4, 32, 64), (6, 32, 128), (4, 128, 128)])
+def test_windows_larger_than_the_image(hw, c1, c2):
     """Tiny images, where the coefficient windows outgrow the image (up to 15 x 15 windows on a
     4 x 4 image): most window positions lie outside the image, and whole position classes
-    have no position inside it for any anchor; every bound of both inputs against the oracle."""
-    wl = small_resnet(331, hw=hw, c1=32, c2=c2, fc=16)
-    log("case", wl.name, "c2", c2)
+    have no position inside it for any anchor; with 128 channels before the stride-2
+    convolution the windowed steps run on the 128 x 128 tiles.  Every bound of both inputs
+    against the oracle."""
+    wl = small_resnet(331, hw=hw, c1=c1, c2=c2, fc=16)
+    log("case", wl.name, "c1", c1, "c2", c2)
     ctx = gpu_ctx(wl.net)
     lb, ub, layers = gpu_crown(ctx, wl)
     for b in range(wl.x0.shape[0]):
