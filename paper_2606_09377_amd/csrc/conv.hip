@@ -192,38 +192,62 @@ __device__ __forceinline__ void convt_epilogue(const ConvTArgs &p, const ConvCla
     ncol[j] = n0 + wn * (BN / WN) + j * 32 + r32;
     bn[j] = (!RELU && ncol[j] < p.C_in) ? p.bias[ncol[j]] : 0.f;
   }
-  // Parameters of group q = 4 i + g into buffer b, one group ahead of their use.  Lanes with
-  // nothing to load (outside the image, past C_in) read element 0, a finite parameter that
-  // meets a zero coefficient: no select on a loaded value, 32-bit offsets from one base.
+  // A ReLU step's relaxation parameters of group q = 4 i + g go into buffer b, one group
+  // ahead of their use.  Lanes with nothing to load (outside the image, past C_in) read
+  // element 0, a finite parameter that meets a zero coefficient: no select on a loaded value,
+  // 32-bit offsets from one base.  An identity step (the only kind with a residual) loads its
+  // residual terms instead, RD groups ahead into a ring of RD + 1 buffers (8 floats each).
   constexpr int NG = MB * 4;
   float4 prm[2][NB][4];
+  constexpr int RD = 3;
+  float rvb[RD + 1][NB][4];
   auto fetch = [&](int q, int b) {
     const int lr = lrow0 + (q >> 2) * 32 + (q & 3) * 8;
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-      const int pb = s_pb[lr + t];
+      if constexpr (RELU) {
+        const int pb = s_pb[lr + t];
 #pragma unroll
-      for (int j = 0; j < NB; ++j) {
-        const uint32_t off = (ncol[j] < p.C_in && pb >= 0) ? (uint32_t)(pb + ncol[j]) : 0u;
-        if constexpr (RELU) prm[b][j][t] = Pp[off];
+        for (int j = 0; j < NB; ++j) {
+          const uint32_t off = (ncol[j] < p.C_in && pb >= 0) ? (uint32_t)(pb + ncol[j]) : 0u;
+          prm[b][j][t] = Pp[off];
+        }
+      } else {
+        const int64_t rb = s_rb[lr + t];
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+          rvb[b % (RD + 1)][j][t] = resp ? *((ncol[j] < p.C_in && rb >= 0) ? resp + rb + ncol[j] : g_zero4) : 0.f;
       }
     }
   };
   fetch(0, 0);
+  if constexpr (!RELU) {
+#pragma unroll
+    for (int q = 1; q < RD && q < NG; ++q) fetch(q, q);
+  }
   float rp[16];
 #pragma unroll
   for (int q = 0; q < NG; ++q) {
     const int i = q >> 2, g = q & 3, b = q & 1;
     const int lr = lrow0 + i * 32 + g * 8;
-    float rv[NB][4];   // residual terms of this group, loaded before the next group's parameters
+    float rv[NB][4];   // residual terms of this group
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-      const int64_t rb = s_rb[lr + t];
 #pragma unroll
-      for (int j = 0; j < NB; ++j)
-        rv[j][t] = resp ? *((ncol[j] < p.C_in && rb >= 0) ? resp + rb + ncol[j] : g_zero4) : 0.f;
+      for (int j = 0; j < NB; ++j) {
+        if constexpr (RELU) {   // (a ReLU step has no residual: resp is null)
+          const int64_t rb = s_rb[lr + t];
+          rv[j][t] = resp ? *((ncol[j] < p.C_in && rb >= 0) ? resp + rb + ncol[j] : g_zero4) : 0.f;
+        } else {
+          rv[j][t] = rvb[q % (RD + 1)][j][t];
+        }
+      }
     }
-    if (q + 1 < NG) fetch(q + 1, b ^ 1);
+    if constexpr (RELU) {
+      if (q + 1 < NG) fetch(q + 1, b ^ 1);
+    } else {
+      if (q + RD < NG) fetch(q + RD, q + RD);
+    }
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       const int pb = s_pb[lr + t], mo = s_mo[lr + t];
