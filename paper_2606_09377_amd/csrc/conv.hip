@@ -768,73 +768,91 @@ __global__ __launch_bounds__(256, 3) void k_stem(const StemArgs p) {
     }
 
 
-    // ---- G = A_src W: each wave takes 32-position blocks, two at a time (blocks b and b + 4,
-    // both blocks' loads in flight together); lane (r32, half) feeds the MFMAs with 16
-    // consecutive k of its position per 32-k chunk, identically for both operands
+    // ---- G = A_src W: each wave takes 32-position blocks, two at a time (blocks b and b + 4),
+    // as one stream of steps (block pair, 32-channel chunk); lane (r32, half) feeds the MFMAs
+    // with 16 consecutive k of its position per chunk, identically for both operands.  Two
+    // register sets: step s + 1 is requested before step s is multiplied (past the last step
+    // the request repeats it: every request unconditional, so each multiply waits for its own
+    // step only).
     const int r32 = lane & 31, half = lane >> 5;
     const int n_blk = (n_src + 31) / 32;
     const int KC = p.C_out / 32;
-    for (int b0 = wave; b0 < n_blk; b0 += 8) {
-      const bool two = b0 + 4 < n_blk;   // wave-uniform
-      const float *src[2];
+    const int n_pairs = wave < n_blk ? (n_blk - wave + 7) / 8 : 0;
+    const int S = n_pairs * KC;   // wave-uniform
+    auto load_step = [&](int st, f32x4 (&a)[2][4]) {
+      st = min(st, S - 1);
+      const int pr = st / KC, kc = st - pr * KC;
+      const int b0 = wave + 8 * pr;
 #pragma unroll
       for (int q = 0; q < 2; ++q) {
         // positions past the last one repeat it: their G rows are never gathered
         const int pi = min((b0 + 4 * q) * 32 + r32, n_src - 1);
         const int rl = pi / n_row_src, sp = pi - rl * n_row_src;
-        src[q] = p.A + (int64_t)(r0 + rl) * p.row_stride_out + ((int64_t)y_lo * p.S_out + sp) * p.C_out + half * 16;
+        const float *src = p.A + (int64_t)(r0 + rl) * p.row_stride_out + ((int64_t)y_lo * p.S_out + sp) * p.C_out +
+                           kc * 32 + half * 16;
+#pragma unroll
+        for (int h = 0; h < 4; ++h) a[q][h] = *reinterpret_cast<const f32x4 *>(src + 4 * h);
       }
-      f32x16 acc[2][NB];
+    };
+    f32x16 acc[2][NB];
+    auto mma_step = [&](int st, const f32x4 (&a)[2][4]) {
+      const int pr = st / KC, kc = st - pr * KC;
+      if (kc == 0) {
 #pragma unroll
-      for (int q = 0; q < 2; ++q)
+        for (int q = 0; q < 2; ++q)
 #pragma unroll
-        for (int j = 0; j < NB; ++j)
+          for (int j = 0; j < NB; ++j)
 #pragma unroll
-          for (int v = 0; v < 16; ++v) acc[q][j][v] = 0.f;
-      f32x4 a[2][4];
+            for (int v = 0; v < 16; ++v) acc[q][j][v] = 0.f;
+      }
+      f32x4 b[NB][4];
 #pragma unroll
-      for (int q = 0; q < 2; ++q)
-#pragma unroll
-        for (int h = 0; h < 4; ++h) a[q][h] = *reinterpret_cast<const f32x4 *>(src[q] + 4 * h);
-      for (int kc = 0; kc < KC; ++kc) {
-        f32x4 an[2][4];
-        if (kc + 1 < KC) {
-#pragma unroll
-          for (int q = 0; q < 2; ++q)
-#pragma unroll
-            for (int h = 0; h < 4; ++h) an[q][h] = *reinterpret_cast<const f32x4 *>(src[q] + (kc + 1) * 32 + 4 * h);
-        }
-        f32x4 b[NB][4];
-#pragma unroll
-        for (int j = 0; j < NB; ++j)
-#pragma unroll
-          for (int h = 0; h < 4; ++h)
-            b[j][h] = *reinterpret_cast<const f32x4 *>(wt + (32 * j + r32) * WTP + kc * 32 + half * 16 + 4 * h);
+      for (int j = 0; j < NB; ++j)
 #pragma unroll
         for (int h = 0; h < 4; ++h)
+          b[j][h] = *reinterpret_cast<const f32x4 *>(wt + (32 * j + r32) * WTP + kc * 32 + half * 16 + 4 * h);
 #pragma unroll
-          for (int e = 0; e < 4; ++e)
+      for (int h = 0; h < 4; ++h)
 #pragma unroll
-            for (int q = 0; q < 2; ++q)
-#pragma unroll
-              for (int j = 0; j < NB; ++j)
-                acc[q][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[q][h][e], b[j][h][e], acc[q][j], 0, 0, 0);
-        if (kc + 1 < KC) {
+        for (int e = 0; e < 4; ++e)
 #pragma unroll
           for (int q = 0; q < 2; ++q)
 #pragma unroll
-            for (int h = 0; h < 4; ++h) a[q][h] = an[q][h];
+            for (int j = 0; j < NB; ++j)
+              acc[q][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[q][h][e], b[j][h][e], acc[q][j], 0, 0, 0);
+      if (kc == KC - 1) {   // the pair is done: lane holds rows 8 g + 4 half + t (v = 4 g + t)
+        const int b0 = wave + 8 * pr;
+        const bool two = b0 + 4 < n_blk;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          if (q == 1 && !two) break;
+#pragma unroll
+          for (int j = 0; j < NB; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v)
+              G[((b0 + 4 * q) * 32 + (v >> 2) * 8 + half * 4 + (v & 3)) * GP + 32 * j + r32] = acc[q][j][v];
         }
       }
-      // lane holds rows 8 g + 4 half + t (v = 4 g + t) of column 32 j + r32
+    };
+    if (S > 0) {
+      f32x4 a0[2][4], a1[2][4];
+      load_step(0, a0);
+      // an opaque copy: otherwise the loop head merges this load and the loop's into one
 #pragma unroll
-      for (int q = 0; q < 2; ++q) {
-        if (q == 1 && !two) break;
+      for (int q = 0; q < 2; ++q)
 #pragma unroll
-        for (int j = 0; j < NB; ++j)
-#pragma unroll
-          for (int v = 0; v < 16; ++v)
-            G[((b0 + 4 * q) * 32 + (v >> 2) * 8 + half * 4 + (v & 3)) * GP + 32 * j + r32] = acc[q][j][v];
+        for (int h = 0; h < 4; ++h) asm volatile("" : "+v"(a0[q][h]));
+      for (int st = 0;; st += 2) {
+        load_step(st + 1, a1);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_step(st, a0);
+        __builtin_amdgcn_sched_barrier(0);
+        if (st + 1 >= S) break;
+        load_step(st + 2, a0);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_step(st + 1, a1);
+        __builtin_amdgcn_sched_barrier(0);
+        if (st + 2 >= S) break;
       }
     }
     __syncthreads();

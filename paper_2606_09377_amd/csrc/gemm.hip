@@ -425,7 +425,7 @@ __global__ __launch_bounds__(NTHREADS, GEMM_MINB) void k_gemm(const GemmArgs p) 
 
 // Small launches (few row tiles): a workgroup of two waves owns a 32 x 64 tile, each wave one
 // 32-column block, and reads its MFMA operands straight from global memory (no LDS operand
-// staging), four K tiles prefetched in registers.  Each lane takes the same 16 consecutive k of
+// staging), K tiles in a ring of four register sets (three in flight).  Each lane takes the same 16 consecutive k of
 // its row per K tile as in k_gemm, each accumulator sees the same MFMA sequence, and the row
 // sums of the two blocks are added in k_gemm's order, so both kernels give the same bits.
 constexpr int SM_BM = 32, SM_BN = 64;
@@ -446,43 +446,65 @@ __global__ __launch_bounds__(128) void k_gemm_small(const GemmArgs p) {
   f32x16 acc[1][1];
 #pragma unroll
   for (int v = 0; v < 16; ++v) acc[0][0][v] = 0.f;
-  // four K tiles of loads in flight: a lone wave per tile has no other way to hide the latency
-  f32x4 a[BK / 8], b[BK / 8], a1[BK / 8], b1[BK / 8], a2[BK / 8], b2[BK / 8], a3[BK / 8], b3[BK / 8], a4[BK / 8],
-      b4[BK / 8];
-  auto load = [&](int k0, f32x4 *ra, f32x4 *rb) {
+  const int KT_LAST = p.K / BK - 1;   // >= 0: launch_gemm requires K > 0, a multiple of BK
+  // K tiles in a ring of four register sets (three in flight while one is multiplied): a
+  // lone wave per tile has no other way to hide the latency.  The ring is unrolled (no copies
+  // between sets, which would wait for every load in flight) and every request is
+  // unconditional, past the last tile repeating it (cache hits, never multiplied), so each
+  // multiply waits for its own tile only.
+  typedef f32x4 KSet[2][BK / 8];   // [0]: A, [1]: B
+  auto load = [&](int kt, KSet &r) {
+    const int k0 = min(kt, KT_LAST) * BK;
 #pragma unroll
     for (int h = 0; h < BK / 8; ++h) {
-      ra[h] = *reinterpret_cast<const f32x4 *>(Ag + k0 + 4 * h);
-      rb[h] = *reinterpret_cast<const f32x4 *>(Bg + k0 + 4 * h);
-      if constexpr (AFF) {
-        if (p.abs_b) rb[h] = __builtin_elementwise_abs(rb[h]);
-      }
+      r[0][h] = *reinterpret_cast<const f32x4 *>(Ag + k0 + 4 * h);
+      r[1][h] = *reinterpret_cast<const f32x4 *>(Bg + k0 + 4 * h);
     }
   };
-  const int KT = p.K / BK;
-  load(0, a, b);
-  if (KT > 1) load(BK, a1, b1);
-  if (KT > 2) load(2 * BK, a2, b2);
-  if (KT > 3) load(3 * BK, a3, b3);
-  for (int kt = 0; kt < KT; ++kt) {
-    if (kt + 4 < KT) load((kt + 4) * BK, a4, b4);
-#pragma unroll
-    for (int h = 0; h < BK / 8; ++h)
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[h][e], b[h][e], acc[0][0], 0, 0, 0);
+  auto mma = [&](KSet &r) {
 #pragma unroll
     for (int h = 0; h < BK / 8; ++h) {
-      a[h] = a1[h];
-      b[h] = b1[h];
-      a1[h] = a2[h];
-      b1[h] = b2[h];
-      a2[h] = a3[h];
-      b2[h] = b3[h];
-      a3[h] = a4[h];
-      b3[h] = b4[h];
+      f32x4 bb = r[1][h];
+      if constexpr (AFF) {
+        if (p.abs_b) bb = __builtin_elementwise_abs(bb);
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(r[0][h][e], bb[e], acc[0][0], 0, 0, 0);
     }
+  };
+  KSet s0, s1, s2, s3;
+  load(0, s0);
+  load(1, s1);
+  load(2, s2);
+  // opaque copies: otherwise the loop head merges these loads with the loop's (a phi of loads
+  // becomes a load of a phi), which undoes the ring
+#pragma unroll
+  for (int h = 0; h < BK / 8; ++h) asm volatile("" : "+v"(s0[0][h]), "+v"(s0[1][h]), "+v"(s1[0][h]), "+v"(s1[1][h]), "+v"(s2[0][h]), "+v"(s2[1][h]));
+  // whole rounds of four tiles (no exit inside a round: the loop head then knows which loads
+  // are in flight), then the last one to three tiles, already requested
+  const int KT = KT_LAST + 1;
+  int kt = 0;
+  for (; kt + 4 <= KT; kt += 4) {
+    load(kt + 3, s3);
+    __builtin_amdgcn_sched_barrier(0);
+    mma(s0);
+    __builtin_amdgcn_sched_barrier(0);
+    load(kt + 4, s0);
+    __builtin_amdgcn_sched_barrier(0);
+    mma(s1);
+    __builtin_amdgcn_sched_barrier(0);
+    load(kt + 5, s1);
+    __builtin_amdgcn_sched_barrier(0);
+    mma(s2);
+    __builtin_amdgcn_sched_barrier(0);
+    load(kt + 6, s2);
+    __builtin_amdgcn_sched_barrier(0);
+    mma(s3);
+    __builtin_amdgcn_sched_barrier(0);
   }
+  if (kt < KT) mma(s0);
+  if (kt + 1 < KT) mma(s1);
+  if (kt + 2 < KT) mma(s2);
   gemm_epilogue<FWD, AL, AFF, 1, 1>(p, acc, m0, 0, n0, lane, SM_BM, bj, xpart, n0, SM_BN, sflag);
 }
 
