@@ -4,6 +4,7 @@ about to be multiplied only.  Register copies between prefetch sets, or a prefet
 condition, make it wait for every load in flight instead (vmcnt(0) before the multiply),
 which silently turns the prefetch off.  Compile the sources for gfx950 to assembly (code
 built here) and check the waits inside those kernels' main loops."""
+import functools
 import os
 import re
 import shutil
@@ -23,6 +24,7 @@ def _hipcc():
     pytest.skip("hipcc not found")
 
 
+@functools.lru_cache(maxsize=None)
 def _asm(src):
     with tempfile.TemporaryDirectory() as d:
         out = os.path.join(d, "k.s")
