@@ -39,8 +39,9 @@ def _kernels(asm, prefix):
     """{name: lines} of the kernels whose mangled name starts with prefix."""
     out = {}
     for m in re.finditer(r"^(" + re.escape(prefix) + r"[^\s:]*):", asm, re.M):
-        end = asm.index(".Lfunc_end", m.end())
-        out[m.group(1)] = [l.strip() for l in asm[m.end():end].splitlines()]
+        end = asm.find(".Lfunc_end", m.end())
+        if end > 0:   # a function body, not another label of that name
+            out[m.group(1)] = [l.strip() for l in asm[m.end():end].splitlines()]
     return out
 
 
