@@ -425,10 +425,9 @@ __global__ __launch_bounds__(NTHREADS, GEMM_MINB) void k_gemm(const GemmArgs p) 
 
 // Small launches (few row tiles): a workgroup of two waves owns a 32 x 64 tile, each wave one
 // 32-column block, and reads its MFMA operands straight from global memory (no LDS operand
-// staging), K tiles in a ring of four register sets (three in flight).  Each lane takes the
-// same 16 consecutive k of its row per K tile as in k_gemm, each accumulator sees the same
-// MFMA sequence, and the row sums of the two blocks are added in k_gemm's order, so both
-// kernels give the same bits.
+// staging), K tiles in a ring of four register sets (three in flight).  Each lane takes the same 16 consecutive k of
+// its row per K tile as in k_gemm, each accumulator sees the same MFMA sequence, and the row
+// sums of the two blocks are added in k_gemm's order, so both kernels give the same bits.
 constexpr int SM_BM = 32, SM_BN = 64;
 constexpr int64_t SMALL_GRID = 512;   // 128 x 128 tiles below which the small kernel runs
 
