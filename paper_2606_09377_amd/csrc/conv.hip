@@ -285,7 +285,9 @@ __device__ __forceinline__ void convt_epilogue(const ConvTArgs &p, const ConvCla
             x += a * bn[j];
           }
         }
-        if (store) outp[ob + ncol[j]] = ap;
+        // non-temporal: the next step streams these coefficients back from HBM anyway (GBs
+        // per step), and caching them evicts the source rows this kernel's gathers re-read
+        if (store) __builtin_nontemporal_store(ap, outp + ob + ncol[j]);
       }
       rp[g * 4 + t] = x;
     }
